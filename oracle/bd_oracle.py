@@ -1,0 +1,338 @@
+"""Plain, slow, fp64 reference of the BudgetDraft sparse-drafter / full-verifier path.
+
+TEST INFRASTRUCTURE.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this module.  It shares no code
+with the HIP path: inputs arrive as bf16 bit patterns (``uint16``) or fp32
+arrays and are widened here, exactly, to float64.
+
+Every function states the passage of the paper it follows.  Where the paper
+is silent, the reading taken is stated in the docstring (the selection
+policy, window, pooling and tie rules come from the workload description of
+this build, not from the paper, which only names chunk-level selection by
+"cumulative attention weight" in Sec. 3.4).
+
+Conventions (shared with the C ABI):
+  * Query head h reads KV head g(h) = h // G, G = Hq / Hkv (contiguous groups).
+  * Causal rule: a key at position t is visible to a query at position p iff
+    0 <= t <= p.  Sequence s holds cache rows 0 .. L_s-1, the query tail
+    included; the last query row sits at position L_s - 1.
+  * scale: the caller's fp32 softmax scale, promoted exactly to float64.
+  * An empty key set gives output 0 and log-sum-exp -inf.
+
+Parity status: every function here is pinned by the CPU tests in
+``tests/test_oracle_pins.py`` (closed forms, invariants, library routines and
+brute force on tiny inputs); none is "parity unpinned".
+"""
+from __future__ import annotations
+
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+
+# --------------------------------------------------------------------------
+# Input widening
+# --------------------------------------------------------------------------
+
+def bf16_to_f64(bits) -> np.ndarray:
+    """bf16 bit patterns -> float64, exactly: (bits << 16) viewed as float32, widened."""
+    b = np.ascontiguousarray(bits, dtype=np.uint16)
+    return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def _scale64(scale: Optional[float], head_dim: int) -> float:
+    if scale is None:
+        scale = 1.0 / np.sqrt(head_dim)
+    return float(np.float64(np.float32(scale)))
+
+
+# --------------------------------------------------------------------------
+# Attention by definition (Eq. 1 and Eq. 2)
+# --------------------------------------------------------------------------
+
+def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, visible: np.ndarray, scale: float):
+    """Softmax attention of query rows over the keys each row may see.
+
+    Eq. (1)/(2): a distribution conditions on a KV cache through attention;
+    for one row, weights p_t = exp(l_t) / sum_u exp(l_u) with
+    l_t = scale * <q, k_t> over the visible keys t, output sum_t p_t v_t.
+
+    q [R][D], k [N][D], v [N][D] float64; visible [R][N] bool.
+    Returns out [R][D] float64 and lse [R] (natural log of sum_t exp l_t).
+    """
+    R, D = q.shape
+    out = np.zeros((R, D), dtype=np.float64)
+    lse = np.full(R, -np.inf, dtype=np.float64)
+    if k.shape[0] == 0:
+        return out, lse
+    logits = scale * (q @ k.T)                       # [R][N]
+    for r in range(R):
+        sel = np.nonzero(visible[r])[0]
+        if sel.size == 0:
+            continue
+        lr = logits[r, sel]
+        m = lr.max()
+        e = np.exp(lr - m)
+        z = e.sum()
+        out[r] = (e @ v[sel]) / z
+        lse[r] = m + np.log(z)
+    return out, lse
+
+
+# --------------------------------------------------------------------------
+# Budgeted KV selection (Alg. 2 "sparsify"; Sec. 3.4 "cumulative attention weight")
+# --------------------------------------------------------------------------
+
+def window_scores(k_g: np.ndarray, q_obs: np.ndarray, L: int, scale: float) -> np.ndarray:
+    """Cumulative attention weight of every cached key under the observation rows.
+
+    Sec. 3.4 scores cache entries "by cumulative attention weight"; here the
+    weights are those of the W observation rows of every query head of the
+    group (reading: probabilities, each row normalised over its own causal
+    key range, summed over rows and heads).
+
+    k_g [L][D] float64 (one KV head), q_obs [W][G][D] float64 at positions
+    L-W .. L-1.  Returns raw [L] float64.
+    """
+    W, G, _ = q_obs.shape
+    raw = np.zeros(L, dtype=np.float64)
+    for h in range(G):
+        logits = scale * (q_obs[:, h, :] @ k_g.T)          # [W][L]
+        for i in range(W):
+            p = L - W + i                                 # position of row i
+            row = logits[i, :p + 1]
+            a = np.exp(row - row.max())
+            a /= a.sum()
+            raw[:p + 1] += a
+    return raw
+
+
+def max_pool(x: np.ndarray, kernel: int) -> np.ndarray:
+    """Stride-1 centred max filter of odd width ``kernel``; windows are cut at both ends."""
+    r = kernel // 2
+    n = x.shape[0]
+    out = x.copy()
+    for o in range(1, r + 1):
+        if o >= n:
+            break
+        out[:n - o] = np.maximum(out[:n - o], x[o:])
+        out[o:] = np.maximum(out[o:], x[:n - o])
+    return out
+
+
+def topk_from_scores(raw: np.ndarray, L: int, window: int, budget: int, pool_kernel: int = 7,
+                     budget_counts_window: bool = True) -> Tuple[np.ndarray, np.ndarray]:
+    """Pool the prefix scores and keep the budget (selection steps after scoring).
+
+    Candidates are the prefix positions [0, N), N = L - W; the W window
+    positions are always kept.  Reading of the budget: B counts the window, so
+    B - W prefix entries are kept (``budget_counts_window=False`` keeps B).
+    Order: larger pooled score first, lower position first among equal scores.
+    Returns (selected positions ascending, window appended) and pooled [N].
+    """
+    N = L - window
+    pooled = max_pool(np.asarray(raw[:N], dtype=np.float64), pool_kernel)
+    keep = budget - window if budget_counts_window else budget
+    keep = max(0, min(keep, N))
+    pos = np.arange(N)
+    order = np.lexsort((pos, -pooled))                  # primary: -pooled, secondary: position
+    chosen = np.sort(order[:keep])
+    sel = np.concatenate([chosen, np.arange(N, L)]).astype(np.int32)
+    return sel, pooled
+
+
+def select_kv(k, q_win, seq_lens, num_q_heads: int, window: int, budget: int, pool_kernel: int = 7,
+              scale: Optional[float] = None, budget_counts_window: bool = True):
+    """K_S^sp(B) as an index set per (sequence, KV head): Alg. 2 "sparsify".
+
+    k: per sequence [Hkv][>=L_s][D] bf16 bits; q_win: per sequence [W][Hq][D]
+    bf16 bits (the last W query rows).  Returns idx [S][Hkv][B] int32 (tail -1),
+    nsel [S] int32 and raw scores (list of [Hkv][L_s] float64).
+
+    B >= L_s keeps every position (the sparse cache equals the full cache).
+    """
+    if window < 1 or budget < window or pool_kernel < 1 or pool_kernel % 2 == 0:
+        raise ValueError("invalid selection arguments")
+    S = len(seq_lens)
+    Hkv = k[0].shape[0]
+    G = num_q_heads // Hkv
+    D = k[0].shape[-1]
+    sc = _scale64(scale, D)
+    out_budget = budget if budget_counts_window else budget + window
+    idx = np.full((S, Hkv, out_budget), -1, dtype=np.int32)
+    nsel = np.zeros(S, dtype=np.int32)
+    raws = []
+    for s in range(S):
+        L = int(seq_lens[s])
+        if window > L:
+            raise ValueError("window longer than the sequence")
+        qw = bf16_to_f64(q_win[s])                       # [W][Hq][D]
+        raw_s = np.zeros((Hkv, L))
+        if budget >= L:
+            idx[s, :, :L] = np.arange(L, dtype=np.int32)
+            nsel[s] = L
+            raws.append(raw_s)
+            continue
+        for g in range(Hkv):
+            kg = bf16_to_f64(k[s][g, :L])
+            raw = window_scores(kg, qw[:, g * G:(g + 1) * G, :], L, sc)
+            sel, _ = topk_from_scores(raw, L, window, budget, pool_kernel, budget_counts_window)
+            idx[s, g, :sel.size] = sel
+            raw_s[g] = raw
+        nsel[s] = out_budget
+        raws.append(raw_s)
+    return idx, nsel, raws
+
+
+# --------------------------------------------------------------------------
+# Drafter decode attention over the selected entries (Eq. 2; Alg. 2 "draft")
+# --------------------------------------------------------------------------
+
+def _valid_entries(idx_row: np.ndarray, n: int, L: int) -> np.ndarray:
+    n = max(0, min(int(n), idx_row.shape[0]))
+    j = idx_row[:n].astype(np.int64)
+    return j[(j >= 0) & (j < L)]
+
+
+def sparse_decode_attn(k, v, q, idx, nsel, seq_lens, scale: Optional[float] = None):
+    """p_S(. | x_<t; K_S^sp(B)) attention for one decode query per head (Eq. 2).
+
+    q [S][Hq][D] bits at position L_s-1; idx [S][Hkv][ld] positions (entries
+    outside [0, L_s) are skipped), nsel [S] used entries.  Returns out
+    [S][Hq][D] float64, lse [S][Hq].
+    """
+    S, Hq, D = q.shape
+    Hkv = k[0].shape[0]
+    G = Hq // Hkv
+    sc = _scale64(scale, D)
+    out = np.zeros((S, Hq, D))
+    lse = np.full((S, Hq), -np.inf)
+    for s in range(S):
+        L = int(seq_lens[s])
+        qs = bf16_to_f64(q[s])
+        for g in range(Hkv):
+            J = _valid_entries(idx[s, g], nsel[s], L)
+            kg = bf16_to_f64(k[s][g][J])
+            vg = bf16_to_f64(v[s][g][J])
+            vis = np.ones((G, J.size), dtype=bool)
+            o, l = attend(qs[g * G:(g + 1) * G], kg, vg, vis, sc)
+            out[s, g * G:(g + 1) * G] = o
+            lse[s, g * G:(g + 1) * G] = l
+    return out, lse
+
+
+# --------------------------------------------------------------------------
+# Verifier full-KV attention at the gamma+1 draft positions (Eq. 1; Alg. 2 "verify")
+# --------------------------------------------------------------------------
+
+def verify_attn(k, v, q, seq_lens, gamma: int, scale: Optional[float] = None):
+    """p_L(. | x_<t; K_L^full) attention for the gamma+1 verifier rows (Eq. 1).
+
+    Row j of q [S][gamma+1][Hq][D] sits at position L_s - gamma - 1 + j and
+    sees keys 0 .. that position.  Returns out [S][gamma+1][Hq][D], lse [S][gamma+1][Hq].
+    """
+    S, R, Hq, D = q.shape
+    assert R == gamma + 1
+    Hkv = k[0].shape[0]
+    G = Hq // Hkv
+    sc = _scale64(scale, D)
+    out = np.zeros((S, R, Hq, D))
+    lse = np.full((S, R, Hq), -np.inf)
+    for s in range(S):
+        L = int(seq_lens[s])
+        qs = bf16_to_f64(q[s])                           # [R][Hq][D]
+        pos = L - gamma - 1 + np.arange(R)
+        t = np.arange(L)
+        vis_rows = t[None, :] <= pos[:, None]            # [R][L]
+        for g in range(Hkv):
+            kg = bf16_to_f64(k[s][g, :L])
+            vg = bf16_to_f64(v[s][g, :L])
+            qg = qs[:, g * G:(g + 1) * G, :].reshape(R * G, D)        # row-major (j, h)
+            vis = np.repeat(vis_rows, G, axis=0)
+            o, l = attend(qg, kg, vg, vis, sc)
+            out[s, :, g * G:(g + 1) * G] = o.reshape(R, G, D)
+            lse[s, :, g * G:(g + 1) * G] = l.reshape(R, G)
+    return out, lse
+
+
+# --------------------------------------------------------------------------
+# Multi-view block attention (Alg. 1 steps 3-4: full-cache and sparse-cache branches)
+# --------------------------------------------------------------------------
+
+def multiview_attn(k, v, q_blk, idx_views, nsel_views, seq_lens, scale: Optional[float] = None,
+                   with_full: bool = True):
+    """Continuation block attended under several sparse views and the full cache.
+
+    Alg. 1: the continuation rows attend Clone(K_S^full) (full branch, step 3)
+    and K_S^sp(B) for a sampled budget (sparse branch, step 4), with real
+    position ids.  Row c of q_blk [S][C][Hq][D] sits at position L_s - C + c.
+    View v sees {t in idx_views[v, s, g, :nsel] : t <= position}; the full
+    branch sees {t <= position}.
+    Returns out_views [V][S][C][Hq][D] and out_full [S][C][Hq][D] (or None).
+    """
+    S, C, Hq, D = q_blk.shape
+    nv = len(idx_views)
+    Hkv = k[0].shape[0]
+    G = Hq // Hkv
+    sc = _scale64(scale, D)
+    out_v = np.zeros((nv, S, C, Hq, D))
+    out_f = np.zeros((S, C, Hq, D)) if with_full else None
+    for s in range(S):
+        L = int(seq_lens[s])
+        qs = bf16_to_f64(q_blk[s])
+        pos = L - C + np.arange(C)
+        for g in range(Hkv):
+            qg = qs[:, g * G:(g + 1) * G, :].reshape(C * G, D)
+            kg_all = bf16_to_f64(k[s][g, :L])
+            vg_all = bf16_to_f64(v[s][g, :L])
+            for vi in range(nv):
+                J = _valid_entries(idx_views[vi][s, g], nsel_views[vi][s], L)
+                vis = np.repeat(J[None, :] <= pos[:, None], G, axis=0)
+                o, _ = attend(qg, kg_all[J], vg_all[J], vis, sc)
+                out_v[vi, s, :, g * G:(g + 1) * G] = o.reshape(C, G, D)
+            if with_full:
+                t = np.arange(L)
+                vis = np.repeat(t[None, :] <= pos[:, None], G, axis=0)
+                o, _ = attend(qg, kg_all, vg_all, vis, sc)
+                out_f[s, :, g * G:(g + 1) * G] = o.reshape(C, G, D)
+    return out_v, out_f
+
+
+# --------------------------------------------------------------------------
+# Greedy acceptance (Eq. 3; Alg. 2 accept and bonus token)
+# --------------------------------------------------------------------------
+
+def greedy_argmax(row: np.ndarray) -> int:
+    """argmax_v of one logit row, lowest index among equal maxima (Eq. 3, Eq. 5)."""
+    r = np.asarray(row, dtype=np.float64)
+    if not np.all(np.isfinite(r)):
+        raise ValueError("logits must be finite")
+    m = r.max()
+    return int(np.nonzero(r == m)[0][0])
+
+
+def accept_len(logits, draft, gamma: int):
+    """Accepted-prefix length and bonus token of greedy speculative decoding.
+
+    Eq. (3): draft i is accepted iff it equals the verifier's greedy token.
+    Alg. 2: k is the largest count with every draft i <= k accepted; the
+    verifier's token after the accepted prefix is appended as a bonus.
+    Indexing (0-based): logits row i is the verifier's prediction for draft i
+    (row 0 belongs to the last committed token); bonus = greedy token of row k.
+
+    logits [S][gamma+1][V] (any float), draft [S][gamma] int.
+    Returns accept [S], bonus [S], argmax [S][gamma+1], all int32.
+    """
+    S = len(logits)
+    am = np.zeros((S, gamma + 1), dtype=np.int32)
+    acc = np.zeros(S, dtype=np.int32)
+    bonus = np.zeros(S, dtype=np.int32)
+    for s in range(S):
+        for i in range(gamma + 1):
+            am[s, i] = greedy_argmax(logits[s][i])
+        kk = 0
+        while kk < gamma and int(draft[s][kk]) == am[s, kk]:
+            kk += 1
+        acc[s] = kk
+        bonus[s] = am[s, kk]
+    return acc, bonus, am

@@ -1,0 +1,494 @@
+"""Pins of the fp64 oracle to things other than itself (CPU only).
+
+Each test ties one oracle function to a closed form, an invariant, a library
+routine or brute force on a tiny input, chosen so that a plausible slip (a
+dropped term, an off-by-one in the causal range, a wrong head grouping, a
+transposed operand, a wrong tie rule) fails at least one of them.
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+
+SIG = float(np.float64(np.float32(1.0 / math.sqrt(128))))
+
+
+def bits(x):
+    return synth.f32_to_bf16_bits(np.asarray(x, dtype=np.float32))
+
+
+# ---------------------------------------------------------------- widening
+
+def test_bf16_widening_known_patterns():
+    b = np.array([0x3F80, 0xC040, 0x0001, 0x7F7F, 0x8000, 0x0000], dtype=np.uint16)
+    got = O.bf16_to_f64(b)
+    want = [1.0, -3.0, 2.0 ** -133, (2 - 2 ** -7) * 2.0 ** 127, -0.0, 0.0]
+    assert got.tolist() == want
+    assert math.copysign(1.0, got[4]) == -1.0
+
+
+def test_generator_rounding_is_rne():
+    x = np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -1.0 - 2 ** -8, 1.0 + 2 ** -8 + 2 ** -20], dtype=np.float32)
+    assert synth.f32_to_bf16_bits(x).tolist() == [0x3F80, 0x3F82, 0xBF80, 0x3F81]
+
+
+# ---------------------------------------------------------------- attention by definition
+
+def _pyloop_attend(q, k, v, vis, scale):
+    """Literal loops with math.exp: the textbook softmax-weighted sum."""
+    R, D = q.shape
+    out = [[0.0] * D for _ in range(R)]
+    for r in range(R):
+        ls = [(t, scale * sum(q[r][d] * k[t][d] for d in range(D))) for t in range(k.shape[0]) if vis[r][t]]
+        if not ls:
+            continue
+        m = max(l for _, l in ls)
+        z = sum(math.exp(l - m) for _, l in ls)
+        for t, l in ls:
+            w = math.exp(l - m) / z
+            for d in range(D):
+                out[r][d] += w * v[t][d]
+    return np.array(out)
+
+
+def test_attend_matches_python_loops_tiny():
+    g = np.random.default_rng(1)
+    q, k, v = g.standard_normal((3, 5)), g.standard_normal((7, 5)), g.standard_normal((7, 5))
+    vis = g.random((3, 7)) < 0.6
+    vis[:, 0] = True
+    o, _ = O.attend(q, k, v, vis, 0.37)
+    np.testing.assert_allclose(o, _pyloop_attend(q, k, v, vis, 0.37), rtol=1e-13, atol=1e-13)
+
+
+def test_attend_matches_torch_sdpa_fp64():
+    g = np.random.default_rng(2)
+    q, k, v = g.standard_normal((6, 128)), g.standard_normal((50, 128)), g.standard_normal((50, 128))
+    vis = g.random((6, 50)) < 0.5
+    vis[:, 3] = True
+    o, lse = O.attend(q, k, v, vis, SIG)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[None], torch.from_numpy(k)[None], torch.from_numpy(v)[None],
+        attn_mask=torch.from_numpy(vis)[None], scale=SIG)[0].numpy()
+    np.testing.assert_allclose(o, ref, rtol=1e-12, atol=1e-12)
+    lg = SIG * q @ k.T
+    ref_lse = [np.logaddexp.reduce(lg[r][vis[r]]) for r in range(6)]
+    np.testing.assert_allclose(lse, ref_lse, rtol=1e-13)
+
+
+def test_attend_two_key_closed_form():
+    # l1 = scale * a, l2 = 0 -> p1 = 1 / (1 + exp(-scale*a)); v1 = 1, v2 = 0 -> out = p1.
+    a = 3.0
+    q = np.zeros((1, 4)); q[0, 0] = 1.0
+    k = np.zeros((2, 4)); k[0, 0] = a
+    v = np.zeros((2, 4)); v[0, :] = 1.0
+    o, lse = O.attend(q, k, v, np.ones((1, 2), bool), 0.5)
+    assert abs(o[0, 0] - 1 / (1 + math.exp(-1.5))) < 1e-15
+    assert abs(lse[0] - math.log(math.exp(1.5) + 1.0)) < 1e-14
+
+
+def test_attend_empty_row():
+    o, lse = O.attend(np.ones((2, 4)), np.ones((3, 4)), np.ones((3, 4)), np.zeros((2, 3), bool), 1.0)
+    assert np.all(o == 0) and np.all(lse == -np.inf)
+
+
+# ---------------------------------------------------------------- selection: scores
+
+def _zero_k_raw(L, W, G):
+    """K == 0: every logit is 0, row i (position L-W+i) is uniform over L-W+i+1 keys."""
+    raw = np.zeros(L)
+    for i in range(W):
+        p = L - W + i
+        raw[:p + 1] += G / (p + 1)
+    return raw
+
+
+def test_window_scores_zero_k_closed_form():
+    L, W, G = 40, 6, 3
+    g = np.random.default_rng(3)
+    raw = O.window_scores(np.zeros((L, 16)), g.standard_normal((W, G, 16)), L, 0.25)
+    np.testing.assert_allclose(raw, _zero_k_raw(L, W, G), rtol=1e-14)
+    # prefix entries all equal; window entries strictly decreasing (fewer rows see later keys)
+    assert np.all(raw[:L - W] == raw[0])
+    assert np.all(np.diff(raw[L - W:]) < 0)
+
+
+def test_window_scores_sum_is_rows_times_heads():
+    g = np.random.default_rng(4)
+    L, W, G = 300, 8, 4
+    raw = O.window_scores(g.standard_normal((L, 32)), g.standard_normal((W, G, 32)), L, 0.3)
+    assert abs(raw.sum() - W * G) < 1e-11
+
+
+def test_window_scores_match_library_softmax():
+    from scipy.special import softmax
+    g = np.random.default_rng(5)
+    L, W, G, D = 25, 4, 2, 8
+    k, q = g.standard_normal((L, D)), g.standard_normal((W, G, D))
+    want = np.zeros(L)
+    for h in range(G):
+        for i in range(W):
+            p = L - W + i
+            want[:p + 1] += softmax(0.4 * (k[:p + 1] @ q[i, h]))
+    np.testing.assert_allclose(O.window_scores(k, q, L, 0.4), want, rtol=1e-13)
+
+
+def test_window_scores_last_key_seen_only_by_last_row():
+    # A key at L-1 with a huge logit: only row W-1 (at position L-1) sees it.
+    L, W, D = 20, 4, 4
+    k = np.zeros((L, D)); k[L - 1, 0] = 100.0
+    q = np.zeros((W, 1, D)); q[:, 0, 0] = 1.0
+    raw = O.window_scores(k, q, L, 1.0)
+    e = math.exp(100.0)
+    assert abs(raw[L - 1] - e / (e + L - 1)) < 1e-15
+    # rows 0..W-2 are uniform over their ranges and never see L-1
+    want0 = sum(1.0 / (L - W + i + 1) for i in range(W - 1)) + 1.0 / (e + L - 1)
+    assert abs(raw[0] - want0) < 1e-14
+
+
+# ---------------------------------------------------------------- selection: pooling and top-k
+
+def test_max_pool_matches_sliding_window_max():
+    from numpy.lib.stride_tricks import sliding_window_view
+    g = np.random.default_rng(6)
+    for n, kern in [(1, 7), (3, 7), (50, 7), (50, 1), (50, 3), (9, 9)]:
+        x = g.random(n)
+        r = kern // 2
+        padded = np.concatenate([np.full(r, -np.inf), x, np.full(r, -np.inf)])
+        want = sliding_window_view(padded, kern).max(axis=1)
+        np.testing.assert_array_equal(O.max_pool(x, kern), want)
+
+
+def _dominates(pooled, chosen):
+    """Every chosen candidate ranks above every other under (-pooled, position)."""
+    others = [t for t in range(len(pooled)) if t not in set(chosen)]
+    return all((-pooled[a], a) < (-pooled[b], b) for a in chosen for b in others)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_topk_brute_force_tiny(seed):
+    g = np.random.default_rng(100 + seed)
+    L, W, B = 14, 3, 7
+    raw = np.round(g.random(L) * 4) / 4          # coarse values -> many exact ties
+    sel, pooled = O.topk_from_scores(raw, L, W, B, 3)
+    keep = B - W
+    N = L - W
+    winners = [c for c in itertools.combinations(range(N), keep) if _dominates(pooled, c)]
+    assert len(winners) == 1
+    assert sel[:keep].tolist() == list(winners[0])
+    assert sel[keep:].tolist() == list(range(N, L))
+
+
+def test_topk_equals_stable_argsort_and_nests():
+    g = np.random.default_rng(7)
+    L, W = 500, 16
+    raw = np.floor(g.random(L) * 50)               # plenty of ties
+    prev = None
+    for B in [W, 40, 100, 200, 480]:
+        sel, pooled = O.topk_from_scores(raw, L, W, B, 7)
+        want = np.sort(np.argsort(-pooled, kind="stable")[:B - W])
+        assert sel[:B - W].tolist() == want.tolist()
+        if prev is not None:
+            assert set(prev) <= set(sel.tolist())
+        prev = sel.tolist()
+
+
+def test_topk_ties_take_lowest_positions():
+    sel, _ = O.topk_from_scores(np.ones(30), 30, 5, 12, 7)
+    assert sel.tolist() == list(range(7)) + list(range(25, 30))
+
+
+# ---------------------------------------------------------------- selection end to end
+
+def _cfg_small(L=256, Hq=8, Hkv=2, W=16):
+    g = np.random.default_rng(8)
+    k = bits(g.standard_normal((1, Hkv, L, 128)))
+    q = bits(g.standard_normal((1, W, Hq, 128)))
+    return k, q
+
+
+def test_select_identity_and_window_only():
+    k, q = _cfg_small()
+    idx, nsel, _ = O.select_kv(k, q, [256], 8, 16, 256)
+    assert nsel[0] == 256 and np.all(idx[0] == np.arange(256))
+    idx, nsel, _ = O.select_kv(k, q, [200], 8, 16, 300)
+    assert nsel[0] == 200 and np.all(idx[0, :, :200] == np.arange(200)) and np.all(idx[0, :, 200:] == -1)
+    idx, nsel, _ = O.select_kv(k, q, [256], 8, 16, 16)
+    assert nsel[0] == 16 and np.all(idx[0] == np.arange(240, 256))
+
+
+def test_select_zero_keys_takes_lowest_prefix():
+    _, q = _cfg_small()
+    k = np.zeros((1, 2, 256, 128), np.uint16)
+    idx, _, raws = O.select_kv(k, q, [256], 8, 16, 64)
+    assert np.all(idx[0] == np.r_[np.arange(48), np.arange(240, 256)])
+    np.testing.assert_allclose(raws[0][0], _zero_k_raw(256, 16, 4), rtol=1e-14)
+
+
+def test_select_single_spike_keeps_its_neighbourhood():
+    L, W, t0 = 256, 16, 100
+    g = np.random.default_rng(9)
+    q = np.zeros((1, W, 8, 128), np.float32); q[..., 0] = 1.0
+    k = 0.01 * g.standard_normal((1, 2, L, 128)).astype(np.float32)
+    k[0, :, t0, 0] = 60.0
+    idx, _, _ = O.select_kv(bits(k), bits(q), [L], 8, W, 32)
+    for gg in range(2):
+        assert set(range(t0 - 3, t0 + 4)) <= set(idx[0, gg].tolist())
+
+
+def test_select_uses_contiguous_head_groups():
+    # KV head 0 has one strong key; only query heads 4..7 (group 1 under h // G) point at it.
+    L, W = 128, 8
+    q = np.zeros((1, W, 8, 128), np.float32); q[0, :, 4:, 0] = 5.0
+    k = np.zeros((1, 2, L, 128), np.float32); k[0, 0, 10, 0] = 5.0
+    idx, _, raws = O.select_kv(bits(k), bits(q), [L], 8, W, 24)
+    np.testing.assert_allclose(raws[0][0], _zero_k_raw(L, W, 4), rtol=1e-14)   # group 0: q == 0
+    assert idx[0, 0, :16].tolist() == list(range(16))
+
+
+def test_select_config0_heavy_hitters_selected():
+    cfg = synth.CONFIGS[0]
+    L = cfg.seq_len
+    qt = synth.query_tail(cfg, 0)
+    k, _ = synth.kv_sequence(cfg, 0, q_tail=qt)
+    idx, nsel, raws = O.select_kv([k], [qt[-cfg.window:]], [L], cfg.num_q_heads, cfg.window, 256)
+    hh = synth.heavy_hitter_positions(cfg, L, 0)
+    assert nsel[0] == 256
+    for g in range(cfg.num_kv_heads):
+        prefix = idx[0, g, :256 - 32]
+        d = np.abs(prefix[:, None].astype(np.int64) - hh[None, :]).min(axis=1)
+        assert np.all(d <= 3)                               # every kept prefix slot is next to a hitter
+        assert abs(raws[0][g].sum() - 32 * 4) < 1e-9
+
+
+def test_select_rejects_bad_arguments():
+    k, q = _cfg_small()
+    for W, B, P in [(0, 64, 7), (16, 8, 7), (16, 64, 4)]:
+        with pytest.raises(ValueError):
+            O.select_kv(k, q[:, :max(W, 1)], [256], 8, W, B, P)
+
+
+# ---------------------------------------------------------------- sparse decode (Eq. 2)
+
+def _kv(S, Hkv, L, seed, v_const=None):
+    g = np.random.default_rng(seed)
+    k = bits(g.standard_normal((S, Hkv, L, 128)))
+    v = bits(g.standard_normal((S, Hkv, L, 128))) if v_const is None else bits(np.full((S, Hkv, L, 128), v_const))
+    return k, v
+
+
+def test_decode_single_entry_returns_its_value_row():
+    k, v = _kv(1, 2, 64, 10)
+    q = bits(np.random.default_rng(11).standard_normal((1, 8, 128)))
+    idx = np.full((1, 2, 4), -1, np.int32); idx[0, 0, 0] = 17; idx[0, 1, 0] = 5
+    out, lse = O.sparse_decode_attn(k, v, q, idx, [4], [64])
+    np.testing.assert_array_equal(out[0, :4], np.repeat(O.bf16_to_f64(v[0, 0, 17])[None], 4, 0))
+    np.testing.assert_array_equal(out[0, 4:], np.repeat(O.bf16_to_f64(v[0, 1, 5])[None], 4, 0))
+
+
+def test_decode_zero_query_is_mean_and_lse_log_n():
+    k, v = _kv(1, 2, 64, 12)
+    q = np.zeros((1, 8, 128), np.uint16)
+    idx = np.tile(np.array([1, 9, 30, 63, -1, 200], np.int32), (1, 2, 1))
+    out, lse = O.sparse_decode_attn(k, v, q, idx, [6], [64])
+    want = O.bf16_to_f64(v[0, 0, [1, 9, 30, 63]]).mean(0)
+    np.testing.assert_allclose(out[0, 0], want, rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(lse[0], math.log(4), rtol=1e-15)
+
+
+def test_decode_value_one_and_grouping():
+    S, Hkv, L = 2, 4, 32
+    g = np.random.default_rng(13)
+    k = bits(g.standard_normal((S, Hkv, L, 128)))
+    v = np.zeros((S, Hkv, L, 128), np.float32)
+    for gg in range(Hkv):
+        v[:, gg] = gg + 1.0                      # V == KV-head number + 1
+    q = bits(g.standard_normal((S, 8, 128)))
+    idx = np.tile(np.arange(0, 32, 3, dtype=np.int32), (S, Hkv, 1))
+    out, _ = O.sparse_decode_attn(k, bits(v), q, idx, [11, 11], [L, L])
+    for h in range(8):
+        np.testing.assert_allclose(out[:, h], h // 2 + 1.0, rtol=1e-14)
+
+
+def test_decode_is_order_invariant_and_nsel_clamps():
+    k, v = _kv(1, 2, 128, 14)
+    q = bits(np.random.default_rng(15).standard_normal((1, 8, 128)))
+    sel = np.random.default_rng(16).choice(128, 40, replace=False).astype(np.int32)
+    a, la = O.sparse_decode_attn(k, v, q, np.tile(np.sort(sel), (1, 2, 1)), [40], [128])
+    b, lb = O.sparse_decode_attn(k, v, q, np.tile(sel, (1, 2, 1)), [40], [128])
+    np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-13)
+    c, _ = O.sparse_decode_attn(k, v, q, np.tile(sel, (1, 2, 1)), [999], [128])   # nsel > ld_idx
+    np.testing.assert_allclose(a, c, rtol=1e-12, atol=1e-13)
+    e, le = O.sparse_decode_attn(k, v, q, np.tile(sel, (1, 2, 1)), [0], [128])
+    assert np.all(e == 0) and np.all(le == -np.inf)
+
+
+def test_decode_matches_torch_sdpa():
+    S, Hkv, G, L = 2, 2, 4, 96
+    k, v = _kv(S, Hkv, L, 17)
+    q = bits(np.random.default_rng(18).standard_normal((S, Hkv * G, 128)))
+    idx = np.stack([np.stack([synth.random_index_set(99, s, gg, L, 30) for gg in range(Hkv)]) for s in range(S)])
+    out, _ = O.sparse_decode_attn(k, v, q, idx, [30, 30], [L, L])
+    for s in range(S):
+        for h in range(Hkv * G):
+            J = idx[s, h // G]
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                torch.from_numpy(O.bf16_to_f64(q[s, h]))[None, None],
+                torch.from_numpy(O.bf16_to_f64(k[s, h // G, J]))[None],
+                torch.from_numpy(O.bf16_to_f64(v[s, h // G, J]))[None], scale=SIG)[0, 0].numpy()
+            np.testing.assert_allclose(out[s, h], ref, rtol=1e-12, atol=1e-13)
+
+
+# ---------------------------------------------------------------- verify (Eq. 1)
+
+def test_verify_causal_closed_form():
+    # K == 0, V[t] = t: row j (position L-gamma-1+j) averages 0..position -> position / 2.
+    S, Hkv, L, gamma = 1, 2, 50, 5
+    k = np.zeros((S, Hkv, L, 128), np.uint16)
+    v = bits(np.broadcast_to(np.arange(L, dtype=np.float32)[None, None, :, None], (S, Hkv, L, 128)))
+    q = bits(np.random.default_rng(19).standard_normal((S, gamma + 1, 8, 128)))
+    out, lse = O.verify_attn(k, v, q, [L], gamma)
+    for j in range(gamma + 1):
+        p = L - gamma - 1 + j
+        np.testing.assert_allclose(out[0, j], p / 2.0, rtol=1e-14)
+        np.testing.assert_allclose(lse[0, j], math.log(p + 1), rtol=1e-14)
+
+
+def test_verify_rows_equal_truncated_full_decode_and_gamma0():
+    S, Hkv, G, L, gamma = 1, 2, 4, 80, 4
+    k, v = _kv(S, Hkv, L, 20)
+    q = bits(np.random.default_rng(21).standard_normal((S, gamma + 1, Hkv * G, 128)))
+    out, lse = O.verify_attn(k, v, q, [L], gamma)
+    for j in range(gamma + 1):
+        p = L - gamma - 1 + j
+        idx = np.tile(np.arange(p + 1, dtype=np.int32), (S, Hkv, 1))
+        d, dl = O.sparse_decode_attn(k, v, q[:, j], idx, [p + 1], [L])
+        np.testing.assert_allclose(out[:, j], d, rtol=1e-12, atol=1e-13)
+        o0, _ = O.verify_attn(k[:, :, :p + 1], v[:, :, :p + 1], q[:, j:j + 1], [p + 1], 0)
+        np.testing.assert_allclose(o0[:, 0], d, rtol=1e-12, atol=1e-13)
+
+
+def test_verify_matches_torch_sdpa_causal():
+    S, Hkv, G, L, gamma = 2, 2, 2, 70, 5
+    k, v = _kv(S, Hkv, L, 22)
+    q = bits(np.random.default_rng(23).standard_normal((S, gamma + 1, Hkv * G, 128)))
+    out, _ = O.verify_attn(k, v, q, [L, L], gamma)
+    mask = np.arange(L)[None, :] <= (L - gamma - 1 + np.arange(gamma + 1))[:, None]
+    for s in range(S):
+        for h in range(Hkv * G):
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                torch.from_numpy(O.bf16_to_f64(q[s, :, h]))[None],
+                torch.from_numpy(O.bf16_to_f64(k[s, h // G]))[None],
+                torch.from_numpy(O.bf16_to_f64(v[s, h // G]))[None],
+                attn_mask=torch.from_numpy(mask)[None], scale=SIG)[0].numpy()
+            np.testing.assert_allclose(out[s, :, h], ref, rtol=1e-12, atol=1e-13)
+
+
+def test_verify_ragged_lengths():
+    S, Hkv, Lmax, gamma = 2, 1, 40, 2
+    k, v = _kv(S, Hkv, Lmax, 24)
+    q = bits(np.random.default_rng(25).standard_normal((S, gamma + 1, 2, 128)))
+    out, _ = O.verify_attn(k, v, q, [40, 17], gamma)
+    o1, _ = O.verify_attn(k[1:, :, :17], v[1:, :, :17], q[1:], [17], gamma)
+    np.testing.assert_array_equal(out[1:], o1)
+
+
+# ---------------------------------------------------------------- multi-view (Alg. 1)
+
+def test_multiview_cross_identities():
+    S, Hkv, G, L, C = 1, 2, 2, 90, 8
+    k, v = _kv(S, Hkv, L, 26)
+    q = bits(np.random.default_rng(27).standard_normal((S, C, Hkv * G, 128)))
+    full_idx = np.tile(np.arange(L, dtype=np.int32), (S, Hkv, 1))
+    sub = np.stack([np.stack([np.r_[synth.random_index_set(5, 0, gg, L - C, 20), np.arange(L - C, L)]
+                              for gg in range(Hkv)])]).astype(np.int32)
+    ov, of = O.multiview_attn(k, v, q, [full_idx, sub], [[L], [28]], [L])
+    np.testing.assert_allclose(ov[0], of, rtol=1e-12, atol=1e-13)           # B >= L view == full branch
+    d, _ = O.sparse_decode_attn(k, v, q[:, C - 1], sub, [28], [L])          # last row == decode
+    np.testing.assert_allclose(ov[1, :, C - 1], d, rtol=1e-12, atol=1e-13)
+    vf, _ = O.verify_attn(k, v, q, [L], C - 1)                              # full branch == verify
+    np.testing.assert_allclose(of, vf, rtol=1e-12, atol=1e-13)
+
+
+def test_multiview_causal_closed_form():
+    S, Hkv, L, C = 1, 1, 40, 6
+    k = np.zeros((S, Hkv, L, 128), np.uint16)
+    v = bits(np.broadcast_to(np.arange(L, dtype=np.float32)[None, None, :, None], (S, Hkv, L, 128)))
+    q = bits(np.random.default_rng(28).standard_normal((S, C, 2, 128)))
+    J = np.array([[[3, 11, 20, 34, 35, 36, 37, 38, 39]]], np.int32)
+    ov, of = O.multiview_attn(k, v, q, [J], [[9]], [L])
+    for c in range(C):
+        p = L - C + c
+        np.testing.assert_allclose(ov[0, 0, c], np.mean([t for t in J[0, 0] if t <= p]), rtol=1e-14)
+        np.testing.assert_allclose(of[0, c], p / 2.0, rtol=1e-14)
+
+
+# ---------------------------------------------------------------- accept (Eq. 3, Alg. 2)
+
+def test_accept_planted_prefix_lengths():
+    cfg = synth.CONFIGS[2]
+    for s in range(cfg.num_seqs):
+        lg, dr, tok, m = synth.logits_and_drafts(cfg, s, vocab=3000)
+        acc, bonus, am = O.accept_len(lg[None], dr[None], cfg.gamma)
+        assert am[0].tolist() == tok.tolist()
+        assert acc[0] == m and bonus[0] == tok[m]
+
+
+def test_accept_matches_numpy_argmax_and_range():
+    g = np.random.default_rng(29)
+    lg = np.floor(g.standard_normal((5, 4, 40)) * 2).astype(np.float32)     # many ties
+    dr = g.integers(0, 40, (5, 3)).astype(np.int32)
+    dr[0] = [int(np.argmax(lg[0, i])) for i in range(3)]                     # fully accepted row
+    acc, bonus, am = O.accept_len(lg, dr, 3)
+    assert am.tolist() == np.argmax(lg, axis=2).tolist()                     # first occurrence
+    assert acc[0] == 3 and bonus[0] == am[0, 3]
+    assert np.all((acc >= 0) & (acc <= 3))
+    for s in range(5):
+        kk = 0
+        while kk < 3 and dr[s, kk] == am[s, kk]:
+            kk += 1
+        assert acc[s] == kk and bonus[s] == am[s, kk]
+
+
+def test_accept_gamma0_and_signed_zero_tie():
+    lg = np.zeros((1, 1, 8), np.float32)
+    lg[0, 0, 2] = -0.0
+    acc, bonus, am = O.accept_len(lg, np.zeros((1, 0), np.int32), 0)
+    assert acc[0] == 0 and bonus[0] == 0 and am[0, 0] == 0
+    lg = np.full((1, 1, 8), -1.0, np.float32); lg[0, 0, 5] = -0.0; lg[0, 0, 6] = 0.0
+    assert O.accept_len(lg, np.zeros((1, 0), np.int32), 0)[1][0] == 5
+
+
+def test_accept_rejects_nan():
+    lg = np.zeros((1, 2, 4), np.float32); lg[0, 1, 1] = np.nan
+    with pytest.raises(ValueError):
+        O.accept_len(lg, np.zeros((1, 1), np.int32), 1)
+
+
+# ---------------------------------------------------------------- hand-derived golden fixtures
+
+def _golden():
+    import json
+    import os
+    with open(os.path.join(os.path.dirname(__file__), "golden", "closed_forms.json")) as f:
+        return json.load(f)
+
+
+def test_golden_select_zero_keys():
+    gd = _golden()["select_zero_keys"]
+    L, W, G, B = gd["L"], gd["W"], gd["G"], gd["B"]
+    q = bits(np.random.default_rng(30).standard_normal((1, W, G, 128)))
+    idx, nsel, raws = O.select_kv(np.zeros((1, 1, L, 128), np.uint16), q, [L], G, W, B)
+    want = [n / d for n, d in gd["raw_num_den"]]
+    np.testing.assert_allclose(raws[0][0], want, rtol=1e-15)
+    assert idx[0, 0].tolist() == gd["idx"] and nsel[0] == B
+
+
+def test_golden_accept_worked_example():
+    gd = _golden()["accept_worked"]
+    acc, bonus, am = O.accept_len(np.array([gd["logits"]], np.float32), np.array([gd["draft"]], np.int32), gd["gamma"])
+    assert am[0].tolist() == gd["argmax"] and acc[0] == gd["accept"] and bonus[0] == gd["bonus"]
