@@ -1,0 +1,244 @@
+#!/usr/bin/env python3
+"""Speculative-decoding step of the sparse-drafter / full-verifier path on one MI355X.
+
+Workload (16K collapse regime): 8 sequences x 16,384 cached tokens, 32 query
+heads, 8 KV heads, head_dim 128, bf16 caches; drafter budget B = 1024 (the
+selection runs once, outside the timed step, as after prefill); draft length
+gamma = 5; vocab 128,256.  A step is one pass of Alg. 2's per-round work:
+
+    gamma x bd_sparse_decode_attn   (drafter cache, B selected entries)
+    1     x bd_verify_attn          (verifier cache, gamma+1 rows, full KV)
+    1     x bd_accept_len           (fp32 logits [8][6][128256])
+
+The drafter and the verifier have separate caches of the same shape.  The step
+is captured once in a HIP graph and replayed; inputs stay resident in HBM.
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "draft+verify attention µs/step and HBM GB/s at 16K ctx, B=1024, γ=5"
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--budget", type=int, default=1024)
+    ap.add_argument("--kernel-iters", type=int, default=20, help="eager steps timed kernel by kernel")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(S, Hq, Hkv, L, B, gamma, V, D=128):
+    """Bytes each call must move at least once (K/V once per KV head, q, idx, outputs, logits)."""
+    dec = S * Hkv * B * D * 2 * 2 + S * Hkv * B * 4 + 2 * S * Hq * D * 2
+    ver = S * Hkv * L * D * 2 * 2 + 2 * S * (gamma + 1) * Hq * D * 2
+    acc = S * (gamma + 1) * V * 4 + S * gamma * 4
+    return dec, ver, acc
+
+
+def traffic_from_profile(kernel_src_hash: str):
+    """HBM bytes per verify launch from the committed rocprofv3 counter summary, if it was
+    taken on the current kernel source; otherwise None."""
+    path = os.path.join(ROOT, "profiles", "verify_attn_16k_b8_counters.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("attn_source_sha256") != kernel_src_hash:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(host, S, Hq, L, B, gamma):
+    """The fp64 oracle, as it stands, on one full step of the same workload (host cores)."""
+    import numpy as np
+
+    import oracle as O
+    import synth
+
+    threads = len(os.sched_getaffinity(0))
+    qs, kS, vS, kL, vL, logits, draft = host
+    lens = [L] * S
+    cfg = synth.CONFIGS[2]
+    idx = np.stack([np.stack([np.r_[synth.random_index_set(2, s, g, L - cfg.window, B - cfg.window),
+                                    np.arange(L - cfg.window, L)] for g in range(cfg.num_kv_heads)])
+                    for s in range(S)]).astype(np.int32)
+    t0 = time.perf_counter()
+    for i in range(gamma):
+        O.sparse_decode_attn(kS, vS, qs[:, -(gamma + 1) + i], idx, [B] * S, lens)
+    O.verify_attn(kL, vL, qs[:, -(gamma + 1):], lens, gamma)
+    O.accept_len(logits, draft, gamma)
+    dt = time.perf_counter() - t0
+    return {"value": round(dt * 1e6, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
+            "sample": f"one full step (5 sparse decodes B={B}, verify, accept) on all {S} sequences, fp64 numpy"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the path needs no collectives (sequences and KV heads are "
+              "independent); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2606_00144_amd as bd
+    import synth
+
+    torch.cuda.init()
+    dev = torch.device("cuda:0")
+    cfg = synth.CONFIGS[2]
+    S, Hq, Hkv, L, W, gamma, V = (cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.window,
+                                  cfg.gamma, cfg.vocab)
+    B = args.budget
+
+    log("generating inputs")
+    qs, kS, vS = synth.kv_batch(cfg)
+    _, kL, vL = synth.kv_batch(cfg, tag_k=synth.TAG_K_VERIFIER, tag_v=synth.TAG_V_VERIFIER)
+    lg = [synth.logits_and_drafts(cfg, s) for s in range(S)]
+    host = (np.stack(qs), np.stack(kS), np.stack(vS), np.stack(kL), np.stack(vL),
+            np.stack([x[0] for x in lg]), np.stack([x[1] for x in lg]))
+
+    def bf(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    q_all = bf(host[0])                                           # [S][T][Hq][D]
+    kS_d, vS_d, kL_d, vL_d = bf(host[1]), bf(host[2]), bf(host[3]), bf(host[4])
+    logits = torch.from_numpy(host[5]).to(dev)
+    draft = torch.from_numpy(host[6]).to(dev)
+    lens = torch.full((S,), L, dtype=torch.int32, device=dev)
+    T = q_all.shape[1]
+    q_dec = [q_all[:, T - gamma - 1 + i].contiguous() for i in range(gamma)]
+    q_ver = q_all[:, T - gamma - 1:].contiguous()
+    q_win = q_all[:, T - W:].contiguous()
+
+    log("selecting the drafter's sparse cache (once, as after prefill)")
+    idx, nsel = bd.bd_select_kv(kS_d, q_win, lens, B)
+    torch.cuda.synchronize()
+
+    out_dec = torch.empty((gamma, S, Hq, 128), dtype=torch.bfloat16, device=dev)
+    out_ver = torch.empty_like(q_ver)
+    acc = torch.empty((S,), dtype=torch.int32, device=dev)
+    bonus = torch.empty((S,), dtype=torch.int32, device=dev)
+    ws_dec, ws_ver, ws_acc = bd.Workspace(), bd.Workspace(), bd.Workspace()
+
+    def decode(i):
+        bd.bd_sparse_decode_attn(kS_d, vS_d, q_dec[i], idx, nsel, lens, out=out_dec[i], workspace=ws_dec)
+
+    def verify():
+        bd.bd_verify_attn(kL_d, vL_d, q_ver, lens, out=out_ver, workspace=ws_ver)
+
+    def accept():
+        bd.bd_accept_len(logits, draft, workspace=ws_acc, outputs=(acc, bonus, None))
+
+    def step():
+        for i in range(gamma):
+            decode(i)
+        verify()
+        accept()
+
+    # eager reference step, then capture the step once in a HIP graph
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    ref = (out_dec.clone(), out_ver.clone(), acc.clone(), bonus.clone())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for r in range(3):                                            # every replay matches the eager step
+        graph.replay()
+        torch.cuda.synchronize()
+        got = (out_dec, out_ver, acc, bonus)
+        for a, b in zip(got, ref):
+            assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a,
+                               b.view(torch.int16) if b.dtype == torch.bfloat16 else b), f"graph replay {r}"
+        step()                                                    # eager work between replays
+        torch.cuda.synchronize()
+    planted = [x[3] for x in lg]
+    assert acc.cpu().tolist() == planted, "accept lengths differ from the planted prefixes"
+
+    log(f"timing {args.steps} graph replays after {args.warmup} warm-up")
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    us_step = wall * 1e6 / args.steps
+
+    # per-kernel durations: HIP events around each launch, on the stream the kernel runs on
+    log("timing kernels one by one")
+    names = ["sparse_decode_attn"] * gamma + ["verify_attn", "accept_len"]
+    fns = [lambda i=i: decode(i) for i in range(gamma)] + [verify, accept]
+    times = {n: [] for n in set(names)}
+    ev = []
+    for _ in range(args.kernel_iters):
+        for n, fn in zip(names, fns):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            ev.append((n, a, b))
+    torch.cuda.synchronize()
+    for n, a, b in ev:
+        times[n].append(a.elapsed_time(b) * 1e3)
+    kern_us = {n: float(np.median(v)) for n, v in times.items()}
+
+    dec_b, ver_b, acc_b = algorithmic_bytes(S, Hq, Hkv, L, B, gamma, V)
+    step_bytes = gamma * dec_b + ver_b + acc_b
+    src_hash = hashlib.sha256(open(os.path.join(ROOT, "paper_2606_00144_amd", "csrc", "attn.hip"), "rb").read()).hexdigest()
+    ver_gbs = ver_b / (kern_us["verify_attn"] * 1e-6) / 1e9
+    roofline = {"bound": "hbm", "kernel": "verify_attn", "achieved": round(ver_gbs, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(ver_gbs / HBM_PEAK_GBS, 4), "traffic": traffic_from_profile(src_hash),
+                "bytes_per_launch": ver_b, "avg_us": round(kern_us["verify_attn"], 2)}
+
+    result = {
+        "metric": METRIC, "value": round(us_step, 2), "unit": "us/step", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(us_step / 1e3, 5),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 K/V/Q with 0.5% planted heavy hitters; planted-argmax fp32 logits)",
+        "config": {"workload": "16k-collapse-b8: 8 seqs x 16384 ctx, 32 q heads / 8 kv heads x 128, "
+                               f"B={B}, gamma={gamma}, vocab {V}, separate drafter and verifier caches",
+                   "num_seqs": S, "seq_len": L, "budget": B, "gamma": gamma, "vocab": V},
+        "step_gbps": round(step_bytes / (us_step * 1e-6) / 1e9, 1),
+        "step_bytes": step_bytes,
+        "kernels_us": {n: round(v, 2) for n, v in kern_us.items()},
+        "kernels_gbps": {"sparse_decode_attn": round(dec_b / (kern_us["sparse_decode_attn"] * 1e-6) / 1e9, 1),
+                         "verify_attn": round(ver_gbs, 1),
+                         "accept_len": round(acc_b / (kern_us["accept_len"] * 1e-6) / 1e9, 1)},
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on the host (one step)")
+        result["cpu_baseline"] = cpu_baseline(host, S, Hq, L, B, gamma)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,208 @@
+/*
+ * libbd: the BudgetDraft sparse-drafter / full-verifier hot path on MI355X (gfx950).
+ *
+ * Greedy speculative decoding with a drafter that reads a budgeted subset of
+ * its KV cache and a verifier that reads its full cache (Sec. 3.1, Alg. 2),
+ * and the continuation-block attention of multi-view training (Alg. 1).
+ * Five operations, each an asynchronous launch on a caller-given HIP stream:
+ *
+ *   bd_select_kv           budgeted KV selection (Alg. 2 "sparsify")
+ *   bd_sparse_decode_attn  drafter attention over the selected entries (Eq. 2)
+ *   bd_multiview_attn      a query block under several budgets + the full cache (Alg. 1)
+ *   bd_verify_attn         verifier attention at the gamma+1 draft positions (Eq. 1)
+ *   bd_accept_len          greedy accepted-prefix length and bonus token (Eq. 3)
+ *
+ * Common conventions
+ *   - Tensors are raw device pointers.  bf16 data are passed as uint16_t bit
+ *     patterns; head_dim must be 128.
+ *   - GQA: query head h reads KV head h / G, G = num_q_heads / num_kv_heads.
+ *   - Positions: sequence s holds cache rows 0 .. L_s-1 (L_s = seq_lens[s]),
+ *     query rows included.  A query at position p sees keys t with 0 <= t <= p.
+ *     Keys and queries are post-RoPE; positions are used only for the causal rule.
+ *   - Softmax scale is the caller's `scale` (normally 1/sqrt(128)); softmax and
+ *     accumulation are fp32, outputs are rounded to bf16 (nearest-even), and
+ *     log-sum-exp outputs are fp32 natural logs.  A row with no visible key
+ *     gets output 0 and log-sum-exp -inf.
+ *   - Ownership: the caller owns every buffer; inputs are only read; outputs
+ *     are overwritten in full; the library keeps no pointer after returning.
+ *   - Workspace: each operation takes caller-allocated device memory of at
+ *     least bd_<op>_workspace_bytes(...) bytes (256-byte aligned).  It must be
+ *     all zero before its first use; every call that runs to completion leaves
+ *     its counters at zero again, so one workspace can serve any number of
+ *     later calls of the SAME operation issued on the same stream.  Calls that
+ *     overlap in time (two streams) must not share a workspace.  The library
+ *     never allocates device memory.
+ *   - Errors: arguments are checked on the host before anything is launched;
+ *     on error nothing is launched and no output is touched.  A launch failure
+ *     reported by the HIP runtime is BD_ERR_DEVICE.  No C++ exception crosses
+ *     this interface.  bd_last_error() gives the reason of the last failure
+ *     on the calling thread.
+ *   - Device-side bounds: entries of idx outside [0, L_s) are skipped, counts
+ *     above the stated maxima are clamped, and paged keys whose page number is
+ *     outside [0, num_pages) are skipped, so malformed device data cannot make
+ *     a kernel read out of bounds.
+ */
+#ifndef BD_H_
+#define BD_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BD_ABI_VERSION 1
+#define BD_HEAD_DIM 128
+/* Longest candidate prefix L_s - W that bd_select_kv ranks in one pass. */
+#define BD_SELECT_MAX_PREFIX 32768
+
+typedef int32_t bd_status;
+#define BD_OK 0
+#define BD_ERR_INVALID_ARG 1 /* a pointer, size or shape that the contract forbids */
+#define BD_ERR_UNSUPPORTED 2 /* a valid request this build does not implement (head_dim != 128, ...) */
+#define BD_ERR_WORKSPACE 3   /* workspace missing, too small or misaligned */
+#define BD_ERR_DEVICE 4      /* the HIP runtime rejected a launch */
+
+/* KV cache of one layer: K and V of every sequence and KV head.
+ *
+ * Contiguous layout (page_table == NULL): element (s, g, t, d) lives at
+ *   s*stride_seq + g*stride_head + t*stride_tok + d          (elements).
+ * Paged layout (page_table != NULL): element (s, g, t, d) lives at
+ *   page_table[s*max_pages_per_seq + t/page_size]*stride_page
+ *     + g*stride_head + (t % page_size)*stride_tok + d.
+ * In both layouts d is contiguous.  K and V share the layout. */
+typedef struct bd_kv_desc {
+  const uint16_t* k;          /* bf16 keys */
+  const uint16_t* v;          /* bf16 values (ignored, may be NULL, for bd_select_kv) */
+  int32_t num_seqs;           /* S >= 1 */
+  int32_t num_kv_heads;       /* Hkv >= 1 */
+  int32_t head_dim;           /* must be 128 */
+  int32_t max_seq_len;        /* host bound: every seq_lens[s] <= max_seq_len */
+  const int32_t* seq_lens;    /* device [S]: L_s, clamped to [0, max_seq_len] */
+  int64_t stride_seq;         /* contiguous layout only */
+  int64_t stride_head;
+  int64_t stride_tok;
+  const int32_t* page_table;  /* NULL, or device [S][max_pages_per_seq] page numbers */
+  int32_t page_size;          /* paged: tokens per page (>= 1) */
+  int32_t max_pages_per_seq;  /* paged: max_seq_len <= max_pages_per_seq * page_size */
+  int32_t num_pages;          /* paged: pages in the pool */
+  int64_t stride_page;        /* paged: elements between pages */
+} bd_kv_desc;
+
+const char* bd_status_string(bd_status status);
+/* Reason of the last non-BD_OK status returned on this thread (static storage). */
+const char* bd_last_error(void);
+int32_t bd_abi_version(void);
+
+/* ------------------------------------------------------------------------
+ * bd_select_kv -- budgeted KV selection, K_S^sp(B) of Eq. (2).
+ *
+ * Alg. 2 sparsifies the drafter's prefix cache once after prefill; Sec. 3.4
+ * keeps the entries with the largest cumulative attention weight.  For every
+ * sequence s and KV head g:
+ *   1. raw[t] = sum over the G query heads of g and the W observation rows i
+ *      (row i at position L_s-W+i) of softmax_t(scale * <q_{h,i}, k_t>), each
+ *      row normalised over its causal range t <= L_s-W+i;
+ *   2. pooled[t] = max of raw over [t-r, t+r] cut to [0, N), r = pool_kernel/2,
+ *      for the N = L_s - W prefix positions;
+ *   3. keep the B - W prefix positions ranked first by (pooled descending,
+ *      position ascending), in ascending order, then append the W window
+ *      positions N .. L_s-1.
+ * If B >= L_s every position 0 .. L_s-1 is kept (the sparse cache is the full
+ * cache) and the scores of that sequence are not computed.
+ *
+ * q_win      [S][W][Hq][128] bf16: the last W query rows of each sequence.
+ * lse_win    NULL, or [S][W][Hq] fp32 natural-log log-sum-exp of each window
+ *            row over its causal range; when given, one pass over K suffices.
+ * idx_out    [S][Hkv][budget] int32 ascending positions; slots past nsel = -1.
+ * nsel_out   [S] int32: min(budget, L_s).
+ * scores_out NULL, or [S][Hkv][max_seq_len] fp32 raw scores (step 1) for
+ *            t < L_s of every sequence with B < L_s; other entries untouched.
+ * Requirements: 1 <= window <= budget; pool_kernel odd >= 1; every
+ * L_s >= window; max_seq_len - window <= BD_SELECT_MAX_PREFIX; K only (kv->v unused).
+ * ---------------------------------------------------------------------- */
+size_t bd_select_kv_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
+                                    int32_t window, int32_t max_seq_len);
+bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_heads, int32_t window,
+                       int32_t budget, int32_t pool_kernel, float scale, const float* lse_win,
+                       int32_t* idx_out, int32_t* nsel_out, float* scores_out,
+                       void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * bd_sparse_decode_attn -- drafter decode attention over K_S^sp(B) (Eq. 2; Alg. 2 "draft").
+ *
+ * One query per head at position L_s-1 attends the entries
+ * idx[s][g][0 .. nsel[s]-1] of its KV head (entries outside [0, L_s) are
+ * skipped; order does not matter).
+ * q       [S][Hq][128] bf16.
+ * idx     [S][Hkv][ld_idx] int32; nsel [S] int32, clamped to [0, ld_idx].
+ * out     [S][Hq][128] bf16; lse_out NULL or [S][Hq] fp32.
+ * ---------------------------------------------------------------------- */
+size_t bd_sparse_decode_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
+                                             int32_t ld_idx);
+bd_status bd_sparse_decode_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads,
+                                const int32_t* idx, int32_t ld_idx, const int32_t* nsel, float scale,
+                                uint16_t* out, float* lse_out,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * bd_multiview_attn -- continuation block under several sparse views and
+ * the full cache (Alg. 1 steps 3 and 4).
+ *
+ * Row c of the block sits at position L_s - C + c.  Under view v it sees
+ * {t in idx_views[v][s][g][0 .. nsel_views[v][s]-1] : t <= its position};
+ * under the full branch it sees every t <= its position.
+ * q_blk      [S][C][Hq][128] bf16.
+ * idx_views  [V][S][Hkv][ld_idx] int32; nsel_views [V][S] int32.
+ * out_views  [V][S][C][Hq][128] bf16 (may be NULL only when V == 0).
+ * out_full   NULL (full branch skipped) or [S][C][Hq][128] bf16.
+ * Requirements: C >= 1, V >= 0, V + (out_full != NULL) >= 1.
+ * ---------------------------------------------------------------------- */
+size_t bd_multiview_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
+                                         int32_t block_len, int32_t num_views, int32_t ld_idx,
+                                         int32_t max_seq_len, int32_t with_full);
+bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t num_q_heads, int32_t block_len,
+                            int32_t num_views, const int32_t* idx_views, int32_t ld_idx,
+                            const int32_t* nsel_views, float scale, uint16_t* out_views, uint16_t* out_full,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * bd_verify_attn -- verifier attention over the full cache at the gamma+1
+ * draft positions (Eq. 1; Alg. 2 "verify").
+ *
+ * Row j (0 .. gamma) sits at position L_s - gamma - 1 + j and sees keys
+ * 0 .. that position (causal among the drafts).
+ * q       [S][gamma+1][Hq][128] bf16.
+ * out     [S][gamma+1][Hq][128] bf16; lse_out NULL or [S][gamma+1][Hq] fp32.
+ * ---------------------------------------------------------------------- */
+size_t bd_verify_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
+                                      int32_t gamma, int32_t max_seq_len);
+bd_status bd_verify_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, int32_t gamma, float scale,
+                         uint16_t* out, float* lse_out,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * bd_accept_len -- greedy acceptance (Eq. 3; Alg. 2 accept + bonus token).
+ *
+ * a*_i = lowest index among the maxima of logits row i (i = 0 .. gamma;
+ * -0.0 equals +0.0).  Row i is the verifier's prediction for draft i.
+ * accept = largest k <= gamma with draft[i] == a*_i for every i < k;
+ * bonus = a*_k.
+ * logits  row (s, i) at logits + (s*(gamma+1) + i) * row_stride, fp32, finite.
+ * draft   [S][gamma] int32.
+ * accept_out [S] int32; bonus_out NULL or [S]; argmax_out NULL or [S][gamma+1].
+ * Requirements: gamma >= 0, vocab >= 1, row_stride >= vocab.
+ * ---------------------------------------------------------------------- */
+size_t bd_accept_len_workspace_bytes(int32_t num_seqs, int32_t gamma, int32_t vocab);
+bd_status bd_accept_len(const float* logits, int64_t row_stride, const int32_t* draft, int32_t num_seqs,
+                        int32_t gamma, int32_t vocab, int32_t* accept_out, int32_t* bonus_out,
+                        int32_t* argmax_out, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BD_H_ */

@@ -65,17 +65,15 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, visible: np.ndarray, sca
     lse = np.full(R, -np.inf, dtype=np.float64)
     if k.shape[0] == 0:
         return out, lse
+    visible = np.asarray(visible, dtype=bool)
+    has = visible.any(axis=1)                        # rows with at least one key
     logits = scale * (q @ k.T)                       # [R][N]
-    for r in range(R):
-        sel = np.nonzero(visible[r])[0]
-        if sel.size == 0:
-            continue
-        lr = logits[r, sel]
-        m = lr.max()
-        e = np.exp(lr - m)
-        z = e.sum()
-        out[r] = (e @ v[sel]) / z
-        lse[r] = m + np.log(z)
+    m = np.where(visible, logits, -np.inf).max(axis=1)
+    m = np.where(has, m, 0.0)
+    e = np.where(visible, np.exp(np.where(visible, logits, 0.0) - m[:, None]), 0.0)   # unnormalised weights
+    z = e.sum(axis=1)
+    out[has] = (e[has] @ v) / z[has, None]
+    lse[has] = m[has] + np.log(z[has])
     return out, lse
 
 

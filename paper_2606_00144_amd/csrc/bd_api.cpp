@@ -1,0 +1,288 @@
+// C ABI of libbd: host-side argument checks, workspace sizing and launches.
+//
+// Every entry point validates its arguments completely before touching the
+// HIP runtime, so a rejected call launches nothing and leaves outputs alone.
+// The only HIP calls made are kernel launches and hipGetLastError.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+
+#include "bd.h"
+#include "bd_kernels.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+bd_status fail(bd_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Checks shared by every operation that reads the KV cache.
+bd_status check_kv(const bd_kv_desc* kv, bool need_v, int32_t num_q_heads) {
+  if (!kv) return fail(BD_ERR_INVALID_ARG, "kv descriptor is NULL");
+  if (kv->head_dim != BD_HEAD_DIM) return fail(BD_ERR_UNSUPPORTED, "head_dim %d is not 128", kv->head_dim);
+  if (!kv->k || (need_v && !kv->v)) return fail(BD_ERR_INVALID_ARG, "K or V pointer is NULL");
+  if (!aligned(kv->k, 16) || (need_v && !aligned(kv->v, 16)))
+    return fail(BD_ERR_INVALID_ARG, "K and V must be 16-byte aligned");
+  if (!kv->seq_lens) return fail(BD_ERR_INVALID_ARG, "seq_lens is NULL");
+  if (kv->num_seqs < 1 || kv->num_kv_heads < 1) return fail(BD_ERR_INVALID_ARG, "num_seqs and num_kv_heads must be >= 1");
+  if (kv->max_seq_len < 0) return fail(BD_ERR_INVALID_ARG, "max_seq_len < 0");
+  if (num_q_heads < 1 || num_q_heads % kv->num_kv_heads != 0)
+    return fail(BD_ERR_INVALID_ARG, "num_q_heads %d is not a positive multiple of num_kv_heads %d", num_q_heads,
+                kv->num_kv_heads);
+  if (kv->stride_head < 0 || kv->stride_tok < 0 || kv->stride_head % 8 || kv->stride_tok % 8)
+    return fail(BD_ERR_INVALID_ARG, "stride_head and stride_tok must be non-negative multiples of 8 elements");
+  if (kv->page_table) {
+    if (kv->page_size < 1 || kv->max_pages_per_seq < 1 || kv->num_pages < 1)
+      return fail(BD_ERR_INVALID_ARG, "paged layout needs page_size, max_pages_per_seq and num_pages >= 1");
+    if ((int64_t)kv->max_seq_len > (int64_t)kv->max_pages_per_seq * kv->page_size)
+      return fail(BD_ERR_INVALID_ARG, "max_seq_len exceeds max_pages_per_seq * page_size");
+    if (kv->stride_page < 0 || kv->stride_page % 8)
+      return fail(BD_ERR_INVALID_ARG, "stride_page must be a non-negative multiple of 8 elements");
+  } else {
+    if (kv->stride_seq < 0 || kv->stride_seq % 8)
+      return fail(BD_ERR_INVALID_ARG, "stride_seq must be a non-negative multiple of 8 elements");
+  }
+  return BD_OK;
+}
+
+bd_status check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return BD_OK;
+  if (!ws) return fail(BD_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", need);
+  if (!aligned(ws, 256)) return fail(BD_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (have < need) return fail(BD_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  return BD_OK;
+}
+
+bd_status launched(hipError_t e) {
+  if (e != hipSuccess) return fail(BD_ERR_DEVICE, "launch failed: %s", hipGetErrorString(e));
+  return BD_OK;
+}
+
+// Common launch of the attention kernel.
+bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t nq, int32_t num_views,
+                   const int32_t* idx, int32_t ld_idx, const int32_t* nsel, float scale, uint16_t* out_views,
+                   float* lse_views, uint16_t* out_full, float* lse_full, void* ws, size_t ws_bytes,
+                   hipStream_t stream) {
+  const bd::AttnPlan pl =
+      bd::plan_attn(kv->num_seqs, kv->num_kv_heads, Hq, nq, num_views, ld_idx, kv->max_seq_len, out_full != nullptr);
+  if (pl.nblk < 0 || (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f > INT32_MAX)
+    return fail(BD_ERR_UNSUPPORTED, "problem too large for one launch");
+  bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
+  if (st != BD_OK) return st;
+  if (pl.nblk == 0) return BD_OK;
+  bd::AttnParams p{};
+  p.kv = bd::make_kv_view(*kv);
+  p.q = q;
+  p.out_g = out_views;
+  p.out_f = out_full;
+  p.lse_g = lse_views;
+  p.lse_f = lse_full;
+  p.idx = idx;
+  p.nsel = nsel;
+  p.ld_idx = ld_idx;
+  p.S = kv->num_seqs;
+  p.Hkv = kv->num_kv_heads;
+  p.Hq = Hq;
+  p.G = Hq / kv->num_kv_heads;
+  p.nq = nq;
+  p.R = pl.R;
+  p.n_rb = pl.n_rb;
+  p.nsplit_g = pl.nsplit_g;
+  p.kps_g = pl.kps_g;
+  p.nsplit_f = pl.nsplit_f;
+  p.kps_f = pl.kps_f;
+  p.units_g = pl.units_g;
+  p.nblk_g = pl.units_g * pl.nsplit_g;
+  p.scale_log2 = scale * 1.4426950408889634f;
+  p.counters = static_cast<uint32_t*>(ws);
+  p.part = pl.record_bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + pl.counter_bytes) : nullptr;
+  return launched(bd::launch_attn(p, pl.nt, kv->page_table != nullptr, pl.nblk, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* bd_status_string(bd_status s) {
+  switch (s) {
+    case BD_OK: return "ok";
+    case BD_ERR_INVALID_ARG: return "invalid argument";
+    case BD_ERR_UNSUPPORTED: return "unsupported";
+    case BD_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case BD_ERR_DEVICE: return "device error";
+    default: return "unknown status";
+  }
+}
+
+const char* bd_last_error(void) { return g_last_error; }
+
+int32_t bd_abi_version(void) { return BD_ABI_VERSION; }
+
+// ---------------------------------------------------------------- select
+size_t bd_select_kv_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads, int32_t window,
+                                    int32_t max_seq_len) {
+  if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || window < 1 || max_seq_len < 0) return 0;
+  return bd::plan_select(num_seqs, num_kv_heads, num_q_heads, window, max_seq_len).ws_bytes;
+}
+
+bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_heads, int32_t window,
+                       int32_t budget, int32_t pool_kernel, float scale, const float* lse_win, int32_t* idx_out,
+                       int32_t* nsel_out, float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  bd_status st = check_kv(kv, false, num_q_heads);
+  if (st != BD_OK) return st;
+  if (window < 1 || budget < window) return fail(BD_ERR_INVALID_ARG, "need 1 <= window <= budget (window %d, budget %d)", window, budget);
+  if (pool_kernel < 1 || pool_kernel % 2 == 0) return fail(BD_ERR_INVALID_ARG, "pool_kernel must be odd and >= 1");
+  if (pool_kernel > 255) return fail(BD_ERR_UNSUPPORTED, "pool_kernel above 255");
+  if (!std::isfinite(scale)) return fail(BD_ERR_INVALID_ARG, "scale is not finite");
+  if (!q_win || !aligned(q_win, 16)) return fail(BD_ERR_INVALID_ARG, "q_win is NULL or not 16-byte aligned");
+  if (!idx_out || !nsel_out) return fail(BD_ERR_INVALID_ARG, "idx_out and nsel_out are required");
+  if ((int64_t)kv->max_seq_len - window > BD_SELECT_MAX_PREFIX)
+    return fail(BD_ERR_UNSUPPORTED, "max_seq_len - window exceeds %d", BD_SELECT_MAX_PREFIX);
+  if (window * (num_q_heads / kv->num_kv_heads) > 4096) return fail(BD_ERR_UNSUPPORTED, "window * group above 4096 rows");
+  const bd::SelectPlan pl = bd::plan_select(kv->num_seqs, kv->num_kv_heads, num_q_heads, window, kv->max_seq_len);
+  st = check_ws(ws, ws_bytes, pl.ws_bytes);
+  if (st != BD_OK) return st;
+  bd::SelectParams p{};
+  p.kv = bd::make_kv_view(*kv);
+  p.q_win = q_win;
+  p.lse_win = lse_win;
+  p.S = kv->num_seqs;
+  p.Hkv = kv->num_kv_heads;
+  p.Hq = num_q_heads;
+  p.G = num_q_heads / kv->num_kv_heads;
+  p.W = window;
+  p.budget = budget;
+  p.pool_kernel = pool_kernel;
+  p.R = window * p.G;
+  p.n_rb = pl.n_rb;
+  p.nsplit = pl.nsplit;
+  p.kps = pl.kps;
+  p.max_L = kv->max_seq_len;
+  p.scale_log2 = scale * 1.4426950408889634f;
+  char* w = static_cast<char*>(ws);
+  p.stats = reinterpret_cast<float*>(w);
+  p.raw_part = reinterpret_cast<float*>(w + pl.stats_bytes);
+  p.raw = scores_out ? scores_out : reinterpret_cast<float*>(w + pl.stats_bytes + pl.raw_part_bytes);
+  p.idx_out = idx_out;
+  p.nsel_out = nsel_out;
+  return launched(bd::launch_select(p, kv->page_table != nullptr, stream));
+}
+
+// ---------------------------------------------------------------- sparse decode
+size_t bd_sparse_decode_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
+                                             int32_t ld_idx) {
+  if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || ld_idx < 0) return 0;
+  return bd::plan_attn(num_seqs, num_kv_heads, num_q_heads, 1, 1, ld_idx, 0, false).ws_bytes;
+}
+
+bd_status bd_sparse_decode_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, const int32_t* idx,
+                                int32_t ld_idx, const int32_t* nsel, float scale, uint16_t* out, float* lse_out,
+                                void* ws, size_t ws_bytes, hipStream_t stream) {
+  bd_status st = check_kv(kv, true, num_q_heads);
+  if (st != BD_OK) return st;
+  if (!q || !aligned(q, 16) || !out || !aligned(out, 16))
+    return fail(BD_ERR_INVALID_ARG, "q and out must be non-NULL and 16-byte aligned");
+  if (ld_idx < 0 || (ld_idx > 0 && (!idx || !nsel))) return fail(BD_ERR_INVALID_ARG, "idx / nsel / ld_idx invalid");
+  if (!nsel) return fail(BD_ERR_INVALID_ARG, "nsel is NULL");
+  if (!std::isfinite(scale)) return fail(BD_ERR_INVALID_ARG, "scale is not finite");
+  return run_attn(kv, q, num_q_heads, 1, 1, idx, ld_idx, nsel, scale, out, lse_out, nullptr, nullptr, ws, ws_bytes,
+                  stream);
+}
+
+// ---------------------------------------------------------------- multiview
+size_t bd_multiview_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
+                                         int32_t block_len, int32_t num_views, int32_t ld_idx, int32_t max_seq_len,
+                                         int32_t with_full) {
+  if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || block_len < 1 || num_views < 0 || ld_idx < 0 ||
+      max_seq_len < 0)
+    return 0;
+  return bd::plan_attn(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld_idx, max_seq_len, with_full != 0)
+      .ws_bytes;
+}
+
+bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t num_q_heads, int32_t block_len,
+                            int32_t num_views, const int32_t* idx_views, int32_t ld_idx, const int32_t* nsel_views,
+                            float scale, uint16_t* out_views, uint16_t* out_full, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+  bd_status st = check_kv(kv, true, num_q_heads);
+  if (st != BD_OK) return st;
+  if (block_len < 1 || num_views < 0 || num_views + (out_full ? 1 : 0) < 1)
+    return fail(BD_ERR_INVALID_ARG, "need block_len >= 1 and at least one view or the full branch");
+  if (!q_blk || !aligned(q_blk, 16)) return fail(BD_ERR_INVALID_ARG, "q_blk is NULL or not 16-byte aligned");
+  if (num_views > 0 && (!idx_views || !nsel_views || !out_views || !aligned(out_views, 16) || ld_idx < 0))
+    return fail(BD_ERR_INVALID_ARG, "views need idx_views, nsel_views, ld_idx >= 0 and a 16-byte aligned out_views");
+  if (out_full && !aligned(out_full, 16)) return fail(BD_ERR_INVALID_ARG, "out_full is not 16-byte aligned");
+  if (!std::isfinite(scale)) return fail(BD_ERR_INVALID_ARG, "scale is not finite");
+  if ((int64_t)block_len * (num_q_heads / kv->num_kv_heads) > (1 << 20))
+    return fail(BD_ERR_UNSUPPORTED, "block_len * group too large");
+  return run_attn(kv, q_blk, num_q_heads, block_len, num_views, idx_views, num_views > 0 ? ld_idx : 0, nsel_views,
+                  scale, out_views, nullptr, out_full, nullptr, ws, ws_bytes, stream);
+}
+
+// ---------------------------------------------------------------- verify
+size_t bd_verify_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads, int32_t gamma,
+                                      int32_t max_seq_len) {
+  if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || gamma < 0 || max_seq_len < 0) return 0;
+  return bd::plan_attn(num_seqs, num_kv_heads, num_q_heads, gamma + 1, 0, 0, max_seq_len, true).ws_bytes;
+}
+
+bd_status bd_verify_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, int32_t gamma, float scale,
+                         uint16_t* out, float* lse_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  bd_status st = check_kv(kv, true, num_q_heads);
+  if (st != BD_OK) return st;
+  if (gamma < 0 || gamma > 4095) return fail(BD_ERR_INVALID_ARG, "gamma %d outside [0, 4095]", gamma);
+  if (!q || !aligned(q, 16) || !out || !aligned(out, 16))
+    return fail(BD_ERR_INVALID_ARG, "q and out must be non-NULL and 16-byte aligned");
+  if (!std::isfinite(scale)) return fail(BD_ERR_INVALID_ARG, "scale is not finite");
+  return run_attn(kv, q, num_q_heads, gamma + 1, 0, nullptr, 0, nullptr, scale, nullptr, nullptr, out, lse_out, ws,
+                  ws_bytes, stream);
+}
+
+// ---------------------------------------------------------------- accept
+size_t bd_accept_len_workspace_bytes(int32_t num_seqs, int32_t gamma, int32_t vocab) {
+  if (num_seqs < 1 || gamma < 0 || vocab < 1) return 0;
+  return bd::plan_accept(num_seqs, gamma, vocab).ws_bytes;
+}
+
+bd_status bd_accept_len(const float* logits, int64_t row_stride, const int32_t* draft, int32_t num_seqs, int32_t gamma,
+                        int32_t vocab, int32_t* accept_out, int32_t* bonus_out, int32_t* argmax_out, void* ws,
+                        size_t ws_bytes, hipStream_t stream) {
+  if (!logits || !accept_out) return fail(BD_ERR_INVALID_ARG, "logits and accept_out are required");
+  if (num_seqs < 1 || vocab < 1 || gamma < 0) return fail(BD_ERR_INVALID_ARG, "need num_seqs >= 1, vocab >= 1, gamma >= 0");
+  if (gamma > 63) return fail(BD_ERR_UNSUPPORTED, "gamma above 63");
+  if (gamma > 0 && !draft) return fail(BD_ERR_INVALID_ARG, "draft is NULL");
+  if (row_stride < vocab) return fail(BD_ERR_INVALID_ARG, "row_stride %lld < vocab %d", (long long)row_stride, vocab);
+  if ((int64_t)num_seqs * (gamma + 1) * 1024 > INT32_MAX) return fail(BD_ERR_UNSUPPORTED, "too many rows");
+  const bd::AcceptPlan pl = bd::plan_accept(num_seqs, gamma, vocab);
+  bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
+  if (st != BD_OK) return st;
+  bd::AcceptParams p{};
+  p.logits = logits;
+  p.row_stride = row_stride;
+  p.draft = draft;
+  p.S = num_seqs;
+  p.gamma = gamma;
+  p.vocab = vocab;
+  p.nsplit = pl.nsplit;
+  p.chunk = pl.chunk;
+  p.vec4 = aligned(logits, 16) && (row_stride % 4 == 0);
+  p.accept_out = accept_out;
+  p.bonus_out = bonus_out;
+  p.argmax_out = argmax_out;
+  p.counters = static_cast<uint32_t*>(ws);
+  p.part = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + pl.counter_bytes);
+  return launched(bd::launch_accept(p, stream));
+}
+
+}  // extern "C"

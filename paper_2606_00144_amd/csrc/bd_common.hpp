@@ -1,0 +1,112 @@
+// Device-side building blocks shared by the libbd kernels (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "bd.h"
+
+namespace bd {
+
+constexpr int kD = BD_HEAD_DIM;   // head dimension, fixed at 128
+constexpr int kWave = 64;         // CDNA wavefront width
+constexpr int kNumXcd = 8;        // MI355X: 256 CUs in 8 accelerator complex dies
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Device copy of bd_kv_desc (kernel argument).
+struct KvView {
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* seq_lens;
+  const int32_t* page_table;
+  int64_t stride_seq, stride_head, stride_tok, stride_page;
+  int32_t num_seqs, num_kv_heads, max_seq_len;
+  int32_t page_size, max_pages_per_seq, num_pages;
+};
+
+inline KvView make_kv_view(const bd_kv_desc& d) {
+  KvView v;
+  v.k = d.k; v.v = d.v; v.seq_lens = d.seq_lens; v.page_table = d.page_table;
+  v.stride_seq = d.stride_seq; v.stride_head = d.stride_head; v.stride_tok = d.stride_tok;
+  v.stride_page = d.stride_page;
+  v.num_seqs = d.num_seqs; v.num_kv_heads = d.num_kv_heads; v.max_seq_len = d.max_seq_len;
+  v.page_size = d.page_size; v.max_pages_per_seq = d.max_pages_per_seq; v.num_pages = d.num_pages;
+  return v;
+}
+
+// Cache length of sequence s, clamped to [0, max_seq_len].
+__device__ inline int seq_len(const KvView& kv, int s) {
+  int L = kv.seq_lens[s];
+  return L < 0 ? 0 : (L > kv.max_seq_len ? kv.max_seq_len : L);
+}
+
+// Element offset of row t of KV head g of sequence s, or -1 when the row's
+// page number is outside the pool (the key is then treated as absent).
+template <bool PAGED>
+__device__ inline int64_t row_offset(const KvView& kv, int s, int g, int t) {
+  if constexpr (PAGED) {
+    const int pg = kv.page_table[(int64_t)s * kv.max_pages_per_seq + t / kv.page_size];
+    if ((unsigned)pg >= (unsigned)kv.num_pages) return -1;
+    return (int64_t)pg * kv.stride_page + (int64_t)g * kv.stride_head + (int64_t)(t % kv.page_size) * kv.stride_tok;
+  } else {
+    return (int64_t)s * kv.stride_seq + (int64_t)g * kv.stride_head + (int64_t)t * kv.stride_tok;
+  }
+}
+
+// Workgroups are handed to the 8 XCDs round-robin (block b runs on XCD b % 8).
+// Remap so that each XCD receives one contiguous range of logical ids: work
+// items that share data (the splits of one (sequence, head) unit, the row
+// blocks of one key range) then share one XCD's L2.
+__device__ inline int xcd_remap(int b, int n) {
+  const int q = n / kNumXcd, r = n % kNumXcd;
+  const int x = b % kNumXcd, j = b / kNumXcd;
+  return x * q + (x < r ? x : r) + j;
+}
+
+// ---- cross-lane reductions ------------------------------------------------
+
+// xor-shuffle through the LDS crossbar (ds_bpermute); works across all 64 lanes.
+__device__ inline float shfl_xor_f(float x, int m) {
+  const int src = (int)(threadIdx.x ^ m) & (kWave - 1);
+  return __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(x)));
+}
+
+// Sum over each aligned group of 16 lanes, result in every lane (DPP only).
+__device__ inline float sum16(float x) {
+  x += __builtin_amdgcn_update_dpp(0.0f, x, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+  x += __builtin_amdgcn_update_dpp(0.0f, x, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+  x += __builtin_amdgcn_update_dpp(0.0f, x, 0x141, 0xF, 0xF, false);  // row_half_mirror
+  x += __builtin_amdgcn_update_dpp(0.0f, x, 0x140, 0xF, 0xF, false);  // row_mirror
+  return x;
+}
+
+// ---- bf16 helpers ---------------------------------------------------------
+
+__device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+__device__ inline uint32_t f32_to_bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ inline uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_rne(lo) | (f32_to_bf16_rne(hi) << 16);
+}
+
+__device__ inline bf16x8 as_bf16x8(u32x4 w) { return __builtin_bit_cast(bf16x8, w); }
+
+__device__ inline u32x4 load16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+// Order-preserving map of a finite float to uint32 (-0.0 folds onto +0.0).
+__device__ inline uint32_t float_order_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+}  // namespace bd

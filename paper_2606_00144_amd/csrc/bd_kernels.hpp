@@ -1,0 +1,102 @@
+// Kernel parameter blocks and launchers of libbd (shared by the host API and the kernels).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "bd_common.hpp"
+
+namespace bd {
+
+// Largest number of gathered entries one attention workgroup handles.
+constexpr int kMaxGatherSplit = 1024;
+
+// ---- attention (decode / verify / multiview) -------------------------------
+struct AttnParams {
+  KvView kv;
+  const uint16_t* q;        // [S][nq][Hq][D]
+  uint16_t* out_g;          // gathered views: [V][S][nq][Hq][D]
+  uint16_t* out_f;          // full branch: [S][nq][Hq][D]
+  float* lse_g;             // nullable [V][S][nq][Hq]
+  float* lse_f;             // nullable [S][nq][Hq]
+  const int32_t* idx;       // [V][S][Hkv][ld_idx]
+  const int32_t* nsel;      // [V][S]
+  int32_t ld_idx;
+  int32_t S, Hkv, Hq, G;
+  int32_t nq;               // query rows per head (1, gamma+1 or C)
+  int32_t R;                // rows per (s, g): nq * G
+  int32_t n_rb;             // row blocks of 16*NT rows
+  int32_t nsplit_g, kps_g;  // gathered units: splits and entries per split
+  int32_t nsplit_f, kps_f;  // full units: splits and keys per split
+  int32_t units_g;          // gathered units (their blocks come first)
+  int32_t nblk_g;           // blocks of gathered units
+  float scale_log2;         // softmax scale * log2(e)
+  float* part;              // partial records
+  uint32_t* counters;       // one per unit
+};
+
+struct AttnPlan {
+  int nt, n_rb, R;
+  int nsplit_g, kps_g, nsplit_f, kps_f;
+  int units_g, units_f, nblk;
+  size_t counter_bytes, record_bytes, ws_bytes;
+};
+
+AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full);
+hipError_t launch_attn(const AttnParams& p, int nt, bool paged, int nblocks, hipStream_t stream);
+size_t attn_record_floats(int nt);
+
+// ---- greedy acceptance -----------------------------------------------------
+struct AcceptParams {
+  const float* logits;
+  int64_t row_stride;
+  const int32_t* draft;
+  int32_t S, gamma, vocab;
+  int32_t nsplit, chunk;    // vocab chunks per row and floats per chunk
+  int32_t vec4;             // rows 16-byte aligned: vector loads
+  int32_t* accept_out;
+  int32_t* bonus_out;
+  int32_t* argmax_out;
+  uint64_t* part;           // [S][gamma+1][nsplit]
+  uint32_t* counters;       // [S]
+};
+
+struct AcceptPlan {
+  int nsplit, chunk;
+  size_t counter_bytes, ws_bytes;
+};
+
+AcceptPlan plan_accept(int S, int gamma, int vocab);
+hipError_t launch_accept(const AcceptParams& p, hipStream_t stream);
+
+// ---- budgeted selection ----------------------------------------------------
+struct SelectParams {
+  KvView kv;
+  const uint16_t* q_win;    // [S][W][Hq][D]
+  const float* lse_win;     // nullable [S][W][Hq]
+  int32_t S, Hkv, Hq, G, W;
+  int32_t budget, pool_kernel;
+  int32_t R;                // rows per (s, g): W * G
+  int32_t n_rb;             // row blocks of 128 rows
+  int32_t nsplit, kps;      // key splits of the scoring passes
+  int32_t max_L;
+  float scale_log2;
+  float* stats;             // [S][Hkv][n_rb][nsplit][128][2] per-split row max / sum
+  float* raw_part;          // [S][Hkv][n_rb][max_L] per-row-block column sums
+  float* raw;               // [S][Hkv][max_L] total raw scores (scores_out or workspace)
+  int32_t* idx_out;         // [S][Hkv][budget]
+  int32_t* nsel_out;        // [S]
+};
+
+struct SelectPlan {
+  int n_rb, nsplit, kps;
+  size_t stats_bytes, raw_part_bytes, raw_bytes, ws_bytes;
+};
+
+SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L);
+hipError_t launch_select(const SelectParams& p, bool paged, hipStream_t stream);
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+}  // namespace bd

@@ -1,0 +1,405 @@
+// Budgeted KV selection (Alg. 2 "sparsify"; Sec. 3.4: keep the entries with
+// the largest cumulative attention weight).
+//
+// Three launches:
+//   1. score pass 1 (skipped when the caller gives the window rows'
+//      log-sum-exp): every (sequence, KV head, row block, key split) computes
+//      the running max and sum of exp of each observation row over its keys;
+//   2. score pass 2: merges those statistics into each row's log-sum-exp and
+//      streams K again, adding every row's normalised weight of every key
+//      into that key's column sum (complete within a row block, so no atomics);
+//   3. top-B: one 1024-thread workgroup per (sequence, KV head) sums the row
+//      blocks, max-pools the prefix, finds the (B-W)-th largest pooled score
+//      with a 4 x 8-bit radix select over the float bit patterns (scores are
+//      non-negative, so the bits order like the values), and compacts the
+//      chosen positions in ascending order; ties at the threshold take the
+//      lowest positions, then the window is appended.
+//
+// The scoring product is a real dense contraction ((W*G) x 128 x L per
+// (s, g)), so it runs on MFMA with the attention kernel's orientation: keys on
+// the M side, observation rows on the N side.  Lane l then holds 4 keys of
+// row l%16: row statistics stay lane-local, and a key's column sum is a
+// 16-lane DPP reduction.
+
+#include "bd_common.hpp"
+#include "bd_kernels.hpp"
+
+namespace bd {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * kWave;
+constexpr int kSub = 16;            // keys per MFMA sub-tile
+constexpr int kStatRows = 128;      // stats record stride (rows)
+constexpr int kTargetBlocks = 1024;
+constexpr int kTopkThreads = 1024;
+constexpr int kMaxPerThread = BD_SELECT_MAX_PREFIX / kTopkThreads;   // 32
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ inline void merge_ml(float& m, float& l, float m2, float l2) {
+  const float M = fmaxf(m, m2);
+  if (M == -INFINITY) { m = M; l = 0.f; return; }
+  l = l * exp2f(m - M) + l2 * exp2f(m2 - M);
+  m = M;
+}
+
+template <int NT>
+struct ScoreSmem {
+  float m[kWaves][16 * NT];
+  float l[kWaves][16 * NT];
+  float lse2[16 * NT];
+};
+
+template <bool PAGED>
+__device__ inline void load_keys(u32x4 (&kr)[4], const KvView& kv, int s, int g, int t, int kend, int lg) {
+  const int64_t off = t < kend ? row_offset<PAGED>(kv, s, g, t) : -1;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) kr[j] = off >= 0 ? load16(kv.k + off + 32 * lg + 8 * j) : u32x4{0u, 0u, 0u, 0u};
+}
+
+template <int NT, bool PAGED, int PASS>
+__global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
+  __shared__ ScoreSmem<NT> sm;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int lg = lane >> 4, lr = lane & 15;
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int rb = bid % p.n_rb;
+  const int rest = bid / p.n_rb;
+  const int split = rest % p.nsplit;
+  const int pair = rest / p.nsplit;
+  const int g = pair % p.Hkv, s = pair / p.Hkv;
+  const int L = seq_len(p.kv, s);
+  if (p.budget >= L) return;               // whole cache kept: nothing to score
+  const int k0 = split * p.kps;
+  int k1 = k0 + p.kps;
+  if (k1 > L) k1 = L;
+  const int64_t stat_base = (((int64_t)pair * p.n_rb + rb) * p.nsplit) * kStatRows * 2;
+
+  // observation rows of this lane: n = rb*16*NT + 16*nt + lane%16 -> (window row i, head h)
+  bf16x8 qop[NT][4];
+  int rowpos[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int n = rb * 16 * NT + 16 * nt + lr;
+    const bool valid = n < p.R;
+    const int i = valid ? n / p.G : 0;
+    const int h = g * p.G + (valid ? n % p.G : 0);
+    rowpos[nt] = valid ? L - p.W + i : -1;          // padded rows see no key
+    const uint16_t* qrow = p.q_win + (((int64_t)s * p.W + i) * p.Hq + h) * kD + 32 * lg;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = as_bf16x8(valid ? load16(qrow + 8 * kk) : u32x4{0u, 0u, 0u, 0u});
+  }
+
+  float rm[NT], rl[NT], lse2[NT];
+  if constexpr (PASS == 2) {
+    if (tid < 16 * NT) {
+      const int n = rb * 16 * NT + tid;
+      float v = 0.f;
+      if (n < p.R) {
+        if (p.lse_win) {
+          const int i = n / p.G, h = g * p.G + n % p.G;
+          v = p.lse_win[((int64_t)s * p.W + i) * p.Hq + h] * kLog2e;
+        } else {
+          float m = -INFINITY, l = 0.f;
+          for (int sp = 0; sp < p.nsplit; ++sp) {
+            const float* st = p.stats + stat_base + ((int64_t)sp * kStatRows + tid) * 2;
+            merge_ml(m, l, st[0], st[1]);
+          }
+          v = l > 0.f ? m + __log2f(l) : INFINITY;   // empty row contributes nothing
+        }
+      }
+      sm.lse2[tid] = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) lse2[nt] = sm.lse2[16 * nt + lr];
+  } else {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) { rm[nt] = -INFINITY; rl[nt] = 0.f; }
+  }
+
+  float* raw_part = p.raw_part + ((int64_t)pair * p.n_rb + rb) * p.max_L;
+  const int nsub = k1 > k0 ? (k1 - k0 + kSub - 1) / kSub : 0;
+
+  auto step = [&](const u32x4 (&kr)[4], int t0) {
+    f32x4 acc[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      f32x4 a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[j]), qop[nt][j], a, 0, 0, 0);
+      acc[nt] = a;
+    }
+    const int tb = t0 + 4 * lg;              // keys tb .. tb+3 of this lane
+    if constexpr (PASS == 1) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        float x[4], mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int t = tb + i;
+          x[i] = (t < k1 && t <= rowpos[nt]) ? acc[nt][i] * p.scale_log2 : -INFINITY;
+          mx = fmaxf(mx, x[i]);
+        }
+        const float M = fmaxf(rm[nt], mx);
+        if (M != -INFINITY) {
+          float add = 0.f;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) add += exp2f(x[i] - M);
+          rl[nt] = rl[nt] * exp2f(rm[nt] - M) + add;
+          rm[nt] = M;
+        }
+      }
+    } else {
+      float col[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int t = tb + i;
+          if (t < k1 && t <= rowpos[nt]) col[i] += exp2f(acc[nt][i] * p.scale_log2 - lse2[nt]);
+        }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) col[i] = sum16(col[i]);
+      if (lr < 4) {
+        const float v = lr == 0 ? col[0] : lr == 1 ? col[1] : lr == 2 ? col[2] : col[3];
+        const int t = tb + lr;
+        if (t < k1) raw_part[t] = v;
+      }
+    }
+  };
+
+  if (wave < nsub) {
+    u32x4 ka[4], kb[4];
+    load_keys<PAGED>(ka, p.kv, s, g, k0 + kSub * wave + lr, k1, lg);
+    int it = wave;
+    while (true) {
+      const int nx = it + kWaves;
+      if (nx < nsub) load_keys<PAGED>(kb, p.kv, s, g, k0 + kSub * nx + lr, k1, lg);
+      step(ka, k0 + kSub * it);
+      if (nx >= nsub) break;
+      const int nx2 = nx + kWaves;
+      if (nx2 < nsub) load_keys<PAGED>(ka, p.kv, s, g, k0 + kSub * nx2 + lr, k1, lg);
+      step(kb, k0 + kSub * nx);
+      if (nx2 >= nsub) break;
+      it = nx2;
+    }
+  }
+
+  if constexpr (PASS == 1) {
+    // merge the 4 lane groups, then the 4 waves, and publish per-row (max, sum) of this split
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+#pragma unroll
+      for (int m = 16; m <= 32; m <<= 1) {
+        const float m2 = shfl_xor_f(rm[nt], m), l2 = shfl_xor_f(rl[nt], m);
+        merge_ml(rm[nt], rl[nt], m2, l2);
+      }
+      if (lg == 0) {
+        sm.m[wave][16 * nt + lr] = rm[nt];
+        sm.l[wave][16 * nt + lr] = rl[nt];
+      }
+    }
+    __syncthreads();
+    if (tid < 16 * NT) {
+      float m = sm.m[0][tid], l = sm.l[0][tid];
+      for (int w = 1; w < kWaves; ++w) merge_ml(m, l, sm.m[w][tid], sm.l[w][tid]);
+      float* st = p.stats + stat_base + ((int64_t)split * kStatRows + tid) * 2;
+      st[0] = m;
+      st[1] = l;
+    }
+  }
+}
+
+// ---- top-B -------------------------------------------------------------------
+
+__device__ inline int block_exclusive_scan(int x, int* wsum, int& total) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int kW = kTopkThreads / kWave;
+  int v = x;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(v, o);
+    if (lane >= o) v += y;
+  }
+  if (lane == kWave - 1) wsum[wave] = v;
+  __syncthreads();
+  if (wave == 0) {
+    int w = lane < kW ? wsum[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < kW; o <<= 1) {
+      const int y = __shfl_up(w, o);
+      if (lane >= o) w += y;
+    }
+    if (lane < kW) wsum[lane] = w;
+  }
+  __syncthreads();
+  const int before = (wave > 0 ? wsum[wave - 1] : 0) + v - x;
+  total = wsum[kW - 1];
+  __syncthreads();
+  return before;
+}
+
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
+  __shared__ uint32_t hist[256];
+  __shared__ int wsum[kTopkThreads / kWave];
+  __shared__ uint32_t s_digit, s_krem;
+  const int tid = threadIdx.x;
+  const int pair = blockIdx.x;
+  const int g = pair % p.Hkv, s = pair / p.Hkv;
+  const int L = seq_len(p.kv, s);
+  const int B = p.budget, W = p.W;
+  int32_t* idx_row = p.idx_out + (int64_t)pair * B;
+
+  if (B >= L) {
+    for (int t = tid; t < B; t += kTopkThreads) idx_row[t] = t < L ? t : -1;
+    if (g == 0 && tid == 0) p.nsel_out[s] = L;
+    return;
+  }
+  if (g == 0 && tid == 0) p.nsel_out[s] = B;
+
+  // 1. total raw scores (row blocks summed in order)
+  float* raw = p.raw + (int64_t)pair * p.max_L;
+  const float* part = p.raw_part + (int64_t)pair * p.n_rb * p.max_L;
+  for (int t = tid; t < L; t += kTopkThreads) {
+    float v = 0.f;
+    for (int r = 0; r < p.n_rb; ++r) v += part[(int64_t)r * p.max_L + t];
+    raw[t] = v;
+  }
+  __syncthreads();
+
+  // 2. pooled keys of this thread's contiguous segment of the prefix [0, N)
+  const int N = L - W, K = B - W, rad = p.pool_kernel / 2;
+  const int E = (N + kTopkThreads - 1) / kTopkThreads;
+  const int t0 = tid * E;
+  uint32_t key[kMaxPerThread];
+#pragma unroll
+  for (int e = 0; e < kMaxPerThread; ++e) {
+    const int t = t0 + e;
+    uint32_t k = 0;
+    if (e < E && t < N) {
+      const int lo = t - rad < 0 ? 0 : t - rad;
+      const int hi = t + rad > N - 1 ? N - 1 : t + rad;
+      float m = raw[lo];
+      for (int u = lo + 1; u <= hi; ++u) m = fmaxf(m, raw[u]);
+      k = __float_as_uint(m);                // m >= 0: bit patterns order like values
+    }
+    key[e] = k;
+  }
+
+  // 3. radix select of the K-th largest key; krem = how many keys equal to it are taken
+  uint32_t prefix = 0, pmask = 0, krem = (uint32_t)K;
+  if (K > 0) {
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      if (tid < 256) hist[tid] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < kMaxPerThread; ++e)
+        if (e < E && t0 + e < N && (key[e] & pmask) == prefix) atomicAdd(&hist[(key[e] >> shift) & 255u], 1u);
+      __syncthreads();
+      if (tid < kWave) {
+        uint32_t h[4], c = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) { h[q] = hist[255 - (4 * tid + q)]; c += h[q]; }
+        uint32_t incl = c;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+          const uint32_t y = __shfl_up(incl, o);
+          if (tid >= o) incl += y;
+        }
+        uint32_t a = incl - c;               // keys whose digit is above this lane's four digits
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (a < krem && krem <= a + h[q]) { s_digit = 255u - (uint32_t)(4 * tid + q); s_krem = krem - a; }
+          a += h[q];
+        }
+      }
+      __syncthreads();
+      prefix |= s_digit << shift;
+      pmask |= 255u << shift;
+      krem = s_krem;
+      __syncthreads();
+    }
+  }
+
+  // 4. ordered compaction: all keys above the threshold, the first krem keys equal to it
+  int gt = 0, eq = 0;
+#pragma unroll
+  for (int e = 0; e < kMaxPerThread; ++e)
+    if (K > 0 && e < E && t0 + e < N) { gt += key[e] > prefix; eq += key[e] == prefix; }
+  int tot;
+  const int eq_before = block_exclusive_scan(eq, wsum, tot);
+  int take_eq = (int)krem - eq_before;
+  take_eq = take_eq < 0 ? 0 : (take_eq > eq ? eq : take_eq);
+  const int off0 = block_exclusive_scan(gt + take_eq, wsum, tot);
+  int off = off0, seen = 0;
+#pragma unroll
+  for (int e = 0; e < kMaxPerThread; ++e) {
+    const int t = t0 + e;
+    if (K > 0 && e < E && t < N) {
+      const bool isq = key[e] == prefix;
+      if (key[e] > prefix || (isq && seen < take_eq)) {
+        if (off < K) idx_row[off] = t;      // guard: never write past the B slots of this row
+        ++off;
+      }
+      seen += isq;
+    }
+  }
+  for (int i = tid; i < W; i += kTopkThreads) idx_row[K + i] = N + i;
+}
+
+template <int NT, bool PAGED>
+hipError_t launch_scores(const SelectParams& p, int nblocks, hipStream_t stream) {
+  if (!p.lse_win) {
+    hipLaunchKernelGGL((score_kernel<NT, PAGED, 1>), dim3(nblocks), dim3(kThreads), 0, stream, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((score_kernel<NT, PAGED, 2>), dim3(nblocks), dim3(kThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+int select_nt(int R) {
+  const int tiles = (R + 15) / 16;
+  return tiles <= 1 ? 1 : tiles <= 2 ? 2 : tiles <= 4 ? 4 : 8;
+}
+
+}  // namespace
+
+SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L) {
+  SelectPlan pl;
+  const int G = Hq / Hkv;
+  const int R = W * G;
+  const int nt = select_nt(R);
+  pl.n_rb = (R + 16 * nt - 1) / (16 * nt);
+  const int64_t units = (int64_t)S * Hkv * pl.n_rb;
+  const int64_t per_block = (units * max_L + kTargetBlocks - 1) / kTargetBlocks;
+  int64_t kps = (per_block + kWaves * kSub - 1) / (kWaves * kSub) * (kWaves * kSub);
+  const int64_t cap = ((int64_t)max_L + kWaves * kSub - 1) / (kWaves * kSub) * (kWaves * kSub);
+  if (kps > cap) kps = cap;
+  if (kps < kWaves * kSub) kps = kWaves * kSub;
+  pl.kps = (int)kps;
+  pl.nsplit = max_L > 0 ? (int)((max_L + kps - 1) / kps) : 1;
+  pl.stats_bytes = align256(sizeof(float) * (size_t)units * pl.nsplit * kStatRows * 2);
+  pl.raw_part_bytes = align256(sizeof(float) * (size_t)units * max_L);
+  pl.raw_bytes = align256(sizeof(float) * (size_t)S * Hkv * max_L);
+  pl.ws_bytes = pl.stats_bytes + pl.raw_part_bytes + pl.raw_bytes;
+  return pl;
+}
+
+hipError_t launch_select(const SelectParams& p, bool paged, hipStream_t stream) {
+  const int nt = select_nt(p.R);
+  const int nblocks = p.S * p.Hkv * p.n_rb * p.nsplit;
+  hipError_t e = hipSuccess;
+  switch (nt) {
+    case 1: e = paged ? launch_scores<1, true>(p, nblocks, stream) : launch_scores<1, false>(p, nblocks, stream); break;
+    case 2: e = paged ? launch_scores<2, true>(p, nblocks, stream) : launch_scores<2, false>(p, nblocks, stream); break;
+    case 4: e = paged ? launch_scores<4, true>(p, nblocks, stream) : launch_scores<4, false>(p, nblocks, stream); break;
+    default: e = paged ? launch_scores<8, true>(p, nblocks, stream) : launch_scores<8, false>(p, nblocks, stream); break;
+  }
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(topk_kernel, dim3(p.S * p.Hkv), dim3(kTopkThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace bd

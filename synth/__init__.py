@@ -45,8 +45,11 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     Inputs must be finite.  Storage conversion for generated data only.
     """
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    u = x.view(np.uint32)
+    r = (u >> 16) & 1            # finite inputs: u + 0x8000 cannot wrap in uint32
+    r += 0x7FFF
+    r += u
+    r >>= 16
     return r.astype(np.uint16)
 
 
@@ -214,3 +217,23 @@ def random_index_set(config_id: int, s: int, g: int, L: int, n: int, tag_extra: 
     """A seeded ascending set of n distinct positions in [0, L) (for sparse-attention inputs)."""
     n = min(n, L)
     return np.sort(rng(config_id, TAG_IDX, s, g, tag_extra).choice(L, size=n, replace=False)).astype(np.int32)
+
+
+def kv_batch(cfg: Config, seqs: Optional[Sequence[int]] = None, tag_k: int = TAG_K, tag_v: int = TAG_V,
+             workers: int = 8):
+    """Query tails, K and V of several sequences, generated in parallel (one stream per sequence).
+
+    Returns lists (q_tail, k, v) in the order of ``seqs``.
+    """
+    import concurrent.futures
+
+    seqs = list(range(cfg.num_seqs)) if seqs is None else list(seqs)
+
+    def one(s):
+        qt = query_tail(cfg, s)
+        k, v = kv_sequence(cfg, s, q_tail=qt, tag_k=tag_k, tag_v=tag_v)
+        return qt, k, v
+
+    with concurrent.futures.ThreadPoolExecutor(max_workers=max(1, workers)) as ex:
+        res = list(ex.map(one, seqs))
+    return [r[0] for r in res], [r[1] for r in res], [r[2] for r in res]

@@ -1,0 +1,113 @@
+"""C-ABI checks that need no GPU: the library loads, exports what include/bd.h
+declares, sizes workspaces, and rejects bad arguments on the host before any
+launch (every call here is refused by validation, so no kernel runs)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_00144_amd as bd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bd.h")
+
+FAKE = 0x10000000          # a 256-byte aligned non-NULL address that is never dereferenced
+
+
+def header_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\**\s+\**(bd_[a-z_0-9]+)\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(bd.library_path):
+        from paper_2606_00144_amd import build
+        build.build_library()
+    return bd.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = header_functions()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(bd._SIGNATURES)
+
+
+def test_version_and_status_strings(L):
+    assert L.bd_abi_version() == 1
+    for s in range(5):
+        assert L.bd_status_string(s)
+    assert L.bd_status_string(99) == b"unknown status"
+
+
+def _kv(**over):
+    d = bd.KvDesc()
+    d.k = d.v = FAKE
+    d.num_seqs, d.num_kv_heads, d.head_dim, d.max_seq_len = 2, 8, 128, 4096
+    d.seq_lens = FAKE
+    d.stride_head, d.stride_tok, d.stride_seq = 4096 * 128, 128, 8 * 4096 * 128
+    for k, v in over.items():
+        setattr(d, k, v)
+    return d
+
+
+def _verify(L, kv, hq=32, gamma=5, ws=FAKE, wsb=1 << 40, q=FAKE, out=FAKE, scale=0.088):
+    return L.bd_verify_attn(ctypes.byref(kv) if kv is not None else None, q, hq, gamma, scale, out, None, ws, wsb, None)
+
+
+def test_verify_rejections(L):
+    assert _verify(L, None) == bd.BD_ERR_INVALID_ARG
+    assert _verify(L, _kv(head_dim=64)) == bd.BD_ERR_UNSUPPORTED
+    assert _verify(L, _kv(k=0)) == bd.BD_ERR_INVALID_ARG
+    assert _verify(L, _kv(k=FAKE + 8)) == bd.BD_ERR_INVALID_ARG             # misaligned K
+    assert _verify(L, _kv(seq_lens=0)) == bd.BD_ERR_INVALID_ARG
+    assert _verify(L, _kv(), hq=30) == bd.BD_ERR_INVALID_ARG                # Hq % Hkv != 0
+    assert _verify(L, _kv(), gamma=-1) == bd.BD_ERR_INVALID_ARG
+    assert _verify(L, _kv(), q=0) == bd.BD_ERR_INVALID_ARG
+    assert _verify(L, _kv(), out=FAKE + 2) == bd.BD_ERR_INVALID_ARG
+    assert _verify(L, _kv(), scale=float("nan")) == bd.BD_ERR_INVALID_ARG
+    assert _verify(L, _kv(stride_tok=100)) == bd.BD_ERR_INVALID_ARG
+    assert _verify(L, _kv(page_table=FAKE, page_size=16, max_pages_per_seq=10, num_pages=100,
+                          stride_page=8 * 16 * 128)) == bd.BD_ERR_INVALID_ARG   # 4096 > 10 * 16
+    assert _verify(L, _kv(), ws=None) == bd.BD_ERR_WORKSPACE
+    assert _verify(L, _kv(), ws=FAKE + 64) == bd.BD_ERR_WORKSPACE
+    assert _verify(L, _kv(), wsb=16) == bd.BD_ERR_WORKSPACE
+    assert b"workspace" in L.bd_last_error()
+
+
+def test_decode_select_multiview_accept_rejections(L):
+    kv = _kv()
+    assert L.bd_sparse_decode_attn(ctypes.byref(kv), FAKE, 32, FAKE, -1, FAKE, 0.1, FAKE, None, FAKE, 1 << 40, None) == 1
+    assert L.bd_sparse_decode_attn(ctypes.byref(kv), FAKE, 32, FAKE, 64, None, 0.1, FAKE, None, FAKE, 1 << 40, None) == 1
+    assert L.bd_sparse_decode_attn(ctypes.byref(kv), FAKE, 32, FAKE, 64, FAKE, 0.1, FAKE, None, None, 0, None) == 3
+    sel = lambda **a: L.bd_select_kv(ctypes.byref(a.get("kv", kv)), FAKE, 32, a.get("W", 32), a.get("B", 256),
+                                     a.get("P", 7), 0.1, None, FAKE, FAKE, None, FAKE, 1 << 40, None)
+    assert sel(W=0) == 1
+    assert sel(W=64, B=32) == 1
+    assert sel(P=4) == 1
+    assert sel(P=301) == 2
+    assert sel(kv=_kv(max_seq_len=40000)) == 2                              # prefix above BD_SELECT_MAX_PREFIX
+    mv = lambda **a: L.bd_multiview_attn(ctypes.byref(kv), FAKE, 32, a.get("C", 64), a.get("V", 4), FAKE, 1024, FAKE,
+                                         0.1, a.get("ov", FAKE), a.get("of", FAKE), FAKE, 1 << 40, None)
+    assert mv(C=0) == 1
+    assert mv(V=0, of=None) == 1
+    assert mv(ov=None) == 1
+    acc = lambda **a: L.bd_accept_len(a.get("lg", FAKE), a.get("rs", 32000), a.get("dr", FAKE), 2, a.get("g", 5),
+                                      32000, FAKE, None, None, FAKE, 1 << 40, None)
+    assert acc(lg=None) == 1
+    assert acc(rs=100) == 1
+    assert acc(g=64) == 2
+    assert acc(dr=None) == 1
+
+
+def test_workspace_sizes(L):
+    v = L.bd_verify_attn_workspace_bytes(8, 8, 32, 5, 16384)
+    assert v > 0 and v % 256 == 0
+    assert L.bd_sparse_decode_attn_workspace_bytes(8, 8, 32, 1024) > 0
+    assert L.bd_select_kv_workspace_bytes(8, 8, 32, 32, 16384) >= 8 * 8 * 16384 * 4
+    assert L.bd_multiview_attn_workspace_bytes(4, 8, 32, 64, 4, 2048, 8192, 1) > 0
+    assert L.bd_accept_len_workspace_bytes(8, 5, 128256) > 0
+    assert L.bd_verify_attn_workspace_bytes(0, 8, 32, 5, 16384) == 0        # invalid shape -> 0

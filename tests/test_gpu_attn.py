@@ -1,0 +1,240 @@
+"""GPU parity of the attention entry points (decode, verify, multiview) against the fp64 oracle.
+
+Every call goes through the C ABI (ctypes binding).  Outputs are compared
+element by element: |gpu - oracle| <= 2e-2 + 1e-2 |oracle| on bf16 outputs,
+1e-3 absolute on fp32 log-sum-exp.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2606_00144_amd as bd
+import synth
+from gpu_utils import (assert_close, assert_lse, bf16_dev, bf16_host64, case, config_data, i32_dev, paged_kv)
+
+pytestmark = pytest.mark.gpu
+
+
+def _rand_bits(shape, seed, scale=1.0):
+    g = np.random.default_rng(seed)
+    return synth.f32_to_bf16_bits(scale * g.standard_normal(shape, dtype=np.float32))
+
+
+def _sparse_idx(cid, S, Hkv, L, B, W=32):
+    """Seeded index lists shaped like a selection: B-W prefix positions + the window."""
+    idx = np.full((S, Hkv, B), -1, np.int32)
+    for s in range(S):
+        for g in range(Hkv):
+            pre = synth.random_index_set(cid, s, g, L - W, B - W)
+            idx[s, g] = np.r_[pre, np.arange(L - W, L)]
+    return idx
+
+
+def _decode_check(k, v, q, idx, nsel, lens, what, kdev=None, vdev=None, page_table=None, **kw):
+    kd = bf16_dev(k) if kdev is None else kdev
+    vd = bf16_dev(v) if vdev is None else vdev
+    case(f"decode {what}")
+    out, lse = bd.bd_sparse_decode_attn(kd, vd, bf16_dev(q), i32_dev(idx), i32_dev(nsel), i32_dev(lens),
+                                        return_lse=True, page_table=page_table, **kw)
+    torch.cuda.synchronize()
+    ro, rl = O.sparse_decode_attn(k, v, q, idx, nsel, lens)
+    assert_close(bf16_host64(out), ro, what)
+    assert_lse(lse.cpu().numpy().astype(np.float64), rl, what)
+    return out
+
+
+# ------------------------------------------------------------------ decode
+
+def test_decode_config0_oracle_selection():
+    cfg = synth.CONFIGS[0]
+    qt, k, v = config_data(0)
+    lens = [cfg.seq_len]
+    idx, nsel, _ = O.select_kv(k, qt[:, -cfg.window:], lens, cfg.num_q_heads, cfg.window, 256)
+    _decode_check(k, v, qt[:, -1], idx, nsel, lens, "cfg0 B=256")
+
+
+@pytest.mark.parametrize("B", [256, 512, 1024, 2048])
+def test_decode_config1_budgets(B):
+    cfg = synth.CONFIGS[1]
+    qt, k, v = config_data(1)
+    idx = _sparse_idx(1, 1, cfg.num_kv_heads, cfg.seq_len, B)
+    _decode_check(k, v, qt[:, -1], idx, [B], [cfg.seq_len], f"cfg1 B={B}")
+
+
+def test_decode_config2_full_size():
+    cfg = synth.CONFIGS[2]
+    qt, k, v = config_data(2)
+    for B in cfg.budgets:
+        idx = _sparse_idx(2, cfg.num_seqs, cfg.num_kv_heads, cfg.seq_len, B)
+        _decode_check(k, v, qt[:, -1], idx, [B] * cfg.num_seqs, [cfg.seq_len] * cfg.num_seqs, f"cfg2 B={B}")
+
+
+def test_decode_edge_cases():
+    S, Hkv, G, L = 3, 2, 4, 300
+    k, v = _rand_bits((S, Hkv, L, 128), 1), _rand_bits((S, Hkv, L, 128), 2)
+    q = _rand_bits((S, Hkv * G, 128), 3)
+    lens = [300, 129, 17]
+    idx = np.full((S, Hkv, 70), -1, np.int32)
+    g = np.random.default_rng(4)
+    idx[0] = g.permutation(L)[:70].reshape(1, 70).repeat(Hkv, 0)      # unsorted
+    idx[1, :, :40] = g.integers(-5, 200, size=(Hkv, 40))              # -1s, negatives and >= L entries
+    idx[2, :, :1] = 9                                                 # single entry
+    nsel = [70, 1000, 1]                                              # nsel > ld clamps
+    _decode_check(k, v, q, idx, nsel, lens, "edge mix")
+    # no entries at all: output 0, lse -inf
+    out = _decode_check(k, v, q, idx, [0, 0, 0], lens, "empty")
+    assert torch.count_nonzero(out).item() == 0
+    # a single entry returns its value row bit for bit
+    out = bd.bd_sparse_decode_attn(bf16_dev(k), bf16_dev(v), bf16_dev(q), i32_dev(idx), i32_dev([1, 1, 1]), i32_dev(lens))
+    torch.cuda.synchronize()
+    got = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got[2, :4], np.repeat(v[2, 0, 9][None], 4, 0))
+    # V == 1: softmax weights are normalised on the device, output exactly 1.0
+    ones = synth.f32_to_bf16_bits(np.ones((S, Hkv, L, 128), np.float32))
+    out = bd.bd_sparse_decode_attn(bf16_dev(k), bf16_dev(ones), bf16_dev(q), i32_dev(idx), i32_dev([70, 40, 1]), i32_dev(lens))
+    torch.cuda.synchronize()
+    o = bf16_host64(out)
+    assert np.all(o[0] == 1.0) and np.all(o[2] == 1.0)
+
+
+def test_decode_permutation_and_determinism():
+    cfg = synth.CONFIGS[1]
+    qt, k, v = config_data(1)
+    idx = _sparse_idx(1, 1, cfg.num_kv_heads, cfg.seq_len, 1024)
+    perm = idx[:, :, np.random.default_rng(5).permutation(1024)]
+    kd, vd, qd, lens = bf16_dev(k), bf16_dev(v), bf16_dev(qt[:, -1]), i32_dev([cfg.seq_len])
+    case("decode permutation / determinism")
+    a = bd.bd_sparse_decode_attn(kd, vd, qd, i32_dev(idx), i32_dev([1024]), lens)
+    b = bd.bd_sparse_decode_attn(kd, vd, qd, i32_dev(idx), i32_dev([1024]), lens)
+    c = bd.bd_sparse_decode_attn(kd, vd, qd, i32_dev(perm), i32_dev([1024]), lens)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    ref, _ = O.sparse_decode_attn(k, v, qt[:, -1], idx, [1024], [cfg.seq_len])
+    assert_close(bf16_host64(c), ref, "permuted idx")
+
+
+# ------------------------------------------------------------------ verify
+
+def _verify_check(k, v, q, lens, gamma, what, kdev=None, vdev=None, page_table=None, **kw):
+    kd = bf16_dev(k) if kdev is None else kdev
+    vd = bf16_dev(v) if vdev is None else vdev
+    case(f"verify {what}")
+    out, lse = bd.bd_verify_attn(kd, vd, bf16_dev(q), i32_dev(lens), return_lse=True, page_table=page_table, **kw)
+    torch.cuda.synchronize()
+    ro, rl = O.verify_attn(k, v, q, lens, gamma)
+    assert_close(bf16_host64(out), ro, what)
+    assert_lse(lse.cpu().numpy().astype(np.float64), rl, what)
+    return out
+
+
+@pytest.mark.parametrize("cid", [0, 1])
+def test_verify_configs(cid):
+    cfg = synth.CONFIGS[cid]
+    qt, k, v = config_data(cid)
+    g1 = cfg.gamma + 1
+    _verify_check(k, v, qt[:, -g1:], [cfg.seq_len] * cfg.num_seqs, cfg.gamma, f"cfg{cid}")
+
+
+def test_verify_config2_full_size():
+    cfg = synth.CONFIGS[2]
+    qt, k, v = config_data(2)
+    g1 = cfg.gamma + 1
+    _verify_check(k, v, qt[:, -g1:], [cfg.seq_len] * cfg.num_seqs, cfg.gamma, "cfg2 16K")
+
+
+@pytest.mark.parametrize("Hq,Hkv,gamma", [(8, 2, 5), (4, 4, 5), (16, 2, 5), (8, 2, 0), (32, 8, 3)])
+def test_verify_ragged_shapes(Hq, Hkv, gamma):
+    S, Lmax = 4, 200
+    k, v = _rand_bits((S, Hkv, Lmax, 128), 10), _rand_bits((S, Hkv, Lmax, 128), 11)
+    q = _rand_bits((S, gamma + 1, Hq, 128), 12)
+    lens = [200, 33, gamma + 1, 97]
+    _verify_check(k, v, q, lens, gamma, f"ragged Hq={Hq} Hkv={Hkv} gamma={gamma}")
+
+
+def test_verify_matches_decode_over_everything():
+    cfg = synth.CONFIGS[0]
+    qt, k, v = config_data(0)
+    L, g1 = cfg.seq_len, cfg.gamma + 1
+    kd, vd = bf16_dev(k), bf16_dev(v)
+    idx = np.tile(np.arange(L, dtype=np.int32), (1, cfg.num_kv_heads, 1))
+    case("verify vs decode over the whole cache")
+    ov = bd.bd_verify_attn(kd, vd, bf16_dev(qt[:, -g1:]), i32_dev([L]))
+    od = bd.bd_sparse_decode_attn(kd, vd, bf16_dev(qt[:, -1]), i32_dev(idx), i32_dev([L]), i32_dev([L]))
+    torch.cuda.synchronize()
+    assert_close(bf16_host64(od), bf16_host64(ov)[:, -1], "decode(all) vs verify row gamma")
+
+
+def test_verify_paged_ragged_mha():
+    cfg = synth.CONFIGS[4]
+    lens_all = synth.seq_lens(cfg)
+    pick = [0, 1, 2, 3, 4, 5]
+    lens = lens_all[pick]
+    ks, vs, qs = [], [], []
+    for s in pick:
+        qt = synth.query_tail(cfg, s)
+        k, v = synth.kv_sequence(cfg, s, q_tail=qt)
+        ks.append(k), vs.append(v), qs.append(qt[-(cfg.gamma + 1):])
+    table, npages = synth.page_table(cfg, lens)
+    kd, vd = paged_kv(ks, vs, table, npages, cfg.page_size)
+    _verify_check(ks, vs, np.stack(qs), lens, cfg.gamma, "paged cfg4 sample", kdev=kd, vdev=vd,
+                  page_table=i32_dev(table))
+    idx = np.stack([np.stack([np.r_[synth.random_index_set(4, s, g, int(lens[i]) - 32, 1024 - 32),
+                                    np.arange(lens[i] - 32, lens[i])] for g in range(cfg.num_kv_heads)])
+                    for i, s in enumerate(pick)]).astype(np.int32)
+    _decode_check(ks, vs, np.stack([q[-1] for q in qs]), idx, [1024] * len(pick), lens, "paged cfg4 sample",
+                  kdev=kd, vdev=vd, page_table=i32_dev(table))
+
+
+# ------------------------------------------------------------------ multiview
+
+def _multiview_check(k, v, qb, idx_views, nsel_views, lens, what, full=True):
+    case(f"multiview {what}")
+    ov, of = bd.bd_multiview_attn(bf16_dev(k), bf16_dev(v), bf16_dev(qb), i32_dev(idx_views), i32_dev(nsel_views),
+                                  i32_dev(lens), full=full)
+    torch.cuda.synchronize()
+    rv, rf = O.multiview_attn(k, v, qb, list(idx_views), list(nsel_views), lens, with_full=full)
+    assert_close(bf16_host64(ov), rv, what + " views")
+    if full:
+        assert_close(bf16_host64(of), rf, what + " full")
+
+
+def test_multiview_small_with_selected_views():
+    S, Hkv, G, L, C = 2, 2, 4, 1500, 64
+    k, v = _rand_bits((S, Hkv, L, 128), 20), _rand_bits((S, Hkv, L, 128), 21)
+    qb = _rand_bits((S, C, Hkv * G, 128), 22)
+    budgets = [128, 256, 1024, 2048]                  # the last keeps the whole cache
+    ld = max(budgets)
+    idx_v = np.full((len(budgets), S, Hkv, ld), -1, np.int32)
+    nsel_v = np.zeros((len(budgets), S), np.int32)
+    for i, B in enumerate(budgets):
+        idx, nsel, _ = O.select_kv(k, qb, [L, L], Hkv * G, C, B)
+        idx_v[i, :, :, :idx.shape[2]] = idx
+        nsel_v[i] = nsel
+    _multiview_check(k, v, qb, idx_v, nsel_v, [L, L], "small")
+
+
+def test_multiview_config3_sampled():
+    cfg = synth.CONFIGS[3]
+    qt, k, v = config_data(3)
+    C = cfg.block_len
+    budgets = synth.view_budgets(cfg)
+    ld = int(budgets.max())
+    S = cfg.num_seqs
+    idx_v = np.full((len(budgets), S, cfg.num_kv_heads, ld), -1, np.int32)
+    nsel_v = np.zeros((len(budgets), S), np.int32)
+    for i, B in enumerate(budgets):
+        idx_v[i, :, :, :int(B)] = _sparse_idx(3, S, cfg.num_kv_heads, cfg.seq_len, int(B), W=C)
+        nsel_v[i] = B
+    qb = qt[:, -C:]
+    lens = [cfg.seq_len] * S
+    case("multiview cfg3 full size")
+    ov, of = bd.bd_multiview_attn(bf16_dev(k), bf16_dev(v), bf16_dev(qb), i32_dev(idx_v), i32_dev(nsel_v), i32_dev(lens))
+    torch.cuda.synchronize()
+    gv, gf = bf16_host64(ov), bf16_host64(of)
+    # oracle on one sequence (all heads, all views, full branch)
+    s = 1
+    rv, rf = O.multiview_attn(k[s:s + 1], v[s:s + 1], qb[s:s + 1], [iv[s:s + 1] for iv in idx_v],
+                              [nv[s:s + 1] for nv in nsel_v], lens[:1])
+    assert_close(gv[:, s:s + 1], rv, "cfg3 views seq 1")
+    assert_close(gf[s:s + 1], rf, "cfg3 full seq 1")
