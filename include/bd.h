@@ -26,12 +26,13 @@
  *   - Ownership: the caller owns every buffer; inputs are only read; outputs
  *     are overwritten in full; the library keeps no pointer after returning.
  *   - Workspace: each operation takes caller-allocated device memory of at
- *     least bd_<op>_workspace_bytes(...) bytes (256-byte aligned).  It must be
- *     all zero before its first use; every call that runs to completion leaves
- *     its counters at zero again, so one workspace can serve any number of
- *     later calls of the SAME operation issued on the same stream.  Calls that
- *     overlap in time (two streams) must not share a workspace.  The library
- *     never allocates device memory.
+ *     least bd_<op>_workspace_bytes(...) bytes (256-byte aligned).  Its first
+ *     BD_WS_COUNTER_BYTES hold completion counters and must be zero before the
+ *     first use; every call that runs to completion leaves them zero again and
+ *     writes its other scratch only past them.  One workspace can therefore
+ *     serve any sequence of calls, of any operation and shape, issued on one
+ *     stream.  Calls that overlap in time (two streams) must not share a
+ *     workspace.  The library never allocates device memory.
  *   - Errors: arguments are checked on the host before anything is launched;
  *     on error nothing is launched and no output is touched.  A launch failure
  *     reported by the HIP runtime is BD_ERR_DEVICE.  No C++ exception crosses
@@ -58,6 +59,9 @@ extern "C" {
 #define BD_HEAD_DIM 128
 /* Longest candidate prefix L_s - W that bd_select_kv ranks in one pass. */
 #define BD_SELECT_MAX_PREFIX 32768
+/* Leading workspace bytes reserved for completion counters (one uint32 per
+ * work unit; a call with more than BD_WS_COUNTER_BYTES/4 units is unsupported). */
+#define BD_WS_COUNTER_BYTES 262144
 
 typedef int32_t bd_status;
 #define BD_OK 0

@@ -149,10 +149,11 @@ def kv_desc(k: torch.Tensor, v: Optional[torch.Tensor], seq_lens: torch.Tensor,
 
 
 class Workspace:
-    """Zero-initialised device scratch, reused across calls of one operation.
+    """Zero-initialised device scratch, reused across calls.
 
-    Every completed call leaves its counters at zero, so reuse on one stream
-    needs no clearing.  One instance must not serve calls that overlap in time.
+    Every completed call leaves the leading counter region at zero and writes
+    its other scratch only past it, so reuse on one stream needs no clearing.
+    One instance must not serve calls that overlap in time.
     """
 
     def __init__(self):
@@ -161,7 +162,7 @@ class Workspace:
     def get(self, nbytes: int, device) -> Optional[torch.Tensor]:
         if nbytes == 0:
             return None
-        if self.buf is None or self.buf.numel() < nbytes or self.buf.device != torch.device(device):
+        if self.buf is None or self.buf.numel() < nbytes + 256 or self.buf.device != torch.device(device):
             self.buf = torch.zeros(nbytes + 256, dtype=torch.uint8, device=device)
         return self.buf
 
@@ -271,7 +272,8 @@ def bd_accept_len(logits: torch.Tensor, draft: torch.Tensor, *, return_argmax: b
                   workspace: Optional[Workspace] = None, outputs=None):
     """Greedy acceptance.  logits fp32 [S, gamma+1, V] (last dim contiguous); draft int32 [S, gamma]."""
     _require(logits.dtype == torch.float32 and logits.dim() == 3 and logits.stride(2) == 1
-             and logits.stride(0) == logits.shape[1] * logits.stride(1), "logits must be fp32 [S,gamma+1,V] with packed rows")
+             and (logits.shape[0] == 1 or logits.stride(0) == logits.shape[1] * logits.stride(1)),
+             "logits must be fp32 [S,gamma+1,V] with evenly spaced rows")
     S, R, V = logits.shape
     gamma = R - 1
     _require(draft.dtype == torch.int32 and draft.shape == (S, gamma) and draft.is_contiguous(), "draft must be int32 [S,gamma]")

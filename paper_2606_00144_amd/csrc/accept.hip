@@ -71,19 +71,17 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptParams p) {
     if (tid == 0) {
       uint64_t bb = red[0];
       for (int w = 1; w < kThreads / kWave; ++w) bb = umax64(bb, red[w]);
-      p.part[(int64_t)rs * p.nsplit + split] = bb;
-      __threadfence();
-      const uint32_t prev = atomicAdd(&p.counters[s], 1u);
-      last = prev == (uint32_t)(per_seq - 1);
+      store_coherent(p.part + (int64_t)rs * p.nsplit + split, bb);
+      wait_vmem();
+      last = arrive(&p.counters[s], (uint32_t)per_seq);
     }
     __syncthreads();
     if (!last) return;
-    __threadfence();
     // merge: thread i < rows takes row i (rows <= 64 is checked on the host)
     if (tid < rows) {
       const uint64_t* pr = p.part + ((int64_t)s * rows + tid) * p.nsplit;
       uint64_t bb = 0;
-      for (int sp = 0; sp < p.nsplit; ++sp) bb = umax64(bb, pr[sp]);
+      for (int sp = 0; sp < p.nsplit; ++sp) bb = umax64(bb, load_coherent(pr + sp));
       rowbest[tid] = bb;
     }
   } else if (tid == 0) {
@@ -97,7 +95,7 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptParams p) {
     while (k < p.gamma && p.draft[(int64_t)s * p.gamma + k] == (int32_t)(0xFFFFFFFFu - (uint32_t)rowbest[k])) ++k;
     p.accept_out[s] = k;
     if (p.bonus_out) p.bonus_out[s] = (int32_t)(0xFFFFFFFFu - (uint32_t)rowbest[k]);
-    if (per_seq > 1) p.counters[s] = 0u;
+    if (per_seq > 1) reset_counter(&p.counters[s]);
   }
   if (p.argmax_out && tid < rows)
     p.argmax_out[(int64_t)s * rows + tid] = (int32_t)(0xFFFFFFFFu - (uint32_t)rowbest[tid]);
@@ -116,7 +114,7 @@ AcceptPlan plan_accept(int S, int gamma, int vocab) {
   chunk = (chunk + 3) & ~int64_t(3);
   pl.chunk = (int)chunk;
   pl.nsplit = (int)((vocab + chunk - 1) / chunk);
-  pl.counter_bytes = align256(sizeof(uint32_t) * (size_t)S);
+  pl.counter_bytes = BD_WS_COUNTER_BYTES;
   pl.ws_bytes = pl.counter_bytes + align256(sizeof(uint64_t) * (size_t)rows * pl.nsplit);
   return pl;
 }

@@ -46,7 +46,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 template <int NT>
 struct RowBlock {
   static constexpr int kRows = 16 * NT;
-  static constexpr int kRec = kRows * (2 + kD);   // floats of one partial record
+  static constexpr int kRec = kRows * (3 + kD);   // floats of one partial record: m, l, lx, o[128]
 };
 
 // LDS scratch of one workgroup.
@@ -55,6 +55,7 @@ struct AttnSmem {
   alignas(16) float o[kWaves][16 * NT][kD];     // per-wave unnormalised outputs
   float m[kWaves][16 * NT];
   float l[kWaves][16 * NT];
+  float lx[kWaves][16 * NT];
   int32_t sidx[kMaxGatherSplit];    // gathered positions of this split
   int32_t last;
 };
@@ -120,7 +121,8 @@ template <int NT>
 struct RowState {
   f32x4 o[NT][8];     // O^T[d-tile][row tile]
   float m[NT];        // running max (log2 domain), shared by the 4 lane groups
-  float l[NT];        // running sum, this lane's keys only
+  float l[NT];        // running sum of the bf16-rounded weights the PV product uses (normaliser)
+  float lx[NT];       // running sum of the unrounded weights (log-sum-exp); both this lane's keys only
 };
 
 template <int NT, bool PAGED>
@@ -156,17 +158,20 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
     const float mnew = fmaxf(st.m[nt], mx);
     const float muse = mnew == -INFINITY ? 0.f : mnew;
     const float alpha = exp2f(st.m[nt] - muse);
-    float psum = 0.f;
+    float psum = 0.f, pxsum = 0.f;
     u32x4 pw;
 #pragma unroll
     for (int i = 0; i < 8; i += 2) {
       // the sum uses the bf16-rounded weights that the PV product sees
-      const uint32_t w = pack_bf16x2(exp2f(sv[i] - muse), exp2f(sv[i + 1] - muse));
+      const float p0 = exp2f(sv[i] - muse), p1 = exp2f(sv[i + 1] - muse);
+      const uint32_t w = pack_bf16x2(p0, p1);
+      pxsum += p0 + p1;
       psum += bf16_lo(w) + bf16_hi(w);
       pw[i >> 1] = w;
     }
     pop[nt] = as_bf16x8(pw);
     st.l[nt] = st.l[nt] * alpha + psum;
+    st.lx[nt] = st.lx[nt] * alpha + pxsum;
     st.m[nt] = mnew;
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] *= alpha;
@@ -247,6 +252,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   for (int nt = 0; nt < NT; ++nt) {
     st.m[nt] = -INFINITY;
     st.l[nt] = 0.f;
+    st.lx[nt] = 0.f;
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -273,13 +279,16 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   // ---- wave state -> LDS: row r = 16*nt + lane%16; lane group lg holds d in [32lg, 32lg+32)
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    float l = st.l[nt];
+    float l = st.l[nt], lx = st.lx[nt];
     l += shfl_xor_f(l, 16);
     l += shfl_xor_f(l, 32);
+    lx += shfl_xor_f(lx, 16);
+    lx += shfl_xor_f(lx, 32);
     const int r = 16 * nt + lr;
     if (lg == 0) {
       sm.m[wave][r] = st.m[nt];
       sm.l[wave][r] = l;
+      sm.lx[wave][r] = lx;
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -298,13 +307,14 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm.m[w][r]);
   const float Muse = M == -INFINITY ? 0.f : M;
-  float Lsum = 0.f, acc[kPerThread];
+  float Lsum = 0.f, Lx = 0.f, acc[kPerThread];
 #pragma unroll
   for (int e = 0; e < kPerThread; ++e) acc[e] = 0.f;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) {
     const float wt = exp2f(sm.m[w][r] - Muse);
     Lsum += wt * sm.l[w][r];
+    Lx += wt * sm.lx[w][r];
 #pragma unroll
     for (int e = 0; e < kPerThread; ++e) acc[e] += wt * sm.o[w][r][d0 + e];
   }
@@ -318,7 +328,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   uint16_t* out = gather ? p.out_g + (int64_t)view * view_rows * kD : p.out_f;
   float* lse = gather ? (p.lse_g ? p.lse_g + (int64_t)view * view_rows : nullptr) : p.lse_f;
 
-  auto write_final = [&](float Mf, float Lf, const float* a) {
+  auto write_final = [&](float Mf, float Lf, float Lxf, const float* a) {
     if (!row_valid) return;
     const float inv = Lf > 0.f ? 1.f / Lf : 0.f;
     uint32_t w[kPerThread / 2];
@@ -328,53 +338,53 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
 #pragma unroll
     for (int e = 0; e < kPerThread / 8; ++e)
       *reinterpret_cast<u32x4*>(dst + 8 * e) = u32x4{w[4 * e], w[4 * e + 1], w[4 * e + 2], w[4 * e + 3]};
-    if (lse && d0 == 0) lse[orow] = Lf > 0.f ? (Mf + __log2f(Lf)) * kLn2 : -INFINITY;
+    if (lse && d0 == 0) lse[orow] = Lxf > 0.f ? (Mf + __log2f(Lxf)) * kLn2 : -INFINITY;
   };
 
   if (nsplit == 1) {
-    write_final(M, Lsum, acc);
+    write_final(M, Lsum, Lx, acc);
     return;
   }
 
-  // ---- publish this split's partial record, the last split merges all of them
+  // ---- publish this split's partial record (rows that exist only); the last split merges them
   float* rec_base = p.part + (gather ? 0 : (int64_t)p.units_g * p.nsplit_g * RB::kRec);
   const int unit_local = gather ? unit : unit - p.units_g;
   float* rec = rec_base + ((int64_t)unit_local * nsplit + split) * RB::kRec;
-  if (d0 == 0) {
-    rec[2 * r] = M;
-    rec[2 * r + 1] = Lsum;
-  }
-  float* ro = rec + 2 * RB::kRows + r * kD + d0;
+  if (row_valid) {
+    if (d0 == 0) {
+      store_coherent(rec + 3 * r, M);
+      store_coherent(rec + 3 * r + 1, Lsum);
+      store_coherent(rec + 3 * r + 2, Lx);
+    }
+    float* ro = rec + 3 * RB::kRows + r * kD + d0;
 #pragma unroll
-  for (int e = 0; e < kPerThread; e += 4)
-    *reinterpret_cast<f32x4*>(ro + e) = f32x4{acc[e], acc[e + 1], acc[e + 2], acc[e + 3]};
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const uint32_t prev = atomicAdd(&p.counters[unit], 1u);
-    sm.last = prev == (uint32_t)(nsplit - 1);
+    for (int e = 0; e < kPerThread; ++e) store_coherent(ro + e, acc[e]);
   }
+  wait_vmem();
+  __syncthreads();
+  if (tid == 0) sm.last = arrive(&p.counters[unit], (uint32_t)nsplit);
   __syncthreads();
   if (!sm.last) return;
-  __threadfence();
+  if (tid == 0) reset_counter(&p.counters[unit]);   // ready for the next call
+  if (!row_valid) return;
 
   const float* urec = rec_base + (int64_t)unit_local * nsplit * RB::kRec;
   float Mg = -INFINITY;
-  for (int sp = 0; sp < nsplit; ++sp) Mg = fmaxf(Mg, urec[(int64_t)sp * RB::kRec + 2 * r]);
+  for (int sp = 0; sp < nsplit; ++sp) Mg = fmaxf(Mg, load_coherent(urec + (int64_t)sp * RB::kRec + 3 * r));
   const float Mgu = Mg == -INFINITY ? 0.f : Mg;
-  float Lg = 0.f, ag[kPerThread];
+  float Lg = 0.f, Lxg = 0.f, ag[kPerThread];
 #pragma unroll
   for (int e = 0; e < kPerThread; ++e) ag[e] = 0.f;
   for (int sp = 0; sp < nsplit; ++sp) {
     const float* rs = urec + (int64_t)sp * RB::kRec;
-    const float wt = exp2f(rs[2 * r] - Mgu);
-    Lg += wt * rs[2 * r + 1];
-    const float* os = rs + 2 * RB::kRows + r * kD + d0;
+    const float wt = exp2f(load_coherent(rs + 3 * r) - Mgu);
+    Lg += wt * load_coherent(rs + 3 * r + 1);
+    Lxg += wt * load_coherent(rs + 3 * r + 2);
+    const float* os = rs + 3 * RB::kRows + r * kD + d0;
 #pragma unroll
-    for (int e = 0; e < kPerThread; ++e) ag[e] += wt * os[e];
+    for (int e = 0; e < kPerThread; ++e) ag[e] += wt * load_coherent(os + e);
   }
-  write_final(Mg, Lg, ag);
-  if (tid == 0) p.counters[unit] = 0u;   // leave the counter ready for the next call
+  write_final(Mg, Lg, Lxg, ag);
 }
 
 }  // namespace
@@ -402,7 +412,7 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
   pl.nsplit_f = max_L > 0 ? (int)((max_L + kf - 1) / kf) : 1;
   const int64_t blocks = (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f;
   pl.nblk = (int)blocks;
-  pl.counter_bytes = align256(sizeof(uint32_t) * (size_t)(pl.units_g + pl.units_f));
+  pl.counter_bytes = BD_WS_COUNTER_BYTES;   // fixed: scratch of any call never lands on a counter
   const bool split = (pl.units_g && pl.nsplit_g > 1) || (pl.units_f && pl.nsplit_f > 1);
   pl.record_bytes = split ? align256(sizeof(float) * attn_record_floats(pl.nt) * (size_t)blocks) : 0;
   pl.ws_bytes = pl.counter_bytes + pl.record_bytes;

@@ -78,6 +78,8 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
       bd::plan_attn(kv->num_seqs, kv->num_kv_heads, Hq, nq, num_views, ld_idx, kv->max_seq_len, out_full != nullptr);
   if (pl.nblk < 0 || (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f > INT32_MAX)
     return fail(BD_ERR_UNSUPPORTED, "problem too large for one launch");
+  if ((int64_t)pl.units_g + pl.units_f > BD_WS_COUNTER_BYTES / 4)
+    return fail(BD_ERR_UNSUPPORTED, "more than %d work units", BD_WS_COUNTER_BYTES / 4);
   bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
   if (st != BD_OK) return st;
   if (pl.nblk == 0) return BD_OK;
@@ -170,7 +172,7 @@ bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_
   p.kps = pl.kps;
   p.max_L = kv->max_seq_len;
   p.scale_log2 = scale * 1.4426950408889634f;
-  char* w = static_cast<char*>(ws);
+  char* w = static_cast<char*>(ws) + BD_WS_COUNTER_BYTES;   // the counter region stays untouched
   p.stats = reinterpret_cast<float*>(w);
   p.raw_part = reinterpret_cast<float*>(w + pl.stats_bytes);
   p.raw = scores_out ? scores_out : reinterpret_cast<float*>(w + pl.stats_bytes + pl.raw_part_bytes);
@@ -264,6 +266,7 @@ bd_status bd_accept_len(const float* logits, int64_t row_stride, const int32_t* 
   if (gamma > 0 && !draft) return fail(BD_ERR_INVALID_ARG, "draft is NULL");
   if (row_stride < vocab) return fail(BD_ERR_INVALID_ARG, "row_stride %lld < vocab %d", (long long)row_stride, vocab);
   if ((int64_t)num_seqs * (gamma + 1) * 1024 > INT32_MAX) return fail(BD_ERR_UNSUPPORTED, "too many rows");
+  if (num_seqs > BD_WS_COUNTER_BYTES / 4) return fail(BD_ERR_UNSUPPORTED, "more than %d sequences", BD_WS_COUNTER_BYTES / 4);
   const bd::AcceptPlan pl = bd::plan_accept(num_seqs, gamma, vocab);
   bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
   if (st != BD_OK) return st;

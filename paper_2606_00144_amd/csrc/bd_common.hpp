@@ -83,6 +83,43 @@ __device__ inline float sum16(float x) {
   return x;
 }
 
+// ---- data handed from one workgroup to another -----------------------------
+//
+// The splits of a unit publish partial results for the last workgroup to
+// finish.  They are written and read with relaxed agent-scope atomic accesses,
+// which gfx950 performs at the device coherence point (the `sc1` cache
+// policy), so neither side needs a cache-wide fence: the writer waits until
+// its stores are acknowledged (vmcnt(0)) before bumping the counter, and the
+// reader issues its loads only after seeing the final count.  (A
+// __threadfence() here would write back and invalidate the whole L2 of the
+// XCD once per workgroup.)
+__device__ inline void store_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void store_coherent(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline float load_coherent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint64_t load_coherent(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Wait until every vector memory operation of this wave has completed.
+__device__ inline void wait_vmem() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), expcnt/lgkmcnt unconstrained
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+// Count one finished split of a unit; true in the workgroup that finished last.
+__device__ inline bool arrive(uint32_t* counter, uint32_t total) {
+  const uint32_t prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  return prev == total - 1;
+}
+__device__ inline void reset_counter(uint32_t* counter) {
+  __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ---- bf16 helpers ---------------------------------------------------------
 
 __device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }

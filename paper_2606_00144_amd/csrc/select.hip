@@ -383,7 +383,7 @@ SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L) {
   pl.stats_bytes = align256(sizeof(float) * (size_t)units * pl.nsplit * kStatRows * 2);
   pl.raw_part_bytes = align256(sizeof(float) * (size_t)units * max_L);
   pl.raw_bytes = align256(sizeof(float) * (size_t)S * Hkv * max_L);
-  pl.ws_bytes = pl.stats_bytes + pl.raw_part_bytes + pl.raw_bytes;
+  pl.ws_bytes = BD_WS_COUNTER_BYTES + pl.stats_bytes + pl.raw_part_bytes + pl.raw_bytes;
   return pl;
 }
 

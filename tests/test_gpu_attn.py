@@ -238,3 +238,32 @@ def test_multiview_config3_sampled():
                               [nv[s:s + 1] for nv in nsel_v], lens[:1])
     assert_close(gv[:, s:s + 1], rv, "cfg3 views seq 1")
     assert_close(gf[s:s + 1], rf, "cfg3 full seq 1")
+
+
+def test_one_workspace_serves_every_operation_and_shape():
+    """Counters must start at zero for every call even after calls of other shapes left scratch behind."""
+    ws = bd.Workspace()
+    g = np.random.default_rng(40)
+    shapes = [(2, 8, 2, 300, 5), (6, 32, 32, 2000, 5), (1, 16, 2, 700, 0), (3, 32, 8, 4000, 3), (6, 32, 32, 1500, 5)]
+    for it, (S, Hq, Hkv, L, gamma) in enumerate(shapes):
+        k, v = _rand_bits((S, Hkv, L, 128), 50 + it), _rand_bits((S, Hkv, L, 128), 60 + it)
+        q = _rand_bits((S, gamma + 1, Hq, 128), 70 + it)
+        lens = g.integers(gamma + 1, L + 1, size=S).tolist()
+        case(f"shared workspace verify {S}x{Hq}/{Hkv}x{L} gamma={gamma}")
+        out = bd.bd_verify_attn(bf16_dev(k), bf16_dev(v), bf16_dev(q), i32_dev(lens), workspace=ws)
+        torch.cuda.synchronize()
+        assert_close(bf16_host64(out), O.verify_attn(k, v, q, lens, gamma)[0], f"shared ws verify {it}")
+        B = min(256, L)
+        idx = np.stack([np.stack([np.sort(g.choice(L, B, replace=False)) for _ in range(Hkv)]) for _ in range(S)]).astype(np.int32)
+        case(f"shared workspace decode {S}x{Hq}/{Hkv}x{L}")
+        out = bd.bd_sparse_decode_attn(bf16_dev(k), bf16_dev(v), bf16_dev(q[:, -1]), i32_dev(idx), i32_dev([B] * S),
+                                       i32_dev(lens), workspace=ws)
+        torch.cuda.synchronize()
+        assert_close(bf16_host64(out), O.sparse_decode_attn(k, v, q[:, -1], idx, [B] * S, lens)[0], f"shared ws decode {it}")
+        lg = g.standard_normal((S, gamma + 1, 5000)).astype(np.float32)
+        dr = g.integers(0, 5000, (S, gamma)).astype(np.int32)
+        case("shared workspace accept")
+        acc, bonus = bd.bd_accept_len(torch.from_numpy(lg).cuda(), i32_dev(dr), workspace=ws)
+        torch.cuda.synchronize()
+        ra, rb, _ = O.accept_len(lg, dr, gamma)
+        assert np.array_equal(acc.cpu().numpy(), ra) and np.array_equal(bonus.cpu().numpy(), rb)
