@@ -40,8 +40,9 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * kWave;
 constexpr int kTile = 32;                      // keys per wave iteration
-constexpr int64_t kTargetBlocks = 512;         // workgroups per launch the splits aim for
+constexpr int64_t kTargetBlocks = 256;         // workgroups per launch the splits aim for (one per CU)
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kSlack = 8.f;                  // lazy-rescale headroom, log2 units
 
 template <int NT>
 struct RowBlock {
@@ -49,60 +50,135 @@ struct RowBlock {
   static constexpr int kRec = kRows * (3 + kD);   // floats of one partial record: m, l, lx, o[128]
 };
 
-// LDS scratch of one workgroup.
+// Key slots of one split: row offset (16-byte units) and position of every
+// key, resolved once per workgroup (idx gather, page-table lookup, bounds) so
+// that the streaming loop issues only unconditional loads.  kAhead extra tiles
+// per wave of padding slots (position -1, offset 0: a safe address) let every
+// wave prefetch past its last tile without a branch.
+// Each wave streams its tiles through kRing LDS slots with direct-to-LDS
+// loads (global_load_lds_dwordx4), which need no registers while in flight: a
+// tile is copied to registers just before its step and its slot is refilled at
+// once, so kRing tiles stay in flight during every step.
+constexpr int kRing = 2;
+constexpr int kTileLoads = 16;                  // 16-byte loads per lane per tile: K 8, V 8
+constexpr int kTileBytes = kTileLoads * kWave * 16;
+constexpr int kMaxAhead = kRing;
+constexpr int kSlotCap = kMaxSplitKeys + kMaxAhead * kWaves * kTile;
+
+// LDS scratch of one workgroup: the slot table while streaming, the per-wave
+// partial outputs while merging (separated by a barrier).
 template <int NT>
 struct AttnSmem {
-  alignas(16) float o[kWaves][16 * NT][kD];     // per-wave unnormalised outputs
-  float m[kWaves][16 * NT];
-  float l[kWaves][16 * NT];
-  float lx[kWaves][16 * NT];
-  int32_t sidx[kMaxGatherSplit];    // gathered positions of this split
+  union {
+    struct {
+      alignas(16) int32_t roff[kSlotCap];
+      alignas(16) int32_t tpos[kSlotCap];
+      alignas(16) uint8_t ring[kWaves][kRing][kTileBytes];   // per-wave tile slots filled by DMA
+    } slots;
+    struct {
+      alignas(16) float o[kWaves][16 * NT][kD];     // per-wave unnormalised outputs
+      float m[kWaves][16 * NT];
+      float l[kWaves][16 * NT];
+      float lx[kWaves][16 * NT];
+    } merge;
+  } u;
   int32_t last;
-};
-
-// Resolve the key position of slot u (0..31) of a tile starting at slot b.
-struct KeySlots {
-  bool gather;
-  const int32_t* sidx;   // LDS copy of idx[e_begin .. e_end)
-  int e_begin, e_end;    // slot range of this split
-  int L;
-  __device__ int pos(int slot) const {   // absolute slot -> position or -1
-    if (slot >= e_end) return -1;
-    const int t = gather ? sidx[slot - e_begin] : slot;
-    return (t >= 0 && t < L) ? t : -1;
-  }
 };
 
 template <int NT, bool PAGED>
 struct TileRegs {
   u32x4 k[2][4];     // [key subtile][k-step]: 16 keys x 64 B per lane group
   u32x4 v[8];        // 8 key rows x 16 B
-  int tpos[8];       // positions of the 8 score slots (-1 = absent)
+  u32x4 tp[2];       // positions of the 8 score slots (-1 = absent), slot i in tp[i/4][i%4]
 };
 
+// Row offsets (16-byte units) of the 10 key rows a lane loads for one tile:
+// K rows slot0+lr and slot0+16+lr, V rows slot0 + 16h + 4*(lane/16) + 0..3.
+struct TileRows {
+  uint32_t k[2];
+  u32x4 v[2];
+};
+
+// Read a tile's row offsets from the LDS slot table: loads and their wait in one asm statement.
+__device__ inline void read_rows(TileRows& A, uint32_t roff_lds, int slot0, int lane) {
+  const int lg = lane >> 4, lr = lane & 15;
+  const uint32_t ak = roff_lds + 4 * (slot0 + lr);
+  const uint32_t av = roff_lds + 4 * (slot0 + 4 * lg);
+  asm volatile(
+      "ds_read_b32 %0, %4\n"
+      "ds_read_b32 %1, %4 offset:64\n"
+      "ds_read_b128 %2, %5\n"
+      "ds_read_b128 %3, %5 offset:64\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(A.k[0]), "=&v"(A.k[1]), "=&v"(A.v[0]), "=&v"(A.v[1])
+      : "v"(ak), "v"(av));
+}
+
+// Copy the landed tile in LDS slot `src` into registers and read the row offsets of the
+// tile to prefetch next, all in one asm statement ending in its own wait.
 template <int NT, bool PAGED>
-__device__ inline void load_tile(TileRegs<NT, PAGED>& T, const KvView& kv, const KeySlots& ks, int s, int g,
-                                 int slot0, int lane) {
+__device__ inline void read_tile_and_rows(TileRegs<NT, PAGED>& T, TileRows& A, uint32_t src, uint32_t tpos_lds,
+                                          int slot0, uint32_t roff_lds, int next0, int lane) {
+  const int lg = lane >> 4, lr = lane & 15;
+  const uint32_t at = src + 16 * lane;
+  const uint32_t ap = tpos_lds + 4 * (slot0 + 4 * lg);
+  const uint32_t ak = roff_lds + 4 * (next0 + lr);
+  const uint32_t av = roff_lds + 4 * (next0 + 4 * lg);
+  asm volatile(
+      "ds_read_b128 %0, %22\n"
+      "ds_read_b128 %1, %22 offset:1024\n"
+      "ds_read_b128 %2, %22 offset:2048\n"
+      "ds_read_b128 %3, %22 offset:3072\n"
+      "ds_read_b128 %4, %22 offset:4096\n"
+      "ds_read_b128 %5, %22 offset:5120\n"
+      "ds_read_b128 %6, %22 offset:6144\n"
+      "ds_read_b128 %7, %22 offset:7168\n"
+      "ds_read_b128 %8, %22 offset:8192\n"
+      "ds_read_b128 %9, %22 offset:9216\n"
+      "ds_read_b128 %10, %22 offset:10240\n"
+      "ds_read_b128 %11, %22 offset:11264\n"
+      "ds_read_b128 %12, %22 offset:12288\n"
+      "ds_read_b128 %13, %22 offset:13312\n"
+      "ds_read_b128 %14, %22 offset:14336\n"
+      "ds_read_b128 %15, %22 offset:15360\n"
+      "ds_read_b128 %16, %23\n"
+      "ds_read_b128 %17, %23 offset:64\n"
+      "ds_read_b32 %18, %24\n"
+      "ds_read_b32 %19, %24 offset:64\n"
+      "ds_read_b128 %20, %25\n"
+      "ds_read_b128 %21, %25 offset:64\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(T.k[0][0]), "=&v"(T.k[0][1]), "=&v"(T.k[0][2]), "=&v"(T.k[0][3]), "=&v"(T.k[1][0]),
+        "=&v"(T.k[1][1]), "=&v"(T.k[1][2]), "=&v"(T.k[1][3]), "=&v"(T.v[0]), "=&v"(T.v[1]), "=&v"(T.v[2]),
+        "=&v"(T.v[3]), "=&v"(T.v[4]), "=&v"(T.v[5]), "=&v"(T.v[6]), "=&v"(T.v[7]), "=&v"(T.tp[0]), "=&v"(T.tp[1]),
+        "=&v"(A.k[0]), "=&v"(A.k[1]), "=&v"(A.v[0]), "=&v"(A.v[1])
+      : "v"(at), "v"(ap), "v"(ak), "v"(av));
+}
+
+__device__ inline void dma16(const uint16_t* g, uint8_t* l) {
+  __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)l, 16, 0, 0);
+}
+
+// Issue the direct-to-LDS loads of a tile into `dst`: load q of a lane lands at
+// dst + q*1 KiB + 16*lane (q 0..7: K subtile q/4, k-step q%4; q 8..15: V row slot q-8).
+// Row offsets are clamped to the layout's extent (validated on the host), so no
+// value can address outside the K/V allocation.
+__device__ inline void dma_tile(const KvView& kv, const TileRows& A, uint32_t max_roff, uint8_t* dst, int lane) {
   const int lg = lane >> 4, lr = lane & 15;
 #pragma unroll
   for (int sub = 0; sub < 2; ++sub) {
-    const int t = ks.pos(slot0 + 16 * sub + lr);
-    int64_t off = t >= 0 ? row_offset<PAGED>(kv, s, g, t) : -1;
+    const uint32_t ro = A.k[sub] < max_roff ? A.k[sub] : max_roff;
+    const uint16_t* kr = kv.k + ((uint64_t)ro << 3) + 32 * lg;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (off >= 0) T.k[sub][j] = load16(kv.k + off + 32 * lg + 8 * j);
-      else T.k[sub][j] = u32x4{0u, 0u, 0u, 0u};
+    for (int j = 0; j < 4; ++j) dma16(kr + 8 * j, dst + (4 * sub + j) * 1024);
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t ro = A.v[h][i] < max_roff ? A.v[h][i] : max_roff;
+      dma16(kv.v + ((uint64_t)ro << 3) + 8 * lr, dst + (8 + 4 * h + i) * 1024);
     }
-  }
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int slot = 16 * (i >> 2) + 4 * lg + (i & 3);
-    const int t = ks.pos(slot0 + slot);
-    int64_t off = t >= 0 ? row_offset<PAGED>(kv, s, g, t) : -1;
-    T.tpos[i] = off >= 0 ? t : -1;
-    if (off >= 0) T.v[i] = load16(kv.v + off + 8 * lr);
-    else T.v[i] = u32x4{0u, 0u, 0u, 0u};
-  }
 }
 
 // Transposed V operand for d-tile dt: slot i holds V[key slot i][8*(lane%16) + dt].
@@ -141,6 +217,9 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
       sacc[sub][nt] = a;
     }
 
+  // online softmax with a lazily raised reference max: the accumulators are rescaled only when a
+  // tile's max exceeds the reference by more than kSlack (log2 units), so weights stay <= 2^kSlack
+  // and the common tile costs no rescale at all
   bf16x8 pop[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
@@ -148,33 +227,34 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const float x = sacc[i >> 2][nt][i & 3] * scale_log2;
-      const bool vis = T.tpos[i] >= 0 && T.tpos[i] <= rowpos[nt];
-      sv[i] = vis ? x : -INFINITY;
+      const int tpos = (int)T.tp[i >> 2][i & 3];
+      const bool vis = tpos >= 0 && tpos <= rowpos[nt];
+      sv[i] = vis ? sacc[i >> 2][nt][i & 3] * scale_log2 : -INFINITY;
       mx = fmaxf(mx, sv[i]);
     }
-    mx = fmaxf(mx, shfl_xor_f(mx, 16));
-    mx = fmaxf(mx, shfl_xor_f(mx, 32));
-    const float mnew = fmaxf(st.m[nt], mx);
-    const float muse = mnew == -INFINITY ? 0.f : mnew;
-    const float alpha = exp2f(st.m[nt] - muse);
+    mx = max_xor32(max_xor16(mx));
+    if (mx > st.m[nt] + kSlack) {
+      const float alpha = __builtin_amdgcn_exp2f(st.m[nt] - mx);   // 0 on the first visible tile
+      st.l[nt] *= alpha;
+      st.lx[nt] *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] *= alpha;
+      st.m[nt] = mx;
+    }
+    const float muse = st.m[nt] == -INFINITY ? 0.f : st.m[nt];
     float psum = 0.f, pxsum = 0.f;
     u32x4 pw;
 #pragma unroll
     for (int i = 0; i < 8; i += 2) {
-      // the sum uses the bf16-rounded weights that the PV product sees
-      const float p0 = exp2f(sv[i] - muse), p1 = exp2f(sv[i + 1] - muse);
+      const float p0 = __builtin_amdgcn_exp2f(sv[i] - muse), p1 = __builtin_amdgcn_exp2f(sv[i + 1] - muse);
       const uint32_t w = pack_bf16x2(p0, p1);
       pxsum += p0 + p1;
-      psum += bf16_lo(w) + bf16_hi(w);
+      psum += bf16_lo(w) + bf16_hi(w);   // the normaliser sums the rounded weights the PV product sees
       pw[i >> 1] = w;
     }
     pop[nt] = as_bf16x8(pw);
-    st.l[nt] = st.l[nt] * alpha + psum;
-    st.lx[nt] = st.lx[nt] * alpha + pxsum;
-    st.m[nt] = mnew;
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] *= alpha;
+    st.l[nt] += psum;
+    st.lx[nt] += pxsum;
   }
 
 #pragma unroll
@@ -223,14 +303,46 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   int e_end = e_begin + kps;
   if (e_end > n_keys) e_end = n_keys;
 
-  if (gather) {
-    for (int i = tid; i < kps; i += kThreads) {
-      const int e = e_begin + i;
-      sm.sidx[i] = e < e_end ? idx_row[e] : -1;
+  const int ntiles = e_end > e_begin ? (e_end - e_begin + kTile - 1) / kTile : 0;
+  const int nslots = (ntiles + kMaxAhead * kWaves) * kTile;     // <= kSlotCap: padding tiles included
+  {
+    // all idx and page-table loads are issued before any result is used
+    constexpr int kPer = (kSlotCap + kThreads - 1) / kThreads;
+    int tv[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int e = e_begin + tid + k * kThreads;
+      int t = -1;
+      if (e < e_end) t = gather ? idx_row[e] : e;
+      tv[k] = (t >= 0 && t < L) ? t : -1;
     }
-    __syncthreads();
+    int pg[kPer];
+    if constexpr (PAGED) {
+#pragma unroll
+      for (int k = 0; k < kPer; ++k)
+        pg[k] = tv[k] >= 0 ? p.kv.page_table[(int64_t)s * p.kv.max_pages_per_seq + tv[k] / p.kv.page_size] : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int i = tid + k * kThreads;
+      if (i < nslots) {
+        int t = tv[k];
+        int64_t o;
+        if constexpr (PAGED) {
+          o = (unsigned)pg[k] < (unsigned)p.kv.num_pages
+                  ? (int64_t)pg[k] * p.kv.stride_page + (int64_t)g * p.kv.stride_head +
+                        (int64_t)(t % p.kv.page_size) * p.kv.stride_tok
+                  : -1;
+        } else {
+          o = (int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head + (int64_t)t * p.kv.stride_tok;
+        }
+        if (t < 0 || o < 0) { t = -1; o = 0; }
+        sm.u.slots.roff[i] = (int)(o >> 3);
+        sm.u.slots.tpos[i] = t;
+      }
+    }
   }
-  KeySlots ks{gather, sm.sidx, e_begin, e_end, L};
+  __syncthreads();
 
   // ---- query rows of this lane: row n = rb*RB + 16*nt + lane%16
   bf16x8 qop[NT][4];
@@ -257,24 +369,36 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
     for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // ---- stream this wave's tiles (tile w, w+4, ...), one tile of loads in flight ahead
-  const int ntiles = e_end > e_begin ? (e_end - e_begin + kTile - 1) / kTile : 0;
+  // ---- stream this wave's tiles (tile w, w+4, ...) through its two LDS slots.  The waits are
+  // explicit: the tile about to be read was issued kTileLoads loads before the newest ones.
   if (wave < ntiles) {
-    TileRegs<NT, PAGED> ta, tb;
-    load_tile<NT, PAGED>(ta, p.kv, ks, s, g, e_begin + kTile * wave, lane);
-    int it = wave;
-    while (true) {
-      const int nx = it + kWaves;
-      if (nx < ntiles) load_tile<NT, PAGED>(tb, p.kv, ks, s, g, e_begin + kTile * nx, lane);
-      tile_step<NT, PAGED>(st, ta, qop, rowpos, p.scale_log2);
-      if (nx >= ntiles) break;
-      const int nx2 = nx + kWaves;
-      if (nx2 < ntiles) load_tile<NT, PAGED>(ta, p.kv, ks, s, g, e_begin + kTile * nx2, lane);
-      tile_step<NT, PAGED>(st, tb, qop, rowpos, p.scale_log2);
-      if (nx2 >= ntiles) break;
-      it = nx2;
+    const uint32_t roff_lds = lds_addr(sm.u.slots.roff);
+    const uint32_t tpos_lds = lds_addr(sm.u.slots.tpos);
+    uint8_t* slot_a = sm.u.slots.ring[wave][0];
+    uint8_t* slot_b = sm.u.slots.ring[wave][1];
+    const uint32_t slot_a_lds = lds_addr(slot_a), slot_b_lds = lds_addr(slot_b);
+    TileRows A;
+    read_rows(A, roff_lds, kTile * wave, lane);
+    dma_tile(p.kv, A, p.max_roff, slot_a, lane);
+    read_rows(A, roff_lds, kTile * (wave + kWaves), lane);
+    dma_tile(p.kv, A, p.max_roff, slot_b, lane);
+    TileRegs<NT, PAGED> T;
+    for (int it = wave;; it += 2 * kWaves) {
+      asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+      read_tile_and_rows<NT, PAGED>(T, A, slot_a_lds, tpos_lds, kTile * it, roff_lds, kTile * (it + 2 * kWaves), lane);
+      dma_tile(p.kv, A, p.max_roff, slot_a, lane);
+      tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2);
+      if (it + kWaves >= ntiles) break;
+      asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+      read_tile_and_rows<NT, PAGED>(T, A, slot_b_lds, tpos_lds, kTile * (it + kWaves), roff_lds,
+                                    kTile * (it + 3 * kWaves), lane);
+      dma_tile(p.kv, A, p.max_roff, slot_b, lane);
+      tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2);
+      if (it + 2 * kWaves >= ntiles) break;
     }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the LDS is reused
   }
+  __syncthreads();   // the slot table is dead from here on; its LDS becomes the merge buffer
 
   // ---- wave state -> LDS: row r = 16*nt + lane%16; lane group lg holds d in [32lg, 32lg+32)
 #pragma unroll
@@ -286,13 +410,13 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
     lx += shfl_xor_f(lx, 32);
     const int r = 16 * nt + lr;
     if (lg == 0) {
-      sm.m[wave][r] = st.m[nt];
-      sm.l[wave][r] = l;
-      sm.lx[wave][r] = lx;
+      sm.u.merge.m[wave][r] = st.m[nt];
+      sm.u.merge.l[wave][r] = l;
+      sm.u.merge.lx[wave][r] = lx;
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float* dst = &sm.o[wave][r][32 * lg + 8 * i];
+      float* dst = &sm.u.merge.o[wave][r][32 * lg + 8 * i];
       *reinterpret_cast<f32x4*>(dst) = f32x4{st.o[nt][0][i], st.o[nt][1][i], st.o[nt][2][i], st.o[nt][3][i]};
       *reinterpret_cast<f32x4*>(dst + 4) = f32x4{st.o[nt][4][i], st.o[nt][5][i], st.o[nt][6][i], st.o[nt][7][i]};
     }
@@ -305,18 +429,18 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   const int d0 = (tid % (kD / kPerThread)) * kPerThread;
   float M = -INFINITY;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm.m[w][r]);
+  for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm.u.merge.m[w][r]);
   const float Muse = M == -INFINITY ? 0.f : M;
   float Lsum = 0.f, Lx = 0.f, acc[kPerThread];
 #pragma unroll
   for (int e = 0; e < kPerThread; ++e) acc[e] = 0.f;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) {
-    const float wt = exp2f(sm.m[w][r] - Muse);
-    Lsum += wt * sm.l[w][r];
-    Lx += wt * sm.lx[w][r];
+    const float wt = exp2f(sm.u.merge.m[w][r] - Muse);
+    Lsum += wt * sm.u.merge.l[w][r];
+    Lx += wt * sm.u.merge.lx[w][r];
 #pragma unroll
-    for (int e = 0; e < kPerThread; ++e) acc[e] += wt * sm.o[w][r][d0 + e];
+    for (int e = 0; e < kPerThread; ++e) acc[e] += wt * sm.u.merge.o[w][r][d0 + e];
   }
 
   const int n = rb * RB::kRows + r;
@@ -368,21 +492,43 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   if (tid == 0) reset_counter(&p.counters[unit]);   // ready for the next call
   if (!row_valid) return;
 
+  // merge the splits in split order; every batch of loads is issued before any result is used
   const float* urec = rec_base + (int64_t)unit_local * nsplit * RB::kRec;
+  constexpr int kBatch = 8;
   float Mg = -INFINITY;
-  for (int sp = 0; sp < nsplit; ++sp) Mg = fmaxf(Mg, load_coherent(urec + (int64_t)sp * RB::kRec + 3 * r));
+  for (int sp0 = 0; sp0 < nsplit; sp0 += kBatch) {
+    float mv[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      mv[u] = sp0 + u < nsplit ? load_coherent(urec + (int64_t)(sp0 + u) * RB::kRec + 3 * r) : -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) Mg = fmaxf(Mg, mv[u]);
+  }
   const float Mgu = Mg == -INFINITY ? 0.f : Mg;
   float Lg = 0.f, Lxg = 0.f, ag[kPerThread];
 #pragma unroll
   for (int e = 0; e < kPerThread; ++e) ag[e] = 0.f;
-  for (int sp = 0; sp < nsplit; ++sp) {
-    const float* rs = urec + (int64_t)sp * RB::kRec;
-    const float wt = exp2f(load_coherent(rs + 3 * r) - Mgu);
-    Lg += wt * load_coherent(rs + 3 * r + 1);
-    Lxg += wt * load_coherent(rs + 3 * r + 2);
-    const float* os = rs + 3 * RB::kRows + r * kD + d0;
+  constexpr int kOBatch = 4;
+  for (int sp0 = 0; sp0 < nsplit; sp0 += kOBatch) {
+    float mv[kOBatch], lv[kOBatch], lxv[kOBatch], ov[kOBatch][kPerThread];
 #pragma unroll
-    for (int e = 0; e < kPerThread; ++e) ag[e] += wt * load_coherent(os + e);
+    for (int u = 0; u < kOBatch; ++u) {
+      const bool ok = sp0 + u < nsplit;
+      const float* rs = urec + (int64_t)(ok ? sp0 + u : 0) * RB::kRec;
+      mv[u] = ok ? load_coherent(rs + 3 * r) : -INFINITY;
+      lv[u] = ok ? load_coherent(rs + 3 * r + 1) : 0.f;
+      lxv[u] = ok ? load_coherent(rs + 3 * r + 2) : 0.f;
+#pragma unroll
+      for (int e = 0; e < kPerThread; ++e) ov[u][e] = ok ? load_coherent(rs + 3 * RB::kRows + r * kD + d0 + e) : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kOBatch; ++u) {
+      const float wt = exp2f(mv[u] - Mgu);
+      Lg += wt * lv[u];
+      Lxg += wt * lxv[u];
+#pragma unroll
+      for (int e = 0; e < kPerThread; ++e) ag[e] += wt * ov[u][e];
+    }
   }
   write_final(Mg, Lg, Lxg, ag);
 }
@@ -404,8 +550,9 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
   int64_t kps = round_up((work + kTargetBlocks - 1) / kTargetBlocks, kStep);
   if (kps < kStep) kps = kStep;
   int64_t kg = kps < round_up(ld_idx > 0 ? ld_idx : 1, kStep) ? kps : round_up(ld_idx > 0 ? ld_idx : 1, kStep);
-  if (kg > kMaxGatherSplit) kg = kMaxGatherSplit;
+  if (kg > kMaxSplitKeys) kg = kMaxSplitKeys;
   int64_t kf = kps < round_up(max_L > 0 ? max_L : 1, kStep) ? kps : round_up(max_L > 0 ? max_L : 1, kStep);
+  if (kf > kMaxSplitKeys) kf = kMaxSplitKeys;
   pl.kps_g = (int)kg;
   pl.kps_f = (int)kf;
   pl.nsplit_g = ld_idx > 0 ? (int)((ld_idx + kg - 1) / kg) : 1;

@@ -69,6 +69,17 @@ bd_status launched(hipError_t e) {
   return BD_OK;
 }
 
+// Largest element offset of the K/V layout plus one row; the attention kernel
+// keeps row offsets as int32 in 16-byte units.
+int64_t kv_extent(const bd_kv_desc* kv) {
+  if (kv->page_table)
+    return (int64_t)(kv->num_pages - 1) * kv->stride_page + (int64_t)(kv->num_kv_heads - 1) * kv->stride_head +
+           (int64_t)(kv->page_size - 1) * kv->stride_tok + BD_HEAD_DIM;
+  const int64_t L = kv->max_seq_len > 0 ? kv->max_seq_len : 1;
+  return (int64_t)(kv->num_seqs - 1) * kv->stride_seq + (int64_t)(kv->num_kv_heads - 1) * kv->stride_head +
+         (L - 1) * kv->stride_tok + BD_HEAD_DIM;
+}
+
 // Common launch of the attention kernel.
 bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t nq, int32_t num_views,
                    const int32_t* idx, int32_t ld_idx, const int32_t* nsel, float scale, uint16_t* out_views,
@@ -78,6 +89,8 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
       bd::plan_attn(kv->num_seqs, kv->num_kv_heads, Hq, nq, num_views, ld_idx, kv->max_seq_len, out_full != nullptr);
   if (pl.nblk < 0 || (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f > INT32_MAX)
     return fail(BD_ERR_UNSUPPORTED, "problem too large for one launch");
+  if (kv_extent(kv) > ((int64_t)1 << 34))
+    return fail(BD_ERR_UNSUPPORTED, "K/V layout spans more than 2^34 elements");
   if ((int64_t)pl.units_g + pl.units_f > BD_WS_COUNTER_BYTES / 4)
     return fail(BD_ERR_UNSUPPORTED, "more than %d work units", BD_WS_COUNTER_BYTES / 4);
   bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
@@ -107,6 +120,7 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
   p.units_g = pl.units_g;
   p.nblk_g = pl.units_g * pl.nsplit_g;
   p.scale_log2 = scale * 1.4426950408889634f;
+  p.max_roff = (uint32_t)((kv_extent(kv) - BD_HEAD_DIM) >> 3);
   p.counters = static_cast<uint32_t*>(ws);
   p.part = pl.record_bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + pl.counter_bytes) : nullptr;
   return launched(bd::launch_attn(p, pl.nt, kv->page_table != nullptr, pl.nblk, stream));
@@ -266,7 +280,8 @@ bd_status bd_accept_len(const float* logits, int64_t row_stride, const int32_t* 
   if (gamma > 0 && !draft) return fail(BD_ERR_INVALID_ARG, "draft is NULL");
   if (row_stride < vocab) return fail(BD_ERR_INVALID_ARG, "row_stride %lld < vocab %d", (long long)row_stride, vocab);
   if ((int64_t)num_seqs * (gamma + 1) * 1024 > INT32_MAX) return fail(BD_ERR_UNSUPPORTED, "too many rows");
-  if (num_seqs > BD_WS_COUNTER_BYTES / 4) return fail(BD_ERR_UNSUPPORTED, "more than %d sequences", BD_WS_COUNTER_BYTES / 4);
+  if ((int64_t)num_seqs * (gamma + 2) > BD_WS_COUNTER_BYTES / 4)
+    return fail(BD_ERR_UNSUPPORTED, "more than %d sequence and row counters", BD_WS_COUNTER_BYTES / 4);
   const bd::AcceptPlan pl = bd::plan_accept(num_seqs, gamma, vocab);
   bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
   if (st != BD_OK) return st;
@@ -285,6 +300,7 @@ bd_status bd_accept_len(const float* logits, int64_t row_stride, const int32_t* 
   p.argmax_out = argmax_out;
   p.counters = static_cast<uint32_t*>(ws);
   p.part = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + pl.counter_bytes);
+  p.rowbest = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + pl.counter_bytes + pl.part_bytes);
   return launched(bd::launch_accept(p, stream));
 }
 

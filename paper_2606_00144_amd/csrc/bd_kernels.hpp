@@ -9,8 +9,8 @@
 
 namespace bd {
 
-// Largest number of gathered entries one attention workgroup handles.
-constexpr int kMaxGatherSplit = 1024;
+// Largest number of keys (gathered entries or cache rows) one attention workgroup handles.
+constexpr int kMaxSplitKeys = 2048;
 
 // ---- attention (decode / verify / multiview) -------------------------------
 struct AttnParams {
@@ -32,6 +32,7 @@ struct AttnParams {
   int32_t units_g;          // gathered units (their blocks come first)
   int32_t nblk_g;           // blocks of gathered units
   float scale_log2;         // softmax scale * log2(e)
+  uint32_t max_roff;        // largest valid row offset of the K/V layout, 16-byte units
   float* part;              // partial records
   uint32_t* counters;       // one per unit
 };
@@ -58,13 +59,14 @@ struct AcceptParams {
   int32_t* accept_out;
   int32_t* bonus_out;
   int32_t* argmax_out;
-  uint64_t* part;           // [S][gamma+1][nsplit]
-  uint32_t* counters;       // [S]
+  uint64_t* part;           // [S][gamma+1][nsplit] chunk results
+  uint64_t* rowbest;        // [S][gamma+1] merged row results
+  uint32_t* counters;       // [S] sequence counters, then [S][gamma+1] row counters
 };
 
 struct AcceptPlan {
   int nsplit, chunk;
-  size_t counter_bytes, ws_bytes;
+  size_t counter_bytes, part_bytes, ws_bytes;
 };
 
 AcceptPlan plan_accept(int S, int gamma, int vocab);
