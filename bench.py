@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--budget", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only copy 512 MiB device-to-device five times (counter calibration: known bytes)")
     return ap.parse_args()
 
 
@@ -106,6 +108,14 @@ def main():
 
     torch.cuda.init()
     dev = torch.device("cuda:0")
+    if args.copy_probe:
+        x = torch.ones((128 * 1024 * 1024,), dtype=torch.float32, device=dev)   # 512 MiB
+        y = torch.empty_like(x)
+        for _ in range(5):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": x.numel() * 4, "copies": 5}), flush=True)
+        return
     cfg = synth.CONFIGS[2]
     S, Hq, Hkv, L, W, gamma, V = (cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.window,
                                   cfg.gamma, cfg.vocab)
