@@ -26,6 +26,9 @@ FLAGS = [
     "-Wall", "-Wno-unused-function",
     # keep the compiler from forming packed-fp32 VALU instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in ordinary VGPRs: the kernels fit in 256 of them, and accumulators in
+    # AGPRs make the compiler copy them to VGPRs around every conditional rescale
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 

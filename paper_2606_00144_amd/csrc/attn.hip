@@ -47,7 +47,8 @@ constexpr float kSlack = 8.f;                  // lazy-rescale headroom, log2 un
 template <int NT>
 struct RowBlock {
   static constexpr int kRows = 16 * NT;
-  static constexpr int kRec = kRows * (3 + kD);   // floats of one partial record: m, l, lx, o[128]
+  // floats of one partial record: per row (m, l, lx, unused), then the unnormalised outputs
+  static constexpr int kRec = kRows * (4 + kD);
 };
 
 // Key slots of one split: row offset (16-byte units) and position of every
@@ -82,6 +83,7 @@ struct AttnSmem {
       float lx[kWaves][16 * NT];
     } merge;
   } u;
+  int32_t first_dirty[kWaves];   // per wave: first tile of its table chunks that needs the mask
   int32_t last;
 };
 
@@ -196,15 +198,19 @@ __device__ inline bf16x8 vt_operand(const u32x4 (&v)[8], int dt) {
 template <int NT>
 struct RowState {
   f32x4 o[NT][8];     // O^T[d-tile][row tile]
+  f32x4 l[NT];        // row sums of the bf16-rounded weights the PV product uses (normaliser), accumulated
+                      // by an MFMA against an all-ones operand: every register holds the row's total
   float m[NT];        // running max (log2 domain), shared by the 4 lane groups
-  float l[NT];        // running sum of the bf16-rounded weights the PV product uses (normaliser)
-  float lx[NT];       // running sum of the unrounded weights (log-sum-exp); both this lane's keys only
+  float lx[NT];       // this lane's keys' sum of the unrounded weights (log-sum-exp only)
 };
 
+// One 32-key tile of one wave.  `dirty` (wave-uniform) asks for the visibility mask: only tiles
+// at the causal edge, at the ragged end of a split or holding absent entries need it.  `want_lx`
+// (uniform) keeps the exact weight sum the log-sum-exp output is computed from.
 template <int NT, bool PAGED>
 __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T, const bf16x8 (&qop)[NT][4],
-                                 const int (&rowpos)[NT], float scale_log2) {
-  // scores S^T for 32 keys x 16*NT rows
+                                 const int (&rowpos)[NT], float scale_log2, bool dirty, bool want_lx) {
+  // scores S^T for 32 keys x 16*NT rows (unscaled)
   f32x4 sacc[2][NT];
 #pragma unroll
   for (int sub = 0; sub < 2; ++sub)
@@ -217,44 +223,63 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
       sacc[sub][nt] = a;
     }
 
+  if (dirty) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int tpos = (int)T.tp[i >> 2][i & 3];
+        if (!(tpos >= 0 && tpos <= rowpos[nt])) sacc[i >> 2][nt][i & 3] = -INFINITY;
+      }
+  }
+
   // online softmax with a lazily raised reference max: the accumulators are rescaled only when a
   // tile's max exceeds the reference by more than kSlack (log2 units), so weights stay <= 2^kSlack
-  // and the common tile costs no rescale at all
-  bf16x8 pop[NT];
+  // and the common tile costs no rescale.  The rescale branch is taken by the whole wave when any
+  // row needs it (rows that do not get factor 1), so it stays a scalar branch.
+  float mx[NT];
+  bool raise = false;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    float sv[8];
-    float mx = -INFINITY;
+    float v = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int tpos = (int)T.tp[i >> 2][i & 3];
-      const bool vis = tpos >= 0 && tpos <= rowpos[nt];
-      sv[i] = vis ? sacc[i >> 2][nt][i & 3] * scale_log2 : -INFINITY;
-      mx = fmaxf(mx, sv[i]);
-    }
-    mx = max_xor32(max_xor16(mx));
-    if (mx > st.m[nt] + kSlack) {
-      const float alpha = __builtin_amdgcn_exp2f(st.m[nt] - mx);   // 0 on the first visible tile
+    for (int i = 0; i < 8; ++i) v = fmaxf(v, sacc[i >> 2][nt][i & 3]);
+    mx[nt] = max_xor32(max_xor16(v)) * scale_log2;    // scale > 0: the max commutes with it
+    raise |= mx[nt] > st.m[nt] + kSlack;
+  }
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const bool up = mx[nt] > st.m[nt] + kSlack;
+      const float alpha = up ? __builtin_amdgcn_exp2f(st.m[nt] - mx[nt]) : 1.f;   // 0 on the first visible tile
+      st.m[nt] = up ? mx[nt] : st.m[nt];
       st.l[nt] *= alpha;
       st.lx[nt] *= alpha;
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] *= alpha;
-      st.m[nt] = mx;
     }
+  }
+
+  const bf16x8 ones = as_bf16x8(u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
+  bf16x8 pop[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
     const float muse = st.m[nt] == -INFINITY ? 0.f : st.m[nt];
-    float psum = 0.f, pxsum = 0.f;
+    float pv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) pv[i] = __builtin_amdgcn_exp2f(fmaf(sacc[i >> 2][nt][i & 3], scale_log2, -muse));
     u32x4 pw;
 #pragma unroll
-    for (int i = 0; i < 8; i += 2) {
-      const float p0 = __builtin_amdgcn_exp2f(sv[i] - muse), p1 = __builtin_amdgcn_exp2f(sv[i + 1] - muse);
-      const uint32_t w = pack_bf16x2(p0, p1);
-      pxsum += p0 + p1;
-      psum += bf16_lo(w) + bf16_hi(w);   // the normaliser sums the rounded weights the PV product sees
-      pw[i >> 1] = w;
-    }
+    for (int i = 0; i < 4; ++i) pw[i] = pack_bf16x2(pv[2 * i], pv[2 * i + 1]);
     pop[nt] = as_bf16x8(pw);
-    st.l[nt] += psum;
-    st.lx[nt] += pxsum;
+    if (want_lx) {
+      float sx = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) sx += pv[i];
+      st.lx[nt] += sx;
+    }
+    // the normaliser sums exactly the rounded weights the PV product sees
+    st.l[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pop[nt], st.l[nt], 0, 0, 0);
   }
 
 #pragma unroll
@@ -270,7 +295,8 @@ template <int NT, bool PAGED>
 __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   using RB = RowBlock<NT>;
   __shared__ AttnSmem<NT> sm;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: LDS slot addresses stay scalar
   const int lg = lane >> 4, lr = lane & 15;
 
   // ---- which (kind, unit, split) this workgroup owns
@@ -322,9 +348,14 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
       for (int k = 0; k < kPer; ++k)
         pg[k] = tv[k] >= 0 ? p.kv.page_table[(int64_t)s * p.kv.max_pages_per_seq + tv[k] / p.kv.page_size] : 0;
     }
+    // a tile needs the visibility mask when one of its slots is absent or lies after the
+    // earliest row position of this row block; the first such tile bounds the mask-free ones
+    const int minpos = L - p.nq + (rb * RB::kRows) / p.G;
+    int first_dirty = 0x7FFFFFFF;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
       const int i = tid + k * kThreads;
+      bool bad = false;
       if (i < nslots) {
         int t = tv[k];
         int64_t o;
@@ -339,10 +370,23 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
         if (t < 0 || o < 0) { t = -1; o = 0; }
         sm.u.slots.roff[i] = (int)(o >> 3);
         sm.u.slots.tpos[i] = t;
+        bad = i < ntiles * kTile && (t < 0 || t > minpos);
+      }
+      // chunk k of this wave is slots k*kThreads + 64*wave .. +63: two tiles, the low 32 ballot bits the first
+      const uint64_t mask = __builtin_amdgcn_ballot_w64(bad);
+      if (mask != 0) {
+        const int tile = (k * kThreads + kWave * wave) / kTile + ((uint32_t)mask == 0u ? 1 : 0);
+        first_dirty = tile < first_dirty ? tile : first_dirty;
       }
     }
+    if (lane == 0) sm.first_dirty[wave] = first_dirty;
   }
   __syncthreads();
+  int first_dirty = sm.first_dirty[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) first_dirty = sm.first_dirty[w] < first_dirty ? sm.first_dirty[w] : first_dirty;
+  first_dirty = __builtin_amdgcn_readfirstlane(first_dirty);
+  const bool want_lx = (gather ? p.lse_g : p.lse_f) != nullptr;
 
   // ---- query rows of this lane: row n = rb*RB + 16*nt + lane%16
   bf16x8 qop[NT][4];
@@ -363,7 +407,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     st.m[nt] = -INFINITY;
-    st.l[nt] = 0.f;
+    st.l[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     st.lx[nt] = 0.f;
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -387,13 +431,13 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
       asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
       read_tile_and_rows<NT, PAGED>(T, A, slot_a_lds, tpos_lds, kTile * it, roff_lds, kTile * (it + 2 * kWaves), lane);
       dma_tile(p.kv, A, p.max_roff, slot_a, lane);
-      tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2);
+      tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it >= first_dirty, want_lx);
       if (it + kWaves >= ntiles) break;
       asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
       read_tile_and_rows<NT, PAGED>(T, A, slot_b_lds, tpos_lds, kTile * (it + kWaves), roff_lds,
                                     kTile * (it + 3 * kWaves), lane);
       dma_tile(p.kv, A, p.max_roff, slot_b, lane);
-      tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2);
+      tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it + kWaves >= first_dirty, want_lx);
       if (it + 2 * kWaves >= ntiles) break;
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the LDS is reused
@@ -403,9 +447,8 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   // ---- wave state -> LDS: row r = 16*nt + lane%16; lane group lg holds d in [32lg, 32lg+32)
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    float l = st.l[nt], lx = st.lx[nt];
-    l += shfl_xor_f(l, 16);
-    l += shfl_xor_f(l, 32);
+    const float l = st.l[nt][0];
+    float lx = st.lx[nt];
     lx += shfl_xor_f(lx, 16);
     lx += shfl_xor_f(lx, 32);
     const int r = 16 * nt + lr;
@@ -470,19 +513,23 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
     return;
   }
 
-  // ---- publish this split's partial record (rows that exist only); the last split merges them
-  float* rec_base = p.part + (gather ? 0 : (int64_t)p.units_g * p.nsplit_g * RB::kRec);
+  // ---- publish this split's partial record (rows that exist only); the last split merges them.
+  // Record layout: row stats as one float4 per row, then the outputs thread-major (4-float chunk c
+  // of thread t at chunk index c*kThreads + t), so each store instruction of a wave writes 1 KiB
+  // contiguously; the merging workgroup reads with the same thread mapping.
+  const float* rec_base = p.part + (gather ? 0 : (int64_t)p.units_g * p.nsplit_g * RB::kRec);
   const int unit_local = gather ? unit : unit - p.units_g;
-  float* rec = rec_base + ((int64_t)unit_local * nsplit + split) * RB::kRec;
+  const __amdgpu_buffer_rsrc_t urec =
+      make_rsrc(rec_base + (int64_t)unit_local * nsplit * RB::kRec, (uint32_t)(nsplit * RB::kRec * 4));
+  constexpr int kChunks = kPerThread / 4;
+  constexpr uint32_t kOutOff = 16 * RB::kRows;
   if (row_valid) {
-    if (d0 == 0) {
-      store_coherent(rec + 3 * r, M);
-      store_coherent(rec + 3 * r + 1, Lsum);
-      store_coherent(rec + 3 * r + 2, Lx);
-    }
-    float* ro = rec + 3 * RB::kRows + r * kD + d0;
+    const uint32_t rec = (uint32_t)split * RB::kRec * 4;
+    if (d0 == 0) store16_coherent(urec, rec + 16 * r, f32x4{M, Lsum, Lx, 0.f});
 #pragma unroll
-    for (int e = 0; e < kPerThread; ++e) store_coherent(ro + e, acc[e]);
+    for (int c = 0; c < kChunks; ++c)
+      store16_coherent(urec, rec + kOutOff + 16 * (c * kThreads + tid),
+                       f32x4{acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]});
   }
   wait_vmem();
   __syncthreads();
@@ -492,43 +539,43 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   if (tid == 0) reset_counter(&p.counters[unit]);   // ready for the next call
   if (!row_valid) return;
 
-  // merge the splits in split order; every batch of loads is issued before any result is used
-  const float* urec = rec_base + (int64_t)unit_local * nsplit * RB::kRec;
+  // merge the splits in split order with an online rescale, a batch of records at a time; every
+  // load of a batch is issued before any of its results is used
   constexpr int kBatch = 8;
-  float Mg = -INFINITY;
-  for (int sp0 = 0; sp0 < nsplit; sp0 += kBatch) {
-    float mv[kBatch];
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u)
-      mv[u] = sp0 + u < nsplit ? load_coherent(urec + (int64_t)(sp0 + u) * RB::kRec + 3 * r) : -INFINITY;
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) Mg = fmaxf(Mg, mv[u]);
-  }
-  const float Mgu = Mg == -INFINITY ? 0.f : Mg;
-  float Lg = 0.f, Lxg = 0.f, ag[kPerThread];
+  float Mg = -INFINITY, Lg = 0.f, Lxg = 0.f, ag[kPerThread];
 #pragma unroll
   for (int e = 0; e < kPerThread; ++e) ag[e] = 0.f;
-  constexpr int kOBatch = 4;
-  for (int sp0 = 0; sp0 < nsplit; sp0 += kOBatch) {
-    float mv[kOBatch], lv[kOBatch], lxv[kOBatch], ov[kOBatch][kPerThread];
+  for (int sp0 = 0; sp0 < nsplit; sp0 += kBatch) {
+    f32x4 sv[kBatch], ov[kBatch][kChunks];
 #pragma unroll
-    for (int u = 0; u < kOBatch; ++u) {
+    for (int u = 0; u < kBatch; ++u) {
+      const uint32_t rec = (uint32_t)(sp0 + u) * RB::kRec * 4;
       const bool ok = sp0 + u < nsplit;
-      const float* rs = urec + (int64_t)(ok ? sp0 + u : 0) * RB::kRec;
-      mv[u] = ok ? load_coherent(rs + 3 * r) : -INFINITY;
-      lv[u] = ok ? load_coherent(rs + 3 * r + 1) : 0.f;
-      lxv[u] = ok ? load_coherent(rs + 3 * r + 2) : 0.f;
+      sv[u] = ok ? load16_coherent(urec, rec + 16 * r) : f32x4{-INFINITY, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int e = 0; e < kPerThread; ++e) ov[u][e] = ok ? load_coherent(rs + 3 * RB::kRows + r * kD + d0 + e) : 0.f;
+      for (int c = 0; c < kChunks; ++c)
+        ov[u][c] = ok ? load16_coherent(urec, rec + kOutOff + 16 * (c * kThreads + tid)) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
+    float mb = Mg;
 #pragma unroll
-    for (int u = 0; u < kOBatch; ++u) {
-      const float wt = exp2f(mv[u] - Mgu);
-      Lg += wt * lv[u];
-      Lxg += wt * lxv[u];
+    for (int u = 0; u < kBatch; ++u) mb = fmaxf(mb, sv[u][0]);
+    const float mbu = mb == -INFINITY ? 0.f : mb;
+    const float sc = exp2f(Mg - mbu);
+    Lg *= sc;
+    Lxg *= sc;
 #pragma unroll
-      for (int e = 0; e < kPerThread; ++e) ag[e] += wt * ov[u][e];
+    for (int e = 0; e < kPerThread; ++e) ag[e] *= sc;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const float wt = exp2f(sv[u][0] - mbu);
+      Lg += wt * sv[u][1];
+      Lxg += wt * sv[u][2];
+#pragma unroll
+      for (int c = 0; c < kChunks; ++c)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ag[4 * c + i] += wt * ov[u][c][i];
     }
+    Mg = mb;
   }
   write_final(Mg, Lg, Lxg, ag);
 }

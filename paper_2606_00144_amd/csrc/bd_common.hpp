@@ -135,6 +135,18 @@ __device__ inline float load_coherent(const float* p) {
 __device__ inline uint64_t load_coherent(const uint64_t* p) {
   return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// 16-byte coherent accesses (buffer_store/load_dwordx4 with the sc1 policy) through a buffer
+// resource over [base, base + bytes); accesses outside the range are dropped (stores) or read 0.
+constexpr int kPolicySc1 = 16;
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ inline void store16_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)off, 0, kPolicySc1);
+}
+__device__ inline f32x4 load16_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kPolicySc1));
+}
 // Wait until every vector memory operation of this wave has completed.
 __device__ inline void wait_vmem() {
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0), expcnt/lgkmcnt unconstrained
