@@ -157,6 +157,34 @@ __device__ inline void read_tile_and_rows(TileRegs<NT, PAGED>& T, TileRows& A, u
       : "v"(at), "v"(ap), "v"(ak), "v"(av));
 }
 
+// Copy the landed tile in LDS slot `src` into registers (keys whose row offsets are computed).
+template <int NT, bool PAGED>
+__device__ inline void read_tile(TileRegs<NT, PAGED>& T, uint32_t src, int lane) {
+  const uint32_t at = src + 16 * lane;
+  asm volatile(
+      "ds_read_b128 %0, %16\n"
+      "ds_read_b128 %1, %16 offset:1024\n"
+      "ds_read_b128 %2, %16 offset:2048\n"
+      "ds_read_b128 %3, %16 offset:3072\n"
+      "ds_read_b128 %4, %16 offset:4096\n"
+      "ds_read_b128 %5, %16 offset:5120\n"
+      "ds_read_b128 %6, %16 offset:6144\n"
+      "ds_read_b128 %7, %16 offset:7168\n"
+      "ds_read_b128 %8, %16 offset:8192\n"
+      "ds_read_b128 %9, %16 offset:9216\n"
+      "ds_read_b128 %10, %16 offset:10240\n"
+      "ds_read_b128 %11, %16 offset:11264\n"
+      "ds_read_b128 %12, %16 offset:12288\n"
+      "ds_read_b128 %13, %16 offset:13312\n"
+      "ds_read_b128 %14, %16 offset:14336\n"
+      "ds_read_b128 %15, %16 offset:15360\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(T.k[0][0]), "=&v"(T.k[0][1]), "=&v"(T.k[0][2]), "=&v"(T.k[0][3]), "=&v"(T.k[1][0]),
+        "=&v"(T.k[1][1]), "=&v"(T.k[1][2]), "=&v"(T.k[1][3]), "=&v"(T.v[0]), "=&v"(T.v[1]), "=&v"(T.v[2]),
+        "=&v"(T.v[3]), "=&v"(T.v[4]), "=&v"(T.v[5]), "=&v"(T.v[6]), "=&v"(T.v[7])
+      : "v"(at));
+}
+
 __device__ inline void dma16(const uint16_t* g, uint8_t* l) {
   __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)l, 16, 0, 0);
 }
@@ -207,9 +235,10 @@ struct RowState {
 // One 32-key tile of one wave.  `dirty` (wave-uniform) asks for the visibility mask: only tiles
 // at the causal edge, at the ragged end of a split or holding absent entries need it.  `want_lx`
 // (uniform) keeps the exact weight sum the log-sum-exp output is computed from.
-template <int NT, bool PAGED>
+template <int NT, bool PAGED, class PosFn>
 __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T, const bf16x8 (&qop)[NT][4],
-                                 const int (&rowpos)[NT], float scale_log2, bool dirty, bool want_lx) {
+                                 const int (&rowpos)[NT], float scale_log2, bool dirty, bool want_lx,
+                                 PosFn pos_of) {
   // scores S^T for 32 keys x 16*NT rows (unscaled)
   f32x4 sacc[2][NT];
 #pragma unroll
@@ -228,7 +257,7 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const int tpos = (int)T.tp[i >> 2][i & 3];
+        const int tpos = pos_of(i);   // position of score slot i, -1 when absent
         if (!(tpos >= 0 && tpos <= rowpos[nt])) sacc[i >> 2][nt][i & 3] = -INFINITY;
       }
   }
@@ -331,7 +360,12 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
 
   const int ntiles = e_end > e_begin ? (e_end - e_begin + kTile - 1) / kTile : 0;
   const int nslots = (ntiles + kMaxAhead * kWaves) * kTile;     // <= kSlotCap: padding tiles included
-  {
+  // a tile needs the visibility mask when one of its slots is absent or lies after the earliest
+  // row position of this row block; the first such tile bounds the mask-free ones
+  const int minpos = L - p.nq + (rb * RB::kRows) / p.G;
+  // the causal prefix of a contiguous cache needs no slot table: row offsets are computed
+  const bool arith = !PAGED && !gather;
+  if (!arith) {
     // all idx and page-table loads are issued before any result is used
     constexpr int kPer = (kSlotCap + kThreads - 1) / kThreads;
     int tv[kPer];
@@ -348,9 +382,6 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
       for (int k = 0; k < kPer; ++k)
         pg[k] = tv[k] >= 0 ? p.kv.page_table[(int64_t)s * p.kv.max_pages_per_seq + tv[k] / p.kv.page_size] : 0;
     }
-    // a tile needs the visibility mask when one of its slots is absent or lies after the
-    // earliest row position of this row block; the first such tile bounds the mask-free ones
-    const int minpos = L - p.nq + (rb * RB::kRows) / p.G;
     int first_dirty = 0x7FFFFFFF;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
@@ -380,12 +411,21 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
       }
     }
     if (lane == 0) sm.first_dirty[wave] = first_dirty;
+    __syncthreads();
   }
-  __syncthreads();
-  int first_dirty = sm.first_dirty[0];
+  int first_dirty;
+  if (arith) {
+    // tile t is clean when its keys all lie inside the split and at or before minpos
+    const int c1 = minpos - e_begin - (kTile - 1);
+    const int fd1 = c1 < 0 ? 0 : c1 / kTile + 1;
+    const int fd2 = (e_end - e_begin) / kTile;
+    first_dirty = fd1 < fd2 ? fd1 : fd2;
+  } else {
+    first_dirty = sm.first_dirty[0];
 #pragma unroll
-  for (int w = 1; w < kWaves; ++w) first_dirty = sm.first_dirty[w] < first_dirty ? sm.first_dirty[w] : first_dirty;
-  first_dirty = __builtin_amdgcn_readfirstlane(first_dirty);
+    for (int w = 1; w < kWaves; ++w) first_dirty = sm.first_dirty[w] < first_dirty ? sm.first_dirty[w] : first_dirty;
+    first_dirty = __builtin_amdgcn_readfirstlane(first_dirty);
+  }
   const bool want_lx = (gather ? p.lse_g : p.lse_f) != nullptr;
 
   // ---- query rows of this lane: row n = rb*RB + 16*nt + lane%16
@@ -416,29 +456,75 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   // ---- stream this wave's tiles (tile w, w+4, ...) through its two LDS slots.  The waits are
   // explicit: the tile about to be read was issued kTileLoads loads before the newest ones.
   if (wave < ntiles) {
-    const uint32_t roff_lds = lds_addr(sm.u.slots.roff);
-    const uint32_t tpos_lds = lds_addr(sm.u.slots.tpos);
     uint8_t* slot_a = sm.u.slots.ring[wave][0];
     uint8_t* slot_b = sm.u.slots.ring[wave][1];
     const uint32_t slot_a_lds = lds_addr(slot_a), slot_b_lds = lds_addr(slot_b);
     TileRows A;
-    read_rows(A, roff_lds, kTile * wave, lane);
-    dma_tile(p.kv, A, p.max_roff, slot_a, lane);
-    read_rows(A, roff_lds, kTile * (wave + kWaves), lane);
-    dma_tile(p.kv, A, p.max_roff, slot_b, lane);
     TileRegs<NT, PAGED> T;
-    for (int it = wave;; it += 2 * kWaves) {
-      asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-      read_tile_and_rows<NT, PAGED>(T, A, slot_a_lds, tpos_lds, kTile * it, roff_lds, kTile * (it + 2 * kWaves), lane);
+    if (arith) {
+      // row offset (16-byte units) of key e_begin + slot: one scalar term per tile, lane-constant rest;
+      // keys past the split (padding, ragged end) stay in the allocation through the clamp in
+      // dma_tile and are masked by their positions
+      const uint32_t base16 = (uint32_t)(((int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head) >> 3);
+      const uint32_t tok16 = (uint32_t)(p.kv.stride_tok >> 3);
+      const uint32_t off_k0 = (uint32_t)lr * tok16, off_k1 = (uint32_t)(16 + lr) * tok16;
+      const uint32_t off_v = (uint32_t)(4 * lg) * tok16;
+      auto rows_at = [&](int slot0) {
+        const uint32_t r0 = base16 + (uint32_t)(e_begin + slot0) * tok16;
+        A.k[0] = r0 + off_k0;
+        A.k[1] = r0 + off_k1;
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) A.v[h][i] = r0 + (uint32_t)(16 * h + i) * tok16 + off_v;
+      };
+      auto pos_at = [&](int slot0) {
+        return [=](int i) {
+          const int e = e_begin + slot0 + 16 * (i >> 2) + 4 * lg + (i & 3);
+          return e < e_end ? e : -1;
+        };
+      };
+      rows_at(kTile * wave);
       dma_tile(p.kv, A, p.max_roff, slot_a, lane);
-      tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it >= first_dirty, want_lx);
-      if (it + kWaves >= ntiles) break;
-      asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-      read_tile_and_rows<NT, PAGED>(T, A, slot_b_lds, tpos_lds, kTile * (it + kWaves), roff_lds,
-                                    kTile * (it + 3 * kWaves), lane);
+      rows_at(kTile * (wave + kWaves));
       dma_tile(p.kv, A, p.max_roff, slot_b, lane);
-      tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it + kWaves >= first_dirty, want_lx);
-      if (it + 2 * kWaves >= ntiles) break;
+      for (int it = wave;; it += 2 * kWaves) {
+        asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+        read_tile<NT, PAGED>(T, slot_a_lds, lane);
+        rows_at(kTile * (it + 2 * kWaves));
+        dma_tile(p.kv, A, p.max_roff, slot_a, lane);
+        tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it >= first_dirty, want_lx, pos_at(kTile * it));
+        if (it + kWaves >= ntiles) break;
+        asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+        read_tile<NT, PAGED>(T, slot_b_lds, lane);
+        rows_at(kTile * (it + 3 * kWaves));
+        dma_tile(p.kv, A, p.max_roff, slot_b, lane);
+        tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it + kWaves >= first_dirty, want_lx,
+                             pos_at(kTile * (it + kWaves)));
+        if (it + 2 * kWaves >= ntiles) break;
+      }
+    } else {
+      const uint32_t roff_lds = lds_addr(sm.u.slots.roff);
+      const uint32_t tpos_lds = lds_addr(sm.u.slots.tpos);
+      auto pos_of = [&](int i) { return (int)T.tp[i >> 2][i & 3]; };
+      read_rows(A, roff_lds, kTile * wave, lane);
+      dma_tile(p.kv, A, p.max_roff, slot_a, lane);
+      read_rows(A, roff_lds, kTile * (wave + kWaves), lane);
+      dma_tile(p.kv, A, p.max_roff, slot_b, lane);
+      for (int it = wave;; it += 2 * kWaves) {
+        asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+        read_tile_and_rows<NT, PAGED>(T, A, slot_a_lds, tpos_lds, kTile * it, roff_lds, kTile * (it + 2 * kWaves),
+                                      lane);
+        dma_tile(p.kv, A, p.max_roff, slot_a, lane);
+        tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it >= first_dirty, want_lx, pos_of);
+        if (it + kWaves >= ntiles) break;
+        asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+        read_tile_and_rows<NT, PAGED>(T, A, slot_b_lds, tpos_lds, kTile * (it + kWaves), roff_lds,
+                                      kTile * (it + 3 * kWaves), lane);
+        dma_tile(p.kv, A, p.max_roff, slot_b, lane);
+        tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it + kWaves >= first_dirty, want_lx, pos_of);
+        if (it + 2 * kWaves >= ntiles) break;
+      }
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the LDS is reused
   }
@@ -582,7 +668,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
 
 }  // namespace
 
-AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full) {
+AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full, bool paged) {
   AttnPlan pl{};
   const int G = Hq / Hkv;
   pl.R = nq * G;
@@ -599,7 +685,9 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
   int64_t kg = kps < round_up(ld_idx > 0 ? ld_idx : 1, kStep) ? kps : round_up(ld_idx > 0 ? ld_idx : 1, kStep);
   if (kg > kMaxSplitKeys) kg = kMaxSplitKeys;
   int64_t kf = kps < round_up(max_L > 0 ? max_L : 1, kStep) ? kps : round_up(max_L > 0 ? max_L : 1, kStep);
-  if (kf > kMaxSplitKeys) kf = kMaxSplitKeys;
+  // the full branch over a contiguous cache computes its row offsets, so its splits are not bound
+  // by the slot table
+  if (paged && kf > kMaxSplitKeys) kf = kMaxSplitKeys;
   pl.kps_g = (int)kg;
   pl.kps_f = (int)kf;
   pl.nsplit_g = ld_idx > 0 ? (int)((ld_idx + kg - 1) / kg) : 1;

@@ -86,7 +86,8 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
                    float* lse_views, uint16_t* out_full, float* lse_full, void* ws, size_t ws_bytes,
                    hipStream_t stream) {
   const bd::AttnPlan pl =
-      bd::plan_attn(kv->num_seqs, kv->num_kv_heads, Hq, nq, num_views, ld_idx, kv->max_seq_len, out_full != nullptr);
+      bd::plan_attn(kv->num_seqs, kv->num_kv_heads, Hq, nq, num_views, ld_idx, kv->max_seq_len, out_full != nullptr,
+                    kv->page_table != nullptr);
   if (pl.nblk < 0 || (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f > INT32_MAX)
     return fail(BD_ERR_UNSUPPORTED, "problem too large for one launch");
   if (kv_extent(kv) > ((int64_t)1 << 34))
@@ -199,7 +200,7 @@ bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_
 size_t bd_sparse_decode_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
                                              int32_t ld_idx) {
   if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || ld_idx < 0) return 0;
-  return bd::plan_attn(num_seqs, num_kv_heads, num_q_heads, 1, 1, ld_idx, 0, false).ws_bytes;
+  return bd::plan_attn(num_seqs, num_kv_heads, num_q_heads, 1, 1, ld_idx, 0, false, true).ws_bytes;
 }
 
 bd_status bd_sparse_decode_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, const int32_t* idx,
@@ -223,7 +224,8 @@ size_t bd_multiview_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads,
   if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || block_len < 1 || num_views < 0 || ld_idx < 0 ||
       max_seq_len < 0)
     return 0;
-  return bd::plan_attn(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld_idx, max_seq_len, with_full != 0)
+  return bd::plan_attn(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld_idx, max_seq_len, with_full != 0,
+                       true)
       .ws_bytes;
 }
 
@@ -250,7 +252,7 @@ bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t
 size_t bd_verify_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads, int32_t gamma,
                                       int32_t max_seq_len) {
   if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || gamma < 0 || max_seq_len < 0) return 0;
-  return bd::plan_attn(num_seqs, num_kv_heads, num_q_heads, gamma + 1, 0, 0, max_seq_len, true).ws_bytes;
+  return bd::plan_attn(num_seqs, num_kv_heads, num_q_heads, gamma + 1, 0, 0, max_seq_len, true, true).ws_bytes;
 }
 
 bd_status bd_verify_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, int32_t gamma, float scale,

@@ -9,7 +9,8 @@
 
 namespace bd {
 
-// Largest number of keys (gathered entries or cache rows) one attention workgroup handles.
+// Largest number of keys one attention workgroup takes through its slot table (gathered
+// entries, or cache rows of a paged cache).
 constexpr int kMaxSplitKeys = 2048;
 
 // ---- attention (decode / verify / multiview) -------------------------------
@@ -44,7 +45,10 @@ struct AttnPlan {
   size_t counter_bytes, record_bytes, ws_bytes;
 };
 
-AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full);
+// `paged`: the cache is paged (the full branch then also goes through the slot table, which
+// bounds its splits).  The plan of a paged cache has at least as many splits as that of a
+// contiguous one, so workspace queries that do not know the layout use paged = true.
+AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full, bool paged);
 hipError_t launch_attn(const AttnParams& p, int nt, bool paged, int nblocks, hipStream_t stream);
 size_t attn_record_floats(int nt);
 
