@@ -59,9 +59,13 @@ extern "C" {
 #define BD_HEAD_DIM 128
 /* Longest candidate prefix L_s - W that bd_select_kv ranks in one pass. */
 #define BD_SELECT_MAX_PREFIX 32768
-/* Leading workspace bytes reserved for completion counters (one uint32 per
- * work unit; a call with more than BD_WS_COUNTER_BYTES/4 units is unsupported). */
-#define BD_WS_COUNTER_BYTES 262144
+/* Leading workspace bytes reserved for completion counters and other state that
+ * every completed call returns to zero: one BD_WS_COUNTER_STRIDE-byte line per
+ * counter, so that counters of different work units never share a cache line.
+ * A call needing more than BD_WS_COUNTER_LINES lines is unsupported. */
+#define BD_WS_COUNTER_BYTES 1048576
+#define BD_WS_COUNTER_STRIDE 128
+#define BD_WS_COUNTER_LINES (BD_WS_COUNTER_BYTES / BD_WS_COUNTER_STRIDE)
 
 typedef int32_t bd_status;
 #define BD_OK 0

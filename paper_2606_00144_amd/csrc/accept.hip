@@ -1,11 +1,13 @@
 // Greedy acceptance over verifier logits (Eq. 3; Alg. 2 accept and bonus token).
 //
 // Every (sequence, row, vocab chunk) workgroup scans its chunk once with
-// 16-byte loads and reduces (order key of the value, index) to the maximum,
-// lower index winning ties: the packed key (order(value) << 32) | ~index is
-// maximal exactly there.  The last workgroup of a sequence to finish (atomic
-// counter) merges the chunk results of all gamma+1 rows and counts the
-// leading drafts that equal the verifier's greedy tokens.
+// 16-byte loads.  A thread keeps the first maximum of its own elements (it
+// visits them in increasing index order, so a strict compare keeps the lowest
+// index); the workgroup then reduces packed keys (order(value) << 32) | ~index,
+// which are maximal exactly at the lowest-index maximum, and max-combines its
+// key into the row's slot with a device-scope atomic.  The last chunk of a row
+// to finish counts the row done; the last row of a sequence reads its row
+// maxima and counts the leading drafts that equal the verifier's greedy tokens.
 
 #include "bd_common.hpp"
 #include "bd_kernels.hpp"
@@ -20,6 +22,7 @@ constexpr int kUnroll = 8;          // float4 loads in flight per thread
 __device__ inline uint64_t pack_key(float v, int idx) {
   return ((uint64_t)float_order_key(v) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)idx);
 }
+__device__ inline int key_index(uint64_t k) { return (int)(0xFFFFFFFFu - (uint32_t)k); }
 
 __device__ inline uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
 
@@ -36,19 +39,26 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptParams p) {
   __shared__ int32_t last;
   const int tid = threadIdx.x;
   const int rows = p.gamma + 1;
+  const int nrows = p.S * rows;
   const int b = xcd_remap(blockIdx.x, gridDim.x);
   const int split = b % p.nsplit;
   const int rs = b / p.nsplit;              // s * rows + i
   const int s = rs / rows;
+  uint32_t* seq_counter = counter_line(p.counters, s);
+  uint32_t* row_counter = counter_line(p.counters, p.S + rs);
+  auto row_slot = [&](int r) { return reinterpret_cast<uint64_t*>(counter_line(p.counters, p.S + nrows + r)); };
 
   const float* row = p.logits + (int64_t)rs * p.row_stride;
   const int c0 = split * p.chunk;
   int c1 = c0 + p.chunk;
   if (c1 > p.vocab) c1 = p.vocab;
 
-  uint64_t best = 0;
+  // first maximum of this thread's elements (all finite by contract; a thread whose elements are
+  // all -inf reports its first one)
+  float bv = -INFINITY;
+  int bi = -1, first = -1;
   if (p.vec4) {
-    // each thread's float4 loads of the chunk are all issued before any is reduced
+    // each thread's float4 loads of a round are all issued before any is reduced
     for (int base = c0 + 4 * tid; base < c1; base += 4 * kThreads * kUnroll) {
       f32x4 x[kUnroll];
 #pragma unroll
@@ -56,77 +66,71 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptParams p) {
         const int c = base + u * 4 * kThreads;
         x[u] = c + 4 <= c1 ? *reinterpret_cast<const f32x4*>(row + c) : f32x4{0.f, 0.f, 0.f, 0.f};
       }
+      if (first < 0) first = base;
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         const int c = base + u * 4 * kThreads;
         if (c + 4 <= c1) {
-          best = umax64(best, pack_key(x[u][0], c));
-          best = umax64(best, pack_key(x[u][1], c + 1));
-          best = umax64(best, pack_key(x[u][2], c + 2));
-          best = umax64(best, pack_key(x[u][3], c + 3));
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bool gt = x[u][e] > bv;
+            bv = gt ? x[u][e] : bv;
+            bi = gt ? c + e : bi;
+          }
         } else {
-          for (int e = c; e < c1; ++e) best = umax64(best, pack_key(row[e], e));
+          for (int e = c; e < c1; ++e) {
+            const float v = row[e];
+            if (v > bv) { bv = v; bi = e; }
+          }
         }
       }
     }
   } else {
-    for (int c = c0 + tid; c < c1; c += kThreads) best = umax64(best, pack_key(row[c], c));
+    for (int c = c0 + tid; c < c1; c += kThreads) {
+      if (first < 0) first = c;
+      const float v = row[c];
+      if (v > bv) { bv = v; bi = c; }
+    }
   }
+  uint64_t best = bi >= 0 ? pack_key(bv, bi) : (first >= 0 ? pack_key(-INFINITY, first) : 0ull);
 #pragma unroll
   for (int m = 1; m < kWave; m <<= 1) best = umax64(best, shfl_xor_u64(best, m));
   if ((tid & 63) == 0) red[tid >> 6] = best;
   __syncthreads();
 
-  // Two-level completion: the last chunk of a row merges that row (nsplit arrivals on the row's
-  // counter), the last row of a sequence counts the accepted prefix (gamma+1 arrivals on the
-  // sequence's counter).  Few arrivals per counter keep the atomics from serialising.
-  __shared__ int32_t last_seq;
-  if (p.nsplit > 1) {
-    if (tid == 0) {
-      uint64_t bb = red[0];
-      for (int w = 1; w < kThreads / kWave; ++w) bb = umax64(bb, red[w]);
-      store_coherent(p.part + (int64_t)rs * p.nsplit + split, bb);
-      wait_vmem();
-      last = arrive(&p.counters[p.S + rs], (uint32_t)p.nsplit);
-    }
-    __syncthreads();
-    if (!last) return;
-    if (tid < kWave) {   // one wave merges the row's chunks, 64 loads in flight per pass
-      uint64_t bb = 0;
-      const uint64_t* pr = p.part + (int64_t)rs * p.nsplit;
-      for (int sp = tid; sp < p.nsplit; sp += kWave) bb = umax64(bb, load_coherent(pr + sp));
-#pragma unroll
-      for (int m = 1; m < kWave; m <<= 1) bb = umax64(bb, shfl_xor_u64(bb, m));
-      if (tid == 0) {
-        reset_counter(&p.counters[p.S + rs]);
-        red[0] = bb;
-      }
-    }
-    __syncthreads();
-  } else if (tid == 0) {
+  // Two-level completion keeps the arrivals per counter few: nsplit chunks per row counter,
+  // gamma+1 rows per sequence counter.
+  if (tid == 0) {
     uint64_t bb = red[0];
     for (int w = 1; w < kThreads / kWave; ++w) bb = umax64(bb, red[w]);
-    red[0] = bb;
-  }
-  // red[0] is the merged key of row rs; publish it and let the sequence's last row finish
-  if (tid == 0) {
-    store_coherent(p.rowbest + rs, red[0]);
-    wait_vmem();
-    last_seq = rows == 1 ? 1 : arrive(&p.counters[s], (uint32_t)rows);
+    bool row_done = true;
+    if (p.nsplit > 1) {
+      atomic_max_coherent(row_slot(rs), bb);
+      wait_vmem();
+      row_done = arrive(row_counter, (uint32_t)p.nsplit);
+      if (row_done) reset_counter(row_counter);
+    } else {
+      store_coherent(row_slot(rs), bb);
+      wait_vmem();
+    }
+    last = row_done && (rows == 1 || arrive(seq_counter, (uint32_t)rows));
   }
   __syncthreads();
-  if (!last_seq) return;
-  if (tid < rows) rowbest[tid] = load_coherent(p.rowbest + (int64_t)s * rows + tid);
+  if (!last) return;
+  if (tid < rows) {
+    uint64_t* slot = row_slot(s * rows + tid);
+    rowbest[tid] = load_coherent(slot);
+    store_coherent(slot, 0ull);   // the slots start from zero in the next call
+  }
   __syncthreads();
   if (tid == 0) {
     int k = 0;
-    while (k < p.gamma && p.draft[(int64_t)s * p.gamma + k] == (int32_t)(0xFFFFFFFFu - (uint32_t)rowbest[k])) ++k;
+    while (k < p.gamma && p.draft[(int64_t)s * p.gamma + k] == key_index(rowbest[k])) ++k;
     p.accept_out[s] = k;
-    if (p.bonus_out) p.bonus_out[s] = (int32_t)(0xFFFFFFFFu - (uint32_t)rowbest[k]);
-    if (rows > 1) reset_counter(&p.counters[s]);
+    if (p.bonus_out) p.bonus_out[s] = key_index(rowbest[k]);
+    if (rows > 1) reset_counter(seq_counter);
   }
-  if (p.argmax_out && tid < rows)
-    p.argmax_out[(int64_t)s * rows + tid] = (int32_t)(0xFFFFFFFFu - (uint32_t)rowbest[tid]);
+  if (p.argmax_out && tid < rows) p.argmax_out[(int64_t)s * rows + tid] = key_index(rowbest[tid]);
 }
 
 }  // namespace
@@ -144,9 +148,8 @@ AcceptPlan plan_accept(int S, int gamma, int vocab) {
   chunk = (chunk + 3) & ~int64_t(3);
   pl.chunk = (int)chunk;
   pl.nsplit = (int)((vocab + chunk - 1) / chunk);
-  pl.counter_bytes = BD_WS_COUNTER_BYTES;
-  pl.part_bytes = align256(sizeof(uint64_t) * (size_t)rows * pl.nsplit);
-  pl.ws_bytes = pl.counter_bytes + pl.part_bytes + align256(sizeof(uint64_t) * (size_t)rows);
+  pl.counter_bytes = BD_WS_COUNTER_BYTES;   // counters and row maxima live in the counter region
+  pl.ws_bytes = pl.counter_bytes;
   return pl;
 }
 

@@ -354,6 +354,22 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   } else {
     n_keys = L;
   }
+  // ---- query rows of this lane: row n = rb*RB + 16*nt + lane%16 (loads issued before the slot
+  // table is built, so their latency overlaps it)
+  bf16x8 qop[NT][4];
+  int rowpos[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int n = rb * RB::kRows + 16 * nt + lr;
+    const bool valid = n < p.R;
+    const int j = valid ? n / p.G : 0;
+    const int h = g * p.G + (valid ? n % p.G : 0);
+    rowpos[nt] = valid ? L - p.nq + j : 0x7FFFFFFF;
+    const uint16_t* qrow = p.q + (((int64_t)s * p.nq + j) * p.Hq + h) * kD + 32 * lg;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = as_bf16x8(valid ? load16(qrow + 8 * kk) : u32x4{0u, 0u, 0u, 0u});
+  }
+
   const int e_begin = split * kps;
   int e_end = e_begin + kps;
   if (e_end > n_keys) e_end = n_keys;
@@ -427,21 +443,6 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
     first_dirty = __builtin_amdgcn_readfirstlane(first_dirty);
   }
   const bool want_lx = (gather ? p.lse_g : p.lse_f) != nullptr;
-
-  // ---- query rows of this lane: row n = rb*RB + 16*nt + lane%16
-  bf16x8 qop[NT][4];
-  int rowpos[NT];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const int n = rb * RB::kRows + 16 * nt + lr;
-    const bool valid = n < p.R;
-    const int j = valid ? n / p.G : 0;
-    const int h = g * p.G + (valid ? n % p.G : 0);
-    rowpos[nt] = valid ? L - p.nq + j : 0x7FFFFFFF;
-    const uint16_t* qrow = p.q + (((int64_t)s * p.nq + j) * p.Hq + h) * kD + 32 * lg;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = as_bf16x8(valid ? load16(qrow + 8 * kk) : u32x4{0u, 0u, 0u, 0u});
-  }
 
   RowState<NT> st;
 #pragma unroll
@@ -619,10 +620,10 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   }
   wait_vmem();
   __syncthreads();
-  if (tid == 0) sm.last = arrive(&p.counters[unit], (uint32_t)nsplit);
+  if (tid == 0) sm.last = arrive(counter_line(p.counters, unit), (uint32_t)nsplit);
   __syncthreads();
   if (!sm.last) return;
-  if (tid == 0) reset_counter(&p.counters[unit]);   // ready for the next call
+  if (tid == 0) reset_counter(counter_line(p.counters, unit));   // ready for the next call
   if (!row_valid) return;
 
   // merge the splits in split order with an online rescale, a batch of records at a time; every

@@ -92,8 +92,8 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
     return fail(BD_ERR_UNSUPPORTED, "problem too large for one launch");
   if (kv_extent(kv) > ((int64_t)1 << 34))
     return fail(BD_ERR_UNSUPPORTED, "K/V layout spans more than 2^34 elements");
-  if ((int64_t)pl.units_g + pl.units_f > BD_WS_COUNTER_BYTES / 4)
-    return fail(BD_ERR_UNSUPPORTED, "more than %d work units", BD_WS_COUNTER_BYTES / 4);
+  if ((int64_t)pl.units_g + pl.units_f > BD_WS_COUNTER_LINES)
+    return fail(BD_ERR_UNSUPPORTED, "more than %d work units", BD_WS_COUNTER_LINES);
   bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
   if (st != BD_OK) return st;
   if (pl.nblk == 0) return BD_OK;
@@ -282,8 +282,8 @@ bd_status bd_accept_len(const float* logits, int64_t row_stride, const int32_t* 
   if (gamma > 0 && !draft) return fail(BD_ERR_INVALID_ARG, "draft is NULL");
   if (row_stride < vocab) return fail(BD_ERR_INVALID_ARG, "row_stride %lld < vocab %d", (long long)row_stride, vocab);
   if ((int64_t)num_seqs * (gamma + 1) * 1024 > INT32_MAX) return fail(BD_ERR_UNSUPPORTED, "too many rows");
-  if ((int64_t)num_seqs * (gamma + 2) > BD_WS_COUNTER_BYTES / 4)
-    return fail(BD_ERR_UNSUPPORTED, "more than %d sequence and row counters", BD_WS_COUNTER_BYTES / 4);
+  if ((int64_t)num_seqs * (2 * gamma + 3) > BD_WS_COUNTER_LINES)
+    return fail(BD_ERR_UNSUPPORTED, "more than %d sequence and row counter lines", BD_WS_COUNTER_LINES);
   const bd::AcceptPlan pl = bd::plan_accept(num_seqs, gamma, vocab);
   bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
   if (st != BD_OK) return st;
@@ -301,8 +301,6 @@ bd_status bd_accept_len(const float* logits, int64_t row_stride, const int32_t* 
   p.bonus_out = bonus_out;
   p.argmax_out = argmax_out;
   p.counters = static_cast<uint32_t*>(ws);
-  p.part = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + pl.counter_bytes);
-  p.rowbest = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + pl.counter_bytes + pl.part_bytes);
   return launched(bd::launch_accept(p, stream));
 }
 

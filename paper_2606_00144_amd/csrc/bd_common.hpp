@@ -161,6 +161,13 @@ __device__ inline bool arrive(uint32_t* counter, uint32_t total) {
 __device__ inline void reset_counter(uint32_t* counter) {
   __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// Line i of the workspace's counter region.
+__device__ inline uint32_t* counter_line(uint32_t* region, int64_t i) {
+  return region + i * (BD_WS_COUNTER_STRIDE / 4);
+}
+__device__ inline void atomic_max_coherent(uint64_t* p, uint64_t v) {
+  __hip_atomic_fetch_max(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // ---- bf16 helpers ---------------------------------------------------------
 

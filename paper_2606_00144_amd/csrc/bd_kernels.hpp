@@ -63,14 +63,14 @@ struct AcceptParams {
   int32_t* accept_out;
   int32_t* bonus_out;
   int32_t* argmax_out;
-  uint64_t* part;           // [S][gamma+1][nsplit] chunk results
-  uint64_t* rowbest;        // [S][gamma+1] merged row results
-  uint32_t* counters;       // [S] sequence counters, then [S][gamma+1] row counters
+  // counter region lines: [S] sequence counters, [S][gamma+1] row counters, then [S][gamma+1]
+  // row maxima (packed keys, max-combined by the row's chunks)
+  uint32_t* counters;
 };
 
 struct AcceptPlan {
   int nsplit, chunk;
-  size_t counter_bytes, part_bytes, ws_bytes;
+  size_t counter_bytes, ws_bytes;
 };
 
 AcceptPlan plan_accept(int S, int gamma, int vocab);
