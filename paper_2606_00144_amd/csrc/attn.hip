@@ -464,13 +464,19 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
     TileRegs<NT, PAGED> T;
     if (arith) {
       // row offset (16-byte units) of key e_begin + slot: one scalar term per tile, lane-constant rest;
-      // keys past the split (padding, ragged end) stay in the allocation through the clamp in
+      // keys of the ragged last tile past the split stay in the allocation through the clamp in
       // dma_tile and are masked by their positions
       const uint32_t base16 = (uint32_t)(((int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head) >> 3);
       const uint32_t tok16 = (uint32_t)(p.kv.stride_tok >> 3);
       const uint32_t off_k0 = (uint32_t)lr * tok16, off_k1 = (uint32_t)(16 + lr) * tok16;
       const uint32_t off_v = (uint32_t)(4 * lg) * tok16;
       auto rows_at = [&](int slot0) {
+        if (slot0 >= ntiles * kTile) {   // a padding tile past this wave's last: row 0, a cache-resident address
+          A.k[0] = A.k[1] = 0u;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) A.v[h] = u32x4{0u, 0u, 0u, 0u};
+          return;
+        }
         const uint32_t r0 = base16 + (uint32_t)(e_begin + slot0) * tok16;
         A.k[0] = r0 + off_k0;
         A.k[1] = r0 + off_k1;

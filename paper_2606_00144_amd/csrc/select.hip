@@ -240,9 +240,26 @@ __device__ inline int block_exclusive_scan(int x, int* wsum, int& total) {
   return before;
 }
 
+// Add one to bin `d` of this wave's histogram.  When every active lane of the wave holds the same
+// digit (the common case for the leading digits, which the scores mostly share) one lane adds the
+// count, so the LDS atomics never serialise on a single bin.
+__device__ inline void hist_add(uint32_t* wave_hist, uint32_t d) {
+  const uint64_t active = __builtin_amdgcn_read_exec();
+  const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
+  const uint64_t same = __builtin_amdgcn_ballot_w64(d == d0);
+  if (same == active) {
+    if ((uint32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(active >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)active, 0u)) == 0u)
+      atomicAdd(&wave_hist[d0], (uint32_t)__builtin_popcountll(active));
+  } else {
+    atomicAdd(&wave_hist[d], 1u);
+  }
+}
+
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
-  __shared__ uint32_t hist[256];
-  __shared__ int wsum[kTopkThreads / kWave];
+  constexpr int kTopkWaves = kTopkThreads / kWave;
+  __shared__ float raw_lds[BD_SELECT_MAX_PREFIX];     // the pooled range, staged once
+  __shared__ uint32_t hist[kTopkWaves][256];          // one histogram per wave, summed per pass
+  __shared__ int wsum[kTopkWaves];
   __shared__ uint32_t s_digit, s_krem;
   const int tid = threadIdx.x;
   const int pair = blockIdx.x;
@@ -258,18 +275,19 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
   }
   if (g == 0 && tid == 0) p.nsel_out[s] = B;
 
-  // 1. total raw scores (row blocks summed in order)
+  // 1. total raw scores (row blocks summed in order); the prefix [0, N) is also staged in LDS
+  const int N = L - W, K = B - W, rad = p.pool_kernel / 2;
   float* raw = p.raw + (int64_t)pair * p.max_L;
   const float* part = p.raw_part + (int64_t)pair * p.n_rb * p.max_L;
   for (int t = tid; t < L; t += kTopkThreads) {
     float v = 0.f;
     for (int r = 0; r < p.n_rb; ++r) v += part[(int64_t)r * p.max_L + t];
     raw[t] = v;
+    if (t < N) raw_lds[t] = v;
   }
   __syncthreads();
 
   // 2. pooled keys of this thread's contiguous segment of the prefix [0, N)
-  const int N = L - W, K = B - W, rad = p.pool_kernel / 2;
   const int E = (N + kTopkThreads - 1) / kTopkThreads;
   const int t0 = tid * E;
   uint32_t key[kMaxPerThread];
@@ -280,8 +298,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
     if (e < E && t < N) {
       const int lo = t - rad < 0 ? 0 : t - rad;
       const int hi = t + rad > N - 1 ? N - 1 : t + rad;
-      float m = raw[lo];
-      for (int u = lo + 1; u <= hi; ++u) m = fmaxf(m, raw[u]);
+      float m = raw_lds[lo];
+      for (int u = lo + 1; u <= hi; ++u) m = fmaxf(m, raw_lds[u]);
       k = __float_as_uint(m);                // m >= 0: bit patterns order like values
     }
     key[e] = k;
@@ -290,17 +308,23 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
   // 3. radix select of the K-th largest key; krem = how many keys equal to it are taken
   uint32_t prefix = 0, pmask = 0, krem = (uint32_t)K;
   if (K > 0) {
+    uint32_t* my_hist = hist[threadIdx.x / kWave];
     for (int shift = 24; shift >= 0; shift -= 8) {
-      if (tid < 256) hist[tid] = 0;
+      for (int i = tid; i < kTopkWaves * 256; i += kTopkThreads) (&hist[0][0])[i] = 0;
       __syncthreads();
 #pragma unroll
       for (int e = 0; e < kMaxPerThread; ++e)
-        if (e < E && t0 + e < N && (key[e] & pmask) == prefix) atomicAdd(&hist[(key[e] >> shift) & 255u], 1u);
+        if (e < E && t0 + e < N && (key[e] & pmask) == prefix) hist_add(my_hist, (key[e] >> shift) & 255u);
       __syncthreads();
       if (tid < kWave) {
         uint32_t h[4], c = 0;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) { h[q] = hist[255 - (4 * tid + q)]; c += h[q]; }
+        for (int q = 0; q < 4; ++q) {
+          uint32_t v = 0;
+          for (int w = 0; w < kTopkWaves; ++w) v += hist[w][255 - (4 * tid + q)];
+          h[q] = v;
+          c += v;
+        }
         uint32_t incl = c;
 #pragma unroll
         for (int o = 1; o < kWave; o <<= 1) {
