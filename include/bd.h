@@ -19,7 +19,8 @@
  *   - Positions: sequence s holds cache rows 0 .. L_s-1 (L_s = seq_lens[s]),
  *     query rows included.  A query at position p sees keys t with 0 <= t <= p.
  *     Keys and queries are post-RoPE; positions are used only for the causal rule.
- *   - Softmax scale is the caller's `scale` (normally 1/sqrt(128)); softmax and
+ *   - Softmax scale is the caller's `scale`, positive and finite (normally
+ *     1/sqrt(128)); softmax and
  *     accumulation are fp32, outputs are rounded to bf16 (nearest-even), and
  *     log-sum-exp outputs are fp32 natural logs.  A row with no visible key
  *     gets output 0 and log-sum-exp -inf.

@@ -150,7 +150,7 @@ int32_t bd_abi_version(void) { return BD_ABI_VERSION; }
 size_t bd_select_kv_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads, int32_t window,
                                     int32_t max_seq_len) {
   if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || window < 1 || max_seq_len < 0) return 0;
-  return bd::plan_select(num_seqs, num_kv_heads, num_q_heads, window, max_seq_len).ws_bytes;
+  return bd::plan_select(num_seqs, num_kv_heads, num_q_heads, window, max_seq_len, true).ws_bytes;
 }
 
 bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_heads, int32_t window,
@@ -161,13 +161,16 @@ bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_
   if (window < 1 || budget < window) return fail(BD_ERR_INVALID_ARG, "need 1 <= window <= budget (window %d, budget %d)", window, budget);
   if (pool_kernel < 1 || pool_kernel % 2 == 0) return fail(BD_ERR_INVALID_ARG, "pool_kernel must be odd and >= 1");
   if (pool_kernel > 255) return fail(BD_ERR_UNSUPPORTED, "pool_kernel above 255");
-  if (!std::isfinite(scale)) return fail(BD_ERR_INVALID_ARG, "scale is not finite");
+  if (!std::isfinite(scale) || !(scale > 0.f)) return fail(BD_ERR_INVALID_ARG, "scale must be positive and finite");
   if (!q_win || !aligned(q_win, 16)) return fail(BD_ERR_INVALID_ARG, "q_win is NULL or not 16-byte aligned");
   if (!idx_out || !nsel_out) return fail(BD_ERR_INVALID_ARG, "idx_out and nsel_out are required");
   if ((int64_t)kv->max_seq_len - window > BD_SELECT_MAX_PREFIX)
     return fail(BD_ERR_UNSUPPORTED, "max_seq_len - window exceeds %d", BD_SELECT_MAX_PREFIX);
   if (window * (num_q_heads / kv->num_kv_heads) > 4096) return fail(BD_ERR_UNSUPPORTED, "window * group above 4096 rows");
-  const bd::SelectPlan pl = bd::plan_select(kv->num_seqs, kv->num_kv_heads, num_q_heads, window, kv->max_seq_len);
+  if (kv_extent(kv) > ((int64_t)1 << 34))
+    return fail(BD_ERR_UNSUPPORTED, "K layout spans more than 2^34 elements");
+  const bd::SelectPlan pl = bd::plan_select(kv->num_seqs, kv->num_kv_heads, num_q_heads, window, kv->max_seq_len,
+                                            kv->page_table != nullptr);
   st = check_ws(ws, ws_bytes, pl.ws_bytes);
   if (st != BD_OK) return st;
   bd::SelectParams p{};
@@ -187,6 +190,7 @@ bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_
   p.kps = pl.kps;
   p.max_L = kv->max_seq_len;
   p.scale_log2 = scale * 1.4426950408889634f;
+  p.max_roff = (uint32_t)((kv_extent(kv) - BD_HEAD_DIM) >> 3);
   char* w = static_cast<char*>(ws) + BD_WS_COUNTER_BYTES;   // the counter region stays untouched
   p.stats = reinterpret_cast<float*>(w);
   p.raw_part = reinterpret_cast<float*>(w + pl.stats_bytes);
@@ -212,7 +216,7 @@ bd_status bd_sparse_decode_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t
     return fail(BD_ERR_INVALID_ARG, "q and out must be non-NULL and 16-byte aligned");
   if (ld_idx < 0 || (ld_idx > 0 && (!idx || !nsel))) return fail(BD_ERR_INVALID_ARG, "idx / nsel / ld_idx invalid");
   if (!nsel) return fail(BD_ERR_INVALID_ARG, "nsel is NULL");
-  if (!std::isfinite(scale)) return fail(BD_ERR_INVALID_ARG, "scale is not finite");
+  if (!std::isfinite(scale) || !(scale > 0.f)) return fail(BD_ERR_INVALID_ARG, "scale must be positive and finite");
   return run_attn(kv, q, num_q_heads, 1, 1, idx, ld_idx, nsel, scale, out, lse_out, nullptr, nullptr, ws, ws_bytes,
                   stream);
 }
@@ -241,7 +245,7 @@ bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t
   if (num_views > 0 && (!idx_views || !nsel_views || !out_views || !aligned(out_views, 16) || ld_idx < 0))
     return fail(BD_ERR_INVALID_ARG, "views need idx_views, nsel_views, ld_idx >= 0 and a 16-byte aligned out_views");
   if (out_full && !aligned(out_full, 16)) return fail(BD_ERR_INVALID_ARG, "out_full is not 16-byte aligned");
-  if (!std::isfinite(scale)) return fail(BD_ERR_INVALID_ARG, "scale is not finite");
+  if (!std::isfinite(scale) || !(scale > 0.f)) return fail(BD_ERR_INVALID_ARG, "scale must be positive and finite");
   if ((int64_t)block_len * (num_q_heads / kv->num_kv_heads) > (1 << 20))
     return fail(BD_ERR_UNSUPPORTED, "block_len * group too large");
   return run_attn(kv, q_blk, num_q_heads, block_len, num_views, idx_views, num_views > 0 ? ld_idx : 0, nsel_views,
@@ -262,7 +266,7 @@ bd_status bd_verify_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_
   if (gamma < 0 || gamma > 4095) return fail(BD_ERR_INVALID_ARG, "gamma %d outside [0, 4095]", gamma);
   if (!q || !aligned(q, 16) || !out || !aligned(out, 16))
     return fail(BD_ERR_INVALID_ARG, "q and out must be non-NULL and 16-byte aligned");
-  if (!std::isfinite(scale)) return fail(BD_ERR_INVALID_ARG, "scale is not finite");
+  if (!std::isfinite(scale) || !(scale > 0.f)) return fail(BD_ERR_INVALID_ARG, "scale must be positive and finite");
   return run_attn(kv, q, num_q_heads, gamma + 1, 0, nullptr, 0, nullptr, scale, nullptr, nullptr, out, lse_out, ws,
                   ws_bytes, stream);
 }

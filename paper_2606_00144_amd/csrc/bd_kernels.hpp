@@ -84,10 +84,11 @@ struct SelectParams {
   int32_t S, Hkv, Hq, G, W;
   int32_t budget, pool_kernel;
   int32_t R;                // rows per (s, g): W * G
-  int32_t n_rb;             // row blocks of 128 rows
+  int32_t n_rb;             // row blocks of 16*NT rows
   int32_t nsplit, kps;      // key splits of the scoring passes
   int32_t max_L;
   float scale_log2;
+  uint32_t max_roff;        // largest valid row offset of the K layout, 16-byte units
   float* stats;             // [S][Hkv][n_rb][nsplit][128][2] per-split row max / sum
   float* raw_part;          // [S][Hkv][n_rb][max_L] per-row-block column sums
   float* raw;               // [S][Hkv][max_L] total raw scores (scores_out or workspace)
@@ -100,7 +101,9 @@ struct SelectPlan {
   size_t stats_bytes, raw_part_bytes, raw_bytes, ws_bytes;
 };
 
-SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L);
+// `paged`: the cache is paged (its splits then go through a slot table of bounded size); workspace
+// queries that do not know the layout use paged = true, which has at least as many splits.
+SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L, bool paged);
 hipError_t launch_select(const SelectParams& p, bool paged, hipStream_t stream);
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }

@@ -29,12 +29,18 @@ namespace {
 
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * kWave;
-constexpr int kSub = 16;            // keys per MFMA sub-tile
-constexpr int kStatRows = 128;      // stats record stride (rows)
-constexpr int kTargetBlocks = 1024;
+constexpr int kTile = 32;                        // keys per wave iteration (two MFMA sub-tiles of 16)
+constexpr int kTileLoads = 8;                    // 16-byte loads per lane per tile
+constexpr int kTileBytes = kTileLoads * kWave * 16;
+constexpr int kRing = 4;                         // tiles in flight per wave
+constexpr int kMaxPagedKeys = 4096;              // keys per workgroup through the paged slot table
+constexpr int kSlotCap = kMaxPagedKeys + kRing * kWaves * kTile;
+constexpr int kStatRows = 128;                   // stats record stride (rows)
+constexpr int kTargetBlocks = 256;               // one workgroup per CU
 constexpr int kTopkThreads = 1024;
 constexpr int kMaxPerThread = BD_SELECT_MAX_PREFIX / kTopkThreads;   // 32
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kSlack = 8.f;                    // lazy-rescale headroom of the pass-1 sums, log2 units
 
 __device__ inline void merge_ml(float& m, float& l, float m2, float l2) {
   const float M = fmaxf(m, m2);
@@ -43,24 +49,72 @@ __device__ inline void merge_ml(float& m, float& l, float m2, float l2) {
   m = M;
 }
 
-template <int NT>
+template <int NT, bool PAGED>
 struct ScoreSmem {
+  alignas(16) uint8_t ring[kWaves][kRing][kTileBytes];   // per-wave K tile slots filled by DMA
+  alignas(16) int32_t roff[PAGED ? kSlotCap : 4];        // paged: row offset (16-byte units) per key slot
   float m[kWaves][16 * NT];
   float l[kWaves][16 * NT];
   float lse2[16 * NT];
 };
 
-template <bool PAGED>
-__device__ inline void load_keys(u32x4 (&kr)[4], const KvView& kv, int s, int g, int t, int kend, int lg) {
-  const int64_t off = t < kend ? row_offset<PAGED>(kv, s, g, t) : -1;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) kr[j] = off >= 0 ? load16(kv.k + off + 32 * lg + 8 * j) : u32x4{0u, 0u, 0u, 0u};
+__device__ inline void dma16(const uint16_t* g, uint8_t* l) {
+  __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)l, 16, 0, 0);
 }
 
+// Direct-to-LDS loads of one K tile: load q (sub-tile q/4, k-step q%4) of a lane lands at
+// dst + q*1 KiB + 16*lane; the lane's rows are r[sub] (16-byte units, clamped to the layout).
+__device__ inline void dma_ktile(const uint16_t* k, const uint32_t (&r)[2], uint32_t max_roff, uint8_t* dst, int lane) {
+  const int lg = lane >> 4;
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub) {
+    const uint32_t ro = r[sub] < max_roff ? r[sub] : max_roff;
+    const uint16_t* kr = k + ((uint64_t)ro << 3) + 32 * lg;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dma16(kr + 8 * j, dst + (4 * sub + j) * 1024);
+  }
+}
+
+// Copy a landed K tile into registers (loads and their wait in one asm statement: the compiler
+// would otherwise wait for every direct-to-LDS load in flight before any LDS read).
+__device__ inline void read_ktile(u32x4 (&t)[2][4], uint32_t src, int lane) {
+  const uint32_t a = src + 16 * lane;
+  asm volatile(
+      "ds_read_b128 %0, %8\n"
+      "ds_read_b128 %1, %8 offset:1024\n"
+      "ds_read_b128 %2, %8 offset:2048\n"
+      "ds_read_b128 %3, %8 offset:3072\n"
+      "ds_read_b128 %4, %8 offset:4096\n"
+      "ds_read_b128 %5, %8 offset:5120\n"
+      "ds_read_b128 %6, %8 offset:6144\n"
+      "ds_read_b128 %7, %8 offset:7168\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(t[0][0]), "=&v"(t[0][1]), "=&v"(t[0][2]), "=&v"(t[0][3]), "=&v"(t[1][0]), "=&v"(t[1][1]),
+        "=&v"(t[1][2]), "=&v"(t[1][3])
+      : "v"(a));
+}
+
+// Row offsets of a paged tile's two lane rows from the slot table.
+__device__ inline void read_krows(uint32_t (&r)[2], uint32_t roff_lds, int slot0, int lane) {
+  const uint32_t a = roff_lds + 4 * (slot0 + (lane & 15));
+  asm volatile(
+      "ds_read_b32 %0, %2\n"
+      "ds_read_b32 %1, %2 offset:64\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1])
+      : "v"(a));
+}
+
+// One pass over the causal key range of (sequence, KV head, row block, split).  Each wave streams
+// every 4th 32-key tile through a kRing-deep ring of LDS slots.
+//   PASS 1: per observation row, running max and sum of exp of the scaled logits;
+//   PASS 2: every key's column sum of the rows' normalised weights (complete within the row
+//           block: one plain store per key).
 template <int NT, bool PAGED, int PASS>
 __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
-  __shared__ ScoreSmem<NT> sm;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  __shared__ ScoreSmem<NT, PAGED> sm;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lg = lane >> 4, lr = lane & 15;
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
   const int rb = bid % p.n_rb;
@@ -90,11 +144,38 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
     for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = as_bf16x8(valid ? load16(qrow + 8 * kk) : u32x4{0u, 0u, 0u, 0u});
   }
 
+  const int ntiles = k1 > k0 ? (k1 - k0 + kTile - 1) / kTile : 0;
+  if constexpr (PAGED) {
+    // slot table of this split: all page-table loads issued before any result is used; padding
+    // slots (past the split) hold row 0, a safe, cache-resident address
+    constexpr int kPer = (kSlotCap + kThreads - 1) / kThreads;
+    int pg[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int t = k0 + tid + k * kThreads;
+      pg[k] = t < k1 ? p.kv.page_table[(int64_t)s * p.kv.max_pages_per_seq + t / p.kv.page_size] : -1;
+    }
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int i = tid + k * kThreads;
+      if (i < kSlotCap) {
+        const int t = k0 + i;
+        int64_t o = 0;
+        if ((unsigned)pg[k] < (unsigned)p.kv.num_pages)
+          o = (int64_t)pg[k] * p.kv.stride_page + (int64_t)g * p.kv.stride_head +
+              (int64_t)(t % p.kv.page_size) * p.kv.stride_tok;
+        sm.roff[i] = (int)(o >> 3);
+      }
+    }
+  }
+
+  // lse of each row (pass 2): the caller's, or merged from the pass-1 statistics.  Padded rows get
+  // +inf, so their weights are exactly zero even where no mask is applied.
   float rm[NT], rl[NT], lse2[NT];
   if constexpr (PASS == 2) {
     if (tid < 16 * NT) {
       const int n = rb * 16 * NT + tid;
-      float v = 0.f;
+      float v = INFINITY;
       if (n < p.R) {
         if (p.lse_win) {
           const int i = n / p.G, h = g * p.G + n % p.G;
@@ -110,18 +191,31 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
       }
       sm.lse2[tid] = v;
     }
-    __syncthreads();
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) lse2[nt] = sm.lse2[16 * nt + lr];
   } else {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) { rm[nt] = -INFINITY; rl[nt] = 0.f; }
   }
+  __syncthreads();
+  if constexpr (PASS == 2) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) lse2[nt] = sm.lse2[16 * nt + lr];
+  }
+
+  // tiles whose keys all lie inside the split and at or before the block's earliest row position
+  // need no mask
+  const int minpos = L - p.W + (rb * 16 * NT) / p.G;
+  int first_dirty;
+  {
+    const int c1 = minpos - k0 - (kTile - 1);
+    const int fd1 = c1 < 0 ? 0 : c1 / kTile + 1;
+    const int fd2 = (k1 - k0) / kTile;
+    first_dirty = fd1 < fd2 ? fd1 : fd2;
+  }
 
   float* raw_part = p.raw_part + ((int64_t)pair * p.n_rb + rb) * p.max_L;
-  const int nsub = k1 > k0 ? (k1 - k0 + kSub - 1) / kSub : 0;
 
-  auto step = [&](const u32x4 (&kr)[4], int t0) {
+  // 16 keys x 16*NT rows of one sub-tile; keys tb .. tb+3 belong to this lane
+  auto sub_step = [&](const u32x4 (&kr)[4], int tb, bool dirty) {
     f32x4 acc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -130,35 +224,34 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
       for (int j = 0; j < 4; ++j) a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[j]), qop[nt][j], a, 0, 0, 0);
       acc[nt] = a;
     }
-    const int tb = t0 + 4 * lg;              // keys tb .. tb+3 of this lane
-    if constexpr (PASS == 1) {
+    if (dirty) {
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        float x[4], mx = -INFINITY;
+      for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int t = tb + i;
-          x[i] = (t < k1 && t <= rowpos[nt]) ? acc[nt][i] * p.scale_log2 : -INFINITY;
-          mx = fmaxf(mx, x[i]);
+          if (!(t < k1 && t <= rowpos[nt])) acc[nt][i] = -INFINITY;
         }
-        const float M = fmaxf(rm[nt], mx);
-        if (M != -INFINITY) {
-          float add = 0.f;
+    }
+    if constexpr (PASS == 1) {
+      // per-lane running (max, sum) with a lazily raised reference: weights stay <= 2^kSlack
 #pragma unroll
-          for (int i = 0; i < 4; ++i) add += exp2f(x[i] - M);
-          rl[nt] = rl[nt] * exp2f(rm[nt] - M) + add;
-          rm[nt] = M;
+      for (int nt = 0; nt < NT; ++nt) {
+        const float mx = fmaxf(fmaxf(acc[nt][0], acc[nt][1]), fmaxf(acc[nt][2], acc[nt][3])) * p.scale_log2;
+        if (mx > rm[nt] + kSlack) {
+          rl[nt] *= exp2f(rm[nt] - mx);
+          rm[nt] = mx;
         }
+        const float mu = rm[nt] == -INFINITY ? 0.f : rm[nt];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rl[nt] += __builtin_amdgcn_exp2f(fmaf(acc[nt][i], p.scale_log2, -mu));
       }
     } else {
       float col[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int t = tb + i;
-          if (t < k1 && t <= rowpos[nt]) col[i] += exp2f(acc[nt][i] * p.scale_log2 - lse2[nt]);
-        }
+        for (int i = 0; i < 4; ++i) col[i] += __builtin_amdgcn_exp2f(fmaf(acc[nt][i], p.scale_log2, -lse2[nt]));
 #pragma unroll
       for (int i = 0; i < 4; ++i) col[i] = sum16(col[i]);
       if (lr < 4) {
@@ -169,21 +262,40 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
     }
   };
 
-  if (wave < nsub) {
-    u32x4 ka[4], kb[4];
-    load_keys<PAGED>(ka, p.kv, s, g, k0 + kSub * wave + lr, k1, lg);
-    int it = wave;
-    while (true) {
-      const int nx = it + kWaves;
-      if (nx < nsub) load_keys<PAGED>(kb, p.kv, s, g, k0 + kSub * nx + lr, k1, lg);
-      step(ka, k0 + kSub * it);
-      if (nx >= nsub) break;
-      const int nx2 = nx + kWaves;
-      if (nx2 < nsub) load_keys<PAGED>(ka, p.kv, s, g, k0 + kSub * nx2 + lr, k1, lg);
-      step(kb, k0 + kSub * nx);
-      if (nx2 >= nsub) break;
-      it = nx2;
+  if (wave < ntiles) {
+    const uint32_t ring_lds = lds_addr(sm.ring[wave][0]);
+    const uint32_t roff_lds = lds_addr(sm.roff);
+    const uint32_t base16 = PAGED ? 0u : (uint32_t)(((int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head) >> 3);
+    const uint32_t tok16 = (uint32_t)(p.kv.stride_tok >> 3);
+    auto issue = [&](int tile, int slot) {
+      uint32_t r[2];
+      if constexpr (PAGED) {
+        read_krows(r, roff_lds, kTile * tile, lane);
+      } else if (tile >= ntiles) {
+        r[0] = r[1] = 0u;                  // padding: row 0, a safe, cache-resident address
+      } else {
+        const uint32_t r0 = base16 + (uint32_t)(k0 + kTile * tile) * tok16;
+        r[0] = r0 + (uint32_t)lr * tok16;
+        r[1] = r0 + (uint32_t)(16 + lr) * tok16;
+      }
+      dma_ktile(p.kv.k, r, p.max_roff, sm.ring[wave][slot], lane);
+    };
+#pragma unroll
+    for (int q = 0; q < kRing; ++q) issue(wave + kWaves * q, q);
+    u32x4 kt[2][4];
+    for (int j = 0;; ++j) {
+      const int it = wave + kWaves * j, slot = j % kRing;
+      // the tile about to be read was issued (kRing-1) tiles before the newest
+      asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
+      read_ktile(kt, ring_lds + slot * kTileBytes, lane);
+      issue(it + kRing * kWaves, slot);
+      const int tb = k0 + kTile * it + 4 * lg;
+      const bool dirty = it >= first_dirty;
+      sub_step(kt[0], tb, dirty);
+      sub_step(kt[1], tb + 16, dirty);
+      if (it + kWaves >= ntiles) break;
     }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the block ends
   }
 
   if constexpr (PASS == 1) {
@@ -390,7 +502,7 @@ int select_nt(int R) {
 
 }  // namespace
 
-SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L) {
+SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L, bool paged) {
   SelectPlan pl;
   const int G = Hq / Hkv;
   const int R = W * G;
@@ -398,10 +510,12 @@ SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L) {
   pl.n_rb = (R + 16 * nt - 1) / (16 * nt);
   const int64_t units = (int64_t)S * Hkv * pl.n_rb;
   const int64_t per_block = (units * max_L + kTargetBlocks - 1) / kTargetBlocks;
-  int64_t kps = (per_block + kWaves * kSub - 1) / (kWaves * kSub) * (kWaves * kSub);
-  const int64_t cap = ((int64_t)max_L + kWaves * kSub - 1) / (kWaves * kSub) * (kWaves * kSub);
+  constexpr int64_t kStep = kWaves * kTile;
+  int64_t kps = (per_block + kStep - 1) / kStep * kStep;
+  const int64_t cap = ((int64_t)max_L + kStep - 1) / kStep * kStep;
   if (kps > cap) kps = cap;
-  if (kps < kWaves * kSub) kps = kWaves * kSub;
+  if (paged && kps > kMaxPagedKeys) kps = kMaxPagedKeys;
+  if (kps < kStep) kps = kStep;
   pl.kps = (int)kps;
   pl.nsplit = max_L > 0 ? (int)((max_L + kps - 1) / kps) : 1;
   pl.stats_bytes = align256(sizeof(float) * (size_t)units * pl.nsplit * kStatRows * 2);

@@ -69,6 +69,8 @@ def test_verify_rejections(L):
     assert _verify(L, _kv(), q=0) == bd.BD_ERR_INVALID_ARG
     assert _verify(L, _kv(), out=FAKE + 2) == bd.BD_ERR_INVALID_ARG
     assert _verify(L, _kv(), scale=float("nan")) == bd.BD_ERR_INVALID_ARG
+    assert _verify(L, _kv(), scale=0.0) == bd.BD_ERR_INVALID_ARG
+    assert _verify(L, _kv(), scale=-0.088) == bd.BD_ERR_INVALID_ARG
     assert _verify(L, _kv(stride_tok=100)) == bd.BD_ERR_INVALID_ARG
     assert _verify(L, _kv(page_table=FAKE, page_size=16, max_pages_per_seq=10, num_pages=100,
                           stride_page=8 * 16 * 128)) == bd.BD_ERR_INVALID_ARG   # 4096 > 10 * 16
