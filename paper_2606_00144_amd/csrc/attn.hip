@@ -673,6 +673,376 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   write_final(Mg, Lg, Lxg, ag);
 }
 
+// ---- block mode: many query rows per (sequence, KV head) ---------------------
+//
+// When a unit has more than one 32-row block (the multiview continuation block:
+// C x G rows), re-streaming K/V once per row block would multiply the traffic.
+// A block-mode workgroup has 8 waves, wave w owning row block 8*rg + w, and all
+// of them consume every 32-key tile of the split from a shared LDS ring: each
+// wave issues 2 of a tile's 16 direct-to-LDS loads, and one barrier per tile
+// both publishes the landed tile and frees the slot read in the step before.
+// A wave's online-softmax state is then complete for the split; splits merge
+// through per-row-block records in the last workgroup of the row group.
+
+template <bool B>
+struct BoolTag { static constexpr bool value = B; };
+
+constexpr int kBWaves = 8;
+constexpr int kBThreads = kBWaves * kWave;
+constexpr int kBRing = 6;                          // tile slots; kBRing-1 tiles stay in flight
+constexpr int kBSlotCap = kMaxSplitKeys + kBRing * kTile;
+
+struct BlockSmem {
+  alignas(16) int32_t roff[kBSlotCap];
+  alignas(16) int32_t tpos[kBSlotCap];
+  alignas(16) uint8_t ring[kBRing][kTileBytes];
+  int32_t last;
+};
+
+// Tile data plus, from the slot table, the tile's positions and the two row offsets this wave loads
+// for the tile it issues next.
+__device__ inline void read_block_tile(TileRegs<2, true>& T, uint32_t (&r)[2], uint32_t src, uint32_t tpos_lds,
+                                       int slot0, uint32_t roff_lds, int next0, int rit0, int rit1, int lane) {
+  const int lg = lane >> 4;
+  const uint32_t at = src + 16 * lane;
+  const uint32_t ap = tpos_lds + 4 * (slot0 + 4 * lg);
+  const uint32_t a0 = roff_lds + 4 * (next0 + rit0);
+  const uint32_t a1 = roff_lds + 4 * (next0 + rit1);
+  asm volatile(
+      "ds_read_b128 %0, %20\n"
+      "ds_read_b128 %1, %20 offset:1024\n"
+      "ds_read_b128 %2, %20 offset:2048\n"
+      "ds_read_b128 %3, %20 offset:3072\n"
+      "ds_read_b128 %4, %20 offset:4096\n"
+      "ds_read_b128 %5, %20 offset:5120\n"
+      "ds_read_b128 %6, %20 offset:6144\n"
+      "ds_read_b128 %7, %20 offset:7168\n"
+      "ds_read_b128 %8, %20 offset:8192\n"
+      "ds_read_b128 %9, %20 offset:9216\n"
+      "ds_read_b128 %10, %20 offset:10240\n"
+      "ds_read_b128 %11, %20 offset:11264\n"
+      "ds_read_b128 %12, %20 offset:12288\n"
+      "ds_read_b128 %13, %20 offset:13312\n"
+      "ds_read_b128 %14, %20 offset:14336\n"
+      "ds_read_b128 %15, %20 offset:15360\n"
+      "ds_read_b128 %16, %21\n"
+      "ds_read_b128 %17, %21 offset:64\n"
+      "ds_read_b32 %18, %22\n"
+      "ds_read_b32 %19, %23\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(T.k[0][0]), "=&v"(T.k[0][1]), "=&v"(T.k[0][2]), "=&v"(T.k[0][3]), "=&v"(T.k[1][0]),
+        "=&v"(T.k[1][1]), "=&v"(T.k[1][2]), "=&v"(T.k[1][3]), "=&v"(T.v[0]), "=&v"(T.v[1]), "=&v"(T.v[2]),
+        "=&v"(T.v[3]), "=&v"(T.v[4]), "=&v"(T.v[5]), "=&v"(T.v[6]), "=&v"(T.v[7]), "=&v"(T.tp[0]), "=&v"(T.tp[1]),
+        "=&v"(r[0]), "=&v"(r[1])
+      : "v"(at), "v"(ap), "v"(a0), "v"(a1));
+}
+
+// Load q (0..15) of a tile for this lane: K load q < 8 (sub-tile q/4, k-step q%4), V load q >= 8
+// (row group (q-8)/4, row (q-8)%4); `r` is the row's offset in 16-byte units.
+__device__ inline void dma_load(const KvView& kv, uint32_t r, uint32_t max_roff, int q, uint8_t* dst, int lane) {
+  const int lg = lane >> 4, lr = lane & 15;
+  const uint32_t ro = r < max_roff ? r : max_roff;
+  if (q < 8) dma16(kv.k + ((uint64_t)ro << 3) + 32 * lg + 8 * (q & 3), dst + q * 1024);
+  else dma16(kv.v + ((uint64_t)ro << 3) + 8 * lr, dst + q * 1024);
+}
+
+template <bool PAGED>
+__global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
+  constexpr int NT = 2;
+  using RB = RowBlock<NT>;
+  __shared__ BlockSmem sm;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lg = lane >> 4, lr = lane & 15;
+
+  // ---- which (kind, row group, split) this workgroup owns
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const bool gather = bid < p.nblk_g;
+  const int local = gather ? bid : bid - p.nblk_g;
+  const int nsplit = gather ? p.nsplit_g : p.nsplit_f;
+  const int kps = gather ? p.kps_g : p.kps_f;
+  const int rg = local % p.n_rg;
+  const int rest = local / p.n_rg;
+  const int split = rest % nsplit;
+  const int pair = rest / nsplit;
+  const int g = pair % p.Hkv;
+  const int vs = pair / p.Hkv;
+  const int s = gather ? vs % p.S : vs;
+  const int view = gather ? vs / p.S : 0;
+  const int unit = gather ? pair * p.n_rg + rg : p.units_g + pair * p.n_rg + rg;
+  const int rb = rg * kBWaves + wave;            // this wave's row block
+  const bool has_rows = rb < p.n_rb;
+
+  const int L = seq_len(p.kv, s);
+  int n_keys;
+  const int32_t* idx_row = nullptr;
+  if (gather) {
+    idx_row = p.idx + ((int64_t)vs * p.Hkv + g) * p.ld_idx;
+    int n = p.nsel[vs];
+    n_keys = n < 0 ? 0 : (n > p.ld_idx ? p.ld_idx : n);
+  } else {
+    n_keys = L;
+  }
+  const int e_begin = split * kps;
+  int e_end = e_begin + kps;
+  if (e_end > n_keys) e_end = n_keys;
+  const int ntiles = e_end > e_begin ? (e_end - e_begin + kTile - 1) / kTile : 0;
+
+  // ---- query rows of this wave's lanes: row n = rb*32 + 16*nt + lane%16
+  bf16x8 qop[NT][4];
+  int rowpos[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int n = rb * RB::kRows + 16 * nt + lr;
+    const bool valid = n < p.R;
+    const int j = valid ? n / p.G : 0;
+    const int h = g * p.G + (valid ? n % p.G : 0);
+    rowpos[nt] = valid ? L - p.nq + j : 0x7FFFFFFF;
+    const uint16_t* qrow = p.q + (((int64_t)s * p.nq + j) * p.Hq + h) * kD + 32 * lg;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = as_bf16x8(valid ? load16(qrow + 8 * kk) : u32x4{0u, 0u, 0u, 0u});
+  }
+
+  const bool arith = !PAGED && !gather;
+  if (!arith) {
+    const int nslots = (ntiles + kBRing) * kTile;     // <= kBSlotCap: padding tiles included
+    constexpr int kPer = (kBSlotCap + kBThreads - 1) / kBThreads;
+    int tv[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int e = e_begin + tid + k * kBThreads;
+      int t = -1;
+      if (e < e_end) t = gather ? idx_row[e] : e;
+      tv[k] = (t >= 0 && t < L) ? t : -1;
+    }
+    int pg[kPer];
+    if constexpr (PAGED) {
+#pragma unroll
+      for (int k = 0; k < kPer; ++k)
+        pg[k] = tv[k] >= 0 ? p.kv.page_table[(int64_t)s * p.kv.max_pages_per_seq + tv[k] / p.kv.page_size] : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int i = tid + k * kBThreads;
+      if (i < nslots && i < kBSlotCap) {
+        int t = tv[k];
+        int64_t o;
+        if constexpr (PAGED) {
+          o = (unsigned)pg[k] < (unsigned)p.kv.num_pages
+                  ? (int64_t)pg[k] * p.kv.stride_page + (int64_t)g * p.kv.stride_head +
+                        (int64_t)(t % p.kv.page_size) * p.kv.stride_tok
+                  : -1;
+        } else {
+          o = (int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head + (int64_t)t * p.kv.stride_tok;
+        }
+        if (t < 0 || o < 0) { t = -1; o = 0; }
+        sm.roff[i] = (int)(o >> 3);
+        sm.tpos[i] = t;
+      }
+    }
+    __syncthreads();
+  }
+  const int minpos = L - p.nq + (rb * RB::kRows) / p.G;   // earliest row position of this wave
+  const bool want_lx = (gather ? p.lse_g : p.lse_f) != nullptr;
+
+  RowState<NT> st;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    st.m[nt] = -INFINITY;
+    st.l[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    st.lx[nt] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // ---- the two loads of every tile that this wave issues, and the tile rows they read
+  const int q0 = 2 * wave, q1 = 2 * wave + 1;
+  auto row_in_tile = [&](int q) { return q < 8 ? 16 * (q >> 2) + lr : 16 * ((q - 8) >> 2) + 4 * lg + ((q - 8) & 3); };
+  const int rit0 = row_in_tile(q0), rit1 = row_in_tile(q1);
+  const uint32_t base16 = arith ? (uint32_t)(((int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head) >> 3) : 0u;
+  const uint32_t tok16 = (uint32_t)(p.kv.stride_tok >> 3);
+  const uint32_t roff_lds = lds_addr(sm.roff), tpos_lds = lds_addr(sm.tpos);
+  const uint32_t ring_lds = lds_addr(sm.ring[0]);
+  auto arith_rows = [&](int tile, uint32_t (&r)[2]) {
+    if (tile >= ntiles) { r[0] = r[1] = 0u; return; }   // padding: row 0, a cache-resident address
+    const uint32_t r0 = base16 + (uint32_t)(e_begin + kTile * tile) * tok16;
+    r[0] = r0 + (uint32_t)rit0 * tok16;
+    r[1] = r0 + (uint32_t)rit1 * tok16;
+  };
+  auto issue = [&](int tile, const uint32_t (&r)[2]) {
+    uint8_t* dst = sm.ring[tile % kBRing];
+    dma_load(p.kv, r[0], p.max_roff, q0, dst, lane);
+    dma_load(p.kv, r[1], p.max_roff, q1, dst, lane);
+  };
+
+  // the two streaming variants are separate loops, so neither carries the other's registers
+  auto stream = [&](auto arith_tag) {
+    constexpr bool ARITH = decltype(arith_tag)::value;
+    // prologue: tiles 0 .. kBRing-2
+    for (int t = 0; t < kBRing - 1; ++t) {
+      uint32_t r[2];
+      if constexpr (ARITH) {
+        arith_rows(t, r);
+      } else {
+        asm volatile(
+            "ds_read_b32 %0, %2\n"
+            "ds_read_b32 %1, %3\n"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(r[0]), "=&v"(r[1])
+            : "v"(roff_lds + 4 * (kTile * t + rit0)), "v"(roff_lds + 4 * (kTile * t + rit1)));
+      }
+      issue(t, r);
+    }
+    int fd_arith = 0;
+    if constexpr (ARITH) {
+      const int c1 = minpos - e_begin - (kTile - 1);
+      const int fd1 = c1 < 0 ? 0 : c1 / kTile + 1;
+      const int fd2 = (e_end - e_begin) / kTile;
+      fd_arith = fd1 < fd2 ? fd1 : fd2;
+    }
+    TileRegs<NT, true> T;
+    // tile t+kBRing-1 is issued in step t, after the barrier that frees its slot (read in step t-1)
+    for (int t = 0; t < ntiles; ++t) {
+      // this wave's loads of tile t are older than the kBRing-2 tiles issued after it
+      asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+      static_assert(2 * (kBRing - 2) == 8, "wait count follows the ring depth");
+      const int nxt = t + kBRing - 1;
+      const uint32_t src = ring_lds + (uint32_t)(t % kBRing) * kTileBytes;
+      uint32_t r[2];
+      bool dirty;
+      if constexpr (ARITH) {
+        read_tile<NT, true>(T, src, lane);
+        arith_rows(nxt, r);
+        dirty = t >= fd_arith;
+      } else {
+        read_block_tile(T, r, src, tpos_lds, kTile * t, roff_lds, kTile * nxt, rit0, rit1, lane);
+        bool bad = false;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int tp = (int)T.tp[i >> 2][i & 3];
+          bad |= tp < 0 || tp > minpos;
+        }
+        dirty = __builtin_amdgcn_ballot_w64(bad) != 0;
+      }
+      issue(nxt, r);
+      if (has_rows) {
+        if constexpr (ARITH) {
+          const int slot0 = kTile * t;
+          tile_step<NT, true>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx, [&](int i) {
+            const int e = e_begin + slot0 + 16 * (i >> 2) + 4 * lg + (i & 3);
+            return e < e_end ? e : -1;
+          });
+        } else {
+          tile_step<NT, true>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx,
+                              [&](int i) { return (int)T.tp[i >> 2][i & 3]; });
+        }
+      }
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the block ends
+  };
+  if (ntiles > 0) {
+    if (arith) stream(BoolTag<true>{});
+    else stream(BoolTag<false>{});
+  }
+
+  // ---- per-row results of this wave: (m, l, lx) of rows 16*nt + lane%16
+  float lxw[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    float lx = st.lx[nt];
+    lx += shfl_xor_f(lx, 16);
+    lx += shfl_xor_f(lx, 32);
+    lxw[nt] = lx;
+  }
+  const int64_t view_rows = (int64_t)p.S * p.nq * p.Hq;
+  uint16_t* out = gather ? p.out_g + (int64_t)view * view_rows * kD : p.out_f;
+  float* lse = gather ? (p.lse_g ? p.lse_g + (int64_t)view * view_rows : nullptr) : p.lse_f;
+  // normalise and write rows 16*nt + lane%16; register i of d-tile dt holds d = 32*(lane/16) + 8*i + dt
+  auto write_rows = [&](const float (&M)[NT], const float (&Lw)[NT], const float (&Lx)[NT], const f32x4 (&o)[NT][8]) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int n = rb * RB::kRows + 16 * nt + lr;
+      if (n >= p.R) continue;
+      const int j = n / p.G, h = g * p.G + n % p.G;
+      const int64_t orow = ((int64_t)s * p.nq + j) * p.Hq + h;
+      const float inv = Lw[nt] > 0.f ? 1.f / Lw[nt] : 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        u32x4 w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(o[nt][2 * e][i] * inv, o[nt][2 * e + 1][i] * inv);
+        *reinterpret_cast<u32x4*>(out + orow * kD + 32 * lg + 8 * i) = w;
+      }
+      if (lse && lg == 0) lse[orow] = Lx[nt] > 0.f ? (M[nt] + __log2f(Lx[nt])) * kLn2 : -INFINITY;
+    }
+  };
+
+  if (nsplit == 1) {
+    if (has_rows) {
+      float lw[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) lw[nt] = st.l[nt][0];
+      write_rows(st.m, lw, lxw, st.o);
+    }
+    return;
+  }
+
+  // ---- publish this wave's record for the split: row stats as float4 (m, l, lx, -) per row, then
+  // the outputs as chunk (nt, dt) x lane float4s (1 KiB contiguous per store instruction)
+  const int unit_local = gather ? unit : unit - p.units_g;
+  const float* rec_base = p.part + (gather ? 0 : (int64_t)p.units_g * kBWaves * p.nsplit_g * RB::kRec);
+  const __amdgpu_buffer_rsrc_t urec =
+      make_rsrc(rec_base + ((int64_t)unit_local * kBWaves + wave) * nsplit * RB::kRec, (uint32_t)(nsplit * RB::kRec * 4));
+  constexpr uint32_t kOutOff = 16 * RB::kRows;
+  if (has_rows) {
+    const uint32_t rec = (uint32_t)split * RB::kRec * 4;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      if (lg == 0) store16_coherent(urec, rec + 16 * (16 * nt + lr), f32x4{st.m[nt], st.l[nt][0], lxw[nt], 0.f});
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) store16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + dt) * kWave + lane), st.o[nt][dt]);
+    }
+  }
+  wait_vmem();
+  __syncthreads();
+  if (tid == 0) sm.last = arrive(counter_line(p.counters, unit), (uint32_t)nsplit);
+  __syncthreads();
+  if (!sm.last) return;
+  if (tid == 0) reset_counter(counter_line(p.counters, unit));   // ready for the next call
+  if (!has_rows) return;
+
+  // merge this wave's row block over the splits, in split order, with an online rescale
+  float Mg[NT], Lg[NT], Lxg[NT];
+  f32x4 og[NT][8];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    Mg[nt] = -INFINITY;
+    Lg[nt] = 0.f;
+    Lxg[nt] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) og[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    for (int sp = 0; sp < nsplit; ++sp) {
+      const uint32_t rec = (uint32_t)sp * RB::kRec * 4;
+      const f32x4 sv = load16_coherent(urec, rec + 16 * (16 * nt + lr));
+      f32x4 ov[8];
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) ov[dt] = load16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + dt) * kWave + lane));
+      const float mb = fmaxf(Mg[nt], sv[0]);
+      const float mbu = mb == -INFINITY ? 0.f : mb;
+      const float sc = exp2f(Mg[nt] - mbu), wt = exp2f(sv[0] - mbu);
+      Lg[nt] = Lg[nt] * sc + wt * sv[1];
+      Lxg[nt] = Lxg[nt] * sc + wt * sv[2];
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) og[nt][dt] = og[nt][dt] * sc + ov[dt] * wt;
+      Mg[nt] = mb;
+    }
+  }
+  write_rows(Mg, Lg, Lxg, og);
+}
+
 }  // namespace
 
 AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full, bool paged) {
@@ -682,9 +1052,11 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
   pl.nt = pl.R <= 16 ? 1 : 2;
   const int rows = 16 * pl.nt;
   pl.n_rb = (pl.R + rows - 1) / rows;
-  pl.units_g = num_views * S * Hkv * pl.n_rb;
-  pl.units_f = with_full ? S * Hkv * pl.n_rb : 0;
-  constexpr int64_t kStep = kWaves * kTile;       // one tile per wave
+  pl.block = pl.n_rb >= 2;                        // several 32-row blocks: they share the K/V stream
+  pl.n_rg = pl.block ? (pl.n_rb + kBWaves - 1) / kBWaves : pl.n_rb;
+  pl.units_g = num_views * S * Hkv * pl.n_rg;
+  pl.units_f = with_full ? S * Hkv * pl.n_rg : 0;
+  constexpr int64_t kStep = kWaves * kTile;       // one tile per wave of the split kernel
   auto round_up = [](int64_t x, int64_t m) { return (x + m - 1) / m * m; };
   const int64_t work = (int64_t)pl.units_g * ld_idx + (int64_t)pl.units_f * max_L;
   int64_t kps = round_up((work + kTargetBlocks - 1) / kTargetBlocks, kStep);
@@ -703,7 +1075,8 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
   pl.nblk = (int)blocks;
   pl.counter_bytes = BD_WS_COUNTER_BYTES;   // fixed: scratch of any call never lands on a counter
   const bool split = (pl.units_g && pl.nsplit_g > 1) || (pl.units_f && pl.nsplit_f > 1);
-  pl.record_bytes = split ? align256(sizeof(float) * attn_record_floats(pl.nt) * (size_t)blocks) : 0;
+  const size_t records = (size_t)blocks * (pl.block ? kBWaves : 1);   // block mode: one per row block
+  pl.record_bytes = split ? align256(sizeof(float) * attn_record_floats(pl.nt) * records) : 0;
   pl.ws_bytes = pl.counter_bytes + pl.record_bytes;
   return pl;
 }
@@ -714,9 +1087,14 @@ static hipError_t launch_nt(const AttnParams& p, int nblocks, hipStream_t stream
   return hipGetLastError();
 }
 
-hipError_t launch_attn(const AttnParams& p, int nt, bool paged, int nblocks, hipStream_t stream) {
-  if (nt == 1) return paged ? launch_nt<1, true>(p, nblocks, stream) : launch_nt<1, false>(p, nblocks, stream);
-  return paged ? launch_nt<2, true>(p, nblocks, stream) : launch_nt<2, false>(p, nblocks, stream);
+hipError_t launch_attn(const AttnParams& p, const AttnPlan& pl, bool paged, hipStream_t stream) {
+  if (pl.block) {
+    if (paged) hipLaunchKernelGGL(block_kernel<true>, dim3(pl.nblk), dim3(kBThreads), 0, stream, p);
+    else hipLaunchKernelGGL(block_kernel<false>, dim3(pl.nblk), dim3(kBThreads), 0, stream, p);
+    return hipGetLastError();
+  }
+  if (pl.nt == 1) return paged ? launch_nt<1, true>(p, pl.nblk, stream) : launch_nt<1, false>(p, pl.nblk, stream);
+  return paged ? launch_nt<2, true>(p, pl.nblk, stream) : launch_nt<2, false>(p, pl.nblk, stream);
 }
 
 size_t attn_record_floats(int nt) { return nt == 1 ? RowBlock<1>::kRec : RowBlock<2>::kRec; }

@@ -114,6 +114,7 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
   p.nq = nq;
   p.R = pl.R;
   p.n_rb = pl.n_rb;
+  p.n_rg = pl.n_rg;
   p.nsplit_g = pl.nsplit_g;
   p.kps_g = pl.kps_g;
   p.nsplit_f = pl.nsplit_f;
@@ -124,7 +125,7 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
   p.max_roff = (uint32_t)((kv_extent(kv) - BD_HEAD_DIM) >> 3);
   p.counters = static_cast<uint32_t*>(ws);
   p.part = pl.record_bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + pl.counter_bytes) : nullptr;
-  return launched(bd::launch_attn(p, pl.nt, kv->page_table != nullptr, pl.nblk, stream));
+  return launched(bd::launch_attn(p, pl, kv->page_table != nullptr, stream));
 }
 
 }  // namespace

@@ -28,6 +28,7 @@ struct AttnParams {
   int32_t nq;               // query rows per head (1, gamma+1 or C)
   int32_t R;                // rows per (s, g): nq * G
   int32_t n_rb;             // row blocks of 16*NT rows
+  int32_t n_rg;             // block mode: row groups of 8 row blocks (otherwise n_rb)
   int32_t nsplit_g, kps_g;  // gathered units: splits and entries per split
   int32_t nsplit_f, kps_f;  // full units: splits and keys per split
   int32_t units_g;          // gathered units (their blocks come first)
@@ -40,6 +41,8 @@ struct AttnParams {
 
 struct AttnPlan {
   int nt, n_rb, R;
+  bool block;               // block mode: 8 waves, one 32-row block each, sharing every K/V tile
+  int n_rg;
   int nsplit_g, kps_g, nsplit_f, kps_f;
   int units_g, units_f, nblk;
   size_t counter_bytes, record_bytes, ws_bytes;
@@ -49,7 +52,7 @@ struct AttnPlan {
 // bounds its splits).  The plan of a paged cache has at least as many splits as that of a
 // contiguous one, so workspace queries that do not know the layout use paged = true.
 AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full, bool paged);
-hipError_t launch_attn(const AttnParams& p, int nt, bool paged, int nblocks, hipStream_t stream);
+hipError_t launch_attn(const AttnParams& p, const AttnPlan& pl, bool paged, hipStream_t stream);
 size_t attn_record_floats(int nt);
 
 // ---- greedy acceptance -----------------------------------------------------
