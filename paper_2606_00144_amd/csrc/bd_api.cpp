@@ -195,7 +195,7 @@ bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_
   char* w = static_cast<char*>(ws) + BD_WS_COUNTER_BYTES;   // the counter region stays untouched
   p.stats = reinterpret_cast<float*>(w);
   p.raw_part = reinterpret_cast<float*>(w + pl.stats_bytes);
-  p.raw = scores_out ? scores_out : reinterpret_cast<float*>(w + pl.stats_bytes + pl.raw_part_bytes);
+  p.raw = scores_out;   // nullable: the total scores are exported only on request
   p.idx_out = idx_out;
   p.nsel_out = nsel_out;
   return launched(bd::launch_select(p, kv->page_table != nullptr, stream));

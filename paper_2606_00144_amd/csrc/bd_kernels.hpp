@@ -94,14 +94,14 @@ struct SelectParams {
   uint32_t max_roff;        // largest valid row offset of the K layout, 16-byte units
   float* stats;             // [S][Hkv][n_rb][nsplit][128][2] per-split row max / sum
   float* raw_part;          // [S][Hkv][n_rb][max_L] per-row-block column sums
-  float* raw;               // [S][Hkv][max_L] total raw scores (scores_out or workspace)
+  float* raw;               // nullable [S][Hkv][max_L] total raw scores (the caller's scores_out)
   int32_t* idx_out;         // [S][Hkv][budget]
   int32_t* nsel_out;        // [S]
 };
 
 struct SelectPlan {
   int n_rb, nsplit, kps;
-  size_t stats_bytes, raw_part_bytes, raw_bytes, ws_bytes;
+  size_t stats_bytes, raw_part_bytes, ws_bytes;
 };
 
 // `paged`: the cache is paged (its splits then go through a slot table of bounded size); workspace

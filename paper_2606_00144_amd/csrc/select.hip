@@ -352,25 +352,28 @@ __device__ inline int block_exclusive_scan(int x, int* wsum, int& total) {
   return before;
 }
 
-// Add one to bin `d` of this wave's histogram.  When every active lane of the wave holds the same
-// digit (the common case for the leading digits, which the scores mostly share) one lane adds the
-// count, so the LDS atomics never serialise on a single bin.
-__device__ inline void hist_add(uint32_t* wave_hist, uint32_t d) {
+// Add one to bin `d` of the histogram.  When every active lane of the wave holds the same digit
+// (the common case for the leading digits, which the scores mostly share) one lane adds the count,
+// so the LDS atomics do not serialise on a single bin.
+__device__ inline void hist_add(uint32_t* hist, uint32_t d) {
   const uint64_t active = __builtin_amdgcn_read_exec();
   const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
   const uint64_t same = __builtin_amdgcn_ballot_w64(d == d0);
   if (same == active) {
     if ((uint32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(active >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)active, 0u)) == 0u)
-      atomicAdd(&wave_hist[d0], (uint32_t)__builtin_popcountll(active));
+      atomicAdd(&hist[d0], (uint32_t)__builtin_popcountll(active));
   } else {
-    atomicAdd(&wave_hist[d], 1u);
+    atomicAdd(&hist[d], 1u);
   }
 }
+
+template <int V>
+struct IntTag { static constexpr int value = V; };
 
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
   constexpr int kTopkWaves = kTopkThreads / kWave;
   __shared__ float raw_lds[BD_SELECT_MAX_PREFIX];     // the pooled range, staged once
-  __shared__ uint32_t hist[kTopkWaves][256];          // one histogram per wave, summed per pass
+  __shared__ uint32_t hist[256];
   __shared__ int wsum[kTopkWaves];
   __shared__ uint32_t s_digit, s_krem;
   const int tid = threadIdx.x;
@@ -387,56 +390,89 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
   }
   if (g == 0 && tid == 0) p.nsel_out[s] = B;
 
-  // 1. total raw scores (row blocks summed in order); the prefix [0, N) is also staged in LDS
+  // 1. total raw scores (row blocks summed in order), staged in LDS over the prefix [0, N) and
+  // exported when the caller asked for them; each batch of loads is issued before any is summed
   const int N = L - W, K = B - W, rad = p.pool_kernel / 2;
-  float* raw = p.raw + (int64_t)pair * p.max_L;
+  float* raw = p.raw ? p.raw + (int64_t)pair * p.max_L : nullptr;
   const float* part = p.raw_part + (int64_t)pair * p.n_rb * p.max_L;
-  for (int t = tid; t < L; t += kTopkThreads) {
-    float v = 0.f;
-    for (int r = 0; r < p.n_rb; ++r) v += part[(int64_t)r * p.max_L + t];
-    raw[t] = v;
-    if (t < N) raw_lds[t] = v;
+  for (int c0 = 0; c0 < L; c0 += kMaxPerThread * kTopkThreads) {
+    float v[kMaxPerThread];
+#pragma unroll
+    for (int e = 0; e < kMaxPerThread; ++e) {
+      const int t = c0 + tid + e * kTopkThreads;
+      v[e] = t < L ? part[t] : 0.f;
+    }
+    for (int r = 1; r < p.n_rb; ++r) {
+#pragma unroll
+      for (int e = 0; e < kMaxPerThread; ++e) {
+        const int t = c0 + tid + e * kTopkThreads;
+        if (t < L) v[e] += part[(int64_t)r * p.max_L + t];
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < kMaxPerThread; ++e) {
+      const int t = c0 + tid + e * kTopkThreads;
+      if (t < N) raw_lds[t] = v[e];
+      if (raw && t < L) raw[t] = v[e];
+    }
   }
   __syncthreads();
 
-  // 2. pooled keys of this thread's contiguous segment of the prefix [0, N)
+  // 2. pooled keys of this thread's contiguous segment [t0, t0 + E) of the prefix [0, N): the max
+  // over [t - rad, t + rad] cut to [0, N).  Scores are >= 0, so positions outside count as -1.
   const int E = (N + kTopkThreads - 1) / kTopkThreads;
   const int t0 = tid * E;
   uint32_t key[kMaxPerThread];
+  auto raw_at = [&](int t) { return t >= 0 && t < N ? raw_lds[t] : -1.f; };
+  // small radii: the thread's window of raw values in registers, every load issued before any max
+  auto pool_window = [&](auto rad_tag) {
+    constexpr int R = decltype(rad_tag)::value;
+    float w[kMaxPerThread + 2 * R];
 #pragma unroll
-  for (int e = 0; e < kMaxPerThread; ++e) {
-    const int t = t0 + e;
-    uint32_t k = 0;
-    if (e < E && t < N) {
-      const int lo = t - rad < 0 ? 0 : t - rad;
-      const int hi = t + rad > N - 1 ? N - 1 : t + rad;
-      float m = raw_lds[lo];
-      for (int u = lo + 1; u <= hi; ++u) m = fmaxf(m, raw_lds[u]);
-      k = __float_as_uint(m);                // m >= 0: bit patterns order like values
+    for (int i = 0; i < kMaxPerThread + 2 * R; ++i) w[i] = i < E + 2 * R ? raw_at(t0 - R + i) : -1.f;
+#pragma unroll
+    for (int e = 0; e < kMaxPerThread; ++e) {
+      float m = w[e + R];
+#pragma unroll
+      for (int d = 1; d <= R; ++d) m = fmaxf(m, fmaxf(w[e + R - d], w[e + R + d]));
+      key[e] = e < E && t0 + e < N ? __float_as_uint(m) : 0u;   // m >= 0: bits order like values
     }
-    key[e] = k;
+  };
+  if (rad == 3) {
+    pool_window(IntTag<3>{});
+  } else if (rad == 2) {
+    pool_window(IntTag<2>{});
+  } else if (rad == 1) {
+    pool_window(IntTag<1>{});
+  } else if (rad == 0) {
+    pool_window(IntTag<0>{});
+  } else {
+    float m[kMaxPerThread];
+#pragma unroll
+    for (int e = 0; e < kMaxPerThread; ++e) m[e] = -1.f;
+    for (int d = -rad; d <= rad; ++d) {
+#pragma unroll
+      for (int e = 0; e < kMaxPerThread; ++e)
+        if (e < E) m[e] = fmaxf(m[e], raw_at(t0 + e + d));
+    }
+#pragma unroll
+    for (int e = 0; e < kMaxPerThread; ++e) key[e] = e < E && t0 + e < N ? __float_as_uint(m[e]) : 0u;
   }
 
   // 3. radix select of the K-th largest key; krem = how many keys equal to it are taken
   uint32_t prefix = 0, pmask = 0, krem = (uint32_t)K;
   if (K > 0) {
-    uint32_t* my_hist = hist[threadIdx.x / kWave];
     for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int i = tid; i < kTopkWaves * 256; i += kTopkThreads) (&hist[0][0])[i] = 0;
+      if (tid < 256) hist[tid] = 0;
       __syncthreads();
 #pragma unroll
       for (int e = 0; e < kMaxPerThread; ++e)
-        if (e < E && t0 + e < N && (key[e] & pmask) == prefix) hist_add(my_hist, (key[e] >> shift) & 255u);
+        if (e < E && t0 + e < N && (key[e] & pmask) == prefix) hist_add(hist, (key[e] >> shift) & 255u);
       __syncthreads();
       if (tid < kWave) {
         uint32_t h[4], c = 0;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          uint32_t v = 0;
-          for (int w = 0; w < kTopkWaves; ++w) v += hist[w][255 - (4 * tid + q)];
-          h[q] = v;
-          c += v;
-        }
+        for (int q = 0; q < 4; ++q) { h[q] = hist[255 - (4 * tid + q)]; c += h[q]; }
         uint32_t incl = c;
 #pragma unroll
         for (int o = 1; o < kWave; o <<= 1) {
@@ -520,8 +556,7 @@ SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L, bool paged) {
   pl.nsplit = max_L > 0 ? (int)((max_L + kps - 1) / kps) : 1;
   pl.stats_bytes = align256(sizeof(float) * (size_t)units * pl.nsplit * kStatRows * 2);
   pl.raw_part_bytes = align256(sizeof(float) * (size_t)units * max_L);
-  pl.raw_bytes = align256(sizeof(float) * (size_t)S * Hkv * max_L);
-  pl.ws_bytes = BD_WS_COUNTER_BYTES + pl.stats_bytes + pl.raw_part_bytes + pl.raw_bytes;
+  pl.ws_bytes = BD_WS_COUNTER_BYTES + pl.stats_bytes + pl.raw_part_bytes;
   return pl;
 }
 

@@ -33,9 +33,9 @@ def _run_select(k, q_win, lens, Hq, W, B, page_table=None, kdev=None, **kw):
     return idx.cpu().numpy(), nsel.cpu().numpy(), scores.cpu().numpy()
 
 
-def _check(k, q_win, lens, Hq, W, B, what, **kw):
-    gi, gn, gs = _run_select(k, q_win, lens, Hq, W, B, **kw)
-    oi, on, oraw = O.select_kv(k, q_win, lens, Hq, W, B)
+def _check(k, q_win, lens, Hq, W, B, what, pool_kernel=7, **kw):
+    gi, gn, gs = _run_select(k, q_win, lens, Hq, W, B, pool_kernel=pool_kernel, **kw)
+    oi, on, oraw = O.select_kv(k, q_win, lens, Hq, W, B, pool_kernel=pool_kernel)
     assert np.array_equal(gn, on), what
     S, Hkv = gi.shape[:2]
     near = 0
@@ -46,7 +46,7 @@ def _check(k, q_win, lens, Hq, W, B, what, **kw):
                 assert np.array_equal(gi[s, g], oi[s, g]), (what, s, g)
                 continue
             # (i) exact top-B on the GPU's own scores
-            sel, _ = O.topk_from_scores(gs[s, g, :L].astype(np.float64), L, W, B)
+            sel, _ = O.topk_from_scores(gs[s, g, :L].astype(np.float64), L, W, B, pool_kernel=pool_kernel)
             assert np.array_equal(gi[s, g], sel), (what, "top-B stage", s, g)
             # raw scores: each row sums to 1, so the total is W*G
             G = Hq // Hkv
@@ -55,7 +55,7 @@ def _check(k, q_win, lens, Hq, W, B, what, **kw):
             # (ii) end to end, differences only inside the near-tie band
             diff = set(gi[s, g].tolist()) ^ set(oi[s, g].tolist())
             if diff:
-                pooled = O.max_pool(oraw[s][g][:L - W], 7)
+                pooled = O.max_pool(oraw[s][g][:L - W], pool_kernel)
                 thr = np.sort(pooled)[::-1][B - W - 1]
                 for t in diff:
                     assert abs(pooled[t] - thr) <= DELTA * thr, (what, s, g, t, pooled[t], thr)
@@ -76,6 +76,18 @@ def test_select_config1_budgets(B):
     qt, k, v = config_data(1)
     near = _check(k, qt[:, -cfg.window:], [cfg.seq_len], cfg.num_q_heads, cfg.window, B, f"cfg1 B={B}")
     assert near <= 2
+
+
+@pytest.mark.parametrize("pool_kernel", [1, 3, 5, 7, 9])
+def test_select_pool_kernels(pool_kernel):
+    # every pooling path of the top-B kernel: register windows (radius 0..3) and the general loop
+    S, Hkv, Hq, W = 2, 2, 8, 32
+    lens = [3000, 1337]
+    g = np.random.default_rng(7)
+    k = synth.f32_to_bf16_bits(g.standard_normal((S, Hkv, max(lens), 128)).astype(np.float32))
+    q = synth.f32_to_bf16_bits(g.standard_normal((S, W, Hq, 128)).astype(np.float32))
+    near = _check(k, q, lens, Hq, W, 300, f"pool {pool_kernel}", pool_kernel=pool_kernel)
+    assert near <= 1
 
 
 def test_select_zero_keys_exact_and_identity():
