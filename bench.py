@@ -13,6 +13,11 @@ gamma = 5; vocab 128,256.  A step is one pass of Alg. 2's per-round work:
 The drafter and the verifier have separate caches of the same shape.  The step
 is captured once in a HIP graph and replayed; inputs stay resident in HBM.
 Prints one JSON line.
+
+`--op select` and `--op multiview` time the other two operations of the path on
+their own workloads instead (selection at the same 16K batch; the multi-view
+block at 4 sequences x 8,192 tokens, C = 64, four budgets), each as one JSON
+line of the same form.
 """
 from __future__ import annotations
 
@@ -37,6 +42,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--budget", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--op", choices=("step", "select", "multiview"), default="step")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only copy 512 MiB device-to-device five times (counter calibration: known bytes)")
     return ap.parse_args()
@@ -116,6 +122,10 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": x.numel() * 4, "copies": 5}), flush=True)
         return
+    if args.op == "select":
+        return bench_select(args, bd, synth, torch, np, dev)
+    if args.op == "multiview":
+        return bench_multiview(args, bd, synth, torch, np, dev)
     cfg = synth.CONFIGS[2]
     S, Hq, Hkv, L, W, gamma, V = (cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.window,
                                   cfg.gamma, cfg.vocab)
@@ -260,6 +270,98 @@ def main():
         log("timing the fp64 oracle on the host (one step)")
         result["cpu_baseline"] = cpu_baseline(host, S, Hq, L, B, gamma)
     print(json.dumps(result), flush=True)
+
+
+def _bf(torch, np, bits, dev):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+
+
+def _time_calls(torch, fn, steps, warmup):
+    """Mean µs per call over `steps` back-to-back eager calls (events on the calls' stream)."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        fn()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) * 1e3 / steps
+
+
+def bench_select(args, bd, synth, torch, np, dev):
+    """bd_select_kv on the 16K batch (8 x 16,384, W = 32, pool 7, B = --budget)."""
+    cfg = synth.CONFIGS[2]
+    S, Hq, Hkv, L, W, B = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.window, args.budget
+    log("generating inputs")
+    qs, kS, _ = synth.kv_batch(cfg)
+    k = _bf(torch, np, np.stack(kS), dev)
+    q_win = _bf(torch, np, np.stack(qs)[:, -W:], dev)
+    lens = torch.full((S,), L, dtype=torch.int32, device=dev)
+    ws = bd.Workspace()
+    steps = max(1, min(args.steps, 50))
+    us = _time_calls(torch, lambda: bd.bd_select_kv(k, q_win, lens, B, workspace=ws), steps, min(args.warmup, 5))
+    alg = S * Hkv * L * 128 * 2 + S * W * Hq * 128 * 2 + S * Hkv * B * 4     # K once, window queries, idx
+    gbs = alg / (us * 1e-6) / 1e9
+    print(json.dumps({
+        "metric": "bd_select_kv µs/call and HBM GB/s at 16K ctx (8 seqs, W=32, pool 7)", "value": round(us, 2),
+        "unit": "us/call", "n_gpus": 1, "steps": steps, "warmup": min(args.warmup, 5),
+        "ms_per_step": round(us / 1e3, 5), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded N(0,1) bf16 K/Q with 0.5% planted heavy hitters)",
+        "config": {"workload": f"select-16k-b8: 8 seqs x {L} ctx, {Hq}/{Hkv} heads, W={W}, B={B}",
+                   "num_seqs": S, "seq_len": L, "budget": B},
+        "roofline": {"bound": "hbm", "kernel": "bd_select_kv (two scoring passes + top-B)",
+                     "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "bytes_per_call": alg},
+    }), flush=True)
+
+
+def bench_multiview(args, bd, synth, torch, np, dev):
+    """bd_multiview_attn on the multi-view block (4 x 8,192, C = 64, four budgets, views from bd_select_kv)."""
+    cfg = synth.CONFIGS[3]
+    S, Hq, Hkv, L, C = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.block_len
+    G = Hq // Hkv
+    budgets = [int(b) for b in synth.view_budgets(cfg)]
+    log("generating inputs")
+    qs, ks, vs = synth.kv_batch(cfg)
+    k, v = _bf(torch, np, np.stack(ks), dev), _bf(torch, np, np.stack(vs), dev)
+    q_blk = _bf(torch, np, np.stack(qs)[:, -C:], dev)
+    lens = torch.full((S,), L, dtype=torch.int32, device=dev)
+    ld = max(budgets)
+    idx = torch.full((len(budgets), S, Hkv, ld), -1, dtype=torch.int32, device=dev)
+    nsel = torch.empty((len(budgets), S), dtype=torch.int32, device=dev)
+    for i, Bv in enumerate(budgets):                       # each view is the selection at its budget
+        vi, vn = bd.bd_select_kv(k, q_blk, lens, Bv)
+        idx[i, :, :, :Bv] = vi
+        nsel[i] = vn
+    ws = bd.Workspace()
+    steps = max(1, min(args.steps, 50))
+    fn = lambda: bd.bd_multiview_attn(k, v, q_blk, idx, nsel, lens, workspace=ws)
+    us = _time_calls(torch, fn, steps, min(args.warmup, 5))
+    # algorithmic flops: 4 * 128 per (query row, visible key), full branch and every view
+    pos = np.arange(L - C, L)
+    idx_h = idx.cpu().numpy()
+    full_pairs = S * Hkv * G * int((pos + 1).sum())
+    view_pairs = 0
+    for i, Bv in enumerate(budgets):
+        for s in range(S):
+            for g in range(Hkv):
+                t = np.sort(idx_h[i, s, g, :Bv])
+                view_pairs += G * int(np.searchsorted(t, pos, side="right").sum())
+    flops = 4 * 128 * (full_pairs + view_pairs)
+    tflops = flops / (us * 1e-6) / 1e12
+    print(json.dumps({
+        "metric": "bd_multiview_attn µs/call at 8K ctx (4 seqs, C=64, 4 views + full)", "value": round(us, 2),
+        "unit": "us/call", "n_gpus": 1, "steps": steps, "warmup": min(args.warmup, 5),
+        "ms_per_step": round(us / 1e3, 5), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded N(0,1) bf16 K/V/Q with 1% planted heavy hitters)",
+        "config": {"workload": f"multiview-train-b4-8k: 4 seqs x {L} ctx, {Hq}/{Hkv} heads, C={C}, budgets {budgets}",
+                   "num_seqs": S, "seq_len": L, "block_len": C, "budgets": budgets},
+        "roofline": {"bound": "mfma", "kernel": "block_kernel (views + full branch)", "achieved": round(tflops, 1),
+                     "peak": 2500.0, "unit": "TFLOP/s", "frac": round(tflops / 2500.0, 4), "traffic": None,
+                     "flops_per_call": flops},
+    }), flush=True)
 
 
 if __name__ == "__main__":

@@ -1059,19 +1059,29 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
   constexpr int64_t kStep = kWaves * kTile;       // one tile per wave of the split kernel
   auto round_up = [](int64_t x, int64_t m) { return (x + m - 1) / m * m; };
   const int64_t work = (int64_t)pl.units_g * ld_idx + (int64_t)pl.units_f * max_L;
+  const int64_t g_all = round_up(ld_idx > 0 ? ld_idx : 1, kStep), f_all = round_up(max_L > 0 ? max_L : 1, kStep);
+  // keys per split: the smallest multiple of kStep from work/kTargetBlocks up that keeps the
+  // launch to one workgroup per CU (every kernel here holds one workgroup per CU), so no second
+  // wave of workgroups forms a tail.  The gathered splits are bound by the slot table, and so is
+  // the full branch of a paged cache; the full branch over a contiguous cache computes its row
+  // offsets and is not.
   int64_t kps = round_up((work + kTargetBlocks - 1) / kTargetBlocks, kStep);
   if (kps < kStep) kps = kStep;
-  int64_t kg = kps < round_up(ld_idx > 0 ? ld_idx : 1, kStep) ? kps : round_up(ld_idx > 0 ? ld_idx : 1, kStep);
-  if (kg > kMaxSplitKeys) kg = kMaxSplitKeys;
-  int64_t kf = kps < round_up(max_L > 0 ? max_L : 1, kStep) ? kps : round_up(max_L > 0 ? max_L : 1, kStep);
-  // the full branch over a contiguous cache computes its row offsets, so its splits are not bound
-  // by the slot table
-  if (paged && kf > kMaxSplitKeys) kf = kMaxSplitKeys;
+  int64_t kg, kf, blocks;
+  for (;;) {
+    kg = kps < g_all ? kps : g_all;
+    if (kg > kMaxSplitKeys) kg = kMaxSplitKeys;
+    kf = kps < f_all ? kps : f_all;
+    if (paged && kf > kMaxSplitKeys) kf = kMaxSplitKeys;
+    blocks = (int64_t)pl.units_g * ((g_all + kg - 1) / kg) + (int64_t)pl.units_f * ((f_all + kf - 1) / kf);
+    if (blocks <= kTargetBlocks || (kps >= g_all && kps >= f_all)) break;
+    kps += kStep;
+  }
   pl.kps_g = (int)kg;
   pl.kps_f = (int)kf;
   pl.nsplit_g = ld_idx > 0 ? (int)((ld_idx + kg - 1) / kg) : 1;
   pl.nsplit_f = max_L > 0 ? (int)((max_L + kf - 1) / kf) : 1;
-  const int64_t blocks = (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f;
+  blocks = (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f;
   pl.nblk = (int)blocks;
   pl.counter_bytes = BD_WS_COUNTER_BYTES;   // fixed: scratch of any call never lands on a counter
   const bool split = (pl.units_g && pl.nsplit_g > 1) || (pl.units_f && pl.nsplit_f > 1);
@@ -1095,6 +1105,12 @@ hipError_t launch_attn(const AttnParams& p, const AttnPlan& pl, bool paged, hipS
   }
   if (pl.nt == 1) return paged ? launch_nt<1, true>(p, pl.nblk, stream) : launch_nt<1, false>(p, pl.nblk, stream);
   return paged ? launch_nt<2, true>(p, pl.nblk, stream) : launch_nt<2, false>(p, pl.nblk, stream);
+}
+
+size_t attn_ws_bytes(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full) {
+  const size_t a = plan_attn(S, Hkv, Hq, nq, num_views, ld_idx, max_L, with_full, true).ws_bytes;
+  const size_t b = plan_attn(S, Hkv, Hq, nq, num_views, ld_idx, max_L, with_full, false).ws_bytes;
+  return a > b ? a : b;
 }
 
 size_t attn_record_floats(int nt) { return nt == 1 ? RowBlock<1>::kRec : RowBlock<2>::kRec; }

@@ -205,7 +205,7 @@ bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_
 size_t bd_sparse_decode_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
                                              int32_t ld_idx) {
   if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || ld_idx < 0) return 0;
-  return bd::plan_attn(num_seqs, num_kv_heads, num_q_heads, 1, 1, ld_idx, 0, false, true).ws_bytes;
+  return bd::attn_ws_bytes(num_seqs, num_kv_heads, num_q_heads, 1, 1, ld_idx, 0, false);
 }
 
 bd_status bd_sparse_decode_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, const int32_t* idx,
@@ -229,9 +229,8 @@ size_t bd_multiview_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads,
   if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || block_len < 1 || num_views < 0 || ld_idx < 0 ||
       max_seq_len < 0)
     return 0;
-  return bd::plan_attn(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld_idx, max_seq_len, with_full != 0,
-                       true)
-      .ws_bytes;
+  return bd::attn_ws_bytes(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld_idx, max_seq_len,
+                           with_full != 0);
 }
 
 bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t num_q_heads, int32_t block_len,
@@ -257,7 +256,7 @@ bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t
 size_t bd_verify_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads, int32_t gamma,
                                       int32_t max_seq_len) {
   if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || gamma < 0 || max_seq_len < 0) return 0;
-  return bd::plan_attn(num_seqs, num_kv_heads, num_q_heads, gamma + 1, 0, 0, max_seq_len, true, true).ws_bytes;
+  return bd::attn_ws_bytes(num_seqs, num_kv_heads, num_q_heads, gamma + 1, 0, 0, max_seq_len, true);
 }
 
 bd_status bd_verify_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, int32_t gamma, float scale,

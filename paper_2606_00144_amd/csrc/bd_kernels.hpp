@@ -49,11 +49,13 @@ struct AttnPlan {
 };
 
 // `paged`: the cache is paged (the full branch then also goes through the slot table, which
-// bounds its splits).  The plan of a paged cache has at least as many splits as that of a
-// contiguous one, so workspace queries that do not know the layout use paged = true.
+// bounds its splits).  Workspace queries that do not know the layout take the larger of the two
+// plans (attn_ws_bytes).
 AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full, bool paged);
 hipError_t launch_attn(const AttnParams& p, const AttnPlan& pl, bool paged, hipStream_t stream);
 size_t attn_record_floats(int nt);
+// Workspace bytes that serve either layout (paged or contiguous) of the given shape.
+size_t attn_ws_bytes(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full);
 
 // ---- greedy acceptance -----------------------------------------------------
 struct AcceptParams {
