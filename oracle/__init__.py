@@ -11,6 +11,9 @@ from .bd_oracle import (  # noqa: F401
     max_pool,
     topk_from_scores,
     select_kv,
+    chunk_scores,
+    topk_chunks_from_scores,
+    select_kv_chunks,
     sparse_decode_attn,
     verify_attn,
     multiview_attn,

@@ -182,6 +182,82 @@ def select_kv(k, q_win, seq_lens, num_q_heads: int, window: int, budget: int, po
     return idx, nsel, raws
 
 
+def chunk_scores(raw_prefix: np.ndarray, chunk: int) -> np.ndarray:
+    """Score of every chunk of the prefix: the sum of its positions' cumulative attention weight.
+
+    Sec. 3.4 partitions the prefix cache into chunks of ``chunk`` positions and scores each
+    chunk by cumulative attention weight.  Chunk c covers [c*chunk, min((c+1)*chunk, N)); the
+    last chunk is shorter when N is not a multiple of ``chunk``.
+    """
+    x = np.asarray(raw_prefix, dtype=np.float64)
+    N = x.shape[0]
+    nc = (N + chunk - 1) // chunk
+    out = np.zeros(nc, dtype=np.float64)
+    for c in range(nc):
+        out[c] = x[c * chunk:min((c + 1) * chunk, N)].sum()
+    return out
+
+
+def topk_chunks_from_scores(raw: np.ndarray, L: int, window: int, budget: int,
+                            chunk: int = 8) -> Tuple[np.ndarray, np.ndarray]:
+    """TopKChunks (Sec. 3.4; Alg. 1 step 4, Alg. 2 "sparsify"): the chunk-level selection.
+
+    The prefix [0, N), N = L - W, is cut into chunks of ``chunk`` positions; the top
+    floor((B - W) / chunk) chunks by score are kept (larger score first, lower chunk index
+    among equal scores) and their positions returned in ascending order, then the W window
+    positions (reading: B counts the window, as in the token-level policy; a kept short last
+    chunk contributes fewer than ``chunk`` positions).  Returns (positions, chunk scores).
+    """
+    N = L - window
+    cs = chunk_scores(raw[:N], chunk)
+    nc = cs.shape[0]
+    keep = max(0, min((budget - window) // chunk, nc))
+    order = np.lexsort((np.arange(nc), -cs))            # primary: -score, secondary: chunk index
+    chosen = np.sort(order[:keep])
+    parts = [np.arange(c * chunk, min((c + 1) * chunk, N)) for c in chosen]
+    sel = np.concatenate(parts + [np.arange(N, L)]).astype(np.int32)
+    return sel, cs
+
+
+def select_kv_chunks(k, q_win, seq_lens, num_q_heads: int, window: int, budget: int, chunk: int = 8,
+                     scale: Optional[float] = None):
+    """K_S^sp(B) by TopKChunks per (sequence, KV head): scoring as select_kv, chunk selection.
+
+    Returns idx [S][Hkv][B] int32 (slots past a head's kept positions hold -1), nsel [S]
+    (B, or L_s when B >= L_s) and the raw scores.  B >= L_s keeps every position.
+    """
+    if window < 1 or budget < window or chunk < 1:
+        raise ValueError("invalid selection arguments")
+    S = len(seq_lens)
+    Hkv = k[0].shape[0]
+    G = num_q_heads // Hkv
+    D = k[0].shape[-1]
+    sc = _scale64(scale, D)
+    idx = np.full((S, Hkv, budget), -1, dtype=np.int32)
+    nsel = np.zeros(S, dtype=np.int32)
+    raws = []
+    for s in range(S):
+        L = int(seq_lens[s])
+        if window > L:
+            raise ValueError("window longer than the sequence")
+        qw = bf16_to_f64(q_win[s])
+        raw_s = np.zeros((Hkv, L))
+        if budget >= L:
+            idx[s, :, :L] = np.arange(L, dtype=np.int32)
+            nsel[s] = L
+            raws.append(raw_s)
+            continue
+        for g in range(Hkv):
+            kg = bf16_to_f64(k[s][g, :L])
+            raw = window_scores(kg, qw[:, g * G:(g + 1) * G, :], L, sc)
+            sel, _ = topk_chunks_from_scores(raw, L, window, budget, chunk)
+            idx[s, g, :sel.size] = sel
+            raw_s[g] = raw
+        nsel[s] = budget
+        raws.append(raw_s)
+    return idx, nsel, raws
+
+
 # --------------------------------------------------------------------------
 # Drafter decode attention over the selected entries (Eq. 2; Alg. 2 "draft")
 # --------------------------------------------------------------------------

@@ -272,6 +272,81 @@ def test_select_rejects_bad_arguments():
             O.select_kv(k, q[:, :max(W, 1)], [256], 8, W, B, P)
 
 
+# ---------------------------------------------------------------- chunk-level selection (TopKChunks)
+
+def test_chunk_scores_partition_the_prefix():
+    x = np.arange(1, 20, dtype=np.float64)            # 19 positions -> chunks of 8, 8, 3
+    cs = O.chunk_scores(x, 8)
+    assert cs.tolist() == [sum(range(1, 9)), sum(range(9, 17)), 17 + 18 + 19]
+    assert abs(cs.sum() - x.sum()) < 1e-12
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_topk_chunks_brute_force_tiny(seed):
+    g = np.random.default_rng(300 + seed)
+    L, W, s, B = 30, 4, 3, 13                         # prefix 26 -> 9 chunks (last has 2); keep 3 chunks
+    raw = np.round(g.random(L) * 3) / 3                # coarse values -> ties between chunk sums
+    sel, cs = O.topk_chunks_from_scores(raw, L, W, B, s)
+    nc, keep = 9, (B - W) // s
+    # the kept set is the unique one ranking above every other chunk under (-score, index)
+    winners = [c for c in itertools.combinations(range(nc), keep)
+               if all((-cs[a], a) < (-cs[b], b) for a in c for b in set(range(nc)) - set(c))]
+    assert len(winners) == 1
+    want = [t for c in winners[0] for t in range(c * s, min((c + 1) * s, L - W))] + list(range(L - W, L))
+    assert sel.tolist() == want
+
+
+def test_topk_chunks_of_one_is_the_unpooled_token_selection():
+    g = np.random.default_rng(11)
+    L, W = 400, 16
+    raw = np.floor(g.random(L) * 40)
+    for B in [16, 50, 200]:
+        a, _ = O.topk_chunks_from_scores(raw, L, W, B, 1)
+        b, _ = O.topk_from_scores(raw, L, W, B, 1)
+        assert a.tolist() == b.tolist()
+
+
+def test_topk_chunks_ties_take_lowest_chunks_and_nest():
+    sel, _ = O.topk_chunks_from_scores(np.ones(40), 40, 8, 24, 8)   # 4 chunks tie: keep chunks 0, 1
+    assert sel.tolist() == list(range(16)) + list(range(32, 40))
+    g = np.random.default_rng(12)
+    raw = g.random(1000)
+    prev = None
+    for B in [32, 96, 288, 800]:
+        sel, cs = O.topk_chunks_from_scores(raw, 1000, 32, B, 8)
+        assert sel.size == 32 + 8 * ((B - 32) // 8)
+        if prev is not None:
+            assert set(prev) <= set(sel.tolist())
+        prev = sel.tolist()
+
+
+def test_select_chunks_zero_keys_and_spike():
+    _, q = _cfg_small()
+    k = np.zeros((1, 2, 256, 128), np.uint16)
+    idx, nsel, _ = O.select_kv_chunks(k, q, [256], 8, 16, 64, 8)     # equal scores: lowest 6 chunks
+    assert nsel[0] == 64 and np.all(idx[0] == np.r_[np.arange(48), np.arange(240, 256)])
+    L, W, t0 = 256, 16, 100
+    g = np.random.default_rng(9)
+    qs = np.zeros((1, W, 8, 128), np.float32); qs[..., 0] = 1.0
+    ks = 0.01 * g.standard_normal((1, 2, L, 128)).astype(np.float32)
+    ks[0, :, t0, 0] = 60.0
+    idx, _, _ = O.select_kv_chunks(bits(ks), bits(qs), [L], 8, W, 32, 8)
+    for gg in range(2):                                # the spike's chunk [96, 104) is kept first
+        assert set(range(96, 104)) <= set(idx[0, gg].tolist())
+    idx, nsel, _ = O.select_kv_chunks(k, q, [200], 8, 16, 300, 8)     # B >= L: identity
+    assert nsel[0] == 200 and np.all(idx[0, :, :200] == np.arange(200)) and np.all(idx[0, :, 200:] == -1)
+
+
+def test_select_chunks_short_last_chunk_and_tail():
+    # prefix of 21 positions: chunks of 8, 8, 5; the short chunk holds the spike and is kept
+    L, W = 29, 8
+    raw = np.full(L, 0.1)
+    raw[18] = 50.0
+    sel, cs = O.topk_chunks_from_scores(raw, L, W, 8 + 16, 8)
+    assert sel.tolist() == list(range(8)) + list(range(16, 21)) + list(range(21, 29))
+    assert cs.tolist() == pytest.approx([0.8, 0.8, 50.4])
+
+
 # ---------------------------------------------------------------- sparse decode (Eq. 2)
 
 def _kv(S, Hkv, L, seed, v_const=None):
