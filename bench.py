@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--budget", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--op", choices=("step", "select", "multiview"), default="step")
+    ap.add_argument("--chunk", type=int, default=0,
+                    help="--op select: 0 = token-level selection with pooling, s > 0 = TopKChunks with chunks of s")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only copy 512 MiB device-to-device five times (counter calibration: known bytes)")
     return ap.parse_args()
@@ -301,15 +303,20 @@ def bench_select(args, bd, synth, torch, np, dev):
     lens = torch.full((S,), L, dtype=torch.int32, device=dev)
     ws = bd.Workspace()
     steps = max(1, min(args.steps, 50))
-    us = _time_calls(torch, lambda: bd.bd_select_kv(k, q_win, lens, B, workspace=ws), steps, min(args.warmup, 5))
+    if args.chunk > 0:
+        fn = lambda: bd.bd_select_kv_chunks(k, q_win, lens, B, chunk=args.chunk, workspace=ws)
+    else:
+        fn = lambda: bd.bd_select_kv(k, q_win, lens, B, workspace=ws)
+    us = _time_calls(torch, fn, steps, min(args.warmup, 5))
+    policy = f"TopKChunks s={args.chunk}" if args.chunk > 0 else "pool 7"
     alg = S * Hkv * L * 128 * 2 + S * W * Hq * 128 * 2 + S * Hkv * B * 4     # K once, window queries, idx
     gbs = alg / (us * 1e-6) / 1e9
     print(json.dumps({
-        "metric": "bd_select_kv µs/call and HBM GB/s at 16K ctx (8 seqs, W=32, pool 7)", "value": round(us, 2),
+        "metric": f"bd_select_kv µs/call and HBM GB/s at 16K ctx (8 seqs, W=32, {policy})", "value": round(us, 2),
         "unit": "us/call", "n_gpus": 1, "steps": steps, "warmup": min(args.warmup, 5),
         "ms_per_step": round(us / 1e3, 5), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic (seeded N(0,1) bf16 K/Q with 0.5% planted heavy hitters)",
-        "config": {"workload": f"select-16k-b8: 8 seqs x {L} ctx, {Hq}/{Hkv} heads, W={W}, B={B}",
+        "config": {"workload": f"select-16k-b8: 8 seqs x {L} ctx, {Hq}/{Hkv} heads, W={W}, B={B}, {policy}",
                    "num_seqs": S, "seq_len": L, "budget": B},
         "roofline": {"bound": "hbm", "kernel": "bd_select_kv (two scoring passes + top-B)",
                      "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

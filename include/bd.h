@@ -141,6 +141,28 @@ bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_
                        void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * bd_select_kv_chunks -- chunk-level selection (TopKChunks; Sec. 3.4, Alg. 1
+ * step 4, Alg. 2 "sparsify").
+ *
+ * Step 1 as bd_select_kv.  The prefix [0, N), N = L_s - W, is cut into chunks
+ * of `chunk` positions (chunk c covers [c*chunk, min((c+1)*chunk, N)); the last
+ * one is shorter when chunk does not divide N); a chunk's score is the sum of
+ * its positions' raw scores (fp32, left to right).  The floor((B - W) / chunk)
+ * chunks ranked first by (score descending, chunk index ascending) are kept:
+ * their positions in ascending order, then the W window positions.
+ * idx_out    [S][Hkv][budget] int32; a head's slots past its kept positions
+ *            (fewer than B when chunk does not divide B - W, or a short last
+ *            chunk is kept) are -1, which the attention calls skip.
+ * nsel_out   [S] int32: min(budget, L_s) (slots, not kept positions).
+ * Other arguments, requirements and the workspace are those of bd_select_kv
+ * (bd_select_kv_workspace_bytes); chunk >= 1.
+ * ---------------------------------------------------------------------- */
+bd_status bd_select_kv_chunks(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_heads, int32_t window,
+                              int32_t budget, int32_t chunk, float scale, const float* lse_win,
+                              int32_t* idx_out, int32_t* nsel_out, float* scores_out,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * bd_sparse_decode_attn -- drafter decode attention over K_S^sp(B) (Eq. 2; Alg. 2 "draft").
  *
  * One query per head at position L_s-1 attends the entries

@@ -27,7 +27,7 @@ import torch
 
 __all__ = [
     "BdError", "lib", "library_path", "kv_desc", "Workspace",
-    "bd_select_kv", "bd_sparse_decode_attn", "bd_multiview_attn", "bd_verify_attn", "bd_accept_len",
+    "bd_select_kv", "bd_select_kv_chunks", "bd_sparse_decode_attn", "bd_multiview_attn", "bd_verify_attn", "bd_accept_len",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -64,6 +64,7 @@ _SIGNATURES = {
     "bd_abi_version": (_I32, []),
     "bd_select_kv_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32]),
     "bd_select_kv": (_I32, [_KV, _P, _I32, _I32, _I32, _I32, _F32, _P, _P, _P, _P, _P, _SZ, _P]),
+    "bd_select_kv_chunks": (_I32, [_KV, _P, _I32, _I32, _I32, _I32, _F32, _P, _P, _P, _P, _P, _SZ, _P]),
     "bd_sparse_decode_attn_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32]),
     "bd_sparse_decode_attn": (_I32, [_KV, _P, _I32, _P, _I32, _P, _F32, _P, _P, _P, _SZ, _P]),
     "bd_multiview_attn_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32, _I32, _I32, _I32]),
@@ -189,6 +190,22 @@ def bd_select_kv(k: torch.Tensor, q_win: torch.Tensor, seq_lens: torch.Tensor, b
                  return_scores: bool = False, page_table: Optional[torch.Tensor] = None,
                  max_seq_len: Optional[int] = None, workspace: Optional[Workspace] = None):
     """Budgeted KV selection.  q_win: bf16 [S, W, Hq, 128].  Returns (idx [S,Hkv,B], nsel [S][, scores])."""
+    return _select("bd_select_kv", pool_kernel, k, q_win, seq_lens, budget, scale, lse_win, return_scores,
+                   page_table, max_seq_len, workspace)
+
+
+def bd_select_kv_chunks(k: torch.Tensor, q_win: torch.Tensor, seq_lens: torch.Tensor, budget: int, *,
+                        chunk: int = 8, scale: Optional[float] = None, lse_win: Optional[torch.Tensor] = None,
+                        return_scores: bool = False, page_table: Optional[torch.Tensor] = None,
+                        max_seq_len: Optional[int] = None, workspace: Optional[Workspace] = None):
+    """Chunk-level selection (TopKChunks).  Same arguments and results as bd_select_kv; a head's
+    unused idx slots hold -1."""
+    return _select("bd_select_kv_chunks", chunk, k, q_win, seq_lens, budget, scale, lse_win, return_scores,
+                   page_table, max_seq_len, workspace)
+
+
+def _select(entry, mode_arg, k, q_win, seq_lens, budget, scale, lse_win, return_scores, page_table, max_seq_len,
+            workspace):
     _require(q_win.dtype == torch.bfloat16 and q_win.dim() == 4 and q_win.is_contiguous(), "q_win must be contiguous bf16 [S,W,Hq,128]")
     kv = kv_desc(k, None, seq_lens, page_table, max_seq_len)
     S, W, Hq = q_win.shape[0], q_win.shape[1], q_win.shape[2]
@@ -201,8 +218,8 @@ def bd_select_kv(k: torch.Tensor, q_win: torch.Tensor, seq_lens: torch.Tensor, b
     L = lib()
     nb = L.bd_select_kv_workspace_bytes(S, kv.num_kv_heads, Hq, W, kv.max_seq_len)
     wp, wb = _ws("select", nb, dev, workspace)
-    _check(L.bd_select_kv(ctypes.byref(kv), q_win.data_ptr(), Hq, W, budget, pool_kernel, _scale(scale),
-                          _ptr(lse_win), idx.data_ptr(), nsel.data_ptr(), _ptr(scores), wp, wb, _stream()))
+    _check(getattr(L, entry)(ctypes.byref(kv), q_win.data_ptr(), Hq, W, budget, mode_arg, _scale(scale),
+                             _ptr(lse_win), idx.data_ptr(), nsel.data_ptr(), _ptr(scores), wp, wb, _stream()))
     return (idx, nsel, scores) if return_scores else (idx, nsel)
 
 

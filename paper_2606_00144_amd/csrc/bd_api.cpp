@@ -154,14 +154,18 @@ size_t bd_select_kv_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int3
   return bd::plan_select(num_seqs, num_kv_heads, num_q_heads, window, max_seq_len, true).ws_bytes;
 }
 
-bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_heads, int32_t window,
-                       int32_t budget, int32_t pool_kernel, float scale, const float* lse_win, int32_t* idx_out,
-                       int32_t* nsel_out, float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+namespace {
+// Common host path of both selection policies (chunk == 0: token level with pooling).
+bd_status run_select(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_heads, int32_t window, int32_t budget,
+                     int32_t pool_kernel, int32_t chunk, float scale, const float* lse_win, int32_t* idx_out,
+                     int32_t* nsel_out, float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream) {
   bd_status st = check_kv(kv, false, num_q_heads);
   if (st != BD_OK) return st;
   if (window < 1 || budget < window) return fail(BD_ERR_INVALID_ARG, "need 1 <= window <= budget (window %d, budget %d)", window, budget);
-  if (pool_kernel < 1 || pool_kernel % 2 == 0) return fail(BD_ERR_INVALID_ARG, "pool_kernel must be odd and >= 1");
-  if (pool_kernel > 255) return fail(BD_ERR_UNSUPPORTED, "pool_kernel above 255");
+  if (chunk < 0) return fail(BD_ERR_INVALID_ARG, "chunk must be >= 1");
+  if (chunk == 0 && (pool_kernel < 1 || pool_kernel % 2 == 0))
+    return fail(BD_ERR_INVALID_ARG, "pool_kernel must be odd and >= 1");
+  if (chunk == 0 && pool_kernel > 255) return fail(BD_ERR_UNSUPPORTED, "pool_kernel above 255");
   if (!std::isfinite(scale) || !(scale > 0.f)) return fail(BD_ERR_INVALID_ARG, "scale must be positive and finite");
   if (!q_win || !aligned(q_win, 16)) return fail(BD_ERR_INVALID_ARG, "q_win is NULL or not 16-byte aligned");
   if (!idx_out || !nsel_out) return fail(BD_ERR_INVALID_ARG, "idx_out and nsel_out are required");
@@ -184,7 +188,8 @@ bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_
   p.G = num_q_heads / kv->num_kv_heads;
   p.W = window;
   p.budget = budget;
-  p.pool_kernel = pool_kernel;
+  p.pool_kernel = chunk > 0 ? 1 : pool_kernel;
+  p.chunk = chunk;
   p.R = window * p.G;
   p.n_rb = pl.n_rb;
   p.nsplit = pl.nsplit;
@@ -199,6 +204,22 @@ bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_
   p.idx_out = idx_out;
   p.nsel_out = nsel_out;
   return launched(bd::launch_select(p, kv->page_table != nullptr, stream));
+}
+}  // namespace
+
+bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_heads, int32_t window,
+                       int32_t budget, int32_t pool_kernel, float scale, const float* lse_win, int32_t* idx_out,
+                       int32_t* nsel_out, float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return run_select(kv, q_win, num_q_heads, window, budget, pool_kernel, 0, scale, lse_win, idx_out, nsel_out,
+                    scores_out, ws, ws_bytes, stream);
+}
+
+bd_status bd_select_kv_chunks(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_heads, int32_t window,
+                              int32_t budget, int32_t chunk, float scale, const float* lse_win, int32_t* idx_out,
+                              int32_t* nsel_out, float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (chunk < 1) return fail(BD_ERR_INVALID_ARG, "chunk must be >= 1");
+  return run_select(kv, q_win, num_q_heads, window, budget, 1, chunk, scale, lse_win, idx_out, nsel_out,
+                    scores_out, ws, ws_bytes, stream);
 }
 
 // ---------------------------------------------------------------- sparse decode

@@ -88,6 +88,7 @@ struct SelectParams {
   const float* lse_win;     // nullable [S][W][Hq]
   int32_t S, Hkv, Hq, G, W;
   int32_t budget, pool_kernel;
+  int32_t chunk;            // 0: token-level selection with pooling; > 0: TopKChunks with this chunk size
   int32_t R;                // rows per (s, g): W * G
   int32_t n_rb;             // row blocks of 16*NT rows
   int32_t nsplit, kps;      // key splits of the scoring passes

@@ -418,9 +418,16 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
   }
   __syncthreads();
 
-  // 2. pooled keys of this thread's contiguous segment [t0, t0 + E) of the prefix [0, N): the max
-  // over [t - rad, t + rad] cut to [0, N).  Scores are >= 0, so positions outside count as -1.
-  const int E = (N + kTopkThreads - 1) / kTopkThreads;
+  // 2. the candidates: prefix positions [0, N) with max-pooled scores (token level), or the chunks
+  // of s positions of the prefix with their scores' sums (TopKChunks, chunk c covering
+  // [c*s, min((c+1)*s, N)), summed left to right in fp32).  This thread owns candidates
+  // [t0, t0 + E); the top KE of the M candidates are kept.  Scores are >= 0, so their float bits
+  // order like their values.
+  const int chunk = p.chunk;
+  const int M = chunk > 0 ? (N + chunk - 1) / chunk : N;
+  int KE = chunk > 0 ? K / chunk : K;
+  if (KE > M) KE = M;
+  const int E = (M + kTopkThreads - 1) / kTopkThreads;
   const int t0 = tid * E;
   uint32_t key[kMaxPerThread];
   auto raw_at = [&](int t) { return t >= 0 && t < N ? raw_lds[t] : -1.f; };
@@ -438,7 +445,18 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
       key[e] = e < E && t0 + e < N ? __float_as_uint(m) : 0u;   // m >= 0: bits order like values
     }
   };
-  if (rad == 3) {
+  if (chunk > 0) {
+#pragma unroll
+    for (int e = 0; e < kMaxPerThread; ++e) {
+      const int c = t0 + e;
+      float sum = 0.f;
+      if (e < E && c < M) {
+        const int b = c * chunk, n = N - b < chunk ? N - b : chunk;
+        for (int j = 0; j < n; ++j) sum += raw_lds[b + j];
+      }
+      key[e] = e < E && c < M ? __float_as_uint(sum) : 0u;
+    }
+  } else if (rad == 3) {
     pool_window(IntTag<3>{});
   } else if (rad == 2) {
     pool_window(IntTag<2>{});
@@ -459,15 +477,15 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
     for (int e = 0; e < kMaxPerThread; ++e) key[e] = e < E && t0 + e < N ? __float_as_uint(m[e]) : 0u;
   }
 
-  // 3. radix select of the K-th largest key; krem = how many keys equal to it are taken
-  uint32_t prefix = 0, pmask = 0, krem = (uint32_t)K;
-  if (K > 0) {
+  // 3. radix select of the KE-th largest key; krem = how many keys equal to it are taken
+  uint32_t prefix = 0, pmask = 0, krem = (uint32_t)KE;
+  if (KE > 0) {
     for (int shift = 24; shift >= 0; shift -= 8) {
       if (tid < 256) hist[tid] = 0;
       __syncthreads();
 #pragma unroll
       for (int e = 0; e < kMaxPerThread; ++e)
-        if (e < E && t0 + e < N && (key[e] & pmask) == prefix) hist_add(hist, (key[e] >> shift) & 255u);
+        if (e < E && t0 + e < M && (key[e] & pmask) == prefix) hist_add(hist, (key[e] >> shift) & 255u);
       __syncthreads();
       if (tid < kWave) {
         uint32_t h[4], c = 0;
@@ -494,30 +512,49 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
     }
   }
 
-  // 4. ordered compaction: all keys above the threshold, the first krem keys equal to it
-  int gt = 0, eq = 0;
+  // 4. ordered compaction: all candidates above the threshold, the first krem equal to it; a
+  // candidate contributes its positions (one, or its chunk's), in ascending order
+  auto positions = [&](int c) {
+    if (chunk == 0) return 1;
+    const int b = c * chunk;
+    return N - b < chunk ? N - b : chunk;
+  };
+  int eq = 0;
 #pragma unroll
   for (int e = 0; e < kMaxPerThread; ++e)
-    if (K > 0 && e < E && t0 + e < N) { gt += key[e] > prefix; eq += key[e] == prefix; }
+    if (KE > 0 && e < E && t0 + e < M) eq += key[e] == prefix;
   int tot;
   const int eq_before = block_exclusive_scan(eq, wsum, tot);
   int take_eq = (int)krem - eq_before;
   take_eq = take_eq < 0 ? 0 : (take_eq > eq ? eq : take_eq);
-  const int off0 = block_exclusive_scan(gt + take_eq, wsum, tot);
-  int off = off0, seen = 0;
+  int mine = 0, seen = 0;
+#pragma unroll
+  for (int e = 0; e < kMaxPerThread; ++e)
+    if (KE > 0 && e < E && t0 + e < M) {
+      const bool isq = key[e] == prefix;
+      if (key[e] > prefix || (isq && seen < take_eq)) mine += positions(t0 + e);
+      seen += isq;
+    }
+  int kept;                                   // prefix positions kept: K (token level), <= K (chunks)
+  const int off0 = block_exclusive_scan(mine, wsum, kept);
+  int off = off0;
+  seen = 0;
 #pragma unroll
   for (int e = 0; e < kMaxPerThread; ++e) {
-    const int t = t0 + e;
-    if (K > 0 && e < E && t < N) {
+    const int c = t0 + e;
+    if (KE > 0 && e < E && c < M) {
       const bool isq = key[e] == prefix;
       if (key[e] > prefix || (isq && seen < take_eq)) {
-        if (off < K) idx_row[off] = t;      // guard: never write past the B slots of this row
-        ++off;
+        const int n = positions(c), b = chunk > 0 ? c * chunk : c;
+        for (int j = 0; j < n; ++j, ++off)
+          if (off < K) idx_row[off] = b + j;   // guard: never write past the B - W prefix slots
       }
       seen += isq;
     }
   }
-  for (int i = tid; i < W; i += kTopkThreads) idx_row[K + i] = N + i;
+  if (kept > K) kept = K;
+  for (int i = tid; i < W; i += kTopkThreads) idx_row[kept + i] = N + i;
+  for (int i = kept + W + tid; i < B; i += kTopkThreads) idx_row[i] = -1;   // chunk mode: unused slots
 }
 
 template <int NT, bool PAGED>
