@@ -19,4 +19,6 @@ from .bd_oracle import (  # noqa: F401
     multiview_attn,
     greedy_argmax,
     accept_len,
+    cache_append,
+    cache_rollback,
 )

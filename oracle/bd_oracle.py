@@ -410,3 +410,59 @@ def accept_len(logits, draft, gamma: int):
         acc[s] = kk
         bonus[s] = am[s, kk]
     return acc, bonus, am
+
+
+# --------------------------------------------------------------------------
+# Per-round cache updates (Alg. 2: the drafter's sparse cache grows with the
+# drafted tokens; after verification both caches keep the accepted tokens)
+# --------------------------------------------------------------------------
+
+def cache_append(k, v, seq_lens, k_new, v_new, idx=None, nsel=None):
+    """Write n new rows per sequence at positions L_s .. L_s+n-1 and advance L_s.
+
+    k, v: [S][Hkv][cap][D] bf16 bits (copies are returned); k_new, v_new: [S][n][Hkv][D].
+    Rows at or past the capacity cap are dropped and L_s stops at cap.  With idx
+    [S][Hkv][ld] and nsel [S] (the drafter's sparse cache), each written position
+    is also appended to every head's index list at slots nsel[s] .. (dropped past
+    ld), and nsel advances by the number of appended slots.
+    Returns (k, v, seq_lens[, idx, nsel]).
+    """
+    k, v = np.array(k, copy=True), np.array(v, copy=True)
+    lens = np.array(seq_lens, dtype=np.int32, copy=True)
+    S, Hkv, cap = k.shape[0], k.shape[1], k.shape[2]
+    n = k_new.shape[1]
+    if idx is not None:
+        idx, nsel = np.array(idx, dtype=np.int32, copy=True), np.array(nsel, dtype=np.int32, copy=True)
+    for s in range(S):
+        L = int(lens[s])
+        rows = [i for i in range(n) if L + i < cap]
+        for i in rows:
+            for g in range(Hkv):
+                k[s, g, L + i] = k_new[s, i, g]
+                v[s, g, L + i] = v_new[s, i, g]
+        if idx is not None:
+            m = int(nsel[s])
+            slots = [j for j in range(len(rows)) if m + j < idx.shape[2]]
+            for j in slots:
+                idx[s, :, m + j] = L + rows[j]
+            nsel[s] = m + len(slots)
+        lens[s] = L + len(rows)
+    return (k, v, lens) if idx is None else (k, v, lens, idx, nsel)
+
+
+def cache_rollback(seq_lens, accept, spec: int, nsel=None):
+    """Drop the rejected speculative rows after verification (Alg. 2, cache update).
+
+    Each sequence ends in ``spec`` speculative rows, of which the first accept[s]
+    were accepted (accept is clamped to [0, spec]): spec - accept[s] rows are
+    dropped from L_s (and from nsel[s], the drafter's sparse list, when given),
+    never below zero.  Returns (seq_lens[, nsel]).
+    """
+    lens = np.array(seq_lens, dtype=np.int64)
+    acc = np.clip(np.asarray(accept, dtype=np.int64), 0, spec)
+    drop = spec - acc
+    lens = np.maximum(lens - drop, 0).astype(np.int32)
+    if nsel is None:
+        return lens
+    ns = np.maximum(np.asarray(nsel, dtype=np.int64) - drop, 0).astype(np.int32)
+    return lens, ns

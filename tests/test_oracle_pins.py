@@ -567,3 +567,59 @@ def test_golden_accept_worked_example():
     gd = _golden()["accept_worked"]
     acc, bonus, am = O.accept_len(np.array([gd["logits"]], np.float32), np.array([gd["draft"]], np.int32), gd["gamma"])
     assert am[0].tolist() == gd["argmax"] and acc[0] == gd["accept"] and bonus[0] == gd["bonus"]
+
+
+# ---------------------------------------------------------------- per-round cache updates (Alg. 2)
+
+def test_append_then_decode_equals_decode_over_the_extended_cache():
+    # the drafter's round: rows appended to a cache with spare capacity and to the sparse list
+    # give the same attention as a cache built with those rows from the start
+    S, Hkv, Hq, cap, L0, n = 2, 2, 8, 64, 40, 5
+    g = np.random.default_rng(40)
+    kf = bits(g.standard_normal((S, Hkv, cap, 128)))
+    vf = bits(g.standard_normal((S, Hkv, cap, 128)))
+    k0, v0 = kf.copy(), vf.copy()
+    k0[:, :, L0:] = 0
+    v0[:, :, L0:] = 0
+    k_new = np.ascontiguousarray(kf[:, :, L0:L0 + n].transpose(0, 2, 1, 3))   # [S][n][Hkv][D]
+    v_new = np.ascontiguousarray(vf[:, :, L0:L0 + n].transpose(0, 2, 1, 3))
+    idx = np.full((S, Hkv, 32), -1, np.int32)
+    idx[:, :, :10] = np.arange(0, 40, 4)
+    k1, v1, lens, idx1, nsel1 = O.cache_append(k0, v0, [L0] * S, k_new, v_new, idx, [10] * S)
+    assert lens.tolist() == [L0 + n] * S and nsel1.tolist() == [10 + n] * S
+    assert np.array_equal(k1[:, :, :L0 + n], kf[:, :, :L0 + n]) and np.all(k1[:, :, L0 + n:] == 0)
+    assert idx1[0, 1, 10:15].tolist() == list(range(L0, L0 + n)) and np.all(idx1[:, :, 15:] == -1)
+    q = bits(g.standard_normal((S, Hq, 128)))
+    want_idx = np.full((S, Hkv, 32), -1, np.int32)
+    want_idx[:, :, :10] = np.arange(0, 40, 4)
+    want_idx[:, :, 10:15] = np.arange(L0, L0 + n)
+    a = O.sparse_decode_attn(k1, v1, q, idx1, nsel1, lens)
+    b = O.sparse_decode_attn(kf, vf, q, want_idx, [15] * S, [L0 + n] * S)
+    np.testing.assert_array_equal(a[0], b[0])
+
+
+def test_append_clamps_at_capacity_and_index_width():
+    S, Hkv, cap = 1, 1, 10
+    k = np.zeros((S, Hkv, cap, 128), np.uint16)
+    new = np.full((S, 4, Hkv, 128), 7, np.uint16)
+    k1, v1, lens, idx1, nsel1 = O.cache_append(k, k, [8], new, new, np.full((S, Hkv, 5), -1, np.int32), [4])
+    assert lens.tolist() == [10]                      # two of four rows fit
+    assert np.all(k1[0, 0, 8:] == 7) and np.all(k1[0, 0, :8] == 0)
+    assert nsel1.tolist() == [5] and idx1[0, 0, 4] == 8   # one of two slots fits
+
+
+def test_rollback_keeps_the_accepted_prefix():
+    # verifier: gamma speculative rows, accepted k -> L - (gamma - k); the drafter's list likewise
+    lens, ns = O.cache_rollback([100, 100, 100, 3], [0, 2, 5, 9], 5, nsel=[20, 20, 20, 1])
+    assert lens.tolist() == [95, 97, 100, 3] and ns.tolist() == [15, 17, 20, 1]
+    assert O.cache_rollback([2], [0], 5).tolist() == [0]               # never below zero
+    # append gamma rows then roll back after k accepted == append only the k accepted rows
+    S, cap, gamma = 1, 32, 4
+    g = np.random.default_rng(41)
+    k = bits(g.standard_normal((S, 1, cap, 128)))
+    new = bits(g.standard_normal((S, gamma, 1, 128)))
+    for kacc in range(gamma + 1):
+        _, _, l_all = O.cache_append(k, k, [10], new, new)
+        l_rb = O.cache_rollback(l_all, [kacc], gamma)
+        _, _, l_k = O.cache_append(k, k, [10], new[:, :kacc], new[:, :kacc])
+        assert l_rb.tolist() == l_k.tolist()
