@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--budget", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", choices=("step", "select", "multiview"), default="step")
+    ap.add_argument("--op", choices=("step", "select", "multiview", "updates"), default="step")
     ap.add_argument("--chunk", type=int, default=0,
                     help="--op select: 0 = token-level selection with pooling, s > 0 = TopKChunks with chunks of s")
     ap.add_argument("--copy-probe", action="store_true",
@@ -128,6 +128,8 @@ def main():
         return bench_select(args, bd, synth, torch, np, dev)
     if args.op == "multiview":
         return bench_multiview(args, bd, synth, torch, np, dev)
+    if args.op == "updates":
+        return bench_updates(args, bd, synth, torch, np, dev)
     cfg = synth.CONFIGS[2]
     S, Hq, Hkv, L, W, gamma, V = (cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.window,
                                   cfg.gamma, cfg.vocab)
@@ -368,6 +370,50 @@ def bench_multiview(args, bd, synth, torch, np, dev):
         "roofline": {"bound": "mfma", "kernel": "block_kernel (views + full branch)", "achieved": round(tflops, 1),
                      "peak": 2500.0, "unit": "TFLOP/s", "frac": round(tflops / 2500.0, 4), "traffic": None,
                      "flops_per_call": flops},
+    }), flush=True)
+
+
+def bench_updates(args, bd, synth, torch, np, dev):
+    """One round of Alg. 2's cache updates on the 16K batch: gamma single-row appends to the drafter
+    cache and its sparse list, gamma+1 rows to the verifier cache, then both rollbacks (accept = 0,
+    so every round leaves each cache one row longer)."""
+    cfg = synth.CONFIGS[2]
+    S, Hq, Hkv, L, gamma, B = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.gamma, args.budget
+    steps = max(1, min(args.steps, 50))
+    warm = min(args.warmup, 5)
+    cap = L + steps + warm + 2
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    kS = torch.randn((S, Hkv, cap, 128), device=dev, generator=g).to(torch.bfloat16)
+    vS, kL, vL = torch.empty_like(kS), torch.empty_like(kS), torch.empty_like(kS)
+    lensS = torch.full((S,), L - gamma - 1, dtype=torch.int32, device=dev)
+    lensL = lensS.clone()
+    idx = torch.zeros((S, Hkv, B + gamma * (steps + warm + 1)), dtype=torch.int32, device=dev)
+    nsel = torch.full((S,), B, dtype=torch.int32, device=dev)
+    rows1 = torch.randn((S, 1, Hkv, 128), device=dev, generator=g).to(torch.bfloat16)
+    rowsV = torch.randn((S, gamma + 1, Hkv, 128), device=dev, generator=g).to(torch.bfloat16)
+    acc = torch.zeros((S,), dtype=torch.int32, device=dev)
+
+    def round_():
+        for _ in range(gamma):
+            bd.bd_cache_append(kS, vS, lensS, rows1, rows1, idx=idx, nsel=nsel)
+        bd.bd_cache_append(kL, vL, lensL, rowsV, rowsV)
+        bd.bd_cache_rollback(lensL, acc, gamma)
+        bd.bd_cache_rollback(lensS, acc, gamma - 1, nsel=nsel)
+
+    us = _time_calls(torch, round_, steps, warm)
+    moved = 2 * (gamma + gamma + 1) * S * Hkv * 128 * 2 * 2        # rows read and written, K and V
+    print(json.dumps({
+        "metric": "Alg. 2 cache updates µs/round at 16K ctx (8 seqs: 5 drafter appends, 1 verifier append, 2 rollbacks)",
+        "value": round(us, 2), "unit": "us/round", "n_gpus": 1, "steps": steps, "warmup": warm,
+        "ms_per_step": round(us / 1e3, 5), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (random rows)",
+        "config": {"workload": f"updates-16k-b8: 8 seqs, {Hkv} kv heads, gamma={gamma}, B={B}", "num_seqs": S,
+                   "seq_len": L, "gamma": gamma},
+        "roofline": {"bound": "latency", "kernel": "append_rows/append_advance/rollback (9 launches per round)",
+                     "achieved": round(moved / (us * 1e-6) / 1e9, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(moved / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 6), "traffic": None,
+                     "bytes_per_round": moved},
     }), flush=True)
 
 

@@ -232,6 +232,39 @@ bd_status bd_accept_len(const float* logits, int64_t row_stride, const int32_t* 
                         int32_t gamma, int32_t vocab, int32_t* accept_out, int32_t* bonus_out,
                         int32_t* argmax_out, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * bd_cache_append -- append rows to a cache (Alg. 2: the caches are updated
+ * with the appended tokens; during drafting the sparse cache grows by each
+ * drafted token).
+ *
+ * For every sequence s, the n new rows go to positions L_s .. L_s+n-1, where
+ * L_s = kv->seq_lens[s]; rows at or past kv->max_seq_len (the capacity) are
+ * dropped.  kv->k and kv->v are written (the descriptor's pointers must be
+ * writable), and kv->seq_lens (device) is advanced in place by the rows written.
+ * k_new, v_new [S][n][Hkv][128] bf16, 16-byte aligned.
+ * idx, nsel  NULL, or the drafter's sparse list [S][Hkv][ld_idx] and count [S]
+ *            (device, updated in place): every written position is appended to
+ *            each head's list at slots nsel[s] ..; slots past ld_idx are dropped.
+ * Two launches on `stream` (row copies, then the counts).  Contiguous or paged
+ * layouts (paged: the pages of the new positions must already be mapped).
+ * ---------------------------------------------------------------------- */
+bd_status bd_cache_append(const bd_kv_desc* kv, const uint16_t* k_new, const uint16_t* v_new, int32_t n,
+                          int32_t* idx, int32_t ld_idx, int32_t* nsel, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * bd_cache_rollback -- drop rejected speculative rows after verification
+ * (Alg. 2, cache update after the accept step).
+ *
+ * Each sequence's last `spec` rows are speculative and the first accept[s]
+ * of them (clamped to [0, spec]) were accepted: spec - accept[s] rows are
+ * dropped from seq_lens[s], and from nsel[s] when nsel is given (the
+ * drafter's sparse list, whose last entries are those rows), never below 0.
+ * seq_lens, nsel: device int32 [S], updated in place; accept: device [S]
+ * (e.g. bd_accept_len's accept_out).  One launch on `stream`.
+ * ---------------------------------------------------------------------- */
+bd_status bd_cache_rollback(int32_t* seq_lens, int32_t* nsel, const int32_t* accept, int32_t num_seqs, int32_t spec,
+                            hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -28,6 +28,7 @@ import torch
 __all__ = [
     "BdError", "lib", "library_path", "kv_desc", "Workspace",
     "bd_select_kv", "bd_select_kv_chunks", "bd_sparse_decode_attn", "bd_multiview_attn", "bd_verify_attn", "bd_accept_len",
+    "bd_cache_append", "bd_cache_rollback",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -65,6 +66,8 @@ _SIGNATURES = {
     "bd_select_kv_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32]),
     "bd_select_kv": (_I32, [_KV, _P, _I32, _I32, _I32, _I32, _F32, _P, _P, _P, _P, _P, _SZ, _P]),
     "bd_select_kv_chunks": (_I32, [_KV, _P, _I32, _I32, _I32, _I32, _F32, _P, _P, _P, _P, _P, _SZ, _P]),
+    "bd_cache_append": (_I32, [_KV, _P, _P, _I32, _P, _I32, _P, _P]),
+    "bd_cache_rollback": (_I32, [_P, _P, _P, _I32, _I32, _P]),
     "bd_sparse_decode_attn_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32]),
     "bd_sparse_decode_attn": (_I32, [_KV, _P, _I32, _P, _I32, _P, _F32, _P, _P, _P, _SZ, _P]),
     "bd_multiview_attn_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32, _I32, _I32, _I32]),
@@ -307,3 +310,31 @@ def bd_accept_len(logits: torch.Tensor, draft: torch.Tensor, *, return_argmax: b
     _check(L.bd_accept_len(logits.data_ptr(), logits.stride(1), draft.data_ptr(), S, gamma, V, acc.data_ptr(),
                            bonus.data_ptr(), _ptr(am), wp, wb, _stream()))
     return (acc, bonus, am) if return_argmax else (acc, bonus)
+
+
+def bd_cache_append(k: torch.Tensor, v: torch.Tensor, seq_lens: torch.Tensor, k_new: torch.Tensor,
+                    v_new: torch.Tensor, *, idx: Optional[torch.Tensor] = None, nsel: Optional[torch.Tensor] = None,
+                    page_table: Optional[torch.Tensor] = None, max_seq_len: Optional[int] = None) -> None:
+    """Append rows in place: k_new, v_new bf16 [S, n, Hkv, 128] go to positions seq_lens[s] ..; seq_lens
+    (and, with the sparse list idx [S, Hkv, ld] / nsel [S], the list) advance in place."""
+    _require(k_new.dtype == torch.bfloat16 and k_new.dim() == 4 and k_new.is_contiguous() and k_new.shape == v_new.shape
+             and v_new.is_contiguous() and v_new.dtype == torch.bfloat16, "k_new and v_new must be contiguous bf16 [S,n,Hkv,128]")
+    _require(seq_lens.dtype == torch.int32 and seq_lens.is_contiguous(), "seq_lens must be int32 [S]")
+    if idx is not None:
+        _require(idx.dtype == torch.int32 and idx.dim() == 3 and idx.is_contiguous(), "idx must be contiguous int32 [S,Hkv,ld]")
+        _require(nsel is not None and nsel.dtype == torch.int32 and nsel.is_contiguous(), "nsel must be int32 [S]")
+    kv = kv_desc(k, v, seq_lens, page_table, max_seq_len)
+    _require(k_new.shape[0] == kv.num_seqs and k_new.shape[2] == kv.num_kv_heads, "k_new must be [S,n,Hkv,128]")
+    _check(lib().bd_cache_append(ctypes.byref(kv), k_new.data_ptr(), v_new.data_ptr(), k_new.shape[1], _ptr(idx),
+                                 idx.shape[2] if idx is not None else 0, _ptr(nsel), _stream()))
+
+
+def bd_cache_rollback(seq_lens: torch.Tensor, accept: torch.Tensor, spec: int, *,
+                      nsel: Optional[torch.Tensor] = None) -> None:
+    """Drop spec - accept[s] speculative rows from seq_lens (and nsel) in place."""
+    _require(seq_lens.dtype == torch.int32 and seq_lens.is_contiguous(), "seq_lens must be int32 [S]")
+    _require(accept.dtype == torch.int32 and accept.shape == seq_lens.shape, "accept must be int32 [S]")
+    if nsel is not None:
+        _require(nsel.dtype == torch.int32 and nsel.shape == seq_lens.shape, "nsel must be int32 [S]")
+    _check(lib().bd_cache_rollback(seq_lens.data_ptr(), _ptr(nsel), accept.data_ptr(), seq_lens.shape[0], int(spec),
+                                   _stream()))

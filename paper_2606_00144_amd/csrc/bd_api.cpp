@@ -329,4 +329,34 @@ bd_status bd_accept_len(const float* logits, int64_t row_stride, const int32_t* 
   return launched(bd::launch_accept(p, stream));
 }
 
+// ---------------------------------------------------------------- per-round cache updates
+bd_status bd_cache_append(const bd_kv_desc* kv, const uint16_t* k_new, const uint16_t* v_new, int32_t n,
+                          int32_t* idx, int32_t ld_idx, int32_t* nsel, hipStream_t stream) {
+  bd_status st = check_kv(kv, true, kv ? kv->num_kv_heads : 0);
+  if (st != BD_OK) return st;
+  if (n < 0) return fail(BD_ERR_INVALID_ARG, "n < 0");
+  if (n == 0) return BD_OK;
+  if (!k_new || !v_new || !aligned(k_new, 16) || !aligned(v_new, 16))
+    return fail(BD_ERR_INVALID_ARG, "k_new and v_new must be 16-byte aligned device pointers");
+  if ((idx == nullptr) != (nsel == nullptr)) return fail(BD_ERR_INVALID_ARG, "idx and nsel go together");
+  if (idx && ld_idx < 0) return fail(BD_ERR_INVALID_ARG, "ld_idx < 0");
+  if ((int64_t)kv->num_seqs * n > INT32_MAX) return fail(BD_ERR_UNSUPPORTED, "num_seqs * n too large");
+  bd::AppendParams p{};
+  p.kv = bd::make_kv_view(*kv);
+  p.k_new = k_new;
+  p.v_new = v_new;
+  p.n = n;
+  p.idx = idx;
+  p.nsel = nsel;
+  p.ld_idx = idx ? ld_idx : 0;
+  return launched(bd::launch_append(p, stream));
+}
+
+bd_status bd_cache_rollback(int32_t* seq_lens, int32_t* nsel, const int32_t* accept, int32_t num_seqs, int32_t spec,
+                            hipStream_t stream) {
+  if (!seq_lens || !accept) return fail(BD_ERR_INVALID_ARG, "seq_lens and accept are required");
+  if (num_seqs < 1 || spec < 0) return fail(BD_ERR_INVALID_ARG, "need num_seqs >= 1 and spec >= 0");
+  return launched(bd::launch_rollback(seq_lens, nsel, accept, num_seqs, spec, stream));
+}
+
 }  // extern "C"

@@ -112,6 +112,21 @@ struct SelectPlan {
 SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L, bool paged);
 hipError_t launch_select(const SelectParams& p, bool paged, hipStream_t stream);
 
+// ---- per-round cache updates -------------------------------------------------
+struct AppendParams {
+  KvView kv;                // the cache written (k, v rows; seq_lens advanced in place)
+  const uint16_t* k_new;    // [S][n][Hkv][D]
+  const uint16_t* v_new;
+  int32_t n;
+  int32_t* idx;             // nullable [S][Hkv][ld_idx] sparse list, entries appended
+  int32_t* nsel;            // [S] when idx is given
+  int32_t ld_idx;
+};
+
+hipError_t launch_append(const AppendParams& p, hipStream_t stream);
+hipError_t launch_rollback(int32_t* seq_lens, int32_t* nsel, const int32_t* accept, int32_t S, int32_t spec,
+                           hipStream_t stream);
+
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 }  // namespace bd

@@ -1,0 +1,104 @@
+// Per-round cache updates (Alg. 2: the caches are updated with the appended tokens).
+//
+// Appending writes the new rows' K and V at positions L_s .. L_s+n-1 and, for
+// the drafter's sparse cache, appends those positions to every KV head's index
+// list; a second launch then advances the lengths (every row copy reads the old
+// length first, and stream order separates the two).  Rollback drops the
+// rejected speculative rows after verification.  All of it is integer and byte
+// work: one 16-byte load and store per lane per row chunk.
+
+#include "bd_common.hpp"
+#include "bd_kernels.hpp"
+
+namespace bd {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kChunks = kD * 2 / 16;   // 16-byte chunks of a 128-element bf16 row
+
+__device__ inline int clamp_len(int L, int cap) { return L < 0 ? 0 : (L > cap ? cap : L); }
+
+// Block (s, i): new row i of sequence s, every KV head; thread -> (head, K or V, chunk).
+__global__ __launch_bounds__(kThreads) void append_rows_kernel(AppendParams p) {
+  const int s = blockIdx.x / p.n, i = blockIdx.x % p.n;
+  const int cap = p.kv.max_seq_len;
+  const int L = clamp_len(p.kv.seq_lens[s], cap);
+  const int t = L + i;
+  if (t >= cap) return;                                   // past the capacity: dropped
+  int64_t base = -1;
+  if (p.kv.page_table) {
+    const int pg = p.kv.page_table[(int64_t)s * p.kv.max_pages_per_seq + t / p.kv.page_size];
+    if ((unsigned)pg < (unsigned)p.kv.num_pages) base = (int64_t)pg * p.kv.stride_page + (int64_t)(t % p.kv.page_size) * p.kv.stride_tok;
+  } else {
+    base = (int64_t)s * p.kv.stride_seq + (int64_t)t * p.kv.stride_tok;
+  }
+  const int per_head = 2 * kChunks;                       // K chunks then V chunks
+  for (int w = threadIdx.x; w < p.kv.num_kv_heads * per_head; w += kThreads) {
+    const int g = w / per_head, r = w % per_head;
+    const bool is_v = r >= kChunks;
+    const int c = is_v ? r - kChunks : r;
+    const int64_t src = (((int64_t)s * p.n + i) * p.kv.num_kv_heads + g) * kD + 8 * c;
+    if (base >= 0) {
+      const int64_t dst = base + (int64_t)g * p.kv.stride_head + 8 * c;
+      uint16_t* cache = const_cast<uint16_t*>(is_v ? p.kv.v : p.kv.k);
+      *reinterpret_cast<u32x4*>(cache + dst) = load16((is_v ? p.v_new : p.k_new) + src);
+    }
+  }
+  if (p.idx) {
+    int m = p.nsel[s];
+    m = m < 0 ? 0 : (m > p.ld_idx ? p.ld_idx : m);
+    if (m + i < p.ld_idx)
+      for (int g = threadIdx.x; g < p.kv.num_kv_heads; g += kThreads)
+        p.idx[((int64_t)s * p.kv.num_kv_heads + g) * p.ld_idx + m + i] = t;
+  }
+}
+
+// Thread s: advance the length (and the sparse count) by what append_rows_kernel wrote.
+__global__ __launch_bounds__(kThreads) void append_advance_kernel(AppendParams p) {
+  const int s = blockIdx.x * kThreads + threadIdx.x;
+  if (s >= p.kv.num_seqs) return;
+  const int cap = p.kv.max_seq_len;
+  const int L = clamp_len(p.kv.seq_lens[s], cap);
+  const int w = p.n < cap - L ? p.n : cap - L;
+  const_cast<int32_t*>(p.kv.seq_lens)[s] = L + w;
+  if (p.idx) {
+    int m = p.nsel[s];
+    m = m < 0 ? 0 : (m > p.ld_idx ? p.ld_idx : m);
+    const int a = w < p.ld_idx - m ? w : p.ld_idx - m;
+    p.nsel[s] = m + a;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void rollback_kernel(int32_t* seq_lens, int32_t* nsel, const int32_t* accept,
+                                                           int32_t S, int32_t spec) {
+  const int s = blockIdx.x * kThreads + threadIdx.x;
+  if (s >= S) return;
+  int a = accept[s];
+  a = a < 0 ? 0 : (a > spec ? spec : a);
+  const int drop = spec - a;
+  const int L = seq_lens[s] - drop;
+  seq_lens[s] = L < 0 ? 0 : L;
+  if (nsel) {
+    const int m = nsel[s] - drop;
+    nsel[s] = m < 0 ? 0 : m;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_append(const AppendParams& p, hipStream_t stream) {
+  hipLaunchKernelGGL(append_rows_kernel, dim3(p.kv.num_seqs * p.n), dim3(kThreads), 0, stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(append_advance_kernel, dim3((p.kv.num_seqs + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_rollback(int32_t* seq_lens, int32_t* nsel, const int32_t* accept, int32_t S, int32_t spec,
+                           hipStream_t stream) {
+  hipLaunchKernelGGL(rollback_kernel, dim3((S + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, seq_lens, nsel,
+                     accept, S, spec);
+  return hipGetLastError();
+}
+
+}  // namespace bd

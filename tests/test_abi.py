@@ -113,3 +113,21 @@ def test_workspace_sizes(L):
     assert L.bd_multiview_attn_workspace_bytes(4, 8, 32, 64, 4, 2048, 8192, 1) > 0
     assert L.bd_accept_len_workspace_bytes(8, 5, 128256) > 0
     assert L.bd_verify_attn_workspace_bytes(0, 8, 32, 5, 16384) == 0        # invalid shape -> 0
+
+
+def test_update_rejections(L):
+    A = lambda kv, n=1, kn=FAKE, idx=None, nsel=None, ld=0: L.bd_cache_append(
+        ctypes.byref(kv) if kv is not None else None, kn, FAKE, n, idx, ld, nsel, None)
+    assert A(None) == bd.BD_ERR_INVALID_ARG
+    assert A(_kv(), n=-1) == bd.BD_ERR_INVALID_ARG
+    assert A(_kv(), n=0) == bd.BD_OK                                        # nothing to do, nothing launched
+    assert A(_kv(), kn=0) == bd.BD_ERR_INVALID_ARG
+    assert A(_kv(), kn=FAKE + 4) == bd.BD_ERR_INVALID_ARG                   # misaligned rows
+    assert A(_kv(), idx=FAKE) == bd.BD_ERR_INVALID_ARG                      # idx without nsel
+    assert A(_kv(), idx=FAKE, nsel=FAKE, ld=-1) == bd.BD_ERR_INVALID_ARG
+    assert A(_kv(head_dim=64)) == bd.BD_ERR_UNSUPPORTED
+    R = L.bd_cache_rollback
+    assert R(None, None, FAKE, 2, 5, None) == bd.BD_ERR_INVALID_ARG
+    assert R(FAKE, None, None, 2, 5, None) == bd.BD_ERR_INVALID_ARG
+    assert R(FAKE, None, FAKE, 0, 5, None) == bd.BD_ERR_INVALID_ARG
+    assert R(FAKE, None, FAKE, 2, -1, None) == bd.BD_ERR_INVALID_ARG
