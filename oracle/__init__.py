@@ -21,4 +21,7 @@ from .bd_oracle import (  # noqa: F401
     accept_len,
     cache_append,
     cache_rollback,
+    top1_ce,
+    budget_thresholds,
+    sample_budgets,
 )

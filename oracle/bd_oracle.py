@@ -466,3 +466,59 @@ def cache_rollback(seq_lens, accept, spec: int, nsel=None):
         return lens
     ns = np.maximum(np.asarray(nsel, dtype=np.int64) - drop, 0).astype(np.int32)
     return lens, ns
+
+
+# --------------------------------------------------------------------------
+# Training-side neighbours of the acceptance rule (Sec. 3.3-3.4)
+# --------------------------------------------------------------------------
+
+def top1_ce(student, teacher=None, targets=None):
+    """Top-1 cross-entropy of the drafter against the verifier's greedy targets.
+
+    Eq. (5) gives the target of each continuation row, the lowest-index argmax of
+    the verifier's logits (``teacher``; or ``targets`` given directly); the summand
+    of L_A (Eq. 6) and L_C (Eq. 7) for that row is -log softmax(student row)[target]
+    = logsumexp(student row) - student[target] (natural log).
+    student, teacher: [R][V] fp32; returns (loss [R], target [R] int32, lse [R]) in float64.
+    """
+    x = np.asarray(student, dtype=np.float64)
+    if not np.all(np.isfinite(x)):
+        raise ValueError("student logits must be finite")
+    R = x.shape[0]
+    if teacher is not None:
+        tgt = np.array([greedy_argmax(np.asarray(teacher[r])) for r in range(R)], dtype=np.int32)
+    else:
+        tgt = np.asarray(targets, dtype=np.int32)
+    m = x.max(axis=1)
+    lse = m + np.log(np.exp(x - m[:, None]).sum(axis=1))
+    loss = lse - x[np.arange(R), tgt]
+    return loss, tgt, lse
+
+
+def budget_thresholds(weights) -> np.ndarray:
+    """Cumulative thresholds of Cat(B, w) in fp32: prefix sums of w in order, divided by their total.
+
+    The sampling rule compares fp32 numbers, so both implementations take the
+    decision in fp32 (Sec. 3.4 draws B ~ Cat(B, w) each training step).
+    """
+    w = np.asarray(weights, dtype=np.float32)
+    c = np.zeros(w.size, dtype=np.float32)
+    acc = np.float32(0.0)
+    for i in range(w.size):
+        acc = np.float32(acc + w[i])
+        c[i] = acc
+    return (c / c[-1]).astype(np.float32)
+
+
+def sample_budgets(u, budgets, weights) -> np.ndarray:
+    """B ~ Cat(budgets, weights) by inversion: the first budget whose fp32 cumulative threshold
+    exceeds the uniform draw u in [0, 1) (the last budget if none does)."""
+    thr = budget_thresholds(weights)
+    u = np.asarray(u, dtype=np.float32)
+    out = np.empty(u.size, dtype=np.int32)
+    for i, x in enumerate(u.ravel()):
+        j = 0
+        while j < thr.size - 1 and not (x < thr[j]):
+            j += 1
+        out[i] = budgets[j]
+    return out

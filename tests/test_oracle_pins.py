@@ -623,3 +623,48 @@ def test_rollback_keeps_the_accepted_prefix():
         l_rb = O.cache_rollback(l_all, [kacc], gamma)
         _, _, l_k = O.cache_append(k, k, [10], new[:, :kacc], new[:, :kacc])
         assert l_rb.tolist() == l_k.tolist()
+
+
+# ---------------------------------------------------------------- top-1 CE (Eqs. 5-7) and budget sampling
+
+def test_top1_ce_matches_torch_cross_entropy_and_targets():
+    g = np.random.default_rng(50)
+    R, V = 7, 300
+    st = g.standard_normal((R, V)).astype(np.float32) * 3
+    te = np.round(g.standard_normal((R, V)) * 2).astype(np.float32)      # ties in the teacher rows
+    loss, tgt, lse = O.top1_ce(st, teacher=te)
+    assert tgt.tolist() == [int(np.argmax(te[r])) for r in range(R)]       # first occurrence
+    want = torch.nn.functional.cross_entropy(torch.from_numpy(st).double(), torch.from_numpy(tgt).long(),
+                                             reduction="none").numpy()
+    np.testing.assert_allclose(loss, want, rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(lse, torch.logsumexp(torch.from_numpy(st).double(), 1).numpy(), rtol=1e-13)
+
+
+def test_top1_ce_closed_forms():
+    V = 1000
+    loss, _, lse = O.top1_ce(np.zeros((2, V), np.float32), targets=[0, 999])
+    np.testing.assert_allclose(loss, np.log(V), rtol=1e-14)                # uniform: log V
+    st = np.zeros((1, V), np.float32); st[0, 5] = 40.0
+    loss, _, _ = O.top1_ce(st, targets=[5])
+    np.testing.assert_allclose(loss[0], np.log1p((V - 1) * np.exp(-40.0)), rtol=1e-10)   # target holds the max
+    a, _, _ = O.top1_ce(st + 3.5, targets=[7])                             # shift invariance
+    b, _, _ = O.top1_ce(st, targets=[7])
+    np.testing.assert_allclose(a, b, rtol=1e-12)
+    np.testing.assert_allclose(b, 40.0 + np.log1p((V - 1) * np.exp(-40.0)), rtol=1e-12)
+
+
+def test_budget_sampling_inverts_the_cdf():
+    budgets, w = [256, 512, 1024, 2048], [0.4, 0.3, 0.2, 0.1]
+    thr = O.budget_thresholds(w)
+    assert thr.dtype == np.float32 and thr[-1] == 1.0
+    assert O.sample_budgets([0.0], budgets, w).tolist() == [256]
+    assert O.sample_budgets([np.nextafter(np.float32(1), np.float32(0))], budgets, w).tolist() == [2048]
+    # a draw equal to a threshold falls in the next bucket; just below stays
+    t0 = thr[0]
+    assert O.sample_budgets([t0], budgets, w).tolist() == [512]
+    assert O.sample_budgets([np.nextafter(t0, np.float32(0))], budgets, w).tolist() == [256]
+    # frequencies follow the weights
+    u = np.random.default_rng(51).random(200000).astype(np.float32)
+    b = O.sample_budgets(u, budgets, w)
+    freq = [(b == x).mean() for x in budgets]
+    np.testing.assert_allclose(freq, w, atol=0.005)
