@@ -265,6 +265,42 @@ bd_status bd_cache_append(const bd_kv_desc* kv, const uint16_t* k_new, const uin
 bd_status bd_cache_rollback(int32_t* seq_lens, int32_t* nsel, const int32_t* accept, int32_t num_seqs, int32_t spec,
                             hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * bd_top1_ce -- top-1 cross-entropy of the drafter against the verifier's
+ * greedy targets: the target of row r is the lowest-index argmax of the
+ * verifier's logits (Eq. 5), and loss[r] = logsumexp(student[r]) -
+ * student[r][target] (natural log) is the row's summand of L_A (Eq. 6, full
+ * cache) or L_C (Eq. 7, sparse cache).  The targets' scan and the loss share
+ * one pass over the two logit rows.
+ *
+ * student     [rows][vocab] fp32, rows student_stride elements apart.
+ * teacher     NULL, or [rows][vocab] fp32 verifier logits (teacher_stride):
+ *             the targets are their argmax.
+ * targets     used when teacher is NULL: [rows] int32; an entry outside
+ *             [0, vocab) gives loss NaN and target -1.
+ * loss_out    [rows] fp32; target_out NULL or [rows] int32; lse_out NULL or
+ *             [rows] fp32 (logsumexp of the student row).
+ * Exactly one of teacher and targets; rows <= BD_WS_COUNTER_LINES.
+ * ---------------------------------------------------------------------- */
+size_t bd_top1_ce_workspace_bytes(int32_t rows, int32_t vocab);
+bd_status bd_top1_ce(const float* student, int64_t student_stride, const float* teacher, int64_t teacher_stride,
+                     const int32_t* targets, int32_t rows, int32_t vocab, float* loss_out, int32_t* target_out,
+                     float* lse_out, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * bd_sample_budgets -- B ~ Cat(budgets, weights), one draw per uniform number
+ * (Sec. 3.4 and Alg. 1 step 4 draw the training budget this way).
+ *
+ * Thresholds t_j = (w_0 + ... + w_j) / (w_0 + ... + w_{n-1}) are formed on the
+ * host in fp32 (sums in order, then one division each); out[i] = budgets[j]
+ * for the first j with u[i] < t_j (the last budget if none).  The random
+ * numbers are the caller's: u [count] fp32 in [0, 1) on the device.
+ * budgets, weights: host arrays of n <= 16 entries, weights positive and finite.
+ * out [count] int32 on the device.
+ * ---------------------------------------------------------------------- */
+bd_status bd_sample_budgets(const float* u, int32_t count, const int32_t* budgets, const float* weights, int32_t n,
+                            int32_t* out, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

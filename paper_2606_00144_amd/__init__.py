@@ -28,7 +28,7 @@ import torch
 __all__ = [
     "BdError", "lib", "library_path", "kv_desc", "Workspace",
     "bd_select_kv", "bd_select_kv_chunks", "bd_sparse_decode_attn", "bd_multiview_attn", "bd_verify_attn", "bd_accept_len",
-    "bd_cache_append", "bd_cache_rollback",
+    "bd_cache_append", "bd_cache_rollback", "bd_top1_ce", "bd_sample_budgets",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -68,6 +68,9 @@ _SIGNATURES = {
     "bd_select_kv_chunks": (_I32, [_KV, _P, _I32, _I32, _I32, _I32, _F32, _P, _P, _P, _P, _P, _SZ, _P]),
     "bd_cache_append": (_I32, [_KV, _P, _P, _I32, _P, _I32, _P, _P]),
     "bd_cache_rollback": (_I32, [_P, _P, _P, _I32, _I32, _P]),
+    "bd_top1_ce_workspace_bytes": (_SZ, [_I32, _I32]),
+    "bd_top1_ce": (_I32, [_P, ctypes.c_int64, _P, ctypes.c_int64, _P, _I32, _I32, _P, _P, _P, _P, _SZ, _P]),
+    "bd_sample_budgets": (_I32, [_P, _I32, _P, _P, _I32, _P, _P]),
     "bd_sparse_decode_attn_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32]),
     "bd_sparse_decode_attn": (_I32, [_KV, _P, _I32, _P, _I32, _P, _F32, _P, _P, _P, _SZ, _P]),
     "bd_multiview_attn_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32, _I32, _I32, _I32]),
@@ -338,3 +341,38 @@ def bd_cache_rollback(seq_lens: torch.Tensor, accept: torch.Tensor, spec: int, *
         _require(nsel.dtype == torch.int32 and nsel.shape == seq_lens.shape, "nsel must be int32 [S]")
     _check(lib().bd_cache_rollback(seq_lens.data_ptr(), _ptr(nsel), accept.data_ptr(), seq_lens.shape[0], int(spec),
                                    _stream()))
+
+
+def bd_top1_ce(student: torch.Tensor, *, teacher: Optional[torch.Tensor] = None, targets: Optional[torch.Tensor] = None,
+               return_targets: bool = False, return_lse: bool = False, workspace: Optional[Workspace] = None):
+    """Top-1 CE per row: student fp32 [R, V]; teacher fp32 [R, V] (targets = its argmax) or targets int32 [R]."""
+    _require(student.dtype == torch.float32 and student.dim() == 2 and student.stride(1) == 1, "student must be fp32 [R,V]")
+    R, V = student.shape
+    if teacher is not None:
+        _require(teacher.dtype == torch.float32 and teacher.shape == student.shape and teacher.stride(1) == 1,
+                 "teacher must be fp32 [R,V]")
+    if targets is not None:
+        _require(targets.dtype == torch.int32 and targets.shape == (R,) and targets.is_contiguous(), "targets must be int32 [R]")
+    dev = student.device
+    loss = torch.empty((R,), dtype=torch.float32, device=dev)
+    tgt = torch.empty((R,), dtype=torch.int32, device=dev) if return_targets else None
+    lse = torch.empty((R,), dtype=torch.float32, device=dev) if return_lse else None
+    L = lib()
+    wp, wb = _ws("ce", L.bd_top1_ce_workspace_bytes(R, V), dev, workspace)
+    _check(L.bd_top1_ce(student.data_ptr(), student.stride(0), _ptr(teacher), teacher.stride(0) if teacher is not None else 0,
+                        _ptr(targets), R, V, loss.data_ptr(), _ptr(tgt), _ptr(lse), wp, wb, _stream()))
+    out = [loss] + ([tgt] if return_targets else []) + ([lse] if return_lse else [])
+    return out[0] if len(out) == 1 else tuple(out)
+
+
+def bd_sample_budgets(u: torch.Tensor, budgets, weights) -> torch.Tensor:
+    """B ~ Cat(budgets, weights) for every uniform draw in u (fp32 device tensor)."""
+    _require(u.dtype == torch.float32 and u.is_contiguous(), "u must be contiguous fp32")
+    n = len(budgets)
+    _require(n == len(weights) and n >= 1, "budgets and weights must have the same length")
+    b = (ctypes.c_int32 * n)(*[int(x) for x in budgets])
+    w = (ctypes.c_float * n)(*[float(x) for x in weights])
+    out = torch.empty(u.shape, dtype=torch.int32, device=u.device)
+    _check(lib().bd_sample_budgets(u.data_ptr(), u.numel(), ctypes.cast(b, ctypes.c_void_p),
+                                   ctypes.cast(w, ctypes.c_void_p), n, out.data_ptr(), _stream()))
+    return out

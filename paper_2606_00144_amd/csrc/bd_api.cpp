@@ -359,4 +359,60 @@ bd_status bd_cache_rollback(int32_t* seq_lens, int32_t* nsel, const int32_t* acc
   return launched(bd::launch_rollback(seq_lens, nsel, accept, num_seqs, spec, stream));
 }
 
+// ---------------------------------------------------------------- top-1 CE, budget sampling
+size_t bd_top1_ce_workspace_bytes(int32_t rows, int32_t vocab) {
+  if (rows < 1 || vocab < 1) return 0;
+  return bd::plan_ce(rows, vocab).ws_bytes;
+}
+
+bd_status bd_top1_ce(const float* student, int64_t student_stride, const float* teacher, int64_t teacher_stride,
+                     const int32_t* targets, int32_t rows, int32_t vocab, float* loss_out, int32_t* target_out,
+                     float* lse_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!student || !loss_out) return fail(BD_ERR_INVALID_ARG, "student and loss_out are required");
+  if ((teacher == nullptr) == (targets == nullptr)) return fail(BD_ERR_INVALID_ARG, "give exactly one of teacher and targets");
+  if (rows < 1 || vocab < 1) return fail(BD_ERR_INVALID_ARG, "need rows >= 1 and vocab >= 1");
+  if (student_stride < vocab || (teacher && teacher_stride < vocab))
+    return fail(BD_ERR_INVALID_ARG, "row strides must be >= vocab");
+  if (rows > BD_WS_COUNTER_LINES) return fail(BD_ERR_UNSUPPORTED, "more than %d rows", BD_WS_COUNTER_LINES);
+  const bd::CePlan pl = bd::plan_ce(rows, vocab);
+  if ((int64_t)rows * pl.nsplit > INT32_MAX) return fail(BD_ERR_UNSUPPORTED, "too many rows");
+  bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
+  if (st != BD_OK) return st;
+  bd::CeParams p{};
+  p.student = student;
+  p.s_stride = student_stride;
+  p.teacher = teacher;
+  p.t_stride = teacher ? teacher_stride : 0;
+  p.targets = targets;
+  p.rows = rows;
+  p.vocab = vocab;
+  p.nsplit = pl.nsplit;
+  p.chunk = pl.chunk;
+  p.vec4 = aligned(student, 16) && student_stride % 4 == 0 && (!teacher || (aligned(teacher, 16) && teacher_stride % 4 == 0));
+  p.loss_out = loss_out;
+  p.target_out = target_out;
+  p.lse_out = lse_out;
+  p.counters = static_cast<uint32_t*>(ws);
+  p.part = reinterpret_cast<float*>(static_cast<char*>(ws) + BD_WS_COUNTER_BYTES);
+  return launched(bd::launch_ce(p, stream));
+}
+
+bd_status bd_sample_budgets(const float* u, int32_t count, const int32_t* budgets, const float* weights, int32_t n,
+                            int32_t* out, hipStream_t stream) {
+  if (!u || !out || !budgets || !weights) return fail(BD_ERR_INVALID_ARG, "u, budgets, weights and out are required");
+  if (count < 0 || n < 1 || n > bd::kMaxBudgets) return fail(BD_ERR_INVALID_ARG, "need count >= 0 and 1 <= n <= %d", bd::kMaxBudgets);
+  bd::SampleTable t{};
+  t.n = n;
+  float acc = 0.f;
+  for (int i = 0; i < n; ++i) {
+    if (!std::isfinite(weights[i]) || !(weights[i] > 0.f)) return fail(BD_ERR_INVALID_ARG, "weights must be positive and finite");
+    acc += weights[i];
+    t.thr[i] = acc;
+    t.budgets[i] = budgets[i];
+  }
+  for (int i = 0; i < n; ++i) t.thr[i] = t.thr[i] / acc;
+  if (count == 0) return BD_OK;
+  return launched(bd::launch_sample(u, count, t, out, stream));
+}
+
 }  // extern "C"

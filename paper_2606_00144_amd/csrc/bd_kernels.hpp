@@ -127,6 +127,39 @@ hipError_t launch_append(const AppendParams& p, hipStream_t stream);
 hipError_t launch_rollback(int32_t* seq_lens, int32_t* nsel, const int32_t* accept, int32_t S, int32_t spec,
                            hipStream_t stream);
 
+// ---- top-1 cross-entropy and budget sampling ---------------------------------
+struct CeParams {
+  const float* student;     // [rows] rows of vocab fp32 at s_stride
+  int64_t s_stride;
+  const float* teacher;     // nullable [rows] rows at t_stride: targets = first argmax
+  int64_t t_stride;
+  const int32_t* targets;   // [rows] when teacher is NULL
+  int32_t rows, vocab;
+  int32_t nsplit, chunk;
+  int32_t vec4;             // both row sets 16-byte aligned: vector loads
+  float* loss_out;
+  int32_t* target_out;      // nullable
+  float* lse_out;           // nullable
+  float* part;              // [rows][nsplit] 16-byte chunk records
+  uint32_t* counters;       // counter region: one line per row
+};
+
+struct CePlan {
+  int nsplit, chunk;
+  size_t record_bytes, ws_bytes;
+};
+
+CePlan plan_ce(int rows, int vocab);
+hipError_t launch_ce(const CeParams& p, hipStream_t stream);
+
+constexpr int kMaxBudgets = 16;
+struct SampleTable {
+  int32_t n;
+  int32_t budgets[kMaxBudgets];
+  float thr[kMaxBudgets];   // fp32 cumulative thresholds, the last one 1
+};
+hipError_t launch_sample(const float* u, int32_t count, const SampleTable& t, int32_t* out, hipStream_t stream);
+
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 }  // namespace bd
