@@ -296,6 +296,30 @@ def _time_calls(torch, fn, steps, warmup):
     return a.elapsed_time(b) * 1e3 / steps
 
 
+def _time_graph(torch, fn, steps, warmup):
+    """Mean µs per call of `fn` captured once in a HIP graph and replayed back to back (launch
+    latency of the small kernels is what a serving loop sees; no host work between replays)."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        fn()
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        graph.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) * 1e3 / steps
+
+
 def bench_select(args, bd, synth, torch, np, dev):
     """bd_select_kv on the 16K batch (8 x 16,384, W = 32, pool 7, B = --budget)."""
     cfg = synth.CONFIGS[2]
@@ -383,14 +407,14 @@ def bench_updates(args, bd, synth, torch, np, dev):
     S, Hq, Hkv, L, gamma, B = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.gamma, args.budget
     steps = max(1, min(args.steps, 50))
     warm = min(args.warmup, 5)
-    cap = L + steps + warm + 2
+    cap = L + steps + warm + 4
     g = torch.Generator(device=dev)
     g.manual_seed(0)
     kS = torch.randn((S, Hkv, cap, 128), device=dev, generator=g).to(torch.bfloat16)
     vS, kL, vL = torch.empty_like(kS), torch.empty_like(kS), torch.empty_like(kS)
     lensS = torch.full((S,), L - gamma - 1, dtype=torch.int32, device=dev)
     lensL = lensS.clone()
-    idx = torch.zeros((S, Hkv, B + gamma * (steps + warm + 1)), dtype=torch.int32, device=dev)
+    idx = torch.zeros((S, Hkv, B + gamma * (steps + warm + 2)), dtype=torch.int32, device=dev)
     nsel = torch.full((S,), B, dtype=torch.int32, device=dev)
     rows1 = torch.randn((S, 1, Hkv, 128), device=dev, generator=g).to(torch.bfloat16)
     rowsV = torch.randn((S, gamma + 1, Hkv, 128), device=dev, generator=g).to(torch.bfloat16)
@@ -403,7 +427,7 @@ def bench_updates(args, bd, synth, torch, np, dev):
         bd.bd_cache_rollback(lensL, acc, gamma)
         bd.bd_cache_rollback(lensS, acc, gamma - 1, nsel=nsel)
 
-    us = _time_calls(torch, round_, steps, warm)
+    us = _time_graph(torch, round_, steps, warm)
     moved = 2 * (gamma + gamma + 1) * S * Hkv * 128 * 2 * 2        # rows read and written, K and V
     print(json.dumps({
         "metric": "Alg. 2 cache updates µs/round at 16K ctx (8 seqs: 5 drafter appends, 1 verifier append, 2 rollbacks)",
@@ -430,7 +454,7 @@ def bench_ce(args, bd, synth, torch, np, dev):
     teacher = torch.randn((R, V), device=dev, generator=g) * 2
     ws = bd.Workspace()
     steps, warm = max(1, min(args.steps, 100)), min(args.warmup, 10)
-    us = _time_calls(torch, lambda: bd.bd_top1_ce(student, teacher=teacher, workspace=ws), steps, warm)
+    us = _time_graph(torch, lambda: bd.bd_top1_ce(student, teacher=teacher, workspace=ws), steps, warm)
     alg = 2 * R * V * 4 + R * 4
     gbs = alg / (us * 1e-6) / 1e9
     print(json.dumps({
