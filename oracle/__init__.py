@@ -17,6 +17,8 @@ from .bd_oracle import (  # noqa: F401
     sparse_decode_attn,
     verify_attn,
     multiview_attn,
+    attend_backward,
+    multiview_attn_bwd,
     greedy_argmax,
     accept_len,
     cache_append,

@@ -372,6 +372,78 @@ def multiview_attn(k, v, q_blk, idx_views, nsel_views, seq_lens, scale: Optional
     return out_v, out_f
 
 
+def attend_backward(q, k, v, visible, scale: float, dout):
+    """Gradients of ``attend`` with respect to q, k and v for an upstream gradient dout [R][D].
+
+    With p_rt the softmax weights of row r over its visible keys and out_r = sum_t p_rt v_t:
+    dv_t = sum_r p_rt dout_r; dp_rt = <dout_r, v_t>; D_r = <dout_r, out_r>;
+    ds_rt = p_rt (dp_rt - D_r); dq_r = scale sum_t ds_rt k_t; dk_t = scale sum_r ds_rt q_r.
+    Returns dq [R][D], dk [N][D], dv [N][D] float64.
+    """
+    R, D = q.shape
+    N = k.shape[0]
+    dq, dk, dv = np.zeros((R, D)), np.zeros((N, D)), np.zeros((N, D))
+    if N == 0:
+        return dq, dk, dv
+    out, lse = attend(q, k, v, visible, scale)
+    visible = np.asarray(visible, dtype=bool)
+    has = visible.any(axis=1)
+    logits = scale * (q @ k.T)
+    p = np.where(visible & has[:, None], np.exp(np.where(visible, logits, 0.0) - np.where(has, lse, 0.0)[:, None]), 0.0)
+    dv = p.T @ dout
+    dp = dout @ v.T
+    Dr = (dout * out).sum(axis=1)
+    ds = p * (dp - Dr[:, None])
+    dq = scale * (ds @ k)
+    dk = scale * (ds.T @ q)
+    return dq, dk, dv
+
+
+def multiview_attn_bwd(k, v, q_blk, idx_views, nsel_views, seq_lens, dout_views, dout_full,
+                       scale: Optional[float] = None):
+    """Backward of ``multiview_attn`` for the drafter's training losses.
+
+    Alg. 1 back-propagates L_A and L_C through the continuation's full-cache and
+    sparse-cache branches (steps 3-5); the prefix cache is computed without
+    gradient (step 2), so of the keys and values only the block's own rows,
+    positions L_s-C .. L_s-1, receive gradients.  Gradients of the views and the
+    full branch add up.  dout_views [V][S][C][Hq][D], dout_full [S][C][Hq][D]
+    (or None): upstream gradients of the two outputs.
+    Returns dq [S][C][Hq][D], dk_blk [S][C][Hkv][D], dv_blk [S][C][Hkv][D] float64.
+    """
+    S, C, Hq, D = q_blk.shape
+    nv = len(idx_views)
+    Hkv = k[0].shape[0]
+    G = Hq // Hkv
+    sc = _scale64(scale, D)
+    dq = np.zeros((S, C, Hq, D))
+    dk = np.zeros((S, C, Hkv, D))
+    dv = np.zeros((S, C, Hkv, D))
+    for s in range(S):
+        L = int(seq_lens[s])
+        qs = bf16_to_f64(q_blk[s])
+        pos = L - C + np.arange(C)
+        for g in range(Hkv):
+            qg = qs[:, g * G:(g + 1) * G, :].reshape(C * G, D)
+            kg_all = bf16_to_f64(k[s][g, :L])
+            vg_all = bf16_to_f64(v[s][g, :L])
+            branches = []
+            for vi in range(nv):
+                J = _valid_entries(idx_views[vi][s, g], nsel_views[vi][s], L)
+                branches.append((J, np.asarray(dout_views[vi][s][:, g * G:(g + 1) * G], dtype=np.float64)))
+            if dout_full is not None:
+                branches.append((np.arange(L), np.asarray(dout_full[s][:, g * G:(g + 1) * G], dtype=np.float64)))
+            for J, do in branches:
+                vis = np.repeat(J[None, :] <= pos[:, None], G, axis=0)
+                gq, gk, gv = attend_backward(qg, kg_all[J], vg_all[J], vis, sc, do.reshape(C * G, D))
+                dq[s, :, g * G:(g + 1) * G] += gq.reshape(C, G, D)
+                for j, t in enumerate(J):
+                    if t >= L - C:                        # a block row: it carries a gradient
+                        dk[s, t - (L - C), g] += gk[j]
+                        dv[s, t - (L - C), g] += gv[j]
+    return dq, dk, dv
+
+
 # --------------------------------------------------------------------------
 # Greedy acceptance (Eq. 3; Alg. 2 accept and bonus token)
 # --------------------------------------------------------------------------

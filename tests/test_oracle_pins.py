@@ -669,3 +669,81 @@ def test_budget_sampling_inverts_the_cdf():
     b = O.sample_budgets(u, budgets, w)
     freq = [(b == x).mean() for x in budgets]
     np.testing.assert_allclose(freq, w, atol=0.005)
+
+
+# ---------------------------------------------------------------- multiview backward (Alg. 1 steps 3-5)
+
+def _torch_multiview_grads(k, v, q, idx_views, nsel, lens, dov, dof, sc):
+    """Reference gradients by fp64 autograd of a dense masked-softmax formulation (library routine)."""
+    S, C, Hq, D = q.shape
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    kt = torch.from_numpy(O.bf16_to_f64(k)).requires_grad_(True)
+    vt = torch.from_numpy(O.bf16_to_f64(v)).requires_grad_(True)
+    qt = torch.from_numpy(O.bf16_to_f64(q)).requires_grad_(True)
+    total = 0
+    for s in range(S):
+        L = lens[s]
+        pos = torch.arange(L - C, L)
+        for h in range(Hq):
+            g = h // G
+            logits = sc * qt[s, :, h] @ kt[s, g, :L].T                       # [C][L]
+            masks = []
+            for vi in range(len(idx_views)):
+                J = [int(t) for t in idx_views[vi][s, g, :nsel[vi][s]] if 0 <= t < L]
+                m = torch.zeros((C, L), dtype=torch.bool)
+                for t in J:
+                    m[:, t] |= torch.tensor(True)
+                masks.append((m & (torch.arange(L)[None, :] <= pos[:, None]), torch.from_numpy(dov[vi][s, :, h])))
+            masks.append((torch.arange(L)[None, :] <= pos[:, None], torch.from_numpy(dof[s, :, h])))
+            for m, do in masks:
+                p = torch.softmax(logits.masked_fill(~m, float("-inf")), dim=1)
+                total = total + (do * (p @ vt[s, g, :L])).sum()
+    total.backward()
+    return qt.grad.numpy(), kt.grad.numpy(), vt.grad.numpy()
+
+
+def test_multiview_backward_matches_fp64_autograd():
+    S, Hkv, Hq, L, C = 2, 2, 4, 40, 6
+    g = np.random.default_rng(60)
+    k, v = bits(g.standard_normal((S, Hkv, L, 128))), bits(g.standard_normal((S, Hkv, L, 128)))
+    q = bits(g.standard_normal((S, C, Hq, 128)))
+    lens = [40, 33]
+    idx = [np.full((S, Hkv, 20), -1, np.int32) for _ in range(2)]
+    for vi, B in enumerate([12, 20]):
+        for s in range(S):
+            for gg in range(Hkv):
+                pre = np.sort(g.choice(lens[s] - C, B - C, replace=False))
+                idx[vi][s, gg, :B] = np.r_[pre, np.arange(lens[s] - C, lens[s])]
+    nsel = [np.array([12, 12]), np.array([20, 20])]
+    dov = g.standard_normal((2, S, C, Hq, 128))
+    dof = g.standard_normal((S, C, Hq, 128))
+    sc = float(np.float32(1 / np.sqrt(128)))
+    dq, dk, dv = O.multiview_attn_bwd(k, v, q, idx, nsel, lens, dov, dof)
+    tq, tk, tv = _torch_multiview_grads(k, v, q, idx, nsel, lens, dov, dof, sc)
+    np.testing.assert_allclose(dq, tq, rtol=1e-10, atol=1e-12)
+    for s in range(S):
+        blk = slice(lens[s] - C, lens[s])
+        np.testing.assert_allclose(dk[s], tk[s, :, blk].transpose(1, 0, 2), rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(dv[s], tv[s, :, blk].transpose(1, 0, 2), rtol=1e-10, atol=1e-12)
+
+
+def test_attend_backward_finite_differences():
+    g = np.random.default_rng(61)
+    R, N, D = 3, 5, 8
+    q, k, v = g.standard_normal((R, D)), g.standard_normal((N, D)), g.standard_normal((N, D))
+    vis = np.ones((R, N), bool); vis[0, 3:] = False
+    dout = g.standard_normal((R, D))
+    dq, dk, dv = O.attend_backward(q, k, v, vis, 0.3, dout)
+    f = lambda q_, k_, v_: (O.attend(q_, k_, v_, vis, 0.3)[0] * dout).sum()
+    eps = 1e-6
+    for arr, grad, which in [(q, dq, 0), (k, dk, 1), (v, dv, 2)]:
+        for idx in [(0, 1), (1, 4), (2, 0)]:
+            if idx[0] >= arr.shape[0]:
+                continue
+            a2 = arr.copy(); a2[idx] += eps
+            args = [q, k, v]; args[which] = a2
+            b2 = arr.copy(); b2[idx] -= eps
+            args2 = [q, k, v]; args2[which] = b2
+            fd = (f(*args) - f(*args2)) / (2 * eps)
+            assert abs(fd - grad[idx]) < 1e-6 * max(1.0, abs(fd)), (which, idx, fd, grad[idx])
