@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--budget", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", choices=("step", "select", "multiview", "updates", "ce"), default="step")
+    ap.add_argument("--op", choices=("step", "select", "multiview", "multiview_bwd", "updates", "ce"), default="step")
     ap.add_argument("--chunk", type=int, default=0,
                     help="--op select: 0 = token-level selection with pooling, s > 0 = TopKChunks with chunks of s")
     ap.add_argument("--copy-probe", action="store_true",
@@ -128,6 +128,8 @@ def main():
         return bench_select(args, bd, synth, torch, np, dev)
     if args.op == "multiview":
         return bench_multiview(args, bd, synth, torch, np, dev)
+    if args.op == "multiview_bwd":
+        return bench_multiview_bwd(args, bd, synth, torch, np, dev)
     if args.op == "updates":
         return bench_updates(args, bd, synth, torch, np, dev)
     if args.op == "ce":
@@ -352,11 +354,10 @@ def bench_select(args, bd, synth, torch, np, dev):
     }), flush=True)
 
 
-def bench_multiview(args, bd, synth, torch, np, dev):
-    """bd_multiview_attn on the multi-view block (4 x 8,192, C = 64, four budgets, views from bd_select_kv)."""
+def _multiview_inputs(bd, synth, torch, np, dev):
+    """The multi-view training block (4 x 8,192, C = 64, four budgets), views from bd_select_kv."""
     cfg = synth.CONFIGS[3]
     S, Hq, Hkv, L, C = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.block_len
-    G = Hq // Hkv
     budgets = [int(b) for b in synth.view_budgets(cfg)]
     log("generating inputs")
     qs, ks, vs = synth.kv_batch(cfg)
@@ -370,21 +371,36 @@ def bench_multiview(args, bd, synth, torch, np, dev):
         vi, vn = bd.bd_select_kv(k, q_blk, lens, Bv)
         idx[i, :, :, :Bv] = vi
         nsel[i] = vn
-    ws = bd.Workspace()
-    steps = max(1, min(args.steps, 50))
-    fn = lambda: bd.bd_multiview_attn(k, v, q_blk, idx, nsel, lens, workspace=ws)
-    us = _time_calls(torch, fn, steps, min(args.warmup, 5))
-    # algorithmic flops: 4 * 128 per (query row, visible key), full branch and every view
+    return cfg, budgets, k, v, q_blk, lens, idx, nsel
+
+
+def _visible_pairs(np, idx_h, budgets, S, Hkv, G, L, C):
+    """(query row, visible key) pairs over all branches, and those whose key is a block row."""
     pos = np.arange(L - C, L)
-    idx_h = idx.cpu().numpy()
     full_pairs = S * Hkv * G * int((pos + 1).sum())
+    blk_pairs = S * Hkv * G * (C * (C + 1) // 2)
     view_pairs = 0
     for i, Bv in enumerate(budgets):
         for s in range(S):
             for g in range(Hkv):
                 t = np.sort(idx_h[i, s, g, :Bv])
                 view_pairs += G * int(np.searchsorted(t, pos, side="right").sum())
-    flops = 4 * 128 * (full_pairs + view_pairs)
+                tb = t[t >= L - C] - (L - C)                  # block keys listed in the view
+                blk_pairs += G * int((C - tb).sum())
+    return full_pairs + view_pairs, blk_pairs
+
+
+def bench_multiview(args, bd, synth, torch, np, dev):
+    """bd_multiview_attn on the multi-view block (4 x 8,192, C = 64, four budgets, views from bd_select_kv)."""
+    cfg, budgets, k, v, q_blk, lens, idx, nsel = _multiview_inputs(bd, synth, torch, np, dev)
+    S, Hq, Hkv, L, C = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.block_len
+    ws = bd.Workspace()
+    steps = max(1, min(args.steps, 50))
+    fn = lambda: bd.bd_multiview_attn(k, v, q_blk, idx, nsel, lens, workspace=ws)
+    us = _time_calls(torch, fn, steps, min(args.warmup, 5))
+    # algorithmic flops: 4 * 128 per (query row, visible key), full branch and every view
+    pairs, _ = _visible_pairs(np, idx.cpu().numpy(), budgets, S, Hkv, Hq // Hkv, L, C)
+    flops = 4 * 128 * pairs
     tflops = flops / (us * 1e-6) / 1e12
     print(json.dumps({
         "metric": "bd_multiview_attn µs/call at 8K ctx (4 seqs, C=64, 4 views + full)", "value": round(us, 2),
@@ -394,6 +410,37 @@ def bench_multiview(args, bd, synth, torch, np, dev):
         "config": {"workload": f"multiview-train-b4-8k: 4 seqs x {L} ctx, {Hq}/{Hkv} heads, C={C}, budgets {budgets}",
                    "num_seqs": S, "seq_len": L, "block_len": C, "budgets": budgets},
         "roofline": {"bound": "mfma", "kernel": "block_kernel (views + full branch)", "achieved": round(tflops, 1),
+                     "peak": 2500.0, "unit": "TFLOP/s", "frac": round(tflops / 2500.0, 4), "traffic": None,
+                     "flops_per_call": flops},
+    }), flush=True)
+
+
+def bench_multiview_bwd(args, bd, synth, torch, np, dev):
+    """bd_multiview_attn_bwd on the multi-view block: dQ over every branch, dK/dV of the block rows."""
+    cfg, budgets, k, v, q_blk, lens, idx, nsel = _multiview_inputs(bd, synth, torch, np, dev)
+    S, Hq, Hkv, L, C = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.block_len
+    ov, of, o32v, lv, o32f, lf = bd.bd_multiview_attn(k, v, q_blk, idx, nsel, lens, train=True)
+    g = torch.Generator(device=dev)
+    g.manual_seed(3)
+    dov = torch.randn(ov.shape, device=dev, generator=g).to(torch.bfloat16)
+    dof = torch.randn(of.shape, device=dev, generator=g).to(torch.bfloat16)
+    ws = bd.Workspace()
+    steps = max(1, min(args.steps, 50))
+    fn = lambda: bd.bd_multiview_attn_bwd(k, v, q_blk, idx, nsel, lens, o32v, lv, dov, o32f, lf, dof, workspace=ws)
+    us = _time_calls(torch, fn, steps, min(args.warmup, 5))
+    # algorithmic flops: per (query row, visible key) the score, dP and dQ products (6 * 128); per
+    # (query row, visible block key) also the dK and dV products (4 * 128)
+    pairs, blk = _visible_pairs(np, idx.cpu().numpy(), budgets, S, Hkv, Hq // Hkv, L, C)
+    flops = 6 * 128 * pairs + 4 * 128 * blk
+    tflops = flops / (us * 1e-6) / 1e12
+    print(json.dumps({
+        "metric": "bd_multiview_attn_bwd µs/call at 8K ctx (4 seqs, C=64, 4 views + full)", "value": round(us, 2),
+        "unit": "us/call", "n_gpus": 1, "steps": steps, "warmup": min(args.warmup, 5),
+        "ms_per_step": round(us / 1e3, 5), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded N(0,1) bf16 K/V/Q/dO with 1% planted heavy hitters)",
+        "config": {"workload": f"multiview-train-b4-8k: 4 seqs x {L} ctx, {Hq}/{Hkv} heads, C={C}, budgets {budgets}",
+                   "num_seqs": S, "seq_len": L, "block_len": C, "budgets": budgets},
+        "roofline": {"bound": "mfma", "kernel": "dq_kernel + dkv_kernel", "achieved": round(tflops, 1),
                      "peak": 2500.0, "unit": "TFLOP/s", "frac": round(tflops / 2500.0, 4), "traffic": None,
                      "flops_per_call": flops},
     }), flush=True)

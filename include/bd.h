@@ -4,13 +4,19 @@
  * Greedy speculative decoding with a drafter that reads a budgeted subset of
  * its KV cache and a verifier that reads its full cache (Sec. 3.1, Alg. 2),
  * and the continuation-block attention of multi-view training (Alg. 1).
- * Five operations, each an asynchronous launch on a caller-given HIP stream:
+ * Each operation is an asynchronous launch on a caller-given HIP stream:
  *
  *   bd_select_kv           budgeted KV selection (Alg. 2 "sparsify")
+ *   bd_select_kv_chunks    chunk-level selection (TopKChunks, Sec. 3.4)
  *   bd_sparse_decode_attn  drafter attention over the selected entries (Eq. 2)
  *   bd_multiview_attn      a query block under several budgets + the full cache (Alg. 1)
+ *   bd_multiview_attn_bwd  its gradients for the drafter's training losses (Alg. 1)
  *   bd_verify_attn         verifier attention at the gamma+1 draft positions (Eq. 1)
  *   bd_accept_len          greedy accepted-prefix length and bonus token (Eq. 3)
+ *   bd_cache_append        per-round cache growth (Alg. 2)
+ *   bd_cache_rollback      rejected rows dropped after verification (Alg. 2)
+ *   bd_top1_ce             top-1 cross-entropy against the verifier (Eqs. 5-7)
+ *   bd_sample_budgets      B ~ Cat(B, w) per training sample (Alg. 1)
  *
  * Common conventions
  *   - Tensors are raw device pointers.  bf16 data are passed as uint16_t bit
@@ -189,7 +195,15 @@ bd_status bd_sparse_decode_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t
  * q_blk      [S][C][Hq][128] bf16.
  * idx_views  [V][S][Hkv][ld_idx] int32; nsel_views [V][S] int32.
  * out_views  [V][S][C][Hq][128] bf16 (may be NULL only when V == 0).
+ * lse_views  NULL or [V][S][C][Hq] fp32.
+ * out32_views NULL or [V][S][C][Hq][128] fp32: the outputs before rounding.
  * out_full   NULL (full branch skipped) or [S][C][Hq][128] bf16.
+ * lse_full, out32_full  as for the views (ignored when out_full is NULL).
+ * Training outputs: when out32_views or out32_full is given, every softmax
+ * weight enters the weighted sum of values as two bf16 terms (the rounded
+ * weight and its rounded remainder), so the fp32 outputs carry the weights
+ * to about 2^-17 rather than 2^-9 (the bf16 outputs are then the rounding
+ * of these).  bd_multiview_attn_bwd takes out32 and lse.
  * Requirements: C >= 1, V >= 0, V + (out_full != NULL) >= 1.
  * ---------------------------------------------------------------------- */
 size_t bd_multiview_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
@@ -197,8 +211,48 @@ size_t bd_multiview_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads,
                                          int32_t max_seq_len, int32_t with_full);
 bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t num_q_heads, int32_t block_len,
                             int32_t num_views, const int32_t* idx_views, int32_t ld_idx,
-                            const int32_t* nsel_views, float scale, uint16_t* out_views, uint16_t* out_full,
+                            const int32_t* nsel_views, float scale, uint16_t* out_views, float* lse_views,
+                            float* out32_views, uint16_t* out_full, float* lse_full, float* out32_full,
                             void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * bd_multiview_attn_bwd -- gradients of bd_multiview_attn for the drafter's
+ * training losses (Alg. 1 steps 3-5).
+ *
+ * The losses reach the block's queries through every view and the full
+ * branch, and its keys and values through the cache rows the block itself
+ * wrote (positions L_s - C .. L_s - 1); the prefix cache is computed without
+ * gradient (Alg. 1 step 2) and gets none.  With P the softmax weights of a
+ * branch (from its log-sum-exp) and D_r = <dO_r, O_r>:
+ *   dS = P o (dO V^T - D),  dQ = scale dS K,  dK = scale dS^T Q,  dV = P^T dO,
+ * summed over the branches.  A key listed m times in a view counts m times.
+ * Shapes and visibility are those of bd_multiview_attn:
+ * q_blk      [S][C][Hq][128] bf16; idx_views [V][S][Hkv][ld_idx]; nsel_views [V][S].
+ * out32_views, lse_views  the forward's training outputs of the views (out32_views and
+ *            lse_views of bd_multiview_attn: [V][S][C][Hq][128] and [V][S][C][Hq] fp32);
+ *            dout_views their upstream gradients, [V][S][C][Hq][128] bf16.
+ * out32_full, lse_full, dout_full  the same for the full branch: all three NULL (no
+ *            full branch) or all three given.
+ * D_r = <dO_r, O_r> cancels against <dO_r, v_t> where a row's weight
+ * concentrates on few keys, so O enters as the fp32 training output: a bf16
+ * output there would put its own rounding into every dS of the row.
+ * dq         [S][C][Hq][128] fp32 (required).
+ * dk_blk, dv_blk  NULL (skipped) or both [S][C][Hkv][128] fp32: row c is the
+ *            gradient of cache row L_s - C + c of KV head g (0 where that position is < 0).
+ * Requirements: 1 <= C <= 1024, C * G <= 1048576, V >= 0, at least one branch,
+ * S * Hkv * (1 + ceil(C*G/256)) <= BD_WS_COUNTER_LINES.  Results do not depend on
+ * scheduling (fixed summation order).
+ * ---------------------------------------------------------------------- */
+size_t bd_multiview_attn_bwd_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
+                                             int32_t block_len, int32_t num_views, int32_t ld_idx,
+                                             int32_t max_seq_len, int32_t with_full);
+bd_status bd_multiview_attn_bwd(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t num_q_heads, int32_t block_len,
+                                int32_t num_views, const int32_t* idx_views, int32_t ld_idx,
+                                const int32_t* nsel_views, float scale,
+                                const float* out32_views, const float* lse_views, const uint16_t* dout_views,
+                                const float* out32_full, const float* lse_full, const uint16_t* dout_full,
+                                float* dq, float* dk_blk, float* dv_blk,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * bd_verify_attn -- verifier attention over the full cache at the gamma+1

@@ -334,7 +334,7 @@ def verify_attn(k, v, q, seq_lens, gamma: int, scale: Optional[float] = None):
 # --------------------------------------------------------------------------
 
 def multiview_attn(k, v, q_blk, idx_views, nsel_views, seq_lens, scale: Optional[float] = None,
-                   with_full: bool = True):
+                   with_full: bool = True, return_lse: bool = False):
     """Continuation block attended under several sparse views and the full cache.
 
     Alg. 1: the continuation rows attend Clone(K_S^full) (full branch, step 3)
@@ -342,7 +342,8 @@ def multiview_attn(k, v, q_blk, idx_views, nsel_views, seq_lens, scale: Optional
     position ids.  Row c of q_blk [S][C][Hq][D] sits at position L_s - C + c.
     View v sees {t in idx_views[v, s, g, :nsel] : t <= position}; the full
     branch sees {t <= position}.
-    Returns out_views [V][S][C][Hq][D] and out_full [S][C][Hq][D] (or None).
+    Returns out_views [V][S][C][Hq][D] and out_full [S][C][Hq][D] (or None);
+    with return_lse also their log-sum-exps [V][S][C][Hq] and [S][C][Hq] (or None).
     """
     S, C, Hq, D = q_blk.shape
     nv = len(idx_views)
@@ -351,6 +352,8 @@ def multiview_attn(k, v, q_blk, idx_views, nsel_views, seq_lens, scale: Optional
     sc = _scale64(scale, D)
     out_v = np.zeros((nv, S, C, Hq, D))
     out_f = np.zeros((S, C, Hq, D)) if with_full else None
+    lse_v = np.zeros((nv, S, C, Hq))
+    lse_f = np.zeros((S, C, Hq)) if with_full else None
     for s in range(S):
         L = int(seq_lens[s])
         qs = bf16_to_f64(q_blk[s])
@@ -362,14 +365,16 @@ def multiview_attn(k, v, q_blk, idx_views, nsel_views, seq_lens, scale: Optional
             for vi in range(nv):
                 J = _valid_entries(idx_views[vi][s, g], nsel_views[vi][s], L)
                 vis = np.repeat(J[None, :] <= pos[:, None], G, axis=0)
-                o, _ = attend(qg, kg_all[J], vg_all[J], vis, sc)
+                o, lse = attend(qg, kg_all[J], vg_all[J], vis, sc)
                 out_v[vi, s, :, g * G:(g + 1) * G] = o.reshape(C, G, D)
+                lse_v[vi, s, :, g * G:(g + 1) * G] = lse.reshape(C, G)
             if with_full:
                 t = np.arange(L)
                 vis = np.repeat(t[None, :] <= pos[:, None], G, axis=0)
-                o, _ = attend(qg, kg_all, vg_all, vis, sc)
+                o, lse = attend(qg, kg_all, vg_all, vis, sc)
                 out_f[s, :, g * G:(g + 1) * G] = o.reshape(C, G, D)
-    return out_v, out_f
+                lse_f[s, :, g * G:(g + 1) * G] = lse.reshape(C, G)
+    return (out_v, out_f, lse_v, lse_f) if return_lse else (out_v, out_f)
 
 
 def attend_backward(q, k, v, visible, scale: float, dout):

@@ -8,8 +8,9 @@ raised.
 
 Functions carry the names of the C entry points:
 
-    bd_select_kv, bd_sparse_decode_attn, bd_multiview_attn,
-    bd_verify_attn, bd_accept_len
+    bd_select_kv, bd_select_kv_chunks, bd_sparse_decode_attn,
+    bd_multiview_attn, bd_multiview_attn_bwd, bd_verify_attn, bd_accept_len,
+    bd_cache_append, bd_cache_rollback, bd_top1_ce, bd_sample_budgets
 
 KV caches are bf16 tensors, either contiguous ``[S][Hkv][L][128]`` or paged
 ``[num_pages][Hkv][page_size][128]`` together with an int32 ``page_table``
@@ -27,7 +28,8 @@ import torch
 
 __all__ = [
     "BdError", "lib", "library_path", "kv_desc", "Workspace",
-    "bd_select_kv", "bd_select_kv_chunks", "bd_sparse_decode_attn", "bd_multiview_attn", "bd_verify_attn", "bd_accept_len",
+    "bd_select_kv", "bd_select_kv_chunks", "bd_sparse_decode_attn", "bd_multiview_attn", "bd_multiview_attn_bwd", "bd_verify_attn",
+    "bd_accept_len",
     "bd_cache_append", "bd_cache_rollback", "bd_top1_ce", "bd_sample_budgets",
 ]
 
@@ -74,7 +76,10 @@ _SIGNATURES = {
     "bd_sparse_decode_attn_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32]),
     "bd_sparse_decode_attn": (_I32, [_KV, _P, _I32, _P, _I32, _P, _F32, _P, _P, _P, _SZ, _P]),
     "bd_multiview_attn_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32, _I32, _I32, _I32]),
-    "bd_multiview_attn": (_I32, [_KV, _P, _I32, _I32, _I32, _P, _I32, _P, _F32, _P, _P, _P, _SZ, _P]),
+    "bd_multiview_attn": (_I32, [_KV, _P, _I32, _I32, _I32, _P, _I32, _P, _F32, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "bd_multiview_attn_bwd_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32, _I32, _I32, _I32]),
+    "bd_multiview_attn_bwd": (_I32, [_KV, _P, _I32, _I32, _I32, _P, _I32, _P, _F32, _P, _P, _P, _P, _P, _P,
+                                     _P, _P, _P, _P, _SZ, _P]),
     "bd_verify_attn_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32]),
     "bd_verify_attn": (_I32, [_KV, _P, _I32, _I32, _F32, _P, _P, _P, _SZ, _P]),
     "bd_accept_len_workspace_bytes": (_SZ, [_I32, _I32, _I32]),
@@ -251,9 +256,13 @@ def bd_sparse_decode_attn(k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, idx
 
 def bd_multiview_attn(k: torch.Tensor, v: torch.Tensor, q_blk: torch.Tensor, idx_views: Optional[torch.Tensor],
                       nsel_views: Optional[torch.Tensor], seq_lens: torch.Tensor, *, scale: Optional[float] = None,
-                      full: bool = True, page_table: Optional[torch.Tensor] = None,
+                      full: bool = True, train: bool = False, page_table: Optional[torch.Tensor] = None,
                       max_seq_len: Optional[int] = None, workspace: Optional[Workspace] = None):
-    """Block attention under views and the full cache.  q_blk: bf16 [S, C, Hq, 128]; idx_views int32 [V, S, Hkv, ld]."""
+    """Block attention under views and the full cache.  q_blk: bf16 [S, C, Hq, 128]; idx_views int32 [V, S, Hkv, ld].
+
+    Returns (out_views, out_full).  With train=True also the training outputs the backward takes:
+    (out_views, out_full, out32_views, lse_views, out32_full, lse_full).
+    """
     _require(q_blk.dtype == torch.bfloat16 and q_blk.dim() == 4 and q_blk.is_contiguous(), "q_blk must be contiguous bf16 [S,C,Hq,128]")
     kv = kv_desc(k, v, seq_lens, page_table, max_seq_len)
     S, C, Hq = q_blk.shape[0], q_blk.shape[1], q_blk.shape[2]
@@ -262,14 +271,63 @@ def bd_multiview_attn(k: torch.Tensor, v: torch.Tensor, q_blk: torch.Tensor, idx
     if V:
         _require(idx_views.dtype == torch.int32 and idx_views.is_contiguous(), "idx_views must be contiguous int32 [V,S,Hkv,ld]")
         _require(nsel_views is not None and nsel_views.dtype == torch.int32 and nsel_views.shape == (V, S), "nsel_views must be int32 [V,S]")
-    out_v = torch.empty((V, S, C, Hq, HEAD_DIM), dtype=torch.bfloat16, device=q_blk.device) if V else None
+    dev = q_blk.device
+    out_v = torch.empty((V, S, C, Hq, HEAD_DIM), dtype=torch.bfloat16, device=dev) if V else None
     out_f = torch.empty_like(q_blk) if full else None
+    o32_v = torch.empty((V, S, C, Hq, HEAD_DIM), dtype=torch.float32, device=dev) if (V and train) else None
+    lse_v = torch.empty((V, S, C, Hq), dtype=torch.float32, device=dev) if (V and train) else None
+    o32_f = torch.empty((S, C, Hq, HEAD_DIM), dtype=torch.float32, device=dev) if (full and train) else None
+    lse_f = torch.empty((S, C, Hq), dtype=torch.float32, device=dev) if (full and train) else None
     L = lib()
     nb = L.bd_multiview_attn_workspace_bytes(S, kv.num_kv_heads, Hq, C, V, ld, kv.max_seq_len, int(full))
-    wp, wb = _ws("multiview", nb, q_blk.device, workspace)
+    wp, wb = _ws("multiview", nb, dev, workspace)
     _check(L.bd_multiview_attn(ctypes.byref(kv), q_blk.data_ptr(), Hq, C, V, _ptr(idx_views), ld, _ptr(nsel_views),
-                               _scale(scale), _ptr(out_v), _ptr(out_f), wp, wb, _stream()))
-    return out_v, out_f
+                               _scale(scale), _ptr(out_v), _ptr(lse_v), _ptr(o32_v), _ptr(out_f), _ptr(lse_f),
+                               _ptr(o32_f), wp, wb, _stream()))
+    return (out_v, out_f, o32_v, lse_v, o32_f, lse_f) if train else (out_v, out_f)
+
+
+def bd_multiview_attn_bwd(k: torch.Tensor, v: torch.Tensor, q_blk: torch.Tensor, idx_views: Optional[torch.Tensor],
+                          nsel_views: Optional[torch.Tensor], seq_lens: torch.Tensor,
+                          out32_views: Optional[torch.Tensor], lse_views: Optional[torch.Tensor],
+                          dout_views: Optional[torch.Tensor], out32_full: Optional[torch.Tensor] = None,
+                          lse_full: Optional[torch.Tensor] = None, dout_full: Optional[torch.Tensor] = None, *,
+                          scale: Optional[float] = None, with_dkv: bool = True,
+                          page_table: Optional[torch.Tensor] = None, max_seq_len: Optional[int] = None,
+                          workspace: Optional[Workspace] = None):
+    """Gradients of bd_multiview_attn.  out32/lse are the forward's training outputs (train=True), dout
+    the upstream gradients (bf16, shaped like the outputs).  Returns (dq [S,C,Hq,128], dk_blk, dv_blk [S,C,Hkv,128]) in fp32;
+    dk_blk and dv_blk are None unless with_dkv."""
+    _require(q_blk.dtype == torch.bfloat16 and q_blk.dim() == 4 and q_blk.is_contiguous(), "q_blk must be contiguous bf16 [S,C,Hq,128]")
+    kv = kv_desc(k, v, seq_lens, page_table, max_seq_len)
+    S, C, Hq = q_blk.shape[0], q_blk.shape[1], q_blk.shape[2]
+    V = 0 if idx_views is None else idx_views.shape[0]
+    ld = 0 if idx_views is None else idx_views.shape[3]
+    if V:
+        _require(idx_views.dtype == torch.int32 and idx_views.is_contiguous(), "idx_views must be contiguous int32 [V,S,Hkv,ld]")
+        _require(nsel_views is not None and nsel_views.dtype == torch.int32 and nsel_views.shape == (V, S), "nsel_views must be int32 [V,S]")
+        for t, shp, dt in ((out32_views, (V, S, C, Hq, HEAD_DIM), torch.float32), (dout_views, (V, S, C, Hq, HEAD_DIM), torch.bfloat16),
+                           (lse_views, (V, S, C, Hq), torch.float32)):
+            _require(t is not None and t.dtype == dt and tuple(t.shape) == shp and t.is_contiguous(),
+                     f"view tensors must be contiguous {dt} {shp}")
+    full = dout_full is not None
+    if full:
+        for t, shp, dt in ((out32_full, (S, C, Hq, HEAD_DIM), torch.float32), (dout_full, (S, C, Hq, HEAD_DIM), torch.bfloat16),
+                           (lse_full, (S, C, Hq), torch.float32)):
+            _require(t is not None and t.dtype == dt and tuple(t.shape) == shp and t.is_contiguous(),
+                     f"full-branch tensors must be contiguous {dt} {shp}")
+    dev = q_blk.device
+    dq = torch.empty((S, C, Hq, HEAD_DIM), dtype=torch.float32, device=dev)
+    dk = torch.empty((S, C, kv.num_kv_heads, HEAD_DIM), dtype=torch.float32, device=dev) if with_dkv else None
+    dv = torch.empty_like(dk) if with_dkv else None
+    L = lib()
+    nb = L.bd_multiview_attn_bwd_workspace_bytes(S, kv.num_kv_heads, Hq, C, V, ld, kv.max_seq_len, int(full))
+    wp, wb = _ws("multiview_bwd", nb, dev, workspace)
+    _check(L.bd_multiview_attn_bwd(ctypes.byref(kv), q_blk.data_ptr(), Hq, C, V, _ptr(idx_views), ld,
+                                   _ptr(nsel_views), _scale(scale), _ptr(out32_views), _ptr(lse_views),
+                                   _ptr(dout_views), _ptr(out32_full), _ptr(lse_full), _ptr(dout_full),
+                                   dq.data_ptr(), _ptr(dk), _ptr(dv), wp, wb, _stream()))
+    return dq, dk, dv
 
 
 def bd_verify_attn(k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, seq_lens: torch.Tensor, *,

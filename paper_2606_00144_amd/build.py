@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libbd.so")
 
-SOURCES = ["attn.hip", "select.hip", "accept.hip", "update.hip", "ce.hip", "bd_api.cpp"]
+SOURCES = ["attn.hip", "attn_bwd.hip", "select.hip", "accept.hip", "update.hip", "ce.hip", "bd_api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -33,6 +33,7 @@
 
 #include "bd_common.hpp"
 #include "bd_kernels.hpp"
+#include "attn_tile.hpp"
 
 namespace bd {
 namespace {
@@ -185,10 +186,6 @@ __device__ inline void read_tile(TileRegs<NT, PAGED>& T, uint32_t src, int lane)
       : "v"(at));
 }
 
-__device__ inline void dma16(const uint16_t* g, uint8_t* l) {
-  __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)l, 16, 0, 0);
-}
-
 // Issue the direct-to-LDS loads of a tile into `dst`: load q of a lane lands at
 // dst + q*1 KiB + 16*lane (q 0..7: K subtile q/4, k-step q%4; q 8..15: V row slot q-8).
 // Row offsets are clamped to the layout's extent (validated on the host), so no
@@ -211,18 +208,6 @@ __device__ inline void dma_tile(const KvView& kv, const TileRows& A, uint32_t ma
     }
 }
 
-// Transposed V operand for d-tile dt: slot i holds V[key slot i][8*(lane%16) + dt].
-__device__ inline bf16x8 vt_operand(const u32x4 (&v)[8], int dt) {
-  const int w = dt >> 1;
-  const uint32_t sel = (dt & 1) ? 0x07060302u : 0x05040100u;
-  u32x4 r;
-  r[0] = __builtin_amdgcn_perm(v[1][w], v[0][w], sel);
-  r[1] = __builtin_amdgcn_perm(v[3][w], v[2][w], sel);
-  r[2] = __builtin_amdgcn_perm(v[5][w], v[4][w], sel);
-  r[3] = __builtin_amdgcn_perm(v[7][w], v[6][w], sel);
-  return as_bf16x8(r);
-}
-
 template <int NT>
 struct RowState {
   f32x4 o[NT][8];     // O^T[d-tile][row tile]
@@ -235,7 +220,10 @@ struct RowState {
 // One 32-key tile of one wave.  `dirty` (wave-uniform) asks for the visibility mask: only tiles
 // at the causal edge, at the ragged end of a split or holding absent entries need it.  `want_lx`
 // (uniform) keeps the exact weight sum the log-sum-exp output is computed from.
-template <int NT, bool PAGED, class PosFn>
+// TRAIN: each weight enters the PV product and the normaliser as a bf16 pair hi + lo (lo the rounded
+// remainder), so the output carries the weights to about 2^-17 instead of 2^-9: the fp32 output then
+// serves the backward's <dO, O> (which cancels against <dO, v_t>) without amplifying rounding.
+template <int NT, bool PAGED, bool TRAIN = false, class PosFn>
 __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T, const bf16x8 (&qop)[NT][4],
                                  const int (&rowpos)[NT], float scale_log2, bool dirty, bool want_lx,
                                  PosFn pos_of) {
@@ -291,6 +279,7 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
 
   const bf16x8 ones = as_bf16x8(u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
   bf16x8 pop[NT];
+  bf16x8 plo[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const float muse = st.m[nt] == -INFINITY ? 0.f : st.m[nt];
@@ -301,6 +290,13 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
 #pragma unroll
     for (int i = 0; i < 4; ++i) pw[i] = pack_bf16x2(pv[2 * i], pv[2 * i + 1]);
     pop[nt] = as_bf16x8(pw);
+    if constexpr (TRAIN) {
+      u32x4 lw;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) lw[i] = pack_bf16x2(pv[2 * i] - bf16_lo(pw[i]), pv[2 * i + 1] - bf16_hi(pw[i]));
+      plo[nt] = as_bf16x8(lw);
+      st.l[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, plo[nt], st.l[nt], 0, 0, 0);
+    }
     if (want_lx) {
       float sx = 0.f;
 #pragma unroll
@@ -315,8 +311,10 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
   for (int dt = 0; dt < 8; ++dt) {
     const bf16x8 vt = vt_operand(T.v, dt);
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+    for (int nt = 0; nt < NT; ++nt) {
       st.o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, pop[nt], st.o[nt][dt], 0, 0, 0);
+      if constexpr (TRAIN) st.o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, plo[nt], st.o[nt][dt], 0, 0, 0);
+    }
   }
 }
 
@@ -587,6 +585,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   const int64_t view_rows = (int64_t)p.S * p.nq * p.Hq;
   uint16_t* out = gather ? p.out_g + (int64_t)view * view_rows * kD : p.out_f;
   float* lse = gather ? (p.lse_g ? p.lse_g + (int64_t)view * view_rows : nullptr) : p.lse_f;
+  float* out32 = gather ? (p.o32_g ? p.o32_g + (int64_t)view * view_rows * kD : nullptr) : p.o32_f;
 
   auto write_final = [&](float Mf, float Lf, float Lxf, const float* a) {
     if (!row_valid) return;
@@ -684,9 +683,6 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
 // A wave's online-softmax state is then complete for the split; splits merge
 // through per-row-block records in the last workgroup of the row group.
 
-template <bool B>
-struct BoolTag { static constexpr bool value = B; };
-
 constexpr int kBWaves = 8;
 constexpr int kBThreads = kBWaves * kWave;
 constexpr int kBRing = 6;                          // tile slots; kBRing-1 tiles stay in flight
@@ -746,7 +742,7 @@ __device__ inline void dma_load(const KvView& kv, uint32_t r, uint32_t max_roff,
   else dma16(kv.v + ((uint64_t)ro << 3) + 8 * lr, dst + q * 1024);
 }
 
-template <bool PAGED>
+template <bool PAGED, bool TRAIN>
 __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
   constexpr int NT = 2;
   using RB = RowBlock<NT>;
@@ -806,40 +802,8 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
   const bool arith = !PAGED && !gather;
   if (!arith) {
     const int nslots = (ntiles + kBRing) * kTile;     // <= kBSlotCap: padding tiles included
-    constexpr int kPer = (kBSlotCap + kBThreads - 1) / kBThreads;
-    int tv[kPer];
-#pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-      const int e = e_begin + tid + k * kBThreads;
-      int t = -1;
-      if (e < e_end) t = gather ? idx_row[e] : e;
-      tv[k] = (t >= 0 && t < L) ? t : -1;
-    }
-    int pg[kPer];
-    if constexpr (PAGED) {
-#pragma unroll
-      for (int k = 0; k < kPer; ++k)
-        pg[k] = tv[k] >= 0 ? p.kv.page_table[(int64_t)s * p.kv.max_pages_per_seq + tv[k] / p.kv.page_size] : 0;
-    }
-#pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-      const int i = tid + k * kBThreads;
-      if (i < nslots && i < kBSlotCap) {
-        int t = tv[k];
-        int64_t o;
-        if constexpr (PAGED) {
-          o = (unsigned)pg[k] < (unsigned)p.kv.num_pages
-                  ? (int64_t)pg[k] * p.kv.stride_page + (int64_t)g * p.kv.stride_head +
-                        (int64_t)(t % p.kv.page_size) * p.kv.stride_tok
-                  : -1;
-        } else {
-          o = (int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head + (int64_t)t * p.kv.stride_tok;
-        }
-        if (t < 0 || o < 0) { t = -1; o = 0; }
-        sm.roff[i] = (int)(o >> 3);
-        sm.tpos[i] = t;
-      }
-    }
+    fill_slot_table<PAGED, kBThreads, kBSlotCap>(p.kv, s, g, L, gather ? idx_row : nullptr, e_begin, e_end, nslots,
+                                                 sm.roff, sm.tpos, tid);
     __syncthreads();
   }
   const int minpos = L - p.nq + (rb * RB::kRows) / p.G;   // earliest row position of this wave
@@ -928,12 +892,12 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
       if (has_rows) {
         if constexpr (ARITH) {
           const int slot0 = kTile * t;
-          tile_step<NT, true>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx, [&](int i) {
+          tile_step<NT, true, TRAIN>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx, [&](int i) {
             const int e = e_begin + slot0 + 16 * (i >> 2) + 4 * lg + (i & 3);
             return e < e_end ? e : -1;
           });
         } else {
-          tile_step<NT, true>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx,
+          tile_step<NT, true, TRAIN>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx,
                               [&](int i) { return (int)T.tp[i >> 2][i & 3]; });
         }
       }
@@ -957,6 +921,7 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
   const int64_t view_rows = (int64_t)p.S * p.nq * p.Hq;
   uint16_t* out = gather ? p.out_g + (int64_t)view * view_rows * kD : p.out_f;
   float* lse = gather ? (p.lse_g ? p.lse_g + (int64_t)view * view_rows : nullptr) : p.lse_f;
+  float* out32 = gather ? (p.o32_g ? p.o32_g + (int64_t)view * view_rows * kD : nullptr) : p.o32_f;
   // normalise and write rows 16*nt + lane%16; register i of d-tile dt holds d = 32*(lane/16) + 8*i + dt
   auto write_rows = [&](const float (&M)[NT], const float (&Lw)[NT], const float (&Lx)[NT], const f32x4 (&o)[NT][8]) {
 #pragma unroll
@@ -972,6 +937,11 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(o[nt][2 * e][i] * inv, o[nt][2 * e + 1][i] * inv);
         *reinterpret_cast<u32x4*>(out + orow * kD + 32 * lg + 8 * i) = w;
+        if (TRAIN && out32) {
+          float* o32 = out32 + orow * kD + 32 * lg + 8 * i;
+          *reinterpret_cast<f32x4*>(o32) = f32x4{o[nt][0][i], o[nt][1][i], o[nt][2][i], o[nt][3][i]} * inv;
+          *reinterpret_cast<f32x4*>(o32 + 4) = f32x4{o[nt][4][i], o[nt][5][i], o[nt][6][i], o[nt][7][i]} * inv;
+        }
       }
       if (lse && lg == 0) lse[orow] = Lx[nt] > 0.f ? (M[nt] + __log2f(Lx[nt])) * kLn2 : -INFINITY;
     }
@@ -1045,14 +1015,17 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
 
 }  // namespace
 
-AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full, bool paged) {
+AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full, bool paged,
+                   bool train) {
   AttnPlan pl{};
   const int G = Hq / Hkv;
   pl.R = nq * G;
   pl.nt = pl.R <= 16 ? 1 : 2;
   const int rows = 16 * pl.nt;
   pl.n_rb = (pl.R + rows - 1) / rows;
-  pl.block = pl.n_rb >= 2;                        // several 32-row blocks: they share the K/V stream
+  // several 32-row blocks share the K/V stream in block mode; the training outputs (fp32 output,
+  // two-term weights) exist only there
+  pl.block = pl.n_rb >= 2 || train;
   pl.n_rg = pl.block ? (pl.n_rb + kBWaves - 1) / kBWaves : pl.n_rb;
   pl.units_g = num_views * S * Hkv * pl.n_rg;
   pl.units_f = with_full ? S * Hkv * pl.n_rg : 0;
@@ -1099,18 +1072,29 @@ static hipError_t launch_nt(const AttnParams& p, int nblocks, hipStream_t stream
 
 hipError_t launch_attn(const AttnParams& p, const AttnPlan& pl, bool paged, hipStream_t stream) {
   if (pl.block) {
-    if (paged) hipLaunchKernelGGL(block_kernel<true>, dim3(pl.nblk), dim3(kBThreads), 0, stream, p);
-    else hipLaunchKernelGGL(block_kernel<false>, dim3(pl.nblk), dim3(kBThreads), 0, stream, p);
+    const bool train = p.o32_g || p.o32_f;
+    if (train) {
+      if (paged) hipLaunchKernelGGL((block_kernel<true, true>), dim3(pl.nblk), dim3(kBThreads), 0, stream, p);
+      else hipLaunchKernelGGL((block_kernel<false, true>), dim3(pl.nblk), dim3(kBThreads), 0, stream, p);
+    } else {
+      if (paged) hipLaunchKernelGGL((block_kernel<true, false>), dim3(pl.nblk), dim3(kBThreads), 0, stream, p);
+      else hipLaunchKernelGGL((block_kernel<false, false>), dim3(pl.nblk), dim3(kBThreads), 0, stream, p);
+    }
     return hipGetLastError();
   }
   if (pl.nt == 1) return paged ? launch_nt<1, true>(p, pl.nblk, stream) : launch_nt<1, false>(p, pl.nblk, stream);
   return paged ? launch_nt<2, true>(p, pl.nblk, stream) : launch_nt<2, false>(p, pl.nblk, stream);
 }
 
-size_t attn_ws_bytes(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full) {
-  const size_t a = plan_attn(S, Hkv, Hq, nq, num_views, ld_idx, max_L, with_full, true).ws_bytes;
-  const size_t b = plan_attn(S, Hkv, Hq, nq, num_views, ld_idx, max_L, with_full, false).ws_bytes;
-  return a > b ? a : b;
+size_t attn_ws_bytes(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full,
+                     bool train_capable) {
+  size_t best = 0;
+  for (int paged = 0; paged < 2; ++paged)
+    for (int train = 0; train <= (train_capable ? 1 : 0); ++train) {
+      const size_t b = plan_attn(S, Hkv, Hq, nq, num_views, ld_idx, max_L, with_full, paged != 0, train != 0).ws_bytes;
+      best = b > best ? b : best;
+    }
+  return best;
 }
 
 size_t attn_record_floats(int nt) { return nt == 1 ? RowBlock<1>::kRec : RowBlock<2>::kRec; }

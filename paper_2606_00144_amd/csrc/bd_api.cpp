@@ -84,10 +84,11 @@ int64_t kv_extent(const bd_kv_desc* kv) {
 bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t nq, int32_t num_views,
                    const int32_t* idx, int32_t ld_idx, const int32_t* nsel, float scale, uint16_t* out_views,
                    float* lse_views, uint16_t* out_full, float* lse_full, void* ws, size_t ws_bytes,
-                   hipStream_t stream) {
+                   hipStream_t stream, float* o32_views = nullptr, float* o32_full = nullptr) {
+  const bool train = o32_views || o32_full;
   const bd::AttnPlan pl =
       bd::plan_attn(kv->num_seqs, kv->num_kv_heads, Hq, nq, num_views, ld_idx, kv->max_seq_len, out_full != nullptr,
-                    kv->page_table != nullptr);
+                    kv->page_table != nullptr, train);
   if (pl.nblk < 0 || (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f > INT32_MAX)
     return fail(BD_ERR_UNSUPPORTED, "problem too large for one launch");
   if (kv_extent(kv) > ((int64_t)1 << 34))
@@ -104,6 +105,8 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
   p.out_f = out_full;
   p.lse_g = lse_views;
   p.lse_f = lse_full;
+  p.o32_g = o32_views;
+  p.o32_f = o32_full;
   p.idx = idx;
   p.nsel = nsel;
   p.ld_idx = ld_idx;
@@ -251,12 +254,13 @@ size_t bd_multiview_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads,
       max_seq_len < 0)
     return 0;
   return bd::attn_ws_bytes(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld_idx, max_seq_len,
-                           with_full != 0);
+                           with_full != 0, true);
 }
 
 bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t num_q_heads, int32_t block_len,
                             int32_t num_views, const int32_t* idx_views, int32_t ld_idx, const int32_t* nsel_views,
-                            float scale, uint16_t* out_views, uint16_t* out_full, void* ws, size_t ws_bytes,
+                            float scale, uint16_t* out_views, float* lse_views, float* out32_views,
+                            uint16_t* out_full, float* lse_full, float* out32_full, void* ws, size_t ws_bytes,
                             hipStream_t stream) {
   bd_status st = check_kv(kv, true, num_q_heads);
   if (st != BD_OK) return st;
@@ -266,11 +270,111 @@ bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t
   if (num_views > 0 && (!idx_views || !nsel_views || !out_views || !aligned(out_views, 16) || ld_idx < 0))
     return fail(BD_ERR_INVALID_ARG, "views need idx_views, nsel_views, ld_idx >= 0 and a 16-byte aligned out_views");
   if (out_full && !aligned(out_full, 16)) return fail(BD_ERR_INVALID_ARG, "out_full is not 16-byte aligned");
+  if ((num_views > 0 && out32_views && !aligned(out32_views, 16)) || (out_full && out32_full && !aligned(out32_full, 16)))
+    return fail(BD_ERR_INVALID_ARG, "out32_views and out32_full must be 16-byte aligned");
   if (!std::isfinite(scale) || !(scale > 0.f)) return fail(BD_ERR_INVALID_ARG, "scale must be positive and finite");
   if ((int64_t)block_len * (num_q_heads / kv->num_kv_heads) > (1 << 20))
     return fail(BD_ERR_UNSUPPORTED, "block_len * group too large");
   return run_attn(kv, q_blk, num_q_heads, block_len, num_views, idx_views, num_views > 0 ? ld_idx : 0, nsel_views,
-                  scale, out_views, nullptr, out_full, nullptr, ws, ws_bytes, stream);
+                  scale, out_views, num_views > 0 ? lse_views : nullptr, out_full, out_full ? lse_full : nullptr, ws,
+                  ws_bytes, stream, num_views > 0 ? out32_views : nullptr, out_full ? out32_full : nullptr);
+}
+
+// ---------------------------------------------------------------- multiview backward
+size_t bd_multiview_attn_bwd_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
+                                             int32_t block_len, int32_t num_views, int32_t ld_idx,
+                                             int32_t max_seq_len, int32_t with_full) {
+  if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || block_len < 1 || num_views < 0 || ld_idx < 0 ||
+      max_seq_len < 0)
+    return 0;
+  const int32_t ld = num_views > 0 ? ld_idx : 0;
+  const size_t a = bd::plan_attn_bwd(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld, max_seq_len,
+                                     with_full != 0, true, true).ws_bytes;
+  const size_t b = bd::plan_attn_bwd(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld, max_seq_len,
+                                     with_full != 0, false, true).ws_bytes;
+  return a > b ? a : b;
+}
+
+bd_status bd_multiview_attn_bwd(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t num_q_heads, int32_t block_len,
+                                int32_t num_views, const int32_t* idx_views, int32_t ld_idx,
+                                const int32_t* nsel_views, float scale, const float* out32_views,
+                                const float* lse_views, const uint16_t* dout_views, const float* out32_full,
+                                const float* lse_full, const uint16_t* dout_full, float* dq, float* dk_blk,
+                                float* dv_blk, void* ws, size_t ws_bytes, hipStream_t stream) {
+  bd_status st = check_kv(kv, true, num_q_heads);
+  if (st != BD_OK) return st;
+  const bool full = dout_full != nullptr;
+  if (block_len < 1 || num_views < 0 || num_views + (full ? 1 : 0) < 1)
+    return fail(BD_ERR_INVALID_ARG, "need block_len >= 1 and at least one view or the full branch");
+  if (block_len > bd::kMaxBwdBlock) return fail(BD_ERR_UNSUPPORTED, "block_len above %d", bd::kMaxBwdBlock);
+  if ((int64_t)block_len * (num_q_heads / kv->num_kv_heads) > (1 << 20))
+    return fail(BD_ERR_UNSUPPORTED, "block_len * group too large");
+  if (!q_blk || !aligned(q_blk, 16)) return fail(BD_ERR_INVALID_ARG, "q_blk is NULL or not 16-byte aligned");
+  if (num_views > 0 && (!idx_views || !nsel_views || ld_idx < 0 || !out32_views || !aligned(out32_views, 16) ||
+                        !lse_views || !dout_views || !aligned(dout_views, 16)))
+    return fail(BD_ERR_INVALID_ARG,
+                "views need idx_views, nsel_views, ld_idx >= 0, lse_views and 16-byte aligned out32_views, dout_views");
+  if ((out32_full != nullptr) != full || (lse_full != nullptr) != full)
+    return fail(BD_ERR_INVALID_ARG, "out32_full, lse_full and dout_full must be all NULL or all given");
+  if (full && (!aligned(out32_full, 16) || !aligned(dout_full, 16)))
+    return fail(BD_ERR_INVALID_ARG, "out32_full and dout_full must be 16-byte aligned");
+  if (!dq || !aligned(dq, 16)) return fail(BD_ERR_INVALID_ARG, "dq is NULL or not 16-byte aligned");
+  if ((dk_blk != nullptr) != (dv_blk != nullptr) || (dk_blk && (!aligned(dk_blk, 16) || !aligned(dv_blk, 16))))
+    return fail(BD_ERR_INVALID_ARG, "dk_blk and dv_blk must be both NULL or both given, 16-byte aligned");
+  if (!std::isfinite(scale) || !(scale > 0.f)) return fail(BD_ERR_INVALID_ARG, "scale must be positive and finite");
+  if (kv_extent(kv) > ((int64_t)1 << 34))
+    return fail(BD_ERR_UNSUPPORTED, "K/V layout spans more than 2^34 elements");
+  const int32_t ld = num_views > 0 ? ld_idx : 0;
+  const bool paged = kv->page_table != nullptr;
+  const bd::AttnBwdPlan pl = bd::plan_attn_bwd(kv->num_seqs, kv->num_kv_heads, num_q_heads, block_len, num_views, ld,
+                                               kv->max_seq_len, full, paged, dk_blk != nullptr);
+  if ((int64_t)pl.units + (int64_t)kv->num_seqs * kv->num_kv_heads > BD_WS_COUNTER_LINES)
+    return fail(BD_ERR_UNSUPPORTED, "more than %d work units", BD_WS_COUNTER_LINES);
+  if ((int64_t)pl.nblk_q > INT32_MAX / 2 || (int64_t)pl.nb * 2 * 16 * BD_HEAD_DIM * 4 > INT32_MAX ||
+      (int64_t)pl.nbr * block_len * 2 * BD_HEAD_DIM * 4 > INT32_MAX)
+    return fail(BD_ERR_UNSUPPORTED, "problem too large for one launch");
+  st = check_ws(ws, ws_bytes, pl.ws_bytes);
+  if (st != BD_OK) return st;
+  bd::AttnBwdParams p{};
+  p.kv = bd::make_kv_view(*kv);
+  p.q = q_blk;
+  p.o32_g = out32_views;
+  p.lse_g = lse_views;
+  p.dout_g = dout_views;
+  p.o32_f = out32_full;
+  p.lse_f = lse_full;
+  p.dout_f = dout_full;
+  p.idx = idx_views;
+  p.nsel = nsel_views;
+  p.ld_idx = ld;
+  p.S = kv->num_seqs;
+  p.Hkv = kv->num_kv_heads;
+  p.Hq = num_q_heads;
+  p.G = num_q_heads / kv->num_kv_heads;
+  p.C = block_len;
+  p.V = num_views;
+  p.R = pl.R;
+  p.n_rb = pl.n_rb;
+  p.n_rg = pl.n_rg;
+  p.nsplit_g = pl.nsplit_g;
+  p.kps_g = pl.kps_g;
+  p.nsplit_f = pl.nsplit_f;
+  p.kps_f = pl.kps_f;
+  p.nb = pl.nb;
+  p.units = pl.units;
+  p.nblk_g = pl.nblk_g;
+  p.nbr = pl.nbr;
+  p.scale = scale;
+  p.scale_log2 = scale * 1.4426950408889634f;
+  p.max_roff = (uint32_t)((kv_extent(kv) - BD_HEAD_DIM) >> 3);
+  p.dq = dq;
+  p.dk = dk_blk;
+  p.dv = dv_blk;
+  char* w = static_cast<char*>(ws);
+  p.counters = reinterpret_cast<uint32_t*>(w);
+  p.part_q = pl.q_record_bytes ? reinterpret_cast<float*>(w + pl.counter_bytes) : nullptr;
+  p.part_kv = pl.kv_record_bytes ? reinterpret_cast<float*>(w + pl.counter_bytes + pl.q_record_bytes) : nullptr;
+  return launched(bd::launch_attn_bwd(p, pl, paged, stream));
 }
 
 // ---------------------------------------------------------------- verify

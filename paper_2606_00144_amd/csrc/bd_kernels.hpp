@@ -21,6 +21,8 @@ struct AttnParams {
   uint16_t* out_f;          // full branch: [S][nq][Hq][D]
   float* lse_g;             // nullable [V][S][nq][Hq]
   float* lse_f;             // nullable [S][nq][Hq]
+  float* o32_g;             // nullable fp32 outputs of the views (block mode only; selects the two-term weights)
+  float* o32_f;             // nullable fp32 output of the full branch (block mode only)
   const int32_t* idx;       // [V][S][Hkv][ld_idx]
   const int32_t* nsel;      // [V][S]
   int32_t ld_idx;
@@ -49,13 +51,61 @@ struct AttnPlan {
 };
 
 // `paged`: the cache is paged (the full branch then also goes through the slot table, which
-// bounds its splits).  Workspace queries that do not know the layout take the larger of the two
-// plans (attn_ws_bytes).
-AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full, bool paged);
+// bounds its splits).  `train`: fp32 outputs are requested (block mode with two-term weights).
+// Workspace queries that do not know the layout take the largest of the plans (attn_ws_bytes).
+AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full, bool paged,
+                   bool train = false);
 hipError_t launch_attn(const AttnParams& p, const AttnPlan& pl, bool paged, hipStream_t stream);
 size_t attn_record_floats(int nt);
-// Workspace bytes that serve either layout (paged or contiguous) of the given shape.
-size_t attn_ws_bytes(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full);
+// Workspace bytes that serve either layout (paged or contiguous) of the given shape, and with
+// train_capable also the training outputs.
+size_t attn_ws_bytes(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full,
+                     bool train_capable = false);
+
+// ---- multiview attention backward -------------------------------------------
+// Branch b of a (sequence, KV head) pair is view b (b < V) or the full cache (b == V).
+constexpr int kMaxBwdBlock = 1024;   // block rows C the dK/dV kernel keeps key counts for
+
+struct AttnBwdParams {
+  KvView kv;
+  const uint16_t* q;         // [S][C][Hq][D]
+  const float* o32_g;        // views: fp32 forward outputs [V][S][C][Hq][D]
+  const float* lse_g;        // views: log-sum-exp [V][S][C][Hq]
+  const uint16_t* dout_g;    // views: upstream gradients [V][S][C][Hq][D]
+  const float* o32_f;        // full branch (NULL: none)
+  const float* lse_f;
+  const uint16_t* dout_f;
+  const int32_t* idx;        // [V][S][Hkv][ld_idx]
+  const int32_t* nsel;       // [V][S]
+  int32_t ld_idx;
+  int32_t S, Hkv, Hq, G, C, V;
+  int32_t R;                 // rows per (s, g): C * G
+  int32_t n_rb, n_rg;        // 32-row blocks, groups of 8 of them
+  int32_t nsplit_g, kps_g;   // view splits and entries per split
+  int32_t nsplit_f, kps_f;   // full-branch splits and keys per split
+  int32_t nb;                // dQ partials per unit: V * nsplit_g + (full ? nsplit_f : 0)
+  int32_t units;             // S * Hkv * n_rg (dQ units; their counters come first)
+  int32_t nblk_g;            // dQ workgroups of the views (they come first)
+  int32_t nbr;               // branches: V + (full ? 1 : 0)
+  float scale, scale_log2;
+  uint32_t max_roff;         // largest valid row offset of the K/V layout, 16-byte units
+  float* dq;                 // [S][C][Hq][D]
+  float* dk;                 // nullable [S][C][Hkv][D] (with dv)
+  float* dv;
+  float* part_q;             // dQ partial records
+  float* part_kv;            // dK/dV partial records, one per (s, g, branch)
+  uint32_t* counters;
+};
+
+struct AttnBwdPlan {
+  int n_rb, n_rg, R;
+  int nsplit_g, kps_g, nsplit_f, kps_f, nb, units, nblk_q, nblk_g, nbr;
+  size_t counter_bytes, q_record_bytes, kv_record_bytes, ws_bytes;
+};
+
+AttnBwdPlan plan_attn_bwd(int S, int Hkv, int Hq, int C, int num_views, int ld_idx, int max_L, bool with_full,
+                          bool paged, bool with_dkv);
+hipError_t launch_attn_bwd(const AttnBwdParams& p, const AttnBwdPlan& pl, bool paged, hipStream_t stream);
 
 // ---- greedy acceptance -----------------------------------------------------
 struct AcceptParams {

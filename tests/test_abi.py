@@ -93,10 +93,12 @@ def test_decode_select_multiview_accept_rejections(L):
     assert sel(P=301) == 2
     assert sel(kv=_kv(max_seq_len=40000)) == 2                              # prefix above BD_SELECT_MAX_PREFIX
     mv = lambda **a: L.bd_multiview_attn(ctypes.byref(kv), FAKE, 32, a.get("C", 64), a.get("V", 4), FAKE, 1024, FAKE,
-                                         0.1, a.get("ov", FAKE), a.get("of", FAKE), FAKE, 1 << 40, None)
+                                         0.1, a.get("ov", FAKE), None, None, a.get("of", FAKE), None, a.get("o32f"),
+                                         FAKE, 1 << 40, None)
     assert mv(C=0) == 1
     assert mv(V=0, of=None) == 1
     assert mv(ov=None) == 1
+    assert mv(o32f=FAKE + 8) == 1                                            # misaligned fp32 output
     acc = lambda **a: L.bd_accept_len(a.get("lg", FAKE), a.get("rs", 32000), a.get("dr", FAKE), 2, a.get("g", 5),
                                       32000, FAKE, None, None, FAKE, 1 << 40, None)
     assert acc(lg=None) == 1
@@ -105,12 +107,41 @@ def test_decode_select_multiview_accept_rejections(L):
     assert acc(dr=None) == 1
 
 
+def test_multiview_bwd_rejections(L):
+    kv = _kv()
+
+    def bwd(**a):
+        g = lambda n, d=FAKE: a.get(n, d)
+        return L.bd_multiview_attn_bwd(ctypes.byref(g("kv", kv)), g("q"), 32, g("C", 64), g("V", 4), g("idx"), 1024,
+                                       g("nsel"), g("scale", 0.1), g("ov"), g("lv"), g("dov"), g("of"), g("lf"),
+                                       g("dof"), g("dq"), g("dk"), g("dv"), g("ws"), g("wsb", 1 << 40), None)
+    assert bwd(C=0) == bd.BD_ERR_INVALID_ARG
+    assert bwd(C=2048) == bd.BD_ERR_UNSUPPORTED                             # block above 1024 rows
+    assert bwd(V=0, dof=None, of=None, lf=None) == bd.BD_ERR_INVALID_ARG   # no branch at all
+    assert bwd(lv=None) == bd.BD_ERR_INVALID_ARG                          # views need their lse
+    assert bwd(dov=FAKE + 4) == bd.BD_ERR_INVALID_ARG
+    assert bwd(lf=None) == bd.BD_ERR_INVALID_ARG                          # full branch half given
+    assert bwd(of=None) == bd.BD_ERR_INVALID_ARG
+    assert bwd(dq=None) == bd.BD_ERR_INVALID_ARG
+    assert bwd(dk=None) == bd.BD_ERR_INVALID_ARG                          # dk without dv
+    assert bwd(scale=float("inf")) == bd.BD_ERR_INVALID_ARG
+    assert bwd(q=FAKE + 2) == bd.BD_ERR_INVALID_ARG
+    assert bwd(kv=_kv(v=0)) == bd.BD_ERR_INVALID_ARG
+    assert bwd(ws=None) == bd.BD_ERR_WORKSPACE
+    assert bwd(wsb=1024) == bd.BD_ERR_WORKSPACE
+    big = _kv(num_seqs=4096, num_kv_heads=8, max_seq_len=64, stride_seq=8 * 64 * 128, stride_head=64 * 128)
+    assert bwd(kv=big) == bd.BD_ERR_UNSUPPORTED                           # counter lines exhausted
+
+
 def test_workspace_sizes(L):
     v = L.bd_verify_attn_workspace_bytes(8, 8, 32, 5, 16384)
     assert v > 0 and v % 256 == 0
     assert L.bd_sparse_decode_attn_workspace_bytes(8, 8, 32, 1024) > 0
     assert L.bd_select_kv_workspace_bytes(8, 8, 32, 32, 16384) >= 8 * 8 * 16384 * 4
     assert L.bd_multiview_attn_workspace_bytes(4, 8, 32, 64, 4, 2048, 8192, 1) > 0
+    w = L.bd_multiview_attn_bwd_workspace_bytes(4, 8, 32, 64, 4, 2048, 8192, 1)
+    assert w > (1 << 20) and w % 256 == 0
+    assert L.bd_multiview_attn_bwd_workspace_bytes(4, 8, 32, 0, 4, 2048, 8192, 1) == 0
     assert L.bd_accept_len_workspace_bytes(8, 5, 128256) > 0
     assert L.bd_verify_attn_workspace_bytes(0, 8, 32, 5, 16384) == 0        # invalid shape -> 0
 
