@@ -240,7 +240,7 @@ bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t
  * dk_blk, dv_blk  NULL (skipped) or both [S][C][Hkv][128] fp32: row c is the
  *            gradient of cache row L_s - C + c of KV head g (0 where that position is < 0).
  * Requirements: 1 <= C <= 1024, C * G <= 1048576, V >= 0, at least one branch,
- * S * Hkv * (1 + ceil(C*G/256)) <= BD_WS_COUNTER_LINES.  Results do not depend on
+ * S * Hkv * (ceil(C*G/256) + 1) <= BD_WS_COUNTER_LINES.  Results do not depend on
  * scheduling (fixed summation order).
  * ---------------------------------------------------------------------- */
 size_t bd_multiview_attn_bwd_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,

@@ -13,28 +13,32 @@
 // and the branches add up.  The forward's log-sum-exp gives P directly, so no
 // pass recomputes softmax statistics.
 //
-// dQ kernel.  Like the forward's block mode: a workgroup of 8 waves owns one
-// (branch, sequence, KV head, row group, key split); wave w owns the 32-row
-// block 8*rg + w and every wave consumes every 32-key tile from a shared LDS
-// ring filled by direct-to-LDS loads.  A tile carries K and V in the score
-// operand layout and K a second time in the transposed layout of the dQ
-// product, so every LDS read is a linear 1 KiB per instruction.  Per tile a
-// wave runs three MFMA products (keys on the M side throughout):
+// dQ kernel.  Like the forward's block mode: a workgroup of 8 waves owns a
+// share of one (sequence, KV head, row group) unit's key stream (the views'
+// entry lists followed by the full branch's cache rows, cut into equal ranges
+// at run time, when the list lengths are known); wave w owns the 32-row block
+// 8*rg + w and every wave consumes every 32-key tile from a shared LDS ring
+// filled by direct-to-LDS loads.  A tile carries K and V in the score operand
+// layout and K a second time in the transposed layout of the dQ product, so
+// every LDS read is a linear 1 KiB per instruction.  Per tile a wave runs
+// three MFMA products (keys on the M side throughout):
 //   S^T  [key][row] = K . Q^T          A = K tile,  B = Q^T   (registers)
 //   dP^T [key][row] = V . dO^T         A = V tile,  B = dO^T  (registers)
 //   dQ^T [d][row]  += K^T . dS^T       A = K^T,     B = dS^T  (P, dS never leave registers)
-// Partial dQ of every (branch, split) goes to a record; the last workgroup of
-// the (sequence, KV head, row group) adds them in (branch, split) order, so the
-// result does not depend on which workgroup finishes when.
+// dQ sums over the branches, so one accumulator serves the whole range.  Each
+// workgroup's partial goes to a record; the last workgroup of the unit adds
+// them in workgroup order, so the result does not depend on scheduling.  The
+// workgroup holding a branch's first entry also publishes each row's (lse, D)
+// for dK/dV.
 //
 // dK/dV kernel.  One workgroup of 4 waves per (sequence, KV head, branch);
-// wave w owns the 16 block keys of key tile w (then w+4, ...).  Row tiles of 32
-// query rows are staged in padded row-major LDS (conflict-free for both the
-// row-major and the transposed reads) and each wave runs, per row tile,
+// wave w owns 16 block keys, and the branch's query rows stream through a
+// direct-to-LDS ring in 32-row tiles (Q and dO, each in the A-operand and the
+// transposed layout).  Per tile a wave runs
 //   S  [row][key] = Q . K_blk^T        dP [row][key] = dO . V_blk^T
 //   dV^T [d][key] += dO^T . P          dK^T [d][key] += Q^T . dS
-// (P and dS again as bf16 pairs hi + lo).
-// The branches' partials meet in records summed in branch order by the last.
+// (P and dS as bf16 pairs hi + lo).  The branches' partials meet in records
+// summed in branch order by the last workgroup of the (sequence, KV head).
 
 #include "bd_common.hpp"
 #include "bd_kernels.hpp"
@@ -62,6 +66,16 @@ struct DqSmem {
   alignas(16) uint8_t ring[kQRing][kQTileBytes];
   int32_t last;
 };
+
+// n / d for 0 <= n < 2^22, d >= 1, with inv_d = 1/d: the float estimate is within one of the
+// quotient, and one correction each way makes it exact (a VALU integer division costs tens of
+// instructions, and the dK/dV tile loop needs several per row).
+__device__ inline int div_small(int n, int d, float inv_d) {
+  int q = (int)((float)n * inv_d);
+  q += (q + 1) * d <= n ? 1 : 0;
+  q -= q * d > n ? 1 : 0;
+  return q;
+}
 
 // Tile load q of a lane (0..23).  q < 8: K, score layout (key sub-tile q/4 -> rows 16*(q/4) + lane%16,
 // 16 bytes at d = 32*(lane/16) + 8*(q%4)); 8 <= q < 16: V, same layout; 16 <= q < 24: K, transposed
@@ -208,84 +222,80 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lg = lane >> 4, lr = lane & 15;
 
-  // ---- (branch, sequence, head, row group, split) of this workgroup
+  // ---- unit (sequence, KV head, row group) and this workgroup's share w of the unit's key stream
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const bool gather = bid < p.nblk_g;
-  const int local = gather ? bid : bid - p.nblk_g;
-  const int nsplit = gather ? p.nsplit_g : p.nsplit_f;
-  const int kps = gather ? p.kps_g : p.kps_f;
-  const int rg = local % p.n_rg;
-  const int rest = local / p.n_rg;
-  const int split = rest % nsplit;
-  const int pair = rest / nsplit;
-  const int g = pair % p.Hkv;
-  const int vs = pair / p.Hkv;                   // gather: view*S + s; full: s
-  const int s = gather ? vs % p.S : vs;
-  const int view = gather ? vs / p.S : 0;
-  const int unit = (s * p.Hkv + g) * p.n_rg + rg;
-  const int k_rec = gather ? view * p.nsplit_g + split : p.V * p.nsplit_g + split;
+  const int w = bid % p.nW;
+  const int unit = bid / p.nW;
+  const int rg = unit % p.n_rg;
+  const int pair = unit / p.n_rg;
+  const int g = pair % p.Hkv, s = pair / p.Hkv;
   const int rb = rg * kQWaves + wave;
   const bool has_rows = rb < p.n_rb;
-
   const int L = seq_len(p.kv, s);
-  int n_keys;
-  const int32_t* idx_row = nullptr;
-  if (gather) {
-    idx_row = p.idx + ((int64_t)vs * p.Hkv + g) * p.ld_idx;
-    const int n = p.nsel[vs];
-    n_keys = n < 0 ? 0 : (n > p.ld_idx ? p.ld_idx : n);
-  } else {
-    n_keys = L;
-  }
-  const int e_begin = split * kps;
-  int e_end = e_begin + kps;
-  if (e_end > n_keys) e_end = n_keys;
-  const int ntiles = e_end > e_begin ? (e_end - e_begin + kTile - 1) / kTile : 0;
 
-  // ---- this wave's rows: Q, dO, lse and D = <dO, O>
+  // The key stream of a unit is the views' entry lists followed by the full branch's cache rows;
+  // its actual length is known only here (nsel lives on the device), so the unit's nW workgroups
+  // cut it into equal ranges at run time.  A range crossing a branch boundary runs one piece per
+  // branch (each with the branch's dO, D and lse rows).
+  auto branch_len = [&](int b) -> int {
+    if (b < p.V) {
+      const int n = p.nsel[b * p.S + s];
+      return n < 0 ? 0 : (n > p.ld_idx ? p.ld_idx : n);
+    }
+    return L;
+  };
+  int total = 0;
+  for (int b = 0; b < p.nbr; ++b) total += branch_len(b);
+  int chunk = (total + p.nW - 1) / p.nW;
+  chunk = (chunk + kTile - 1) / kTile * kTile;
+  const int r0 = w * chunk;
+  const int r1 = r0 + chunk < total ? r0 + chunk : total;
+
+  // ---- this wave's rows: Q once; dO, lse and D = <dO, O> per branch
   const int64_t branch_rows = (int64_t)p.S * p.C * p.Hq;
-  const float* outb = gather ? p.o32_g + (int64_t)view * branch_rows * kD : p.o32_f;
-  const uint16_t* doutb = gather ? p.dout_g + (int64_t)view * branch_rows * kD : p.dout_f;
-  const float* lseb = gather ? p.lse_g + (int64_t)view * branch_rows : p.lse_f;
   DqRows rw;
+  int64_t orow[2];
+  bool rvalid[2];
 #pragma unroll
   for (int nt = 0; nt < 2; ++nt) {
     const int n = rb * 32 + 16 * nt + lr;
-    const bool valid = has_rows && n < p.R;
-    const int j = valid ? n / p.G : 0;
-    const int h = g * p.G + (valid ? n % p.G : 0);
-    const int64_t orow = ((int64_t)s * p.C + j) * p.Hq + h;
-    rw.rowpos[nt] = valid ? L - p.C + j : 0x7FFFFFFF;
-    float dsum = 0.f;
+    rvalid[nt] = has_rows && n < p.R;
+    const int j = rvalid[nt] ? n / p.G : 0;
+    const int h = g * p.G + (rvalid[nt] ? n % p.G : 0);
+    orow[nt] = ((int64_t)s * p.C + j) * p.Hq + h;
+    rw.rowpos[nt] = rvalid[nt] ? L - p.C + j : 0x7FFFFFFF;
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int64_t off = orow * kD + 32 * lg + 8 * kk;
-      const u32x4 qv = valid ? load16(p.q + off) : u32x4{0u, 0u, 0u, 0u};
-      const u32x4 dv = valid ? load16(doutb + off) : u32x4{0u, 0u, 0u, 0u};
-      const f32x4 o0 = valid ? *reinterpret_cast<const f32x4*>(outb + off) : f32x4{0.f, 0.f, 0.f, 0.f};
-      const f32x4 o1 = valid ? *reinterpret_cast<const f32x4*>(outb + off + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
-      rw.qop[nt][kk] = as_bf16x8(qv);
-      rw.dop[nt][kk] = as_bf16x8(dv);
+    for (int kk = 0; kk < 4; ++kk)
+      rw.qop[nt][kk] = as_bf16x8(rvalid[nt] ? load16(p.q + orow[nt] * kD + 32 * lg + 8 * kk) : u32x4{0u, 0u, 0u, 0u});
+  }
+  auto load_branch_rows = [&](int b) {
+    const bool gb = b < p.V;
+    const float* outb = gb ? p.o32_g + (int64_t)b * branch_rows * kD : p.o32_f;
+    const uint16_t* doutb = gb ? p.dout_g + (int64_t)b * branch_rows * kD : p.dout_f;
+    const float* lseb = gb ? p.lse_g + (int64_t)b * branch_rows : p.lse_f;
 #pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        dsum += bf16_lo(dv[e]) * o0[2 * e] + bf16_hi(dv[e]) * o0[2 * e + 1];
-        dsum += bf16_lo(dv[e + 2]) * o1[2 * e] + bf16_hi(dv[e + 2]) * o1[2 * e + 1];
+    for (int nt = 0; nt < 2; ++nt) {
+      float dsum = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const int64_t off = orow[nt] * kD + 32 * lg + 8 * kk;
+        const u32x4 dv = rvalid[nt] ? load16(doutb + off) : u32x4{0u, 0u, 0u, 0u};
+        const f32x4 o0 = rvalid[nt] ? *reinterpret_cast<const f32x4*>(outb + off) : f32x4{0.f, 0.f, 0.f, 0.f};
+        const f32x4 o1 = rvalid[nt] ? *reinterpret_cast<const f32x4*>(outb + off + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+        rw.dop[nt][kk] = as_bf16x8(dv);
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          dsum += bf16_lo(dv[e]) * o0[2 * e] + bf16_hi(dv[e]) * o0[2 * e + 1];
+          dsum += bf16_lo(dv[e + 2]) * o1[2 * e] + bf16_hi(dv[e + 2]) * o1[2 * e + 1];
+        }
       }
+      rw.Dr[nt] = sum_xor32(sum_xor16(dsum));
+      const float l2 = rvalid[nt] ? lseb[orow[nt]] * kLog2e : INFINITY;
+      rw.lse2[nt] = l2 == -INFINITY ? INFINITY : l2;   // a row that saw no key has all-zero weights
     }
-    rw.Dr[nt] = sum_xor32(sum_xor16(dsum));
-    const float l2 = valid ? lseb[orow] * kLog2e : INFINITY;
-    rw.lse2[nt] = l2 == -INFINITY ? INFINITY : l2;   // a row that saw no key has all-zero weights
-  }
+  };
 
-  const bool arith = !PAGED && !gather;
-  if (!arith) {
-    const int nslots = (ntiles + kQRing) * kTile;
-    fill_slot_table<PAGED, kQThreads, kQSlotCap>(p.kv, s, g, L, idx_row, e_begin, e_end, nslots, sm.roff, sm.tpos,
-                                                 tid);
-    __syncthreads();
-  }
   const int minpos = L - p.C + (rb * 32) / p.G;   // earliest row position of this wave
-
   f32x4 acc[2][8];
 #pragma unroll
   for (int nt = 0; nt < 2; ++nt)
@@ -296,17 +306,8 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
   const int q0 = 3 * wave;
   const int rit0 = load_row_in_tile(q0, lane), rit1 = load_row_in_tile(q0 + 1, lane),
             rit2 = load_row_in_tile(q0 + 2, lane);
-  const uint32_t base16 = arith ? (uint32_t)(((int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head) >> 3) : 0u;
-  const uint32_t tok16 = (uint32_t)(p.kv.stride_tok >> 3);
   const uint32_t roff_lds = lds_addr(sm.roff), tpos_lds = lds_addr(sm.tpos);
   const uint32_t ring_lds = lds_addr(sm.ring[0]);
-  auto arith_rows = [&](int tile, uint32_t (&r)[3]) {
-    if (tile >= ntiles) { r[0] = r[1] = r[2] = 0u; return; }   // padding: row 0, a cache-resident address
-    const uint32_t r0 = base16 + (uint32_t)(e_begin + kTile * tile) * tok16;
-    r[0] = r0 + (uint32_t)rit0 * tok16;
-    r[1] = r0 + (uint32_t)rit1 * tok16;
-    r[2] = r0 + (uint32_t)rit2 * tok16;
-  };
   auto issue = [&](int tile, const uint32_t (&r)[3]) {
     uint8_t* dst = sm.ring[tile % kQRing];
     dq_dma_load(p.kv, r[0], p.max_roff, q0, dst, lane);
@@ -314,30 +315,20 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
     dq_dma_load(p.kv, r[2], p.max_roff, q0 + 2, dst, lane);
   };
 
-  auto stream = [&](auto arith_tag) {
-    constexpr bool ARITH = decltype(arith_tag)::value;
+  // entries e_begin .. e_end-1 of one branch through the slot table (a piece never exceeds it)
+  auto stream = [&](int e_begin, int e_end) {
+    const int ntiles = (e_end - e_begin + kTile - 1) / kTile;
     for (int t = 0; t < kQRing - 1; ++t) {
       uint32_t r[3];
-      if constexpr (ARITH) {
-        arith_rows(t, r);
-      } else {
-        asm volatile(
-            "ds_read_b32 %0, %3\n"
-            "ds_read_b32 %1, %4\n"
-            "ds_read_b32 %2, %5\n"
-            "s_waitcnt lgkmcnt(0)"
-            : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2])
-            : "v"(roff_lds + 4 * (kTile * t + rit0)), "v"(roff_lds + 4 * (kTile * t + rit1)),
-              "v"(roff_lds + 4 * (kTile * t + rit2)));
-      }
+      asm volatile(
+          "ds_read_b32 %0, %3\n"
+          "ds_read_b32 %1, %4\n"
+          "ds_read_b32 %2, %5\n"
+          "s_waitcnt lgkmcnt(0)"
+          : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2])
+          : "v"(roff_lds + 4 * (kTile * t + rit0)), "v"(roff_lds + 4 * (kTile * t + rit1)),
+            "v"(roff_lds + 4 * (kTile * t + rit2)));
       issue(t, r);
-    }
-    int fd_arith = 0;
-    if constexpr (ARITH) {
-      const int c1 = minpos - e_begin - (kTile - 1);
-      const int fd1 = c1 < 0 ? 0 : c1 / kTile + 1;
-      const int fd2 = (e_end - e_begin) / kTile;
-      fd_arith = fd1 < fd2 ? fd1 : fd2;
     }
     for (int t = 0; t < ntiles; ++t) {
       // this wave's loads of tile t are older than the kQRing-2 tiles issued after it
@@ -347,52 +338,52 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
       const uint32_t src = ring_lds + (uint32_t)(t % kQRing) * kQTileBytes;
       u32x4 kreg[8];
       uint32_t r[3];
-      bool dirty;
       u32x4 tp[2];
-      if constexpr (ARITH) {
-        read8(kreg, src + 16 * lane);
-        arith_rows(nxt, r);
-        dirty = t >= fd_arith;
-      } else {
-        const int next0 = kTile * nxt;
-        read8_pos_rows(kreg, tp, r, src + 16 * lane, tpos_lds + 4 * (kTile * t + 4 * lg),
-                       roff_lds + 4 * (next0 + rit0), roff_lds + 4 * (next0 + rit1), roff_lds + 4 * (next0 + rit2));
-        bool bad = false;
+      const int next0 = kTile * nxt;
+      read8_pos_rows(kreg, tp, r, src + 16 * lane, tpos_lds + 4 * (kTile * t + 4 * lg),
+                     roff_lds + 4 * (next0 + rit0), roff_lds + 4 * (next0 + rit1), roff_lds + 4 * (next0 + rit2));
+      bool bad = false;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int tq = (int)tp[i >> 2][i & 3];
-          bad |= tq < 0 || tq > minpos;
-        }
-        dirty = __builtin_amdgcn_ballot_w64(bad) != 0;
+      for (int i = 0; i < 8; ++i) {
+        const int tq = (int)tp[i >> 2][i & 3];
+        bad |= tq < 0 || tq > minpos;
       }
+      const bool dirty = __builtin_amdgcn_ballot_w64(bad) != 0;
       issue(nxt, r);
-      if (has_rows) {
-        if constexpr (ARITH) {
-          const int slot0 = kTile * t;
-          dq_tile_step(acc, rw, kreg, src, lane, p.scale_log2, dirty, [&](int i) {
-            const int e = e_begin + slot0 + 16 * (i >> 2) + 4 * lg + (i & 3);
-            return e < e_end ? e : -1;
-          });
-        } else {
-          dq_tile_step(acc, rw, kreg, src, lane, p.scale_log2, dirty, [&](int i) { return (int)tp[i >> 2][i & 3]; });
-        }
-      }
+      if (has_rows)
+        dq_tile_step(acc, rw, kreg, src, lane, p.scale_log2, dirty, [&](int i) { return (int)tp[i >> 2][i & 3]; });
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the block ends
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the ring is reused
   };
-  if (ntiles > 0) {
-    if (arith) stream(BoolTag<true>{});
-    else stream(BoolTag<false>{});
+
+  int off = 0;
+  for (int b = 0; b < p.nbr; ++b) {
+    const int n = branch_len(b);
+    const int lo = r0 > off ? r0 : off, hi = r1 < off + n ? r1 : off + n;
+    off += n;
+    if (lo >= hi) continue;
+    const int e0 = lo - (off - n), e1 = hi - (off - n);
+    load_branch_rows(b);
+    if (e0 == 0 && p.rstats && lg == 0) {         // the branch's first workgroup publishes the row stats
+      float* rs = p.rstats + (((int64_t)b * p.S * p.Hkv + pair) * p.R_pad + rb * 32) * 2;
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt)
+        if (rvalid[nt]) *reinterpret_cast<float2*>(rs + 2 * (16 * nt + lr)) = float2{rw.lse2[nt], rw.Dr[nt]};
+    }
+    const int32_t* idx_row = b < p.V ? p.idx + (((int64_t)b * p.S + s) * p.Hkv + g) * p.ld_idx : nullptr;
+    const int nslots = ((e1 - e0 + kTile - 1) / kTile + kQRing) * kTile;
+    __syncthreads();                              // the previous piece's slot table and ring are free
+    fill_slot_table<PAGED, kQThreads, kQSlotCap>(p.kv, s, g, L, idx_row, e0, e1, nslots, sm.roff, sm.tpos, tid);
+    __syncthreads();
+    stream(e0, e1);
   }
 
   // ---- dQ rows 16*nt + lane%16; register i of d-tile dt holds d = 32*(lane/16) + 8*i + dt
   auto write_rows = [&](const f32x4 (&o)[2][8]) {
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
-      const int n = rb * 32 + 16 * nt + lr;
-      if (n >= p.R) continue;
-      const int j = n / p.G, h = g * p.G + n % p.G;
-      float* drow = p.dq + (((int64_t)s * p.C + j) * p.Hq + h) * kD + 32 * lg;
+      if (!rvalid[nt]) continue;
+      float* drow = p.dq + orow[nt] * kD + 32 * lg;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         *reinterpret_cast<f32x4*>(drow + 8 * i) =
@@ -402,16 +393,16 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
       }
     }
   };
-  if (p.nb == 1) {
+  if (p.nW == 1) {
     if (has_rows) write_rows(acc);
     return;
   }
 
-  // ---- publish this wave's partial as record k_rec of its row block: chunk (nt, dt) x lane float4s
+  // ---- publish this wave's partial as record w of its row block: chunk (nt, dt) x lane float4s
   const __amdgpu_buffer_rsrc_t urec =
-      make_rsrc(p.part_q + ((int64_t)unit * kQWaves + wave) * p.nb * kRecFloats, (uint32_t)(p.nb * kRecFloats * 4));
+      make_rsrc(p.part_q + ((int64_t)unit * kQWaves + wave) * p.nW * kRecFloats, (uint32_t)(p.nW * kRecFloats * 4));
   if (has_rows) {
-    const uint32_t rec = (uint32_t)k_rec * kRecFloats * 4;
+    const uint32_t rec = (uint32_t)w * kRecFloats * 4;
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
@@ -419,42 +410,67 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
   }
   wait_vmem();
   __syncthreads();
-  if (tid == 0) sm.last = arrive(counter_line(p.counters, unit), (uint32_t)p.nb);
+  if (tid == 0) sm.last = arrive(counter_line(p.counters, unit), (uint32_t)p.nW);
   __syncthreads();
   if (!sm.last) return;
   if (tid == 0) reset_counter(counter_line(p.counters, unit));
   if (!has_rows) return;
-  // sum the row block's partials in (branch, split) order
+  // sum the row block's partials in workgroup order, one 16-row half at a time; device-scope loads
+  // travel past the XCD's L2, so four records (32 loads) are in flight per round
 #pragma unroll
-  for (int nt = 0; nt < 2; ++nt)
+  for (int nt = 0; nt < 2; ++nt) {
+    f32x4 o[8];
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) acc[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int k = 0; k < p.nb; ++k) {
-    const uint32_t rec = (uint32_t)k * kRecFloats * 4;
+    for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int k = 0; k < p.nW; k += 4) {
+      f32x4 x[4][8];
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
+      for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) acc[nt][dt] += load16_coherent(urec, rec + 16 * ((nt * 8 + dt) * kWave + lane));
+        for (int dt = 0; dt < 8; ++dt)
+          x[kk][dt] = k + kk < p.nW
+                          ? load16_coherent(urec, (uint32_t)(k + kk) * kRecFloats * 4 + 16 * ((nt * 8 + dt) * kWave + lane))
+                          : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) o[dt] += x[kk][dt];
+    }
+    if (!rvalid[nt]) continue;
+    float* drow = p.dq + orow[nt] * kD + 32 * lg;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      *reinterpret_cast<f32x4*>(drow + 8 * i) = f32x4{o[0][i], o[1][i], o[2][i], o[3][i]} * p.scale;
+      *reinterpret_cast<f32x4*>(drow + 8 * i + 4) = f32x4{o[4][i], o[5][i], o[6][i], o[7][i]} * p.scale;
+    }
   }
-  write_rows(acc);
 }
 
 // ---- dK/dV kernel ---------------------------------------------------------------
+// One workgroup of 4 waves per (sequence, KV head, branch); wave w owns the 16 block keys of key
+// tile w (tiles w+4, w+8, ... in later passes).  The branch's query rows stream through an LDS ring
+// in 32-row tiles, each tile carrying Q and dO twice: in the A-operand layout of the S and dP
+// products and in the transposed layout of the dK and dV products, so every LDS read is linear.
 constexpr int kKWaves = 4;
 constexpr int kKThreads = kKWaves * kWave;
-constexpr int kPitch = 2 * kD + 16;   // bytes per staged row: the 16-byte pad spreads rows over the banks
+constexpr int kKRing = 3;                          // row-tile slots; kKRing-1 tiles in flight
+constexpr int kKLoads = 32;                        // 1 KiB pieces per row tile (8 per wave)
+constexpr int kKStatBytes = 32 * 8;                // the tile's rows' (lse2, D) pairs (64 bytes per wave)
+constexpr int kKTileBytes = kKLoads * 1024 + kKStatBytes;
 
 struct DkvSmem {
-  alignas(16) uint8_t q[32 * kPitch];
-  alignas(16) uint8_t dout[32 * kPitch];
-  float lse2[32];
-  float D[32];
-  int32_t cnt[kMaxBwdBlock];   // occurrences of block key c in the branch's key list
+  alignas(16) uint8_t ring[kKRing][kKTileBytes];
+  int32_t cnt[kMaxBwdBlock];                       // occurrences of block key c in the branch's key list
   int32_t last;
 };
 
-__device__ inline u32x4 lds_read16(const uint8_t* base, uint32_t off) {
-  return *reinterpret_cast<const u32x4*>(base + off);
+// Piece q (0..31) of a row tile for this lane: 0..7 Q in the A layout (rows 16*(q/4) + lane%16,
+// 16 bytes at d = 32*(lane/16) + 8*(q%4)), 8..15 Q transposed (rows 16*((q-8)/4) + 4*(lane/16) +
+// (q-8)%4, 16 bytes at d = 8*(lane%16)), 16..31 the same two for dO.
+__device__ inline void row_piece(int q, int lane, int& r, int& d) {
+  const int lg = lane >> 4, lr = lane & 15, x = q & 7;
+  if ((q & 8) == 0) { r = 16 * (x >> 2) + lr; d = 32 * lg + 8 * (x & 3); }
+  else { r = 16 * (x >> 2) + 4 * lg + (x & 3); d = 8 * lr; }
 }
 
 template <bool PAGED>
@@ -465,153 +481,174 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
   const int lg = lane >> 4, lr = lane & 15;
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
   const int br = bid % p.nbr;
-  const int pair = bid / p.nbr;            // s * Hkv + g
+  const int pair = bid / p.nbr;                  // s * Hkv + g
   const int g = pair % p.Hkv, s = pair / p.Hkv;
   const bool gather = br < p.V;
   const int L = seq_len(p.kv, s);
-  const int C = p.C, t0 = L - C;           // block row c sits at position t0 + c
+  const int C = p.C, t0 = L - C;                 // block row c sits at position t0 + c
 
-  // ---- key multiplicities of the branch
+  // ---- key multiplicities of the branch (all idx loads of a round issued before any atomic)
   for (int c = tid; c < C; c += kKThreads) sm.cnt[c] = (!gather && t0 + c >= 0) ? 1 : 0;
   __syncthreads();
   if (gather) {
     const int32_t* idx_row = p.idx + (((int64_t)br * p.S + s) * p.Hkv + g) * p.ld_idx;
     int n = p.nsel[br * p.S + s];
     n = n < 0 ? 0 : (n > p.ld_idx ? p.ld_idx : n);
-    for (int e = tid; e < n; e += kKThreads) {
-      const int t = idx_row[e];
-      if (t >= 0 && t < L && t >= t0) atomicAdd(&sm.cnt[t - t0], 1);
+    constexpr int kPer = 8;
+    for (int e0 = 0; e0 < n; e0 += kPer * kKThreads) {
+      int tv[kPer];
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        const int e = e0 + tid + k * kKThreads;
+        tv[k] = e < n ? idx_row[e] : -1;
+      }
+#pragma unroll
+      for (int k = 0; k < kPer; ++k)
+        if (tv[k] >= 0 && tv[k] < L && tv[k] >= t0) atomicAdd(&sm.cnt[tv[k] - t0], 1);
     }
     __syncthreads();
   }
 
   const int64_t branch_rows = (int64_t)p.S * C * p.Hq;
-  const float* outb = gather ? p.o32_g + (int64_t)br * branch_rows * kD : p.o32_f;
   const uint16_t* doutb = gather ? p.dout_g + (int64_t)br * branch_rows * kD : p.dout_f;
-  const float* lseb = gather ? p.lse_g + (int64_t)br * branch_rows : p.lse_f;
-  const int nkt = (C + 15) / 16;
+  // (lse2, D) of the branch's rows of this (s, g), published by the dQ kernel, rows padded to R_pad
+  const float* stats = p.rstats + ((int64_t)br * p.S * p.Hkv + pair) * p.R_pad * 2;
   const int nrt = (p.R + 31) / 32;
-  float* rec_k = p.part_kv + ((int64_t)pair * p.nbr + br) * C * 2 * kD;
-  float* rec_v = rec_k + (int64_t)C * kD;
+  const int nkt = (C + 15) / 16;
+  auto row_off = [&](int n) -> int64_t {         // rows past R read row 0 (their weights are zero)
+    const int nn = n < p.R ? n : 0;
+    const int j = div_small(nn, p.G, p.inv_G);
+    return ((int64_t)s * C + j) * p.Hq + g * p.G + (nn - j * p.G);
+  };
+  // this wave's 8 pieces of every row tile
+  int prow[8], pd[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) row_piece(8 * wave + k, lane, prow[k], pd[k]);
+  const uint16_t* psrc = wave < 2 ? p.q : doutb;
+  // 9 loads per wave and tile: its 8 pieces, and 64 bytes of the tile's row stats (lanes 0..3)
+  auto issue = [&](int rt) {
+    uint8_t* dst = sm.ring[rt % kKRing];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int n = rt < nrt ? 32 * rt + prow[k] : 0;   // padding tiles re-read row 0
+      dma16(psrc + row_off(n) * kD + pd[k], dst + (8 * wave + k) * 1024);
+    }
+    const int srt = rt < nrt ? rt : 0;
+    if (lane < 4)
+      dma16(reinterpret_cast<const uint16_t*>(stats + srt * 64 + 16 * wave) + 8 * lane,
+            dst + kKLoads * 1024 + 64 * wave);
+  };
+  const uint32_t ring_lds = lds_addr(sm.ring[0]);
+  const __amdgpu_buffer_rsrc_t rrec =
+      make_rsrc(p.part_kv + (int64_t)pair * p.nbr * C * 2 * kD, (uint32_t)((int64_t)p.nbr * C * 2 * kD * 4));
   const bool direct = p.nbr == 1;
-  const __amdgpu_buffer_rsrc_t rrec = make_rsrc(rec_k, (uint32_t)(C * 2 * kD * 4));
-  float* out_k = direct ? p.dk + (int64_t)s * C * p.Hkv * kD : rec_k;
-  float* out_v = direct ? p.dv + (int64_t)s * C * p.Hkv * kD : rec_v;
-  const int64_t out_stride = direct ? (int64_t)p.Hkv * kD : kD;   // floats between block rows
-  const int64_t out_head = direct ? (int64_t)g * kD : 0;
 
   for (int kt0 = 0; kt0 < nkt; kt0 += kKWaves) {
     const int kt = kt0 + wave;
-    const int c = kt * 16 + lr;                        // this lane's block key
+    const int c = 16 * kt + lr;                  // this lane's key
     const bool kvalid = kt < nkt && c < C && t0 + c >= 0;
     const int mult = kvalid ? sm.cnt[c] : 0;
-    const bool active = __builtin_amdgcn_ballot_w64(mult > 0) != 0;
-    // B operands: K_blk^T and V_blk^T, lane l feeding key l%16 with d slots 32*(l/16) + 8*j ..
+    // B operands K_blk^T and V_blk^T: lane l feeds key l%16 with d slots 32*(l/16) + 8*j ..
     bf16x8 kop[4], vop[4];
     {
       int64_t o = -1;
-      if (kvalid && mult > 0) o = row_offset<PAGED>(p.kv, s, g, t0 + c);
+      if (mult > 0) o = row_offset<PAGED>(p.kv, s, g, t0 + c);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         kop[j] = as_bf16x8(o >= 0 ? load16(p.kv.k + o + 32 * lg + 8 * j) : u32x4{0u, 0u, 0u, 0u});
         vop[j] = as_bf16x8(o >= 0 ? load16(p.kv.v + o + 32 * lg + 8 * j) : u32x4{0u, 0u, 0u, 0u});
       }
     }
+    const bool active = __builtin_amdgcn_ballot_w64(mult > 0) != 0;
     f32x4 dk[8], dv[8];
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) dk[dt] = dv[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    __syncthreads();                             // the previous pass's ring reads are done
+    for (int t = 0; t < kKRing - 1; ++t) issue(t);
     for (int rt = 0; rt < nrt; ++rt) {
-      __syncthreads();   // the previous row tile's reads are done
-      // stage Q and dO of rows 32*rt .. +31 (row-major, padded) with lse and D
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int ci = tid + kKThreads * u;
-        const int r = ci >> 4, cc = ci & 15;
-        const int n = 32 * rt + r;
-        const bool valid = n < p.R;
-        const int j = valid ? n / p.G : 0, h = g * p.G + (valid ? n % p.G : 0);
-        const int64_t orow = ((int64_t)s * C + j) * p.Hq + h;
-        const int64_t off = orow * kD + 8 * cc;
-        const u32x4 qv = valid ? load16(p.q + off) : u32x4{0u, 0u, 0u, 0u};
-        const u32x4 dv4 = valid ? load16(doutb + off) : u32x4{0u, 0u, 0u, 0u};
-        const f32x4 o0 = valid ? *reinterpret_cast<const f32x4*>(outb + off) : f32x4{0.f, 0.f, 0.f, 0.f};
-        const f32x4 o1 = valid ? *reinterpret_cast<const f32x4*>(outb + off + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
-        *reinterpret_cast<u32x4*>(sm.q + r * kPitch + 16 * cc) = qv;
-        *reinterpret_cast<u32x4*>(sm.dout + r * kPitch + 16 * cc) = dv4;
-        float dsum = 0.f;
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          dsum += bf16_lo(dv4[e]) * o0[2 * e] + bf16_hi(dv4[e]) * o0[2 * e + 1];
-          dsum += bf16_lo(dv4[e + 2]) * o1[2 * e] + bf16_hi(dv4[e + 2]) * o1[2 * e + 1];
+      // this wave's loads of tile rt are older than the kKRing-2 tiles issued after it
+      asm volatile("s_waitcnt vmcnt(9)\n\ts_barrier" ::: "memory");
+      static_assert(9 * (kKRing - 2) == 9, "wait count follows the ring depth");
+      issue(rt + kKRing - 1);
+      const uint32_t slot = ring_lds + (uint32_t)(rt % kKRing) * kKTileBytes;
+      const uint32_t src = slot + 16 * lane;
+      if (active) {
+        u32x4 qa[8], da[8];
+        read8(qa, src);
+        read8(da, src + 16 * 1024);
+        // (lse2, D) of rows 16*sub + 4*lg + i: 32 contiguous bytes per sub
+        f32x4 st[2][2];
+        {
+          const uint32_t a = slot + kKLoads * 1024 + 32 * lg;
+          asm volatile(
+              "ds_read_b128 %0, %4\n"
+              "ds_read_b128 %1, %4 offset:16\n"
+              "ds_read_b128 %2, %4 offset:128\n"
+              "ds_read_b128 %3, %4 offset:144\n"
+              "s_waitcnt lgkmcnt(0)"
+              : "=&v"(st[0][0]), "=&v"(st[0][1]), "=&v"(st[1][0]), "=&v"(st[1][1])
+              : "v"(a));
         }
-        dsum = sum16(dsum);
-        if (cc == 0) {
-          sm.D[r] = dsum;
-          const float l2 = valid ? lseb[orow] * kLog2e : INFINITY;
-          sm.lse2[r] = l2 == -INFINITY ? INFINITY : l2;
+        float l2[2][4], dd[2][4];
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            l2[sub][i] = st[sub][i >> 1][2 * (i & 1)];
+            dd[sub][i] = st[sub][i >> 1][2 * (i & 1) + 1];
+          }
+        // S [row][key] = Q . K_blk^T and dP [row][key] = dO . V_blk^T: lane l holds rows
+        // 16*sub + 4*lg + i of key l%16
+        f32x4 sp[2], dp[2];
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub) {
+          f32x4 x = {0.f, 0.f, 0.f, 0.f}, y = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(qa[4 * sub + j]), kop[j], x, 0, 0, 0);
+            y = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(da[4 * sub + j]), vop[j], y, 0, 0, 0);
+          }
+          sp[sub] = x;
+          dp[sub] = y;
         }
-      }
-      __syncthreads();
-      if (!active) continue;
-
-      // S and dP with rows on the M side: lane l holds rows 16*sub + 4*(l/16) + i of key l%16
-      f32x4 sp[2], dp[2];
+        u32x4 pw, dsw, pwl, dswl;
 #pragma unroll
-      for (int sub = 0; sub < 2; ++sub) {
-        f32x4 a = {0.f, 0.f, 0.f, 0.f}, b = {0.f, 0.f, 0.f, 0.f};
+        for (int i2 = 0; i2 < 4; ++i2) {
+          float pv[2], dsv[2];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t off = (16 * sub + lr) * kPitch + 64 * lg + 16 * j;
-          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(lds_read16(sm.q, off)), kop[j], a, 0, 0, 0);
-          b = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(lds_read16(sm.dout, off)), vop[j], b, 0, 0, 0);
+          for (int e2 = 0; e2 < 2; ++e2) {
+            const int slot = 2 * i2 + e2;                     // k-slot: row 16*(slot/4) + 4*lg + slot%4
+            const int sub = slot >> 2, i = slot & 3;
+            const int n = 32 * rt + 16 * sub + 4 * lg + i;
+            const bool vis = mult > 0 && n < p.R && c <= div_small(n, p.G, p.inv_G);
+            const float pr = vis ? __builtin_amdgcn_exp2f(fmaf(sp[sub][i], p.scale_log2, -l2[sub][i])) : 0.f;
+            pv[e2] = pr;
+            dsv[e2] = vis ? pr * (dp[sub][i] - dd[sub][i]) : 0.f;   // padding rows hold no stats
+          }
+          pw[i2] = pack_bf16x2(pv[0], pv[1]);
+          dsw[i2] = pack_bf16x2(dsv[0], dsv[1]);
+          pwl[i2] = pack_bf16x2(pv[0] - bf16_lo(pw[i2]), pv[1] - bf16_hi(pw[i2]));
+          dswl[i2] = pack_bf16x2(dsv[0] - bf16_lo(dsw[i2]), dsv[1] - bf16_hi(dsw[i2]));
         }
-        sp[sub] = a;
-        dp[sub] = b;
-      }
-      u32x4 pw, dsw, pwl, dswl;
+        // transposed operands: register 4*h + i holds row 16*h + 4*lg + i, 16 bytes at d = 8*lr
+        read8(qa, src + 8 * 1024);
+        read8(da, src + 24 * 1024);
 #pragma unroll
-      for (int i2 = 0; i2 < 4; ++i2) {
-        float pv[2], dsv[2];
-#pragma unroll
-        for (int e2 = 0; e2 < 2; ++e2) {
-          const int slot = 2 * i2 + e2;                       // k-slot: row 16*(slot/4) + 4*lg + slot%4
-          const int sub = slot >> 2, i = slot & 3;
-          const int r = 16 * sub + 4 * lg + i;
-          const int n = 32 * rt + r;
-          const bool vis = mult > 0 && n < p.R && c <= n / p.G;
-          const float pr = vis ? __builtin_amdgcn_exp2f(fmaf(sp[sub][i], p.scale_log2, -sm.lse2[r])) : 0.f;
-          pv[e2] = pr;
-          dsv[e2] = pr * (dp[sub][i] - sm.D[r]);
+        for (int dt = 0; dt < 8; ++dt) {
+          const bf16x8 a_do = vt_operand(da, dt), a_q = vt_operand(qa, dt);
+          dv[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_do, as_bf16x8(pw), dv[dt], 0, 0, 0);
+          dv[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_do, as_bf16x8(pwl), dv[dt], 0, 0, 0);
+          dk[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_q, as_bf16x8(dsw), dk[dt], 0, 0, 0);
+          dk[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_q, as_bf16x8(dswl), dk[dt], 0, 0, 0);
         }
-        pw[i2] = pack_bf16x2(pv[0], pv[1]);
-        dsw[i2] = pack_bf16x2(dsv[0], dsv[1]);
-        pwl[i2] = pack_bf16x2(pv[0] - bf16_lo(pw[i2]), pv[1] - bf16_hi(pw[i2]));
-        dswl[i2] = pack_bf16x2(dsv[0] - bf16_lo(dsw[i2]), dsv[1] - bf16_hi(dsw[i2]));
-      }
-      // transposed operands: rows 16*h + 4*lg + i (register 4*h + i), 16 bytes at d = 8*lr
-      u32x4 qt[8], dot[8];
-#pragma unroll
-      for (int x = 0; x < 8; ++x) {
-        const uint32_t off = (16 * (x >> 2) + 4 * lg + (x & 3)) * kPitch + 16 * lr;
-        qt[x] = lds_read16(sm.q, off);
-        dot[x] = lds_read16(sm.dout, off);
-      }
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        const bf16x8 a_do = vt_operand(dot, dt), a_q = vt_operand(qt, dt);
-        dv[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_do, as_bf16x8(pw), dv[dt], 0, 0, 0);
-        dv[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_do, as_bf16x8(pwl), dv[dt], 0, 0, 0);
-        dk[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_q, as_bf16x8(dsw), dk[dt], 0, 0, 0);
-        dk[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_q, as_bf16x8(dswl), dk[dt], 0, 0, 0);
       }
     }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the ring is reused
 
-    // block key c: register i of d-tile dt holds d = 32*lg + 8*i + dt; a key listed m times counts m times
+    // key c: register i of d-tile dt holds d = 32*lg + 8*i + dt; a key listed m times counts m times
     if (kt < nkt && c < C) {
       const float mk = (float)mult * (direct ? p.scale : 1.f), mv = (float)mult;
-      float* kr = out_k + (int64_t)c * out_stride + out_head + 32 * lg;
-      float* vr = out_v + (int64_t)c * out_stride + out_head + 32 * lg;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const f32x4 k0 = f32x4{dk[0][i], dk[1][i], dk[2][i], dk[3][i]} * mk;
@@ -619,12 +656,15 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
         const f32x4 v0 = f32x4{dv[0][i], dv[1][i], dv[2][i], dv[3][i]} * mv;
         const f32x4 v1 = f32x4{dv[4][i], dv[5][i], dv[6][i], dv[7][i]} * mv;
         if (direct) {
-          *reinterpret_cast<f32x4*>(kr + 8 * i) = k0;
-          *reinterpret_cast<f32x4*>(kr + 8 * i + 4) = k1;
-          *reinterpret_cast<f32x4*>(vr + 8 * i) = v0;
-          *reinterpret_cast<f32x4*>(vr + 8 * i + 4) = v1;
+          float* kr = p.dk + (((int64_t)s * C + c) * p.Hkv + g) * kD + 32 * lg + 8 * i;
+          float* vr = p.dv + (((int64_t)s * C + c) * p.Hkv + g) * kD + 32 * lg + 8 * i;
+          *reinterpret_cast<f32x4*>(kr) = k0;
+          *reinterpret_cast<f32x4*>(kr + 4) = k1;
+          *reinterpret_cast<f32x4*>(vr) = v0;
+          *reinterpret_cast<f32x4*>(vr + 4) = v1;
         } else {
-          const uint32_t ok = (uint32_t)((c * kD + 32 * lg + 8 * i) * 4), ov = ok + (uint32_t)(C * kD * 4);
+          const uint32_t ok = (uint32_t)((((int64_t)br * C + c) * 2 * kD + 32 * lg + 8 * i) * 4);
+          const uint32_t ov = ok + (uint32_t)(kD * 4);
           store16_coherent(rrec, ok, k0);
           store16_coherent(rrec, ok + 16, k1);
           store16_coherent(rrec, ov, v0);
@@ -643,62 +683,74 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
   __syncthreads();
   if (!sm.last) return;
   if (tid == 0) reset_counter(ctr);
-  const float* recs = p.part_kv + (int64_t)pair * p.nbr * C * 2 * kD;
-  const __amdgpu_buffer_rsrc_t rr = make_rsrc(recs, (uint32_t)((int64_t)p.nbr * C * 2 * kD * 4));
-  const int chunks = C * 2 * kD / 4;                 // float4s of one branch record
-  for (int q = tid; q < chunks; q += kKThreads) {
-    f32x4 sum = {0.f, 0.f, 0.f, 0.f};
-    for (int b = 0; b < p.nbr; ++b) sum += load16_coherent(rr, (uint32_t)(((int64_t)b * chunks + q) * 16));
-    const int fl = 4 * q;                            // float index within [dk | dv] of one branch
-    const bool isv = fl >= C * kD;
-    const int rem = isv ? fl - C * kD : fl;
-    const int cc = rem / kD, d = rem % kD;
-    float* dst = (isv ? p.dv : p.dk) + (((int64_t)s * C + cc) * p.Hkv + g) * kD + d;
-    *reinterpret_cast<f32x4*>(dst) = isv ? sum : sum * p.scale;
+  // Device-scope loads travel past the XCD's L2, so a round of them costs about a microsecond:
+  // each round issues 4 chunks of up to 8 branches (32 loads) before summing any.
+  const int chunks = C * 2 * kD / 4;             // float4s of one branch record: [C][dK | dV][128]
+  constexpr int kBr = 8;
+  for (int q0 = 0; q0 < chunks; q0 += 4 * kKThreads) {
+    f32x4 sum[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) sum[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int b0 = 0; b0 < p.nbr; b0 += kBr) {
+      f32x4 x[kBr][4];
+#pragma unroll
+      for (int bb = 0; bb < kBr; ++bb)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int q = q0 + tid + u * kKThreads;
+          x[bb][u] = q < chunks && b0 + bb < p.nbr
+                         ? load16_coherent(rrec, (uint32_t)(((int64_t)(b0 + bb) * chunks + q) * 16))
+                         : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+      for (int bb = 0; bb < kBr; ++bb)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) sum[u] += x[bb][u];   // branch order (absent branches add 0)
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int q = q0 + tid + u * kKThreads;
+      if (q >= chunks) continue;
+      const int fl = 4 * q;
+      const int cc = fl / (2 * kD), rem = fl % (2 * kD);
+      const bool isv = rem >= kD;
+      const int d = isv ? rem - kD : rem;
+      float* dst = (isv ? p.dv : p.dk) + (((int64_t)s * C + cc) * p.Hkv + g) * kD + d;
+      *reinterpret_cast<f32x4*>(dst) = isv ? sum[u] : sum[u] * p.scale;
+    }
   }
 }
 
 }  // namespace
 
 AttnBwdPlan plan_attn_bwd(int S, int Hkv, int Hq, int C, int num_views, int ld_idx, int max_L, bool with_full,
-                          bool paged, bool with_dkv) {
+                          bool with_dkv) {
   AttnBwdPlan pl{};
   const int G = Hq / Hkv;
   pl.R = C * G;
   pl.n_rb = (pl.R + 31) / 32;
   pl.n_rg = (pl.n_rb + kQWaves - 1) / kQWaves;
   pl.units = S * Hkv * pl.n_rg;
-  const int64_t units_g = (int64_t)num_views * pl.units, units_f = with_full ? pl.units : 0;
-  auto round_up = [](int64_t x, int64_t m) { return (x + m - 1) / m * m; };
-  const int64_t work = units_g * ld_idx + units_f * max_L;
-  const int64_t g_all = round_up(ld_idx > 0 ? ld_idx : 1, kTile), f_all = round_up(max_L > 0 ? max_L : 1, kTile);
-  // keys per split: from work / kTargetBlocks up, the smallest multiple of the tile that keeps the
-  // launch to one workgroup per CU; view splits and paged full splits are bound by the slot table
-  int64_t kps = round_up((work + kTargetBlocks - 1) / kTargetBlocks, kTile);
-  if (kps < kTile) kps = kTile;
-  int64_t kg, kf, blocks;
-  for (;;) {
-    kg = kps < g_all ? kps : g_all;
-    if (kg > kMaxSplitKeys) kg = kMaxSplitKeys;
-    kf = kps < f_all ? kps : f_all;
-    if (paged && kf > kMaxSplitKeys) kf = kMaxSplitKeys;
-    blocks = units_g * ((g_all + kg - 1) / kg) + units_f * ((f_all + kf - 1) / kf);
-    if (blocks <= kTargetBlocks || (kps >= g_all && kps >= f_all)) break;
-    kps += kTile;
-  }
-  pl.kps_g = (int)kg;
-  pl.kps_f = (int)kf;
-  pl.nsplit_g = ld_idx > 0 ? (int)((ld_idx + kg - 1) / kg) : 1;
-  pl.nsplit_f = max_L > 0 ? (int)((max_L + kf - 1) / kf) : 1;
-  pl.nb = num_views * pl.nsplit_g + (with_full ? pl.nsplit_f : 0);
-  pl.nblk_g = (int)(units_g * pl.nsplit_g);
-  pl.nblk_q = (int)(units_g * pl.nsplit_g + units_f * pl.nsplit_f);
   pl.nbr = num_views + (with_full ? 1 : 0);
+  pl.nkt = (C + 15) / 16;
+  // workgroups per unit: enough to fill the CUs once, and enough that no range overflows the slot
+  // table (a range is a share ceil(total / nW) <= kMaxSplitKeys rounded up to whole tiles, which
+  // stays <= kMaxSplitKeys as that is a multiple of the tile)
+  static_assert(kMaxSplitKeys % kTile == 0, "ranges round up to whole tiles");
+  const int64_t stream_max = (int64_t)num_views * ld_idx + (with_full ? max_L : 0);
+  int64_t nw = (kTargetBlocks + pl.units - 1) / pl.units;
+  const int64_t nw_table = (stream_max + kMaxSplitKeys - 1) / kMaxSplitKeys;
+  if (nw < nw_table) nw = nw_table;
+  if (nw < 1) nw = 1;
+  pl.nW = (int)nw;
+  pl.nblk_q = (int)((int64_t)pl.units * nw);
+  pl.nblk_kv = with_dkv ? S * Hkv * pl.nbr : 0;
   pl.counter_bytes = BD_WS_COUNTER_BYTES;
-  pl.q_record_bytes = pl.nb > 1 ? align256(sizeof(float) * kRecFloats * (size_t)pl.units * kQWaves * pl.nb) : 0;
-  pl.kv_record_bytes =
-      with_dkv && pl.nbr > 1 ? align256(sizeof(float) * (size_t)S * Hkv * pl.nbr * C * 2 * kD) : 0;
-  pl.ws_bytes = pl.counter_bytes + pl.q_record_bytes + pl.kv_record_bytes;
+  pl.q_record_bytes = nw > 1 ? align256(sizeof(float) * kRecFloats * (size_t)pl.units * kQWaves * nw) : 0;
+  pl.kv_record_bytes = with_dkv && pl.nbr > 1 ? align256(sizeof(float) * (size_t)pl.nblk_kv * C * 2 * kD) : 0;
+  pl.R_pad = pl.n_rb * 32;
+  pl.d_bytes = with_dkv ? align256(sizeof(float) * 2 * (size_t)pl.nbr * S * Hkv * pl.R_pad) : 0;
+  pl.ws_bytes = pl.counter_bytes + pl.q_record_bytes + pl.kv_record_bytes + pl.d_bytes;
   return pl;
 }
 
@@ -709,10 +761,9 @@ hipError_t launch_attn_bwd(const AttnBwdParams& p, const AttnBwdPlan& pl, bool p
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  if (p.dk) {
-    const int nblk = p.S * p.Hkv * p.nbr;
-    if (paged) hipLaunchKernelGGL(dkv_kernel<true>, dim3(nblk), dim3(kKThreads), 0, stream, p);
-    else hipLaunchKernelGGL(dkv_kernel<false>, dim3(nblk), dim3(kKThreads), 0, stream, p);
+  if (pl.nblk_kv > 0) {
+    if (paged) hipLaunchKernelGGL(dkv_kernel<true>, dim3(pl.nblk_kv), dim3(kKThreads), 0, stream, p);
+    else hipLaunchKernelGGL(dkv_kernel<false>, dim3(pl.nblk_kv), dim3(kKThreads), 0, stream, p);
     return hipGetLastError();
   }
   return hipSuccess;

@@ -288,11 +288,8 @@ size_t bd_multiview_attn_bwd_workspace_bytes(int32_t num_seqs, int32_t num_kv_he
       max_seq_len < 0)
     return 0;
   const int32_t ld = num_views > 0 ? ld_idx : 0;
-  const size_t a = bd::plan_attn_bwd(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld, max_seq_len,
-                                     with_full != 0, true, true).ws_bytes;
-  const size_t b = bd::plan_attn_bwd(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld, max_seq_len,
-                                     with_full != 0, false, true).ws_bytes;
-  return a > b ? a : b;
+  return bd::plan_attn_bwd(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld, max_seq_len,
+                           with_full != 0, true).ws_bytes;
 }
 
 bd_status bd_multiview_attn_bwd(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t num_q_heads, int32_t block_len,
@@ -327,11 +324,12 @@ bd_status bd_multiview_attn_bwd(const bd_kv_desc* kv, const uint16_t* q_blk, int
   const int32_t ld = num_views > 0 ? ld_idx : 0;
   const bool paged = kv->page_table != nullptr;
   const bd::AttnBwdPlan pl = bd::plan_attn_bwd(kv->num_seqs, kv->num_kv_heads, num_q_heads, block_len, num_views, ld,
-                                               kv->max_seq_len, full, paged, dk_blk != nullptr);
+                                               kv->max_seq_len, full, dk_blk != nullptr);
   if ((int64_t)pl.units + (int64_t)kv->num_seqs * kv->num_kv_heads > BD_WS_COUNTER_LINES)
     return fail(BD_ERR_UNSUPPORTED, "more than %d work units", BD_WS_COUNTER_LINES);
-  if ((int64_t)pl.nblk_q > INT32_MAX / 2 || (int64_t)pl.nb * 2 * 16 * BD_HEAD_DIM * 4 > INT32_MAX ||
-      (int64_t)pl.nbr * block_len * 2 * BD_HEAD_DIM * 4 > INT32_MAX)
+  if ((int64_t)pl.units * pl.nW > INT32_MAX / 2 || (int64_t)pl.nW * 2 * 16 * BD_HEAD_DIM * 4 > INT32_MAX ||
+      (int64_t)pl.nbr * block_len * 2 * BD_HEAD_DIM * 4 > INT32_MAX ||
+      (int64_t)kv->num_seqs * kv->num_kv_heads * pl.nbr > INT32_MAX / 2)
     return fail(BD_ERR_UNSUPPORTED, "problem too large for one launch");
   st = check_ws(ws, ws_bytes, pl.ws_bytes);
   if (st != BD_OK) return st;
@@ -353,17 +351,14 @@ bd_status bd_multiview_attn_bwd(const bd_kv_desc* kv, const uint16_t* q_blk, int
   p.G = num_q_heads / kv->num_kv_heads;
   p.C = block_len;
   p.V = num_views;
+  p.inv_G = 1.f / (float)p.G;
   p.R = pl.R;
   p.n_rb = pl.n_rb;
   p.n_rg = pl.n_rg;
-  p.nsplit_g = pl.nsplit_g;
-  p.kps_g = pl.kps_g;
-  p.nsplit_f = pl.nsplit_f;
-  p.kps_f = pl.kps_f;
-  p.nb = pl.nb;
+  p.nW = pl.nW;
   p.units = pl.units;
-  p.nblk_g = pl.nblk_g;
   p.nbr = pl.nbr;
+  p.nkt = pl.nkt;
   p.scale = scale;
   p.scale_log2 = scale * 1.4426950408889634f;
   p.max_roff = (uint32_t)((kv_extent(kv) - BD_HEAD_DIM) >> 3);
@@ -374,6 +369,9 @@ bd_status bd_multiview_attn_bwd(const bd_kv_desc* kv, const uint16_t* q_blk, int
   p.counters = reinterpret_cast<uint32_t*>(w);
   p.part_q = pl.q_record_bytes ? reinterpret_cast<float*>(w + pl.counter_bytes) : nullptr;
   p.part_kv = pl.kv_record_bytes ? reinterpret_cast<float*>(w + pl.counter_bytes + pl.q_record_bytes) : nullptr;
+  p.rstats = pl.d_bytes ? reinterpret_cast<float*>(w + pl.counter_bytes + pl.q_record_bytes + pl.kv_record_bytes)
+                        : nullptr;
+  p.R_pad = pl.R_pad;
   return launched(bd::launch_attn_bwd(p, pl, paged, stream));
 }
 

@@ -64,7 +64,7 @@ size_t attn_ws_bytes(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, 
 
 // ---- multiview attention backward -------------------------------------------
 // Branch b of a (sequence, KV head) pair is view b (b < V) or the full cache (b == V).
-constexpr int kMaxBwdBlock = 1024;   // block rows C the dK/dV kernel keeps key counts for
+constexpr int kMaxBwdBlock = 1024;   // largest block C the backward accepts (key counts live in LDS)
 
 struct AttnBwdParams {
   KvView kv;
@@ -81,30 +81,31 @@ struct AttnBwdParams {
   int32_t S, Hkv, Hq, G, C, V;
   int32_t R;                 // rows per (s, g): C * G
   int32_t n_rb, n_rg;        // 32-row blocks, groups of 8 of them
-  int32_t nsplit_g, kps_g;   // view splits and entries per split
-  int32_t nsplit_f, kps_f;   // full-branch splits and keys per split
-  int32_t nb;                // dQ partials per unit: V * nsplit_g + (full ? nsplit_f : 0)
+  int32_t nW;                // dQ workgroups per unit, each a share of the unit's key stream
   int32_t units;             // S * Hkv * n_rg (dQ units; their counters come first)
-  int32_t nblk_g;            // dQ workgroups of the views (they come first)
   int32_t nbr;               // branches: V + (full ? 1 : 0)
+  int32_t nkt;               // 16-key tiles of the block
   float scale, scale_log2;
+  float inv_G;               // 1 / G
   uint32_t max_roff;         // largest valid row offset of the K/V layout, 16-byte units
   float* dq;                 // [S][C][Hq][D]
   float* dk;                 // nullable [S][C][Hkv][D] (with dv)
   float* dv;
-  float* part_q;             // dQ partial records
-  float* part_kv;            // dK/dV partial records, one per (s, g, branch)
+  float* part_q;             // dQ partial records: [unit][wave][nW] of 32 x 128
+  float* part_kv;            // dK/dV partial records: [(s, g)][branch] of C x (dK | dV) x 128
+  float* rstats;             // with dK/dV: per branch row (lse in log2 units, D = <dO, O>),
+                             // [nbr][S * Hkv][R_pad][2], published by the dQ kernel
+  int32_t R_pad;             // rows rounded up to 32
   uint32_t* counters;
 };
 
 struct AttnBwdPlan {
-  int n_rb, n_rg, R;
-  int nsplit_g, kps_g, nsplit_f, kps_f, nb, units, nblk_q, nblk_g, nbr;
-  size_t counter_bytes, q_record_bytes, kv_record_bytes, ws_bytes;
+  int n_rb, n_rg, R, R_pad, units, nbr, nkt, nW, nblk_q, nblk_kv;
+  size_t counter_bytes, q_record_bytes, kv_record_bytes, d_bytes, ws_bytes;
 };
 
 AttnBwdPlan plan_attn_bwd(int S, int Hkv, int Hq, int C, int num_views, int ld_idx, int max_L, bool with_full,
-                          bool paged, bool with_dkv);
+                          bool with_dkv);
 hipError_t launch_attn_bwd(const AttnBwdParams& p, const AttnBwdPlan& pl, bool paged, hipStream_t stream);
 
 // ---- greedy acceptance -----------------------------------------------------
