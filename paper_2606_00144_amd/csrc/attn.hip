@@ -208,6 +208,15 @@ __device__ inline void dma_tile(const KvView& kv, const TileRows& A, uint32_t ma
     }
 }
 
+// V rows already in the tile registers.
+template <int NT, bool PAGED>
+__device__ inline auto pass_v(const TileRegs<NT, PAGED>& T) {
+  return [&T](u32x4 (&v)[8]) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = T.v[i];
+  };
+}
+
 template <int NT>
 struct RowState {
   f32x4 o[NT][8];     // O^T[d-tile][row tile]
@@ -223,10 +232,12 @@ struct RowState {
 // TRAIN: each weight enters the PV product and the normaliser as a bf16 pair hi + lo (lo the rounded
 // remainder), so the output carries the weights to about 2^-17 instead of 2^-9: the fp32 output then
 // serves the backward's <dO, O> (which cancels against <dO, v_t>) without amplifying rounding.
-template <int NT, bool PAGED, bool TRAIN = false, class PosFn>
+// `get_v` delivers the tile's V rows (8 x 16 bytes per lane) just before the PV product, so a caller
+// may read them from LDS only then.
+template <int NT, bool PAGED, bool TRAIN = false, class PosFn, class VFn>
 __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T, const bf16x8 (&qop)[NT][4],
                                  const int (&rowpos)[NT], float scale_log2, bool dirty, bool want_lx,
-                                 PosFn pos_of) {
+                                 PosFn pos_of, VFn get_v) {
   // scores S^T for 32 keys x 16*NT rows (unscaled)
   f32x4 sacc[2][NT];
 #pragma unroll
@@ -307,9 +318,11 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
     st.l[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pop[nt], st.l[nt], 0, 0, 0);
   }
 
+  u32x4 vrows[8];
+  get_v(vrows);
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) {
-    const bf16x8 vt = vt_operand(T.v, dt);
+    const bf16x8 vt = vt_operand(vrows, dt);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       st.o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, pop[nt], st.o[nt][dt], 0, 0, 0);
@@ -498,14 +511,14 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
         read_tile<NT, PAGED>(T, slot_a_lds, lane);
         rows_at(kTile * (it + 2 * kWaves));
         dma_tile(p.kv, A, p.max_roff, slot_a, lane);
-        tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it >= first_dirty, want_lx, pos_at(kTile * it));
+        tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it >= first_dirty, want_lx, pos_at(kTile * it), pass_v(T));
         if (it + kWaves >= ntiles) break;
         asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
         read_tile<NT, PAGED>(T, slot_b_lds, lane);
         rows_at(kTile * (it + 3 * kWaves));
         dma_tile(p.kv, A, p.max_roff, slot_b, lane);
         tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it + kWaves >= first_dirty, want_lx,
-                             pos_at(kTile * (it + kWaves)));
+                             pos_at(kTile * (it + kWaves)), pass_v(T));
         if (it + 2 * kWaves >= ntiles) break;
       }
     } else {
@@ -521,13 +534,13 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
         read_tile_and_rows<NT, PAGED>(T, A, slot_a_lds, tpos_lds, kTile * it, roff_lds, kTile * (it + 2 * kWaves),
                                       lane);
         dma_tile(p.kv, A, p.max_roff, slot_a, lane);
-        tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it >= first_dirty, want_lx, pos_of);
+        tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it >= first_dirty, want_lx, pos_of, pass_v(T));
         if (it + kWaves >= ntiles) break;
         asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
         read_tile_and_rows<NT, PAGED>(T, A, slot_b_lds, tpos_lds, kTile * (it + kWaves), roff_lds,
                                       kTile * (it + 3 * kWaves), lane);
         dma_tile(p.kv, A, p.max_roff, slot_b, lane);
-        tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it + kWaves >= first_dirty, want_lx, pos_of);
+        tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it + kWaves >= first_dirty, want_lx, pos_of, pass_v(T));
         if (it + 2 * kWaves >= ntiles) break;
       }
     }
@@ -585,7 +598,6 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   const int64_t view_rows = (int64_t)p.S * p.nq * p.Hq;
   uint16_t* out = gather ? p.out_g + (int64_t)view * view_rows * kD : p.out_f;
   float* lse = gather ? (p.lse_g ? p.lse_g + (int64_t)view * view_rows : nullptr) : p.lse_f;
-  float* out32 = gather ? (p.o32_g ? p.o32_g + (int64_t)view * view_rows * kD : nullptr) : p.o32_f;
 
   auto write_final = [&](float Mf, float Lf, float Lxf, const float* a) {
     if (!row_valid) return;
@@ -677,11 +689,13 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
 // When a unit has more than one 32-row block (the multiview continuation block:
 // C x G rows), re-streaming K/V once per row block would multiply the traffic.
 // A block-mode workgroup has 8 waves, wave w owning row block 8*rg + w, and all
-// of them consume every 32-key tile of the split from a shared LDS ring: each
+// of them consume every 32-key tile of its range from a shared LDS ring: each
 // wave issues 2 of a tile's 16 direct-to-LDS loads, and one barrier per tile
 // both publishes the landed tile and frees the slot read in the step before.
-// A wave's online-softmax state is then complete for the split; splits merge
-// through per-row-block records in the last workgroup of the row group.
+// The ranges are equal shares of the (sequence, KV head, row group)'s whole key
+// stream, every view and the full branch in turn, cut at run time when the
+// views' lengths are known; pieces of a branch met by several workgroups merge
+// through per-row-block records in the last of them.
 
 constexpr int kBWaves = 8;
 constexpr int kBThreads = kBWaves * kWave;
@@ -695,42 +709,47 @@ struct BlockSmem {
   int32_t last;
 };
 
-// Tile data plus, from the slot table, the tile's positions and the two row offsets this wave loads
-// for the tile it issues next.
-__device__ inline void read_block_tile(TileRegs<2, true>& T, uint32_t (&r)[2], uint32_t src, uint32_t tpos_lds,
-                                       int slot0, uint32_t roff_lds, int next0, int rit0, int rit1, int lane) {
+// K pieces of the tile in slot `src`, its positions and the two row offsets this wave loads for the
+// tile it issues next (the V pieces are read later, just before the PV product).
+__device__ inline void read_block_tile_k(TileRegs<2, true>& T, uint32_t (&r)[2], uint32_t src, uint32_t tpos_lds,
+                                         int slot0, uint32_t roff_lds, int next0, int rit0, int rit1, int lane) {
   const int lg = lane >> 4;
   const uint32_t at = src + 16 * lane;
   const uint32_t ap = tpos_lds + 4 * (slot0 + 4 * lg);
   const uint32_t a0 = roff_lds + 4 * (next0 + rit0);
   const uint32_t a1 = roff_lds + 4 * (next0 + rit1);
   asm volatile(
-      "ds_read_b128 %0, %20\n"
-      "ds_read_b128 %1, %20 offset:1024\n"
-      "ds_read_b128 %2, %20 offset:2048\n"
-      "ds_read_b128 %3, %20 offset:3072\n"
-      "ds_read_b128 %4, %20 offset:4096\n"
-      "ds_read_b128 %5, %20 offset:5120\n"
-      "ds_read_b128 %6, %20 offset:6144\n"
-      "ds_read_b128 %7, %20 offset:7168\n"
-      "ds_read_b128 %8, %20 offset:8192\n"
-      "ds_read_b128 %9, %20 offset:9216\n"
-      "ds_read_b128 %10, %20 offset:10240\n"
-      "ds_read_b128 %11, %20 offset:11264\n"
-      "ds_read_b128 %12, %20 offset:12288\n"
-      "ds_read_b128 %13, %20 offset:13312\n"
-      "ds_read_b128 %14, %20 offset:14336\n"
-      "ds_read_b128 %15, %20 offset:15360\n"
-      "ds_read_b128 %16, %21\n"
-      "ds_read_b128 %17, %21 offset:64\n"
-      "ds_read_b32 %18, %22\n"
-      "ds_read_b32 %19, %23\n"
+      "ds_read_b128 %0, %12\n"
+      "ds_read_b128 %1, %12 offset:1024\n"
+      "ds_read_b128 %2, %12 offset:2048\n"
+      "ds_read_b128 %3, %12 offset:3072\n"
+      "ds_read_b128 %4, %12 offset:4096\n"
+      "ds_read_b128 %5, %12 offset:5120\n"
+      "ds_read_b128 %6, %12 offset:6144\n"
+      "ds_read_b128 %7, %12 offset:7168\n"
+      "ds_read_b128 %8, %13\n"
+      "ds_read_b128 %9, %13 offset:64\n"
+      "ds_read_b32 %10, %14\n"
+      "ds_read_b32 %11, %15\n"
       "s_waitcnt lgkmcnt(0)"
       : "=&v"(T.k[0][0]), "=&v"(T.k[0][1]), "=&v"(T.k[0][2]), "=&v"(T.k[0][3]), "=&v"(T.k[1][0]),
-        "=&v"(T.k[1][1]), "=&v"(T.k[1][2]), "=&v"(T.k[1][3]), "=&v"(T.v[0]), "=&v"(T.v[1]), "=&v"(T.v[2]),
-        "=&v"(T.v[3]), "=&v"(T.v[4]), "=&v"(T.v[5]), "=&v"(T.v[6]), "=&v"(T.v[7]), "=&v"(T.tp[0]), "=&v"(T.tp[1]),
-        "=&v"(r[0]), "=&v"(r[1])
+        "=&v"(T.k[1][1]), "=&v"(T.k[1][2]), "=&v"(T.k[1][3]), "=&v"(T.tp[0]), "=&v"(T.tp[1]), "=&v"(r[0]), "=&v"(r[1])
       : "v"(at), "v"(ap), "v"(a0), "v"(a1));
+}
+// Eight 1 KiB pieces (V rows of a tile) into registers, with their wait.
+__device__ inline void read_v8(u32x4 (&x)[8], uint32_t a) {
+  asm volatile(
+      "ds_read_b128 %0, %8\n"
+      "ds_read_b128 %1, %8 offset:1024\n"
+      "ds_read_b128 %2, %8 offset:2048\n"
+      "ds_read_b128 %3, %8 offset:3072\n"
+      "ds_read_b128 %4, %8 offset:4096\n"
+      "ds_read_b128 %5, %8 offset:5120\n"
+      "ds_read_b128 %6, %8 offset:6144\n"
+      "ds_read_b128 %7, %8 offset:7168\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3]), "=&v"(x[4]), "=&v"(x[5]), "=&v"(x[6]), "=&v"(x[7])
+      : "v"(a));
 }
 
 // Load q (0..15) of a tile for this lane: K load q < 8 (sub-tile q/4, k-step q%4), V load q >= 8
@@ -751,38 +770,35 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lg = lane >> 4, lr = lane & 15;
 
-  // ---- which (kind, row group, split) this workgroup owns
+  // ---- unit (sequence, KV head, row group) and this workgroup's share w of the unit's key stream
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const bool gather = bid < p.nblk_g;
-  const int local = gather ? bid : bid - p.nblk_g;
-  const int nsplit = gather ? p.nsplit_g : p.nsplit_f;
-  const int kps = gather ? p.kps_g : p.kps_f;
-  const int rg = local % p.n_rg;
-  const int rest = local / p.n_rg;
-  const int split = rest % nsplit;
-  const int pair = rest / nsplit;
-  const int g = pair % p.Hkv;
-  const int vs = pair / p.Hkv;
-  const int s = gather ? vs % p.S : vs;
-  const int view = gather ? vs / p.S : 0;
-  const int unit = gather ? pair * p.n_rg + rg : p.units_g + pair * p.n_rg + rg;
+  const int w = bid % p.nW;
+  const int unit = bid / p.nW;
+  const int rg = unit % p.n_rg;
+  const int pair = unit / p.n_rg;
+  const int g = pair % p.Hkv, s = pair / p.Hkv;
   const int rb = rg * kBWaves + wave;            // this wave's row block
   const bool has_rows = rb < p.n_rb;
-
   const int L = seq_len(p.kv, s);
-  int n_keys;
-  const int32_t* idx_row = nullptr;
-  if (gather) {
-    idx_row = p.idx + ((int64_t)vs * p.Hkv + g) * p.ld_idx;
-    int n = p.nsel[vs];
-    n_keys = n < 0 ? 0 : (n > p.ld_idx ? p.ld_idx : n);
-  } else {
-    n_keys = L;
-  }
-  const int e_begin = split * kps;
-  int e_end = e_begin + kps;
-  if (e_end > n_keys) e_end = n_keys;
-  const int ntiles = e_end > e_begin ? (e_end - e_begin + kTile - 1) / kTile : 0;
+
+  // The key stream of a unit is the views' entry lists followed by the full branch's cache rows;
+  // its length is known only here (nsel lives on the device), so the unit's nW workgroups cut it
+  // into equal ranges at run time.  A range runs one piece per branch it meets.  A branch met by
+  // one workgroup is finished there; otherwise each piece leaves a record and the last of the
+  // branch's workgroups merges them in stream order.
+  auto branch_len = [&](int b) -> int {
+    if (b < p.V) {
+      const int n = p.nsel[b * p.S + s];
+      return n < 0 ? 0 : (n > p.ld_idx ? p.ld_idx : n);
+    }
+    return L;
+  };
+  int total = 0;
+  for (int b = 0; b < p.nbr; ++b) total += branch_len(b);
+  int chunk = (total + p.nW - 1) / p.nW;
+  chunk = (chunk + kTile - 1) / kTile * kTile;
+  const int r0 = w * chunk;
+  const int r1 = r0 + chunk < total ? r0 + chunk : total;
 
   // ---- query rows of this wave's lanes: row n = rb*32 + 16*nt + lane%16
   bf16x8 qop[NT][4];
@@ -798,132 +814,28 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = as_bf16x8(valid ? load16(qrow + 8 * kk) : u32x4{0u, 0u, 0u, 0u});
   }
-
-  const bool arith = !PAGED && !gather;
-  if (!arith) {
-    const int nslots = (ntiles + kBRing) * kTile;     // <= kBSlotCap: padding tiles included
-    fill_slot_table<PAGED, kBThreads, kBSlotCap>(p.kv, s, g, L, gather ? idx_row : nullptr, e_begin, e_end, nslots,
-                                                 sm.roff, sm.tpos, tid);
-    __syncthreads();
-  }
   const int minpos = L - p.nq + (rb * RB::kRows) / p.G;   // earliest row position of this wave
-  const bool want_lx = (gather ? p.lse_g : p.lse_f) != nullptr;
-
-  RowState<NT> st;
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    st.m[nt] = -INFINITY;
-    st.l[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    st.lx[nt] = 0.f;
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
 
   // ---- the two loads of every tile that this wave issues, and the tile rows they read
   const int q0 = 2 * wave, q1 = 2 * wave + 1;
   auto row_in_tile = [&](int q) { return q < 8 ? 16 * (q >> 2) + lr : 16 * ((q - 8) >> 2) + 4 * lg + ((q - 8) & 3); };
   const int rit0 = row_in_tile(q0), rit1 = row_in_tile(q1);
-  const uint32_t base16 = arith ? (uint32_t)(((int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head) >> 3) : 0u;
-  const uint32_t tok16 = (uint32_t)(p.kv.stride_tok >> 3);
   const uint32_t roff_lds = lds_addr(sm.roff), tpos_lds = lds_addr(sm.tpos);
   const uint32_t ring_lds = lds_addr(sm.ring[0]);
-  auto arith_rows = [&](int tile, uint32_t (&r)[2]) {
-    if (tile >= ntiles) { r[0] = r[1] = 0u; return; }   // padding: row 0, a cache-resident address
-    const uint32_t r0 = base16 + (uint32_t)(e_begin + kTile * tile) * tok16;
-    r[0] = r0 + (uint32_t)rit0 * tok16;
-    r[1] = r0 + (uint32_t)rit1 * tok16;
-  };
   auto issue = [&](int tile, const uint32_t (&r)[2]) {
     uint8_t* dst = sm.ring[tile % kBRing];
     dma_load(p.kv, r[0], p.max_roff, q0, dst, lane);
     dma_load(p.kv, r[1], p.max_roff, q1, dst, lane);
   };
 
-  // the two streaming variants are separate loops, so neither carries the other's registers
-  auto stream = [&](auto arith_tag) {
-    constexpr bool ARITH = decltype(arith_tag)::value;
-    // prologue: tiles 0 .. kBRing-2
-    for (int t = 0; t < kBRing - 1; ++t) {
-      uint32_t r[2];
-      if constexpr (ARITH) {
-        arith_rows(t, r);
-      } else {
-        asm volatile(
-            "ds_read_b32 %0, %2\n"
-            "ds_read_b32 %1, %3\n"
-            "s_waitcnt lgkmcnt(0)"
-            : "=&v"(r[0]), "=&v"(r[1])
-            : "v"(roff_lds + 4 * (kTile * t + rit0)), "v"(roff_lds + 4 * (kTile * t + rit1)));
-      }
-      issue(t, r);
-    }
-    int fd_arith = 0;
-    if constexpr (ARITH) {
-      const int c1 = minpos - e_begin - (kTile - 1);
-      const int fd1 = c1 < 0 ? 0 : c1 / kTile + 1;
-      const int fd2 = (e_end - e_begin) / kTile;
-      fd_arith = fd1 < fd2 ? fd1 : fd2;
-    }
-    TileRegs<NT, true> T;
-    // tile t+kBRing-1 is issued in step t, after the barrier that frees its slot (read in step t-1)
-    for (int t = 0; t < ntiles; ++t) {
-      // this wave's loads of tile t are older than the kBRing-2 tiles issued after it
-      asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
-      static_assert(2 * (kBRing - 2) == 8, "wait count follows the ring depth");
-      const int nxt = t + kBRing - 1;
-      const uint32_t src = ring_lds + (uint32_t)(t % kBRing) * kTileBytes;
-      uint32_t r[2];
-      bool dirty;
-      if constexpr (ARITH) {
-        read_tile<NT, true>(T, src, lane);
-        arith_rows(nxt, r);
-        dirty = t >= fd_arith;
-      } else {
-        read_block_tile(T, r, src, tpos_lds, kTile * t, roff_lds, kTile * nxt, rit0, rit1, lane);
-        bool bad = false;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int tp = (int)T.tp[i >> 2][i & 3];
-          bad |= tp < 0 || tp > minpos;
-        }
-        dirty = __builtin_amdgcn_ballot_w64(bad) != 0;
-      }
-      issue(nxt, r);
-      if (has_rows) {
-        if constexpr (ARITH) {
-          const int slot0 = kTile * t;
-          tile_step<NT, true, TRAIN>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx, [&](int i) {
-            const int e = e_begin + slot0 + 16 * (i >> 2) + 4 * lg + (i & 3);
-            return e < e_end ? e : -1;
-          });
-        } else {
-          tile_step<NT, true, TRAIN>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx,
-                              [&](int i) { return (int)T.tp[i >> 2][i & 3]; });
-        }
-      }
-    }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the block ends
-  };
-  if (ntiles > 0) {
-    if (arith) stream(BoolTag<true>{});
-    else stream(BoolTag<false>{});
-  }
-
-  // ---- per-row results of this wave: (m, l, lx) of rows 16*nt + lane%16
-  float lxw[NT];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    float lx = st.lx[nt];
-    lx += shfl_xor_f(lx, 16);
-    lx += shfl_xor_f(lx, 32);
-    lxw[nt] = lx;
-  }
+  // ---- branch b's outputs of rows 16*nt + lane%16; register i of d-tile dt holds d = 32*(lane/16) + 8*i + dt
   const int64_t view_rows = (int64_t)p.S * p.nq * p.Hq;
-  uint16_t* out = gather ? p.out_g + (int64_t)view * view_rows * kD : p.out_f;
-  float* lse = gather ? (p.lse_g ? p.lse_g + (int64_t)view * view_rows : nullptr) : p.lse_f;
-  float* out32 = gather ? (p.o32_g ? p.o32_g + (int64_t)view * view_rows * kD : nullptr) : p.o32_f;
-  // normalise and write rows 16*nt + lane%16; register i of d-tile dt holds d = 32*(lane/16) + 8*i + dt
-  auto write_rows = [&](const float (&M)[NT], const float (&Lw)[NT], const float (&Lx)[NT], const f32x4 (&o)[NT][8]) {
+  auto write_rows = [&](int b, const float (&M)[NT], const float (&Lw)[NT], const float (&Lx)[NT],
+                        const f32x4 (&o)[NT][8]) {
+    const bool gb = b < p.V;
+    uint16_t* out = gb ? p.out_g + (int64_t)b * view_rows * kD : p.out_f;
+    float* lse = gb ? (p.lse_g ? p.lse_g + (int64_t)b * view_rows : nullptr) : p.lse_f;
+    float* out32 = gb ? (p.o32_g ? p.o32_g + (int64_t)b * view_rows * kD : nullptr) : p.o32_f;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int n = rb * RB::kRows + 16 * nt + lr;
@@ -933,10 +845,10 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
       const float inv = Lw[nt] > 0.f ? 1.f / Lw[nt] : 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        u32x4 w;
+        u32x4 wv;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(o[nt][2 * e][i] * inv, o[nt][2 * e + 1][i] * inv);
-        *reinterpret_cast<u32x4*>(out + orow * kD + 32 * lg + 8 * i) = w;
+        for (int e = 0; e < 4; ++e) wv[e] = pack_bf16x2(o[nt][2 * e][i] * inv, o[nt][2 * e + 1][i] * inv);
+        *reinterpret_cast<u32x4*>(out + orow * kD + 32 * lg + 8 * i) = wv;
         if (TRAIN && out32) {
           float* o32 = out32 + orow * kD + 32 * lg + 8 * i;
           *reinterpret_cast<f32x4*>(o32) = f32x4{o[nt][0][i], o[nt][1][i], o[nt][2][i], o[nt][3][i]} * inv;
@@ -947,70 +859,180 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
     }
   };
 
-  if (nsplit == 1) {
-    if (has_rows) {
-      float lw[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) lw[nt] = st.l[nt][0];
-      write_rows(st.m, lw, lxw, st.o);
-    }
-    return;
-  }
-
-  // ---- publish this wave's record for the split: row stats as float4 (m, l, lx, -) per row, then
-  // the outputs as chunk (nt, dt) x lane float4s (1 KiB contiguous per store instruction)
-  const int unit_local = gather ? unit : unit - p.units_g;
-  const float* rec_base = p.part + (gather ? 0 : (int64_t)p.units_g * kBWaves * p.nsplit_g * RB::kRec);
-  const __amdgpu_buffer_rsrc_t urec =
-      make_rsrc(rec_base + ((int64_t)unit_local * kBWaves + wave) * nsplit * RB::kRec, (uint32_t)(nsplit * RB::kRec * 4));
+  // ---- records of the unit: piece (b, w) at slot base(b) + w - wlo(b), one record per row block
+  const int rec_per_unit = p.nW + p.nbr - 1;
+  const float* unit_rec = p.part + (int64_t)unit * rec_per_unit * kBWaves * RB::kRec;
   constexpr uint32_t kOutOff = 16 * RB::kRows;
-  if (has_rows) {
-    const uint32_t rec = (uint32_t)split * RB::kRec * 4;
+
+  int off = 0, rbase = 0;
+  uint64_t to_merge = 0;                          // branches this workgroup merges (nbr <= 64)
+  for (int b = 0; b < p.nbr; ++b) {
+    const int n = branch_len(b);
+    const int off_b = off;
+    off += n;
+    if (n == 0) {
+      // no entries: its rows see nothing; the workgroup whose range holds the branch's place writes it
+      int owner = chunk > 0 ? off_b / chunk : 0;
+      if (owner > p.nW - 1) owner = p.nW - 1;
+      if (owner == w && has_rows) {
+        const float m0[NT] = {-INFINITY, -INFINITY}, z[NT] = {0.f, 0.f};
+        f32x4 oz[NT][8];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) oz[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        write_rows(b, m0, z, z, oz);
+      }
+      continue;
+    }
+    const int wlo = off_b / chunk, whi = (off_b + n - 1) / chunk;
+    const int nwg = whi - wlo + 1;
+    const int slot_b = rbase;
+    rbase += nwg;
+    const int lo = r0 > off_b ? r0 : off_b, hi = r1 < off_b + n ? r1 : off_b + n;
+    if (lo >= hi) continue;
+    const int e_begin = lo - off_b, e_end = hi - off_b;
+    const bool gather = b < p.V;
+    const int32_t* idx_row = gather ? p.idx + (((int64_t)b * p.S + s) * p.Hkv + g) * p.ld_idx : nullptr;
+    const bool want_lx = (gather ? p.lse_g : p.lse_f) != nullptr;
+    const int ntiles = (e_end - e_begin + kTile - 1) / kTile;
+
+    __syncthreads();                              // the previous piece's slot table and ring are free
+    fill_slot_table<PAGED, kBThreads, kBSlotCap>(p.kv, s, g, L, idx_row, e_begin, e_end, (ntiles + kBRing) * kTile,
+                                                 sm.roff, sm.tpos, tid);
+    __syncthreads();
+
+    RowState<NT> st;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      if (lg == 0) store16_coherent(urec, rec + 16 * (16 * nt + lr), f32x4{st.m[nt], st.l[nt][0], lxw[nt], 0.f});
+      st.m[nt] = -INFINITY;
+      st.l[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      st.lx[nt] = 0.f;
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) store16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + dt) * kWave + lane), st.o[nt][dt]);
+      for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-  }
-  wait_vmem();
-  __syncthreads();
-  if (tid == 0) sm.last = arrive(counter_line(p.counters, unit), (uint32_t)nsplit);
-  __syncthreads();
-  if (!sm.last) return;
-  if (tid == 0) reset_counter(counter_line(p.counters, unit));   // ready for the next call
-  if (!has_rows) return;
+    // prologue: tiles 0 .. kBRing-2
+    for (int t = 0; t < kBRing - 1; ++t) {
+      uint32_t r[2];
+      asm volatile(
+          "ds_read_b32 %0, %2\n"
+          "ds_read_b32 %1, %3\n"
+          "s_waitcnt lgkmcnt(0)"
+          : "=&v"(r[0]), "=&v"(r[1])
+          : "v"(roff_lds + 4 * (kTile * t + rit0)), "v"(roff_lds + 4 * (kTile * t + rit1)));
+      issue(t, r);
+    }
+    TileRegs<NT, true> T;
+    // tile t+kBRing-1 is issued in step t, after the barrier that frees its slot (read in step t-1)
+    for (int t = 0; t < ntiles; ++t) {
+      // this wave's loads of tile t are older than the kBRing-2 tiles issued after it
+      asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+      static_assert(2 * (kBRing - 2) == 8, "wait count follows the ring depth");
+      const int nxt = t + kBRing - 1;
+      const uint32_t src = ring_lds + (uint32_t)(t % kBRing) * kTileBytes;
+      uint32_t r[2];
+      read_block_tile_k(T, r, src, tpos_lds, kTile * t, roff_lds, kTile * nxt, rit0, rit1, lane);
+      bool bad = false;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int tp = (int)T.tp[i >> 2][i & 3];
+        bad |= tp < 0 || tp > minpos;
+      }
+      const bool dirty = __builtin_amdgcn_ballot_w64(bad) != 0;
+      issue(nxt, r);
+      if (has_rows)
+        tile_step<NT, true, TRAIN>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx,
+                                   [&](int i) { return (int)T.tp[i >> 2][i & 3]; },
+                                   [&](u32x4 (&v)[8]) { read_v8(v, src + 8 * 1024 + 16 * lane); });
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the ring is reused
 
-  // merge this wave's row block over the splits, in split order, with an online rescale
-  float Mg[NT], Lg[NT], Lxg[NT];
-  f32x4 og[NT][8];
+    // ---- per-row results of this wave: (m, l, lx) of rows 16*nt + lane%16
+    float lxw[NT], lw[NT];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    Mg[nt] = -INFINITY;
-    Lg[nt] = 0.f;
-    Lxg[nt] = 0.f;
+    for (int nt = 0; nt < NT; ++nt) {
+      float lx = st.lx[nt];
+      lx += shfl_xor_f(lx, 16);
+      lx += shfl_xor_f(lx, 32);
+      lxw[nt] = lx;
+      lw[nt] = st.l[nt][0];
+    }
+    if (nwg == 1) {                               // the whole branch ran here
+      if (has_rows) write_rows(b, st.m, lw, lxw, st.o);
+      continue;
+    }
+
+    // ---- publish the piece as record slot_b + w - wlo of this row block: row stats as float4
+    // (m, l, lx, -) per row, then the outputs as chunk (nt, dt) x lane float4s
+    const __amdgpu_buffer_rsrc_t urec =
+        make_rsrc(unit_rec + ((int64_t)slot_b * kBWaves + wave) * RB::kRec, (uint32_t)(nwg * kBWaves * RB::kRec * 4));
+    if (has_rows) {
+      const uint32_t rec = (uint32_t)(w - wlo) * kBWaves * RB::kRec * 4;
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) og[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
+      for (int nt = 0; nt < NT; ++nt) {
+        if (lg == 0) store16_coherent(urec, rec + 16 * (16 * nt + lr), f32x4{st.m[nt], lw[nt], lxw[nt], 0.f});
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const uint32_t rec = (uint32_t)sp * RB::kRec * 4;
-      const f32x4 sv = load16_coherent(urec, rec + 16 * (16 * nt + lr));
-      f32x4 ov[8];
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) ov[dt] = load16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + dt) * kWave + lane));
-      const float mb = fmaxf(Mg[nt], sv[0]);
-      const float mbu = mb == -INFINITY ? 0.f : mb;
-      const float sc = exp2f(Mg[nt] - mbu), wt = exp2f(sv[0] - mbu);
-      Lg[nt] = Lg[nt] * sc + wt * sv[1];
-      Lxg[nt] = Lxg[nt] * sc + wt * sv[2];
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) og[nt][dt] = og[nt][dt] * sc + ov[dt] * wt;
-      Mg[nt] = mb;
+        for (int dt = 0; dt < 8; ++dt)
+          store16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + dt) * kWave + lane), st.o[nt][dt]);
+      }
+    }
+    wait_vmem();
+    __syncthreads();
+    uint32_t* ctr = counter_line(p.counters, (int64_t)unit * p.nbr + b);
+    if (tid == 0) sm.last = arrive(ctr, (uint32_t)nwg);
+    __syncthreads();
+    if (sm.last) {
+      if (tid == 0) reset_counter(ctr);           // ready for the next call
+      to_merge |= 1ull << b;                      // merged after the last piece, when its state is gone
     }
   }
-  write_rows(Mg, Lg, Lxg, og);
+
+  // ---- branches whose pieces this workgroup completed: merge each row block over the pieces, in
+  // stream order, with an online rescale
+  off = 0;
+  rbase = 0;
+  for (int b = 0; b < p.nbr; ++b) {
+    const int n = branch_len(b);
+    const int off_b = off;
+    off += n;
+    if (n == 0) continue;
+    const int wlo = off_b / chunk, whi = (off_b + n - 1) / chunk;
+    const int nwg = whi - wlo + 1;
+    const int slot_b = rbase;
+    rbase += nwg;
+    if (!((to_merge >> b) & 1ull) || !has_rows) continue;
+    const __amdgpu_buffer_rsrc_t urec =
+        make_rsrc(unit_rec + ((int64_t)slot_b * kBWaves + wave) * RB::kRec, (uint32_t)(nwg * kBWaves * RB::kRec * 4));
+    float Mg[NT], Lg[NT], Lxg[NT];
+    f32x4 og[NT][8];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      Mg[nt] = -INFINITY;
+      Lg[nt] = 0.f;
+      Lxg[nt] = 0.f;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) og[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      for (int k = 0; k < nwg; ++k) {
+        const uint32_t rec = (uint32_t)k * kBWaves * RB::kRec * 4;
+        const f32x4 sv = load16_coherent(urec, rec + 16 * (16 * nt + lr));
+        f32x4 ov[8];
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) ov[dt] = load16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + dt) * kWave + lane));
+        const float mb = fmaxf(Mg[nt], sv[0]);
+        const float mbu = mb == -INFINITY ? 0.f : mb;
+        const float sc = exp2f(Mg[nt] - mbu), wt = exp2f(sv[0] - mbu);
+        Lg[nt] = Lg[nt] * sc + wt * sv[1];
+        Lxg[nt] = Lxg[nt] * sc + wt * sv[2];
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) og[nt][dt] = og[nt][dt] * sc + ov[dt] * wt;
+        Mg[nt] = mb;
+      }
+    }
+    write_rows(b, Mg, Lg, Lxg, og);
+  }
 }
 
 }  // namespace
@@ -1027,6 +1049,26 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
   // two-term weights) exist only there
   pl.block = pl.n_rb >= 2 || train;
   pl.n_rg = pl.block ? (pl.n_rb + kBWaves - 1) / kBWaves : pl.n_rb;
+  pl.counter_bytes = BD_WS_COUNTER_BYTES;   // fixed: scratch of any call never lands on a counter
+  if (pl.block) {
+    // workgroups per (sequence, KV head, row group) unit, each taking an equal share of the unit's
+    // key stream: enough to fill the CUs once, and enough that no share (rounded up to whole tiles)
+    // overflows the slot table
+    pl.units = S * Hkv * pl.n_rg;
+    pl.nbr = num_views + (with_full ? 1 : 0);
+    const int64_t stream_max = (int64_t)num_views * ld_idx + (with_full ? max_L : 0);
+    int64_t nw = (kTargetBlocks + pl.units - 1) / pl.units;
+    const int64_t nw_table = (stream_max + kMaxSplitKeys - 1) / kMaxSplitKeys;
+    if (nw < nw_table) nw = nw_table;
+    if (nw < 1) nw = 1;
+    pl.nW = (int)nw;
+    const int64_t blocks = (int64_t)pl.units * nw;
+    pl.nblk = blocks > INT32_MAX ? -1 : (int)blocks;
+    const size_t records = (size_t)pl.units * (nw + pl.nbr - 1) * kBWaves;   // one per piece and row block
+    pl.record_bytes = nw > 1 ? align256(sizeof(float) * attn_record_floats(2) * records) : 0;
+    pl.ws_bytes = pl.counter_bytes + pl.record_bytes;
+    return pl;
+  }
   pl.units_g = num_views * S * Hkv * pl.n_rg;
   pl.units_f = with_full ? S * Hkv * pl.n_rg : 0;
   constexpr int64_t kStep = kWaves * kTile;       // one tile per wave of the split kernel
@@ -1056,10 +1098,8 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
   pl.nsplit_f = max_L > 0 ? (int)((max_L + kf - 1) / kf) : 1;
   blocks = (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f;
   pl.nblk = (int)blocks;
-  pl.counter_bytes = BD_WS_COUNTER_BYTES;   // fixed: scratch of any call never lands on a counter
   const bool split = (pl.units_g && pl.nsplit_g > 1) || (pl.units_f && pl.nsplit_f > 1);
-  const size_t records = (size_t)blocks * (pl.block ? kBWaves : 1);   // block mode: one per row block
-  pl.record_bytes = split ? align256(sizeof(float) * attn_record_floats(pl.nt) * records) : 0;
+  pl.record_bytes = split ? align256(sizeof(float) * attn_record_floats(pl.nt) * (size_t)blocks) : 0;
   pl.ws_bytes = pl.counter_bytes + pl.record_bytes;
   return pl;
 }

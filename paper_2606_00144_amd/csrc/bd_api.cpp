@@ -89,12 +89,15 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
   const bd::AttnPlan pl =
       bd::plan_attn(kv->num_seqs, kv->num_kv_heads, Hq, nq, num_views, ld_idx, kv->max_seq_len, out_full != nullptr,
                     kv->page_table != nullptr, train);
-  if (pl.nblk < 0 || (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f > INT32_MAX)
+  if (pl.nblk < 0 || (!pl.block && (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f > INT32_MAX))
     return fail(BD_ERR_UNSUPPORTED, "problem too large for one launch");
   if (kv_extent(kv) > ((int64_t)1 << 34))
     return fail(BD_ERR_UNSUPPORTED, "K/V layout spans more than 2^34 elements");
-  if ((int64_t)pl.units_g + pl.units_f > BD_WS_COUNTER_LINES)
+  if ((pl.block ? (int64_t)pl.units * pl.nbr : (int64_t)pl.units_g + pl.units_f) > BD_WS_COUNTER_LINES)
     return fail(BD_ERR_UNSUPPORTED, "more than %d work units", BD_WS_COUNTER_LINES);
+  if (pl.block && (int64_t)(pl.nW + pl.nbr) * 8 * bd::attn_record_floats(2) * 4 > INT32_MAX)
+    return fail(BD_ERR_UNSUPPORTED, "too many partial records per unit");
+  if (pl.block && pl.nbr > 64) return fail(BD_ERR_UNSUPPORTED, "more than 63 views with a block of more than 32 rows");
   bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
   if (st != BD_OK) return st;
   if (pl.nblk == 0) return BD_OK;
@@ -124,6 +127,9 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
   p.kps_f = pl.kps_f;
   p.units_g = pl.units_g;
   p.nblk_g = pl.units_g * pl.nsplit_g;
+  p.V = num_views;
+  p.nbr = pl.nbr;
+  p.nW = pl.nW;
   p.scale_log2 = scale * 1.4426950408889634f;
   p.max_roff = (uint32_t)((kv_extent(kv) - BD_HEAD_DIM) >> 3);
   p.counters = static_cast<uint32_t*>(ws);

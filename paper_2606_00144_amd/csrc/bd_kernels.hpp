@@ -35,6 +35,8 @@ struct AttnParams {
   int32_t nsplit_f, kps_f;  // full units: splits and keys per split
   int32_t units_g;          // gathered units (their blocks come first)
   int32_t nblk_g;           // blocks of gathered units
+  int32_t V, nbr;           // block mode: views, and branches (views + full)
+  int32_t nW;               // block mode: workgroups per (s, g, row group), equal shares of its key stream
   float scale_log2;         // softmax scale * log2(e)
   uint32_t max_roff;        // largest valid row offset of the K/V layout, 16-byte units
   float* part;              // partial records
@@ -47,6 +49,7 @@ struct AttnPlan {
   int n_rg;
   int nsplit_g, kps_g, nsplit_f, kps_f;
   int units_g, units_f, nblk;
+  int units, nbr, nW;       // block mode: (s, g, row group) units, branches, workgroups per unit
   size_t counter_bytes, record_bytes, ws_bytes;
 };
 
