@@ -747,3 +747,35 @@ def test_attend_backward_finite_differences():
             args2 = [q, k, v]; args2[which] = b2
             fd = (f(*args) - f(*args2)) / (2 * eps)
             assert abs(fd - grad[idx]) < 1e-6 * max(1.0, abs(fd)), (which, idx, fd, grad[idx])
+
+
+def test_multiview_backward_counts_repeated_entries():
+    """A view over a multiset: a key listed twice takes two softmax weights (the forward's reading)
+    and its gradient is the sum over its entries.  fp64 autograd through index_select with a
+    repeated index accumulates exactly that."""
+    g = np.random.default_rng(62)
+    S, Hkv, Hq, L, C = 1, 1, 2, 24, 4
+    k, v = bits(g.standard_normal((S, Hkv, L, 128))), bits(g.standard_normal((S, Hkv, L, 128)))
+    q = bits(g.standard_normal((S, C, Hq, 128)))
+    J = np.array([0, 3, 3, 7, 21, 22, 22, 23, 9, -1, 30], np.int64)   # repeats, a block row twice, absent tails
+    idx = [J.astype(np.int32).reshape(1, 1, -1)]
+    nsel = [np.array([len(J)])]
+    dov = g.standard_normal((1, S, C, Hq, 128))
+    dq, dk, dv = O.multiview_attn_bwd(k, v, q, idx, nsel, [L], dov, None)
+    sc = float(np.float32(1 / np.sqrt(128)))
+    kt = torch.from_numpy(O.bf16_to_f64(k[0, 0])).requires_grad_(True)
+    vt = torch.from_numpy(O.bf16_to_f64(v[0, 0])).requires_grad_(True)
+    qt = torch.from_numpy(O.bf16_to_f64(q[0])).requires_grad_(True)               # [C][Hq][D]
+    Jv = torch.from_numpy(J[(J >= 0) & (J < L)])
+    kj, vj = kt.index_select(0, Jv), vt.index_select(0, Jv)
+    pos = torch.arange(L - C, L)
+    total = 0.0
+    for h in range(Hq):
+        logits = sc * qt[:, h] @ kj.T
+        p = torch.softmax(logits.masked_fill(Jv[None, :] > pos[:, None], float("-inf")), dim=1)
+        total = total + (torch.from_numpy(dov[0, 0, :, h]) * (p @ vj)).sum()
+    total.backward()
+    np.testing.assert_allclose(dq[0], qt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dk[0, :, 0], kt.grad.numpy()[L - C:], rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dv[0, :, 0], vt.grad.numpy()[L - C:], rtol=1e-10, atol=1e-12)
+    assert np.abs(kt.grad.numpy()[22]).max() > 0                                 # the repeated block row has a gradient
