@@ -267,3 +267,26 @@ def test_one_workspace_serves_every_operation_and_shape():
         torch.cuda.synchronize()
         ra, rb, _ = O.accept_len(lg, dr, gamma)
         assert np.array_equal(acc.cpu().numpy(), ra) and np.array_equal(bonus.cpu().numpy(), rb)
+
+
+def test_multiview_block_mode_unbalanced_views_and_empty_branches():
+    """Block mode with views far shorter than the list capacity, an empty view, an all-absent view and a
+    sequence shorter than the block: every branch's rows are written, empty ones as 0."""
+    S, Hkv, G, C = 3, 2, 4, 48
+    lens = [2000, 30, 777]
+    Lm = max(lens)
+    k, v = _rand_bits((S, Hkv, Lm, 128), 110), _rand_bits((S, Hkv, Lm, 128), 111)
+    qb = _rand_bits((S, C, Hkv * G, 128), 112)
+    g = np.random.default_rng(113)
+    ld = 2048
+    budgets = [64, 0, 5, 1500]
+    idx_v = np.full((len(budgets), S, Hkv, ld), -1, np.int32)
+    nsel_v = np.zeros((len(budgets), S), np.int32)
+    for i, B in enumerate(budgets):
+        for s, L in enumerate(lens):
+            n = min(B, L)
+            for h in range(Hkv):
+                idx_v[i, s, h, :n] = np.sort(g.choice(L, n, replace=False))
+            nsel_v[i, s] = n
+    idx_v[2, :, :, :5] = -1                            # view 2: five slots, all absent
+    _multiview_check(k, v, qb, idx_v, nsel_v, lens, "block mode, unbalanced and empty views")

@@ -222,3 +222,22 @@ def test_bwd_deterministic_and_workspace_reuse():
     b = _run(k, v, qb, idx_v, nsel_v, [L, L], "det 2", seed=9, workspace=ws, check_fwd=False)
     for x, y in zip(a, b):
         assert torch.equal(x, y)
+
+
+def test_bwd_two_row_groups_and_many_views():
+    """C * G = 320 rows per KV head (two row groups of up to 8 row blocks, the second partly empty) and
+    nine views of mixed lengths (two empty): the block-mode forward and both backward kernels."""
+    S, Hkv, G, L, C = 2, 2, 5, 900, 64
+    k, v = _rand_bits((S, Hkv, L, 128), 100), _rand_bits((S, Hkv, L, 128), 101)
+    qb = _rand_bits((S, C, Hkv * G, 128), 102)
+    g = np.random.default_rng(103)
+    V, ld = 9, 400
+    idx_v = np.full((V, S, Hkv, ld), -1, np.int32)
+    nsel_v = np.zeros((V, S), np.int32)
+    for i in range(V):
+        n = [0, 37, 400, 129, 0, 256, 64, 311, 100][i]
+        for s in range(S):
+            for h in range(Hkv):
+                idx_v[i, s, h, :n] = np.sort(g.choice(L, n, replace=False))
+            nsel_v[i, s] = n
+    _run(k, v, qb, idx_v, nsel_v, [L, L - 3], "two row groups, nine views", seed=10)
