@@ -13,6 +13,11 @@ struct BoolTag { static constexpr bool value = B; };
 __device__ inline void dma16(const uint16_t* g, uint8_t* l) {
   __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)l, 16, 0, 0);
 }
+// The same with the non-temporal policy (nt), for data read once per call.
+constexpr int kPolicyNt = 2;
+__device__ inline void dma16_nt(const uint16_t* g, uint8_t* l) {
+  __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)l, 16, 0, kPolicyNt);
+}
 
 // Transposed operand for d-tile dt from 8 rows of 16 bytes per lane (row slot i = register i,
 // bytes 16*(lane%16) of the row): slot i of the result holds row i's element 8*(lane%16) + dt.
