@@ -78,7 +78,8 @@ struct AttnSmem {
       alignas(16) uint8_t ring[kWaves][kRing][kTileBytes];   // per-wave tile slots filled by DMA
     } slots;
     struct {
-      alignas(16) float o[kWaves][16 * NT][kD];     // per-wave unnormalised outputs
+      alignas(16) float o[kWaves][16 * NT][kD + 4]; // per-wave unnormalised outputs (rows padded: the
+                                                    // 16 rows a store instruction writes hit distinct banks)
       float m[kWaves][16 * NT];
       float l[kWaves][16 * NT];
       float lx[kWaves][16 * NT];
@@ -337,6 +338,25 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
   }
 }
 
+// Kernel arguments reach the waves through the scalar cache, one 64-byte line per miss, and the
+// compiler fetches each where it is first used: a memory round trip apiece, several in a row before
+// the first data load and again before the merge.  Naming them all at entry has every line
+// requested at once, so the arguments cost one round trip.  The statements touch no memory (so the
+// uniform loads after them stay scalar) and return 0, which the caller adds to its block index.
+__device__ inline int fetch_args(const AttnParams& p) {
+  int z0, z1, z2;
+  asm("s_mov_b32 %0, 0" : "=s"(z0) : "s"(p.kv.k), "s"(p.kv.v), "s"(p.kv.seq_lens), "s"(p.kv.page_table),
+      "s"(p.kv.stride_seq), "s"(p.kv.stride_head), "s"(p.kv.stride_tok), "s"(p.kv.stride_page),
+      "s"(p.kv.max_seq_len), "s"(p.kv.page_size), "s"(p.kv.max_pages_per_seq), "s"(p.kv.num_pages));
+  asm("s_mov_b32 %0, 0" : "=s"(z1) : "s"(z0), "s"(p.q), "s"(p.out_g), "s"(p.out_f), "s"(p.lse_g), "s"(p.lse_f),
+      "s"(p.idx), "s"(p.nsel), "s"(p.ld_idx), "s"(p.S), "s"(p.Hkv), "s"(p.Hq), "s"(p.G), "s"(p.nq), "s"(p.R),
+      "s"(p.n_rb));
+  asm("s_mov_b32 %0, 0" : "=s"(z2) : "s"(z1), "s"(p.nsplit_g), "s"(p.kps_g), "s"(p.nsplit_f), "s"(p.kps_f),
+      "s"(p.units_g), "s"(p.nblk_g), "s"(p.nblk), "s"(p.scale_log2), "s"(p.max_roff), "s"(p.part),
+      "s"(p.counters));
+  return z2;
+}
+
 template <int NT, bool PAGED>
 __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   using RB = RowBlock<NT>;
@@ -346,48 +366,64 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   const int lg = lane >> 4, lr = lane & 15;
 
   // ---- which (kind, unit, split) this workgroup owns
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int bid = xcd_remap(blockIdx.x + fetch_args(p), p.nblk);
   const bool gather = bid < p.nblk_g;
   const int local = gather ? bid : bid - p.nblk_g;
   const int nsplit = gather ? p.nsplit_g : p.nsplit_f;
   const int kps = gather ? p.kps_g : p.kps_f;
-  const int rb = local % p.n_rb;
-  const int rest = local / p.n_rb;
-  const int split = rest % nsplit;
-  const int pair = rest / nsplit;          // gather: (view, s, g); full: (s, g)
-  const int g = pair % p.Hkv;
-  const int vs = pair / p.Hkv;             // gather: view*S + s; full: s
-  const int s = gather ? vs % p.S : vs;
-  const int view = gather ? vs / p.S : 0;
+  // block indices are far below 2^22: float-reciprocal divisions
+  const int rest = div_small(local, p.n_rb);
+  const int rb = local - rest * p.n_rb;
+  const int pair = div_small(rest, nsplit);  // gather: (view, s, g); full: (s, g)
+  const int split = rest - pair * nsplit;
+  const int vs = div_small(pair, p.Hkv);     // gather: view*S + s; full: s
+  const int g = pair - vs * p.Hkv;
+  const int view = gather ? div_small(vs, p.S) : 0;
+  const int s = vs - view * p.S;
   const int unit = gather ? pair * p.n_rb + rb : p.units_g + pair * p.n_rb + rb;
 
-  const int L = seq_len(p.kv, s);
-  int n_keys;
-  const int32_t* idx_row = nullptr;
-  if (gather) {
-    idx_row = p.idx + ((int64_t)vs * p.Hkv + g) * p.ld_idx;
-    int n = p.nsel[vs];
-    n_keys = n < 0 ? 0 : (n > p.ld_idx ? p.ld_idx : n);
-  } else {
-    n_keys = L;
-  }
-  // ---- query rows of this lane: row n = rb*RB + 16*nt + lane%16 (loads issued before the slot
-  // table is built, so their latency overlaps it)
+  // ---- prologue: every load it needs (cache length, entry count, query rows, the split's idx
+  // entries) is issued before any of them is used, so they share one memory round trip
+  const int L_raw = p.kv.seq_lens[s];
+  const int n_raw = *(gather ? p.nsel + vs : p.kv.seq_lens + s);
+  const int32_t* idx_row = gather ? p.idx + ((int64_t)vs * p.Hkv + g) * p.ld_idx : nullptr;
+  // query rows of this lane: row n = rb*RB + 16*nt + lane%16
   bf16x8 qop[NT][4];
-  int rowpos[NT];
+  int qj[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const int n = rb * RB::kRows + 16 * nt + lr;
     const bool valid = n < p.R;
-    const int j = valid ? n / p.G : 0;
-    const int h = g * p.G + (valid ? n % p.G : 0);
-    rowpos[nt] = valid ? L - p.nq + j : 0x7FFFFFFF;
+    const int jn = div_small(n, p.G);
+    const int j = valid ? jn : 0;
+    const int h = g * p.G + (valid ? n - jn * p.G : 0);
+    qj[nt] = valid ? j : -1;
     const uint16_t* qrow = p.q + (((int64_t)s * p.nq + j) * p.Hq + h) * kD + 32 * lg;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = as_bf16x8(valid ? load16(qrow + 8 * kk) : u32x4{0u, 0u, 0u, 0u});
   }
-
+  // the causal prefix of a contiguous cache needs no slot table: row offsets are computed
+  const bool arith = !PAGED && !gather;
   const int e_begin = split * kps;
+  // slot-table entries: the idx loads do not wait for the entry count (every entry of the split
+  // below ld_idx lies in the list's row; those past the count are dropped once it has arrived)
+  constexpr int kPer = (kSlotCap + kThreads - 1) / kThreads;
+  int tv[kPer];
+  if (!arith) {
+    const int e_lim = gather ? (e_begin + kps < p.ld_idx ? e_begin + kps : p.ld_idx) : e_begin + kps;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int e = e_begin + tid + k * kThreads;
+      tv[k] = e < e_lim ? (gather ? idx_row[e] : e) : -1;
+    }
+  }
+
+  const int L = L_raw < 0 ? 0 : (L_raw > p.kv.max_seq_len ? p.kv.max_seq_len : L_raw);
+  const int n_keys = gather ? (n_raw < 0 ? 0 : (n_raw > p.ld_idx ? p.ld_idx : n_raw)) : L;
+  int rowpos[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) rowpos[nt] = qj[nt] >= 0 ? L - p.nq + qj[nt] : 0x7FFFFFFF;
+
   int e_end = e_begin + kps;
   if (e_end > n_keys) e_end = n_keys;
 
@@ -395,18 +431,14 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   const int nslots = (ntiles + kMaxAhead * kWaves) * kTile;     // <= kSlotCap: padding tiles included
   // a tile needs the visibility mask when one of its slots is absent or lies after the earliest
   // row position of this row block; the first such tile bounds the mask-free ones
-  const int minpos = L - p.nq + (rb * RB::kRows) / p.G;
-  // the causal prefix of a contiguous cache needs no slot table: row offsets are computed
-  const bool arith = !PAGED && !gather;
+  const int minpos = L - p.nq + div_small(rb * RB::kRows, p.G);
   if (!arith) {
-    // all idx and page-table loads are issued before any result is used
-    constexpr int kPer = (kSlotCap + kThreads - 1) / kThreads;
-    int tv[kPer];
+    // entries past the split's end or outside [0, L) become padding; all page-table loads are
+    // issued before any result is used
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
       const int e = e_begin + tid + k * kThreads;
-      int t = -1;
-      if (e < e_end) t = gather ? idx_row[e] : e;
+      const int t = e < e_end ? tv[k] : -1;
       tv[k] = (t >= 0 && t < L) ? t : -1;
     }
     int pg[kPer];
@@ -415,24 +447,30 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
       for (int k = 0; k < kPer; ++k)
         pg[k] = tv[k] >= 0 ? p.kv.page_table[(int64_t)s * p.kv.max_pages_per_seq + tv[k] / p.kv.page_size] : 0;
     }
+    // row offsets in 16-byte units: 32-bit products for a contiguous cache (strides are multiples
+    // of 8 elements and every offset stays below max_roff < 2^32, both checked on the host)
+    const uint32_t base16 = (uint32_t)(((int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head) >> 3);
+    const uint32_t tok16 = (uint32_t)(p.kv.stride_tok >> 3);
     int first_dirty = 0x7FFFFFFF;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
+      if (k * kThreads >= nslots) break;     // uniform: the rest of the table is unused
       const int i = tid + k * kThreads;
       bool bad = false;
       if (i < nslots) {
         int t = tv[k];
-        int64_t o;
+        uint32_t ro;
         if constexpr (PAGED) {
-          o = (unsigned)pg[k] < (unsigned)p.kv.num_pages
-                  ? (int64_t)pg[k] * p.kv.stride_page + (int64_t)g * p.kv.stride_head +
-                        (int64_t)(t % p.kv.page_size) * p.kv.stride_tok
-                  : -1;
+          const int64_t o = (unsigned)pg[k] < (unsigned)p.kv.num_pages
+                                ? (int64_t)pg[k] * p.kv.stride_page + (int64_t)g * p.kv.stride_head +
+                                      (int64_t)(t % p.kv.page_size) * p.kv.stride_tok
+                                : -1;
+          if (t < 0 || o < 0) t = -1;
+          ro = t < 0 ? 0u : (uint32_t)(o >> 3);
         } else {
-          o = (int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head + (int64_t)t * p.kv.stride_tok;
+          ro = t < 0 ? 0u : base16 + (uint32_t)t * tok16;
         }
-        if (t < 0 || o < 0) { t = -1; o = 0; }
-        sm.u.slots.roff[i] = (int)(o >> 3);
+        sm.u.slots.roff[i] = (int)ro;
         sm.u.slots.tpos[i] = t;
         bad = i < ntiles * kTile && (t < 0 || t > minpos);
       }
@@ -1116,7 +1154,9 @@ static hipError_t launch_nt(const AttnParams& p, int nblocks, hipStream_t stream
   return hipGetLastError();
 }
 
-hipError_t launch_attn(const AttnParams& p, const AttnPlan& pl, bool paged, hipStream_t stream) {
+hipError_t launch_attn(const AttnParams& args, const AttnPlan& pl, bool paged, hipStream_t stream) {
+  AttnParams p = args;
+  p.nblk = pl.nblk;
   if (pl.block) {
     const bool train = p.o32_g || p.o32_f;
     if (train) {

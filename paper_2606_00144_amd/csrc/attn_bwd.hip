@@ -67,16 +67,6 @@ struct DqSmem {
   int32_t last;
 };
 
-// n / d for 0 <= n < 2^22, d >= 1, with inv_d = 1/d: the float estimate is within one of the
-// quotient, and one correction each way makes it exact (a VALU integer division costs tens of
-// instructions, and the dK/dV tile loop needs several per row).
-__device__ inline int div_small(int n, int d, float inv_d) {
-  int q = (int)((float)n * inv_d);
-  q += (q + 1) * d <= n ? 1 : 0;
-  q -= q * d > n ? 1 : 0;
-  return q;
-}
-
 // Tile load q of a lane (0..23).  q < 8: K, score layout (key sub-tile q/4 -> rows 16*(q/4) + lane%16,
 // 16 bytes at d = 32*(lane/16) + 8*(q%4)); 8 <= q < 16: V, same layout; 16 <= q < 24: K, transposed
 // layout (rows 16*((q-16)/4) + 4*(lane/16) + (q-16)%4, 16 bytes at d = 8*(lane%16)).

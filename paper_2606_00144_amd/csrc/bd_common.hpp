@@ -66,6 +66,17 @@ __device__ inline int xcd_remap(int b, int n) {
   return x * q + (x < r ? x : r) + j;
 }
 
+// n / d for 0 <= n < 2^22, d >= 1, with inv_d = 1/d to within an ulp: the float estimate is within
+// one of the quotient, and one correction each way makes it exact (a VALU integer division costs
+// tens of instructions).
+__device__ inline int div_small(int n, int d, float inv_d) {
+  int q = (int)((float)n * inv_d);
+  q += (q + 1) * d <= n ? 1 : 0;
+  q -= q * d > n ? 1 : 0;
+  return q;
+}
+__device__ inline int div_small(int n, int d) { return div_small(n, d, __builtin_amdgcn_rcpf((float)d)); }
+
 // ---- cross-lane reductions ------------------------------------------------
 
 // xor-shuffle through the LDS crossbar (ds_bpermute); works across all 64 lanes.

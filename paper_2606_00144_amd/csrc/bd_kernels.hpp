@@ -37,6 +37,7 @@ struct AttnParams {
   int32_t nblk_g;           // blocks of gathered units
   int32_t V, nbr;           // block mode: views, and branches (views + full)
   int32_t nW;               // block mode: workgroups per (s, g, row group), equal shares of its key stream
+  int32_t nblk;             // workgroups of the launch (set by launch_attn)
   float scale_log2;         // softmax scale * log2(e)
   uint32_t max_roff;        // largest valid row offset of the K/V layout, 16-byte units
   float* part;              // partial records
