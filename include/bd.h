@@ -77,7 +77,8 @@ extern "C" {
 typedef int32_t bd_status;
 #define BD_OK 0
 #define BD_ERR_INVALID_ARG 1 /* a pointer, size or shape that the contract forbids */
-#define BD_ERR_UNSUPPORTED 2 /* a valid request this build does not implement (head_dim != 128, ...) */
+#define BD_ERR_UNSUPPORTED 2 /* a valid request this build does not implement (head_dim != 128,
+                               launches of 2^22 or more workgroups, ...) */
 #define BD_ERR_WORKSPACE 3   /* workspace missing, too small or misaligned */
 #define BD_ERR_DEVICE 4      /* the HIP runtime rejected a launch */
 
@@ -279,7 +280,9 @@ bd_status bd_verify_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_
  * logits  row (s, i) at logits + (s*(gamma+1) + i) * row_stride, fp32, finite.
  * draft   [S][gamma] int32.
  * accept_out [S] int32; bonus_out NULL or [S]; argmax_out NULL or [S][gamma+1].
- * Requirements: gamma >= 0, vocab >= 1, row_stride >= vocab.
+ * Requirements: gamma >= 0, vocab >= 1, row_stride >= vocab.  BD_ERR_UNSUPPORTED
+ * for gamma > 63 and for shapes whose launch would exceed 2^22 - 1 workgroups
+ * (S*(gamma+1)*ceil(vocab/8192) and more).
  * ---------------------------------------------------------------------- */
 size_t bd_accept_len_workspace_bytes(int32_t num_seqs, int32_t gamma, int32_t vocab);
 bd_status bd_accept_len(const float* logits, int64_t row_stride, const int32_t* draft, int32_t num_seqs,

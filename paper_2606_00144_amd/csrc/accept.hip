@@ -33,6 +33,17 @@ __device__ inline uint64_t shfl_xor_u64(uint64_t x, int m) {
   return ((uint64_t)hi << 32) | lo;
 }
 
+// Every kernel argument requested at entry, so the argument lines cost one memory round trip (the
+// compiler would otherwise fetch each where it is first used).  The statements touch no memory and
+// return 0, which the caller adds to its block index.
+__device__ inline int fetch_args(const AcceptParams& p) {
+  int z;
+  asm("s_mov_b32 %0, 0" : "=s"(z) : "s"(p.logits), "s"(p.row_stride), "s"(p.draft), "s"(p.S), "s"(p.gamma),
+      "s"(p.vocab), "s"(p.nsplit), "s"(p.chunk), "s"(p.vec4), "s"(p.accept_out), "s"(p.bonus_out),
+      "s"(p.argmax_out), "s"(p.counters), "s"(p.nblk));
+  return z;
+}
+
 __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptParams p) {
   __shared__ uint64_t red[kThreads / kWave];
   __shared__ uint64_t rowbest[64];
@@ -40,10 +51,12 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptParams p) {
   const int tid = threadIdx.x;
   const int rows = p.gamma + 1;
   const int nrows = p.S * rows;
-  const int b = xcd_remap(blockIdx.x, gridDim.x);
-  const int split = b % p.nsplit;
-  const int rs = b / p.nsplit;              // s * rows + i
-  const int s = rs / rows;
+  const int b = xcd_remap(blockIdx.x + fetch_args(p), p.nblk);
+  const int rs = div_small(b, p.nsplit);    // s * rows + i
+  const int split = b - rs * p.nsplit;
+  const int s = div_small(rs, rows);
+  // this sequence's drafts, loaded with the first loads (only the sequence's last workgroup uses them)
+  const int my_draft = tid < p.gamma ? p.draft[(int64_t)s * p.gamma + tid] : -1;
   uint32_t* seq_counter = counter_line(p.counters, s);
   uint32_t* row_counter = counter_line(p.counters, p.S + rs);
   auto row_slot = [&](int r) { return reinterpret_cast<uint64_t*>(counter_line(p.counters, p.S + nrows + r)); };
@@ -123,14 +136,19 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptParams p) {
     store_coherent(slot, 0ull);   // the slots start from zero in the next call
   }
   __syncthreads();
-  if (tid == 0) {
-    int k = 0;
-    while (k < p.gamma && p.draft[(int64_t)s * p.gamma + k] == key_index(rowbest[k])) ++k;
-    p.accept_out[s] = k;
-    if (p.bonus_out) p.bonus_out[s] = key_index(rowbest[k]);
-    if (rows > 1) reset_counter(seq_counter);
+  // accepted drafts: the leading run of matches, one ballot over the gamma comparisons (gamma <= 63,
+  // so bit gamma is clear and the run ends there at the latest)
+  if (tid < kWave) {
+    const uint64_t key = tid < rows ? rowbest[tid] : 0ull;
+    const uint64_t match = __builtin_amdgcn_ballot_w64(tid < p.gamma && my_draft == key_index(key));
+    const int k = __builtin_ctzll(~match);
+    if (tid == 0) {
+      p.accept_out[s] = k;
+      if (p.bonus_out) p.bonus_out[s] = key_index(rowbest[k]);
+      if (rows > 1) reset_counter(seq_counter);
+    }
+    if (p.argmax_out && tid < rows) p.argmax_out[(int64_t)s * rows + tid] = key_index(key);
   }
-  if (p.argmax_out && tid < rows) p.argmax_out[(int64_t)s * rows + tid] = key_index(rowbest[tid]);
 }
 
 }  // namespace
@@ -154,8 +172,9 @@ AcceptPlan plan_accept(int S, int gamma, int vocab) {
 }
 
 hipError_t launch_accept(const AcceptParams& p, hipStream_t stream) {
-  const int nblocks = p.S * (p.gamma + 1) * p.nsplit;
-  hipLaunchKernelGGL(accept_kernel, dim3(nblocks), dim3(kThreads), 0, stream, p);
+  AcceptParams a = p;
+  a.nblk = p.S * (p.gamma + 1) * p.nsplit;
+  hipLaunchKernelGGL(accept_kernel, dim3(a.nblk), dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 

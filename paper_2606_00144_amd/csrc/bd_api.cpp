@@ -101,6 +101,7 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
   bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
   if (st != BD_OK) return st;
   if (pl.nblk == 0) return BD_OK;
+  if (pl.nblk >= (1 << 22)) return fail(BD_ERR_UNSUPPORTED, "more than 2^22 - 1 workgroups");
   bd::AttnParams p{};
   p.kv = bd::make_kv_view(*kv);
   p.q = q;
@@ -418,6 +419,8 @@ bd_status bd_accept_len(const float* logits, int64_t row_stride, const int32_t* 
   if ((int64_t)num_seqs * (2 * gamma + 3) > BD_WS_COUNTER_LINES)
     return fail(BD_ERR_UNSUPPORTED, "more than %d sequence and row counter lines", BD_WS_COUNTER_LINES);
   const bd::AcceptPlan pl = bd::plan_accept(num_seqs, gamma, vocab);
+  if ((int64_t)num_seqs * (gamma + 1) * pl.nsplit >= (1 << 22))
+    return fail(BD_ERR_UNSUPPORTED, "more than 2^22 - 1 workgroups");
   bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
   if (st != BD_OK) return st;
   bd::AcceptParams p{};

@@ -120,6 +120,7 @@ struct AcceptParams {
   int32_t S, gamma, vocab;
   int32_t nsplit, chunk;    // vocab chunks per row and floats per chunk
   int32_t vec4;             // rows 16-byte aligned: vector loads
+  int32_t nblk;             // workgroups of the launch (set by launch_accept)
   int32_t* accept_out;
   int32_t* bonus_out;
   int32_t* argmax_out;
