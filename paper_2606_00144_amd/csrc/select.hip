@@ -27,18 +27,19 @@
 namespace bd {
 namespace {
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;                        // two per SIMD: one wave's MFMA and loads overlap another's VALU
 constexpr int kThreads = kWaves * kWave;
 constexpr int kTile = 32;                        // keys per wave iteration (two MFMA sub-tiles of 16)
 constexpr int kTileLoads = 8;                    // 16-byte loads per lane per tile
 constexpr int kTileBytes = kTileLoads * kWave * 16;
-constexpr int kRing = 4;                         // tiles in flight per wave
+constexpr int kRing = 2;                         // tile slots per wave: one in flight while one is computed
 constexpr int kMaxPagedKeys = 4096;              // keys per workgroup through the paged slot table
 constexpr int kSlotCap = kMaxPagedKeys + kRing * kWaves * kTile;
 constexpr int kStatRows = 128;                   // stats record stride (rows)
 constexpr int kTargetBlocks = 256;               // one workgroup per CU
 constexpr int kTopkThreads = 1024;
 constexpr int kMaxPerThread = BD_SELECT_MAX_PREFIX / kTopkThreads;   // 32
+constexpr int kRadixBins0 = 4096;               // bins of the first radix digit (12 bits)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kSlack = 8.f;                    // lazy-rescale headroom of the pass-1 sums, log2 units
 
@@ -106,7 +107,7 @@ __device__ inline void read_krows(uint32_t (&r)[2], uint32_t roff_lds, int slot0
 }
 
 // One pass over the causal key range of (sequence, KV head, row block, split).  Each wave streams
-// every 4th 32-key tile through a kRing-deep ring of LDS slots.
+// every kWaves-th 32-key tile through a kRing-deep ring of LDS slots.
 //   PASS 1: per observation row, running max and sum of exp of the scaled logits;
 //   PASS 2: every key's column sum of the rows' normalised weights (complete within the row
 //           block: one plain store per key).
@@ -171,7 +172,9 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
 
   // lse of each row (pass 2): the caller's, or merged from the pass-1 statistics.  Padded rows get
   // +inf, so their weights are exactly zero even where no mask is applied.
-  float rm[NT], rl[NT], lse2[NT];
+  // pass 1 per row: reference mu (log2 units, 0 until the first visible key), sum rl of exp2 relative
+  // to it, and the raw (unscaled) logit above which mu is raised
+  float rm[NT], rl[NT], rthr[NT], lse2[NT];
   if constexpr (PASS == 2) {
     if (tid < 16 * NT) {
       const int n = rb * 16 * NT + tid;
@@ -193,7 +196,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
     }
   } else {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) { rm[nt] = -INFINITY; rl[nt] = 0.f; }
+    for (int nt = 0; nt < NT; ++nt) { rm[nt] = 0.f; rl[nt] = 0.f; rthr[nt] = -INFINITY; }
   }
   __syncthreads();
   if constexpr (PASS == 2) {
@@ -234,18 +237,31 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
         }
     }
     if constexpr (PASS == 1) {
-      // per-lane running (max, sum) with a lazily raised reference: weights stay <= 2^kSlack
+      // per-lane running sum with a lazily raised reference: weights stay <= 2^kSlack.  The check
+      // compares raw logits with a per-row threshold, and the raise is a wave-uniform branch (the
+      // common tile pays two max and one compare per row tile, no exponential)
+      float mx[NT];
+      bool raise = false;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        const float mx = fmaxf(fmaxf(acc[nt][0], acc[nt][1]), fmaxf(acc[nt][2], acc[nt][3])) * p.scale_log2;
-        if (mx > rm[nt] + kSlack) {
-          rl[nt] *= exp2f(rm[nt] - mx);
-          rm[nt] = mx;
-        }
-        const float mu = rm[nt] == -INFINITY ? 0.f : rm[nt];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) rl[nt] += __builtin_amdgcn_exp2f(fmaf(acc[nt][i], p.scale_log2, -mu));
+        mx[nt] = fmaxf(fmaxf(acc[nt][0], acc[nt][1]), fmaxf(acc[nt][2], acc[nt][3]));
+        raise |= mx[nt] > rthr[nt];
       }
+      if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          if (mx[nt] > rthr[nt]) {
+            const float m2 = mx[nt] * p.scale_log2;    // scale > 0: the max commutes with it
+            rl[nt] = rl[nt] > 0.f ? rl[nt] * exp2f(rm[nt] - m2) : 0.f;
+            rm[nt] = m2;
+            rthr[nt] = (m2 + kSlack) / p.scale_log2;
+          }
+        }
+      }
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rl[nt] += __builtin_amdgcn_exp2f(fmaf(acc[nt][i], p.scale_log2, -rm[nt]));
     } else {
       float col[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -286,7 +302,8 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
     for (int j = 0;; ++j) {
       const int it = wave + kWaves * j, slot = j % kRing;
       // the tile about to be read was issued (kRing-1) tiles before the newest
-      asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
+      static_assert(kRing == 2, "the wait below assumes one tile (8 loads) issued after the one read");
+      asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
       read_ktile(kt, ring_lds + slot * kTileBytes, lane);
       issue(it + kRing * kWaves, slot);
       const int tb = k0 + kTile * it + 4 * lg;
@@ -299,9 +316,10 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
   }
 
   if constexpr (PASS == 1) {
-    // merge the 4 lane groups, then the 4 waves, and publish per-row (max, sum) of this split
+    // merge the 4 lane groups, then the waves, and publish per-row (max, sum) of this split
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
+      if (!(rl[nt] > 0.f)) rm[nt] = -INFINITY;   // no visible key: the empty (max, sum)
 #pragma unroll
       for (int m = 16; m <= 32; m <<= 1) {
         const float m2 = shfl_xor_f(rm[nt], m), l2 = shfl_xor_f(rl[nt], m);
@@ -370,12 +388,17 @@ __device__ inline void hist_add(uint32_t* hist, uint32_t d) {
 template <int V>
 struct IntTag { static constexpr int value = V; };
 
+// Code size matters here: every wave runs each phase once, so a fully unrolled kernel is bound
+// by instruction fetch (75 KB of straight-line code measured 39 us).  Only the pooling keeps its
+// candidates in registers; it stores them in LDS, striped (candidate e of thread t at
+// e*kTopkThreads + t, conflict-free), and every later phase is a short loop over them.
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
   constexpr int kTopkWaves = kTopkThreads / kWave;
-  __shared__ float raw_lds[BD_SELECT_MAX_PREFIX];     // the pooled range, staged once
-  __shared__ uint32_t hist[256];
+  __shared__ float raw_lds[BD_SELECT_MAX_PREFIX];     // the pooled range, staged once; then the keys
+  __shared__ uint32_t hist[kRadixBins0];
   __shared__ int wsum[kTopkWaves];
   __shared__ uint32_t s_digit, s_krem;
+  uint32_t* keys = reinterpret_cast<uint32_t*>(raw_lds);
   const int tid = threadIdx.x;
   const int pair = blockIdx.x;
   const int g = pair % p.Hkv, s = pair / p.Hkv;
@@ -395,22 +418,23 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
   const int N = L - W, K = B - W, rad = p.pool_kernel / 2;
   float* raw = p.raw ? p.raw + (int64_t)pair * p.max_L : nullptr;
   const float* part = p.raw_part + (int64_t)pair * p.n_rb * p.max_L;
-  for (int c0 = 0; c0 < L; c0 += kMaxPerThread * kTopkThreads) {
-    float v[kMaxPerThread];
+  constexpr int kStageBatch = 16;
+  for (int c0 = 0; c0 < L; c0 += kStageBatch * kTopkThreads) {
+    float v[kStageBatch];
 #pragma unroll
-    for (int e = 0; e < kMaxPerThread; ++e) {
+    for (int e = 0; e < kStageBatch; ++e) {
       const int t = c0 + tid + e * kTopkThreads;
       v[e] = t < L ? part[t] : 0.f;
     }
     for (int r = 1; r < p.n_rb; ++r) {
 #pragma unroll
-      for (int e = 0; e < kMaxPerThread; ++e) {
+      for (int e = 0; e < kStageBatch; ++e) {
         const int t = c0 + tid + e * kTopkThreads;
         if (t < L) v[e] += part[(int64_t)r * p.max_L + t];
       }
     }
 #pragma unroll
-    for (int e = 0; e < kMaxPerThread; ++e) {
+    for (int e = 0; e < kStageBatch; ++e) {
       const int t = c0 + tid + e * kTopkThreads;
       if (t < N) raw_lds[t] = v[e];
       if (raw && t < L) raw[t] = v[e];
@@ -431,20 +455,6 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
   const int t0 = tid * E;
   uint32_t key[kMaxPerThread];
   auto raw_at = [&](int t) { return t >= 0 && t < N ? raw_lds[t] : -1.f; };
-  // small radii: the thread's window of raw values in registers, every load issued before any max
-  auto pool_window = [&](auto rad_tag) {
-    constexpr int R = decltype(rad_tag)::value;
-    float w[kMaxPerThread + 2 * R];
-#pragma unroll
-    for (int i = 0; i < kMaxPerThread + 2 * R; ++i) w[i] = i < E + 2 * R ? raw_at(t0 - R + i) : -1.f;
-#pragma unroll
-    for (int e = 0; e < kMaxPerThread; ++e) {
-      float m = w[e + R];
-#pragma unroll
-      for (int d = 1; d <= R; ++d) m = fmaxf(m, fmaxf(w[e + R - d], w[e + R + d]));
-      key[e] = e < E && t0 + e < N ? __float_as_uint(m) : 0u;   // m >= 0: bits order like values
-    }
-  };
   if (chunk > 0) {
 #pragma unroll
     for (int e = 0; e < kMaxPerThread; ++e) {
@@ -456,14 +466,19 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
       }
       key[e] = e < E && c < M ? __float_as_uint(sum) : 0u;
     }
-  } else if (rad == 3) {
-    pool_window(IntTag<3>{});
-  } else if (rad == 2) {
-    pool_window(IntTag<2>{});
-  } else if (rad == 1) {
-    pool_window(IntTag<1>{});
-  } else if (rad == 0) {
-    pool_window(IntTag<0>{});
+  } else if (rad <= 3) {
+    // radius <= 3: the thread's window of raw values in registers (every load issued before any
+    // max), one code path for every such radius (maxima past the radius are masked)
+    float w[kMaxPerThread + 6];
+#pragma unroll
+    for (int i = 0; i < kMaxPerThread + 6; ++i) w[i] = i < E + 6 ? raw_at(t0 - 3 + i) : -1.f;
+#pragma unroll
+    for (int e = 0; e < kMaxPerThread; ++e) {
+      float m = w[e + 3];
+#pragma unroll
+      for (int d = 1; d <= 3; ++d) m = fmaxf(m, d <= rad ? fmaxf(w[e + 3 - d], w[e + 3 + d]) : -1.f);
+      key[e] = e < E && t0 + e < N ? __float_as_uint(m) : 0u;   // m >= 0: bits order like values
+    }
   } else {
     float m[kMaxPerThread];
 #pragma unroll
@@ -476,37 +491,44 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
 #pragma unroll
     for (int e = 0; e < kMaxPerThread; ++e) key[e] = e < E && t0 + e < N ? __float_as_uint(m[e]) : 0u;
   }
+  __syncthreads();                            // every raw value read: the LDS now holds the keys
+#pragma unroll
+  for (int e = 0; e < kMaxPerThread; ++e)
+    if (e < E) keys[e * kTopkThreads + tid] = key[e];
+  __syncthreads();
+  auto key_at = [&](int e) { return keys[e * kTopkThreads + tid]; };
 
-  // 3. radix select of the KE-th largest key; krem = how many keys equal to it are taken
+  // 3. radix select of the KE-th largest key over digits of 12, 10 and 10 bits; krem = how many keys
+  // equal to it are taken.  A 12-bit first digit (sign, exponent, 3 mantissa bits) spreads each
+  // binade over 8 bins: with 8 bits the scores' few exponents piled thousands of LDS atomics onto a
+  // handful of bins.
   uint32_t prefix = 0, pmask = 0, krem = (uint32_t)KE;
   if (KE > 0) {
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      if (tid < 256) hist[tid] = 0;
+    for (int pass = 0; pass < 3; ++pass) {
+      const int bits = pass == 0 ? 12 : 10, shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
+      const uint32_t nb = 1u << bits, dm = nb - 1;
+      for (int i = tid; i < (int)nb; i += kTopkThreads) hist[i] = 0;
       __syncthreads();
-#pragma unroll
-      for (int e = 0; e < kMaxPerThread; ++e)
-        if (e < E && t0 + e < M && (key[e] & pmask) == prefix) hist_add(hist, (key[e] >> shift) & 255u);
+#pragma unroll 4
+      for (int e = 0; e < E; ++e) {
+        const uint32_t k = key_at(e);
+        if (t0 + e < M && (k & pmask) == prefix) hist_add(hist, (k >> shift) & dm);
+      }
       __syncthreads();
-      if (tid < kWave) {
-        uint32_t h[4], c = 0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) { h[q] = hist[255 - (4 * tid + q)]; c += h[q]; }
-        uint32_t incl = c;
-#pragma unroll
-        for (int o = 1; o < kWave; o <<= 1) {
-          const uint32_t y = __shfl_up(incl, o);
-          if (tid >= o) incl += y;
-        }
-        uint32_t a = incl - c;               // keys whose digit is above this lane's four digits
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if (a < krem && krem <= a + h[q]) { s_digit = 255u - (uint32_t)(4 * tid + q); s_krem = krem - a; }
-          a += h[q];
-        }
+      // thread tid owns digits nb-1 - (per*tid + q): a block scan counts the keys above them
+      const int per = (int)nb / kTopkThreads;
+      uint32_t c = 0;
+      for (int q = 0; q < per; ++q) c += hist[nb - 1 - (per * tid + q)];
+      int tot;
+      uint32_t a = (uint32_t)block_exclusive_scan((int)c, wsum, tot);
+      for (int q = 0; q < per; ++q) {
+        const uint32_t h = hist[nb - 1 - (per * tid + q)];
+        if (a < krem && krem <= a + h) { s_digit = nb - 1 - (uint32_t)(per * tid + q); s_krem = krem - a; }
+        a += h;
       }
       __syncthreads();
       prefix |= s_digit << shift;
-      pmask |= 255u << shift;
+      pmask |= dm << shift;
       krem = s_krem;
       __syncthreads();
     }
@@ -519,38 +541,35 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
     const int b = c * chunk;
     return N - b < chunk ? N - b : chunk;
   };
+  const int Ev = KE > 0 ? (M - t0 < E ? (M - t0 > 0 ? M - t0 : 0) : E) : 0;   // this thread's candidates
   int eq = 0;
-#pragma unroll
-  for (int e = 0; e < kMaxPerThread; ++e)
-    if (KE > 0 && e < E && t0 + e < M) eq += key[e] == prefix;
+#pragma unroll 4
+  for (int e = 0; e < Ev; ++e) eq += key_at(e) == prefix;
   int tot;
   const int eq_before = block_exclusive_scan(eq, wsum, tot);
   int take_eq = (int)krem - eq_before;
   take_eq = take_eq < 0 ? 0 : (take_eq > eq ? eq : take_eq);
   int mine = 0, seen = 0;
-#pragma unroll
-  for (int e = 0; e < kMaxPerThread; ++e)
-    if (KE > 0 && e < E && t0 + e < M) {
-      const bool isq = key[e] == prefix;
-      if (key[e] > prefix || (isq && seen < take_eq)) mine += positions(t0 + e);
-      seen += isq;
-    }
+#pragma unroll 4
+  for (int e = 0; e < Ev; ++e) {
+    const uint32_t k = key_at(e);
+    const bool isq = k == prefix;
+    if (k > prefix || (isq && seen < take_eq)) mine += positions(t0 + e);
+    seen += isq;
+  }
   int kept;                                   // prefix positions kept: K (token level), <= K (chunks)
-  const int off0 = block_exclusive_scan(mine, wsum, kept);
-  int off = off0;
+  int off = block_exclusive_scan(mine, wsum, kept);
   seen = 0;
-#pragma unroll
-  for (int e = 0; e < kMaxPerThread; ++e) {
+  for (int e = 0; e < Ev; ++e) {
     const int c = t0 + e;
-    if (KE > 0 && e < E && c < M) {
-      const bool isq = key[e] == prefix;
-      if (key[e] > prefix || (isq && seen < take_eq)) {
-        const int n = positions(c), b = chunk > 0 ? c * chunk : c;
-        for (int j = 0; j < n; ++j, ++off)
-          if (off < K) idx_row[off] = b + j;   // guard: never write past the B - W prefix slots
-      }
-      seen += isq;
+    const uint32_t k = key_at(e);
+    const bool isq = k == prefix;
+    if (k > prefix || (isq && seen < take_eq)) {
+      const int n = positions(c), b = chunk > 0 ? c * chunk : c;
+      for (int j = 0; j < n; ++j, ++off)
+        if (off < K) idx_row[off] = b + j;    // guard: never write past the B - W prefix slots
     }
+    seen += isq;
   }
   if (kept > K) kept = K;
   for (int i = tid; i < W; i += kTopkThreads) idx_row[kept + i] = N + i;
