@@ -215,6 +215,45 @@ __device__ inline void dma_tile(const KvView& kv, const TileRows& A, uint32_t ma
     }
 }
 
+// V^T operands of all 8 d-tiles straight from a row-major V tile in LDS with the transposing
+// read ds_read_b64_tr_b16.  Within each 16-lane group that read hands lane i, element j, element
+// i%4 of the 8 bytes that lane 4j + i/4 addressed.  The caller passes a[j] = the lane's address
+// for d-tiles 2j and 2j+1 (k-slots 0..3); +8 selects the odd d-tile, +4096 the k-slots 4..7 (tile
+// rows 16..31).  Result vt[dt], slot k of lane l: V[key slot 16*(k/4) + 4*(l/16) + k%4]
+// [d = 32*((l%16)/4) + 4*dt + l%4], so accumulator register r of d-tile dt in lane l holds
+// d = 32*(l/16) + 4*dt + r.  One statement, ending in its own wait (direct-to-LDS loads in flight
+// must not make it wait for them).
+__device__ inline void read_vt_tr(bf16x8 (&vt)[8], const uint32_t (&a)[4]) {
+  uint64_t x[16];
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %16\n"
+      "ds_read_b64_tr_b16 %1, %16 offset:4096\n"
+      "ds_read_b64_tr_b16 %2, %16 offset:8\n"
+      "ds_read_b64_tr_b16 %3, %16 offset:4104\n"
+      "ds_read_b64_tr_b16 %4, %17\n"
+      "ds_read_b64_tr_b16 %5, %17 offset:4096\n"
+      "ds_read_b64_tr_b16 %6, %17 offset:8\n"
+      "ds_read_b64_tr_b16 %7, %17 offset:4104\n"
+      "ds_read_b64_tr_b16 %8, %18\n"
+      "ds_read_b64_tr_b16 %9, %18 offset:4096\n"
+      "ds_read_b64_tr_b16 %10, %18 offset:8\n"
+      "ds_read_b64_tr_b16 %11, %18 offset:4104\n"
+      "ds_read_b64_tr_b16 %12, %19\n"
+      "ds_read_b64_tr_b16 %13, %19 offset:4096\n"
+      "ds_read_b64_tr_b16 %14, %19 offset:8\n"
+      "ds_read_b64_tr_b16 %15, %19 offset:4104\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3]), "=&v"(x[4]), "=&v"(x[5]), "=&v"(x[6]), "=&v"(x[7]),
+        "=&v"(x[8]), "=&v"(x[9]), "=&v"(x[10]), "=&v"(x[11]), "=&v"(x[12]), "=&v"(x[13]), "=&v"(x[14]),
+        "=&v"(x[15])
+      : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]));
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) {
+    const uint64_t lo = x[2 * dt], hi = x[2 * dt + 1];
+    vt[dt] = as_bf16x8(u32x4{(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)});
+  }
+}
+
 // V rows already in the tile registers.
 template <int NT, bool PAGED>
 __device__ inline auto pass_v(const TileRegs<NT, PAGED>& T) {
@@ -240,8 +279,10 @@ struct RowState {
 // remainder), so the output carries the weights to about 2^-17 instead of 2^-9: the fp32 output then
 // serves the backward's <dO, O> (which cancels against <dO, v_t>) without amplifying rounding.
 // `get_v` delivers the tile's V rows (8 x 16 bytes per lane) just before the PV product, so a caller
-// may read them from LDS only then.
-template <int NT, bool PAGED, bool TRAIN = false, class PosFn, class VFn>
+// may read them from LDS only then.  VTR: `get_v` delivers the 8 V^T operands themselves
+// (read_vt_tr's layout: register r of d-tile dt in lane l holds d = 32*(l/16) + 4*dt + r);
+// otherwise they are transposed here (register i of d-tile dt holds d = 32*(l/16) + 8*i + dt).
+template <int NT, bool PAGED, bool TRAIN = false, bool VTR = false, class PosFn, class VFn>
 __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T, const bf16x8 (&qop)[NT][4],
                                  const int (&rowpos)[NT], float scale_log2, bool dirty, bool want_lx,
                                  PosFn pos_of, VFn get_v) {
@@ -325,16 +366,23 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
     st.l[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pop[nt], st.l[nt], 0, 0, 0);
   }
 
-  u32x4 vrows[8];
-  get_v(vrows);
-#pragma unroll
-  for (int dt = 0; dt < 8; ++dt) {
-    const bf16x8 vt = vt_operand(vrows, dt);
+  auto pv = [&](int dt, const bf16x8& vt) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       st.o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, pop[nt], st.o[nt][dt], 0, 0, 0);
       if constexpr (TRAIN) st.o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, plo[nt], st.o[nt][dt], 0, 0, 0);
     }
+  };
+  if constexpr (VTR) {
+    bf16x8 vts[8];
+    get_v(vts);
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) pv(dt, vts[dt]);
+  } else {
+    u32x4 vrows[8];
+    get_v(vrows);
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) pv(dt, vt_operand(vrows, dt));
   }
 }
 
@@ -780,29 +828,16 @@ __device__ inline void read_block_tile_k(TileRegs<2, true>& T, uint32_t (&r)[2],
         "=&v"(T.k[1][1]), "=&v"(T.k[1][2]), "=&v"(T.k[1][3]), "=&v"(T.tp[0]), "=&v"(T.tp[1]), "=&v"(r[0]), "=&v"(r[1])
       : "v"(at), "v"(ap), "v"(a0), "v"(a1));
 }
-// Eight 1 KiB pieces (V rows of a tile) into registers, with their wait.
-__device__ inline void read_v8(u32x4 (&x)[8], uint32_t a) {
-  asm volatile(
-      "ds_read_b128 %0, %8\n"
-      "ds_read_b128 %1, %8 offset:1024\n"
-      "ds_read_b128 %2, %8 offset:2048\n"
-      "ds_read_b128 %3, %8 offset:3072\n"
-      "ds_read_b128 %4, %8 offset:4096\n"
-      "ds_read_b128 %5, %8 offset:5120\n"
-      "ds_read_b128 %6, %8 offset:6144\n"
-      "ds_read_b128 %7, %8 offset:7168\n"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3]), "=&v"(x[4]), "=&v"(x[5]), "=&v"(x[6]), "=&v"(x[7])
-      : "v"(a));
-}
-
-// Load q (0..15) of a tile for this lane: K load q < 8 (sub-tile q/4, k-step q%4), V load q >= 8
-// (row group (q-8)/4, row (q-8)%4); `r` is the row's offset in 16-byte units.
+// Load q (0..15) of a tile for this lane; `r` is the row's offset in 16-byte units.  K loads
+// q < 8 (sub-tile q/4, k-step q%4) land in the score operand order.  V loads q >= 8 write tile
+// rows 4*(q-8) + lane/16, row-major (row r at byte 8192 + 256*r of the tile) with the row's 16-byte
+// chunks XOR-swizzled by r%4 (chunk c stored at position c ^ (r%4)), so the transposing reads of
+// read_vt_tr spread over the LDS banks.
 __device__ inline void dma_load(const KvView& kv, uint32_t r, uint32_t max_roff, int q, uint8_t* dst, int lane) {
   const int lg = lane >> 4, lr = lane & 15;
   const uint32_t ro = r < max_roff ? r : max_roff;
   if (q < 8) dma16(kv.k + ((uint64_t)ro << 3) + 32 * lg + 8 * (q & 3), dst + q * 1024);
-  else dma16(kv.v + ((uint64_t)ro << 3) + 8 * lr, dst + q * 1024);
+  else dma16(kv.v + ((uint64_t)ro << 3) + 8 * (lr ^ lg), dst + q * 1024);
 }
 
 template <bool PAGED, bool TRAIN>
@@ -862,8 +897,14 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
 
   // ---- the two loads of every tile that this wave issues, and the tile rows they read
   const int q0 = 2 * wave, q1 = 2 * wave + 1;
-  auto row_in_tile = [&](int q) { return q < 8 ? 16 * (q >> 2) + lr : 16 * ((q - 8) >> 2) + 4 * lg + ((q - 8) & 3); };
+  auto row_in_tile = [&](int q) { return q < 8 ? 16 * (q >> 2) + lr : 4 * (q - 8) + lg; };
   const int rit0 = row_in_tile(q0), rit1 = row_in_tile(q1);
+  // transposing V reads (read_vt_tr): this lane addresses tile row 4*(lane/16) + (lane%16)/4
+  // (k-slots 0..3; +4096 for 4..7), d from 32*(lane%4) + 8*j, at its swizzled chunk position
+  uint32_t vtr_off[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    vtr_off[j] = 8192u + 256u * (uint32_t)(4 * lg + (lr >> 2)) + 16u * (uint32_t)((4 * (lr & 3) + j) ^ (lr >> 2));
   const uint32_t roff_lds = lds_addr(sm.roff), tpos_lds = lds_addr(sm.tpos);
   const uint32_t ring_lds = lds_addr(sm.ring[0]);
   auto issue = [&](int tile, const uint32_t (&r)[2]) {
@@ -872,7 +913,7 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
     dma_load(p.kv, r[1], p.max_roff, q1, dst, lane);
   };
 
-  // ---- branch b's outputs of rows 16*nt + lane%16; register i of d-tile dt holds d = 32*(lane/16) + 8*i + dt
+  // ---- branch b's outputs of rows 16*nt + lane%16; register r of d-tile dt holds d = 32*(lane/16) + 4*dt + r
   const int64_t view_rows = (int64_t)p.S * p.nq * p.Hq;
   auto write_rows = [&](int b, const float (&M)[NT], const float (&Lw)[NT], const float (&Lx)[NT],
                         const f32x4 (&o)[NT][8]) {
@@ -888,15 +929,15 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
       const int64_t orow = ((int64_t)s * p.nq + j) * p.Hq + h;
       const float inv = Lw[nt] > 0.f ? 1.f / Lw[nt] : 0.f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        u32x4 wv;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) wv[e] = pack_bf16x2(o[nt][2 * e][i] * inv, o[nt][2 * e + 1][i] * inv);
-        *reinterpret_cast<u32x4*>(out + orow * kD + 32 * lg + 8 * i) = wv;
+      for (int k = 0; k < 4; ++k) {      // d = 32*lg + 8*k + 0..7: d-tiles 2k and 2k+1
+        const f32x4 a = o[nt][2 * k] * inv, b = o[nt][2 * k + 1] * inv;
+        const u32x4 wv = {pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]),
+                          pack_bf16x2(b[2], b[3])};
+        *reinterpret_cast<u32x4*>(out + orow * kD + 32 * lg + 8 * k) = wv;
         if (TRAIN && out32) {
-          float* o32 = out32 + orow * kD + 32 * lg + 8 * i;
-          *reinterpret_cast<f32x4*>(o32) = f32x4{o[nt][0][i], o[nt][1][i], o[nt][2][i], o[nt][3][i]} * inv;
-          *reinterpret_cast<f32x4*>(o32 + 4) = f32x4{o[nt][4][i], o[nt][5][i], o[nt][6][i], o[nt][7][i]} * inv;
+          float* o32 = out32 + orow * kD + 32 * lg + 8 * k;
+          *reinterpret_cast<f32x4*>(o32) = a;
+          *reinterpret_cast<f32x4*>(o32 + 4) = b;
         }
       }
       if (lse && lg == 0) lse[orow] = Lx[nt] > 0.f ? (M[nt] + __log2f(Lx[nt])) * kLn2 : -INFINITY;
@@ -966,28 +1007,49 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
           : "v"(roff_lds + 4 * (kTile * t + rit0)), "v"(roff_lds + 4 * (kTile * t + rit1)));
       issue(t, r);
     }
-    TileRegs<NT, true> T;
-    // tile t+kBRing-1 is issued in step t, after the barrier that frees its slot (read in step t-1)
-    for (int t = 0; t < ntiles; ++t) {
-      // this wave's loads of tile t are older than the kBRing-2 tiles issued after it
-      asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
-      static_assert(2 * (kBRing - 2) == 8, "wait count follows the ring depth");
-      const int nxt = t + kBRing - 1;
-      const uint32_t src = ring_lds + (uint32_t)(t % kBRing) * kTileBytes;
-      uint32_t r[2];
-      read_block_tile_k(T, r, src, tpos_lds, kTile * t, roff_lds, kTile * nxt, rit0, rit1, lane);
-      bool bad = false;
+    // tile t+kBRing-1 is issued in step t, after the barrier that frees its slot (read in step t-1).
+    // A wave without query rows (the row count is not a multiple of the block) only keeps the
+    // ring going: its own loop, so that the accumulators of the computing loop have one definition
+    // per step (a conditional step made the compiler copy every accumulator after its MFMA).
+    static_assert(2 * (kBRing - 2) == 8, "wait count follows the ring depth");
+    if (has_rows) {
+      TileRegs<NT, true> T;
+      for (int t = 0; t < ntiles; ++t) {
+        // this wave's loads of tile t are older than the kBRing-2 tiles issued after it
+        asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+        const int nxt = t + kBRing - 1;
+        const uint32_t src = ring_lds + (uint32_t)(t % kBRing) * kTileBytes;
+        uint32_t r[2];
+        read_block_tile_k(T, r, src, tpos_lds, kTile * t, roff_lds, kTile * nxt, rit0, rit1, lane);
+        bool bad = false;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int tp = (int)T.tp[i >> 2][i & 3];
-        bad |= tp < 0 || tp > minpos;
+        for (int i = 0; i < 8; ++i) {
+          const int tp = (int)T.tp[i >> 2][i & 3];
+          bad |= tp < 0 || tp > minpos;
+        }
+        const bool dirty = __builtin_amdgcn_ballot_w64(bad) != 0;
+        issue(nxt, r);
+        tile_step<NT, true, TRAIN, true>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx,
+                                         [&](int i) { return (int)T.tp[i >> 2][i & 3]; },
+                                         [&](bf16x8 (&vt)[8]) {
+                                           const uint32_t a[4] = {src + vtr_off[0], src + vtr_off[1],
+                                                                  src + vtr_off[2], src + vtr_off[3]};
+                                           read_vt_tr(vt, a);
+                                         });
       }
-      const bool dirty = __builtin_amdgcn_ballot_w64(bad) != 0;
-      issue(nxt, r);
-      if (has_rows)
-        tile_step<NT, true, TRAIN>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx,
-                                   [&](int i) { return (int)T.tp[i >> 2][i & 3]; },
-                                   [&](u32x4 (&v)[8]) { read_v8(v, src + 8 * 1024 + 16 * lane); });
+    } else {
+      for (int t = 0; t < ntiles; ++t) {
+        asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+        const int nxt = t + kBRing - 1;
+        uint32_t r[2];
+        asm volatile(
+            "ds_read_b32 %0, %2\n"
+            "ds_read_b32 %1, %3\n"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(r[0]), "=&v"(r[1])
+            : "v"(roff_lds + 4 * (kTile * nxt + rit0)), "v"(roff_lds + 4 * (kTile * nxt + rit1)));
+        issue(nxt, r);
+      }
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the ring is reused
 
