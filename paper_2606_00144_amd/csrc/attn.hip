@@ -792,13 +792,23 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
 constexpr int kBWaves = 8;
 constexpr int kBThreads = kBWaves * kWave;
 constexpr int kBRing = 6;                          // tile slots; kBRing-1 tiles stay in flight
-constexpr int kBSlotCap = kMaxSplitKeys + kBRing * kTile;
+constexpr int kBMaxPieces = 64;                    // branches per unit (host-checked)
+// a workgroup's range holds at most kMaxSplitKeys entries, each piece pads its last tile, and the
+// prefetches run kBRing tiles past the end
+constexpr int kBSlotCap = kMaxSplitKeys + (kBMaxPieces + kBRing) * kTile;
+
+// One piece of a workgroup's range: entries [e0, e1) of branch b, from slot-table tile t0; the
+// branch spans nwg workgroups, its records start at slot `slot`, this piece's is number wo.
+struct BlockPiece {
+  int32_t b, e0, e1, t0, nwg, slot, wo;
+};
 
 struct BlockSmem {
   alignas(16) int32_t roff[kBSlotCap];
   alignas(16) int32_t tpos[kBSlotCap];
   alignas(16) uint8_t ring[kBRing][kTileBytes];
-  int32_t last;
+  BlockPiece pc[kBMaxPieces];
+  int32_t blen[kBMaxPieces];                       // branch lengths
 };
 
 // K pieces of the tile in slot `src`, its positions and the two row offsets this wave loads for the
@@ -840,6 +850,57 @@ __device__ inline void dma_load(const KvView& kv, uint32_t r, uint32_t max_roff,
   else dma16(kv.v + ((uint64_t)ro << 3) + 8 * (lr ^ lg), dst + q * 1024);
 }
 
+// Branch b's outputs of row block rb (rows 16*nt + lane%16 of it) from an unnormalised state:
+// register r of d-tile dt holds d = 32*(lane/16) + 4*dt + r.  Rows past R are not written.
+template <bool TRAIN>
+__device__ inline void block_write_rows(const AttnParams& p, int s, int g, int rb, int b, const float (&M)[2],
+                                        const float (&Lw)[2], const float (&Lx)[2], const f32x4 (&o)[2][8],
+                                        int lane) {
+  constexpr int NT = 2;
+  const int lg = lane >> 4, lr = lane & 15;
+  const int64_t view_rows = (int64_t)p.S * p.nq * p.Hq;
+  const bool gb = b < p.V;
+  uint16_t* out = gb ? p.out_g + (int64_t)b * view_rows * kD : p.out_f;
+  float* lse = gb ? (p.lse_g ? p.lse_g + (int64_t)b * view_rows : nullptr) : p.lse_f;
+  float* out32 = gb ? (p.o32_g ? p.o32_g + (int64_t)b * view_rows * kD : nullptr) : p.o32_f;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int n = rb * RowBlock<NT>::kRows + 16 * nt + lr;
+    if (n >= p.R) continue;
+    const int j = n / p.G, h = g * p.G + n % p.G;
+    const int64_t orow = ((int64_t)s * p.nq + j) * p.Hq + h;
+    const float inv = Lw[nt] > 0.f ? 1.f / Lw[nt] : 0.f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {      // d = 32*lg + 8*k + 0..7: d-tiles 2k and 2k+1
+      const f32x4 a = o[nt][2 * k] * inv, c = o[nt][2 * k + 1] * inv;
+      const u32x4 wv = {pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(c[0], c[1]),
+                        pack_bf16x2(c[2], c[3])};
+      *reinterpret_cast<u32x4*>(out + orow * kD + 32 * lg + 8 * k) = wv;
+      if (TRAIN && out32) {
+        float* o32 = out32 + orow * kD + 32 * lg + 8 * k;
+        *reinterpret_cast<f32x4*>(o32) = a;
+        *reinterpret_cast<f32x4*>(o32 + 4) = c;
+      }
+    }
+    if (lse && lg == 0) lse[orow] = Lx[nt] > 0.f ? (M[nt] + __log2f(Lx[nt])) * kLn2 : -INFINITY;
+  }
+}
+
+// Length of branch b of sequence s in the unit's key stream (the views' entry lists, then the full
+// branch's L cache rows), and the equal share of the stream each of the unit's nW workgroups takes,
+// rounded up to whole tiles; both kernels of block mode cut the stream this way.
+__device__ inline int block_branch_len(const AttnParams& p, int s, int L, int b) {
+  if (b < p.V) {
+    const int n = p.nsel[b * p.S + s];
+    return n < 0 ? 0 : (n > p.ld_idx ? p.ld_idx : n);
+  }
+  return L;
+}
+__device__ inline int block_chunk(int total, int nW) {
+  const int c = (total + nW - 1) / nW;
+  return (c + kTile - 1) / kTile * kTile;
+}
+
 template <bool PAGED, bool TRAIN>
 __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
   constexpr int NT = 2;
@@ -862,20 +923,15 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
 
   // The key stream of a unit is the views' entry lists followed by the full branch's cache rows;
   // its length is known only here (nsel lives on the device), so the unit's nW workgroups cut it
-  // into equal ranges at run time.  A range runs one piece per branch it meets.  A branch met by
-  // one workgroup is finished there; otherwise each piece leaves a record and the last of the
-  // branch's workgroups merges them in stream order.
-  auto branch_len = [&](int b) -> int {
-    if (b < p.V) {
-      const int n = p.nsel[b * p.S + s];
-      return n < 0 ? 0 : (n > p.ld_idx ? p.ld_idx : n);
-    }
-    return L;
-  };
+  // into equal ranges at run time.  A range holds one piece per branch it meets, and all its pieces
+  // stream through one slot table and one ring.  A branch met by one workgroup is finished there;
+  // otherwise each piece leaves a record and the last of the branch's workgroups merges them in
+  // stream order.
+  if (tid < p.nbr) sm.blen[tid] = block_branch_len(p, s, L, tid);   // nbr <= kBMaxPieces <= kBThreads
+  __syncthreads();
   int total = 0;
-  for (int b = 0; b < p.nbr; ++b) total += branch_len(b);
-  int chunk = (total + p.nW - 1) / p.nW;
-  chunk = (chunk + kTile - 1) / kTile * kTile;
+  for (int b = 0; b < p.nbr; ++b) total += sm.blen[b];
+  const int chunk = block_chunk(total, p.nW);
   const int r0 = w * chunk;
   const int r1 = r0 + chunk < total ? r0 + chunk : total;
 
@@ -913,232 +969,315 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
     dma_load(p.kv, r[1], p.max_roff, q1, dst, lane);
   };
 
-  // ---- branch b's outputs of rows 16*nt + lane%16; register r of d-tile dt holds d = 32*(lane/16) + 4*dt + r
-  const int64_t view_rows = (int64_t)p.S * p.nq * p.Hq;
-  auto write_rows = [&](int b, const float (&M)[NT], const float (&Lw)[NT], const float (&Lx)[NT],
-                        const f32x4 (&o)[NT][8]) {
-    const bool gb = b < p.V;
-    uint16_t* out = gb ? p.out_g + (int64_t)b * view_rows * kD : p.out_f;
-    float* lse = gb ? (p.lse_g ? p.lse_g + (int64_t)b * view_rows : nullptr) : p.lse_f;
-    float* out32 = gb ? (p.o32_g ? p.o32_g + (int64_t)b * view_rows * kD : nullptr) : p.o32_f;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int n = rb * RB::kRows + 16 * nt + lr;
-      if (n >= p.R) continue;
-      const int j = n / p.G, h = g * p.G + n % p.G;
-      const int64_t orow = ((int64_t)s * p.nq + j) * p.Hq + h;
-      const float inv = Lw[nt] > 0.f ? 1.f / Lw[nt] : 0.f;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {      // d = 32*lg + 8*k + 0..7: d-tiles 2k and 2k+1
-        const f32x4 a = o[nt][2 * k] * inv, b = o[nt][2 * k + 1] * inv;
-        const u32x4 wv = {pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]),
-                          pack_bf16x2(b[2], b[3])};
-        *reinterpret_cast<u32x4*>(out + orow * kD + 32 * lg + 8 * k) = wv;
-        if (TRAIN && out32) {
-          float* o32 = out32 + orow * kD + 32 * lg + 8 * k;
-          *reinterpret_cast<f32x4*>(o32) = a;
-          *reinterpret_cast<f32x4*>(o32 + 4) = b;
-        }
-      }
-      if (lse && lg == 0) lse[orow] = Lx[nt] > 0.f ? (M[nt] + __log2f(Lx[nt])) * kLn2 : -INFINITY;
-    }
-  };
+  auto write_rows = [&](int b, const float (&M)[2], const float (&Lw)[2], const float (&Lx)[2],
+                        const f32x4 (&o)[2][8]) { block_write_rows<TRAIN>(p, s, g, rb, b, M, Lw, Lx, o, lane); };
 
   // ---- records of the unit: piece (b, w) at slot base(b) + w - wlo(b), one record per row block
   const int rec_per_unit = p.nW + p.nbr - 1;
   const float* unit_rec = p.part + (int64_t)unit * rec_per_unit * kBWaves * RB::kRec;
   constexpr uint32_t kOutOff = 16 * RB::kRows;
 
-  int off = 0, rbase = 0;
-  uint64_t to_merge = 0;                          // branches this workgroup merges (nbr <= 64)
-  for (int b = 0; b < p.nbr; ++b) {
-    const int n = branch_len(b);
-    const int off_b = off;
-    off += n;
-    if (n == 0) {
-      // no entries: its rows see nothing; the workgroup whose range holds the branch's place writes it
-      int owner = chunk > 0 ? off_b / chunk : 0;
-      if (owner > p.nW - 1) owner = p.nW - 1;
-      if (owner == w && has_rows) {
-        const float m0[NT] = {-INFINITY, -INFINITY}, z[NT] = {0.f, 0.f};
-        f32x4 oz[NT][8];
+  // ---- this workgroup's pieces, in stream order: entries [e0, e1) of every branch its range meets.
+  // A piece takes whole tiles of the slot table (the last one padded), so that a tile never mixes
+  // branches.  Empty branches are written by the workgroup whose range holds their place.
+  int npc = 0, ntl = 0;
+  {
+    int off = 0, rbase = 0;
+    for (int b = 0; b < p.nbr; ++b) {
+      const int n = sm.blen[b];
+      const int off_b = off;
+      off += n;
+      if (n == 0) {
+        int owner = chunk > 0 ? off_b / chunk : 0;
+        if (owner > p.nW - 1) owner = p.nW - 1;
+        if (owner == w && has_rows) {
+          const float m0[NT] = {-INFINITY, -INFINITY}, z[NT] = {0.f, 0.f};
+          f32x4 oz[NT][8];
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
+          for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-          for (int dt = 0; dt < 8; ++dt) oz[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        write_rows(b, m0, z, z, oz);
+            for (int dt = 0; dt < 8; ++dt) oz[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+          write_rows(b, m0, z, z, oz);
+        }
+        continue;
       }
-      continue;
+      const int wlo = off_b / chunk, whi = (off_b + n - 1) / chunk;
+      const int slot_b = rbase;
+      rbase += whi - wlo + 1;
+      const int lo = r0 > off_b ? r0 : off_b, hi = r1 < off_b + n ? r1 : off_b + n;
+      if (lo >= hi) continue;
+      if (tid == 0) {
+        sm.pc[npc] = BlockPiece{b, lo - off_b, hi - off_b, ntl, whi - wlo + 1, slot_b, w - wlo};
+      }
+      ntl += (hi - lo + kTile - 1) / kTile;
+      ++npc;
     }
-    const int wlo = off_b / chunk, whi = (off_b + n - 1) / chunk;
-    const int nwg = whi - wlo + 1;
-    const int slot_b = rbase;
-    rbase += nwg;
-    const int lo = r0 > off_b ? r0 : off_b, hi = r1 < off_b + n ? r1 : off_b + n;
-    if (lo >= hi) continue;
-    const int e_begin = lo - off_b, e_end = hi - off_b;
-    const bool gather = b < p.V;
-    const int32_t* idx_row = gather ? p.idx + (((int64_t)b * p.S + s) * p.Hkv + g) * p.ld_idx : nullptr;
-    const bool want_lx = (gather ? p.lse_g : p.lse_f) != nullptr;
-    const int ntiles = (e_end - e_begin + kTile - 1) / kTile;
+  }
+  __syncthreads();
 
-    __syncthreads();                              // the previous piece's slot table and ring are free
-    fill_slot_table<PAGED, kBThreads, kBSlotCap>(p.kv, s, g, L, idx_row, e_begin, e_end, (ntiles + kBRing) * kTile,
-                                                 sm.roff, sm.tpos, tid);
-    __syncthreads();
+  // ---- one slot table for every piece: all idx (and page-table) loads issued before any is used
+  {
+    constexpr int kPer = (kBSlotCap + kBThreads - 1) / kBThreads;
+    const int nslots = (ntl + kBRing) * kTile;     // padding tiles past the last for the prefetches
+    int tv[kPer];
+    int k = 0;                                     // piece of this thread's slot (slots increase with j)
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int i = tid + j * kBThreads;
+      const int tile = i / kTile;
+      while (k + 1 < npc && sm.pc[k + 1].t0 <= tile) ++k;
+      int t = -1;
+      if (tile < ntl) {
+        const BlockPiece pc = sm.pc[k];
+        const int e = pc.e0 + (i - kTile * pc.t0);
+        if (e < pc.e1) {
+          t = pc.b < p.V ? p.idx[(((int64_t)pc.b * p.S + s) * p.Hkv + g) * p.ld_idx + e] : e;
+        }
+      }
+      tv[j] = t;
+    }
+    int pg[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      tv[j] = (tv[j] >= 0 && tv[j] < L) ? tv[j] : -1;
+      if constexpr (PAGED)
+        pg[j] = tv[j] >= 0 ? p.kv.page_table[(int64_t)s * p.kv.max_pages_per_seq + tv[j] / p.kv.page_size] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int i = tid + j * kBThreads;
+      if (i < nslots && i < kBSlotCap) {
+        int t = tv[j];
+        int64_t o;
+        if constexpr (PAGED) {
+          o = (unsigned)pg[j] < (unsigned)p.kv.num_pages
+                  ? (int64_t)pg[j] * p.kv.stride_page + (int64_t)g * p.kv.stride_head +
+                        (int64_t)(t % p.kv.page_size) * p.kv.stride_tok
+                  : -1;
+        } else {
+          o = (int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head + (int64_t)t * p.kv.stride_tok;
+        }
+        if (t < 0 || o < 0) { t = -1; o = 0; }
+        sm.roff[i] = (int)(o >> 3);
+        sm.tpos[i] = t;
+      }
+    }
+  }
+  __syncthreads();
 
+  // ---- stream every tile of every piece through the ring: tiles 0 .. kBRing-2 first
+  for (int t = 0; t < kBRing - 1; ++t) {
+    uint32_t r[2];
+    asm volatile(
+        "ds_read_b32 %0, %2\n"
+        "ds_read_b32 %1, %3\n"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r[0]), "=&v"(r[1])
+        : "v"(roff_lds + 4 * (kTile * t + rit0)), "v"(roff_lds + 4 * (kTile * t + rit1)));
+    issue(t, r);
+  }
+  // Tile t+kBRing-1 is issued in step t, after the barrier that frees its slot (read in step t-1).
+  // At the last tile of a piece the wave finishes the piece: its rows' outputs when the piece is the
+  // whole branch, else a record (stored now, counted once every piece is done) and a fresh state.
+  // A wave without query rows (the row count is not a multiple of the block) only keeps the ring
+  // going: its own loop, so that the accumulators of the computing loop have one definition per
+  // step (a conditional step made the compiler copy every accumulator after its MFMA).
+  static_assert(2 * (kBRing - 2) == 8, "wait count follows the ring depth");
+  if (has_rows) {
     RowState<NT> st;
+    auto reset = [&] {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      st.m[nt] = -INFINITY;
-      st.l[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      st.lx[nt] = 0.f;
+      for (int nt = 0; nt < NT; ++nt) {
+        st.m[nt] = -INFINITY;
+        st.l[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        st.lx[nt] = 0.f;
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    };
+    reset();
+    int k = 0;
+    BlockPiece pc = sm.pc[0];
+    int t_end = pc.t0 + (pc.e1 - pc.e0 + kTile - 1) / kTile;
+    bool want_lx = (pc.b < p.V ? p.lse_g : p.lse_f) != nullptr;
+    TileRegs<NT, true> T;
+    for (int t = 0; t < ntl; ++t) {
+      // this wave's loads of tile t are older than the kBRing-2 tiles issued after it
+      asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+      const int nxt = t + kBRing - 1;
+      const uint32_t src = ring_lds + (uint32_t)(t % kBRing) * kTileBytes;
+      uint32_t r[2];
+      read_block_tile_k(T, r, src, tpos_lds, kTile * t, roff_lds, kTile * nxt, rit0, rit1, lane);
+      bool bad = false;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int tp = (int)T.tp[i >> 2][i & 3];
+        bad |= tp < 0 || tp > minpos;
+      }
+      const bool dirty = __builtin_amdgcn_ballot_w64(bad) != 0;
+      issue(nxt, r);
+      tile_step<NT, true, TRAIN, true>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx,
+                                       [&](int i) { return (int)T.tp[i >> 2][i & 3]; },
+                                       [&](bf16x8 (&vt)[8]) {
+                                         const uint32_t a[4] = {src + vtr_off[0], src + vtr_off[1],
+                                                                src + vtr_off[2], src + vtr_off[3]};
+                                         read_vt_tr(vt, a);
+                                       });
+      if (t + 1 == t_end) {
+        // ---- piece k done: per-row (m, l, lx) of rows 16*nt + lane%16
+        float lxw[NT], lw[NT];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          float lx = st.lx[nt];
+          lx += shfl_xor_f(lx, 16);
+          lx += shfl_xor_f(lx, 32);
+          lxw[nt] = lx;
+          lw[nt] = st.l[nt][0];
+        }
+        if (pc.nwg == 1) {
+          write_rows(pc.b, st.m, lw, lxw, st.o);
+        } else {
+          // record pc.wo of the branch's pieces for this row block: row stats as float4
+          // (m, l, lx, -) per row, then the outputs as chunk (nt, dt) x lane float4s
+          const __amdgpu_buffer_rsrc_t urec = make_rsrc(unit_rec + ((int64_t)pc.slot * kBWaves + wave) * RB::kRec,
+                                                        (uint32_t)(pc.nwg * kBWaves * RB::kRec * 4));
+          const uint32_t rec = (uint32_t)pc.wo * kBWaves * RB::kRec * 4;
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            if (lg == 0) store16_coherent(urec, rec + 16 * (16 * nt + lr), f32x4{st.m[nt], lw[nt], lxw[nt], 0.f});
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt)
+              store16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + dt) * kWave + lane), st.o[nt][dt]);
+          }
+        }
+        reset();
+        if (++k < npc) {
+          pc = sm.pc[k];
+          t_end = pc.t0 + (pc.e1 - pc.e0 + kTile - 1) / kTile;
+          want_lx = (pc.b < p.V ? p.lse_g : p.lse_f) != nullptr;
+        }
+      }
     }
-    // prologue: tiles 0 .. kBRing-2
-    for (int t = 0; t < kBRing - 1; ++t) {
+  } else {
+    for (int t = 0; t < ntl; ++t) {
+      asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+      const int nxt = t + kBRing - 1;
       uint32_t r[2];
       asm volatile(
           "ds_read_b32 %0, %2\n"
           "ds_read_b32 %1, %3\n"
           "s_waitcnt lgkmcnt(0)"
           : "=&v"(r[0]), "=&v"(r[1])
-          : "v"(roff_lds + 4 * (kTile * t + rit0)), "v"(roff_lds + 4 * (kTile * t + rit1)));
-      issue(t, r);
-    }
-    // tile t+kBRing-1 is issued in step t, after the barrier that frees its slot (read in step t-1).
-    // A wave without query rows (the row count is not a multiple of the block) only keeps the
-    // ring going: its own loop, so that the accumulators of the computing loop have one definition
-    // per step (a conditional step made the compiler copy every accumulator after its MFMA).
-    static_assert(2 * (kBRing - 2) == 8, "wait count follows the ring depth");
-    if (has_rows) {
-      TileRegs<NT, true> T;
-      for (int t = 0; t < ntiles; ++t) {
-        // this wave's loads of tile t are older than the kBRing-2 tiles issued after it
-        asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
-        const int nxt = t + kBRing - 1;
-        const uint32_t src = ring_lds + (uint32_t)(t % kBRing) * kTileBytes;
-        uint32_t r[2];
-        read_block_tile_k(T, r, src, tpos_lds, kTile * t, roff_lds, kTile * nxt, rit0, rit1, lane);
-        bool bad = false;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int tp = (int)T.tp[i >> 2][i & 3];
-          bad |= tp < 0 || tp > minpos;
-        }
-        const bool dirty = __builtin_amdgcn_ballot_w64(bad) != 0;
-        issue(nxt, r);
-        tile_step<NT, true, TRAIN, true>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx,
-                                         [&](int i) { return (int)T.tp[i >> 2][i & 3]; },
-                                         [&](bf16x8 (&vt)[8]) {
-                                           const uint32_t a[4] = {src + vtr_off[0], src + vtr_off[1],
-                                                                  src + vtr_off[2], src + vtr_off[3]};
-                                           read_vt_tr(vt, a);
-                                         });
-      }
-    } else {
-      for (int t = 0; t < ntiles; ++t) {
-        asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
-        const int nxt = t + kBRing - 1;
-        uint32_t r[2];
-        asm volatile(
-            "ds_read_b32 %0, %2\n"
-            "ds_read_b32 %1, %3\n"
-            "s_waitcnt lgkmcnt(0)"
-            : "=&v"(r[0]), "=&v"(r[1])
-            : "v"(roff_lds + 4 * (kTile * nxt + rit0)), "v"(roff_lds + 4 * (kTile * nxt + rit1)));
-        issue(nxt, r);
-      }
-    }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the ring is reused
-
-    // ---- per-row results of this wave: (m, l, lx) of rows 16*nt + lane%16
-    float lxw[NT], lw[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      float lx = st.lx[nt];
-      lx += shfl_xor_f(lx, 16);
-      lx += shfl_xor_f(lx, 32);
-      lxw[nt] = lx;
-      lw[nt] = st.l[nt][0];
-    }
-    if (nwg == 1) {                               // the whole branch ran here
-      if (has_rows) write_rows(b, st.m, lw, lxw, st.o);
-      continue;
-    }
-
-    // ---- publish the piece as record slot_b + w - wlo of this row block: row stats as float4
-    // (m, l, lx, -) per row, then the outputs as chunk (nt, dt) x lane float4s
-    const __amdgpu_buffer_rsrc_t urec =
-        make_rsrc(unit_rec + ((int64_t)slot_b * kBWaves + wave) * RB::kRec, (uint32_t)(nwg * kBWaves * RB::kRec * 4));
-    if (has_rows) {
-      const uint32_t rec = (uint32_t)(w - wlo) * kBWaves * RB::kRec * 4;
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        if (lg == 0) store16_coherent(urec, rec + 16 * (16 * nt + lr), f32x4{st.m[nt], lw[nt], lxw[nt], 0.f});
-#pragma unroll
-        for (int dt = 0; dt < 8; ++dt)
-          store16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + dt) * kWave + lane), st.o[nt][dt]);
-      }
-    }
-    wait_vmem();
-    __syncthreads();
-    uint32_t* ctr = counter_line(p.counters, (int64_t)unit * p.nbr + b);
-    if (tid == 0) sm.last = arrive(ctr, (uint32_t)nwg);
-    __syncthreads();
-    if (sm.last) {
-      if (tid == 0) reset_counter(ctr);           // ready for the next call
-      to_merge |= 1ull << b;                      // merged after the last piece, when its state is gone
+          : "v"(roff_lds + 4 * (kTile * nxt + rit0)), "v"(roff_lds + 4 * (kTile * nxt + rit1)));
+      issue(nxt, r);
     }
   }
 
-  // ---- branches whose pieces this workgroup completed: merge each row block over the pieces, in
-  // stream order, with an online rescale
-  off = 0;
-  rbase = 0;
-  for (int b = 0; b < p.nbr; ++b) {
-    const int n = branch_len(b);
-    const int off_b = off;
-    off += n;
-    if (n == 0) continue;
-    const int wlo = off_b / chunk, whi = (off_b + n - 1) / chunk;
-    const int nwg = whi - wlo + 1;
-    const int slot_b = rbase;
-    rbase += nwg;
-    if (!((to_merge >> b) & 1ull) || !has_rows) continue;
-    const __amdgpu_buffer_rsrc_t urec =
-        make_rsrc(unit_rec + ((int64_t)slot_b * kBWaves + wave) * RB::kRec, (uint32_t)(nwg * kBWaves * RB::kRec * 4));
-    float Mg[NT], Lg[NT], Lxg[NT];
-    f32x4 og[NT][8];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      Mg[nt] = -INFINITY;
-      Lg[nt] = 0.f;
-      Lxg[nt] = 0.f;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) og[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      for (int k = 0; k < nwg; ++k) {
-        const uint32_t rec = (uint32_t)k * kBWaves * RB::kRec * 4;
-        const f32x4 sv = load16_coherent(urec, rec + 16 * (16 * nt + lr));
-        f32x4 ov[8];
-#pragma unroll
-        for (int dt = 0; dt < 8; ++dt) ov[dt] = load16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + dt) * kWave + lane));
-        const float mb = fmaxf(Mg[nt], sv[0]);
-        const float mbu = mb == -INFINITY ? 0.f : mb;
-        const float sc = exp2f(Mg[nt] - mbu), wt = exp2f(sv[0] - mbu);
-        Lg[nt] = Lg[nt] * sc + wt * sv[1];
-        Lxg[nt] = Lxg[nt] * sc + wt * sv[2];
-#pragma unroll
-        for (int dt = 0; dt < 8; ++dt) og[nt][dt] = og[nt][dt] * sc + ov[dt] * wt;
-        Mg[nt] = mb;
-      }
-    }
-    write_rows(b, Mg, Lg, Lxg, og);
+  // records of split branches are merged by block_merge_kernel, launched next on the stream
+}
+
+// Merge of the split branches: one wave per (unit, branch, row block, row tile nt, half dh of the
+// d-tiles).  The branch's pieces were stored as records by the workgroups of block_kernel that met
+// it; they are combined here in stream order with an online rescale and written out.  A separate
+// launch spreads the merge over the whole chip: merged by the workgroup that finished last, a branch
+// split over 7 workgroups pulled 7 records of 128 KiB into one CU, ~16 us at one CU's bandwidth.
+// Every load a wave needs is issued before any result is used: the branch lengths (lane b holds
+// branch b's), then up to kMBatch records at a time.
+constexpr int kMBatch = 8;
+template <bool TRAIN>
+__global__ __launch_bounds__(kWave) void block_merge_kernel(AttnParams p) {
+  constexpr int NT = 2;
+  using RB = RowBlock<NT>;
+  const int lane = threadIdx.x, lg = lane >> 4, lr = lane & 15;
+  int id = blockIdx.x;
+  const int dh = id & 1, nt = (id >> 1) & 1;
+  id >>= 2;
+  const int rbl = id % kBWaves;
+  const int ub = id / kBWaves;
+  const int b = ub % p.nbr, unit = ub / p.nbr;
+  const int rg = unit % p.n_rg, pair = unit / p.n_rg;
+  const int g = pair % p.Hkv, s = pair / p.Hkv;
+  const int rb = rg * kBWaves + rbl;
+  if (rb >= p.n_rb) return;
+  const int L = seq_len(p.kv, s);
+  const int my_len = lane < p.nbr ? block_branch_len(p, s, L, lane) : 0;   // nbr <= 64 lanes
+  // the branch's offset in the stream, its length, the stream total and the branch's record slot
+  // (one slot per workgroup that met each earlier non-empty branch)
+  int total = 0, off_b = 0, n = 0;
+  for (int bb = 0; bb < p.nbr; ++bb) {
+    const int nb = __builtin_amdgcn_readlane(my_len, bb);
+    if (bb == b) { off_b = total; n = nb; }
+    total += nb;
   }
+  const int chunk = block_chunk(total, p.nW);
+  if (n == 0) return;
+  const int wlo = off_b / chunk, whi = (off_b + n - 1) / chunk;
+  const int nwg = whi - wlo + 1;
+  if (nwg == 1) return;                            // finished by its one workgroup
+  int rbase = 0;
+  for (int bb = 0, off = 0; bb < b; ++bb) {
+    const int nb = __builtin_amdgcn_readlane(my_len, bb);
+    if (nb > 0) rbase += (off + nb - 1) / chunk - off / chunk + 1;
+    off += nb;
+  }
+  const int rec_per_unit = p.nW + p.nbr - 1;
+  const float* unit_rec = p.part + (int64_t)unit * rec_per_unit * kBWaves * RB::kRec;
+  const __amdgpu_buffer_rsrc_t urec =
+      make_rsrc(unit_rec + ((int64_t)rbase * kBWaves + rbl) * RB::kRec, (uint32_t)(nwg * kBWaves * RB::kRec * 4));
+  constexpr uint32_t kOutOff = 16 * RB::kRows;
+  float Mg = -INFINITY, Lg = 0.f, Lxg = 0.f;
+  f32x4 og[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) og[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int k0 = 0; k0 < nwg; k0 += kMBatch) {
+    f32x4 sv[kMBatch], ov[kMBatch][4];
+#pragma unroll
+    for (int u = 0; u < kMBatch; ++u) {
+      const uint32_t rec = (uint32_t)(k0 + u) * kBWaves * RB::kRec * 4;
+      const bool ok = k0 + u < nwg;
+      sv[u] = ok ? load16_coherent(urec, rec + 16 * (16 * nt + lr)) : f32x4{-INFINITY, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        ov[u][i] = ok ? load16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + 4 * dh + i) * kWave + lane))
+                      : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int u = 0; u < kMBatch; ++u) {
+      if (k0 + u >= nwg) break;
+      const float mb = fmaxf(Mg, sv[u][0]);
+      const float mbu = mb == -INFINITY ? 0.f : mb;
+      const float sc = exp2f(Mg - mbu), wt = exp2f(sv[u][0] - mbu);
+      Lg = Lg * sc + wt * sv[u][1];
+      Lxg = Lxg * sc + wt * sv[u][2];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) og[i] = og[i] * sc + ov[u][i] * wt;
+      Mg = mb;
+    }
+  }
+  // rows 16*nt + lane%16 of row block rb; register r of d-tile 4*dh + i holds d = 32*lg + 16*dh + 4*i + r
+  const int nrow = rb * RB::kRows + 16 * nt + lr;
+  if (nrow >= p.R) return;
+  const int64_t view_rows = (int64_t)p.S * p.nq * p.Hq;
+  const bool gb = b < p.V;
+  uint16_t* out = gb ? p.out_g + (int64_t)b * view_rows * kD : p.out_f;
+  float* lse = gb ? (p.lse_g ? p.lse_g + (int64_t)b * view_rows : nullptr) : p.lse_f;
+  float* out32 = gb ? (p.o32_g ? p.o32_g + (int64_t)b * view_rows * kD : nullptr) : p.o32_f;
+  const int j = nrow / p.G, h = g * p.G + nrow % p.G;
+  const int64_t orow = ((int64_t)s * p.nq + j) * p.Hq + h;
+  const float inv = Lg > 0.f ? 1.f / Lg : 0.f;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const f32x4 a = og[2 * k] * inv, c = og[2 * k + 1] * inv;
+    const u32x4 wv = {pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(c[0], c[1]),
+                      pack_bf16x2(c[2], c[3])};
+    const int d0 = 32 * lg + 16 * dh + 8 * k;
+    *reinterpret_cast<u32x4*>(out + orow * kD + d0) = wv;
+    if (TRAIN && out32) {
+      *reinterpret_cast<f32x4*>(out32 + orow * kD + d0) = a;
+      *reinterpret_cast<f32x4*>(out32 + orow * kD + d0 + 4) = c;
+    }
+  }
+  if (lse && lg == 0 && dh == 0) lse[orow] = Lxg > 0.f ? (Mg + __log2f(Lxg)) * kLn2 : -INFINITY;
 }
 
 }  // namespace
@@ -1227,6 +1366,13 @@ hipError_t launch_attn(const AttnParams& args, const AttnPlan& pl, bool paged, h
     } else {
       if (paged) hipLaunchKernelGGL((block_kernel<true, false>), dim3(pl.nblk), dim3(kBThreads), 0, stream, p);
       else hipLaunchKernelGGL((block_kernel<false, false>), dim3(pl.nblk), dim3(kBThreads), 0, stream, p);
+    }
+    if (pl.nW > 1) {                               // some branch may be split: merge its records
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      const int64_t mblocks = (int64_t)pl.units * pl.nbr * kBWaves * 4;   // (row tile, d half) waves
+      if (train) hipLaunchKernelGGL((block_merge_kernel<true>), dim3((unsigned)mblocks), dim3(kWave), 0, stream, p);
+      else hipLaunchKernelGGL((block_merge_kernel<false>), dim3((unsigned)mblocks), dim3(kWave), 0, stream, p);
     }
     return hipGetLastError();
   }
