@@ -887,8 +887,7 @@ __device__ inline void block_write_rows(const AttnParams& p, int s, int g, int r
 }
 
 // Length of branch b of sequence s in the unit's key stream (the views' entry lists, then the full
-// branch's L cache rows), and the equal share of the stream each of the unit's nW workgroups takes,
-// rounded up to whole tiles; both kernels of block mode cut the stream this way.
+// branch's L cache rows).
 __device__ inline int block_branch_len(const AttnParams& p, int s, int L, int b) {
   if (b < p.V) {
     const int n = p.nsel[b * p.S + s];
@@ -896,10 +895,33 @@ __device__ inline int block_branch_len(const AttnParams& p, int s, int L, int b)
   }
   return L;
 }
-__device__ inline int block_chunk(int total, int nW) {
-  const int c = (total + nW - 1) / nW;
-  return (c + kTile - 1) / kTile * kTile;
-}
+
+// How a unit's key stream is cut among its nW workgroups: equal shares of weighted work, a gathered
+// view entry weighing kWGather and a cache row of the full branch kWFull (measured: a tile of
+// gathered rows takes 1.78 us of a workgroup's loop, a contiguous one 1.43 us).  Views come first,
+// so stream position x (vt = the views' total) weighs kWGather*x up to vt and kWFull per row after.
+// Every share's weight is at least kWGather, so each workgroup below the stream's end gets entries;
+// both kernels of block mode cut the stream with this.
+constexpr int kWGather = 5, kWFull = 4;
+struct BlockCut {
+  int vt, total, chunk;   // chunk: weight per workgroup
+  __device__ BlockCut(int vt_, int total_, int nW) : vt(vt_), total(total_) {
+    const int tw = kWGather * vt + kWFull * (total - vt);
+    const int c = (tw + nW - 1) / nW;
+    chunk = c > kWGather * kTile ? c : kWGather * kTile;
+  }
+  __device__ int weight(int x) const { return x <= vt ? kWGather * x : kWGather * vt + kWFull * (x - vt); }
+  // workgroup whose share holds stream position x
+  __device__ int wg_of(int x) const { return weight(x) / chunk; }
+  // first stream position of workgroup w's share (clamped to the stream's end)
+  __device__ int start_of(int w) const {
+    const int t = w * chunk;
+    int x;
+    if (t <= kWGather * vt) x = (t + kWGather - 1) / kWGather;
+    else x = vt + (t - kWGather * vt + kWFull - 1) / kWFull;
+    return x < total ? x : total;
+  }
+};
 
 template <bool PAGED, bool TRAIN>
 __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
@@ -929,11 +951,13 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
   // stream order.
   if (tid < p.nbr) sm.blen[tid] = block_branch_len(p, s, L, tid);   // nbr <= kBMaxPieces <= kBThreads
   __syncthreads();
-  int total = 0;
-  for (int b = 0; b < p.nbr; ++b) total += sm.blen[b];
-  const int chunk = block_chunk(total, p.nW);
-  const int r0 = w * chunk;
-  const int r1 = r0 + chunk < total ? r0 + chunk : total;
+  int total = 0, vt = 0;
+  for (int b = 0; b < p.nbr; ++b) {
+    total += sm.blen[b];
+    if (b < p.V) vt += sm.blen[b];
+  }
+  const BlockCut cut(vt, total, p.nW);
+  const int r0 = cut.start_of(w), r1 = cut.start_of(w + 1);
 
   // ---- query rows of this wave's lanes: row n = rb*32 + 16*nt + lane%16
   bf16x8 qop[NT][4];
@@ -988,7 +1012,7 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
       const int off_b = off;
       off += n;
       if (n == 0) {
-        int owner = chunk > 0 ? off_b / chunk : 0;
+        int owner = cut.wg_of(off_b);
         if (owner > p.nW - 1) owner = p.nW - 1;
         if (owner == w && has_rows) {
           const float m0[NT] = {-INFINITY, -INFINITY}, z[NT] = {0.f, 0.f};
@@ -1001,7 +1025,7 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
         }
         continue;
       }
-      const int wlo = off_b / chunk, whi = (off_b + n - 1) / chunk;
+      const int wlo = cut.wg_of(off_b), whi = cut.wg_of(off_b + n - 1);
       const int slot_b = rbase;
       rbase += whi - wlo + 1;
       const int lo = r0 > off_b ? r0 : off_b, hi = r1 < off_b + n ? r1 : off_b + n;
@@ -1203,21 +1227,22 @@ __global__ __launch_bounds__(kWave) void block_merge_kernel(AttnParams p) {
   const int my_len = lane < p.nbr ? block_branch_len(p, s, L, lane) : 0;   // nbr <= 64 lanes
   // the branch's offset in the stream, its length, the stream total and the branch's record slot
   // (one slot per workgroup that met each earlier non-empty branch)
-  int total = 0, off_b = 0, n = 0;
+  int total = 0, vt = 0, off_b = 0, n = 0;
   for (int bb = 0; bb < p.nbr; ++bb) {
     const int nb = __builtin_amdgcn_readlane(my_len, bb);
     if (bb == b) { off_b = total; n = nb; }
     total += nb;
+    if (bb < p.V) vt += nb;
   }
-  const int chunk = block_chunk(total, p.nW);
+  const BlockCut cut(vt, total, p.nW);
   if (n == 0) return;
-  const int wlo = off_b / chunk, whi = (off_b + n - 1) / chunk;
+  const int wlo = cut.wg_of(off_b), whi = cut.wg_of(off_b + n - 1);
   const int nwg = whi - wlo + 1;
   if (nwg == 1) return;                            // finished by its one workgroup
   int rbase = 0;
   for (int bb = 0, off = 0; bb < b; ++bb) {
     const int nb = __builtin_amdgcn_readlane(my_len, bb);
-    if (nb > 0) rbase += (off + nb - 1) / chunk - off / chunk + 1;
+    if (nb > 0) rbase += cut.wg_of(off + nb - 1) - cut.wg_of(off) + 1;
     off += nb;
   }
   const int rec_per_unit = p.nW + p.nbr - 1;
@@ -1303,7 +1328,10 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
     pl.nbr = num_views + (with_full ? 1 : 0);
     const int64_t stream_max = (int64_t)num_views * ld_idx + (with_full ? max_L : 0);
     int64_t nw = (kTargetBlocks + pl.units - 1) / pl.units;
-    const int64_t nw_table = (stream_max + kMaxSplitKeys - 1) / kMaxSplitKeys;
+    // a share holds at most chunk/kWFull + 1 entries (chunk = ceil(weighted total / nW)): keep it
+    // within the slot table
+    const int64_t per = (int64_t)kWFull * (kMaxSplitKeys - kTile);
+    const int64_t nw_table = ((int64_t)kWGather * stream_max + per - 1) / per;
     if (nw < nw_table) nw = nw_table;
     if (nw < 1) nw = 1;
     pl.nW = (int)nw;
