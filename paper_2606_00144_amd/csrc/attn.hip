@@ -896,32 +896,10 @@ __device__ inline int block_branch_len(const AttnParams& p, int s, int L, int b)
   return L;
 }
 
-// How a unit's key stream is cut among its nW workgroups: equal shares of weighted work, a gathered
-// view entry weighing kWGather and a cache row of the full branch kWFull (measured: a tile of
-// gathered rows takes 1.78 us of a workgroup's loop, a contiguous one 1.43 us).  Views come first,
-// so stream position x (vt = the views' total) weighs kWGather*x up to vt and kWFull per row after.
-// Every share's weight is at least kWGather, so each workgroup below the stream's end gets entries;
-// both kernels of block mode cut the stream with this.
+// Block mode's cut of a unit's key stream (StreamCut): measured, a tile of gathered rows takes
+// 1.78 us of a workgroup's loop and a contiguous one 1.43 us.
 constexpr int kWGather = 5, kWFull = 4;
-struct BlockCut {
-  int vt, total, chunk;   // chunk: weight per workgroup
-  __device__ BlockCut(int vt_, int total_, int nW) : vt(vt_), total(total_) {
-    const int tw = kWGather * vt + kWFull * (total - vt);
-    const int c = (tw + nW - 1) / nW;
-    chunk = c > kWGather * kTile ? c : kWGather * kTile;
-  }
-  __device__ int weight(int x) const { return x <= vt ? kWGather * x : kWGather * vt + kWFull * (x - vt); }
-  // workgroup whose share holds stream position x
-  __device__ int wg_of(int x) const { return weight(x) / chunk; }
-  // first stream position of workgroup w's share (clamped to the stream's end)
-  __device__ int start_of(int w) const {
-    const int t = w * chunk;
-    int x;
-    if (t <= kWGather * vt) x = (t + kWGather - 1) / kWGather;
-    else x = vt + (t - kWGather * vt + kWFull - 1) / kWFull;
-    return x < total ? x : total;
-  }
-};
+using BlockCut = StreamCut<kWGather, kWFull>;
 
 template <bool PAGED, bool TRAIN>
 __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
@@ -1328,10 +1306,7 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
     pl.nbr = num_views + (with_full ? 1 : 0);
     const int64_t stream_max = (int64_t)num_views * ld_idx + (with_full ? max_L : 0);
     int64_t nw = (kTargetBlocks + pl.units - 1) / pl.units;
-    // a share holds at most chunk/kWFull + 1 entries (chunk = ceil(weighted total / nW)): keep it
-    // within the slot table
-    const int64_t per = (int64_t)kWFull * (kMaxSplitKeys - kTile);
-    const int64_t nw_table = ((int64_t)kWGather * stream_max + per - 1) / per;
+    const int64_t nw_table = stream_cut_min_workgroups<kWGather, kWFull>(stream_max, kMaxSplitKeys);
     if (nw < nw_table) nw = nw_table;
     if (nw < 1) nw = 1;
     pl.nW = (int)nw;

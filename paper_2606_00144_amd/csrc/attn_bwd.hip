@@ -64,7 +64,6 @@ struct DqSmem {
   alignas(16) int32_t roff[kQSlotCap];
   alignas(16) int32_t tpos[kQSlotCap];
   alignas(16) uint8_t ring[kQRing][kQTileBytes];
-  int32_t last;
 };
 
 // Tile load q of a lane (0..23).  q < 8: K, score layout (key sub-tile q/4 -> rows 16*(q/4) + lane%16,
@@ -205,6 +204,13 @@ __device__ inline void dq_tile_step(f32x4 (&acc)[2][8], const DqRows& rw, const 
   }
 }
 
+// The dQ kernel's cut of a unit's key stream (StreamCut): equal shares starting on whole tiles.
+// Weighting gathered entries more, as the forward does, was slower here (163 vs 144 us): a piece
+// costs the dQ kernel its own row loads, slot table and ring start, and spreading the views over
+// more workgroups gave more of them several pieces.
+constexpr int kQWGather = 1, kQWFull = 1;
+using DqCut = StreamCut<kQWGather, kQWFull, kTile>;
+
 template <bool PAGED>
 __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
   __shared__ DqSmem sm;
@@ -225,8 +231,8 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
 
   // The key stream of a unit is the views' entry lists followed by the full branch's cache rows;
   // its actual length is known only here (nsel lives on the device), so the unit's nW workgroups
-  // cut it into equal ranges at run time.  A range crossing a branch boundary runs one piece per
-  // branch (each with the branch's dO, D and lse rows).
+  // cut it into equal weighted shares at run time (DqCut).  A range crossing a branch boundary runs
+  // one piece per branch (each with the branch's dO, D and lse rows).
   auto branch_len = [&](int b) -> int {
     if (b < p.V) {
       const int n = p.nsel[b * p.S + s];
@@ -234,12 +240,14 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
     }
     return L;
   };
-  int total = 0;
-  for (int b = 0; b < p.nbr; ++b) total += branch_len(b);
-  int chunk = (total + p.nW - 1) / p.nW;
-  chunk = (chunk + kTile - 1) / kTile * kTile;
-  const int r0 = w * chunk;
-  const int r1 = r0 + chunk < total ? r0 + chunk : total;
+  int total = 0, vt = 0;
+  for (int b = 0; b < p.nbr; ++b) {
+    const int n = branch_len(b);
+    total += n;
+    if (b < p.V) vt += n;
+  }
+  const DqCut cut(vt, total, p.nW);
+  const int r0 = cut.start_of(w), r1 = cut.start_of(w + 1);
 
   // ---- this wave's rows: Q once; dO, lse and D = <dO, O> per branch
   const int64_t branch_rows = (int64_t)p.S * p.C * p.Hq;
@@ -388,52 +396,62 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
     return;
   }
 
-  // ---- publish this wave's partial as record w of its row block: chunk (nt, dt) x lane float4s
-  const __amdgpu_buffer_rsrc_t urec =
-      make_rsrc(p.part_q + ((int64_t)unit * kQWaves + wave) * p.nW * kRecFloats, (uint32_t)(p.nW * kRecFloats * 4));
+  // ---- publish this wave's partial as record w of its row block: chunk (nt, dt) x lane float4s;
+  // dq_merge_kernel, launched next on the stream, sums them
   if (has_rows) {
+    const __amdgpu_buffer_rsrc_t urec =
+        make_rsrc(p.part_q + ((int64_t)unit * kQWaves + wave) * p.nW * kRecFloats, (uint32_t)(p.nW * kRecFloats * 4));
     const uint32_t rec = (uint32_t)w * kRecFloats * 4;
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) store16_coherent(urec, rec + 16 * ((nt * 8 + dt) * kWave + lane), acc[nt][dt]);
   }
-  wait_vmem();
-  __syncthreads();
-  if (tid == 0) sm.last = arrive(counter_line(p.counters, unit), (uint32_t)p.nW);
-  __syncthreads();
-  if (!sm.last) return;
-  if (tid == 0) reset_counter(counter_line(p.counters, unit));
-  if (!has_rows) return;
-  // sum the row block's partials in workgroup order, one 16-row half at a time; device-scope loads
-  // travel past the XCD's L2, so four records (32 loads) are in flight per round
+}
+
+// Sum of the dQ partials: one wave per (unit, row block, row tile nt, half dh of the d-tiles) adds
+// the nW workgroups' records in workgroup order, so the result does not depend on scheduling.  A
+// separate launch spreads it over the chip: summed by the unit's last workgroup, 8 records of
+// 128 KiB went into one CU (15 us at one CU's bandwidth).  Every load of a batch of kQMBatch
+// records is issued before any is added.
+constexpr int kQMBatch = 8;
+__global__ __launch_bounds__(kWave) void dq_merge_kernel(AttnBwdParams p) {
+  const int lane = threadIdx.x, lg = lane >> 4, lr = lane & 15;
+  int id = blockIdx.x;
+  const int dh = id & 1, nt = (id >> 1) & 1;
+  id >>= 2;
+  const int wave = id % kQWaves, unit = id / kQWaves;
+  const int rg = unit % p.n_rg, pair = unit / p.n_rg;
+  const int g = pair % p.Hkv, s = pair / p.Hkv;
+  const int rb = rg * kQWaves + wave;
+  if (rb >= p.n_rb) return;
+  const int n = rb * 32 + 16 * nt + lr;
+  const __amdgpu_buffer_rsrc_t urec =
+      make_rsrc(p.part_q + ((int64_t)unit * kQWaves + wave) * p.nW * kRecFloats, (uint32_t)(p.nW * kRecFloats * 4));
+  f32x4 o[4];
 #pragma unroll
-  for (int nt = 0; nt < 2; ++nt) {
-    f32x4 o[8];
+  for (int i = 0; i < 4; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < p.nW; k += kQMBatch) {
+    f32x4 x[kQMBatch][4];
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int k = 0; k < p.nW; k += 4) {
-      f32x4 x[4][8];
+    for (int kk = 0; kk < kQMBatch; ++kk)
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
+      for (int i = 0; i < 4; ++i)
+        x[kk][i] = k + kk < p.nW ? load16_coherent(urec, (uint32_t)(k + kk) * kRecFloats * 4 +
+                                                             16 * ((nt * 8 + 4 * dh + i) * kWave + lane))
+                                 : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt)
-          x[kk][dt] = k + kk < p.nW
-                          ? load16_coherent(urec, (uint32_t)(k + kk) * kRecFloats * 4 + 16 * ((nt * 8 + dt) * kWave + lane))
-                          : f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < kQMBatch; ++kk)
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-        for (int dt = 0; dt < 8; ++dt) o[dt] += x[kk][dt];
-    }
-    if (!rvalid[nt]) continue;
-    float* drow = p.dq + orow[nt] * kD + 32 * lg;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<f32x4*>(drow + 8 * i) = f32x4{o[0][i], o[1][i], o[2][i], o[3][i]} * p.scale;
-      *reinterpret_cast<f32x4*>(drow + 8 * i + 4) = f32x4{o[4][i], o[5][i], o[6][i], o[7][i]} * p.scale;
-    }
+      for (int i = 0; i < 4; ++i) o[i] += x[kk][i];
   }
+  if (n >= p.R) return;
+  // register r of d-tile dt = 4*dh + i holds d = 32*lg + 8*r + dt
+  const int j = n / p.G, h = g * p.G + n % p.G;
+  float* drow = p.dq + (((int64_t)s * p.C + j) * p.Hq + h) * kD + 32 * lg + 4 * dh;
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+    *reinterpret_cast<f32x4*>(drow + 8 * r) = f32x4{o[0][r], o[1][r], o[2][r], o[3][r]} * p.scale;
 }
 
 // ---- dK/dV kernel ---------------------------------------------------------------
@@ -724,12 +742,10 @@ AttnBwdPlan plan_attn_bwd(int S, int Hkv, int Hq, int C, int num_views, int ld_i
   pl.nbr = num_views + (with_full ? 1 : 0);
   pl.nkt = (C + 15) / 16;
   // workgroups per unit: enough to fill the CUs once, and enough that no range overflows the slot
-  // table (a range is a share ceil(total / nW) <= kMaxSplitKeys rounded up to whole tiles, which
-  // stays <= kMaxSplitKeys as that is a multiple of the tile)
-  static_assert(kMaxSplitKeys % kTile == 0, "ranges round up to whole tiles");
+  // table (a piece's range is at most kMaxSplitKeys entries)
   const int64_t stream_max = (int64_t)num_views * ld_idx + (with_full ? max_L : 0);
   int64_t nw = (kTargetBlocks + pl.units - 1) / pl.units;
-  const int64_t nw_table = (stream_max + kMaxSplitKeys - 1) / kMaxSplitKeys;
+  const int64_t nw_table = stream_cut_min_workgroups<kQWGather, kQWFull>(stream_max, kMaxSplitKeys);
   if (nw < nw_table) nw = nw_table;
   if (nw < 1) nw = 1;
   pl.nW = (int)nw;
@@ -748,8 +764,14 @@ hipError_t launch_attn_bwd(const AttnBwdParams& p, const AttnBwdPlan& pl, bool p
   if (pl.nblk_q > 0) {
     if (paged) hipLaunchKernelGGL(dq_kernel<true>, dim3(pl.nblk_q), dim3(kQThreads), 0, stream, p);
     else hipLaunchKernelGGL(dq_kernel<false>, dim3(pl.nblk_q), dim3(kQThreads), 0, stream, p);
-    const hipError_t e = hipGetLastError();
+    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (pl.nW > 1) {                               // sum the workgroups' partials
+      const int64_t mblocks = (int64_t)pl.units * kQWaves * 4;   // (row tile, d half) waves
+      hipLaunchKernelGGL(dq_merge_kernel, dim3((unsigned)mblocks), dim3(kWave), 0, stream, p);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
   }
   if (pl.nblk_kv > 0) {
     if (paged) hipLaunchKernelGGL(dkv_kernel<true>, dim3(pl.nblk_kv), dim3(kKThreads), 0, stream, p);

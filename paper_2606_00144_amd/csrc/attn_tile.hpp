@@ -77,4 +77,40 @@ __device__ inline void fill_slot_table(const KvView& kv, int s, int g, int L, co
   }
 }
 
+// How a (sequence, KV head, row group) unit's key stream (the views' entry lists, then the full
+// branch's cache rows) is cut among its nW workgroups: equal shares of weighted work, a gathered
+// view entry weighing WG and a cache row of the full branch WF (gathered tiles cost more per tile).
+// Views come first, so stream position x (vt = the views' total) weighs WG*x up to vt and WF per
+// row after.  A share weighs at least WG*32, so every workgroup below the stream's end gets entries
+// and the workgroups that meet a branch are consecutive.  All kernels over a unit's stream cut it
+// with the same weights.
+// ROUND: the share's weight is rounded up to a multiple of ROUND (with WG = WF = 1 and ROUND = 32,
+// equal shares that start on whole tiles of the stream).
+template <int WG, int WF, int ROUND = 1>
+struct StreamCut {
+  int vt, total, chunk;   // chunk: weight per workgroup
+  __device__ StreamCut(int vt_, int total_, int nW) : vt(vt_), total(total_) {
+    const int tw = WG * vt + WF * (total - vt);
+    int c = (tw + nW - 1) / nW;
+    c = (c + ROUND - 1) / ROUND * ROUND;
+    chunk = c > WG * 32 ? c : WG * 32;
+  }
+  __device__ int weight(int x) const { return x <= vt ? WG * x : WG * vt + WF * (x - vt); }
+  // workgroup whose share holds stream position x
+  __device__ int wg_of(int x) const { return weight(x) / chunk; }
+  // first stream position of workgroup w's share (clamped to the stream's end)
+  __device__ int start_of(int w) const {
+    const int t = w * chunk;
+    const int x = t <= WG * vt ? (t + WG - 1) / WG : vt + (t - WG * vt + WF - 1) / WF;
+    return x < total ? x : total;
+  }
+};
+// Most entries a share can hold: chunk / WF + 1 with chunk = ceil(weighted total / nW); the
+// smallest nW keeping that within `cap` for a stream of at most stream_max entries.
+template <int WG, int WF>
+inline int64_t stream_cut_min_workgroups(int64_t stream_max, int cap) {
+  const int64_t per = (int64_t)WF * (cap - 32);
+  return (WG * stream_max + per - 1) / per;
+}
+
 }  // namespace bd
