@@ -21,6 +21,8 @@
 // row l%16: row statistics stay lane-local, and a key's column sum is a
 // 16-lane DPP reduction.
 
+#include <type_traits>
+
 #include "bd_common.hpp"
 #include "bd_kernels.hpp"
 
@@ -217,8 +219,11 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
 
   float* raw_part = p.raw_part + ((int64_t)pair * p.n_rb + rb) * p.max_L;
 
-  // 16 keys x 16*NT rows of one sub-tile; keys tb .. tb+3 belong to this lane
-  auto sub_step = [&](const u32x4 (&kr)[4], int tb, bool dirty) {
+  // 16 keys x 16*NT rows of one sub-tile; keys tb .. tb+3 belong to this lane.  `dirty` is a
+  // compile-time flag: a runtime one was if-converted, and every tile paid the mask (a compare, a
+  // select and a mask merge per score: a third of the loop's VALU instructions).
+  auto sub_step = [&](const u32x4 (&kr)[4], int tb, auto dirty_tag) {
+    constexpr bool dirty = decltype(dirty_tag)::value;
     f32x4 acc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -227,7 +232,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
       for (int j = 0; j < 4; ++j) a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[j]), qop[nt][j], a, 0, 0, 0);
       acc[nt] = a;
     }
-    if (dirty) {
+    if constexpr (dirty) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
@@ -299,7 +304,9 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
 #pragma unroll
     for (int q = 0; q < kRing; ++q) issue(wave + kWaves * q, q);
     u32x4 kt[2][4];
-    for (int j = 0;; ++j) {
+    int j = 0;
+    // step j of this wave (tile wave + kWaves*j); true after its last tile
+    auto step = [&](auto dirty_tag) -> bool {
       const int it = wave + kWaves * j, slot = j % kRing;
       // the tile about to be read was issued (kRing-1) tiles before the newest
       static_assert(kRing == 2, "the wait below assumes one tile (8 loads) issued after the one read");
@@ -307,11 +314,15 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
       read_ktile(kt, ring_lds + slot * kTileBytes, lane);
       issue(it + kRing * kWaves, slot);
       const int tb = k0 + kTile * it + 4 * lg;
-      const bool dirty = it >= first_dirty;
-      sub_step(kt[0], tb, dirty);
-      sub_step(kt[1], tb + 16, dirty);
-      if (it + kWaves >= ntiles) break;
-    }
+      sub_step(kt[0], tb, dirty_tag);
+      sub_step(kt[1], tb + 16, dirty_tag);
+      ++j;
+      return it + kWaves >= ntiles;
+    };
+    // a wave's tiles increase, so its mask-free ones come first
+    bool last = false;
+    while (!last && wave + kWaves * j < first_dirty) last = step(std::integral_constant<bool, false>{});
+    while (!last) last = step(std::integral_constant<bool, true>{});
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the block ends
   }
 
