@@ -290,3 +290,27 @@ def test_multiview_block_mode_unbalanced_views_and_empty_branches():
             nsel_v[i, s] = n
     idx_v[2, :, :, :5] = -1                            # view 2: five slots, all absent
     _multiview_check(k, v, qb, idx_v, nsel_v, lens, "block mode, unbalanced and empty views")
+
+
+def test_multiview_many_small_views_share_one_range():
+    """60 views of at most 8 entries and the full branch: the first workgroup's share of each unit's stream
+    holds dozens of pieces, each padded to whole tiles of one slot table (up to 64 branches are
+    accepted); the full branch is split across workgroups and merged by the second kernel.  One
+    sequence is shorter than most views' entries, so their out-of-range entries are skipped."""
+    S, Hkv, G, C = 2, 8, 4, 64
+    lens = [4000, 700]
+    Lm = max(lens)
+    k, v = _rand_bits((S, Hkv, Lm, 128), 130), _rand_bits((S, Hkv, Lm, 128), 131)
+    qb = _rand_bits((S, C, Hkv * G, 128), 132)
+    g = np.random.default_rng(133)
+    V, ld = 60, 8
+    idx_v = np.full((V, S, Hkv, ld), -1, np.int32)
+    nsel_v = np.zeros((V, S), np.int32)
+    for i in range(V):
+        for s in range(S):
+            n = int(g.integers(0, ld + 1))
+            for h in range(Hkv):
+                idx_v[i, s, h, :n] = g.integers(0, lens[0], n)      # may repeat; past L_s for s = 1
+            nsel_v[i, s] = n
+    _multiview_check(k, v, qb, idx_v, nsel_v, lens, "60 small views")
+
