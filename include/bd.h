@@ -205,7 +205,9 @@ bd_status bd_sparse_decode_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t
  * weight and its rounded remainder), so the fp32 outputs carry the weights
  * to about 2^-17 rather than 2^-9 (the bf16 outputs are then the rounding
  * of these).  bd_multiview_attn_bwd takes out32 and lse.
- * Requirements: C >= 1, V >= 0, V + (out_full != NULL) >= 1.
+ * Requirements: C >= 1, V >= 0, V + (out_full != NULL) >= 1; with more than
+ * 32 query rows per KV head (C * G > 32) or training outputs, at most 64
+ * branches (V + (out_full != NULL)), else BD_ERR_UNSUPPORTED.
  * ---------------------------------------------------------------------- */
 size_t bd_multiview_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
                                          int32_t block_len, int32_t num_views, int32_t ld_idx,
@@ -240,8 +242,8 @@ bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t
  * dq         [S][C][Hq][128] fp32 (required).
  * dk_blk, dv_blk  NULL (skipped) or both [S][C][Hkv][128] fp32: row c is the
  *            gradient of cache row L_s - C + c of KV head g (0 where that position is < 0).
- * Requirements: 1 <= C <= 1024, C * G <= 1048576, V >= 0, at least one branch,
- * S * Hkv * (ceil(C*G/256) + 1) <= BD_WS_COUNTER_LINES.  Results do not depend on
+ * Requirements: 1 <= C <= 1024, C * G <= 1048576, V >= 0, between one and 64
+ * branches (V + full), S * Hkv * (ceil(C*G/256) + 1) <= BD_WS_COUNTER_LINES.  Results do not depend on
  * scheduling (fixed summation order).
  * ---------------------------------------------------------------------- */
 size_t bd_multiview_attn_bwd_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,

@@ -205,9 +205,9 @@ __device__ inline void dq_tile_step(f32x4 (&acc)[2][8], const DqRows& rw, const 
 }
 
 // The dQ kernel's cut of a unit's key stream (StreamCut): equal shares starting on whole tiles.
-// Weighting gathered entries more, as the forward does, was slower here (163 vs 144 us): a piece
-// costs the dQ kernel its own row loads, slot table and ring start, and spreading the views over
-// more workgroups gave more of them several pieces.
+// Weighting gathered entries more, as the forward does, was slower here (163 vs 144 us; 178 vs
+// 137 us with all pieces of a range in one slot table): the gathered tiles of the views, each row
+// a separate 256-byte read of three tile pieces, slow down as more workgroups stream them at once.
 constexpr int kQWGather = 1, kQWFull = 1;
 using DqCut = StreamCut<kQWGather, kQWFull, kTile>;
 

@@ -334,6 +334,7 @@ bd_status bd_multiview_attn_bwd(const bd_kv_desc* kv, const uint16_t* q_blk, int
                                                kv->max_seq_len, full, dk_blk != nullptr);
   if ((int64_t)pl.units + (int64_t)kv->num_seqs * kv->num_kv_heads > BD_WS_COUNTER_LINES)
     return fail(BD_ERR_UNSUPPORTED, "more than %d work units", BD_WS_COUNTER_LINES);
+  if (pl.nbr > 64) return fail(BD_ERR_UNSUPPORTED, "more than 64 branches (views and the full cache)");
   if ((int64_t)pl.units * pl.nW > INT32_MAX / 2 || (int64_t)pl.nW * 2 * 16 * BD_HEAD_DIM * 4 > INT32_MAX ||
       (int64_t)pl.nbr * block_len * 2 * BD_HEAD_DIM * 4 > INT32_MAX ||
       (int64_t)kv->num_seqs * kv->num_kv_heads * pl.nbr > INT32_MAX / 2)

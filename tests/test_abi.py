@@ -99,6 +99,7 @@ def test_decode_select_multiview_accept_rejections(L):
     assert mv(V=0, of=None) == 1
     assert mv(ov=None) == 1
     assert mv(o32f=FAKE + 8) == 1                                            # misaligned fp32 output
+    assert mv(V=64) == 2                                     # block mode: 64 views + the full cache > 64 branches
     acc = lambda **a: L.bd_accept_len(a.get("lg", FAKE), a.get("rs", 32000), a.get("dr", FAKE), 2, a.get("g", 5),
                                       32000, FAKE, None, None, FAKE, 1 << 40, None)
     assert acc(lg=None) == 1
@@ -131,6 +132,7 @@ def test_multiview_bwd_rejections(L):
     assert bwd(wsb=1024) == bd.BD_ERR_WORKSPACE
     big = _kv(num_seqs=4096, num_kv_heads=8, max_seq_len=64, stride_seq=8 * 64 * 128, stride_head=64 * 128)
     assert bwd(kv=big) == bd.BD_ERR_UNSUPPORTED                           # counter lines exhausted
+    assert bwd(V=64) == bd.BD_ERR_UNSUPPORTED                             # 65 branches
 
 
 def test_workspace_sizes(L):
