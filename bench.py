@@ -86,8 +86,8 @@ def cpu_baseline(host, S, Hq, L, B, gamma):
     threads = len(os.sched_getaffinity(0))
     qs, kS, vS, kL, vL, logits, draft = host
     lens = [L] * S
-    cfg = synth.CONFIGS[2]
-    idx = np.stack([np.stack([np.r_[synth.random_index_set(2, s, g, L - cfg.window, B - cfg.window),
+    cfg = synth.workload("16k-collapse-b8")
+    idx = np.stack([np.stack([np.r_[synth.random_index_set(cfg.config_id, s, g, L - cfg.window, B - cfg.window),
                                     np.arange(L - cfg.window, L)] for g in range(cfg.num_kv_heads)])
                     for s in range(S)]).astype(np.int32)
     t0 = time.perf_counter()
@@ -134,7 +134,7 @@ def main():
         return bench_updates(args, bd, synth, torch, np, dev)
     if args.op == "ce":
         return bench_ce(args, bd, synth, torch, np, dev)
-    cfg = synth.CONFIGS[2]
+    cfg = synth.workload("16k-collapse-b8")
     S, Hq, Hkv, L, W, gamma, V = (cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.window,
                                   cfg.gamma, cfg.vocab)
     B = args.budget
@@ -326,7 +326,7 @@ def _time_graph(torch, fn, steps, warmup, per_graph=1):
 
 def bench_select(args, bd, synth, torch, np, dev):
     """bd_select_kv on the 16K batch (8 x 16,384, W = 32, pool 7, B = --budget)."""
-    cfg = synth.CONFIGS[2]
+    cfg = synth.workload("16k-collapse-b8")
     S, Hq, Hkv, L, W, B = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.window, args.budget
     log("generating inputs")
     qs, kS, _ = synth.kv_batch(cfg)
@@ -358,7 +358,7 @@ def bench_select(args, bd, synth, torch, np, dev):
 
 def _multiview_inputs(bd, synth, torch, np, dev):
     """The multi-view training block (4 x 8,192, C = 64, four budgets), views from bd_select_kv."""
-    cfg = synth.CONFIGS[3]
+    cfg = synth.workload("multiview-train-b4-8k")
     S, Hq, Hkv, L, C = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.block_len
     budgets = [int(b) for b in synth.view_budgets(cfg)]
     log("generating inputs")
@@ -452,7 +452,7 @@ def bench_updates(args, bd, synth, torch, np, dev):
     """One round of Alg. 2's cache updates on the 16K batch: gamma single-row appends to the drafter
     cache and its sparse list, gamma+1 rows to the verifier cache, then both rollbacks (accept = 0,
     so every round leaves each cache one row longer)."""
-    cfg = synth.CONFIGS[2]
+    cfg = synth.workload("16k-collapse-b8")
     S, Hq, Hkv, L, gamma, B = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.gamma, args.budget
     steps = max(1, min(args.steps, 50))
     warm = min(args.warmup, 5)
@@ -495,7 +495,7 @@ def bench_updates(args, bd, synth, torch, np, dev):
 def bench_ce(args, bd, synth, torch, np, dev):
     """Top-1 CE with the targets' scan fused (Eqs. 5-7) on the multi-view training shape: the 4 x 64
     continuation rows, vocabulary 32,000; student and teacher logits fp32."""
-    cfg = synth.CONFIGS[3]
+    cfg = synth.workload("multiview-train-b4-8k")
     R, V = cfg.num_seqs * cfg.block_len, 32000
     g = torch.Generator(device=dev)
     g.manual_seed(0)

@@ -102,6 +102,12 @@ CONFIGS: List[Config] = [
     Config(4, "ragged-paged-b64-mha", 64, 32, 32, 16384, 0.01, 32, (1024,), 5, 32000,
            ragged_min_len=4096, page_size=16),
 ]
+WORKLOADS = {c.name: c for c in CONFIGS}
+
+
+def workload(name: str) -> Config:
+    """The synthetic workload of that name (its config_id seeds its generators)."""
+    return WORKLOADS[name]
 
 
 def seq_lens(cfg: Config) -> np.ndarray:

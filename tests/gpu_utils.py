@@ -53,14 +53,14 @@ def assert_close(gpu: np.ndarray, ref: np.ndarray, what: str, atol=ATOL, rtol=RT
 def assert_lse(gpu: np.ndarray, ref: np.ndarray, what: str):
     both_inf = np.isneginf(gpu) & np.isneginf(ref)
     assert np.array_equal(np.isneginf(gpu), np.isneginf(ref)), f"{what}: -inf pattern differs"
-    d = np.where(both_inf, 0.0, np.abs(gpu - ref))
+    d = np.abs(np.where(both_inf, 0.0, gpu) - np.where(both_inf, 0.0, ref))   # -inf - -inf is not a number
     assert d.max(initial=0.0) <= LSE_ATOL, f"{what}: lse error {d.max()}"
 
 
 @functools.lru_cache(maxsize=4)
-def config_data(cid: int, verifier: bool = False):
-    """Per-sequence bf16 bits of a fixed-length config: (q_tail [S][T][Hq][D], k, v [S][Hkv][L][D])."""
-    cfg = synth.CONFIGS[cid]
+def config_data(name: str, verifier: bool = False):
+    """Per-sequence bf16 bits of a fixed-length workload: (q_tail [S][T][Hq][D], k, v [S][Hkv][L][D])."""
+    cfg = synth.workload(name)
     tags = (synth.TAG_K_VERIFIER, synth.TAG_V_VERIFIER) if verifier else (synth.TAG_K, synth.TAG_V)
     qs, ks, vs = synth.kv_batch(cfg, tag_k=tags[0], tag_v=tags[1])
     return np.stack(qs), np.stack(ks), np.stack(vs)

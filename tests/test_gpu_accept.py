@@ -23,13 +23,13 @@ def _run(logits: np.ndarray, draft: np.ndarray, what: str):
     return ra
 
 
-@pytest.mark.parametrize("cid", [0, 2])
-def test_accept_configs(cid):
-    cfg = synth.CONFIGS[cid]
+@pytest.mark.parametrize("name", ["tiny-4k-gqa4", "16k-collapse-b8"])
+def test_accept_workloads(name):
+    cfg = synth.workload(name)
     data = [synth.logits_and_drafts(cfg, s) for s in range(cfg.num_seqs)]
     logits = np.stack([d[0] for d in data])
     draft = np.stack([d[1] for d in data])
-    ra = _run(logits, draft, f"cfg{cid}")
+    ra = _run(logits, draft, name)
     assert ra.tolist() == [d[3] for d in data]                # planted prefix lengths
 
 

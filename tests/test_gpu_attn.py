@@ -21,12 +21,12 @@ def _rand_bits(shape, seed, scale=1.0):
     return synth.f32_to_bf16_bits(scale * g.standard_normal(shape, dtype=np.float32))
 
 
-def _sparse_idx(cid, S, Hkv, L, B, W=32):
+def _sparse_idx(cfg, S, Hkv, L, B, W=32):
     """Seeded index lists shaped like a selection: B-W prefix positions + the window."""
     idx = np.full((S, Hkv, B), -1, np.int32)
     for s in range(S):
         for g in range(Hkv):
-            pre = synth.random_index_set(cid, s, g, L - W, B - W)
+            pre = synth.random_index_set(cfg.config_id, s, g, L - W, B - W)
             idx[s, g] = np.r_[pre, np.arange(L - W, L)]
     return idx
 
@@ -46,28 +46,28 @@ def _decode_check(k, v, q, idx, nsel, lens, what, kdev=None, vdev=None, page_tab
 
 # ------------------------------------------------------------------ decode
 
-def test_decode_config0_oracle_selection():
-    cfg = synth.CONFIGS[0]
-    qt, k, v = config_data(0)
+def test_decode_tiny4k_oracle_selection():
+    cfg = synth.workload("tiny-4k-gqa4")
+    qt, k, v = config_data("tiny-4k-gqa4")
     lens = [cfg.seq_len]
     idx, nsel, _ = O.select_kv(k, qt[:, -cfg.window:], lens, cfg.num_q_heads, cfg.window, 256)
-    _decode_check(k, v, qt[:, -1], idx, nsel, lens, "cfg0 B=256")
+    _decode_check(k, v, qt[:, -1], idx, nsel, lens, "tiny 4K B=256")
 
 
 @pytest.mark.parametrize("B", [256, 512, 1024, 2048])
-def test_decode_config1_budgets(B):
-    cfg = synth.CONFIGS[1]
-    qt, k, v = config_data(1)
-    idx = _sparse_idx(1, 1, cfg.num_kv_heads, cfg.seq_len, B)
-    _decode_check(k, v, qt[:, -1], idx, [B], [cfg.seq_len], f"cfg1 B={B}")
+def test_decode_layer8k_budgets(B):
+    cfg = synth.workload("llama3-8b-layer-8k")
+    qt, k, v = config_data("llama3-8b-layer-8k")
+    idx = _sparse_idx(synth.workload("llama3-8b-layer-8k"), 1, cfg.num_kv_heads, cfg.seq_len, B)
+    _decode_check(k, v, qt[:, -1], idx, [B], [cfg.seq_len], f"8K layer B={B}")
 
 
-def test_decode_config2_full_size():
-    cfg = synth.CONFIGS[2]
-    qt, k, v = config_data(2)
+def test_decode_batch16k_full_size():
+    cfg = synth.workload("16k-collapse-b8")
+    qt, k, v = config_data("16k-collapse-b8")
     for B in cfg.budgets:
-        idx = _sparse_idx(2, cfg.num_seqs, cfg.num_kv_heads, cfg.seq_len, B)
-        _decode_check(k, v, qt[:, -1], idx, [B] * cfg.num_seqs, [cfg.seq_len] * cfg.num_seqs, f"cfg2 B={B}")
+        idx = _sparse_idx(synth.workload("16k-collapse-b8"), cfg.num_seqs, cfg.num_kv_heads, cfg.seq_len, B)
+        _decode_check(k, v, qt[:, -1], idx, [B] * cfg.num_seqs, [cfg.seq_len] * cfg.num_seqs, f"16K batch B={B}")
 
 
 def test_decode_edge_cases():
@@ -99,9 +99,9 @@ def test_decode_edge_cases():
 
 
 def test_decode_permutation_and_determinism():
-    cfg = synth.CONFIGS[1]
-    qt, k, v = config_data(1)
-    idx = _sparse_idx(1, 1, cfg.num_kv_heads, cfg.seq_len, 1024)
+    cfg = synth.workload("llama3-8b-layer-8k")
+    qt, k, v = config_data("llama3-8b-layer-8k")
+    idx = _sparse_idx(synth.workload("llama3-8b-layer-8k"), 1, cfg.num_kv_heads, cfg.seq_len, 1024)
     perm = idx[:, :, np.random.default_rng(5).permutation(1024)]
     kd, vd, qd, lens = bf16_dev(k), bf16_dev(v), bf16_dev(qt[:, -1]), i32_dev([cfg.seq_len])
     case("decode permutation / determinism")
@@ -128,19 +128,19 @@ def _verify_check(k, v, q, lens, gamma, what, kdev=None, vdev=None, page_table=N
     return out
 
 
-@pytest.mark.parametrize("cid", [0, 1])
-def test_verify_configs(cid):
-    cfg = synth.CONFIGS[cid]
-    qt, k, v = config_data(cid)
+@pytest.mark.parametrize("name", ["tiny-4k-gqa4", "llama3-8b-layer-8k"])
+def test_verify_workloads(name):
+    cfg = synth.workload(name)
+    qt, k, v = config_data(name)
     g1 = cfg.gamma + 1
-    _verify_check(k, v, qt[:, -g1:], [cfg.seq_len] * cfg.num_seqs, cfg.gamma, f"cfg{cid}")
+    _verify_check(k, v, qt[:, -g1:], [cfg.seq_len] * cfg.num_seqs, cfg.gamma, name)
 
 
-def test_verify_config2_full_size():
-    cfg = synth.CONFIGS[2]
-    qt, k, v = config_data(2)
+def test_verify_batch16k_full_size():
+    cfg = synth.workload("16k-collapse-b8")
+    qt, k, v = config_data("16k-collapse-b8")
     g1 = cfg.gamma + 1
-    _verify_check(k, v, qt[:, -g1:], [cfg.seq_len] * cfg.num_seqs, cfg.gamma, "cfg2 16K")
+    _verify_check(k, v, qt[:, -g1:], [cfg.seq_len] * cfg.num_seqs, cfg.gamma, "16K batch 16K")
 
 
 @pytest.mark.parametrize("Hq,Hkv,gamma", [(8, 2, 5), (4, 4, 5), (16, 2, 5), (8, 2, 0), (32, 8, 3)])
@@ -153,8 +153,8 @@ def test_verify_ragged_shapes(Hq, Hkv, gamma):
 
 
 def test_verify_matches_decode_over_everything():
-    cfg = synth.CONFIGS[0]
-    qt, k, v = config_data(0)
+    cfg = synth.workload("tiny-4k-gqa4")
+    qt, k, v = config_data("tiny-4k-gqa4")
     L, g1 = cfg.seq_len, cfg.gamma + 1
     kd, vd = bf16_dev(k), bf16_dev(v)
     idx = np.tile(np.arange(L, dtype=np.int32), (1, cfg.num_kv_heads, 1))
@@ -166,7 +166,7 @@ def test_verify_matches_decode_over_everything():
 
 
 def test_verify_paged_ragged_mha():
-    cfg = synth.CONFIGS[4]
+    cfg = synth.workload("ragged-paged-b64-mha")
     lens_all = synth.seq_lens(cfg)
     pick = [0, 1, 2, 3, 4, 5]
     lens = lens_all[pick]
@@ -177,12 +177,12 @@ def test_verify_paged_ragged_mha():
         ks.append(k), vs.append(v), qs.append(qt[-(cfg.gamma + 1):])
     table, npages = synth.page_table(cfg, lens)
     kd, vd = paged_kv(ks, vs, table, npages, cfg.page_size)
-    _verify_check(ks, vs, np.stack(qs), lens, cfg.gamma, "paged cfg4 sample", kdev=kd, vdev=vd,
+    _verify_check(ks, vs, np.stack(qs), lens, cfg.gamma, "paged ragged paged sample", kdev=kd, vdev=vd,
                   page_table=i32_dev(table))
-    idx = np.stack([np.stack([np.r_[synth.random_index_set(4, s, g, int(lens[i]) - 32, 1024 - 32),
+    idx = np.stack([np.stack([np.r_[synth.random_index_set(cfg.config_id, s, g, int(lens[i]) - 32, 1024 - 32),
                                     np.arange(lens[i] - 32, lens[i])] for g in range(cfg.num_kv_heads)])
                     for i, s in enumerate(pick)]).astype(np.int32)
-    _decode_check(ks, vs, np.stack([q[-1] for q in qs]), idx, [1024] * len(pick), lens, "paged cfg4 sample",
+    _decode_check(ks, vs, np.stack([q[-1] for q in qs]), idx, [1024] * len(pick), lens, "paged ragged paged sample",
                   kdev=kd, vdev=vd, page_table=i32_dev(table))
 
 
@@ -214,9 +214,9 @@ def test_multiview_small_with_selected_views():
     _multiview_check(k, v, qb, idx_v, nsel_v, [L, L], "small")
 
 
-def test_multiview_config3_sampled():
-    cfg = synth.CONFIGS[3]
-    qt, k, v = config_data(3)
+def test_multiview_multiview4x8k_sampled():
+    cfg = synth.workload("multiview-train-b4-8k")
+    qt, k, v = config_data("multiview-train-b4-8k")
     C = cfg.block_len
     budgets = synth.view_budgets(cfg)
     ld = int(budgets.max())
@@ -224,11 +224,11 @@ def test_multiview_config3_sampled():
     idx_v = np.full((len(budgets), S, cfg.num_kv_heads, ld), -1, np.int32)
     nsel_v = np.zeros((len(budgets), S), np.int32)
     for i, B in enumerate(budgets):
-        idx_v[i, :, :, :int(B)] = _sparse_idx(3, S, cfg.num_kv_heads, cfg.seq_len, int(B), W=C)
+        idx_v[i, :, :, :int(B)] = _sparse_idx(synth.workload("multiview-train-b4-8k"), S, cfg.num_kv_heads, cfg.seq_len, int(B), W=C)
         nsel_v[i] = B
     qb = qt[:, -C:]
     lens = [cfg.seq_len] * S
-    case("multiview cfg3 full size")
+    case("multiview multiview 4x8K full size")
     ov, of = bd.bd_multiview_attn(bf16_dev(k), bf16_dev(v), bf16_dev(qb), i32_dev(idx_v), i32_dev(nsel_v), i32_dev(lens))
     torch.cuda.synchronize()
     gv, gf = bf16_host64(ov), bf16_host64(of)
@@ -236,8 +236,8 @@ def test_multiview_config3_sampled():
     s = 1
     rv, rf = O.multiview_attn(k[s:s + 1], v[s:s + 1], qb[s:s + 1], [iv[s:s + 1] for iv in idx_v],
                               [nv[s:s + 1] for nv in nsel_v], lens[:1])
-    assert_close(gv[:, s:s + 1], rv, "cfg3 views seq 1")
-    assert_close(gf[s:s + 1], rf, "cfg3 full seq 1")
+    assert_close(gv[:, s:s + 1], rv, "multiview 4x8K views seq 1")
+    assert_close(gf[s:s + 1], rf, "multiview 4x8K full seq 1")
 
 
 def test_one_workspace_serves_every_operation_and_shape():

@@ -187,11 +187,11 @@ def test_bwd_paged_cache():
     _run(k, v, qb, idx_v, nsel_v, lens, "paged", seed=7, kdev=kd, vdev=vd, page_table=i32_dev(table))
 
 
-def test_bwd_config3_full_size_sampled():
+def test_bwd_multiview4x8k_full_size_sampled():
     """The multi-view training block at full size (4 x 8,192, C = 64, four budgets + full); the oracle
     checks one sequence, all heads and branches."""
-    cfg = synth.CONFIGS[3]
-    qt, k, v = config_data(3)
+    cfg = synth.workload("multiview-train-b4-8k")
+    qt, k, v = config_data("multiview-train-b4-8k")
     C = cfg.block_len
     budgets = synth.view_budgets(cfg)
     S = cfg.num_seqs
@@ -201,11 +201,11 @@ def test_bwd_config3_full_size_sampled():
     for i, B in enumerate(budgets):
         for s in range(S):
             for h in range(cfg.num_kv_heads):
-                pre = synth.random_index_set(3, s, h, cfg.seq_len - C, int(B) - C)
+                pre = synth.random_index_set(cfg.config_id, s, h, cfg.seq_len - C, int(B) - C)
                 idx_v[i, s, h, :int(B)] = np.r_[pre, np.arange(cfg.seq_len - C, cfg.seq_len)]
         nsel_v[i] = B
     lens = [cfg.seq_len] * S
-    _run(k, v, qt[:, -C:], idx_v, nsel_v, lens, "cfg3 full size", seed=8, seqs=[2], check_fwd=False)
+    _run(k, v, qt[:, -C:], idx_v, nsel_v, lens, "multiview 4x8K full size", seed=8, seqs=[2], check_fwd=False)
 
 
 def test_bwd_deterministic_and_workspace_reuse():

@@ -63,18 +63,18 @@ def _check(k, q_win, lens, Hq, W, B, what, pool_kernel=7, **kw):
     return near
 
 
-def test_select_config0():
-    cfg = synth.CONFIGS[0]
-    qt, k, v = config_data(0)
-    near = _check(k, qt[:, -cfg.window:], [cfg.seq_len], cfg.num_q_heads, cfg.window, 256, "cfg0")
+def test_select_tiny4k():
+    cfg = synth.workload("tiny-4k-gqa4")
+    qt, k, v = config_data("tiny-4k-gqa4")
+    near = _check(k, qt[:, -cfg.window:], [cfg.seq_len], cfg.num_q_heads, cfg.window, 256, "tiny 4K")
     assert near <= 1
 
 
 @pytest.mark.parametrize("B", [256, 512, 1024, 2048])
-def test_select_config1_budgets(B):
-    cfg = synth.CONFIGS[1]
-    qt, k, v = config_data(1)
-    near = _check(k, qt[:, -cfg.window:], [cfg.seq_len], cfg.num_q_heads, cfg.window, B, f"cfg1 B={B}")
+def test_select_layer8k_budgets(B):
+    cfg = synth.workload("llama3-8b-layer-8k")
+    qt, k, v = config_data("llama3-8b-layer-8k")
+    near = _check(k, qt[:, -cfg.window:], [cfg.seq_len], cfg.num_q_heads, cfg.window, B, f"8K layer B={B}")
     assert near <= 2
 
 
@@ -128,7 +128,7 @@ def test_select_lse_input_matches_two_pass():
 
 
 def test_select_ragged_paged_mha():
-    cfg = synth.CONFIGS[4]
+    cfg = synth.workload("ragged-paged-b64-mha")
     lens = synth.seq_lens(cfg)[:4]
     ks, vs, qw = [], [], []
     for s in range(4):
@@ -137,6 +137,6 @@ def test_select_ragged_paged_mha():
         ks.append(kk), vs.append(vv), qw.append(qt[-cfg.window:])
     table, npages = synth.page_table(cfg, lens)
     kd, _ = paged_kv(ks, vs, table, npages, cfg.page_size)
-    near = _check(ks, np.stack(qw), lens, cfg.num_q_heads, cfg.window, 1024, "cfg4 paged",
+    near = _check(ks, np.stack(qw), lens, cfg.num_q_heads, cfg.window, 1024, "ragged paged paged",
                   page_table=i32_dev(table), kdev=kd)
     assert near <= 4

@@ -71,18 +71,18 @@ def _check(k, q_win, lens, Hq, W, B, s, what):
     return gi, near
 
 
-def test_select_chunks_config0():
-    cfg = synth.CONFIGS[0]
-    qt, k, _ = config_data(0)
-    _, near = _check(k, qt[:, -cfg.window:], [cfg.seq_len], cfg.num_q_heads, cfg.window, 256, 8, "cfg0")
+def test_select_chunks_tiny4k():
+    cfg = synth.workload("tiny-4k-gqa4")
+    qt, k, _ = config_data("tiny-4k-gqa4")
+    _, near = _check(k, qt[:, -cfg.window:], [cfg.seq_len], cfg.num_q_heads, cfg.window, 256, 8, "tiny 4K")
     assert near <= 1
 
 
 @pytest.mark.parametrize("B", [256, 1024])
-def test_select_chunks_config1(B):
-    cfg = synth.CONFIGS[1]
-    qt, k, _ = config_data(1)
-    _, near = _check(k, qt[:, -cfg.window:], [cfg.seq_len], cfg.num_q_heads, cfg.window, B, 8, f"cfg1 B={B}")
+def test_select_chunks_layer8k(B):
+    cfg = synth.workload("llama3-8b-layer-8k")
+    qt, k, _ = config_data("llama3-8b-layer-8k")
+    _, near = _check(k, qt[:, -cfg.window:], [cfg.seq_len], cfg.num_q_heads, cfg.window, B, 8, f"8K layer B={B}")
     assert near <= 2
 
 

@@ -250,8 +250,8 @@ def test_select_uses_contiguous_head_groups():
     assert idx[0, 0, :16].tolist() == list(range(16))
 
 
-def test_select_config0_heavy_hitters_selected():
-    cfg = synth.CONFIGS[0]
+def test_select_tiny4k_heavy_hitters_selected():
+    cfg = synth.workload("tiny-4k-gqa4")
     L = cfg.seq_len
     qt = synth.query_tail(cfg, 0)
     k, _ = synth.kv_sequence(cfg, 0, q_tail=qt)
@@ -505,7 +505,7 @@ def test_multiview_causal_closed_form():
 # ---------------------------------------------------------------- accept (Eq. 3, Alg. 2)
 
 def test_accept_planted_prefix_lengths():
-    cfg = synth.CONFIGS[2]
+    cfg = synth.workload("16k-collapse-b8")
     for s in range(cfg.num_seqs):
         lg, dr, tok, m = synth.logits_and_drafts(cfg, s, vocab=3000)
         acc, bonus, am = O.accept_len(lg[None], dr[None], cfg.gamma)
