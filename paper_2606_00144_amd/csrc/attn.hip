@@ -215,45 +215,6 @@ __device__ inline void dma_tile(const KvView& kv, const TileRows& A, uint32_t ma
     }
 }
 
-// V^T operands of all 8 d-tiles straight from a row-major V tile in LDS with the transposing
-// read ds_read_b64_tr_b16.  Within each 16-lane group that read hands lane i, element j, element
-// i%4 of the 8 bytes that lane 4j + i/4 addressed.  The caller passes a[j] = the lane's address
-// for d-tiles 2j and 2j+1 (k-slots 0..3); +8 selects the odd d-tile, +4096 the k-slots 4..7 (tile
-// rows 16..31).  Result vt[dt], slot k of lane l: V[key slot 16*(k/4) + 4*(l/16) + k%4]
-// [d = 32*((l%16)/4) + 4*dt + l%4], so accumulator register r of d-tile dt in lane l holds
-// d = 32*(l/16) + 4*dt + r.  One statement, ending in its own wait (direct-to-LDS loads in flight
-// must not make it wait for them).
-__device__ inline void read_vt_tr(bf16x8 (&vt)[8], const uint32_t (&a)[4]) {
-  uint64_t x[16];
-  asm volatile(
-      "ds_read_b64_tr_b16 %0, %16\n"
-      "ds_read_b64_tr_b16 %1, %16 offset:4096\n"
-      "ds_read_b64_tr_b16 %2, %16 offset:8\n"
-      "ds_read_b64_tr_b16 %3, %16 offset:4104\n"
-      "ds_read_b64_tr_b16 %4, %17\n"
-      "ds_read_b64_tr_b16 %5, %17 offset:4096\n"
-      "ds_read_b64_tr_b16 %6, %17 offset:8\n"
-      "ds_read_b64_tr_b16 %7, %17 offset:4104\n"
-      "ds_read_b64_tr_b16 %8, %18\n"
-      "ds_read_b64_tr_b16 %9, %18 offset:4096\n"
-      "ds_read_b64_tr_b16 %10, %18 offset:8\n"
-      "ds_read_b64_tr_b16 %11, %18 offset:4104\n"
-      "ds_read_b64_tr_b16 %12, %19\n"
-      "ds_read_b64_tr_b16 %13, %19 offset:4096\n"
-      "ds_read_b64_tr_b16 %14, %19 offset:8\n"
-      "ds_read_b64_tr_b16 %15, %19 offset:4104\n"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3]), "=&v"(x[4]), "=&v"(x[5]), "=&v"(x[6]), "=&v"(x[7]),
-        "=&v"(x[8]), "=&v"(x[9]), "=&v"(x[10]), "=&v"(x[11]), "=&v"(x[12]), "=&v"(x[13]), "=&v"(x[14]),
-        "=&v"(x[15])
-      : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]));
-#pragma unroll
-  for (int dt = 0; dt < 8; ++dt) {
-    const uint64_t lo = x[2 * dt], hi = x[2 * dt + 1];
-    vt[dt] = as_bf16x8(u32x4{(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)});
-  }
-}
-
 // V rows already in the tile registers.
 template <int NT, bool PAGED>
 __device__ inline auto pass_v(const TileRegs<NT, PAGED>& T) {
@@ -839,15 +800,13 @@ __device__ inline void read_block_tile_k(TileRegs<2, true>& T, uint32_t (&r)[2],
       : "v"(at), "v"(ap), "v"(a0), "v"(a1));
 }
 // Load q (0..15) of a tile for this lane; `r` is the row's offset in 16-byte units.  K loads
-// q < 8 (sub-tile q/4, k-step q%4) land in the score operand order.  V loads q >= 8 write tile
-// rows 4*(q-8) + lane/16, row-major (row r at byte 8192 + 256*r of the tile) with the row's 16-byte
-// chunks XOR-swizzled by r%4 (chunk c stored at position c ^ (r%4)), so the transposing reads of
-// read_vt_tr spread over the LDS banks.
+// q < 8 (sub-tile q/4, k-step q%4) land in the score operand order.  V loads q >= 8 fill the
+// tile's second half as a row-major tile for the transposing reads (rm_row, rm_chunk).
 __device__ inline void dma_load(const KvView& kv, uint32_t r, uint32_t max_roff, int q, uint8_t* dst, int lane) {
   const int lg = lane >> 4, lr = lane & 15;
   const uint32_t ro = r < max_roff ? r : max_roff;
   if (q < 8) dma16(kv.k + ((uint64_t)ro << 3) + 32 * lg + 8 * (q & 3), dst + q * 1024);
-  else dma16(kv.v + ((uint64_t)ro << 3) + 8 * (lr ^ lg), dst + q * 1024);
+  else dma16(kv.v + ((uint64_t)ro << 3) + 8 * rm_chunk(lane), dst + q * 1024);
 }
 
 // Branch b's outputs of row block rb (rows 16*nt + lane%16 of it) from an unnormalised state:
@@ -955,14 +914,12 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
 
   // ---- the two loads of every tile that this wave issues, and the tile rows they read
   const int q0 = 2 * wave, q1 = 2 * wave + 1;
-  auto row_in_tile = [&](int q) { return q < 8 ? 16 * (q >> 2) + lr : 4 * (q - 8) + lg; };
+  auto row_in_tile = [&](int q) { return q < 8 ? 16 * (q >> 2) + lr : rm_row(q - 8, lane); };
   const int rit0 = row_in_tile(q0), rit1 = row_in_tile(q1);
-  // transposing V reads (read_vt_tr): this lane addresses tile row 4*(lane/16) + (lane%16)/4
-  // (k-slots 0..3; +4096 for 4..7), d from 32*(lane%4) + 8*j, at its swizzled chunk position
+  // transposing V reads (read_vt_tr) of the row-major V half of a tile
   uint32_t vtr_off[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
-    vtr_off[j] = 8192u + 256u * (uint32_t)(4 * lg + (lr >> 2)) + 16u * (uint32_t)((4 * (lr & 3) + j) ^ (lr >> 2));
+  for (int j = 0; j < 4; ++j) vtr_off[j] = 8192u + tr_lane_off(lane, j);
   const uint32_t roff_lds = lds_addr(sm.roff), tpos_lds = lds_addr(sm.tpos);
   const uint32_t ring_lds = lds_addr(sm.ring[0]);
   auto issue = [&](int tile, const uint32_t (&r)[2]) {

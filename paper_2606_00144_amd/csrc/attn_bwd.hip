@@ -67,19 +67,19 @@ struct DqSmem {
 };
 
 // Tile load q of a lane (0..23).  q < 8: K, score layout (key sub-tile q/4 -> rows 16*(q/4) + lane%16,
-// 16 bytes at d = 32*(lane/16) + 8*(q%4)); 8 <= q < 16: V, same layout; 16 <= q < 24: K, transposed
-// layout (rows 16*((q-16)/4) + 4*(lane/16) + (q-16)%4, 16 bytes at d = 8*(lane%16)).
+// 16 bytes at d = 32*(lane/16) + 8*(q%4)); 8 <= q < 16: V, same layout; 16 <= q < 24: K again, as a
+// row-major tile for the transposing reads of the dQ product (rm_row, rm_chunk).
 __device__ inline int load_row_in_tile(int q, int lane) {
-  const int lg = lane >> 4, lr = lane & 15;
-  return q < 16 ? 16 * ((q & 7) >> 2) + lr : 16 * ((q - 16) >> 2) + 4 * lg + ((q - 16) & 3);
+  const int lr = lane & 15;
+  return q < 16 ? 16 * ((q & 7) >> 2) + lr : rm_row(q - 16, lane);
 }
 __device__ inline void dq_dma_load(const KvView& kv, uint32_t r, uint32_t max_roff, int q, uint8_t* dst, int lane) {
-  const int lg = lane >> 4, lr = lane & 15;
+  const int lg = lane >> 4;
   const uint32_t ro = r < max_roff ? r : max_roff;
   const uint64_t base = (uint64_t)ro << 3;
   if (q < 8) dma16(kv.k + base + 32 * lg + 8 * (q & 3), dst + q * 1024);
   else if (q < 16) dma16(kv.v + base + 32 * lg + 8 * (q & 3), dst + q * 1024);
-  else dma16(kv.k + base + 8 * lr, dst + q * 1024);
+  else dma16(kv.k + base + 8 * rm_chunk(lane), dst + q * 1024);
 }
 
 // Eight 1 KiB pieces of a tile (loads q0 .. q0+7) into registers, with their wait.
@@ -133,9 +133,12 @@ struct DqRows {
 // already read; the V and transposed-K pieces are read from the slot at `src`.  dS enters the product
 // as a bf16 pair hi + lo (lo the rounded remainder): where a row's weight concentrates, dS terms of
 // both signs nearly cancel in dQ and a single bf16 rounding of dS would dominate the result's error.
+// ktr_off: this lane's read_vt_tr offsets of the tile's row-major K (16 KiB + tr_lane_off); dQ^T
+// register r of d-tile dt then holds d = 32*(lane/16) + 4*dt + r.
 template <class PosFn>
 __device__ inline void dq_tile_step(f32x4 (&acc)[2][8], const DqRows& rw, const u32x4 (&kreg)[8], uint32_t src,
-                                    int lane, float scale_log2, bool dirty, PosFn pos_of) {
+                                    const uint32_t (&ktr_off)[4], int lane, float scale_log2, bool dirty,
+                                    PosFn pos_of) {
   f32x4 p[2][2];
 #pragma unroll
   for (int sub = 0; sub < 2; ++sub)
@@ -191,11 +194,14 @@ __device__ inline void dq_tile_step(f32x4 (&acc)[2][8], const DqRows& rw, const 
     dslo[nt] = as_bf16x8(wl);
   }
 
-  u32x4 kt[8];
-  read8(kt, src + 16 * 1024 + 16 * lane);
+  bf16x8 kts[8];
+  {
+    const uint32_t a4[4] = {src + ktr_off[0], src + ktr_off[1], src + ktr_off[2], src + ktr_off[3]};
+    read_vt_tr(kts, a4);
+  }
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) {
-    const bf16x8 a = vt_operand(kt, dt);
+    const bf16x8 a = kts[dt];
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
       acc[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, dsop[nt], acc[nt][dt], 0, 0, 0);
@@ -304,6 +310,9 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
   const int q0 = 3 * wave;
   const int rit0 = load_row_in_tile(q0, lane), rit1 = load_row_in_tile(q0 + 1, lane),
             rit2 = load_row_in_tile(q0 + 2, lane);
+  uint32_t ktr_off[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) ktr_off[j] = 16384u + tr_lane_off(lane, j);
   const uint32_t roff_lds = lds_addr(sm.roff), tpos_lds = lds_addr(sm.tpos);
   const uint32_t ring_lds = lds_addr(sm.ring[0]);
   auto issue = [&](int tile, const uint32_t (&r)[3]) {
@@ -349,7 +358,8 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
       const bool dirty = __builtin_amdgcn_ballot_w64(bad) != 0;
       issue(nxt, r);
       if (has_rows)
-        dq_tile_step(acc, rw, kreg, src, lane, p.scale_log2, dirty, [&](int i) { return (int)tp[i >> 2][i & 3]; });
+        dq_tile_step(acc, rw, kreg, src, ktr_off, lane, p.scale_log2, dirty,
+                     [&](int i) { return (int)tp[i >> 2][i & 3]; });
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the ring is reused
   };
@@ -376,19 +386,14 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
     stream(e0, e1);
   }
 
-  // ---- dQ rows 16*nt + lane%16; register i of d-tile dt holds d = 32*(lane/16) + 8*i + dt
+  // ---- dQ rows 16*nt + lane%16; register r of d-tile dt holds d = 32*(lane/16) + 4*dt + r
   auto write_rows = [&](const f32x4 (&o)[2][8]) {
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
       if (!rvalid[nt]) continue;
       float* drow = p.dq + orow[nt] * kD + 32 * lg;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        *reinterpret_cast<f32x4*>(drow + 8 * i) =
-            f32x4{o[nt][0][i], o[nt][1][i], o[nt][2][i], o[nt][3][i]} * p.scale;
-        *reinterpret_cast<f32x4*>(drow + 8 * i + 4) =
-            f32x4{o[nt][4][i], o[nt][5][i], o[nt][6][i], o[nt][7][i]} * p.scale;
-      }
+      for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<f32x4*>(drow + 4 * dt) = o[nt][dt] * p.scale;
     }
   };
   if (p.nW == 1) {
@@ -446,12 +451,11 @@ __global__ __launch_bounds__(kWave) void dq_merge_kernel(AttnBwdParams p) {
       for (int i = 0; i < 4; ++i) o[i] += x[kk][i];
   }
   if (n >= p.R) return;
-  // register r of d-tile dt = 4*dh + i holds d = 32*lg + 8*r + dt
+  // register r of d-tile dt = 4*dh + i holds d = 32*lg + 4*dt + r
   const int j = n / p.G, h = g * p.G + n % p.G;
-  float* drow = p.dq + (((int64_t)s * p.C + j) * p.Hq + h) * kD + 32 * lg + 4 * dh;
+  float* drow = p.dq + (((int64_t)s * p.C + j) * p.Hq + h) * kD + 32 * lg + 16 * dh;
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
-    *reinterpret_cast<f32x4*>(drow + 8 * r) = f32x4{o[0][r], o[1][r], o[2][r], o[3][r]} * p.scale;
+  for (int i = 0; i < 4; ++i) *reinterpret_cast<f32x4*>(drow + 4 * i) = o[i] * p.scale;
 }
 
 // ---- dK/dV kernel ---------------------------------------------------------------
