@@ -41,7 +41,12 @@ constexpr int kStatRows = 128;                   // stats record stride (rows)
 constexpr int kTargetBlocks = 256;               // one workgroup per CU
 constexpr int kTopkThreads = 1024;
 constexpr int kMaxPerThread = BD_SELECT_MAX_PREFIX / kTopkThreads;   // 32
-constexpr int kRadixBins0 = 4096;               // bins of the first radix digit (12 bits)
+constexpr int kHistWords = 4096;                // radix histogram words: bins x copies of each digit
+// Radix digits of the top-B keys, most significant first (bits, lowest bit, histogram copies).
+constexpr int kDigits = 3;
+__device__ inline int digit_bits(int i) { return i == 0 ? 8 : (i == 1 ? 11 : 12); }
+__device__ inline int digit_shift(int i) { return i == 0 ? 23 : (i == 1 ? 12 : 0); }
+__device__ inline int digit_copies(int i) { return i == 0 ? 16 : (i == 1 ? 2 : 1); }
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kSlack = 8.f;                    // lazy-rescale headroom of the pass-1 sums, log2 units
 
@@ -354,45 +359,48 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
 
 // ---- top-B -------------------------------------------------------------------
 
-__device__ inline int block_exclusive_scan(int x, int* wsum, int& total) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  constexpr int kW = kTopkThreads / kWave;
-  int v = x;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int y = __shfl_up(v, o);
-    if (lane >= o) v += y;
-  }
-  if (lane == kWave - 1) wsum[wave] = v;
-  __syncthreads();
-  if (wave == 0) {
-    int w = lane < kW ? wsum[lane] : 0;
-#pragma unroll
-    for (int o = 1; o < kW; o <<= 1) {
-      const int y = __shfl_up(w, o);
-      if (lane >= o) w += y;
-    }
-    if (lane < kW) wsum[lane] = w;
-  }
-  __syncthreads();
-  const int before = (wave > 0 ? wsum[wave - 1] : 0) + v - x;
-  total = wsum[kW - 1];
-  __syncthreads();
-  return before;
+// Inclusive prefix sum over the 64 lanes of a wave with DPP moves (no LDS round trips): shifts by
+// 1, 2, 4 and 8 lanes within each row of 16 (lanes without a source add 0), then rows 1 and 3 add
+// lane 15 of the row below and rows 2 and 3 add lane 31.
+__device__ inline uint32_t wave_inclusive_scan(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);   // row_shr:1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);   // row_shr:2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);   // row_shr:4
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);   // row_shr:8
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);   // row_bcast:15
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);   // row_bcast:31
+  return v;
 }
 
-// Add one to bin `d` of the histogram.  When every active lane of the wave holds the same digit
-// (the common case for the leading digits, which the scores mostly share) one lane adds the count,
-// so the LDS atomics do not serialise on a single bin.
-__device__ inline void hist_add(uint32_t* hist, uint32_t d) {
+// Exclusive prefix sum of x over the workgroup's threads in thread order; total = the sum of all.
+// Every wave scans the wave totals itself, so one barrier separates the two levels; the last one
+// lets the next call reuse wsum.
+__device__ inline uint32_t block_exclusive_scan(uint32_t x, uint32_t* wsum, uint32_t& total) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int kW = kTopkThreads / kWave;
+  const uint32_t v = wave_inclusive_scan(x);
+  if (lane == kWave - 1) wsum[wave] = v;
+  __syncthreads();
+  const uint32_t ws = wave_inclusive_scan(lane < kW ? wsum[lane] : 0u);
+  const uint32_t below = wave > 0 ? (uint32_t)__builtin_amdgcn_readlane((int)ws, wave - 1) : 0u;
+  total = (uint32_t)__builtin_amdgcn_readlane((int)ws, kW - 1);
+  __syncthreads();
+  return below + v - x;
+}
+
+// Add one to bin `d` of a histogram held in `stride` copies (bin d's copy c at d*stride + c; this
+// lane adds to copy `copy`).  When every active lane of the wave holds the same digit one lane adds
+// the count to copy 0.  Otherwise each lane adds one: an LDS atomic serialises the lanes that meet
+// on one word, and the copies spread lanes with equal digits over `stride` words.
+__device__ inline void hist_add(uint32_t* hist, uint32_t d, uint32_t stride, uint32_t copy) {
   const uint64_t active = __builtin_amdgcn_read_exec();
   const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
   const uint64_t same = __builtin_amdgcn_ballot_w64(d == d0);
   if (same == active) {
     if ((uint32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(active >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)active, 0u)) == 0u)
-      atomicAdd(&hist[d0], (uint32_t)__builtin_popcountll(active));
+      atomicAdd(&hist[d0 * stride], (uint32_t)__builtin_popcountll(active));
   } else {
-    atomicAdd(&hist[d], 1u);
+    atomicAdd(&hist[d * stride + copy], 1u);
   }
 }
 
@@ -401,16 +409,22 @@ struct IntTag { static constexpr int value = V; };
 
 // Code size matters here: every wave runs each phase once, so a fully unrolled kernel is bound
 // by instruction fetch (75 KB of straight-line code measured 39 us).  Only the pooling keeps its
-// candidates in registers; it stores them in LDS, striped (candidate e of thread t at
-// e*kTopkThreads + t, conflict-free), and every later phase is a short loop over them.
+// candidates in registers; it stores them in LDS and every later phase is a short loop over them.
+// One workgroup runs the whole (sequence, KV head), so the phases are bound by the CU's own LDS and
+// VALU throughput: candidate c belongs to thread c % kTopkThreads (slot e = c / kTopkThreads), so
+// a wave's lanes hold consecutive candidates: pooling reads consecutive LDS words (no bank
+// conflicts), the keys sit at keys[c], and the ordered compaction ranks candidates by ballots.
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
   constexpr int kTopkWaves = kTopkThreads / kWave;
-  __shared__ float raw_lds[BD_SELECT_MAX_PREFIX];     // the pooled range, staged once; then the keys
-  __shared__ uint32_t hist[kRadixBins0];
-  __shared__ int wsum[kTopkWaves];
+  constexpr int kPad = 4;                              // -1 words on either side of the staged range
+  constexpr int kCells = kMaxPerThread * kTopkWaves;   // (slot, wave) cells of the compaction
+  static_assert(2 * kCells <= kHistWords, "compaction counts live in the histogram's space");
+  __shared__ float raw_lds[BD_SELECT_MAX_PREFIX + 2 * kPad];   // the pooled range, staged once; then the keys
+  __shared__ __align__(16) uint32_t hist[kHistWords];
+  __shared__ uint32_t wsum[kTopkWaves];
   __shared__ uint32_t s_digit, s_krem;
   uint32_t* keys = reinterpret_cast<uint32_t*>(raw_lds);
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int pair = blockIdx.x;
   const int g = pair % p.Hkv, s = pair / p.Hkv;
   const int L = seq_len(p.kv, s);
@@ -424,8 +438,9 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
   }
   if (g == 0 && tid == 0) p.nsel_out[s] = B;
 
-  // 1. total raw scores (row blocks summed in order), staged in LDS over the prefix [0, N) and
-  // exported when the caller asked for them; each batch of loads is issued before any is summed
+  // 1. total raw scores (row blocks summed in order), staged in LDS over the prefix [0, N) at
+  // raw_lds[kPad + t] and exported when the caller asked for them; each batch of loads is issued
+  // before any is summed
   const int N = L - W, K = B - W, rad = p.pool_kernel / 2;
   float* raw = p.raw ? p.raw + (int64_t)pair * p.max_L : nullptr;
   const float* part = p.raw_part + (int64_t)pair * p.n_rb * p.max_L;
@@ -447,95 +462,141 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
 #pragma unroll
     for (int e = 0; e < kStageBatch; ++e) {
       const int t = c0 + tid + e * kTopkThreads;
-      if (t < N) raw_lds[t] = v[e];
+      if (t < N) raw_lds[kPad + t] = v[e];
       if (raw && t < L) raw[t] = v[e];
     }
   }
+  if (tid < kPad) { raw_lds[tid] = -1.f; raw_lds[kPad + N + tid] = -1.f; }
   __syncthreads();
 
   // 2. the candidates: prefix positions [0, N) with max-pooled scores (token level), or the chunks
   // of s positions of the prefix with their scores' sums (TopKChunks, chunk c covering
-  // [c*s, min((c+1)*s, N)), summed left to right in fp32).  This thread owns candidates
-  // [t0, t0 + E); the top KE of the M candidates are kept.  Scores are >= 0, so their float bits
-  // order like their values.
+  // [c*s, min((c+1)*s, N)), summed left to right in fp32).  The top KE of the M candidates are
+  // kept.  Scores are >= 0, so their float bits order like their values.
   const int chunk = p.chunk;
   const int M = chunk > 0 ? (N + chunk - 1) / chunk : N;
   int KE = chunk > 0 ? K / chunk : K;
   if (KE > M) KE = M;
-  const int E = (M + kTopkThreads - 1) / kTopkThreads;
-  const int t0 = tid * E;
+  const int E = (M + kTopkThreads - 1) / kTopkThreads;   // slots in use
+  const float* rl = raw_lds + kPad;
   uint32_t key[kMaxPerThread];
-  auto raw_at = [&](int t) { return t >= 0 && t < N ? raw_lds[t] : -1.f; };
   if (chunk > 0) {
 #pragma unroll
     for (int e = 0; e < kMaxPerThread; ++e) {
-      const int c = t0 + e;
+      const int c = e * kTopkThreads + tid;
       float sum = 0.f;
       if (e < E && c < M) {
         const int b = c * chunk, n = N - b < chunk ? N - b : chunk;
-        for (int j = 0; j < n; ++j) sum += raw_lds[b + j];
+        for (int j = 0; j < n; ++j) sum += rl[b + j];
       }
       key[e] = e < E && c < M ? __float_as_uint(sum) : 0u;
     }
-  } else if (rad <= 3) {
-    // radius <= 3: the thread's window of raw values in registers (every load issued before any
-    // max), one code path for every such radius (maxima past the radius are masked)
-    float w[kMaxPerThread + 6];
+  } else if (rad <= kPad - 1) {
+    // radius <= 3: the -1 words around the range stand in for positions outside it (every
+    // pooled score is >= 0), so no bounds checks.  Groups of 8 slots, all reads of a group issued
+    // together; a slot past E reads words inside the array and is masked.
+    auto pool = [&](auto rtag) {
+      constexpr int R = decltype(rtag)::value;
 #pragma unroll
-    for (int i = 0; i < kMaxPerThread + 6; ++i) w[i] = i < E + 6 ? raw_at(t0 - 3 + i) : -1.f;
+      for (int e0 = 0; e0 < kMaxPerThread; e0 += 8) {
+        if (e0 < E) {
 #pragma unroll
-    for (int e = 0; e < kMaxPerThread; ++e) {
-      float m = w[e + 3];
+          for (int j = 0; j < 8; ++j) {
+            const int e = e0 + j, c = e * kTopkThreads + tid;
+            float m = rl[c];
 #pragma unroll
-      for (int d = 1; d <= 3; ++d) m = fmaxf(m, d <= rad ? fmaxf(w[e + 3 - d], w[e + 3 + d]) : -1.f);
-      key[e] = e < E && t0 + e < N ? __float_as_uint(m) : 0u;   // m >= 0: bits order like values
-    }
+            for (int d = 1; d <= R; ++d) m = fmaxf(m, fmaxf(rl[c - d], rl[c + d]));
+            key[e] = e < E && c < N ? __float_as_uint(m) : 0u;
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) key[e0 + j] = 0u;
+        }
+      }
+    };
+    if (rad == 3) pool(IntTag<3>{});
+    else if (rad == 2) pool(IntTag<2>{});
+    else if (rad == 1) pool(IntTag<1>{});
+    else pool(IntTag<0>{});
   } else {
+    auto raw_at = [&](int t) { return t >= 0 && t < N ? rl[t] : -1.f; };
     float m[kMaxPerThread];
 #pragma unroll
     for (int e = 0; e < kMaxPerThread; ++e) m[e] = -1.f;
     for (int d = -rad; d <= rad; ++d) {
 #pragma unroll
       for (int e = 0; e < kMaxPerThread; ++e)
-        if (e < E) m[e] = fmaxf(m[e], raw_at(t0 + e + d));
+        if (e < E) m[e] = fmaxf(m[e], raw_at(e * kTopkThreads + tid + d));
     }
 #pragma unroll
-    for (int e = 0; e < kMaxPerThread; ++e) key[e] = e < E && t0 + e < N ? __float_as_uint(m[e]) : 0u;
+    for (int e = 0; e < kMaxPerThread; ++e)
+      key[e] = e < E && e * kTopkThreads + tid < N ? __float_as_uint(m[e]) : 0u;
   }
   __syncthreads();                            // every raw value read: the LDS now holds the keys
 #pragma unroll
   for (int e = 0; e < kMaxPerThread; ++e)
     if (e < E) keys[e * kTopkThreads + tid] = key[e];
   __syncthreads();
-  auto key_at = [&](int e) { return keys[e * kTopkThreads + tid]; };
+  // Keys in batches of kBatch slots, every read issued before the first is used (an LDS atomic or a
+  // ballot between a read and the next would otherwise wait for the LDS round trip each slot).
+  // Slots past E read slot E-1 again: the caller's c < M test rejects them.
+  constexpr int kBatch = 8;
+  auto load_keys = [&](uint32_t (&k)[kBatch], int e0) {
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) k[j] = keys[(e0 + j < E ? e0 + j : E - 1) * kTopkThreads + tid];
+  };
 
-  // 3. radix select of the KE-th largest key over digits of 12, 10 and 10 bits; krem = how many keys
-  // equal to it are taken.  A 12-bit first digit (sign, exponent, 3 mantissa bits) spreads each
-  // binade over 8 bins: with 8 bits the scores' few exponents piled thousands of LDS atomics onto a
-  // handful of bins.
+  // 3. radix select of the KE-th largest key over digits of 8, 11 and 12 bits: the exponent, then
+  // the mantissa's top 11 and low 12 bits (the sign bit is always clear); krem = how many keys
+  // equal to it are taken.  Most scores share a few exponents and their neighbours share leading
+  // mantissa bits, so lane l adds to copy l % 16 (exponent) or l % 2 (top mantissa bits) of the
+  // histogram: with one copy of a 12-bit first digit about 18 lanes of a wave met on one word and
+  // the serialised atomics took 5 us of the kernel.
   uint32_t prefix = 0, pmask = 0, krem = (uint32_t)KE;
   if (KE > 0) {
-    for (int pass = 0; pass < 3; ++pass) {
-      const int bits = pass == 0 ? 12 : 10, shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
+    for (int pass = 0; pass < kDigits; ++pass) {
+      const int bits = digit_bits(pass), shift = digit_shift(pass);
+      const uint32_t ncopy = (uint32_t)digit_copies(pass);
+      const uint32_t copy = (uint32_t)lane & (ncopy - 1u);
       const uint32_t nb = 1u << bits, dm = nb - 1;
-      for (int i = tid; i < (int)nb; i += kTopkThreads) hist[i] = 0;
+      for (int i = tid; i < (int)(nb * ncopy); i += kTopkThreads) hist[i] = 0;
       __syncthreads();
-#pragma unroll 4
-      for (int e = 0; e < E; ++e) {
-        const uint32_t k = key_at(e);
-        if (t0 + e < M && (k & pmask) == prefix) hist_add(hist, (k >> shift) & dm);
+      for (int e0 = 0; e0 < E; e0 += kBatch) {
+        uint32_t k[kBatch];
+        load_keys(k, e0);
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j)
+          if ((e0 + j) * kTopkThreads + tid < M && (k[j] & pmask) == prefix)
+            hist_add(hist, (k[j] >> shift) & dm, ncopy, copy);
       }
       __syncthreads();
       // thread tid owns digits nb-1 - (per*tid + q): a block scan counts the keys above them
-      const int per = (int)nb / kTopkThreads;
-      uint32_t c = 0;
-      for (int q = 0; q < per; ++q) c += hist[nb - 1 - (per * tid + q)];
-      int tot;
-      uint32_t a = (uint32_t)block_exclusive_scan((int)c, wsum, tot);
-      for (int q = 0; q < per; ++q) {
-        const uint32_t h = hist[nb - 1 - (per * tid + q)];
-        if (a < krem && krem <= a + h) { s_digit = nb - 1 - (uint32_t)(per * tid + q); s_krem = krem - a; }
-        a += h;
+      constexpr int kMaxPer = kHistWords / kTopkThreads;
+      const int per = (int)nb >= kTopkThreads ? (int)nb / kTopkThreads : 1;
+      uint32_t h[kMaxPer], c = 0;
+#pragma unroll
+      for (int q = 0; q < kMaxPer; ++q) {
+        const uint32_t x = (uint32_t)(per * tid + q), d = nb - 1 - x;
+        h[q] = 0;
+        if (q < per && x < nb) {
+          if (ncopy >= 4) {
+            const uint4* w = reinterpret_cast<const uint4*>(hist + d * ncopy);
+            for (uint32_t i = 0; i < ncopy / 4; ++i) { const uint4 v = w[i]; h[q] += v.x + v.y + v.z + v.w; }
+          } else if (ncopy == 2) {
+            const uint2 v = *reinterpret_cast<const uint2*>(hist + d * 2);
+            h[q] = v.x + v.y;
+          } else {
+            h[q] = hist[d];
+          }
+        }
+        c += h[q];
+      }
+      uint32_t tot;
+      uint32_t a = block_exclusive_scan(c, wsum, tot);
+#pragma unroll
+      for (int q = 0; q < kMaxPer; ++q) {
+        if (q < per && a < krem && krem <= a + h[q]) { s_digit = nb - 1 - (uint32_t)(per * tid + q); s_krem = krem - a; }
+        a += h[q];
       }
       __syncthreads();
       prefix |= s_digit << shift;
@@ -545,46 +606,83 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
     }
   }
 
-  // 4. ordered compaction: all candidates above the threshold, the first krem equal to it; a
-  // candidate contributes its positions (one, or its chunk's), in ascending order
-  auto positions = [&](int c) {
-    if (chunk == 0) return 1;
-    const int b = c * chunk;
-    return N - b < chunk ? N - b : chunk;
-  };
-  const int Ev = KE > 0 ? (M - t0 < E ? (M - t0 > 0 ? M - t0 : 0) : E) : 0;   // this thread's candidates
-  int eq = 0;
-#pragma unroll 4
-  for (int e = 0; e < Ev; ++e) eq += key_at(e) == prefix;
-  int tot;
-  const int eq_before = block_exclusive_scan(eq, wsum, tot);
-  int take_eq = (int)krem - eq_before;
-  take_eq = take_eq < 0 ? 0 : (take_eq > eq ? eq : take_eq);
-  int mine = 0, seen = 0;
-#pragma unroll 4
-  for (int e = 0; e < Ev; ++e) {
-    const uint32_t k = key_at(e);
-    const bool isq = k == prefix;
-    if (k > prefix || (isq && seen < take_eq)) mine += positions(t0 + e);
-    seen += isq;
-  }
-  int kept;                                   // prefix positions kept: K (token level), <= K (chunks)
-  int off = block_exclusive_scan(mine, wsum, kept);
-  seen = 0;
-  for (int e = 0; e < Ev; ++e) {
-    const int c = t0 + e;
-    const uint32_t k = key_at(e);
-    const bool isq = k == prefix;
-    if (k > prefix || (isq && seen < take_eq)) {
-      const int n = positions(c), b = chunk > 0 ? c * chunk : c;
-      for (int j = 0; j < n; ++j, ++off)
-        if (off < K) idx_row[off] = b + j;    // guard: never write past the B - W prefix slots
+  // 4. ordered compaction: all candidates above the threshold, the first krem equal to it, in
+  // ascending order.  Cell (e, wave) holds candidates e*kTopkThreads + 64*wave + [0, 64): ballots
+  // count each cell's keys above and equal to the threshold, two scans over the cells in candidate
+  // order give each cell its first equal key's rank and its first output slot, and a lane adds the
+  // ballot's lanes below it.  A candidate contributes its positions (one, or its chunk's: every
+  // chunk but the last has s of them, so a taken candidate's first slot is its rank times s).
+  uint32_t* c_eq = hist;                      // per cell: equal keys, then equal keys before it
+  uint32_t* c_gt = hist + kCells;             // per cell: keys above, then output slots before it
+  const uint64_t below = (1ull << lane) - 1ull;
+  const bool any = KE > 0;
+  for (int e0 = 0; e0 < E; e0 += kBatch) {
+    uint32_t k[kBatch];
+    load_keys(k, e0);
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int e = e0 + j, c = e * kTopkThreads + tid;
+      const uint64_t beq = __builtin_amdgcn_ballot_w64(any && c < M && k[j] == prefix);
+      const uint64_t bgt = __builtin_amdgcn_ballot_w64(any && c < M && k[j] > prefix);
+      if (lane == 0 && e < E) {
+        c_eq[e * kTopkWaves + wave] = (uint32_t)__builtin_popcountll(beq);
+        c_gt[e * kTopkWaves + wave] = (uint32_t)__builtin_popcountll(bgt);
+      }
     }
-    seen += isq;
+  }
+  __syncthreads();
+  const int ncell = E * kTopkWaves;
+  const uint32_t n_eq = tid < ncell ? c_eq[tid] : 0u, n_gt = tid < ncell ? c_gt[tid] : 0u;
+  // One scan of both counts packed as equal << 16 | above (each sum is at most 32768).  The equal
+  // keys are taken in candidate order until krem of them are, so min(krem, equal keys before) of
+  // them lie in earlier cells.
+  uint32_t tot;
+  const uint32_t before = block_exclusive_scan(n_eq << 16 | n_gt, wsum, tot);
+  const uint32_t eq_before = before >> 16, take_before = (before & 0xFFFFu) + min(krem, eq_before);
+  const int taken = (int)((tot & 0xFFFFu) + min(krem, tot >> 16));   // candidates kept
+  // Prefix positions kept: unit per taken candidate, less the missing positions of a short last
+  // chunk when it is taken (all other equal keys precede it, so an equal last key is taken only
+  // when every equal key is).  The window and the unused slots are written first.
+  const int unit = chunk > 0 ? chunk : 1;
+  int kept = taken * unit;
+  if (chunk > 0 && M > 0) {
+    const uint32_t kl = keys[M - 1];
+    if (any && (kl > prefix || (kl == prefix && krem == tot >> 16))) kept -= unit - (N - (M - 1) * chunk);
   }
   if (kept > K) kept = K;
   for (int i = tid; i < W; i += kTopkThreads) idx_row[kept + i] = N + i;
   for (int i = kept + W + tid; i < B; i += kTopkThreads) idx_row[i] = -1;   // chunk mode: unused slots
+  if (tid < ncell) { c_eq[tid] = eq_before; c_gt[tid] = take_before; }
+  __syncthreads();
+  for (int e0 = 0; e0 < E; e0 += kBatch) {
+    uint32_t k[kBatch], eqb[kBatch], tkb[kBatch];
+    load_keys(k, e0);
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int cell = (e0 + j < E ? e0 + j : E - 1) * kTopkWaves + wave;
+      eqb[j] = c_eq[cell];
+      tkb[j] = c_gt[cell];
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int c = (e0 + j) * kTopkThreads + tid;
+      const bool isq = any && c < M && k[j] == prefix;
+      const uint64_t beq = __builtin_amdgcn_ballot_w64(isq);
+      const bool take = (any && c < M && k[j] > prefix) ||
+                        (isq && eqb[j] + (uint32_t)__builtin_popcountll(beq & below) < krem);
+      const uint64_t bt = __builtin_amdgcn_ballot_w64(take);
+      if (take) {
+        const int off = ((int)tkb[j] + __builtin_popcountll(bt & below)) * unit;
+        if (chunk == 0) {
+          if (off < K) idx_row[off] = c;      // guard: never write past the B - W prefix slots
+        } else {
+          const int b = c * chunk, n = N - b < chunk ? N - b : chunk;
+          for (int i = 0; i < n; ++i)
+            if (off + i < K) idx_row[off + i] = b + i;
+        }
+      }
+    }
+  }
 }
 
 template <int NT, bool PAGED>

@@ -90,6 +90,18 @@ def test_select_pool_kernels(pool_kernel):
     assert near <= 1
 
 
+def test_select_longest_prefix():
+    # L - W = BD_SELECT_MAX_PREFIX = 32768 prefix positions: every candidate slot of the top-B kernel
+    # (32 per thread) and both ends of its staged range, beside a shorter sequence
+    Hkv, Hq, W = 1, 4, 32
+    lens = [32768 + W, 20000]
+    g = np.random.default_rng(8)
+    k = synth.f32_to_bf16_bits(g.standard_normal((2, Hkv, max(lens), 128)).astype(np.float32))
+    q = synth.f32_to_bf16_bits(g.standard_normal((2, W, Hq, 128)).astype(np.float32))
+    near = _check(k, q, lens, Hq, W, 2048, "prefix 32768")
+    assert near <= 1
+
+
 def test_select_zero_keys_exact_and_identity():
     S, Hkv, Hq, L, W = 2, 2, 8, 700, 16
     q = synth.f32_to_bf16_bits(np.random.default_rng(1).standard_normal((S, W, Hq, 128)).astype(np.float32))

@@ -98,6 +98,27 @@ def test_select_chunks_ragged_lengths_and_sizes(s):
     assert near <= 1
 
 
+@pytest.mark.parametrize("s", [5, 16])
+def test_select_chunks_short_last_chunk_taken(s):
+    # the prefix's last chunk is short and holds a key aligned with every query: it is kept, and the
+    # window follows its last position directly (the kept count is not a multiple of s)
+    S, Hkv, Hq, W, L, B = 2, 2, 8, 32, 1000, 200
+    N = L - W
+    assert N % s != 0
+    g = np.random.default_rng(24 + s)
+    kf = g.standard_normal((S, Hkv, L, 128)).astype(np.float32)
+    qf = g.standard_normal((S, W, Hq, 128)).astype(np.float32)
+    kf[:, :, N - 1] = 100.0 * qf.mean(axis=(1, 2))[:, None, :] / np.linalg.norm(qf.mean(axis=(1, 2)), axis=-1)[:, None, None]
+    k, q = synth.f32_to_bf16_bits(kf), synth.f32_to_bf16_bits(qf)
+    gi, _ = _check(k, q, [L, L], Hq, W, B, s, f"short last chunk s={s}")
+    last = (N - 1) // s
+    for si in range(S):
+        for h in range(Hkv):
+            row = gi[si, h].tolist()
+            assert last in _kept_chunks(row, N, s), (si, h)
+            assert row[row.index(N - 1) + 1] == N, (si, h)    # the window follows the short chunk
+
+
 def test_select_chunks_zero_keys_exact_and_decode_skips_unused_slots():
     S, Hkv, Hq, L, W = 1, 2, 8, 700, 16
     g = np.random.default_rng(22)
