@@ -26,19 +26,20 @@
 //   dP^T [key][row] = V . dO^T         A = V tile,  B = dO^T  (registers)
 //   dQ^T [d][row]  += K^T . dS^T       A = K^T,     B = dS^T  (P, dS never leave registers)
 // dQ sums over the branches, so one accumulator serves the whole range.  Each
-// workgroup's partial goes to a record; the last workgroup of the unit adds
-// them in workgroup order, so the result does not depend on scheduling.  The
+// workgroup's partial goes to a record; a merge kernel adds a unit's records
+// in workgroup order, so the result does not depend on scheduling.  The
 // workgroup holding a branch's first entry also publishes each row's (lse, D)
 // for dK/dV.
 //
-// dK/dV kernel.  One workgroup of 4 waves per (sequence, KV head, branch);
-// wave w owns 16 block keys, and the branch's query rows stream through a
-// direct-to-LDS ring in 32-row tiles (Q and dO, each in the A-operand and the
-// transposed layout).  Per tile a wave runs
+// dK/dV kernel.  One workgroup of 8 waves per (sequence, KV head, branch), two
+// groups of 4 taking alternate row tiles; wave w of a group owns 16 block
+// keys, and the branch's query rows stream through a direct-to-LDS ring in
+// 32-row tiles (Q and dO, each in the A-operand and the transposed layout).
+// Per tile a wave runs
 //   S  [row][key] = Q . K_blk^T        dP [row][key] = dO . V_blk^T
 //   dV^T [d][key] += dO^T . P          dK^T [d][key] += Q^T . dS
 // (P and dS as bf16 pairs hi + lo).  The branches' partials meet in records
-// summed in branch order by the last workgroup of the (sequence, KV head).
+// that a merge kernel sums in branch order.
 
 #include "bd_common.hpp"
 #include "bd_kernels.hpp"
@@ -459,13 +460,17 @@ __global__ __launch_bounds__(kWave) void dq_merge_kernel(AttnBwdParams p) {
 }
 
 // ---- dK/dV kernel ---------------------------------------------------------------
-// One workgroup of 4 waves per (sequence, KV head, branch); wave w owns the 16 block keys of key
-// tile w (tiles w+4, w+8, ... in later passes).  The branch's query rows stream through an LDS ring
-// in 32-row tiles, each tile carrying Q and dO twice: in the A-operand layout of the S and dP
-// products and in the transposed layout of the dK and dV products, so every LDS read is linear.
-constexpr int kKWaves = 4;
+// One workgroup of 8 waves per (sequence, KV head, branch) in two groups of 4: wave w of a group
+// owns the 16 block keys of key tile w (tiles w+4, w+8, ... in later passes), group 0 takes the
+// even 32-row tiles of the branch's query rows and group 1 the odd ones, and the groups' partial
+// sums are added in LDS at the end (two waves per SIMD: one wave's MFMA chains and LDS reads
+// overlap the other's).  The row tiles stream through an LDS ring, each tile carrying Q and dO
+// twice: in the A-operand layout of the S and dP products and in the transposed layout of the dK
+// and dV products, so every LDS read is linear.
+constexpr int kKGroupWaves = 4;
+constexpr int kKWaves = 2 * kKGroupWaves;
 constexpr int kKThreads = kKWaves * kWave;
-constexpr int kKRing = 3;                          // row-tile slots; kKRing-1 tiles in flight
+constexpr int kKRing = 4;                          // row-tile slots: two per group, one in flight
 constexpr int kKLoads = 32;                        // 1 KiB pieces per row tile (8 per wave)
 constexpr int kKStatBytes = 32 * 8;                // the tile's rows' (lse2, D) pairs (64 bytes per wave)
 constexpr int kKTileBytes = kKLoads * 1024 + kKStatBytes;
@@ -473,7 +478,6 @@ constexpr int kKTileBytes = kKLoads * 1024 + kKStatBytes;
 struct DkvSmem {
   alignas(16) uint8_t ring[kKRing][kKTileBytes];
   int32_t cnt[kMaxBwdBlock];                       // occurrences of block key c in the branch's key list
-  int32_t last;
 };
 
 // Piece q (0..31) of a row tile for this lane: 0..7 Q in the A layout (rows 16*(q/4) + lane%16,
@@ -490,6 +494,7 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
   __shared__ DkvSmem sm;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave / kKGroupWaves, wk = wave % kKGroupWaves;
   const int lg = lane >> 4, lr = lane & 15;
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
   const int br = bid % p.nbr;
@@ -532,31 +537,35 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
     const int j = div_small(nn, p.G, p.inv_G);
     return ((int64_t)s * C + j) * p.Hq + g * p.G + (nn - j * p.G);
   };
-  // this wave's 8 pieces of every row tile
+  // this wave's 8 pieces of its group's row tiles
   int prow[8], pd[8];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) row_piece(8 * wave + k, lane, prow[k], pd[k]);
-  const uint16_t* psrc = wave < 2 ? p.q : doutb;
+  for (int k = 0; k < 8; ++k) row_piece(8 * wk + k, lane, prow[k], pd[k]);
+  const uint16_t* psrc = wk < 2 ? p.q : doutb;
+  // step i: group g works on row tile 2i + g in ring slot g + 2*(i % 2)
+  const int nit = (nrt + 1) / 2;
+  auto slot_of = [&](int i) { return grp + 2 * (i & 1); };
   // 9 loads per wave and tile: its 8 pieces, and 64 bytes of the tile's row stats (lanes 0..3)
-  auto issue = [&](int rt) {
-    uint8_t* dst = sm.ring[rt % kKRing];
+  auto issue = [&](int i) {
+    const int rt = 2 * i + grp;
+    uint8_t* dst = sm.ring[slot_of(i)];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      const int n = rt < nrt ? 32 * rt + prow[k] : 0;   // padding tiles re-read row 0
-      dma16(psrc + row_off(n) * kD + pd[k], dst + (8 * wave + k) * 1024);
+      const int n = rt < nrt ? 32 * rt + prow[k] : 0;   // a padding tile re-reads row 0
+      dma16(psrc + row_off(n) * kD + pd[k], dst + (8 * wk + k) * 1024);
     }
     const int srt = rt < nrt ? rt : 0;
     if (lane < 4)
-      dma16(reinterpret_cast<const uint16_t*>(stats + srt * 64 + 16 * wave) + 8 * lane,
-            dst + kKLoads * 1024 + 64 * wave);
+      dma16(reinterpret_cast<const uint16_t*>(stats + srt * 64 + 16 * wk) + 8 * lane,
+            dst + kKLoads * 1024 + 64 * wk);
   };
   const uint32_t ring_lds = lds_addr(sm.ring[0]);
   const __amdgpu_buffer_rsrc_t rrec =
       make_rsrc(p.part_kv + (int64_t)pair * p.nbr * C * 2 * kD, (uint32_t)((int64_t)p.nbr * C * 2 * kD * 4));
   const bool direct = p.nbr == 1;
 
-  for (int kt0 = 0; kt0 < nkt; kt0 += kKWaves) {
-    const int kt = kt0 + wave;
+  for (int kt0 = 0; kt0 < nkt; kt0 += kKGroupWaves) {
+    const int kt = kt0 + wk;
     const int c = 16 * kt + lr;                  // this lane's key
     const bool kvalid = kt < nkt && c < C && t0 + c >= 0;
     const int mult = kvalid ? sm.cnt[c] : 0;
@@ -576,16 +585,17 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) dk[dt] = dv[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    __syncthreads();                             // the previous pass's ring reads are done
-    for (int t = 0; t < kKRing - 1; ++t) issue(t);
-    for (int rt = 0; rt < nrt; ++rt) {
-      // this wave's loads of tile rt are older than the kKRing-2 tiles issued after it
-      asm volatile("s_waitcnt vmcnt(9)\n\ts_barrier" ::: "memory");
-      static_assert(9 * (kKRing - 2) == 9, "wait count follows the ring depth");
-      issue(rt + kKRing - 1);
-      const uint32_t slot = ring_lds + (uint32_t)(rt % kKRing) * kKTileBytes;
+    __syncthreads();                             // the previous pass's LDS reads are done
+    issue(0);
+    for (int i = 0; i < nit; ++i) {
+      // step i's tile landed for every wave of the group, and step i-1's slot is free: the next
+      // tile of the group goes there while this one is computed
+      asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+      if (i + 1 < nit) issue(i + 1);
+      const int rt = 2 * i + grp;
+      const uint32_t slot = ring_lds + (uint32_t)slot_of(i) * kKTileBytes;
       const uint32_t src = slot + 16 * lane;
-      if (active) {
+      if (active && rt < nrt) {
         u32x4 qa[8], da[8];
         read8(qa, src);
         read8(da, src + 16 * 1024);
@@ -656,10 +666,27 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
         }
       }
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the ring is reused
+    // group 1 hands its partial sums to group 0 through the ring (16 KiB per wave)
+    __syncthreads();                             // every ring read of the last step is done
+    f32x4* red = reinterpret_cast<f32x4*>(sm.ring[0]) + wk * 16 * kWave + lane;
+    if (grp == 1) {
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        red[dt * kWave] = dk[dt];
+        red[(8 + dt) * kWave] = dv[dt];
+      }
+    }
+    __syncthreads();
+    if (grp == 0) {
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        dk[dt] += red[dt * kWave];
+        dv[dt] += red[(8 + dt) * kWave];
+      }
+    }
 
     // key c: register i of d-tile dt holds d = 32*lg + 8*i + dt; a key listed m times counts m times
-    if (kt < nkt && c < C) {
+    if (grp == 0 && kt < nkt && c < C) {
       const float mk = (float)mult * (direct ? p.scale : 1.f), mv = (float)mult;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -685,52 +712,39 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
       }
     }
   }
-  if (direct) return;
+}
 
-  // ---- the last branch of (s, g) to finish adds the branches' partials in branch order
-  wait_vmem();
-  __syncthreads();
-  uint32_t* ctr = counter_line(p.counters, (int64_t)p.units + pair);
-  if (tid == 0) sm.last = arrive(ctr, (uint32_t)p.nbr);
-  __syncthreads();
-  if (!sm.last) return;
-  if (tid == 0) reset_counter(ctr);
-  // Device-scope loads travel past the XCD's L2, so a round of them costs about a microsecond:
-  // each round issues 4 chunks of up to 8 branches (32 loads) before summing any.
-  const int chunks = C * 2 * kD / 4;             // float4s of one branch record: [C][dK | dV][128]
+// Sum of the branches' dK/dV partials of every (sequence, KV head) in branch order, spread over the
+// chip (the last of a pair's workgroups summing them alone was bound by one CU's bandwidth).  One
+// thread per 16 bytes of a pair's record [C][dK | dV][128]; every load of a batch of 8 branches
+// is issued before any is summed.
+constexpr int kKMThreads = 256;
+__global__ __launch_bounds__(kKMThreads) void dkv_merge_kernel(AttnBwdParams p) {
+  const int chunks = p.C * 2 * kD / 4;           // float4s of one branch record
+  const int per_pair = (chunks + kKMThreads - 1) / kKMThreads;
+  const int pair = blockIdx.x / per_pair;
+  const int q = (blockIdx.x % per_pair) * kKMThreads + threadIdx.x;
+  if (q >= chunks) return;
+  const int g = pair % p.Hkv, s = pair / p.Hkv;
+  const __amdgpu_buffer_rsrc_t rrec =
+      make_rsrc(p.part_kv + (int64_t)pair * p.nbr * p.C * 2 * kD, (uint32_t)((int64_t)p.nbr * p.C * 2 * kD * 4));
   constexpr int kBr = 8;
-  for (int q0 = 0; q0 < chunks; q0 += 4 * kKThreads) {
-    f32x4 sum[4];
+  f32x4 sum = {0.f, 0.f, 0.f, 0.f};
+  for (int b0 = 0; b0 < p.nbr; b0 += kBr) {
+    f32x4 x[kBr];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) sum[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int b0 = 0; b0 < p.nbr; b0 += kBr) {
-      f32x4 x[kBr][4];
+    for (int bb = 0; bb < kBr; ++bb)
+      x[bb] = b0 + bb < p.nbr ? load16_coherent(rrec, (uint32_t)(((int64_t)(b0 + bb) * chunks + q) * 16))
+                              : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int bb = 0; bb < kBr; ++bb)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int q = q0 + tid + u * kKThreads;
-          x[bb][u] = q < chunks && b0 + bb < p.nbr
-                         ? load16_coherent(rrec, (uint32_t)(((int64_t)(b0 + bb) * chunks + q) * 16))
-                         : f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-#pragma unroll
-      for (int bb = 0; bb < kBr; ++bb)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) sum[u] += x[bb][u];   // branch order (absent branches add 0)
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int q = q0 + tid + u * kKThreads;
-      if (q >= chunks) continue;
-      const int fl = 4 * q;
-      const int cc = fl / (2 * kD), rem = fl % (2 * kD);
-      const bool isv = rem >= kD;
-      const int d = isv ? rem - kD : rem;
-      float* dst = (isv ? p.dv : p.dk) + (((int64_t)s * C + cc) * p.Hkv + g) * kD + d;
-      *reinterpret_cast<f32x4*>(dst) = isv ? sum[u] : sum[u] * p.scale;
-    }
+    for (int bb = 0; bb < kBr; ++bb) sum += x[bb];   // branch order (absent branches add 0)
   }
+  const int fl = 4 * q;
+  const int cc = fl / (2 * kD), rem = fl % (2 * kD);
+  const bool isv = rem >= kD;
+  const int d = isv ? rem - kD : rem;
+  float* dst = (isv ? p.dv : p.dk) + (((int64_t)s * p.C + cc) * p.Hkv + g) * kD + d;
+  *reinterpret_cast<f32x4*>(dst) = isv ? sum : sum * p.scale;
 }
 
 }  // namespace
@@ -780,6 +794,11 @@ hipError_t launch_attn_bwd(const AttnBwdParams& p, const AttnBwdPlan& pl, bool p
   if (pl.nblk_kv > 0) {
     if (paged) hipLaunchKernelGGL(dkv_kernel<true>, dim3(pl.nblk_kv), dim3(kKThreads), 0, stream, p);
     else hipLaunchKernelGGL(dkv_kernel<false>, dim3(pl.nblk_kv), dim3(kKThreads), 0, stream, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || pl.nbr == 1) return e;
+    const int64_t per_pair = ((int64_t)p.C * 2 * kD / 4 + kKMThreads - 1) / kKMThreads;
+    const int64_t mblocks = (int64_t)p.S * p.Hkv * per_pair;
+    hipLaunchKernelGGL(dkv_merge_kernel, dim3((unsigned)mblocks), dim3(kKMThreads), 0, stream, p);
     return hipGetLastError();
   }
   return hipSuccess;
