@@ -111,6 +111,16 @@ def test_bwd_small_selected_views_and_full():
     _run(k, v, qb, idx_v, nsel_v, [L, L], "small", seed=1)
 
 
+def test_bwd_block_above_64_rows():
+    """C = 100 with G = 2: 7 key tiles of 16 (two passes over the dK/dV kernel's 4 key tiles per wave
+    group) and 7 row tiles of 32 (an odd count, so the second wave group's last tile is padding)."""
+    S, Hkv, G, L, C = 2, 2, 2, 1200, 100
+    k, v = _rand_bits((S, Hkv, L, 128), 60), _rand_bits((S, Hkv, L, 128), 61)
+    qb = _rand_bits((S, C, Hkv * G, 128), 62)
+    idx_v, nsel_v = _selected_views(k, qb, [L, L], Hkv * G, C, [256, 512])
+    _run(k, v, qb, idx_v, nsel_v, [L, L], "C=100 G=2", seed=6)
+
+
 def test_bwd_ragged_lengths_odd_block_and_group():
     """C = 13 rows with G = 3 (39 rows per head: a ragged 32-row block), ragged L, one L below C."""
     S, Hkv, G, C = 3, 2, 3, 13
