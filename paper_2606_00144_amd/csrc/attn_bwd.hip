@@ -403,7 +403,7 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
   }
 
   // ---- publish this wave's partial as record w of its row block: chunk (nt, dt) x lane float4s;
-  // dq_merge_kernel, launched next on the stream, sums them
+  // bwd_merge_kernel, launched after the dK/dV kernel, sums them
   if (has_rows) {
     const __amdgpu_buffer_rsrc_t urec =
         make_rsrc(p.part_q + ((int64_t)unit * kQWaves + wave) * p.nW * kRecFloats, (uint32_t)(p.nW * kRecFloats * 4));
@@ -419,11 +419,10 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
 // the nW workgroups' records in workgroup order, so the result does not depend on scheduling.  A
 // separate launch spreads it over the chip: summed by the unit's last workgroup, 8 records of
 // 128 KiB went into one CU (15 us at one CU's bandwidth).  Every load of a batch of kQMBatch
-// records is issued before any is added.
+// records is issued before any is added.  Block `id` of the merge kernel's dQ part.
 constexpr int kQMBatch = 8;
-__global__ __launch_bounds__(kWave) void dq_merge_kernel(AttnBwdParams p) {
+__device__ inline void dq_merge_block(const AttnBwdParams& p, int id) {
   const int lane = threadIdx.x, lg = lane >> 4, lr = lane & 15;
-  int id = blockIdx.x;
   const int dh = id & 1, nt = (id >> 1) & 1;
   id >>= 2;
   const int wave = id % kQWaves, unit = id / kQWaves;
@@ -717,13 +716,13 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
 // Sum of the branches' dK/dV partials of every (sequence, KV head) in branch order, spread over the
 // chip (the last of a pair's workgroups summing them alone was bound by one CU's bandwidth).  One
 // thread per 16 bytes of a pair's record [C][dK | dV][128]; every load of a batch of 8 branches
-// is issued before any is summed.
-constexpr int kKMThreads = 256;
-__global__ __launch_bounds__(kKMThreads) void dkv_merge_kernel(AttnBwdParams p) {
+// is issued before any is summed.  Block `id` of the merge kernel's dK/dV part.
+__device__ inline int dkv_merge_blocks_per_pair(int C) { return (C * 2 * kD / 4 + kWave - 1) / kWave; }
+__device__ inline void dkv_merge_block(const AttnBwdParams& p, int id) {
   const int chunks = p.C * 2 * kD / 4;           // float4s of one branch record
-  const int per_pair = (chunks + kKMThreads - 1) / kKMThreads;
-  const int pair = blockIdx.x / per_pair;
-  const int q = (blockIdx.x % per_pair) * kKMThreads + threadIdx.x;
+  const int per_pair = dkv_merge_blocks_per_pair(p.C);
+  const int pair = id / per_pair;
+  const int q = (id % per_pair) * kWave + threadIdx.x;
   if (q >= chunks) return;
   const int g = pair % p.Hkv, s = pair / p.Hkv;
   const __amdgpu_buffer_rsrc_t rrec =
@@ -745,6 +744,15 @@ __global__ __launch_bounds__(kKMThreads) void dkv_merge_kernel(AttnBwdParams p) 
   const int d = isv ? rem - kD : rem;
   float* dst = (isv ? p.dv : p.dk) + (((int64_t)s * p.C + cc) * p.Hkv + g) * kD + d;
   *reinterpret_cast<f32x4*>(dst) = isv ? sum : sum * p.scale;
+}
+
+// Both sums in one launch of one-wave blocks: blocks [0, nq) sum the dQ partials, the rest the
+// dK/dV partials.  The dK/dV kernel reads only what the dQ kernel publishes, so it runs before
+// this merge and the two sums share the chip.
+__global__ __launch_bounds__(kWave) void bwd_merge_kernel(AttnBwdParams p, int nq) {
+  const int b = blockIdx.x;
+  if (b < nq) dq_merge_block(p, b);
+  else dkv_merge_block(p, b - nq);
 }
 
 }  // namespace
@@ -784,24 +792,22 @@ hipError_t launch_attn_bwd(const AttnBwdParams& p, const AttnBwdPlan& pl, bool p
     else hipLaunchKernelGGL(dq_kernel<false>, dim3(pl.nblk_q), dim3(kQThreads), 0, stream, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (pl.nW > 1) {                               // sum the workgroups' partials
-      const int64_t mblocks = (int64_t)pl.units * kQWaves * 4;   // (row tile, d half) waves
-      hipLaunchKernelGGL(dq_merge_kernel, dim3((unsigned)mblocks), dim3(kWave), 0, stream, p);
-      e = hipGetLastError();
-      if (e != hipSuccess) return e;
-    }
   }
   if (pl.nblk_kv > 0) {
     if (paged) hipLaunchKernelGGL(dkv_kernel<true>, dim3(pl.nblk_kv), dim3(kKThreads), 0, stream, p);
     else hipLaunchKernelGGL(dkv_kernel<false>, dim3(pl.nblk_kv), dim3(kKThreads), 0, stream, p);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || pl.nbr == 1) return e;
-    const int64_t per_pair = ((int64_t)p.C * 2 * kD / 4 + kKMThreads - 1) / kKMThreads;
-    const int64_t mblocks = (int64_t)p.S * p.Hkv * per_pair;
-    hipLaunchKernelGGL(dkv_merge_kernel, dim3((unsigned)mblocks), dim3(kKMThreads), 0, stream, p);
-    return hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  return hipSuccess;
+  // (unit, row block, row tile, d half) waves for dQ when the workgroups' partials need a sum;
+  // (pair, 16-byte column block) waves for dK/dV when more than one branch contributes
+  const int64_t nq = pl.nblk_q > 0 && pl.nW > 1 ? (int64_t)pl.units * kQWaves * 4 : 0;
+  const int64_t nkv = pl.nblk_kv > 0 && pl.nbr > 1
+                          ? (int64_t)p.S * p.Hkv * (((int64_t)p.C * 2 * kD / 4 + kWave - 1) / kWave)
+                          : 0;
+  if (nq + nkv == 0) return hipSuccess;
+  hipLaunchKernelGGL(bwd_merge_kernel, dim3((unsigned)(nq + nkv)), dim3(kWave), 0, stream, p, (int)nq);
+  return hipGetLastError();
 }
 
 }  // namespace bd
