@@ -144,8 +144,9 @@ def select_kv(k, q_win, seq_lens, num_q_heads: int, window: int, budget: int, po
     """K_S^sp(B) as an index set per (sequence, KV head): Alg. 2 "sparsify".
 
     k: per sequence [Hkv][>=L_s][D] bf16 bits; q_win: per sequence [W][Hq][D]
-    bf16 bits (the last W query rows).  Returns idx [S][Hkv][B] int32 (tail -1),
-    nsel [S] int32 and raw scores (list of [Hkv][L_s] float64).
+    bf16 bits (the last W query rows).  Returns idx [S][Hkv][B] int32 (tail -1; B + W slots with
+    ``budget_counts_window=False``), nsel [S] int32 (min(slots, L_s)) and raw scores (list of
+    [Hkv][L_s] float64).
 
     B >= L_s keeps every position (the sparse cache equals the full cache).
     """
@@ -177,7 +178,7 @@ def select_kv(k, q_win, seq_lens, num_q_heads: int, window: int, budget: int, po
             sel, _ = topk_from_scores(raw, L, window, budget, pool_kernel, budget_counts_window)
             idx[s, g, :sel.size] = sel
             raw_s[g] = raw
-        nsel[s] = out_budget
+        nsel[s] = min(out_budget, L)
         raws.append(raw_s)
     return idx, nsel, raws
 
@@ -199,19 +200,24 @@ def chunk_scores(raw_prefix: np.ndarray, chunk: int) -> np.ndarray:
 
 
 def topk_chunks_from_scores(raw: np.ndarray, L: int, window: int, budget: int,
-                            chunk: int = 8) -> Tuple[np.ndarray, np.ndarray]:
+                            chunk: int = 8, budget_counts_window: bool = False) -> Tuple[np.ndarray, np.ndarray]:
     """TopKChunks (Sec. 3.4; Alg. 1 step 4, Alg. 2 "sparsify"): the chunk-level selection.
 
-    The prefix [0, N), N = L - W, is cut into chunks of ``chunk`` positions; the top
-    floor((B - W) / chunk) chunks by score are kept (larger score first, lower chunk index
-    among equal scores) and their positions returned in ascending order, then the W window
-    positions (reading: B counts the window, as in the token-level policy; a kept short last
-    chunk contributes fewer than ``chunk`` positions).  Returns (positions, chunk scores).
+    Sec. 3.4 cuts the prefix cache into chunks of s = ``chunk`` positions, scores every chunk by
+    cumulative attention weight and retains the top floor(B / s) chunks; the continuation rows
+    (here the W scoring rows at positions N .. L-1, N = L - W) attend on top of them (Alg. 1
+    step 4).  So the prefix [0, N) is cut into chunks (the last one shorter when s does not divide
+    N), the top floor(B / s) chunks are kept (larger score first, lower chunk index among equal
+    scores), their positions returned in ascending order, and the W window positions appended.
+    ``budget_counts_window=True`` takes the other reading, where B also pays for the window:
+    floor((B - W) / s) chunks.  A kept short last chunk contributes fewer than s positions.
+    Returns (positions, chunk scores).
     """
     N = L - window
     cs = chunk_scores(raw[:N], chunk)
     nc = cs.shape[0]
-    keep = max(0, min((budget - window) // chunk, nc))
+    prefix_budget = budget - window if budget_counts_window else budget
+    keep = max(0, min(prefix_budget // chunk, nc))
     order = np.lexsort((np.arange(nc), -cs))            # primary: -score, secondary: chunk index
     chosen = np.sort(order[:keep])
     parts = [np.arange(c * chunk, min((c + 1) * chunk, N)) for c in chosen]
@@ -220,11 +226,13 @@ def topk_chunks_from_scores(raw: np.ndarray, L: int, window: int, budget: int,
 
 
 def select_kv_chunks(k, q_win, seq_lens, num_q_heads: int, window: int, budget: int, chunk: int = 8,
-                     scale: Optional[float] = None):
+                     scale: Optional[float] = None, budget_counts_window: bool = False):
     """K_S^sp(B) by TopKChunks per (sequence, KV head): scoring as select_kv, chunk selection.
 
-    Returns idx [S][Hkv][B] int32 (slots past a head's kept positions hold -1), nsel [S]
-    (B, or L_s when B >= L_s) and the raw scores.  B >= L_s keeps every position.
+    Each head's list has ``ld`` slots, ld = B + W (the paper's count: B pays for prefix chunks
+    only) or B (``budget_counts_window``).  Returns idx [S][Hkv][ld] int32 (slots past a head's
+    kept positions hold -1), nsel [S] = min(ld, L_s) (slots, not kept positions) and the raw
+    scores.  B >= L_s keeps every position (nsel = L_s).
     """
     if window < 1 or budget < window or chunk < 1:
         raise ValueError("invalid selection arguments")
@@ -233,7 +241,8 @@ def select_kv_chunks(k, q_win, seq_lens, num_q_heads: int, window: int, budget: 
     G = num_q_heads // Hkv
     D = k[0].shape[-1]
     sc = _scale64(scale, D)
-    idx = np.full((S, Hkv, budget), -1, dtype=np.int32)
+    ld = budget if budget_counts_window else budget + window
+    idx = np.full((S, Hkv, ld), -1, dtype=np.int32)
     nsel = np.zeros(S, dtype=np.int32)
     raws = []
     for s in range(S):
@@ -250,10 +259,10 @@ def select_kv_chunks(k, q_win, seq_lens, num_q_heads: int, window: int, budget: 
         for g in range(Hkv):
             kg = bf16_to_f64(k[s][g, :L])
             raw = window_scores(kg, qw[:, g * G:(g + 1) * G, :], L, sc)
-            sel, _ = topk_chunks_from_scores(raw, L, window, budget, chunk)
+            sel, _ = topk_chunks_from_scores(raw, L, window, budget, chunk, budget_counts_window)
             idx[s, g, :sel.size] = sel
             raw_s[g] = raw
-        nsel[s] = budget
+        nsel[s] = min(ld, L)
         raws.append(raw_s)
     return idx, nsel, raws
 

@@ -281,13 +281,16 @@ def test_chunk_scores_partition_the_prefix():
     assert abs(cs.sum() - x.sum()) < 1e-12
 
 
+@pytest.mark.parametrize("counts_window", [False, True])
 @pytest.mark.parametrize("seed", range(6))
-def test_topk_chunks_brute_force_tiny(seed):
+def test_topk_chunks_brute_force_tiny(seed, counts_window):
     g = np.random.default_rng(300 + seed)
-    L, W, s, B = 30, 4, 3, 13                         # prefix 26 -> 9 chunks (last has 2); keep 3 chunks
+    L, W, s, B = 30, 4, 3, 13                         # prefix 26 -> 9 chunks (last has 2)
     raw = np.round(g.random(L) * 3) / 3                # coarse values -> ties between chunk sums
-    sel, cs = O.topk_chunks_from_scores(raw, L, W, B, s)
-    nc, keep = 9, (B - W) // s
+    sel, cs = O.topk_chunks_from_scores(raw, L, W, B, s, budget_counts_window=counts_window)
+    # Sec. 3.4 keeps floor(B/s) = 4 chunks of the prefix; the other reading floor((B-W)/s) = 3
+    nc, keep = 9, ((B - W) if counts_window else B) // s
+    assert keep == (3 if counts_window else 4)
     # the kept set is the unique one ranking above every other chunk under (-score, index)
     winners = [c for c in itertools.combinations(range(nc), keep)
                if all((-cs[a], a) < (-cs[b], b) for a in c for b in set(range(nc)) - set(c))]
@@ -296,45 +299,75 @@ def test_topk_chunks_brute_force_tiny(seed):
     assert sel.tolist() == want
 
 
-def test_topk_chunks_of_one_is_the_unpooled_token_selection():
+@pytest.mark.parametrize("counts_window", [False, True])
+def test_topk_chunks_of_one_is_the_unpooled_token_selection(counts_window):
     g = np.random.default_rng(11)
     L, W = 400, 16
     raw = np.floor(g.random(L) * 40)
     for B in [16, 50, 200]:
-        a, _ = O.topk_chunks_from_scores(raw, L, W, B, 1)
-        b, _ = O.topk_from_scores(raw, L, W, B, 1)
+        a, _ = O.topk_chunks_from_scores(raw, L, W, B, 1, budget_counts_window=counts_window)
+        b, _ = O.topk_from_scores(raw, L, W, B, 1, budget_counts_window=counts_window)
         assert a.tolist() == b.tolist()
 
 
 def test_topk_chunks_ties_take_lowest_chunks_and_nest():
-    sel, _ = O.topk_chunks_from_scores(np.ones(40), 40, 8, 24, 8)   # 4 chunks tie: keep chunks 0, 1
+    # 4 chunks tie: the paper's count keeps floor(24/8) = 3 (chunks 0, 1, 2), the other reading 2
+    sel, _ = O.topk_chunks_from_scores(np.ones(40), 40, 8, 24, 8)
+    assert sel.tolist() == list(range(24)) + list(range(32, 40))
+    sel, _ = O.topk_chunks_from_scores(np.ones(40), 40, 8, 24, 8, budget_counts_window=True)
     assert sel.tolist() == list(range(16)) + list(range(32, 40))
     g = np.random.default_rng(12)
     raw = g.random(1000)
-    prev = None
-    for B in [32, 96, 288, 800]:
-        sel, cs = O.topk_chunks_from_scores(raw, 1000, 32, B, 8)
-        assert sel.size == 32 + 8 * ((B - 32) // 8)
-        if prev is not None:
-            assert set(prev) <= set(sel.tolist())
-        prev = sel.tolist()
+    for cw in (False, True):
+        prev = None
+        for B in [32, 96, 288, 800]:
+            sel, cs = O.topk_chunks_from_scores(raw, 1000, 32, B, 8, budget_counts_window=cw)
+            assert sel.size == 32 + 8 * (((B - 32) if cw else B) // 8)
+            if prev is not None:
+                assert set(prev) <= set(sel.tolist())
+            prev = sel.tolist()
+
+
+def test_topk_chunks_training_view_holds_floor_b_over_s_chunks_plus_the_block():
+    # Alg. 1 step 4 at the training shape: a block of C = 64 continuation rows scores the prefix of
+    # length P = L - C; the view is the top floor(B/8) chunks of the prefix, the block on top
+    g = np.random.default_rng(13)
+    L, C = 8192, 64
+    raw = g.random(L)
+    cs = O.chunk_scores(raw[:L - C], 8)
+    for B in [256, 512, 1024, 2048, 1000]:
+        sel, _ = O.topk_chunks_from_scores(raw, L, C, B, 8)
+        assert sel.size == 8 * (B // 8) + C
+        assert sel[-C:].tolist() == list(range(L - C, L))
+        kept = sorted({int(t) // 8 for t in sel[:-C]})
+        assert len(kept) == B // 8
+        assert min(cs[kept]) >= max(np.delete(cs, kept))     # every kept chunk outranks every other
 
 
 def test_select_chunks_zero_keys_and_spike():
     _, q = _cfg_small()
     k = np.zeros((1, 2, 256, 128), np.uint16)
-    idx, nsel, _ = O.select_kv_chunks(k, q, [256], 8, 16, 64, 8)     # equal scores: lowest 6 chunks
-    assert nsel[0] == 64 and np.all(idx[0] == np.r_[np.arange(48), np.arange(240, 256)])
+    # equal scores: the lowest floor(64/8) = 8 chunks, then the window; B + W slots
+    idx, nsel, _ = O.select_kv_chunks(k, q, [256], 8, 16, 64, 8)
+    assert idx.shape == (1, 2, 80) and nsel[0] == 80
+    assert np.all(idx[0] == np.r_[np.arange(64), np.arange(240, 256)])
+    idx, nsel, _ = O.select_kv_chunks(k, q, [256], 8, 16, 64, 8, budget_counts_window=True)   # 6 chunks
+    assert idx.shape == (1, 2, 64) and nsel[0] == 64
+    assert np.all(idx[0] == np.r_[np.arange(48), np.arange(240, 256)])
     L, W, t0 = 256, 16, 100
     g = np.random.default_rng(9)
     qs = np.zeros((1, W, 8, 128), np.float32); qs[..., 0] = 1.0
     ks = 0.01 * g.standard_normal((1, 2, L, 128)).astype(np.float32)
     ks[0, :, t0, 0] = 60.0
-    idx, _, _ = O.select_kv_chunks(bits(ks), bits(qs), [L], 8, W, 32, 8)
+    idx, _, _ = O.select_kv_chunks(bits(ks), bits(qs), [L], 8, W, 16, 8)
     for gg in range(2):                                # the spike's chunk [96, 104) is kept first
         assert set(range(96, 104)) <= set(idx[0, gg].tolist())
     idx, nsel, _ = O.select_kv_chunks(k, q, [200], 8, 16, 300, 8)     # B >= L: identity
     assert nsel[0] == 200 and np.all(idx[0, :, :200] == np.arange(200)) and np.all(idx[0, :, 200:] == -1)
+    # B < L but B + W > L: slots past L are -1 and nsel = L
+    idx, nsel, _ = O.select_kv_chunks(k, q, [200], 8, 16, 190, 8)
+    assert idx.shape[2] == 206 and nsel[0] == 200
+    assert np.all(idx[0, :, :200] == np.arange(200)) and np.all(idx[0, :, 200:] == -1)
 
 
 def test_select_chunks_short_last_chunk_and_tail():
@@ -342,9 +375,11 @@ def test_select_chunks_short_last_chunk_and_tail():
     L, W = 29, 8
     raw = np.full(L, 0.1)
     raw[18] = 50.0
-    sel, cs = O.topk_chunks_from_scores(raw, L, W, 8 + 16, 8)
+    sel, cs = O.topk_chunks_from_scores(raw, L, W, 16, 8)
     assert sel.tolist() == list(range(8)) + list(range(16, 21)) + list(range(21, 29))
     assert cs.tolist() == pytest.approx([0.8, 0.8, 50.4])
+    sel2, _ = O.topk_chunks_from_scores(raw, L, W, 8 + 16, 8, budget_counts_window=True)
+    assert sel2.tolist() == sel.tolist()
 
 
 # ---------------------------------------------------------------- sparse decode (Eq. 2)
