@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define BD_ABI_VERSION 1
+#define BD_ABI_VERSION 2
 #define BD_HEAD_DIM 128
 /* Longest candidate prefix L_s - W that bd_select_kv ranks in one pass. */
 #define BD_SELECT_MAX_PREFIX 32768
@@ -154,19 +154,26 @@ bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_
  * Step 1 as bd_select_kv.  The prefix [0, N), N = L_s - W, is cut into chunks
  * of `chunk` positions (chunk c covers [c*chunk, min((c+1)*chunk, N)); the last
  * one is shorter when chunk does not divide N); a chunk's score is the sum of
- * its positions' raw scores (fp32, left to right).  The floor((B - W) / chunk)
- * chunks ranked first by (score descending, chunk index ascending) are kept:
- * their positions in ascending order, then the W window positions.
- * idx_out    [S][Hkv][budget] int32; a head's slots past its kept positions
- *            (fewer than B when chunk does not divide B - W, or a short last
- *            chunk is kept) are -1, which the attention calls skip.
- * nsel_out   [S] int32: min(budget, L_s) (slots, not kept positions).
+ * its positions' raw scores (fp32, left to right).  Sec. 3.4 retains the top
+ * floor(B / chunk) chunks of the prefix cache, and the W rows that scored it
+ * (the continuation block of Alg. 1) attend on top of them:
+ *   budget_counts_window = 0  keep floor(B / chunk) chunks, then the W window
+ *                             positions: ld = B + W index slots per head;
+ *   budget_counts_window = 1  B also pays for the window: floor((B - W) / chunk)
+ *                             chunks, then the window; ld = B slots.
+ * The kept chunks (ranked by score descending, chunk index ascending) give
+ * their positions in ascending order, then the window positions N .. L_s-1.
+ * idx_out    [S][Hkv][ld] int32; a head's slots past its kept positions (fewer
+ *            than ld when chunk does not divide the prefix budget, or a short
+ *            last chunk is kept) are -1, which the attention calls skip.
+ * nsel_out   [S] int32: min(ld, L_s) (slots, not kept positions); L_s when
+ *            B >= L_s, where every position is kept.
  * Other arguments, requirements and the workspace are those of bd_select_kv
- * (bd_select_kv_workspace_bytes); chunk >= 1.
+ * (bd_select_kv_workspace_bytes); chunk >= 1; budget_counts_window 0 or 1.
  * ---------------------------------------------------------------------- */
 bd_status bd_select_kv_chunks(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_heads, int32_t window,
-                              int32_t budget, int32_t chunk, float scale, const float* lse_win,
-                              int32_t* idx_out, int32_t* nsel_out, float* scores_out,
+                              int32_t budget, int32_t chunk, int32_t budget_counts_window, float scale,
+                              const float* lse_win, int32_t* idx_out, int32_t* nsel_out, float* scores_out,
                               void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------

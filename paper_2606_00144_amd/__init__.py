@@ -67,7 +67,7 @@ _SIGNATURES = {
     "bd_abi_version": (_I32, []),
     "bd_select_kv_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32]),
     "bd_select_kv": (_I32, [_KV, _P, _I32, _I32, _I32, _I32, _F32, _P, _P, _P, _P, _P, _SZ, _P]),
-    "bd_select_kv_chunks": (_I32, [_KV, _P, _I32, _I32, _I32, _I32, _F32, _P, _P, _P, _P, _P, _SZ, _P]),
+    "bd_select_kv_chunks": (_I32, [_KV, _P, _I32, _I32, _I32, _I32, _I32, _F32, _P, _P, _P, _P, _P, _SZ, _P]),
     "bd_cache_append": (_I32, [_KV, _P, _P, _I32, _P, _I32, _P, _P]),
     "bd_cache_rollback": (_I32, [_P, _P, _P, _I32, _I32, _P]),
     "bd_top1_ce_workspace_bytes": (_SZ, [_I32, _I32]),
@@ -201,27 +201,31 @@ def bd_select_kv(k: torch.Tensor, q_win: torch.Tensor, seq_lens: torch.Tensor, b
                  return_scores: bool = False, page_table: Optional[torch.Tensor] = None,
                  max_seq_len: Optional[int] = None, workspace: Optional[Workspace] = None):
     """Budgeted KV selection.  q_win: bf16 [S, W, Hq, 128].  Returns (idx [S,Hkv,B], nsel [S][, scores])."""
-    return _select("bd_select_kv", pool_kernel, k, q_win, seq_lens, budget, scale, lse_win, return_scores,
-                   page_table, max_seq_len, workspace)
+    return _select("bd_select_kv", (pool_kernel,), budget, k, q_win, seq_lens, budget, scale, lse_win,
+                   return_scores, page_table, max_seq_len, workspace)
 
 
 def bd_select_kv_chunks(k: torch.Tensor, q_win: torch.Tensor, seq_lens: torch.Tensor, budget: int, *,
-                        chunk: int = 8, scale: Optional[float] = None, lse_win: Optional[torch.Tensor] = None,
-                        return_scores: bool = False, page_table: Optional[torch.Tensor] = None,
-                        max_seq_len: Optional[int] = None, workspace: Optional[Workspace] = None):
-    """Chunk-level selection (TopKChunks).  Same arguments and results as bd_select_kv; a head's
-    unused idx slots hold -1."""
-    return _select("bd_select_kv_chunks", chunk, k, q_win, seq_lens, budget, scale, lse_win, return_scores,
-                   page_table, max_seq_len, workspace)
+                        chunk: int = 8, budget_counts_window: bool = False, scale: Optional[float] = None,
+                        lse_win: Optional[torch.Tensor] = None, return_scores: bool = False,
+                        page_table: Optional[torch.Tensor] = None, max_seq_len: Optional[int] = None,
+                        workspace: Optional[Workspace] = None):
+    """Chunk-level selection (TopKChunks): the top floor(B/chunk) prefix chunks, then the window
+    (budget_counts_window=True: floor((B-W)/chunk) chunks).  Returns (idx [S,Hkv,ld], nsel [S][, scores])
+    with ld = B + W (or B); a head's unused idx slots hold -1."""
+    W = q_win.shape[1]
+    ld = budget if budget_counts_window else budget + W
+    return _select("bd_select_kv_chunks", (chunk, int(bool(budget_counts_window))), ld, k, q_win, seq_lens, budget,
+                   scale, lse_win, return_scores, page_table, max_seq_len, workspace)
 
 
-def _select(entry, mode_arg, k, q_win, seq_lens, budget, scale, lse_win, return_scores, page_table, max_seq_len,
+def _select(entry, mode_args, ld, k, q_win, seq_lens, budget, scale, lse_win, return_scores, page_table, max_seq_len,
             workspace):
     _require(q_win.dtype == torch.bfloat16 and q_win.dim() == 4 and q_win.is_contiguous(), "q_win must be contiguous bf16 [S,W,Hq,128]")
     kv = kv_desc(k, None, seq_lens, page_table, max_seq_len)
     S, W, Hq = q_win.shape[0], q_win.shape[1], q_win.shape[2]
     dev = q_win.device
-    idx = torch.empty((S, kv.num_kv_heads, budget), dtype=torch.int32, device=dev)
+    idx = torch.empty((S, kv.num_kv_heads, ld), dtype=torch.int32, device=dev)
     nsel = torch.empty((S,), dtype=torch.int32, device=dev)
     scores = torch.zeros((S, kv.num_kv_heads, kv.max_seq_len), dtype=torch.float32, device=dev) if return_scores else None
     if lse_win is not None:
@@ -229,7 +233,7 @@ def _select(entry, mode_arg, k, q_win, seq_lens, budget, scale, lse_win, return_
     L = lib()
     nb = L.bd_select_kv_workspace_bytes(S, kv.num_kv_heads, Hq, W, kv.max_seq_len)
     wp, wb = _ws("select", nb, dev, workspace)
-    _check(getattr(L, entry)(ctypes.byref(kv), q_win.data_ptr(), Hq, W, budget, mode_arg, _scale(scale),
+    _check(getattr(L, entry)(ctypes.byref(kv), q_win.data_ptr(), Hq, W, budget, *mode_args, _scale(scale),
                              _ptr(lse_win), idx.data_ptr(), nsel.data_ptr(), _ptr(scores), wp, wb, _stream()))
     return (idx, nsel, scores) if return_scores else (idx, nsel)
 

@@ -166,12 +166,16 @@ size_t bd_select_kv_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int3
 
 namespace {
 // Common host path of both selection policies (chunk == 0: token level with pooling).
+// counts_window: the budget pays for the W window positions too (B - W prefix positions), else
+// for prefix positions only (B of them, B + W index slots).
 bd_status run_select(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_heads, int32_t window, int32_t budget,
-                     int32_t pool_kernel, int32_t chunk, float scale, const float* lse_win, int32_t* idx_out,
-                     int32_t* nsel_out, float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+                     int32_t pool_kernel, int32_t chunk, bool counts_window, float scale, const float* lse_win,
+                     int32_t* idx_out, int32_t* nsel_out, float* scores_out, void* ws, size_t ws_bytes,
+                     hipStream_t stream) {
   bd_status st = check_kv(kv, false, num_q_heads);
   if (st != BD_OK) return st;
   if (window < 1 || budget < window) return fail(BD_ERR_INVALID_ARG, "need 1 <= window <= budget (window %d, budget %d)", window, budget);
+  if (!counts_window && (int64_t)budget + window > INT32_MAX) return fail(BD_ERR_INVALID_ARG, "budget + window overflows");
   if (chunk < 0) return fail(BD_ERR_INVALID_ARG, "chunk must be >= 1");
   if (chunk == 0 && (pool_kernel < 1 || pool_kernel % 2 == 0))
     return fail(BD_ERR_INVALID_ARG, "pool_kernel must be odd and >= 1");
@@ -200,6 +204,8 @@ bd_status run_select(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_
   p.budget = budget;
   p.pool_kernel = chunk > 0 ? 1 : pool_kernel;
   p.chunk = chunk;
+  p.keep = counts_window ? budget - window : budget;
+  p.ld = p.keep + window;
   p.R = window * p.G;
   p.n_rb = pl.n_rb;
   p.nsplit = pl.nsplit;
@@ -220,16 +226,19 @@ bd_status run_select(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_
 bd_status bd_select_kv(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_heads, int32_t window,
                        int32_t budget, int32_t pool_kernel, float scale, const float* lse_win, int32_t* idx_out,
                        int32_t* nsel_out, float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream) {
-  return run_select(kv, q_win, num_q_heads, window, budget, pool_kernel, 0, scale, lse_win, idx_out, nsel_out,
-                    scores_out, ws, ws_bytes, stream);
+  return run_select(kv, q_win, num_q_heads, window, budget, pool_kernel, 0, true, scale, lse_win, idx_out,
+                    nsel_out, scores_out, ws, ws_bytes, stream);
 }
 
 bd_status bd_select_kv_chunks(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_heads, int32_t window,
-                              int32_t budget, int32_t chunk, float scale, const float* lse_win, int32_t* idx_out,
-                              int32_t* nsel_out, float* scores_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+                              int32_t budget, int32_t chunk, int32_t budget_counts_window, float scale,
+                              const float* lse_win, int32_t* idx_out, int32_t* nsel_out, float* scores_out, void* ws,
+                              size_t ws_bytes, hipStream_t stream) {
   if (chunk < 1) return fail(BD_ERR_INVALID_ARG, "chunk must be >= 1");
-  return run_select(kv, q_win, num_q_heads, window, budget, 1, chunk, scale, lse_win, idx_out, nsel_out,
-                    scores_out, ws, ws_bytes, stream);
+  if (budget_counts_window != 0 && budget_counts_window != 1)
+    return fail(BD_ERR_INVALID_ARG, "budget_counts_window must be 0 or 1");
+  return run_select(kv, q_win, num_q_heads, window, budget, 1, chunk, budget_counts_window != 0, scale, lse_win,
+                    idx_out, nsel_out, scores_out, ws, ws_bytes, stream);
 }
 
 // ---------------------------------------------------------------- sparse decode
@@ -390,17 +399,27 @@ size_t bd_verify_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, in
   return bd::attn_ws_bytes(num_seqs, num_kv_heads, num_q_heads, gamma + 1, 0, 0, max_seq_len, true);
 }
 
-bd_status bd_verify_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, int32_t gamma, float scale,
-                         uint16_t* out, float* lse_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+namespace {
+bd_status check_verify(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, int32_t gamma, float scale,
+                       const uint16_t* out) {
   bd_status st = check_kv(kv, true, num_q_heads);
   if (st != BD_OK) return st;
   if (gamma < 0 || gamma > 4095) return fail(BD_ERR_INVALID_ARG, "gamma %d outside [0, 4095]", gamma);
   if (!q || !aligned(q, 16) || !out || !aligned(out, 16))
     return fail(BD_ERR_INVALID_ARG, "q and out must be non-NULL and 16-byte aligned");
   if (!std::isfinite(scale) || !(scale > 0.f)) return fail(BD_ERR_INVALID_ARG, "scale must be positive and finite");
+  return BD_OK;
+}
+}  // namespace
+
+bd_status bd_verify_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, int32_t gamma, float scale,
+                         uint16_t* out, float* lse_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  const bd_status st = check_verify(kv, q, num_q_heads, gamma, scale, out);
+  if (st != BD_OK) return st;
   return run_attn(kv, q, num_q_heads, gamma + 1, 0, nullptr, 0, nullptr, scale, nullptr, nullptr, out, lse_out, ws,
                   ws_bytes, stream);
 }
+
 
 // ---------------------------------------------------------------- accept
 size_t bd_accept_len_workspace_bytes(int32_t num_seqs, int32_t gamma, int32_t vocab) {

@@ -145,6 +145,8 @@ struct SelectParams {
   int32_t S, Hkv, Hq, G, W;
   int32_t budget, pool_kernel;
   int32_t chunk;            // 0: token-level selection with pooling; > 0: TopKChunks with this chunk size
+  int32_t keep;             // prefix positions the budget pays for: budget - W, or budget (B excludes the window)
+  int32_t ld;               // index slots per (s, g): keep + W
   int32_t R;                // rows per (s, g): W * G
   int32_t n_rb;             // row blocks of 16*NT rows
   int32_t nsplit, kps;      // key splits of the scoring passes
@@ -154,7 +156,7 @@ struct SelectParams {
   float* stats;             // [S][Hkv][n_rb][nsplit][128][2] per-split row max / sum
   float* raw_part;          // [S][Hkv][n_rb][max_L] per-row-block column sums
   float* raw;               // nullable [S][Hkv][max_L] total raw scores (the caller's scores_out)
-  int32_t* idx_out;         // [S][Hkv][budget]
+  int32_t* idx_out;         // [S][Hkv][ld]
   int32_t* nsel_out;        // [S]
 };
 

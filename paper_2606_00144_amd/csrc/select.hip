@@ -9,11 +9,12 @@
 //      streams K again, adding every row's normalised weight of every key
 //      into that key's column sum (complete within a row block, so no atomics);
 //   3. top-B: one 1024-thread workgroup per (sequence, KV head) sums the row
-//      blocks, max-pools the prefix, finds the (B-W)-th largest pooled score
-//      with a 4 x 8-bit radix select over the float bit patterns (scores are
-//      non-negative, so the bits order like the values), and compacts the
-//      chosen positions in ascending order; ties at the threshold take the
-//      lowest positions, then the window is appended.
+//      blocks, max-pools the prefix (or sums its chunks), finds the K-th
+//      largest candidate score with a radix select over the float bit patterns
+//      (digits of 8, 11 and 12 bits; scores are non-negative, so the bits order
+//      like the values), and compacts the chosen positions in ascending order;
+//      ties at the threshold take the lowest positions, then the window is
+//      appended.
 //
 // The scoring product is a real dense contraction ((W*G) x 128 x L per
 // (s, g)), so it runs on MFMA with the attention kernel's orientation: keys on
@@ -428,20 +429,20 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
   const int pair = blockIdx.x;
   const int g = pair % p.Hkv, s = pair / p.Hkv;
   const int L = seq_len(p.kv, s);
-  const int B = p.budget, W = p.W;
-  int32_t* idx_row = p.idx_out + (int64_t)pair * B;
+  const int B = p.budget, W = p.W, ld = p.ld;
+  int32_t* idx_row = p.idx_out + (int64_t)pair * ld;
 
   if (B >= L) {
-    for (int t = tid; t < B; t += kTopkThreads) idx_row[t] = t < L ? t : -1;
+    for (int t = tid; t < ld; t += kTopkThreads) idx_row[t] = t < L ? t : -1;
     if (g == 0 && tid == 0) p.nsel_out[s] = L;
     return;
   }
-  if (g == 0 && tid == 0) p.nsel_out[s] = B;
+  if (g == 0 && tid == 0) p.nsel_out[s] = ld < L ? ld : L;
 
   // 1. total raw scores (row blocks summed in order), staged in LDS over the prefix [0, N) at
   // raw_lds[kPad + t] and exported when the caller asked for them; each batch of loads is issued
   // before any is summed
-  const int N = L - W, K = B - W, rad = p.pool_kernel / 2;
+  const int N = L - W, K = p.keep, rad = p.pool_kernel / 2;
   float* raw = p.raw ? p.raw + (int64_t)pair * p.max_L : nullptr;
   const float* part = p.raw_part + (int64_t)pair * p.n_rb * p.max_L;
   constexpr int kStageBatch = 16;
@@ -651,7 +652,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
   }
   if (kept > K) kept = K;
   for (int i = tid; i < W; i += kTopkThreads) idx_row[kept + i] = N + i;
-  for (int i = kept + W + tid; i < B; i += kTopkThreads) idx_row[i] = -1;   // chunk mode: unused slots
+  for (int i = kept + W + tid; i < ld; i += kTopkThreads) idx_row[i] = -1;   // unused slots
   if (tid < ncell) { c_eq[tid] = eq_before; c_gt[tid] = take_before; }
   __syncthreads();
   for (int e0 = 0; e0 < E; e0 += kBatch) {
@@ -674,7 +675,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(SelectParams p) {
       if (take) {
         const int off = ((int)tkb[j] + __builtin_popcountll(bt & below)) * unit;
         if (chunk == 0) {
-          if (off < K) idx_row[off] = c;      // guard: never write past the B - W prefix slots
+          if (off < K) idx_row[off] = c;      // guard: never write past the K prefix slots
         } else {
           const int b = c * chunk, n = N - b < chunk ? N - b : chunk;
           for (int i = 0; i < n; ++i)

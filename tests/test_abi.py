@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_status_strings(L):
-    assert L.bd_abi_version() == 1
+    assert L.bd_abi_version() == 2
     for s in range(5):
         assert L.bd_status_string(s)
     assert L.bd_status_string(99) == b"unknown status"
@@ -92,6 +92,12 @@ def test_decode_select_multiview_accept_rejections(L):
     assert sel(P=4) == 1
     assert sel(P=301) == 2
     assert sel(kv=_kv(max_seq_len=40000)) == 2                              # prefix above BD_SELECT_MAX_PREFIX
+    ch = lambda **a: L.bd_select_kv_chunks(ctypes.byref(kv), FAKE, 32, 32, a.get("B", 256), a.get("s", 8),
+                                           a.get("cw", 0), 0.1, None, FAKE, FAKE, None, FAKE, 1 << 40, None)
+    assert ch(s=0) == 1
+    assert ch(cw=2) == 1                                                     # the switch is 0 or 1
+    assert ch(B=16) == 1                                                     # budget below the window
+    assert ch(B=2 ** 31 - 8) == 1                                            # B + W slots overflow int32
     mv = lambda **a: L.bd_multiview_attn(ctypes.byref(kv), FAKE, 32, a.get("C", 64), a.get("V", 4), FAKE, 1024, FAKE,
                                          0.1, a.get("ov", FAKE), None, None, a.get("of", FAKE), None, a.get("o32f"),
                                          FAKE, 1 << 40, None)

@@ -35,13 +35,37 @@ def _kept_chunks(idx_row, N, s):
     return sorted({int(t) // s for t in idx_row if 0 <= t < N})
 
 
-def _check(k, q_win, lens, Hq, W, B, s, what):
-    case(f"select chunks {what} B={B} s={s}")
+def _oracle(k, q_win, lens, Hq, W, B, s, cw, raws=None):
+    """The oracle's selection; with raws (oracle scores per sequence, [Hkv][L]) given, only its
+    ranking steps run (the scores do not depend on B)."""
+    if raws is None:
+        return O.select_kv_chunks(k, q_win, lens, Hq, W, B, s, budget_counts_window=cw)
+    S, Hkv = len(lens), k.shape[1]
+    ld = B if cw else B + W
+    idx = np.full((S, Hkv, ld), -1, np.int32)
+    nsel = np.zeros(S, np.int32)
+    for si, L in enumerate(lens):
+        if B >= L:
+            idx[si, :, :L] = np.arange(L)
+            nsel[si] = L
+            continue
+        for g in range(Hkv):
+            sel, _ = O.topk_chunks_from_scores(raws[si][g], L, W, B, s, budget_counts_window=cw)
+            idx[si, g, :sel.size] = sel
+        nsel[si] = min(ld, L)
+    return idx, nsel, raws
+
+
+def _check(k, q_win, lens, Hq, W, B, s, what, cw=False, raws=None, lse_win=None):
+    case(f"select chunks {what} B={B} s={s} counts_window={cw}")
     idx, nsel, scores = bd.bd_select_kv_chunks(bf16_dev(k), bf16_dev(q_win), i32_dev(lens), B, chunk=s,
-                                               return_scores=True)
+                                               budget_counts_window=cw, return_scores=True,
+                                               lse_win=None if lse_win is None else torch.from_numpy(lse_win).cuda())
     torch.cuda.synchronize()
     gi, gn, gs = idx.cpu().numpy(), nsel.cpu().numpy(), scores.cpu().numpy()
-    oi, on, oraw = O.select_kv_chunks(k, q_win, lens, Hq, W, B, s)
+    oi, on, oraw = _oracle(k, q_win, lens, Hq, W, B, s, cw, raws)
+    ld = B if cw else B + W
+    assert gi.shape[2] == ld and oi.shape == gi.shape, what
     assert np.array_equal(gn, on), what
     near = 0
     for si in range(len(lens)):
@@ -51,14 +75,14 @@ def _check(k, q_win, lens, Hq, W, B, s, what):
                 assert np.array_equal(gi[si, g], oi[si, g]), (what, si, g)
                 continue
             N = L - W
-            keep = min((B - W) // s, (N + s - 1) // s)
+            keep = min(((B - W) if cw else B) // s, (N + s - 1) // s)
             # layout: kept chunk positions ascending, the window, then -1
             cs32 = _fp32_chunk_sums(gs[si, g], N, s)
             order = np.lexsort((np.arange(cs32.size), -cs32.astype(np.float64)))
             want_chunks = np.sort(order[:keep])
             want = [t for c in want_chunks for t in range(c * s, min((c + 1) * s, N))]
             want = want + list(range(N, L))
-            want = want + [-1] * (B - len(want))
+            want = want + [-1] * (ld - len(want))
             assert gi[si, g].tolist() == want, (what, "chunk ranking stage", si, g)
             # (ii) end to end
             diff = set(_kept_chunks(gi[si, g], N, s)) ^ set(_kept_chunks(oi[si, g], N, s))
@@ -71,10 +95,11 @@ def _check(k, q_win, lens, Hq, W, B, s, what):
     return gi, near
 
 
-def test_select_chunks_tiny4k():
+@pytest.mark.parametrize("cw", [False, True])
+def test_select_chunks_tiny4k(cw):
     cfg = synth.workload("tiny-4k-gqa4")
     qt, k, _ = config_data("tiny-4k-gqa4")
-    _, near = _check(k, qt[:, -cfg.window:], [cfg.seq_len], cfg.num_q_heads, cfg.window, 256, 8, "tiny 4K")
+    _, near = _check(k, qt[:, -cfg.window:], [cfg.seq_len], cfg.num_q_heads, cfg.window, 256, 8, "tiny 4K", cw)
     assert near <= 1
 
 
@@ -94,8 +119,9 @@ def test_select_chunks_ragged_lengths_and_sizes(s):
     g = np.random.default_rng(21)
     k = synth.f32_to_bf16_bits(g.standard_normal((S, Hkv, max(lens), 128)).astype(np.float32))
     q = synth.f32_to_bf16_bits(g.standard_normal((S, W, Hq, 128)).astype(np.float32))
-    _, near = _check(k, q, lens, Hq, W, 300, s, f"ragged s={s}")
-    assert near <= 1
+    for cw in (False, True):
+        _, near = _check(k, q, lens, Hq, W, 300, s, f"ragged s={s}", cw)
+        assert near <= 1
 
 
 @pytest.mark.parametrize("s", [5, 16])
@@ -110,13 +136,14 @@ def test_select_chunks_short_last_chunk_taken(s):
     qf = g.standard_normal((S, W, Hq, 128)).astype(np.float32)
     kf[:, :, N - 1] = 100.0 * qf.mean(axis=(1, 2))[:, None, :] / np.linalg.norm(qf.mean(axis=(1, 2)), axis=-1)[:, None, None]
     k, q = synth.f32_to_bf16_bits(kf), synth.f32_to_bf16_bits(qf)
-    gi, _ = _check(k, q, [L, L], Hq, W, B, s, f"short last chunk s={s}")
     last = (N - 1) // s
-    for si in range(S):
-        for h in range(Hkv):
-            row = gi[si, h].tolist()
-            assert last in _kept_chunks(row, N, s), (si, h)
-            assert row[row.index(N - 1) + 1] == N, (si, h)    # the window follows the short chunk
+    for cw in (False, True):
+        gi, _ = _check(k, q, [L, L], Hq, W, B, s, f"short last chunk s={s}", cw=cw)
+        for si in range(S):
+            for h in range(Hkv):
+                row = gi[si, h].tolist()
+                assert last in _kept_chunks(row, N, s), (si, h)
+                assert row[row.index(N - 1) + 1] == N, (si, h)    # the window follows the short chunk
 
 
 def test_select_chunks_zero_keys_exact_and_decode_skips_unused_slots():
@@ -124,8 +151,10 @@ def test_select_chunks_zero_keys_exact_and_decode_skips_unused_slots():
     g = np.random.default_rng(22)
     q = synth.f32_to_bf16_bits(g.standard_normal((S, W, Hq, 128)).astype(np.float32))
     k = np.zeros((S, Hkv, L, 128), np.uint16)
-    gi, _ = _check(k, q, [L], Hq, W, 100, 8, "zero keys")          # 10 chunks of 8, 4 slots of -1
+    gi, _ = _check(k, q, [L], Hq, W, 100, 8, "zero keys", cw=True)   # 10 chunks of 8, 4 slots of -1
     assert gi[0, 0].tolist() == list(range(80)) + list(range(684, 700)) + [-1] * 4
+    gp, _ = _check(k, q, [L], Hq, W, 100, 8, "zero keys")             # paper count: 12 chunks, 4 slots of -1
+    assert gp[0, 0].tolist() == list(range(96)) + list(range(684, 700)) + [-1] * 4
     # the attention calls skip the -1 slots: decode over this selection equals the oracle's
     kr = synth.f32_to_bf16_bits(g.standard_normal((S, Hkv, L, 128)).astype(np.float32))
     v = synth.f32_to_bf16_bits(g.standard_normal((S, Hkv, L, 128)).astype(np.float32))
@@ -144,5 +173,45 @@ def test_select_chunks_identity_when_budget_covers_the_cache():
     g = np.random.default_rng(23)
     k = synth.f32_to_bf16_bits(g.standard_normal((S, Hkv, 300, 128)).astype(np.float32))
     q = synth.f32_to_bf16_bits(g.standard_normal((S, W, Hq, 128)).astype(np.float32))
-    gi, _ = _check(k, q, [300, 120], Hq, W, 320, 8, "identity")
+    gi, _ = _check(k, q, [300, 120], Hq, W, 320, 8, "identity", cw=True)
     assert gi[1, 0].tolist() == list(range(120)) + [-1] * 200
+    gi, _ = _check(k, q, [300, 120], Hq, W, 320, 8, "identity")
+    assert gi[1, 0].tolist() == list(range(120)) + [-1] * 216
+    # B < L <= B + W: every prefix chunk fits, slots past L are -1
+    gi, _ = _check(k, q, [300, 120], Hq, W, 290, 8, "budget covers the prefix")
+    assert gi[0, 0].tolist() == list(range(300)) + [-1] * 6
+
+
+def _multiview_view_scores(cfg, qt, k):
+    """Oracle scores of the multiview workload's block (W = C = 64 rows, G = 4: 256 rows per KV head)."""
+    C, G = cfg.block_len, cfg.num_q_heads // cfg.num_kv_heads
+    sc = float(np.float64(np.float32(1.0 / np.sqrt(128))))
+    raws = []
+    for si in range(cfg.num_seqs):
+        qw = O.bf16_to_f64(qt[si, -C:])
+        raws.append([O.window_scores(O.bf16_to_f64(k[si, g]), qw[:, g * G:(g + 1) * G], cfg.seq_len, sc)
+                     for g in range(cfg.num_kv_heads)])
+    return raws
+
+
+def test_select_chunks_training_views_paper_count():
+    """Alg. 1 step 4 at the multiview training shape: the 64-row block scores the 8,128-position
+    prefix of each of the 4 sequences, and every budget B in {256, 512, 1024, 2048} keeps the top
+    floor(B/8) chunks with the block on top (Sec. 3.4), B + 64 slots per head."""
+    cfg = synth.workload("multiview-train-b4-8k")
+    qt, k, _ = config_data("multiview-train-b4-8k")
+    C = cfg.block_len
+    raws = _multiview_view_scores(cfg, qt, k)
+    lens = [cfg.seq_len] * cfg.num_seqs
+    for B in (256, 512, 1024, 2048):
+        gi, near = _check(k, np.ascontiguousarray(qt[:, -C:]), lens, cfg.num_q_heads, C, B, 8,
+                          "multiview views", raws=raws)
+        assert near <= 2
+        for si in range(cfg.num_seqs):
+            for g in range(cfg.num_kv_heads):
+                row = gi[si, g]
+                assert (row >= 0).sum() == 8 * (B // 8) + C        # floor(B/8) whole chunks + the block
+                assert row[8 * (B // 8):8 * (B // 8) + C].tolist() == list(range(cfg.seq_len - C, cfg.seq_len))
+        # the other reading at the same shape
+        _check(k, np.ascontiguousarray(qt[:, -C:]), lens, cfg.num_q_heads, C, B, 8, "multiview views", cw=True,
+               raws=raws)
