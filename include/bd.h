@@ -12,6 +12,7 @@
  *   bd_multiview_attn      a query block under several budgets + the full cache (Alg. 1)
  *   bd_multiview_attn_bwd  its gradients for the drafter's training losses (Alg. 1)
  *   bd_verify_attn         verifier attention at the gamma+1 draft positions (Eq. 1)
+ *   bd_verify_attn_noalloc the same with a fixed in-library scratch (no workspace)
  *   bd_accept_len          greedy accepted-prefix length and bonus token (Eq. 3)
  *   bd_cache_append        per-round cache growth (Alg. 2)
  *   bd_cache_rollback      rejected rows dropped after verification (Alg. 2)
@@ -278,6 +279,26 @@ size_t bd_verify_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, in
 bd_status bd_verify_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, int32_t gamma, float scale,
                          uint16_t* out, float* lse_out,
                          void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * bd_verify_attn_noalloc -- bd_verify_attn without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc).
+ *
+ * Same operation, arguments, kernels and results (bit for bit) as
+ * bd_verify_attn.  Its scratch (completion counters, then split records) is a
+ * fixed array of BD_NOALLOC_SCRATCH_BYTES inside the library, one per GPU, held
+ * until the process ends; nothing is allocated by this call or by the library.
+ * The first call on a device resolves the array's address and clears its counter
+ * region with one small kernel on `stream`.  Every call on a GPU shares that
+ * GPU's array: calls that overlap in time on one GPU (other streams, other host
+ * threads) race and must not be issued.  A shape whose plan needs more scratch
+ * than the fixed size returns BD_ERR_UNSUPPORTED before anything is launched
+ * (the 16K batch of 8 sequences, contiguous or paged, fits).
+ * ---------------------------------------------------------------------- */
+#define BD_NOALLOC_SCRATCH_BYTES 16777216
+bd_status bd_verify_attn_noalloc(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, int32_t gamma,
+                                 float scale, uint16_t* out, float* lse_out, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * bd_accept_len -- greedy acceptance (Eq. 3; Alg. 2 accept + bonus token).

@@ -9,7 +9,7 @@ raised.
 Functions carry the names of the C entry points:
 
     bd_select_kv, bd_select_kv_chunks, bd_sparse_decode_attn,
-    bd_multiview_attn, bd_multiview_attn_bwd, bd_verify_attn, bd_accept_len,
+    bd_multiview_attn, bd_multiview_attn_bwd, bd_verify_attn, bd_verify_attn_noalloc, bd_accept_len,
     bd_cache_append, bd_cache_rollback, bd_top1_ce, bd_sample_budgets
 
 KV caches are bf16 tensors, either contiguous ``[S][Hkv][L][128]`` or paged
@@ -29,7 +29,7 @@ import torch
 __all__ = [
     "BdError", "lib", "library_path", "kv_desc", "Workspace",
     "bd_select_kv", "bd_select_kv_chunks", "bd_sparse_decode_attn", "bd_multiview_attn", "bd_multiview_attn_bwd", "bd_verify_attn",
-    "bd_accept_len",
+    "bd_verify_attn_noalloc", "bd_accept_len",
     "bd_cache_append", "bd_cache_rollback", "bd_top1_ce", "bd_sample_budgets",
 ]
 
@@ -82,6 +82,7 @@ _SIGNATURES = {
                                      _P, _P, _P, _P, _SZ, _P]),
     "bd_verify_attn_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, _I32]),
     "bd_verify_attn": (_I32, [_KV, _P, _I32, _I32, _F32, _P, _P, _P, _SZ, _P]),
+    "bd_verify_attn_noalloc": (_I32, [_KV, _P, _I32, _I32, _F32, _P, _P, _P]),
     "bd_accept_len_workspace_bytes": (_SZ, [_I32, _I32, _I32]),
     "bd_accept_len": (_I32, [_P, _I64, _P, _I32, _I32, _I32, _P, _P, _P, _P, _SZ, _P]),
 }
@@ -351,6 +352,20 @@ def bd_verify_attn(k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, seq_lens: 
     _check(L.bd_verify_attn(ctypes.byref(kv), q.data_ptr(), Hq, gamma, _scale(scale), out.data_ptr(), _ptr(lse),
                             wp, wb, _stream()))
     return (out, lse) if return_lse else out
+
+
+def bd_verify_attn_noalloc(k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, seq_lens: torch.Tensor, *,
+                           out: torch.Tensor, lse: Optional[torch.Tensor] = None, scale: Optional[float] = None,
+                           page_table: Optional[torch.Tensor] = None, max_seq_len: Optional[int] = None) -> None:
+    """bd_verify_attn into caller-given outputs (out bf16 [S, gamma+1, Hq, 128], lse fp32 [S, gamma+1, Hq] or
+    None) with the library's fixed scratch: nothing is allocated, here or in the library."""
+    _require(q.dtype == torch.bfloat16 and q.dim() == 4 and q.is_contiguous(), "q must be contiguous bf16 [S,gamma+1,Hq,128]")
+    _require(out.dtype == torch.bfloat16 and out.shape == q.shape and out.is_contiguous(), "out must be shaped like q")
+    if lse is not None:
+        _require(lse.dtype == torch.float32 and lse.shape == q.shape[:3] and lse.is_contiguous(), "lse must be fp32 [S,gamma+1,Hq]")
+    kv = kv_desc(k, v, seq_lens, page_table, max_seq_len)
+    _check(lib().bd_verify_attn_noalloc(ctypes.byref(kv), q.data_ptr(), q.shape[2], q.shape[1] - 1, _scale(scale),
+                                        out.data_ptr(), _ptr(lse), _stream()))
 
 
 def bd_accept_len(logits: torch.Tensor, draft: torch.Tensor, *, return_argmax: bool = False,

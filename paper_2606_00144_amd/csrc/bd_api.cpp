@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 
 #include "bd.h"
 #include "bd_kernels.hpp"
@@ -69,6 +70,44 @@ bd_status launched(hipError_t e) {
   return BD_OK;
 }
 
+// ---- fixed scratch of the no-allocation entry point ---------------------------------------------
+// Counter region, then split records, of bd_verify_attn_noalloc.  Each GPU the library runs on holds
+// its own copy until the process ends.  In host code `scratch` only names the symbol: its device
+// address comes from hipGetSymbolAddress, once per device, and only that address is passed on.
+static __device__ __align__(256) uint8_t scratch[BD_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+__global__ void zero_words_kernel(uint4* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+// Device address of the current device's scratch.  The first call on a device resolves the address
+// and clears the counter region with a kernel on `stream` (the calls that follow on the stream run
+// after it; a completed call leaves the counters zero again).
+bd_status fixed_scratch(hipStream_t stream, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(BD_ERR_DEVICE, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(BD_ERR_UNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return fail(BD_ERR_DEVICE, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    constexpr int n = BD_WS_COUNTER_BYTES / 16;
+    hipLaunchKernelGGL(zero_words_kernel, dim3(n / 256), dim3(256), 0, stream, static_cast<uint4*>(p), n);
+    e = hipGetLastError();
+    if (e != hipSuccess) return fail(BD_ERR_DEVICE, "clearing the scratch counters: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return BD_OK;
+}
+
 // Largest element offset of the K/V layout plus one row; the attention kernel
 // keeps row offsets as int32 in 16-byte units.
 int64_t kv_extent(const bd_kv_desc* kv) {
@@ -84,7 +123,8 @@ int64_t kv_extent(const bd_kv_desc* kv) {
 bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t nq, int32_t num_views,
                    const int32_t* idx, int32_t ld_idx, const int32_t* nsel, float scale, uint16_t* out_views,
                    float* lse_views, uint16_t* out_full, float* lse_full, void* ws, size_t ws_bytes,
-                   hipStream_t stream, float* o32_views = nullptr, float* o32_full = nullptr) {
+                   hipStream_t stream, float* o32_views = nullptr, float* o32_full = nullptr,
+                   bool use_fixed_scratch = false) {
   const bool train = o32_views || o32_full;
   const bd::AttnPlan pl =
       bd::plan_attn(kv->num_seqs, kv->num_kv_heads, Hq, nq, num_views, ld_idx, kv->max_seq_len, out_full != nullptr,
@@ -98,10 +138,21 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
   if (pl.block && (int64_t)(pl.nW + pl.nbr) * 8 * bd::attn_record_floats(2) * 4 > INT32_MAX)
     return fail(BD_ERR_UNSUPPORTED, "too many partial records per unit");
   if (pl.block && pl.nbr > 64) return fail(BD_ERR_UNSUPPORTED, "more than 63 views with a block of more than 32 rows");
-  bd_status st = check_ws(ws, ws_bytes, pl.ws_bytes);
-  if (st != BD_OK) return st;
+  bd_status st = BD_OK;
+  if (use_fixed_scratch) {
+    if (pl.ws_bytes > (size_t)BD_NOALLOC_SCRATCH_BYTES)
+      return fail(BD_ERR_UNSUPPORTED, "this shape needs %zu bytes of scratch, above the fixed %d", pl.ws_bytes,
+                  BD_NOALLOC_SCRATCH_BYTES);
+  } else {
+    st = check_ws(ws, ws_bytes, pl.ws_bytes);
+    if (st != BD_OK) return st;
+  }
   if (pl.nblk == 0) return BD_OK;
   if (pl.nblk >= (1 << 22)) return fail(BD_ERR_UNSUPPORTED, "more than 2^22 - 1 workgroups");
+  if (use_fixed_scratch) {
+    st = fixed_scratch(stream, &ws);
+    if (st != BD_OK) return st;
+  }
   bd::AttnParams p{};
   p.kv = bd::make_kv_view(*kv);
   p.q = q;
@@ -420,6 +471,13 @@ bd_status bd_verify_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_
                   ws_bytes, stream);
 }
 
+bd_status bd_verify_attn_noalloc(const bd_kv_desc* kv, const uint16_t* q, int32_t num_q_heads, int32_t gamma,
+                                 float scale, uint16_t* out, float* lse_out, hipStream_t stream) {
+  const bd_status st = check_verify(kv, q, num_q_heads, gamma, scale, out);
+  if (st != BD_OK) return st;
+  return run_attn(kv, q, num_q_heads, gamma + 1, 0, nullptr, 0, nullptr, scale, nullptr, nullptr, out, lse_out,
+                  nullptr, 0, stream, nullptr, nullptr, true);
+}
 
 // ---------------------------------------------------------------- accept
 size_t bd_accept_len_workspace_bytes(int32_t num_seqs, int32_t gamma, int32_t vocab) {

@@ -80,6 +80,20 @@ def test_verify_rejections(L):
     assert b"workspace" in L.bd_last_error()
 
 
+def test_verify_noalloc_rejections(L):
+    # refused by host validation: nothing is launched and no device is touched
+    na = lambda kv, **a: L.bd_verify_attn_noalloc(ctypes.byref(kv), a.get("q", FAKE), 32, a.get("g", 5), 0.088,
+                                                  a.get("out", FAKE), None, None)
+    assert na(_kv(), g=-1) == bd.BD_ERR_INVALID_ARG
+    assert na(_kv(), out=FAKE + 2) == bd.BD_ERR_INVALID_ARG
+    assert na(_kv(head_dim=64)) == bd.BD_ERR_UNSUPPORTED
+    # 64 sequences x 32 KV heads paged up to 16384 rows: the plan's records exceed the fixed scratch
+    big = _kv(num_seqs=64, num_kv_heads=32, max_seq_len=16384, page_table=FAKE, page_size=16,
+              max_pages_per_seq=1024, num_pages=65536, stride_page=32 * 16 * 128, stride_head=16 * 128)
+    assert na(big) == bd.BD_ERR_UNSUPPORTED
+    assert b"scratch" in L.bd_last_error()
+
+
 def test_decode_select_multiview_accept_rejections(L):
     kv = _kv()
     assert L.bd_sparse_decode_attn(ctypes.byref(kv), FAKE, 32, FAKE, -1, FAKE, 0.1, FAKE, None, FAKE, 1 << 40, None) == 1
