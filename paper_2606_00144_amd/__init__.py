@@ -200,35 +200,51 @@ def _ws(op: str, nbytes: int, device, workspace: Optional[Workspace]):
 def bd_select_kv(k: torch.Tensor, q_win: torch.Tensor, seq_lens: torch.Tensor, budget: int, *,
                  pool_kernel: int = 7, scale: Optional[float] = None, lse_win: Optional[torch.Tensor] = None,
                  return_scores: bool = False, page_table: Optional[torch.Tensor] = None,
-                 max_seq_len: Optional[int] = None, workspace: Optional[Workspace] = None):
-    """Budgeted KV selection.  q_win: bf16 [S, W, Hq, 128].  Returns (idx [S,Hkv,B], nsel [S][, scores])."""
+                 max_seq_len: Optional[int] = None, workspace: Optional[Workspace] = None, outputs=None):
+    """Budgeted KV selection.  q_win: bf16 [S, W, Hq, 128].  Returns (idx [S,Hkv,B], nsel [S][, scores]).
+    outputs: optional preallocated (idx, nsel[, scores])."""
     return _select("bd_select_kv", (pool_kernel,), budget, k, q_win, seq_lens, budget, scale, lse_win,
-                   return_scores, page_table, max_seq_len, workspace)
+                   return_scores, page_table, max_seq_len, workspace, outputs)
 
 
 def bd_select_kv_chunks(k: torch.Tensor, q_win: torch.Tensor, seq_lens: torch.Tensor, budget: int, *,
                         chunk: int = 8, budget_counts_window: bool = False, scale: Optional[float] = None,
                         lse_win: Optional[torch.Tensor] = None, return_scores: bool = False,
                         page_table: Optional[torch.Tensor] = None, max_seq_len: Optional[int] = None,
-                        workspace: Optional[Workspace] = None):
+                        workspace: Optional[Workspace] = None, outputs=None):
     """Chunk-level selection (TopKChunks): the top floor(B/chunk) prefix chunks, then the window
     (budget_counts_window=True: floor((B-W)/chunk) chunks).  Returns (idx [S,Hkv,ld], nsel [S][, scores])
     with ld = B + W (or B); a head's unused idx slots hold -1."""
     W = q_win.shape[1]
     ld = budget if budget_counts_window else budget + W
     return _select("bd_select_kv_chunks", (chunk, int(bool(budget_counts_window))), ld, k, q_win, seq_lens, budget,
-                   scale, lse_win, return_scores, page_table, max_seq_len, workspace)
+                   scale, lse_win, return_scores, page_table, max_seq_len, workspace, outputs)
+
+
+def _out(given, shape, dtype, dev, what):
+    """A caller-given output (checked) or a new one."""
+    if given is None:
+        return torch.empty(shape, dtype=dtype, device=dev)
+    _require(given.dtype == dtype and tuple(given.shape) == tuple(shape) and given.is_contiguous(),
+             f"{what} must be contiguous {dtype} {tuple(shape)}")
+    return given
 
 
 def _select(entry, mode_args, ld, k, q_win, seq_lens, budget, scale, lse_win, return_scores, page_table, max_seq_len,
-            workspace):
+            workspace, outputs=None):
     _require(q_win.dtype == torch.bfloat16 and q_win.dim() == 4 and q_win.is_contiguous(), "q_win must be contiguous bf16 [S,W,Hq,128]")
     kv = kv_desc(k, None, seq_lens, page_table, max_seq_len)
     S, W, Hq = q_win.shape[0], q_win.shape[1], q_win.shape[2]
     dev = q_win.device
-    idx = torch.empty((S, kv.num_kv_heads, ld), dtype=torch.int32, device=dev)
-    nsel = torch.empty((S,), dtype=torch.int32, device=dev)
-    scores = torch.zeros((S, kv.num_kv_heads, kv.max_seq_len), dtype=torch.float32, device=dev) if return_scores else None
+    given = tuple(outputs) + (None,) * 3 if outputs is not None else (None,) * 3
+    idx = _out(given[0], (S, kv.num_kv_heads, ld), torch.int32, dev, "idx")
+    nsel = _out(given[1], (S,), torch.int32, dev, "nsel")
+    scores = None
+    if return_scores:
+        scores = given[2] if given[2] is not None else torch.zeros((S, kv.num_kv_heads, kv.max_seq_len),
+                                                                    dtype=torch.float32, device=dev)
+        _require(scores.dtype == torch.float32 and tuple(scores.shape) == (S, kv.num_kv_heads, kv.max_seq_len)
+                 and scores.is_contiguous(), "scores must be contiguous fp32 [S,Hkv,max_seq_len]")
     if lse_win is not None:
         _require(lse_win.dtype == torch.float32 and lse_win.is_contiguous() and lse_win.shape == (S, W, Hq), "lse_win must be fp32 [S,W,Hq]")
     L = lib()
@@ -242,15 +258,17 @@ def _select(entry, mode_args, ld, k, q_win, seq_lens, budget, scale, lse_win, re
 def bd_sparse_decode_attn(k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, idx: torch.Tensor, nsel: torch.Tensor,
                           seq_lens: torch.Tensor, *, scale: Optional[float] = None, return_lse: bool = False,
                           page_table: Optional[torch.Tensor] = None, max_seq_len: Optional[int] = None,
-                          out: Optional[torch.Tensor] = None, workspace: Optional[Workspace] = None):
-    """Drafter decode attention over selected entries.  q: bf16 [S, Hq, 128]; idx int32 [S, Hkv, ld]."""
+                          out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                          workspace: Optional[Workspace] = None):
+    """Drafter decode attention over selected entries.  q: bf16 [S, Hq, 128]; idx int32 [S, Hkv, ld].
+    out / lse: optional preallocated outputs."""
     _require(q.dtype == torch.bfloat16 and q.dim() == 3 and q.is_contiguous(), "q must be contiguous bf16 [S,Hq,128]")
     _require(idx.dtype == torch.int32 and idx.dim() == 3 and idx.is_contiguous(), "idx must be contiguous int32 [S,Hkv,ld]")
     _require(nsel.dtype == torch.int32 and nsel.is_contiguous(), "nsel must be int32 [S]")
     kv = kv_desc(k, v, seq_lens, page_table, max_seq_len)
     S, Hq = q.shape[0], q.shape[1]
-    out = torch.empty_like(q) if out is None else out
-    lse = torch.empty((S, Hq), dtype=torch.float32, device=q.device) if return_lse else None
+    out = _out(out, q.shape, torch.bfloat16, q.device, "out")
+    lse = _out(lse, (S, Hq), torch.float32, q.device, "lse") if return_lse else None
     L = lib()
     nb = L.bd_sparse_decode_attn_workspace_bytes(S, kv.num_kv_heads, Hq, idx.shape[2])
     wp, wb = _ws("decode", nb, q.device, workspace)
@@ -262,11 +280,12 @@ def bd_sparse_decode_attn(k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, idx
 def bd_multiview_attn(k: torch.Tensor, v: torch.Tensor, q_blk: torch.Tensor, idx_views: Optional[torch.Tensor],
                       nsel_views: Optional[torch.Tensor], seq_lens: torch.Tensor, *, scale: Optional[float] = None,
                       full: bool = True, train: bool = False, page_table: Optional[torch.Tensor] = None,
-                      max_seq_len: Optional[int] = None, workspace: Optional[Workspace] = None):
+                      max_seq_len: Optional[int] = None, workspace: Optional[Workspace] = None, outputs=None):
     """Block attention under views and the full cache.  q_blk: bf16 [S, C, Hq, 128]; idx_views int32 [V, S, Hkv, ld].
 
     Returns (out_views, out_full).  With train=True also the training outputs the backward takes:
-    (out_views, out_full, out32_views, lse_views, out32_full, lse_full).
+    (out_views, out_full, out32_views, lse_views, out32_full, lse_full).  outputs: optional
+    preallocated tensors in that order (None entries are allocated).
     """
     _require(q_blk.dtype == torch.bfloat16 and q_blk.dim() == 4 and q_blk.is_contiguous(), "q_blk must be contiguous bf16 [S,C,Hq,128]")
     kv = kv_desc(k, v, seq_lens, page_table, max_seq_len)
@@ -277,12 +296,13 @@ def bd_multiview_attn(k: torch.Tensor, v: torch.Tensor, q_blk: torch.Tensor, idx
         _require(idx_views.dtype == torch.int32 and idx_views.is_contiguous(), "idx_views must be contiguous int32 [V,S,Hkv,ld]")
         _require(nsel_views is not None and nsel_views.dtype == torch.int32 and nsel_views.shape == (V, S), "nsel_views must be int32 [V,S]")
     dev = q_blk.device
-    out_v = torch.empty((V, S, C, Hq, HEAD_DIM), dtype=torch.bfloat16, device=dev) if V else None
-    out_f = torch.empty_like(q_blk) if full else None
-    o32_v = torch.empty((V, S, C, Hq, HEAD_DIM), dtype=torch.float32, device=dev) if (V and train) else None
-    lse_v = torch.empty((V, S, C, Hq), dtype=torch.float32, device=dev) if (V and train) else None
-    o32_f = torch.empty((S, C, Hq, HEAD_DIM), dtype=torch.float32, device=dev) if (full and train) else None
-    lse_f = torch.empty((S, C, Hq), dtype=torch.float32, device=dev) if (full and train) else None
+    given = tuple(outputs) + (None,) * 6 if outputs is not None else (None,) * 6
+    out_v = _out(given[0], (V, S, C, Hq, HEAD_DIM), torch.bfloat16, dev, "out_views") if V else None
+    out_f = _out(given[1], (S, C, Hq, HEAD_DIM), torch.bfloat16, dev, "out_full") if full else None
+    o32_v = _out(given[2], (V, S, C, Hq, HEAD_DIM), torch.float32, dev, "out32_views") if (V and train) else None
+    lse_v = _out(given[3], (V, S, C, Hq), torch.float32, dev, "lse_views") if (V and train) else None
+    o32_f = _out(given[4], (S, C, Hq, HEAD_DIM), torch.float32, dev, "out32_full") if (full and train) else None
+    lse_f = _out(given[5], (S, C, Hq), torch.float32, dev, "lse_full") if (full and train) else None
     L = lib()
     nb = L.bd_multiview_attn_workspace_bytes(S, kv.num_kv_heads, Hq, C, V, ld, kv.max_seq_len, int(full))
     wp, wb = _ws("multiview", nb, dev, workspace)
@@ -299,8 +319,8 @@ def bd_multiview_attn_bwd(k: torch.Tensor, v: torch.Tensor, q_blk: torch.Tensor,
                           lse_full: Optional[torch.Tensor] = None, dout_full: Optional[torch.Tensor] = None, *,
                           scale: Optional[float] = None, with_dkv: bool = True,
                           page_table: Optional[torch.Tensor] = None, max_seq_len: Optional[int] = None,
-                          workspace: Optional[Workspace] = None):
-    """Gradients of bd_multiview_attn.  out32/lse are the forward's training outputs (train=True), dout
+                          workspace: Optional[Workspace] = None, grads=None):
+    """Gradients of bd_multiview_attn (grads: optional preallocated (dq, dk, dv)).  out32/lse are the forward's training outputs (train=True), dout
     the upstream gradients (bf16, shaped like the outputs).  Returns (dq [S,C,Hq,128], dk_blk, dv_blk [S,C,Hkv,128]) in fp32;
     dk_blk and dv_blk are None unless with_dkv."""
     _require(q_blk.dtype == torch.bfloat16 and q_blk.dim() == 4 and q_blk.is_contiguous(), "q_blk must be contiguous bf16 [S,C,Hq,128]")
@@ -322,9 +342,10 @@ def bd_multiview_attn_bwd(k: torch.Tensor, v: torch.Tensor, q_blk: torch.Tensor,
             _require(t is not None and t.dtype == dt and tuple(t.shape) == shp and t.is_contiguous(),
                      f"full-branch tensors must be contiguous {dt} {shp}")
     dev = q_blk.device
-    dq = torch.empty((S, C, Hq, HEAD_DIM), dtype=torch.float32, device=dev)
-    dk = torch.empty((S, C, kv.num_kv_heads, HEAD_DIM), dtype=torch.float32, device=dev) if with_dkv else None
-    dv = torch.empty_like(dk) if with_dkv else None
+    given = tuple(grads) + (None,) * 3 if grads is not None else (None,) * 3
+    dq = _out(given[0], (S, C, Hq, HEAD_DIM), torch.float32, dev, "dq")
+    dk = _out(given[1], (S, C, kv.num_kv_heads, HEAD_DIM), torch.float32, dev, "dk") if with_dkv else None
+    dv = _out(given[2], (S, C, kv.num_kv_heads, HEAD_DIM), torch.float32, dev, "dv") if with_dkv else None
     L = lib()
     nb = L.bd_multiview_attn_bwd_workspace_bytes(S, kv.num_kv_heads, Hq, C, V, ld, kv.max_seq_len, int(full))
     wp, wb = _ws("multiview_bwd", nb, dev, workspace)
@@ -338,14 +359,15 @@ def bd_multiview_attn_bwd(k: torch.Tensor, v: torch.Tensor, q_blk: torch.Tensor,
 def bd_verify_attn(k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, seq_lens: torch.Tensor, *,
                    scale: Optional[float] = None, return_lse: bool = False, page_table: Optional[torch.Tensor] = None,
                    max_seq_len: Optional[int] = None, out: Optional[torch.Tensor] = None,
-                   workspace: Optional[Workspace] = None):
-    """Verifier attention at the gamma+1 draft positions.  q: bf16 [S, gamma+1, Hq, 128]."""
+                   lse: Optional[torch.Tensor] = None, workspace: Optional[Workspace] = None):
+    """Verifier attention at the gamma+1 draft positions.  q: bf16 [S, gamma+1, Hq, 128].
+    out / lse: optional preallocated outputs."""
     _require(q.dtype == torch.bfloat16 and q.dim() == 4 and q.is_contiguous(), "q must be contiguous bf16 [S,gamma+1,Hq,128]")
     kv = kv_desc(k, v, seq_lens, page_table, max_seq_len)
     S, R, Hq = q.shape[0], q.shape[1], q.shape[2]
     gamma = R - 1
-    out = torch.empty_like(q) if out is None else out
-    lse = torch.empty((S, R, Hq), dtype=torch.float32, device=q.device) if return_lse else None
+    out = _out(out, q.shape, torch.bfloat16, q.device, "out")
+    lse = _out(lse, (S, R, Hq), torch.float32, q.device, "lse") if return_lse else None
     L = lib()
     nb = L.bd_verify_attn_workspace_bytes(S, kv.num_kv_heads, Hq, gamma, kv.max_seq_len)
     wp, wb = _ws("verify", nb, q.device, workspace)

@@ -101,6 +101,10 @@ CONFIGS: List[Config] = [
     Config(3, "multiview-train-b4-8k", 4, 32, 8, 8192, 0.01, 64, (), 5, 0, block_len=64, num_views=4),
     Config(4, "ragged-paged-b64-mha", 64, 32, 32, 16384, 0.01, 32, (1024,), 5, 32000,
            ragged_min_len=4096, page_size=16),
+    # the paper's training shape (Sec. 4: T = 16,384 = P + C with C = 256, batch size 1): one
+    # sequence, the 256-row continuation block scores the prefix, and the views take every budget of
+    # the training set {256, 512, 1024, 2048} (Sec. 3.4) beside the full branch
+    Config(5, "train-c256-16k", 1, 32, 8, 16384, 0.01, 256, (256, 512, 1024, 2048), 5, 0, block_len=256),
 ]
 WORKLOADS = {c.name: c for c in CONFIGS}
 

@@ -18,78 +18,11 @@ import torch
 import oracle as O
 import paper_2606_00144_amd as bd
 import synth
-from gpu_utils import assert_close, assert_lse, bf16_dev, bf16_host64, case, config_data, i32_dev, paged_kv
+from gpu_utils import (bf16_dev, case, check_chunk_selection, config_data, i32_dev, oracle_chunk_selection,
+                       oracle_scores, paged_kv)
+from mv_check import _rand_bits, _run
 
 pytestmark = pytest.mark.gpu
-
-GRAD_ATOL_FRAC, GRAD_RTOL = 1e-3, 1e-3
-
-
-def _rand_bits(shape, seed, scale=1.0):
-    g = np.random.default_rng(seed)
-    return synth.f32_to_bf16_bits(scale * g.standard_normal(shape, dtype=np.float32))
-
-
-def _grad_close(gpu, ref, what):
-    atol = GRAD_ATOL_FRAC * max(float(np.abs(ref).max(initial=0.0)), 1e-30)
-    return assert_close(gpu, ref, what, atol=atol, rtol=GRAD_RTOL)
-
-
-def _out32_close(gpu, ref, what):
-    atol = 1e-4 * max(float(np.abs(ref).max(initial=0.0)), 1e-30)
-    return assert_close(gpu.cpu().numpy().astype(np.float64), ref, what, atol=atol, rtol=1e-4)
-
-
-def _run(k, v, qb, idx_v, nsel_v, lens, what, full=True, seed=0, kdev=None, vdev=None, page_table=None,
-         check_fwd=True, seqs=None, with_dkv=True, workspace=None):
-    """Training forward, backward with seeded dO; compare dq / dk / dv (on `seqs`, default all) with the oracle."""
-    S, C, Hq = qb.shape[0], qb.shape[1], qb.shape[2]
-    V = 0 if idx_v is None else len(idx_v)
-    kd = bf16_dev(k) if kdev is None else kdev
-    vd = bf16_dev(v) if vdev is None else vdev
-    iv = i32_dev(idx_v) if V else None
-    nv = i32_dev(nsel_v) if V else None
-    ld = i32_dev(lens)
-    case(f"multiview bwd forward {what}")
-    ov, of, o32v, lv, o32f, lf = bd.bd_multiview_attn(kd, vd, bf16_dev(qb), iv, nv, ld, full=full, train=True,
-                                                      page_table=page_table, max_seq_len=int(max(lens)))
-    dov_bits = _rand_bits((V, S, C, Hq, 128), 1000 + seed) if V else None
-    dof_bits = _rand_bits((S, C, Hq, 128), 2000 + seed) if full else None
-    case(f"multiview bwd {what}")
-    dq, dk, dv = bd.bd_multiview_attn_bwd(kd, vd, bf16_dev(qb), iv, nv, ld, o32v, lv,
-                                          bf16_dev(dov_bits) if V else None, o32f, lf,
-                                          bf16_dev(dof_bits) if full else None, with_dkv=with_dkv,
-                                          page_table=page_table, max_seq_len=int(max(lens)), workspace=workspace)
-    torch.cuda.synchronize()
-    seqs = list(range(S)) if seqs is None else seqs
-    for s in seqs:
-        sl = slice(s, s + 1)
-        ks = [k[s]] if isinstance(k, list) else k[sl]
-        vs = [v[s]] if isinstance(v, list) else v[sl]
-        iv_s = [x[sl] for x in idx_v] if V else []
-        nv_s = [x[sl] for x in nsel_v] if V else []
-        dov = [synth.bf16_bits_to_f32(dov_bits[i, sl]).astype(np.float64) for i in range(V)]
-        dof = synth.bf16_bits_to_f32(dof_bits[sl]).astype(np.float64) if full else None
-        if check_fwd:
-            rv, rf, rlv, rlf = O.multiview_attn(ks, vs, qb[sl], iv_s, nv_s, lens[s:s + 1], with_full=full,
-                                                return_lse=True)
-            if V:
-                assert_close(bf16_host64(ov[:, sl]), rv, f"{what} seq {s} views out")
-                assert_lse(lv[:, sl].cpu().numpy().astype(np.float64), rlv, f"{what} seq {s} views lse")
-                _out32_close(o32v[:, sl], rv, f"{what} seq {s} views out32")
-            if full:
-                assert_close(bf16_host64(of[sl]), rf, f"{what} seq {s} full out")
-                assert_lse(lf[sl].cpu().numpy().astype(np.float64), rlf, f"{what} seq {s} full lse")
-                _out32_close(o32f[sl], rf, f"{what} seq {s} full out32")
-        rq, rk, rvv = O.multiview_attn_bwd(ks, vs, qb[sl], iv_s, nv_s, lens[s:s + 1], dov, dof)
-        _grad_close(dq[sl].cpu().numpy().astype(np.float64), rq, f"{what} seq {s} dq")
-        if with_dkv:
-            _grad_close(dk[sl].cpu().numpy().astype(np.float64), rk, f"{what} seq {s} dk")
-            _grad_close(dv[sl].cpu().numpy().astype(np.float64), rvv, f"{what} seq {s} dv")
-        else:
-            assert dk is None and dv is None
-    return dq, dk, dv
-
 
 def _selected_views(k, qb, lens, Hq, C, budgets):
     S, Hkv = k.shape[0], k.shape[1]
@@ -197,9 +130,9 @@ def test_bwd_paged_cache():
     _run(k, v, qb, idx_v, nsel_v, lens, "paged", seed=7, kdev=kd, vdev=vd, page_table=i32_dev(table))
 
 
-def test_bwd_multiview4x8k_full_size_sampled():
-    """The multi-view training block at full size (4 x 8,192, C = 64, four budgets + full); the oracle
-    checks one sequence, all heads and branches."""
+def test_bwd_multiview4x8k_full_size():
+    """The multi-view training block at full size (4 x 8,192, C = 64, four budgets + full) over seeded
+    index lists; every sequence, head and branch is checked, forward and backward."""
     cfg = synth.workload("multiview-train-b4-8k")
     qt, k, v = config_data("multiview-train-b4-8k")
     C = cfg.block_len
@@ -215,7 +148,7 @@ def test_bwd_multiview4x8k_full_size_sampled():
                 idx_v[i, s, h, :int(B)] = np.r_[pre, np.arange(cfg.seq_len - C, cfg.seq_len)]
         nsel_v[i] = B
     lens = [cfg.seq_len] * S
-    _run(k, v, qt[:, -C:], idx_v, nsel_v, lens, "multiview 4x8K full size", seed=8, seqs=[2], check_fwd=False)
+    _run(k, v, qt[:, -C:], idx_v, nsel_v, lens, "multiview 4x8K full size", seed=8)
 
 
 def test_bwd_deterministic_and_workspace_reuse():
@@ -251,3 +184,35 @@ def test_bwd_two_row_groups_and_many_views():
                 idx_v[i, s, h, :n] = np.sort(g.choice(L, n, replace=False))
             nsel_v[i, s] = n
     _run(k, v, qb, idx_v, nsel_v, [L, L - 3], "two row groups, nine views", seed=10)
+
+
+@pytest.mark.timeout(600)
+def test_training_shape_c256_16k_chunk_views():
+    """Sec. 4's training shape: T = 16,384 (P = 16,128, C = 256), batch 1, GQA 32/8, so C * G = 1,024
+    query rows per KV head (four row groups).  The views are the paper's TopKChunks selections (the top
+    floor(B/8) chunks of the prefix, the block on top) for every budget of the training set, selected on
+    the GPU with the block scoring the prefix; then the forward (bf16 and training outputs) and the
+    backward over those views and the full branch, against the oracle."""
+    cfg = synth.workload("train-c256-16k")
+    qt, k, v = config_data("train-c256-16k")
+    C, Hkv, s = cfg.block_len, cfg.num_kv_heads, 8
+    lens = [cfg.seq_len]
+    qb = np.ascontiguousarray(qt[:, -C:])
+    raws = oracle_scores(k, qb, lens, cfg.num_q_heads)
+    kd = bf16_dev(k)
+    budgets = list(cfg.budgets)
+    ld = max(budgets) + C
+    idx_v = np.full((len(budgets), 1, Hkv, ld), -1, np.int32)
+    nsel_v = np.zeros((len(budgets), 1), np.int32)
+    for i, B in enumerate(budgets):
+        case(f"training shape: chunk selection B={B}")
+        idx, nsel, scores = bd.bd_select_kv_chunks(kd, bf16_dev(qb), i32_dev(lens), B, chunk=s, return_scores=True)
+        torch.cuda.synchronize()
+        gi, gn, gs = idx.cpu().numpy(), nsel.cpu().numpy(), scores.cpu().numpy()
+        oi, on = oracle_chunk_selection(raws, lens, Hkv, C, B, s, False)
+        near = check_chunk_selection(gi, gn, gs, oi, on, raws, lens, C, B, s, False, f"training shape B={B}")
+        assert near <= 2, near
+        assert ((gi >= 0).sum(axis=2) == s * (B // s) + C).all()
+        idx_v[i, :, :, :B + C] = gi
+        nsel_v[i] = gn
+    _run(k, v, qb, idx_v, nsel_v, lens, "training shape C=256 16K", seed=12, kdev=kd)

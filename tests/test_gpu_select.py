@@ -139,6 +139,37 @@ def test_select_lse_input_matches_two_pass():
     _check(k, q, [L, L], Hq, W, 200, "two-pass")
 
 
+@pytest.mark.parametrize("Hq,Hkv,W", [(8, 8, 16), (4, 2, 4), (2, 2, 1)])
+def test_select_one_row_tile(Hq, Hkv, W):
+    # W * G <= 16 observation rows per KV head: the one-row-tile scoring path (padded rows see no key)
+    S = 2
+    lens = [2500, 777]
+    g = np.random.default_rng(31 + W)
+    k = synth.f32_to_bf16_bits(g.standard_normal((S, Hkv, max(lens), 128)).astype(np.float32))
+    q = synth.f32_to_bf16_bits(g.standard_normal((S, W, Hq, 128)).astype(np.float32))
+    near = _check(k, q, lens, Hq, W, 200, f"one row tile Hq={Hq} Hkv={Hkv} W={W}")
+    assert near <= 1
+
+
+def test_select_lse_input_indices_match_the_oracle():
+    # the one-pass variant (the caller gives each window row's log-sum-exp) on the 8K layer: its indices
+    # under the same two-part protocol as the two-pass selection
+    cfg = synth.workload("llama3-8b-layer-8k")
+    qt, k, _ = config_data("llama3-8b-layer-8k")
+    W, L, Hq, G = cfg.window, cfg.seq_len, cfg.num_q_heads, cfg.num_q_heads // cfg.num_kv_heads
+    qw = np.ascontiguousarray(qt[:, -W:])
+    sc = float(np.float32(1 / np.sqrt(128)))
+    kf, qf = O.bf16_to_f64(k[0]), O.bf16_to_f64(qw[0])
+    lse = np.zeros((1, W, Hq), np.float32)
+    for h in range(Hq):
+        lg = sc * (qf[:, h] @ kf[h // G].T)                        # [W][L]
+        for i in range(W):
+            lse[0, i, h] = np.logaddexp.reduce(lg[i, :L - W + i + 1])
+    for B in (256, 1024):
+        near = _check(k, qw, [L], Hq, W, B, f"lse input B={B}", lse_win=torch.from_numpy(lse).cuda())
+        assert near <= 2
+
+
 def test_select_ragged_paged_mha():
     cfg = synth.workload("ragged-paged-b64-mha")
     lens = synth.seq_lens(cfg)[:4]

@@ -14,46 +14,10 @@ import torch
 import oracle as O
 import paper_2606_00144_amd as bd
 import synth
-from gpu_utils import assert_close, assert_lse, bf16_dev, bf16_host64, case, config_data, i32_dev
+from gpu_utils import (assert_close, assert_lse, bf16_dev, bf16_host64, case, check_chunk_selection, config_data,
+                       i32_dev, oracle_chunk_selection, oracle_scores)
 
 pytestmark = pytest.mark.gpu
-DELTA = 1e-4
-
-
-def _fp32_chunk_sums(raw32, N, s):
-    nc = (N + s - 1) // s
-    pad = np.zeros(nc * s, np.float32)
-    pad[:N] = raw32[:N]
-    pad = pad.reshape(nc, s)
-    acc = np.zeros(nc, np.float32)
-    for j in range(s):                       # left to right, rounded to fp32 after every addition
-        acc = (acc + pad[:, j]).astype(np.float32)
-    return acc
-
-
-def _kept_chunks(idx_row, N, s):
-    return sorted({int(t) // s for t in idx_row if 0 <= t < N})
-
-
-def _oracle(k, q_win, lens, Hq, W, B, s, cw, raws=None):
-    """The oracle's selection; with raws (oracle scores per sequence, [Hkv][L]) given, only its
-    ranking steps run (the scores do not depend on B)."""
-    if raws is None:
-        return O.select_kv_chunks(k, q_win, lens, Hq, W, B, s, budget_counts_window=cw)
-    S, Hkv = len(lens), k.shape[1]
-    ld = B if cw else B + W
-    idx = np.full((S, Hkv, ld), -1, np.int32)
-    nsel = np.zeros(S, np.int32)
-    for si, L in enumerate(lens):
-        if B >= L:
-            idx[si, :, :L] = np.arange(L)
-            nsel[si] = L
-            continue
-        for g in range(Hkv):
-            sel, _ = O.topk_chunks_from_scores(raws[si][g], L, W, B, s, budget_counts_window=cw)
-            idx[si, g, :sel.size] = sel
-        nsel[si] = min(ld, L)
-    return idx, nsel, raws
 
 
 def _check(k, q_win, lens, Hq, W, B, s, what, cw=False, raws=None, lse_win=None):
@@ -63,36 +27,11 @@ def _check(k, q_win, lens, Hq, W, B, s, what, cw=False, raws=None, lse_win=None)
                                                lse_win=None if lse_win is None else torch.from_numpy(lse_win).cuda())
     torch.cuda.synchronize()
     gi, gn, gs = idx.cpu().numpy(), nsel.cpu().numpy(), scores.cpu().numpy()
-    oi, on, oraw = _oracle(k, q_win, lens, Hq, W, B, s, cw, raws)
-    ld = B if cw else B + W
-    assert gi.shape[2] == ld and oi.shape == gi.shape, what
-    assert np.array_equal(gn, on), what
-    near = 0
-    for si in range(len(lens)):
-        L = int(lens[si])
-        for g in range(gi.shape[1]):
-            if B >= L:
-                assert np.array_equal(gi[si, g], oi[si, g]), (what, si, g)
-                continue
-            N = L - W
-            keep = min(((B - W) if cw else B) // s, (N + s - 1) // s)
-            # layout: kept chunk positions ascending, the window, then -1
-            cs32 = _fp32_chunk_sums(gs[si, g], N, s)
-            order = np.lexsort((np.arange(cs32.size), -cs32.astype(np.float64)))
-            want_chunks = np.sort(order[:keep])
-            want = [t for c in want_chunks for t in range(c * s, min((c + 1) * s, N))]
-            want = want + list(range(N, L))
-            want = want + [-1] * (ld - len(want))
-            assert gi[si, g].tolist() == want, (what, "chunk ranking stage", si, g)
-            # (ii) end to end
-            diff = set(_kept_chunks(gi[si, g], N, s)) ^ set(_kept_chunks(oi[si, g], N, s))
-            if diff:
-                cs = O.chunk_scores(oraw[si][g][:N], s)
-                thr = np.sort(cs)[::-1][keep - 1]
-                for c in diff:
-                    assert abs(cs[c] - thr) <= DELTA * thr, (what, si, g, c, cs[c], thr)
-                near += 1
-    return gi, near
+    if raws is None:
+        oi, on, raws = O.select_kv_chunks(k, q_win, lens, Hq, W, B, s, budget_counts_window=cw)
+    else:
+        oi, on = oracle_chunk_selection(raws, lens, k.shape[1], W, B, s, cw)
+    return gi, check_chunk_selection(gi, gn, gs, oi, on, raws, lens, W, B, s, cw, what)
 
 
 @pytest.mark.parametrize("cw", [False, True])
@@ -142,7 +81,7 @@ def test_select_chunks_short_last_chunk_taken(s):
         for si in range(S):
             for h in range(Hkv):
                 row = gi[si, h].tolist()
-                assert last in _kept_chunks(row, N, s), (si, h)
+                assert last in sorted({int(t) // s for t in row if 0 <= t < N}), (si, h)
                 assert row[row.index(N - 1) + 1] == N, (si, h)    # the window follows the short chunk
 
 
@@ -182,18 +121,6 @@ def test_select_chunks_identity_when_budget_covers_the_cache():
     assert gi[0, 0].tolist() == list(range(300)) + [-1] * 6
 
 
-def _multiview_view_scores(cfg, qt, k):
-    """Oracle scores of the multiview workload's block (W = C = 64 rows, G = 4: 256 rows per KV head)."""
-    C, G = cfg.block_len, cfg.num_q_heads // cfg.num_kv_heads
-    sc = float(np.float64(np.float32(1.0 / np.sqrt(128))))
-    raws = []
-    for si in range(cfg.num_seqs):
-        qw = O.bf16_to_f64(qt[si, -C:])
-        raws.append([O.window_scores(O.bf16_to_f64(k[si, g]), qw[:, g * G:(g + 1) * G], cfg.seq_len, sc)
-                     for g in range(cfg.num_kv_heads)])
-    return raws
-
-
 def test_select_chunks_training_views_paper_count():
     """Alg. 1 step 4 at the multiview training shape: the 64-row block scores the 8,128-position
     prefix of each of the 4 sequences, and every budget B in {256, 512, 1024, 2048} keeps the top
@@ -201,8 +128,8 @@ def test_select_chunks_training_views_paper_count():
     cfg = synth.workload("multiview-train-b4-8k")
     qt, k, _ = config_data("multiview-train-b4-8k")
     C = cfg.block_len
-    raws = _multiview_view_scores(cfg, qt, k)
     lens = [cfg.seq_len] * cfg.num_seqs
+    raws = oracle_scores(k, qt[:, -C:], lens, cfg.num_q_heads)
     for B in (256, 512, 1024, 2048):
         gi, near = _check(k, np.ascontiguousarray(qt[:, -C:]), lens, cfg.num_q_heads, C, B, 8,
                           "multiview views", raws=raws)
