@@ -536,22 +536,32 @@ def cache_append(k, v, seq_lens, k_new, v_new, idx=None, nsel=None):
     return (k, v, lens) if idx is None else (k, v, lens, idx, nsel)
 
 
-def cache_rollback(seq_lens, accept, spec: int, nsel=None):
+def cache_rollback(seq_lens, accept, spec: int, nsel=None, base_lens=None, base_nsel=None):
     """Drop the rejected speculative rows after verification (Alg. 2, cache update).
 
-    Each sequence ends in ``spec`` speculative rows, of which the first accept[s]
-    were accepted (accept is clamped to [0, spec]): spec - accept[s] rows are
-    dropped from L_s (and from nsel[s], the drafter's sparse list, when given),
-    never below zero.  Returns (seq_lens[, nsel]).
+    Each sequence ends in ``spec`` speculative rows, of which the first accept[s] were accepted
+    (accept is clamped to [0, spec]).  Without base lengths, spec - accept[s] rows are dropped from
+    L_s (and from nsel[s], the drafter's sparse list, when given), never below zero.  With the
+    lengths from before the speculative appends (``base_lens``, and ``base_nsel`` for the list),
+    L_s becomes min(L_s, base_lens[s] + accept[s]) and nsel[s] min(nsel[s], base_nsel[s] + accept[s]):
+    an accepted row is kept only if it was written, so rows an append dropped at the capacity (or
+    list entries dropped past the list's end) are never taken off a second time.
+    Returns (seq_lens[, nsel]).
     """
     lens = np.array(seq_lens, dtype=np.int64)
     acc = np.clip(np.asarray(accept, dtype=np.int64), 0, spec)
-    drop = spec - acc
-    lens = np.maximum(lens - drop, 0).astype(np.int32)
+    if base_lens is None:
+        lens = np.maximum(lens - (spec - acc), 0).astype(np.int32)
+    else:
+        lens = np.minimum(lens, np.asarray(base_lens, dtype=np.int64) + acc).astype(np.int32)
     if nsel is None:
         return lens
-    ns = np.maximum(np.asarray(nsel, dtype=np.int64) - drop, 0).astype(np.int32)
-    return lens, ns
+    ns = np.asarray(nsel, dtype=np.int64)
+    if base_nsel is None:
+        ns = np.maximum(ns - (spec - acc), 0)
+    else:
+        ns = np.minimum(ns, np.asarray(base_nsel, dtype=np.int64) + acc)
+    return lens, ns.astype(np.int32)
 
 
 # --------------------------------------------------------------------------

@@ -660,6 +660,31 @@ def test_rollback_keeps_the_accepted_prefix():
         assert l_rb.tolist() == l_k.tolist()
 
 
+@pytest.mark.parametrize("L0,nsel0,ld", [(10, 5, 32), (29, 5, 32), (10, 30, 32), (31, 31, 32), (32, 32, 32)])
+def test_rollback_from_base_lengths_equals_appending_only_the_accepted_rows(L0, nsel0, ld):
+    # capacity 32 rows, a list of ld slots: appending gamma speculative rows and rolling back to the
+    # base lengths plus the accepted count must equal appending only the accepted rows, also where the
+    # appends ran into the capacity or the end of the list (rows and slots that were never written)
+    S, cap, gamma = 1, 32, 4
+    g = np.random.default_rng(42)
+    k = bits(g.standard_normal((S, 1, cap, 128)))
+    new = bits(g.standard_normal((S, gamma, 1, 128)))
+    idx = np.full((S, 1, ld), -1, np.int32)
+    idx[0, 0, :nsel0] = np.arange(nsel0) % max(L0, 1)
+    for kacc in range(gamma + 1):
+        _, _, l_all, i_all, n_all = O.cache_append(k, k, [L0], new, new, idx, [nsel0])
+        l_rb, n_rb = O.cache_rollback(l_all, [kacc], gamma, nsel=n_all, base_lens=[L0], base_nsel=[nsel0])
+        _, _, l_k, i_k, n_k = O.cache_append(k, k, [L0], new[:, :kacc], new[:, :kacc], idx, [nsel0])
+        assert l_rb.tolist() == l_k.tolist() and n_rb.tolist() == n_k.tolist(), kacc
+        assert np.array_equal(i_all[0, 0, :n_rb[0]], i_k[0, 0, :n_k[0]])
+    # the subtractive rule assumes every speculative row was written: with a full list it would
+    # take committed entries off, the base rule does not
+    if nsel0 + gamma > ld:
+        _, _, l_all, _, n_all = O.cache_append(k, k, [L0], new, new, idx, [nsel0])
+        _, n_sub = O.cache_rollback(l_all, [0], gamma, nsel=n_all)
+        assert n_sub[0] < nsel0
+
+
 # ---------------------------------------------------------------- top-1 CE (Eqs. 5-7) and budget sampling
 
 def test_top1_ce_matches_torch_cross_entropy_and_targets():
