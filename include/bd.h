@@ -15,7 +15,7 @@
  *   bd_verify_attn_noalloc the same with a fixed in-library scratch (no workspace)
  *   bd_accept_len          greedy accepted-prefix length and bonus token (Eq. 3)
  *   bd_cache_append        per-round cache growth (Alg. 2)
- *   bd_cache_rollback      rejected rows dropped after verification (Alg. 2)
+ *   bd_cache_rollback      the accepted speculative rows kept after verification (Alg. 2)
  *   bd_top1_ce             top-1 cross-entropy against the verifier (Eqs. 5-7)
  *   bd_sample_budgets      B ~ Cat(B, w) per training sample (Alg. 1)
  *
@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define BD_ABI_VERSION 2
+#define BD_ABI_VERSION 3
 #define BD_HEAD_DIM 128
 /* Longest candidate prefix L_s - W that bd_select_kv ranks in one pass. */
 #define BD_SELECT_MAX_PREFIX 32768
@@ -339,18 +339,25 @@ bd_status bd_cache_append(const bd_kv_desc* kv, const uint16_t* k_new, const uin
                           int32_t* idx, int32_t ld_idx, int32_t* nsel, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
- * bd_cache_rollback -- drop rejected speculative rows after verification
+ * bd_cache_rollback -- keep the accepted speculative rows after verification
  * (Alg. 2, cache update after the accept step).
  *
- * Each sequence's last `spec` rows are speculative and the first accept[s]
- * of them (clamped to [0, spec]) were accepted: spec - accept[s] rows are
- * dropped from seq_lens[s], and from nsel[s] when nsel is given (the
- * drafter's sparse list, whose last entries are those rows), never below 0.
- * seq_lens, nsel: device int32 [S], updated in place; accept: device [S]
- * (e.g. bd_accept_len's accept_out).  One launch on `stream`.
+ * Each sequence's last `spec` rows are speculative and the first accept[s] of
+ * them (clamped to [0, spec]) were accepted.
+ *   base_lens given (the lengths before this round's speculative appends, e.g. a
+ *     device copy of seq_lens taken before them): seq_lens[s] = min(seq_lens[s],
+ *     base_lens[s] + accept[s]); with base_nsel likewise nsel[s] = min(nsel[s],
+ *     base_nsel[s] + accept[s]).  Rows an append dropped at the capacity, and
+ *     list entries it dropped past ld_idx, were never counted, so an accepted row
+ *     stays only if it was written and no committed row or entry is removed.
+ *   base_lens / base_nsel NULL: spec - accept[s] is subtracted (never below 0),
+ *     which is right only when every speculative row and list entry was written.
+ * seq_lens, nsel: device int32 [S], updated in place (nsel may be NULL; base_nsel
+ * needs nsel); accept: device [S] (e.g. bd_accept_len's accept_out); base_lens,
+ * base_nsel: NULL or device [S].  One launch on `stream`.
  * ---------------------------------------------------------------------- */
 bd_status bd_cache_rollback(int32_t* seq_lens, int32_t* nsel, const int32_t* accept, int32_t num_seqs, int32_t spec,
-                            hipStream_t stream);
+                            const int32_t* base_lens, const int32_t* base_nsel, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * bd_top1_ce -- top-1 cross-entropy of the drafter against the verifier's

@@ -69,7 +69,7 @@ _SIGNATURES = {
     "bd_select_kv": (_I32, [_KV, _P, _I32, _I32, _I32, _I32, _F32, _P, _P, _P, _P, _P, _SZ, _P]),
     "bd_select_kv_chunks": (_I32, [_KV, _P, _I32, _I32, _I32, _I32, _I32, _F32, _P, _P, _P, _P, _P, _SZ, _P]),
     "bd_cache_append": (_I32, [_KV, _P, _P, _I32, _P, _I32, _P, _P]),
-    "bd_cache_rollback": (_I32, [_P, _P, _P, _I32, _I32, _P]),
+    "bd_cache_rollback": (_I32, [_P, _P, _P, _I32, _I32, _P, _P, _P]),
     "bd_top1_ce_workspace_bytes": (_SZ, [_I32, _I32]),
     "bd_top1_ce": (_I32, [_P, ctypes.c_int64, _P, ctypes.c_int64, _P, _I32, _I32, _P, _P, _P, _P, _SZ, _P]),
     "bd_sample_budgets": (_I32, [_P, _I32, _P, _P, _I32, _P, _P]),
@@ -432,14 +432,17 @@ def bd_cache_append(k: torch.Tensor, v: torch.Tensor, seq_lens: torch.Tensor, k_
 
 
 def bd_cache_rollback(seq_lens: torch.Tensor, accept: torch.Tensor, spec: int, *,
-                      nsel: Optional[torch.Tensor] = None) -> None:
-    """Drop spec - accept[s] speculative rows from seq_lens (and nsel) in place."""
+                      nsel: Optional[torch.Tensor] = None, base_lens: Optional[torch.Tensor] = None,
+                      base_nsel: Optional[torch.Tensor] = None) -> None:
+    """Keep the accepted speculative rows in place: with base_lens (and base_nsel), the lengths before the
+    speculative appends, seq_lens = min(seq_lens, base + accept); without, spec - accept is subtracted."""
     _require(seq_lens.dtype == torch.int32 and seq_lens.is_contiguous(), "seq_lens must be int32 [S]")
     _require(accept.dtype == torch.int32 and accept.shape == seq_lens.shape, "accept must be int32 [S]")
-    if nsel is not None:
-        _require(nsel.dtype == torch.int32 and nsel.shape == seq_lens.shape, "nsel must be int32 [S]")
+    for t, n in ((nsel, "nsel"), (base_lens, "base_lens"), (base_nsel, "base_nsel")):
+        if t is not None:
+            _require(t.dtype == torch.int32 and t.shape == seq_lens.shape and t.is_contiguous(), f"{n} must be int32 [S]")
     _check(lib().bd_cache_rollback(seq_lens.data_ptr(), _ptr(nsel), accept.data_ptr(), seq_lens.shape[0], int(spec),
-                                   _stream()))
+                                   _ptr(base_lens), _ptr(base_nsel), _stream()))
 
 
 def bd_top1_ce(student: torch.Tensor, *, teacher: Optional[torch.Tensor] = None, targets: Optional[torch.Tensor] = None,

@@ -542,10 +542,12 @@ bd_status bd_cache_append(const bd_kv_desc* kv, const uint16_t* k_new, const uin
 }
 
 bd_status bd_cache_rollback(int32_t* seq_lens, int32_t* nsel, const int32_t* accept, int32_t num_seqs, int32_t spec,
-                            hipStream_t stream) {
+                            const int32_t* base_lens, const int32_t* base_nsel, hipStream_t stream) {
   if (!seq_lens || !accept) return fail(BD_ERR_INVALID_ARG, "seq_lens and accept are required");
   if (num_seqs < 1 || spec < 0) return fail(BD_ERR_INVALID_ARG, "need num_seqs >= 1 and spec >= 0");
-  return launched(bd::launch_rollback(seq_lens, nsel, accept, num_seqs, spec, stream));
+  if (base_nsel && !nsel) return fail(BD_ERR_INVALID_ARG, "base_nsel without nsel");
+  bd::RollbackParams p{seq_lens, nsel, accept, base_lens, base_nsel, num_seqs, spec};
+  return launched(bd::launch_rollback(p, stream));
 }
 
 // ---------------------------------------------------------------- top-1 CE, budget sampling

@@ -182,8 +182,15 @@ struct AppendParams {
 };
 
 hipError_t launch_append(const AppendParams& p, hipStream_t stream);
-hipError_t launch_rollback(int32_t* seq_lens, int32_t* nsel, const int32_t* accept, int32_t S, int32_t spec,
-                           hipStream_t stream);
+struct RollbackParams {
+  int32_t* seq_lens;        // [S], updated in place
+  int32_t* nsel;            // nullable [S], updated in place
+  const int32_t* accept;    // [S]
+  const int32_t* base_lens; // nullable [S]: lengths before the speculative appends
+  const int32_t* base_nsel; // nullable [S]: list counts before them
+  int32_t S, spec;
+};
+hipError_t launch_rollback(const RollbackParams& p, hipStream_t stream);
 
 // ---- top-1 cross-entropy and budget sampling ---------------------------------
 struct CeParams {

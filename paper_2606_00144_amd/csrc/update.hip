@@ -3,8 +3,8 @@
 // Appending writes the new rows' K and V at positions L_s .. L_s+n-1 and, for
 // the drafter's sparse cache, appends those positions to every KV head's index
 // list; a second launch then advances the lengths (every row copy reads the old
-// length first, and stream order separates the two).  Rollback drops the
-// rejected speculative rows after verification.  All of it is integer and byte
+// length first, and stream order separates the two).  Rollback keeps the
+// accepted speculative rows after verification.  All of it is integer and byte
 // work: one 16-byte load and store per lane per row chunk.
 
 #include "bd_common.hpp"
@@ -69,19 +69,21 @@ __global__ __launch_bounds__(kThreads) void append_advance_kernel(AppendParams p
   }
 }
 
-__global__ __launch_bounds__(kThreads) void rollback_kernel(int32_t* seq_lens, int32_t* nsel, const int32_t* accept,
-                                                           int32_t S, int32_t spec) {
+// Thread s: keep the accepted prefix of the speculative rows.  With the lengths from before the
+// speculative appends, a count becomes min(count, base + accepted) (rows an append dropped were never
+// counted); without them, spec - accepted is subtracted.
+__global__ __launch_bounds__(kThreads) void rollback_kernel(RollbackParams p) {
   const int s = blockIdx.x * kThreads + threadIdx.x;
-  if (s >= S) return;
-  int a = accept[s];
-  a = a < 0 ? 0 : (a > spec ? spec : a);
-  const int drop = spec - a;
-  const int L = seq_lens[s] - drop;
-  seq_lens[s] = L < 0 ? 0 : L;
-  if (nsel) {
-    const int m = nsel[s] - drop;
-    nsel[s] = m < 0 ? 0 : m;
-  }
+  if (s >= p.S) return;
+  int a = p.accept[s];
+  a = a < 0 ? 0 : (a > p.spec ? p.spec : a);
+  auto keep = [&](int cur, const int32_t* base) {
+    const int64_t v = base ? (int64_t)base[s] + a : (int64_t)cur - (p.spec - a);
+    const int64_t c = v < cur ? v : cur;
+    return (int)(c < 0 ? 0 : c);
+  };
+  p.seq_lens[s] = keep(p.seq_lens[s], p.base_lens);
+  if (p.nsel) p.nsel[s] = keep(p.nsel[s], p.base_nsel);
 }
 
 }  // namespace
@@ -94,10 +96,8 @@ hipError_t launch_append(const AppendParams& p, hipStream_t stream) {
   return hipGetLastError();
 }
 
-hipError_t launch_rollback(int32_t* seq_lens, int32_t* nsel, const int32_t* accept, int32_t S, int32_t spec,
-                           hipStream_t stream) {
-  hipLaunchKernelGGL(rollback_kernel, dim3((S + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, seq_lens, nsel,
-                     accept, S, spec);
+hipError_t launch_rollback(const RollbackParams& p, hipStream_t stream) {
+  hipLaunchKernelGGL(rollback_kernel, dim3((p.S + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, p);
   return hipGetLastError();
 }
 

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_status_strings(L):
-    assert L.bd_abi_version() == 2
+    assert L.bd_abi_version() == 3
     for s in range(5):
         assert L.bd_status_string(s)
     assert L.bd_status_string(99) == b"unknown status"
@@ -180,7 +180,8 @@ def test_update_rejections(L):
     assert A(_kv(), idx=FAKE, nsel=FAKE, ld=-1) == bd.BD_ERR_INVALID_ARG
     assert A(_kv(head_dim=64)) == bd.BD_ERR_UNSUPPORTED
     R = L.bd_cache_rollback
-    assert R(None, None, FAKE, 2, 5, None) == bd.BD_ERR_INVALID_ARG
-    assert R(FAKE, None, None, 2, 5, None) == bd.BD_ERR_INVALID_ARG
-    assert R(FAKE, None, FAKE, 0, 5, None) == bd.BD_ERR_INVALID_ARG
-    assert R(FAKE, None, FAKE, 2, -1, None) == bd.BD_ERR_INVALID_ARG
+    assert R(None, None, FAKE, 2, 5, None, None, None) == bd.BD_ERR_INVALID_ARG
+    assert R(FAKE, None, None, 2, 5, None, None, None) == bd.BD_ERR_INVALID_ARG
+    assert R(FAKE, None, FAKE, 0, 5, None, None, None) == bd.BD_ERR_INVALID_ARG
+    assert R(FAKE, None, FAKE, 2, -1, None, None, None) == bd.BD_ERR_INVALID_ARG
+    assert R(FAKE, None, FAKE, 2, 5, FAKE, FAKE, None) == bd.BD_ERR_INVALID_ARG     # base_nsel without nsel

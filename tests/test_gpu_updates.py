@@ -75,6 +75,51 @@ def test_rollback_matches_oracle():
     assert ld_.cpu().tolist() == ol.tolist() and nd.cpu().tolist() == on.tolist()
 
 
+def test_rollback_from_base_lengths_matches_oracle():
+    lens, nsel, acc = [100, 100, 100, 3, 50, 64], [20, 20, 20, 1, 9, 64], [0, 2, 5, 9, -1, 3]
+    base_l, base_n = [95, 97, 99, 0, 45, 64], [15, 18, 20, 0, 9, 62]
+    ol, on = O.cache_rollback(lens, acc, 5, nsel=nsel, base_lens=base_l, base_nsel=base_n)
+    case("rollback from base lengths")
+    ld_, nd = i32_dev(lens), i32_dev(nsel)
+    bd.bd_cache_rollback(ld_, i32_dev(acc), 5, nsel=nd, base_lens=i32_dev(base_l), base_nsel=i32_dev(base_n))
+    torch.cuda.synchronize()
+    assert ld_.cpu().tolist() == ol.tolist() and nd.cpu().tolist() == on.tolist()
+
+
+def test_rounds_that_fill_the_list_and_the_cache():
+    """Several rounds of speculative appends and rollbacks (from the lengths before each round) on a
+    drafter list of fixed width and caches of fixed capacity: the list fills after a few rounds and the
+    caches reach their capacity, and GPU lengths, lists and bytes follow the oracle round by round."""
+    S, Hkv, cap, gamma, ld = 3, 2, 60, 4, 24
+    g = np.random.default_rng(70)
+    k, v = _bits((S, Hkv, cap, 128), 71), _bits((S, Hkv, cap, 128), 72)
+    lens0, nsel0 = [30, 44, 52], [12, 16, 20]
+    idx = np.full((S, Hkv, ld), -1, np.int32)
+    for s in range(S):
+        idx[s, :, :nsel0[s]] = np.sort(g.choice(lens0[s], nsel0[s], replace=False))
+    kd, vd, lensd, idxd, nseld = bf16_dev(k), bf16_dev(v), i32_dev(lens0), i32_dev(idx), i32_dev(nsel0)
+    ok, ov, ol, oi, on = k.copy(), v.copy(), np.array(lens0, np.int32), idx.copy(), np.array(nsel0, np.int32)
+    for r in range(6):
+        base_l, base_n = lensd.clone(), nseld.clone()
+        ob_l, ob_n = ol.copy(), on.copy()
+        for i in range(gamma):
+            kn, vn = _bits((S, 1, Hkv, 128), 100 + 10 * r + i), _bits((S, 1, Hkv, 128), 200 + 10 * r + i)
+            case(f"rounds: round {r} append {i}")
+            bd.bd_cache_append(kd, vd, lensd, bf16_dev(kn), bf16_dev(vn), idx=idxd, nsel=nseld)
+            ok, ov, ol, oi, on = O.cache_append(ok, ov, ol, kn, vn, oi, on)
+        acc = g.integers(0, gamma + 1, size=S).astype(np.int32)
+        bd.bd_cache_rollback(lensd, i32_dev(acc), gamma, nsel=nseld, base_lens=base_l, base_nsel=base_n)
+        ol, on = O.cache_rollback(ol, acc, gamma, nsel=on, base_lens=ob_l, base_nsel=ob_n)
+        torch.cuda.synchronize()
+        assert lensd.cpu().tolist() == ol.tolist(), r
+        assert nseld.cpu().tolist() == on.tolist(), r
+        gi = idxd.cpu().numpy()
+        for s in range(S):
+            assert np.array_equal(gi[s, :, :on[s]], oi[s, :, :on[s]]), (r, s)
+        assert np.array_equal(_u16(kd), ok) and np.array_equal(_u16(vd), ov)
+    assert on.max() == ld and ol.max() == cap          # both limits were reached
+
+
 def test_one_speculative_round_of_alg2():
     S, Hq, Hkv, L0, W, B, gamma = 2, 8, 2, 300, 16, 64, 4
     cap = L0 + gamma + 1
