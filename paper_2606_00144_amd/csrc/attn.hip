@@ -757,6 +757,8 @@ constexpr int kBMaxPieces = 64;                    // branches per unit (host-ch
 // a workgroup's range holds at most kMaxSplitKeys entries, each piece pads its last tile, and the
 // prefetches run kBRing tiles past the end
 constexpr int kBSlotCap = kMaxSplitKeys + (kBMaxPieces + kBRing) * kTile;
+// a block-mode tile: K in the score operand order (8 KiB), then V row-major for the transposing reads
+constexpr int kBTileBytes = 8192 + kRmTileBytes;
 
 // One piece of a workgroup's range: entries [e0, e1) of branch b, from slot-table tile t0; the
 // branch spans nwg workgroups, its records start at slot `slot`, this piece's is number wo.
@@ -767,7 +769,7 @@ struct BlockPiece {
 struct BlockSmem {
   alignas(16) int32_t roff[kBSlotCap];
   alignas(16) int32_t tpos[kBSlotCap];
-  alignas(16) uint8_t ring[kBRing][kTileBytes];
+  alignas(16) uint8_t ring[kBRing][kBTileBytes];
   BlockPiece pc[kBMaxPieces];
   int32_t blen[kBMaxPieces];                       // branch lengths
 };
@@ -806,7 +808,7 @@ __device__ inline void dma_load(const KvView& kv, uint32_t r, uint32_t max_roff,
   const int lg = lane >> 4, lr = lane & 15;
   const uint32_t ro = r < max_roff ? r : max_roff;
   if (q < 8) dma16(kv.k + ((uint64_t)ro << 3) + 32 * lg + 8 * (q & 3), dst + q * 1024);
-  else dma16(kv.v + ((uint64_t)ro << 3) + 8 * rm_chunk(lane), dst + q * 1024);
+  else dma16(kv.v + ((uint64_t)ro << 3) + 8 * rm_chunk(lane), dst + 8192 + rm_block_off(q - 8));
 }
 
 // Branch b's outputs of row block rb (rows 16*nt + lane%16 of it) from an unnormalised state:
@@ -1064,7 +1066,7 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
       // this wave's loads of tile t are older than the kBRing-2 tiles issued after it
       asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
       const int nxt = t + kBRing - 1;
-      const uint32_t src = ring_lds + (uint32_t)(t % kBRing) * kTileBytes;
+      const uint32_t src = ring_lds + (uint32_t)(t % kBRing) * kBTileBytes;
       uint32_t r[2];
       read_block_tile_k(T, r, src, tpos_lds, kTile * t, roff_lds, kTile * nxt, rit0, rit1, lane);
       bool bad = false;

@@ -57,7 +57,7 @@ constexpr int kQWaves = 8;
 constexpr int kQThreads = kQWaves * kWave;
 constexpr int kQRing = 5;                          // tile slots; kQRing-1 tiles in flight
 constexpr int kQLoads = 24;                        // 16-byte loads per lane per tile (3 per wave)
-constexpr int kQTileBytes = kQLoads * kWave * 16;  // 24 KiB
+constexpr int kQTileBytes = 16384 + kRmTileBytes; // K and V in the score layout, then K row-major
 constexpr int kQSlotCap = kMaxSplitKeys + kQRing * kTile;
 constexpr int kRecFloats = 2 * 16 * kD;            // one wave's dQ partial: 32 rows x 128
 
@@ -80,7 +80,7 @@ __device__ inline void dq_dma_load(const KvView& kv, uint32_t r, uint32_t max_ro
   const uint64_t base = (uint64_t)ro << 3;
   if (q < 8) dma16(kv.k + base + 32 * lg + 8 * (q & 3), dst + q * 1024);
   else if (q < 16) dma16(kv.v + base + 32 * lg + 8 * (q & 3), dst + q * 1024);
-  else dma16(kv.k + base + 8 * rm_chunk(lane), dst + q * 1024);
+  else dma16(kv.k + base + 8 * rm_chunk(lane), dst + 16384 + rm_block_off(q - 16));
 }
 
 // Eight 1 KiB pieces of a tile (loads q0 .. q0+7) into registers, with their wait.
