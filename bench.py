@@ -14,10 +14,18 @@ The drafter and the verifier have separate caches of the same shape.  The step
 is captured once in a HIP graph and replayed; inputs stay resident in HBM.
 Prints one JSON line.
 
-`--op select` and `--op multiview` time the other two operations of the path on
-their own workloads instead (selection at the same 16K batch; the multi-view
-block at 4 sequences x 8,192 tokens, C = 64, four budgets), each as one JSON
-line of the same form.
+Besides the step time the line carries each kernel's time warm (back-to-back
+launches over the same inputs, in a graph) and cold (each launch after a 512 MiB
+streaming read, so the 256 MB MALL holds none of its inputs), the step's p10/median/p90
+over single replays, the step at B = 512, and whether decode and verify meet
+60% of the 8 TB/s HBM peak.
+
+`--op select`, `--op multiview`, `--op multiview_bwd`, `--op paged`, `--op
+updates` and `--op ce` time the other operations on their own workloads
+(selection at the same 16K batch; the multi-view block at 4 x 8,192, C = 64,
+four budgets, or with `--mv-workload train-c256-16k` the training shape
+16,384 tokens, C = 256; the ragged paged batch of 64 MHA sequences), each as
+one JSON line of the same form.
 """
 from __future__ import annotations
 
@@ -42,7 +50,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--budget", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", choices=("step", "select", "multiview", "multiview_bwd", "updates", "ce"), default="step")
+    ap.add_argument("--op", choices=("step", "select", "multiview", "multiview_bwd", "paged", "updates", "ce"),
+                    default="step")
+    ap.add_argument("--mv-workload", choices=("multiview-train-b4-8k", "train-c256-16k"), default="multiview-train-b4-8k",
+                    help="--op multiview / multiview_bwd: the multi-view block (4 x 8K, C = 64, token-level views) or "
+                         "the training shape (1 x 16K, C = 256, TopKChunks views of every training budget)")
     ap.add_argument("--chunk", type=int, default=0,
                     help="--op select: 0 = token-level selection with pooling, s > 0 = TopKChunks with chunks of s")
     ap.add_argument("--copy-probe", action="store_true",
@@ -132,6 +144,8 @@ def main():
         return bench_multiview_bwd(args, bd, synth, torch, np, dev)
     if args.op == "updates":
         return bench_updates(args, bd, synth, torch, np, dev)
+    if args.op == "paged":
+        return bench_paged(args, bd, synth, torch, np, dev)
     if args.op == "ce":
         return bench_ce(args, bd, synth, torch, np, dev)
     cfg = synth.workload("16k-collapse-b8")
@@ -161,6 +175,8 @@ def main():
 
     log("selecting the drafter's sparse cache (once, as after prefill)")
     idx, nsel = bd.bd_select_kv(kS_d, q_win, lens, B)
+    B2 = 512 if B != 512 else 1024                                # the other budget of the workload
+    idx2, nsel2 = bd.bd_select_kv(kS_d, q_win, lens, B2)
     torch.cuda.synchronize()
 
     out_dec = torch.empty((gamma, S, Hq, 128), dtype=torch.bfloat16, device=dev)
@@ -169,8 +185,9 @@ def main():
     bonus = torch.empty((S,), dtype=torch.int32, device=dev)
     ws_dec, ws_ver, ws_acc = bd.Workspace(), bd.Workspace(), bd.Workspace()
 
-    def decode(i):
-        bd.bd_sparse_decode_attn(kS_d, vS_d, q_dec[i], idx, nsel, lens, out=out_dec[i], workspace=ws_dec)
+    def decode(i, sel=None):
+        ii, nn = (idx, nsel) if sel is None else sel
+        bd.bd_sparse_decode_attn(kS_d, vS_d, q_dec[i], ii, nn, lens, out=out_dec[i], workspace=ws_dec)
 
     def verify():
         bd.bd_verify_attn(kL_d, vL_d, q_ver, lens, out=out_ver, workspace=ws_ver)
@@ -178,9 +195,9 @@ def main():
     def accept():
         bd.bd_accept_len(logits, draft, workspace=ws_acc, outputs=(acc, bonus, None))
 
-    def step():
+    def step(sel=None):
         for i in range(gamma):
-            decode(i)
+            decode(i, sel)
         verify()
         accept()
 
@@ -218,6 +235,32 @@ def main():
     wall = time.perf_counter() - t0
     us_step = wall * 1e6 / args.steps
 
+    # spread: every replay between its own pair of events, outside the timed region above
+    per = []
+    for _ in range(max(args.steps, 100)):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        graph.replay()
+        b.record()
+        per.append((a, b))
+    torch.cuda.synchronize()
+    per = np.array([a.elapsed_time(b) * 1e3 for a, b in per])
+    pct = {"p10": round(float(np.percentile(per, 10)), 2), "median": round(float(np.median(per)), 2),
+           "p90": round(float(np.percentile(per, 90)), 2), "replays": int(per.size)}
+
+    # the same step at the workload's other budget (its own selection and graph)
+    graph2 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph2):
+        step((idx2, nsel2))
+    for _ in range(args.warmup):
+        graph2.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        graph2.replay()
+    torch.cuda.synchronize()
+    us_step2 = (time.perf_counter() - t0) * 1e6 / args.steps
+
     # per-kernel durations: one HIP graph of back-to-back launches per kernel, replayed after an
     # identical replay so the queue is busy when the start event is recorded; the events sit on
     # the stream the kernels run on
@@ -248,9 +291,25 @@ def main():
         "verify_attn": time_graph(graph_of(verify, 10), 10),
         "accept_len": time_graph(graph_of(accept, 20), 20),
     }
+    # cold: each launch right after a 512 MiB streaming read (more than the 256 MB MALL holds, as the
+    # first draft of a step follows the verifier's 537 MB stream): time(graph of flush + op pairs) -
+    # time(graph of flushes), per launch
+    log("timing kernels cold (each after a 512 MiB read)")
+    flush = cold_flush(torch, dev)
+    n_cold = 10
+    t_flush = time_graph(graph_of(flush, n_cold), n_cold)
+    kern_us_cold = {}
+    for name, fn in (("sparse_decode_attn", lambda: decode(0)), ("verify_attn", verify), ("accept_len", accept)):
+        kern_us_cold[name] = time_graph(graph_of(lambda: (flush(), fn()), n_cold), n_cold) - t_flush
+    del flush
 
     dec_b, ver_b, acc_b = algorithmic_bytes(S, Hq, Hkv, L, B, gamma, V)
     step_bytes = gamma * dec_b + ver_b + acc_b
+    dec2_b = algorithmic_bytes(S, Hq, Hkv, L, B2, gamma, V)[0]
+    step2_bytes = gamma * dec2_b + ver_b + acc_b
+    kbytes = {"sparse_decode_attn": dec_b, "verify_attn": ver_b, "accept_len": acc_b}
+    gbs = lambda n, us: round(kbytes[n] / (us * 1e-6) / 1e9, 1)
+    frac = lambda n, us: round(kbytes[n] / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
     src_hash = hashlib.sha256(open(os.path.join(ROOT, "paper_2606_00144_amd", "csrc", "attn.hip"), "rb").read()).hexdigest()
     ver_gbs = ver_b / (kern_us["verify_attn"] * 1e-6) / 1e9
     roofline = {"bound": "hbm", "kernel": "verify_attn", "achieved": round(ver_gbs, 1), "peak": HBM_PEAK_GBS,
@@ -268,9 +327,15 @@ def main():
         "step_gbps": round(step_bytes / (us_step * 1e-6) / 1e9, 1),
         "step_bytes": step_bytes,
         "kernels_us": {n: round(v, 2) for n, v in kern_us.items()},
-        "kernels_gbps": {"sparse_decode_attn": round(dec_b / (kern_us["sparse_decode_attn"] * 1e-6) / 1e9, 1),
-                         "verify_attn": round(ver_gbs, 1),
-                         "accept_len": round(acc_b / (kern_us["accept_len"] * 1e-6) / 1e9, 1)},
+        "step_us_spread": pct,
+        "kernels_gbps": {n: gbs(n, v) for n, v in kern_us.items()},
+        "kernels_us_cold": {n: round(v, 2) for n, v in kern_us_cold.items()},
+        "kernels_gbps_cold": {n: gbs(n, v) for n, v in kern_us_cold.items()},
+        "targets_60pct_hbm": {n: {"frac_warm": frac(n, kern_us[n]), "frac_cold": frac(n, kern_us_cold[n]),
+                                  "met_warm": frac(n, kern_us[n]) >= 0.6, "met_cold": frac(n, kern_us_cold[n]) >= 0.6}
+                              for n in ("sparse_decode_attn", "verify_attn")},
+        f"step_b{B2}": {"value": round(us_step2, 2), "unit": "us/step", "step_bytes": step2_bytes,
+                        "step_gbps": round(step2_bytes / (us_step2 * 1e-6) / 1e9, 1)},
         "roofline": roofline,
         "cpu_baseline": None,
     }
@@ -278,6 +343,16 @@ def main():
         log("timing the fp64 oracle on the host (one step)")
         result["cpu_baseline"] = cpu_baseline(host, S, Hq, L, B, gamma)
     print(json.dumps(result), flush=True)
+
+
+def cold_flush(torch, dev):
+    """A launch that streams 512 MiB through the memory hierarchy and leaves little dirty data: one
+    float of every 64-byte sector of a 512 MiB buffer copied to a 32 MiB one (an elementwise copy,
+    graph-capturable).  More than the 256 MB MALL is read, so the next kernel finds none of its inputs
+    there; a write flush instead would leave its dirty lines to be written back during that kernel."""
+    src = torch.ones((128 << 20,), dtype=torch.float32, device=dev)
+    dst = torch.empty((8 << 20,), dtype=torch.float32, device=dev)
+    return lambda: dst.copy_(src[::16])
 
 
 def _bf(torch, np, bits, dev):
@@ -356,36 +431,43 @@ def bench_select(args, bd, synth, torch, np, dev):
     }), flush=True)
 
 
-def _multiview_inputs(bd, synth, torch, np, dev):
-    """The multi-view training block (4 x 8,192, C = 64, four budgets), views from bd_select_kv."""
-    cfg = synth.workload("multiview-train-b4-8k")
+def _multiview_inputs(bd, synth, torch, np, dev, name="multiview-train-b4-8k"):
+    """The multi-view block and its views: the 4 x 8,192 block (C = 64, four sampled budgets, views from
+    bd_select_kv), or the training shape (1 x 16,384, C = 256, the TopKChunks views of every training
+    budget: top floor(B/8) prefix chunks with the block on top)."""
+    cfg = synth.workload(name)
     S, Hq, Hkv, L, C = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.block_len
-    budgets = [int(b) for b in synth.view_budgets(cfg)]
+    chunks = name == "train-c256-16k"
+    budgets = list(cfg.budgets) if chunks else [int(b) for b in synth.view_budgets(cfg)]
     log("generating inputs")
     qs, ks, vs = synth.kv_batch(cfg)
     k, v = _bf(torch, np, np.stack(ks), dev), _bf(torch, np, np.stack(vs), dev)
     q_blk = _bf(torch, np, np.stack(qs)[:, -C:], dev)
     lens = torch.full((S,), L, dtype=torch.int32, device=dev)
-    ld = max(budgets)
+    ld = max(budgets) + (C if chunks else 0)
     idx = torch.full((len(budgets), S, Hkv, ld), -1, dtype=torch.int32, device=dev)
     nsel = torch.empty((len(budgets), S), dtype=torch.int32, device=dev)
     for i, Bv in enumerate(budgets):                       # each view is the selection at its budget
-        vi, vn = bd.bd_select_kv(k, q_blk, lens, Bv)
-        idx[i, :, :, :Bv] = vi
+        if chunks:
+            vi, vn = bd.bd_select_kv_chunks(k, q_blk, lens, Bv, chunk=8)
+        else:
+            vi, vn = bd.bd_select_kv(k, q_blk, lens, Bv)
+        idx[i, :, :, :vi.shape[2]] = vi
         nsel[i] = vn
     return cfg, budgets, k, v, q_blk, lens, idx, nsel
 
 
-def _visible_pairs(np, idx_h, budgets, S, Hkv, G, L, C):
+def _visible_pairs(np, idx_h, nsel_h, S, Hkv, G, L, C):
     """(query row, visible key) pairs over all branches, and those whose key is a block row."""
     pos = np.arange(L - C, L)
     full_pairs = S * Hkv * G * int((pos + 1).sum())
     blk_pairs = S * Hkv * G * (C * (C + 1) // 2)
     view_pairs = 0
-    for i, Bv in enumerate(budgets):
+    for i in range(idx_h.shape[0]):
         for s in range(S):
             for g in range(Hkv):
-                t = np.sort(idx_h[i, s, g, :Bv])
+                t = idx_h[i, s, g, :nsel_h[i, s]]
+                t = np.sort(t[(t >= 0) & (t < L)])
                 view_pairs += G * int(np.searchsorted(t, pos, side="right").sum())
                 tb = t[t >= L - C] - (L - C)                  # block keys listed in the view
                 blk_pairs += G * int((C - tb).sum())
@@ -393,23 +475,25 @@ def _visible_pairs(np, idx_h, budgets, S, Hkv, G, L, C):
 
 
 def bench_multiview(args, bd, synth, torch, np, dev):
-    """bd_multiview_attn on the multi-view block (4 x 8,192, C = 64, four budgets, views from bd_select_kv)."""
-    cfg, budgets, k, v, q_blk, lens, idx, nsel = _multiview_inputs(bd, synth, torch, np, dev)
+    """bd_multiview_attn on the multi-view block (4 x 8,192, C = 64, four budgets, views from bd_select_kv),
+    or on the training shape (--mv-workload train-c256-16k)."""
+    cfg, budgets, k, v, q_blk, lens, idx, nsel = _multiview_inputs(bd, synth, torch, np, dev, args.mv_workload)
     S, Hq, Hkv, L, C = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.block_len
     ws = bd.Workspace()
     steps = max(1, min(args.steps, 50))
     fn = lambda: bd.bd_multiview_attn(k, v, q_blk, idx, nsel, lens, workspace=ws)
     us = _time_calls(torch, fn, steps, min(args.warmup, 5))
     # algorithmic flops: 4 * 128 per (query row, visible key), full branch and every view
-    pairs, _ = _visible_pairs(np, idx.cpu().numpy(), budgets, S, Hkv, Hq // Hkv, L, C)
+    pairs, _ = _visible_pairs(np, idx.cpu().numpy(), nsel.cpu().numpy(), S, Hkv, Hq // Hkv, L, C)
     flops = 4 * 128 * pairs
     tflops = flops / (us * 1e-6) / 1e12
     print(json.dumps({
-        "metric": "bd_multiview_attn µs/call at 8K ctx (4 seqs, C=64, 4 views + full)", "value": round(us, 2),
+        "metric": f"bd_multiview_attn µs/call at {L // 1024}K ctx ({S} seqs, C={C}, {len(budgets)} views + full)",
+        "value": round(us, 2),
         "unit": "us/call", "n_gpus": 1, "steps": steps, "warmup": min(args.warmup, 5),
         "ms_per_step": round(us / 1e3, 5), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic (seeded N(0,1) bf16 K/V/Q with 1% planted heavy hitters)",
-        "config": {"workload": f"multiview-train-b4-8k: 4 seqs x {L} ctx, {Hq}/{Hkv} heads, C={C}, budgets {budgets}",
+        "config": {"workload": f"{cfg.name}: {S} seqs x {L} ctx, {Hq}/{Hkv} heads, C={C}, budgets {budgets}",
                    "num_seqs": S, "seq_len": L, "block_len": C, "budgets": budgets},
         "roofline": {"bound": "mfma", "kernel": "block_kernel (views + full branch)", "achieved": round(tflops, 1),
                      "peak": 2500.0, "unit": "TFLOP/s", "frac": round(tflops / 2500.0, 4), "traffic": None,
@@ -418,8 +502,9 @@ def bench_multiview(args, bd, synth, torch, np, dev):
 
 
 def bench_multiview_bwd(args, bd, synth, torch, np, dev):
-    """bd_multiview_attn_bwd on the multi-view block: dQ over every branch, dK/dV of the block rows."""
-    cfg, budgets, k, v, q_blk, lens, idx, nsel = _multiview_inputs(bd, synth, torch, np, dev)
+    """bd_multiview_attn_bwd on the multi-view block (or the training shape): dQ over every branch, dK/dV of
+    the block rows."""
+    cfg, budgets, k, v, q_blk, lens, idx, nsel = _multiview_inputs(bd, synth, torch, np, dev, args.mv_workload)
     S, Hq, Hkv, L, C = cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.seq_len, cfg.block_len
     ov, of, o32v, lv, o32f, lf = bd.bd_multiview_attn(k, v, q_blk, idx, nsel, lens, train=True)
     g = torch.Generator(device=dev)
@@ -432,19 +517,83 @@ def bench_multiview_bwd(args, bd, synth, torch, np, dev):
     us = _time_calls(torch, fn, steps, min(args.warmup, 5))
     # algorithmic flops: per (query row, visible key) the score, dP and dQ products (6 * 128); per
     # (query row, visible block key) also the dK and dV products (4 * 128)
-    pairs, blk = _visible_pairs(np, idx.cpu().numpy(), budgets, S, Hkv, Hq // Hkv, L, C)
+    pairs, blk = _visible_pairs(np, idx.cpu().numpy(), nsel.cpu().numpy(), S, Hkv, Hq // Hkv, L, C)
     flops = 6 * 128 * pairs + 4 * 128 * blk
     tflops = flops / (us * 1e-6) / 1e12
     print(json.dumps({
-        "metric": "bd_multiview_attn_bwd µs/call at 8K ctx (4 seqs, C=64, 4 views + full)", "value": round(us, 2),
+        "metric": f"bd_multiview_attn_bwd µs/call at {L // 1024}K ctx ({S} seqs, C={C}, {len(budgets)} views + full)",
+        "value": round(us, 2),
         "unit": "us/call", "n_gpus": 1, "steps": steps, "warmup": min(args.warmup, 5),
         "ms_per_step": round(us / 1e3, 5), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic (seeded N(0,1) bf16 K/V/Q/dO with 1% planted heavy hitters)",
-        "config": {"workload": f"multiview-train-b4-8k: 4 seqs x {L} ctx, {Hq}/{Hkv} heads, C={C}, budgets {budgets}",
+        "config": {"workload": f"{cfg.name}: {S} seqs x {L} ctx, {Hq}/{Hkv} heads, C={C}, budgets {budgets}",
                    "num_seqs": S, "seq_len": L, "block_len": C, "budgets": budgets},
         "roofline": {"bound": "mfma", "kernel": "dq_kernel + dkv_kernel", "achieved": round(tflops, 1),
                      "peak": 2500.0, "unit": "TFLOP/s", "frac": round(tflops / 2500.0, 4), "traffic": None,
                      "flops_per_call": flops},
+    }), flush=True)
+
+
+def bench_paged(args, bd, synth, torch, np, dev):
+    """Verify and sparse decode on the ragged paged batch: 64 MHA sequences (32 heads) of 4K-16K tokens in
+    16-token pages under a seeded page table, gamma = 5, B = 1024 (the selection over the pool runs once,
+    untimed).  Each call warm (back-to-back) and cold (after a 512 MiB write)."""
+    cfg = synth.workload("ragged-paged-b64-mha")
+    S, Hq, Hkv, W, gamma, B, P = (cfg.num_seqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.window, cfg.gamma,
+                                  cfg.budgets[0], cfg.page_size)
+    lens_h = synth.seq_lens(cfg)
+    log("generating inputs (64 sequences)")
+    qs, ks, vs = synth.kv_batch(cfg, workers=16)
+    table, npages = synth.page_table(cfg, lens_h)
+    pool_k = np.zeros((npages, Hkv, P, 128), np.uint16)
+    pool_v = np.zeros_like(pool_k)
+    for s, L in enumerate(lens_h):
+        for pi in range((int(L) + P - 1) // P):
+            n = min(P, int(L) - pi * P)
+            pool_k[table[s, pi], :, :n] = ks[s][:, pi * P:pi * P + n]
+            pool_v[table[s, pi], :, :n] = vs[s][:, pi * P:pi * P + n]
+    del ks, vs
+    kd, vd = _bf(torch, np, pool_k, dev), _bf(torch, np, pool_v, dev)
+    del pool_k, pool_v
+    pt = torch.from_numpy(table).to(dev)
+    lens = torch.from_numpy(lens_h.astype(np.int32)).to(dev)
+    q_tail = _bf(torch, np, np.stack(qs), dev)
+    q_win = q_tail[:, -W:].contiguous()
+    q_dec = q_tail[:, -1].contiguous()
+    q_ver = q_tail[:, -(gamma + 1):].contiguous()
+    idx, nsel = bd.bd_select_kv(kd, q_win, lens, B, page_table=pt)
+    out_d, out_v = torch.empty_like(q_dec), torch.empty_like(q_ver)
+    ws_d, ws_v = bd.Workspace(), bd.Workspace()
+    dec = lambda: bd.bd_sparse_decode_attn(kd, vd, q_dec, idx, nsel, lens, page_table=pt, out=out_d, workspace=ws_d)
+    ver = lambda: bd.bd_verify_attn(kd, vd, q_ver, lens, page_table=pt, out=out_v, workspace=ws_v)
+    torch.cuda.synchronize()
+    steps, warm = max(1, min(args.steps, 50)), min(args.warmup, 5)
+    us = {"verify_attn": _time_graph(torch, ver, steps, warm, 4), "sparse_decode_attn": _time_graph(torch, dec, steps, warm, 10)}
+    flush = cold_flush(torch, dev)
+    t_flush = _time_graph(torch, flush, steps, warm, 4)
+    us_cold = {"verify_attn": _time_graph(torch, lambda: (flush(), ver()), steps, warm, 4) - t_flush,
+               "sparse_decode_attn": _time_graph(torch, lambda: (flush(), dec()), steps, warm, 4) - t_flush}
+    D = 128
+    nb = {"verify_attn": int(lens_h.sum()) * Hkv * D * 2 * 2 + 2 * S * (gamma + 1) * Hq * D * 2,
+          "sparse_decode_attn": S * Hkv * min(B, int(lens_h.min())) * (D * 2 * 2 + 4) + 2 * S * Hq * D * 2}
+    g = lambda n, t: round(nb[n] / (t * 1e-6) / 1e9, 1)
+    vb = g("verify_attn", us["verify_attn"])
+    print(json.dumps({
+        "metric": "ragged paged batch: verify and sparse decode µs/call and HBM GB/s (64 MHA seqs, 4K-16K ctx)",
+        "value": round(us["verify_attn"], 2), "unit": "us/call (verify)", "n_gpus": 1, "steps": steps, "warmup": warm,
+        "ms_per_step": round(us["verify_attn"] / 1e3, 5), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded N(0,1) bf16 K/V/Q with 1% planted heavy hitters)",
+        "config": {"workload": f"ragged-paged-b64-mha: {S} seqs, ctx {int(lens_h.min())}-{int(lens_h.max())} "
+                               f"(mean {float(lens_h.mean()):.0f}), {Hq}/{Hkv} heads, pages of {P}, B={B}, gamma={gamma}",
+                   "num_seqs": S, "budget": B, "gamma": gamma, "page_size": P},
+        "kernels_us": {n: round(t, 2) for n, t in us.items()},
+        "kernels_gbps": {n: g(n, t) for n, t in us.items()},
+        "kernels_us_cold": {n: round(t, 2) for n, t in us_cold.items()},
+        "kernels_gbps_cold": {n: g(n, t) for n, t in us_cold.items()},
+        "bytes_per_call": nb,
+        "roofline": {"bound": "hbm", "kernel": "verify_attn (paged)", "achieved": vb, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(vb / HBM_PEAK_GBS, 4), "traffic": None,
+                     "bytes_per_launch": nb["verify_attn"]},
     }), flush=True)
 
 
