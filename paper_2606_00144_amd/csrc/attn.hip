@@ -743,16 +743,16 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
 // C x G rows), re-streaming K/V once per row block would multiply the traffic.
 // A block-mode workgroup has 8 waves, wave w owning row block 8*rg + w, and all
 // of them consume every 32-key tile of its range from a shared LDS ring: each
-// wave issues 2 of a tile's 16 direct-to-LDS loads, and one barrier per tile
-// both publishes the landed tile and frees the slot read in the step before.
-// The ranges are equal shares of the (sequence, KV head, row group)'s whole key
-// stream, every view and the full branch in turn, cut at run time when the
-// views' lengths are known; pieces of a branch met by several workgroups merge
-// through per-row-block records in the last of them.
+// wave issues 2 of a tile's 16 direct-to-LDS loads, and one barrier per two
+// tiles both publishes the next two landed tiles and frees the two slots read
+// before it.  The ranges are equal shares of the (sequence, KV head, row
+// group)'s whole key stream, every view and the full branch in turn, cut at run
+// time when the views' lengths are known; pieces of a branch met by several
+// workgroups leave per-row-block records that block_merge_kernel combines.
 
 constexpr int kBWaves = 8;
 constexpr int kBThreads = kBWaves * kWave;
-constexpr int kBRing = 6;                          // tile slots; kBRing-1 tiles stay in flight
+constexpr int kBRing = 7;                          // tile slots: the two being read, up to five in flight
 constexpr int kBMaxPieces = 64;                    // branches per unit (host-checked)
 // a workgroup's range holds at most kMaxSplitKeys entries, each piece pads its last tile, and the
 // prefetches run kBRing tiles past the end
@@ -774,33 +774,6 @@ struct BlockSmem {
   int32_t blen[kBMaxPieces];                       // branch lengths
 };
 
-// K pieces of the tile in slot `src`, its positions and the two row offsets this wave loads for the
-// tile it issues next (the V pieces are read later, just before the PV product).
-__device__ inline void read_block_tile_k(TileRegs<2, true>& T, uint32_t (&r)[2], uint32_t src, uint32_t tpos_lds,
-                                         int slot0, uint32_t roff_lds, int next0, int rit0, int rit1, int lane) {
-  const int lg = lane >> 4;
-  const uint32_t at = src + 16 * lane;
-  const uint32_t ap = tpos_lds + 4 * (slot0 + 4 * lg);
-  const uint32_t a0 = roff_lds + 4 * (next0 + rit0);
-  const uint32_t a1 = roff_lds + 4 * (next0 + rit1);
-  asm volatile(
-      "ds_read_b128 %0, %12\n"
-      "ds_read_b128 %1, %12 offset:1024\n"
-      "ds_read_b128 %2, %12 offset:2048\n"
-      "ds_read_b128 %3, %12 offset:3072\n"
-      "ds_read_b128 %4, %12 offset:4096\n"
-      "ds_read_b128 %5, %12 offset:5120\n"
-      "ds_read_b128 %6, %12 offset:6144\n"
-      "ds_read_b128 %7, %12 offset:7168\n"
-      "ds_read_b128 %8, %13\n"
-      "ds_read_b128 %9, %13 offset:64\n"
-      "ds_read_b32 %10, %14\n"
-      "ds_read_b32 %11, %15\n"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&v"(T.k[0][0]), "=&v"(T.k[0][1]), "=&v"(T.k[0][2]), "=&v"(T.k[0][3]), "=&v"(T.k[1][0]),
-        "=&v"(T.k[1][1]), "=&v"(T.k[1][2]), "=&v"(T.k[1][3]), "=&v"(T.tp[0]), "=&v"(T.tp[1]), "=&v"(r[0]), "=&v"(r[1])
-      : "v"(at), "v"(ap), "v"(a0), "v"(a1));
-}
 // Load q (0..15) of a tile for this lane; `r` is the row's offset in 16-byte units.  K loads
 // q < 8 (sub-tile q/4, k-step q%4) land in the score operand order.  V loads q >= 8 fill the
 // tile's second half as a row-major tile for the transposing reads (rm_row, rm_chunk).
@@ -810,6 +783,212 @@ __device__ inline void dma_load(const KvView& kv, uint32_t r, uint32_t max_roff,
   if (q < 8) dma16(kv.k + ((uint64_t)ro << 3) + 32 * lg + 8 * (q & 3), dst + q * 1024);
   else dma16(kv.v + ((uint64_t)ro << 3) + 8 * rm_chunk(lane), dst + 8192 + rm_block_off(q - 8));
 }
+
+// ---- block mode's tile step, split for software pipelining -------------------
+//
+// Step t of a wave computes the scores of tile t+1 on the matrix cores while the vector units turn
+// the scores of tile t into weights (phase A), then the PV product of tile t while the vector units
+// take the row maxima of tile t+1 (phase B).  Neither half's MFMA work depends on its VALU work, so
+// one wave keeps both units busy instead of alternating between them.  Per tile the arithmetic is
+// tile_step's, in the same order: the results are the same bits.
+
+// Scores S^T = K Q^T of one tile (unscaled): sub-tile sub, register r of lane l holds key
+// 16*sub + 4*(l/16) + r of row 16*nt + l%16.
+template <int NT>
+__device__ inline void block_qk(f32x4 (&s)[2][NT], const u32x4 (&k)[2][4], const bf16x8 (&qop)[NT][4]) {
+  const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        s[sub][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(k[sub][j]), qop[nt][j], j == 0 ? z : s[sub][nt],
+                                                             0, 0, 0);
+}
+
+// Scores of absent keys and of keys past a row's position -> -inf.
+template <int NT>
+__device__ inline void block_mask(f32x4 (&s)[2][NT], const u32x4 (&tp)[2], const int (&rowpos)[NT]) {
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int tpos = (int)tp[i >> 2][i & 3];
+      if (!(tpos >= 0 && tpos <= rowpos[nt])) s[i >> 2][nt][i & 3] = -INFINITY;
+    }
+}
+
+// Row maxima of a tile's scaled scores (log2 domain), shared by the row's 4 lane groups.
+template <int NT>
+__device__ inline void block_tile_max(float (&mx)[NT], const f32x4 (&s)[2][NT], float scale_log2) {
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    float v = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v = fmaxf(v, s[i >> 2][nt][i & 3]);
+    mx[nt] = max_xor32(max_xor16(v)) * scale_log2;    // scale > 0: the max commutes with it
+  }
+}
+
+// Raise the reference max of rows whose tile max exceeds it by more than kSlack, rescaling their
+// accumulators (the lazy rescale of tile_step).
+template <int NT>
+__device__ inline void block_raise(RowState<NT>& st, const float (&mx)[NT]) {
+  bool raise = false;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) raise |= mx[nt] > st.m[nt] + kSlack;
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const bool up = mx[nt] > st.m[nt] + kSlack;
+      const float alpha = up ? __builtin_amdgcn_exp2f(st.m[nt] - mx[nt]) : 1.f;   // 0 on the first visible tile
+      st.m[nt] = up ? mx[nt] : st.m[nt];
+      st.l[nt] *= alpha;
+      st.lx[nt] *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) st.o[nt][dt] *= alpha;
+    }
+  }
+}
+
+// Weights of a tile against the reference max, rounded to bf16 for the PV product (TRAIN: with the
+// bf16 remainder as a second operand), summed into the normaliser by MFMA; `w` keeps them unrounded
+// for the log-sum-exp sum.
+template <int NT, bool TRAIN>
+__device__ inline void block_weights(RowState<NT>& st, const f32x4 (&s)[2][NT], float scale_log2, bf16x8 (&pop)[NT],
+                                     bf16x8 (&plo)[NT], float (&w)[NT][8]) {
+  const bf16x8 ones = as_bf16x8(u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const float muse = st.m[nt] == -INFINITY ? 0.f : st.m[nt];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[nt][i] = __builtin_amdgcn_exp2f(fmaf(s[i >> 2][nt][i & 3], scale_log2, -muse));
+    u32x4 pw;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pw[i] = pack_bf16x2(w[nt][2 * i], w[nt][2 * i + 1]);
+    pop[nt] = as_bf16x8(pw);
+    if constexpr (TRAIN) {
+      u32x4 lw;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        lw[i] = pack_bf16x2(w[nt][2 * i] - bf16_lo(pw[i]), w[nt][2 * i + 1] - bf16_hi(pw[i]));
+      plo[nt] = as_bf16x8(lw);
+      st.l[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, plo[nt], st.l[nt], 0, 0, 0);
+    }
+    st.l[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pop[nt], st.l[nt], 0, 0, 0);
+  }
+}
+
+template <int NT, bool TRAIN>
+__device__ inline void block_pv(RowState<NT>& st, const bf16x8 (&vt)[8], const bf16x8 (&pop)[NT],
+                                const bf16x8 (&plo)[NT]) {
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      st.o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt[dt], pop[nt], st.o[nt][dt], 0, 0, 0);
+      if constexpr (TRAIN) st.o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt[dt], plo[nt], st.o[nt][dt], 0, 0, 0);
+    }
+}
+
+// Scheduling of a phase: N MFMAs, each followed by up to V vector instructions (transcendentals
+// included), so that the in-order issue of one wave alternates between the two units.
+template <int N, int V>
+__device__ inline void interleave_mfma_valu() {
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x402, V, 0);
+  }
+}
+
+// K and the key positions of the tile in LDS slot `slot` (lane's part at slot + 16*lane), one
+// statement ending in its own wait.
+__device__ inline void read_block_k(u32x4 (&k)[2][4], u32x4 (&tp)[2], uint32_t slot, uint32_t ap, int lane) {
+  const uint32_t at = slot + 16 * lane;
+  asm volatile(
+      "ds_read_b128 %0, %10\n"
+      "ds_read_b128 %1, %10 offset:1024\n"
+      "ds_read_b128 %2, %10 offset:2048\n"
+      "ds_read_b128 %3, %10 offset:3072\n"
+      "ds_read_b128 %4, %10 offset:4096\n"
+      "ds_read_b128 %5, %10 offset:5120\n"
+      "ds_read_b128 %6, %10 offset:6144\n"
+      "ds_read_b128 %7, %10 offset:7168\n"
+      "ds_read_b128 %8, %11\n"
+      "ds_read_b128 %9, %11 offset:64\n"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(k[0][0]), "=&v"(k[0][1]), "=&v"(k[0][2]), "=&v"(k[0][3]), "=&v"(k[1][0]), "=&v"(k[1][1]),
+        "=&v"(k[1][2]), "=&v"(k[1][3]), "=&v"(tp[0]), "=&v"(tp[1])
+      : "v"(at), "v"(ap));
+}
+
+// The transposing V reads of read_vt_tr split in two: issue_vt_tr starts them without waiting, so they
+// run under the MFMA and VALU work that follows; wait_vt_tr waits for them and unpacks the operands.
+// The raw registers pass from one statement to the other as in-out operands, so nothing reads them
+// before the wait.
+__device__ inline void issue_vt_tr(uint64_t (&x)[16], uint32_t slot, const uint32_t (&vo)[4]) {
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %16\n"
+      "ds_read_b64_tr_b16 %1, %16 offset:4128\n"
+      "ds_read_b64_tr_b16 %2, %16 offset:8\n"
+      "ds_read_b64_tr_b16 %3, %16 offset:4136\n"
+      "ds_read_b64_tr_b16 %4, %17\n"
+      "ds_read_b64_tr_b16 %5, %17 offset:4128\n"
+      "ds_read_b64_tr_b16 %6, %17 offset:8\n"
+      "ds_read_b64_tr_b16 %7, %17 offset:4136\n"
+      "ds_read_b64_tr_b16 %8, %18\n"
+      "ds_read_b64_tr_b16 %9, %18 offset:4128\n"
+      "ds_read_b64_tr_b16 %10, %18 offset:8\n"
+      "ds_read_b64_tr_b16 %11, %18 offset:4136\n"
+      "ds_read_b64_tr_b16 %12, %19\n"
+      "ds_read_b64_tr_b16 %13, %19 offset:4128\n"
+      "ds_read_b64_tr_b16 %14, %19 offset:8\n"
+      "ds_read_b64_tr_b16 %15, %19 offset:4136"
+      : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3]), "=&v"(x[4]), "=&v"(x[5]), "=&v"(x[6]), "=&v"(x[7]),
+        "=&v"(x[8]), "=&v"(x[9]), "=&v"(x[10]), "=&v"(x[11]), "=&v"(x[12]), "=&v"(x[13]), "=&v"(x[14]),
+        "=&v"(x[15])
+      : "v"(slot + vo[0]), "v"(slot + vo[1]), "v"(slot + vo[2]), "v"(slot + vo[3]));
+}
+__device__ inline void wait_vt_tr(bf16x8 (&vt)[8], uint64_t (&x)[16]) {
+  asm volatile("s_waitcnt lgkmcnt(0)"
+               : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(x[4]), "+v"(x[5]), "+v"(x[6]), "+v"(x[7]),
+                 "+v"(x[8]), "+v"(x[9]), "+v"(x[10]), "+v"(x[11]), "+v"(x[12]), "+v"(x[13]), "+v"(x[14]),
+                 "+v"(x[15]));
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) {
+    const uint64_t lo = x[2 * dt], hi = x[2 * dt + 1];
+    vt[dt] = as_bf16x8(u32x4{(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)});
+  }
+}
+
+// Whether a tile needs the visibility mask for a wave whose earliest row sits at `minpos`: some slot
+// absent (-1) or past minpos.  As unsigned, -1 exceeds every position.
+__device__ inline bool block_dirty(const u32x4 (&tp)[2], int minpos) {
+  const uint32_t a = max(max(tp[0][0], tp[0][1]), max(tp[0][2], tp[0][3]));
+  const uint32_t b = max(max(tp[1][0], tp[1][1]), max(tp[1][2], tp[1][3]));
+  const bool bad = minpos < 0 || max(a, b) > (uint32_t)minpos;
+  return __builtin_amdgcn_ballot_w64(bad) != 0;
+}
+
+// Split records of the bf16-output path keep the unnormalised outputs in bf16: two d-tiles of one
+// lane in 16 bytes.  Each merged output is a weighted mean of the records' rows, so their rounding
+// (relative 2^-9 per element) adds at most 2^-9 of the output's scale before its own bf16 rounding.
+// The training path (fp32 outputs) keeps fp32 records.
+__device__ inline f32x4 as_f32x4(const u32x4& v) { return __builtin_bit_cast(f32x4, v); }
+__device__ inline u32x4 as_u32x4(const f32x4& v) { return __builtin_bit_cast(u32x4, v); }
+__device__ inline u32x4 pack_record_bf16(const f32x4& a, const f32x4& b) {
+  return u32x4{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3])};
+}
+__device__ inline void unpack_record_bf16(const u32x4& w, f32x4& a, f32x4& b) {
+  a = f32x4{bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
+  b = f32x4{bf16_lo(w[2]), bf16_hi(w[2]), bf16_lo(w[3]), bf16_hi(w[3])};
+}
+
+// Workgroup barrier for LDS traffic: waits for this wave's LDS operations only, not for its global
+// loads in flight.
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // Branch b's outputs of row block rb (rows 16*nt + lane%16 of it) from an unnormalised state:
 // register r of d-tile dt holds d = 32*(lane/16) + 4*dt + r.  Rows past R are not written.
@@ -872,7 +1051,7 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
   const int lg = lane >> 4, lr = lane & 15;
 
   // ---- unit (sequence, KV head, row group) and this workgroup's share w of the unit's key stream
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int bid = xcd_remap(blockIdx.x + fetch_args(p), gridDim.x);   // kernel arguments in one round trip
   const int w = bid % p.nW;
   const int unit = bid / p.nW;
   const int rg = unit % p.n_rg;
@@ -888,15 +1067,10 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
   // stream through one slot table and one ring.  A branch met by one workgroup is finished there;
   // otherwise each piece leaves a record and the last of the branch's workgroups merges them in
   // stream order.
-  if (tid < p.nbr) sm.blen[tid] = block_branch_len(p, s, L, tid);   // nbr <= kBMaxPieces <= kBThreads
-  __syncthreads();
-  int total = 0, vt = 0;
-  for (int b = 0; b < p.nbr; ++b) {
-    total += sm.blen[b];
-    if (b < p.V) vt += sm.blen[b];
-  }
-  const BlockCut cut(vt, total, p.nW);
-  const int r0 = cut.start_of(w), r1 = cut.start_of(w + 1);
+  // The branch lengths, then the query rows: the rows are needed only at the first tile, so the
+  // barriers of the prologue wait for LDS traffic alone (a __syncthreads fence would wait for
+  // every global load in flight, the rows' included, at each of them).
+  const int blen_t = tid < p.nbr ? block_branch_len(p, s, L, tid) : 0;   // nbr <= kBMaxPieces <= kBThreads
 
   // ---- query rows of this wave's lanes: row n = rb*32 + 16*nt + lane%16
   bf16x8 qop[NT][4];
@@ -912,6 +1086,16 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = as_bf16x8(valid ? load16(qrow + 8 * kk) : u32x4{0u, 0u, 0u, 0u});
   }
+
+  if (tid < p.nbr) sm.blen[tid] = blen_t;
+  lds_barrier();
+  int total = 0, vt = 0;
+  for (int b = 0; b < p.nbr; ++b) {
+    total += sm.blen[b];
+    if (b < p.V) vt += sm.blen[b];
+  }
+  const BlockCut cut(vt, total, p.nW);
+  const int r0 = cut.start_of(w), r1 = cut.start_of(w + 1);
   const int minpos = L - p.nq + (rb * RB::kRows) / p.G;   // earliest row position of this wave
 
   // ---- the two loads of every tile that this wave issues, and the tile rows they read
@@ -974,7 +1158,7 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
       ++npc;
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- one slot table for every piece: all idx (and page-table) loads issued before any is used
   {
@@ -1024,10 +1208,10 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
 
-  // ---- stream every tile of every piece through the ring: tiles 0 .. kBRing-2 first
-  for (int t = 0; t < kBRing - 1; ++t) {
+  // ---- stream every tile of every piece through the ring: tiles 0 .. kBRing-3 first
+  for (int t = 0; t < kBRing - 2; ++t) {
     uint32_t r[2];
     asm volatile(
         "ds_read_b32 %0, %2\n"
@@ -1037,13 +1221,31 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
         : "v"(roff_lds + 4 * (kTile * t + rit0)), "v"(roff_lds + 4 * (kTile * t + rit1)));
     issue(t, r);
   }
-  // Tile t+kBRing-1 is issued in step t, after the barrier that frees its slot (read in step t-1).
+  // A head step takes the scores of tile 0; step t then finishes tile t and scores tile t+1 (the
+  // pipelined step above), reading tile t+1's K and tile t's V^T.  Barriers come at even steps: the
+  // one of step t publishes tiles t+1 and t+2 (this wave's loads of them are older than the two tiles
+  // issued after them) and certifies that every wave has finished step t-1, so the slots of tiles t-2
+  // and t-1 (last read in steps t-2 and t-1) take tiles t+5 and t+6.
   // At the last tile of a piece the wave finishes the piece: its rows' outputs when the piece is the
   // whole branch, else a record (stored now, counted once every piece is done) and a fresh state.
   // A wave without query rows (the row count is not a multiple of the block) only keeps the ring
-  // going: its own loop, so that the accumulators of the computing loop have one definition per
-  // step (a conditional step made the compiler copy every accumulator after its MFMA).
-  static_assert(2 * (kBRing - 2) == 8, "wait count follows the ring depth");
+  // going, with the same barriers.
+  static_assert(kBRing == 7, "the wait counts and the issue distance follow the ring depth");
+  auto issue_pair = [&](int t) {   // tiles t+5 and t+6, at even steps after the barrier
+    uint32_t r[4];
+    asm volatile(
+        "ds_read_b32 %0, %4\n"
+        "ds_read_b32 %1, %5\n"
+        "ds_read_b32 %2, %6\n"
+        "ds_read_b32 %3, %7\n"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
+        : "v"(roff_lds + 4 * (kTile * (t + 5) + rit0)), "v"(roff_lds + 4 * (kTile * (t + 5) + rit1)),
+          "v"(roff_lds + 4 * (kTile * (t + 6) + rit0)), "v"(roff_lds + 4 * (kTile * (t + 6) + rit1)));
+    const uint32_t r5[2] = {r[0], r[1]}, r6[2] = {r[2], r[3]};
+    issue(t + 5, r5);
+    issue(t + 6, r6);
+  };
   if (has_rows) {
     RowState<NT> st;
     auto reset = [&] {
@@ -1061,29 +1263,54 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
     BlockPiece pc = sm.pc[0];
     int t_end = pc.t0 + (pc.e1 - pc.e0 + kTile - 1) / kTile;
     bool want_lx = (pc.b < p.V ? p.lse_g : p.lse_f) != nullptr;
-    TileRegs<NT, true> T;
+    u32x4 kr[2][4], tp[2];
+    f32x4 sc[2][NT];        // scores of the tile this step finishes
+    float mx[NT];
+    {
+      asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");   // tile 0 (tiles 1..4 in flight)
+      read_block_k(kr, tp, ring_lds, tpos_lds + 4 * (4 * lg), lane);
+      block_qk<NT>(sc, kr, qop);
+      if (block_dirty(tp, minpos)) block_mask<NT>(sc, tp, rowpos);
+      block_tile_max<NT>(mx, sc, p.scale_log2);
+      block_raise<NT>(st, mx);
+    }
     for (int t = 0; t < ntl; ++t) {
-      // this wave's loads of tile t are older than the kBRing-2 tiles issued after it
-      asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
-      const int nxt = t + kBRing - 1;
-      const uint32_t src = ring_lds + (uint32_t)(t % kBRing) * kBTileBytes;
-      uint32_t r[2];
-      read_block_tile_k(T, r, src, tpos_lds, kTile * t, roff_lds, kTile * nxt, rit0, rit1, lane);
-      bool bad = false;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int tp = (int)T.tp[i >> 2][i & 3];
-        bad |= tp < 0 || tp > minpos;
+      if ((t & 1) == 0) {
+        asm volatile("s_waitcnt vmcnt(4)\n\ts_barrier" ::: "memory");   // tiles t+1, t+2 (t+3, t+4 in flight)
+        issue_pair(t);
       }
-      const bool dirty = __builtin_amdgcn_ballot_w64(bad) != 0;
-      issue(nxt, r);
-      tile_step<NT, true, TRAIN, true>(st, T, qop, rowpos, p.scale_log2, dirty, want_lx,
-                                       [&](int i) { return (int)T.tp[i >> 2][i & 3]; },
-                                       [&](bf16x8 (&vt)[8]) {
-                                         const uint32_t a[4] = {src + vtr_off[0], src + vtr_off[1],
-                                                                src + vtr_off[2], src + vtr_off[3]};
-                                         read_vt_tr(vt, a);
-                                       });
+      read_block_k(kr, tp, ring_lds + (uint32_t)((t + 1) % kBRing) * kBTileBytes,
+                   tpos_lds + 4 * (kTile * (t + 1) + 4 * lg), lane);
+      uint64_t xv[16];
+      issue_vt_tr(xv, ring_lds + (uint32_t)(t % kBRing) * kBTileBytes, vtr_off);
+      const bool dirty = block_dirty(tp, minpos);
+      // phase A: scores of tile t+1 | weights of tile t
+      f32x4 sn[2][NT];
+      bf16x8 pop[NT], plo[NT];
+      float w[NT][8];
+      block_qk<NT>(sn, kr, qop);
+      block_weights<NT, TRAIN>(st, sc, p.scale_log2, pop, plo, w);
+      interleave_mfma_valu<16, 3>();
+      if (want_lx) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          float sx = 0.f;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) sx += w[nt][i];
+          st.lx[nt] += sx;
+        }
+      }
+      if (dirty) block_mask<NT>(sn, tp, rowpos);
+      bf16x8 vt[8];
+      wait_vt_tr(vt, xv);
+      // phase B: PV of tile t | row maxima of tile t+1
+      block_pv<NT, TRAIN>(st, vt, pop, plo);
+      block_tile_max<NT>(mx, sn, p.scale_log2);
+      interleave_mfma_valu<(TRAIN ? 32 : 16), 2>();
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) sc[sub][nt] = sn[sub][nt];
       if (t + 1 == t_end) {
         // ---- piece k done: per-row (m, l, lx) of rows 16*nt + lane%16
         float lxw[NT], lw[NT];
@@ -1099,16 +1326,24 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
           write_rows(pc.b, st.m, lw, lxw, st.o);
         } else {
           // record pc.wo of the branch's pieces for this row block: row stats as float4
-          // (m, l, lx, -) per row, then the outputs as chunk (nt, dt) x lane float4s
+          // (m, l, lx, -) per row, then the outputs as chunk x lane 16-byte pieces: chunk (nt, dt) in
+          // fp32 on the training path, chunk (nt, d-tile pair) in bf16 otherwise
           const __amdgpu_buffer_rsrc_t urec = make_rsrc(unit_rec + ((int64_t)pc.slot * kBWaves + wave) * RB::kRec,
                                                         (uint32_t)(pc.nwg * kBWaves * RB::kRec * 4));
           const uint32_t rec = (uint32_t)pc.wo * kBWaves * RB::kRec * 4;
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) {
             if (lg == 0) store16_coherent(urec, rec + 16 * (16 * nt + lr), f32x4{st.m[nt], lw[nt], lxw[nt], 0.f});
+            if constexpr (TRAIN) {
 #pragma unroll
-            for (int dt = 0; dt < 8; ++dt)
-              store16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + dt) * kWave + lane), st.o[nt][dt]);
+              for (int dt = 0; dt < 8; ++dt)
+                store16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + dt) * kWave + lane), st.o[nt][dt]);
+            } else {
+#pragma unroll
+              for (int q = 0; q < 4; ++q)
+                store16_coherent(urec, rec + kOutOff + 16 * ((nt * 4 + q) * kWave + lane),
+                                 as_f32x4(pack_record_bf16(st.o[nt][2 * q], st.o[nt][2 * q + 1])));
+            }
           }
         }
         reset();
@@ -1118,19 +1353,13 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
           want_lx = (pc.b < p.V ? p.lse_g : p.lse_f) != nullptr;
         }
       }
+      block_raise<NT>(st, mx);
     }
   } else {
-    for (int t = 0; t < ntl; ++t) {
-      asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
-      const int nxt = t + kBRing - 1;
-      uint32_t r[2];
-      asm volatile(
-          "ds_read_b32 %0, %2\n"
-          "ds_read_b32 %1, %3\n"
-          "s_waitcnt lgkmcnt(0)"
-          : "=&v"(r[0]), "=&v"(r[1])
-          : "v"(roff_lds + 4 * (kTile * nxt + rit0)), "v"(roff_lds + 4 * (kTile * nxt + rit1)));
-      issue(nxt, r);
+    asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+    for (int t = 0; t < ntl; t += 2) {
+      asm volatile("s_waitcnt vmcnt(4)\n\ts_barrier" ::: "memory");
+      issue_pair(t);
     }
   }
 
@@ -1198,10 +1427,19 @@ __global__ __launch_bounds__(kWave) void block_merge_kernel(AttnParams p) {
       const uint32_t rec = (uint32_t)(k0 + u) * kBWaves * RB::kRec * 4;
       const bool ok = k0 + u < nwg;
       sv[u] = ok ? load16_coherent(urec, rec + 16 * (16 * nt + lr)) : f32x4{-INFINITY, 0.f, 0.f, 0.f};
+      if constexpr (TRAIN) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        ov[u][i] = ok ? load16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + 4 * dh + i) * kWave + lane))
-                      : f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < 4; ++i)
+          ov[u][i] = ok ? load16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + 4 * dh + i) * kWave + lane))
+                        : f32x4{0.f, 0.f, 0.f, 0.f};
+      } else {
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          const f32x4 w = ok ? load16_coherent(urec, rec + kOutOff + 16 * ((nt * 4 + 2 * dh + k) * kWave + lane))
+                             : f32x4{0.f, 0.f, 0.f, 0.f};
+          unpack_record_bf16(as_u32x4(w), ov[u][2 * k], ov[u][2 * k + 1]);
+        }
+      }
     }
 #pragma unroll
     for (int u = 0; u < kMBatch; ++u) {
