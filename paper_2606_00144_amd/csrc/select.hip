@@ -294,14 +294,18 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
     const uint32_t roff_lds = lds_addr(sm.roff);
     const uint32_t base16 = PAGED ? 0u : (uint32_t)(((int64_t)s * p.kv.stride_seq + (int64_t)g * p.kv.stride_head) >> 3);
     const uint32_t tok16 = (uint32_t)(p.kv.stride_tok >> 3);
+    // pass 2 takes its tiles last first: pass 1 read them first to last, so the most recent (still in
+    // the memory-side cache) are read before the lines pass 1 read first are replaced
+    auto real = [&](int it) { return PASS == 2 ? ntiles - 1 - it : it; };
     auto issue = [&](int tile, int slot) {
       uint32_t r[2];
       if constexpr (PAGED) {
-        read_krows(r, roff_lds, kTile * tile, lane);
+        if (tile >= ntiles) r[0] = r[1] = 0u;
+        else read_krows(r, roff_lds, kTile * real(tile), lane);
       } else if (tile >= ntiles) {
         r[0] = r[1] = 0u;                  // padding: row 0, a safe, cache-resident address
       } else {
-        const uint32_t r0 = base16 + (uint32_t)(k0 + kTile * tile) * tok16;
+        const uint32_t r0 = base16 + (uint32_t)(k0 + kTile * real(tile)) * tok16;
         r[0] = r0 + (uint32_t)lr * tok16;
         r[1] = r0 + (uint32_t)(16 + lr) * tok16;
       }
@@ -319,16 +323,21 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
       asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
       read_ktile(kt, ring_lds + slot * kTileBytes, lane);
       issue(it + kRing * kWaves, slot);
-      const int tb = k0 + kTile * it + 4 * lg;
+      const int tb = k0 + kTile * real(it) + 4 * lg;
       sub_step(kt[0], tb, dirty_tag);
       sub_step(kt[1], tb + 16, dirty_tag);
       ++j;
       return it + kWaves >= ntiles;
     };
-    // a wave's tiles increase, so its mask-free ones come first
+    // a wave's tiles increase in pass 1, so its mask-free ones come first; in pass 2 they come last
     bool last = false;
-    while (!last && wave + kWaves * j < first_dirty) last = step(std::integral_constant<bool, false>{});
-    while (!last) last = step(std::integral_constant<bool, true>{});
+    if constexpr (PASS == 1) {
+      while (!last && wave + kWaves * j < first_dirty) last = step(std::integral_constant<bool, false>{});
+      while (!last) last = step(std::integral_constant<bool, true>{});
+    } else {
+      while (!last && real(wave + kWaves * j) >= first_dirty) last = step(std::integral_constant<bool, true>{});
+      while (!last) last = step(std::integral_constant<bool, false>{});
+    }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // padding loads land before the block ends
   }
 
