@@ -459,8 +459,8 @@ __device__ inline void dq_merge_block(const AttnBwdParams& p, int id) {
 }
 
 // ---- dK/dV kernel ---------------------------------------------------------------
-// One workgroup of 8 waves per (sequence, KV head, branch) in two groups of 4: wave w of a group
-// owns the 16 block keys of key tile w (tiles w+4, w+8, ... in later passes), group 0 takes the
+// One workgroup of 8 waves per (sequence, KV head, branch, pass of 64 block keys) in two groups of
+// 4: wave w of a group owns the 16 block keys of key tile 4*pass + w, group 0 takes the
 // even 32-row tiles of the branch's query rows and group 1 the odd ones, and the groups' partial
 // sums are added in LDS at the end (two waves per SIMD: one wave's MFMA chains and LDS reads
 // overlap the other's).  The row tiles stream through an LDS ring, each tile carrying Q and dO
@@ -497,7 +497,9 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
   const int lg = lane >> 4, lr = lane & 15;
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
   const int br = bid % p.nbr;
-  const int pair = bid / p.nbr;                  // s * Hkv + g
+  const int npass = (p.nkt + kKGroupWaves - 1) / kKGroupWaves;
+  const int kpass = (bid / p.nbr) % npass;       // the block keys' pass: key tiles 4*kpass .. +3
+  const int pair = bid / p.nbr / npass;          // s * Hkv + g
   const int g = pair % p.Hkv, s = pair / p.Hkv;
   const bool gather = br < p.V;
   const int L = seq_len(p.kv, s);
@@ -563,7 +565,8 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
       make_rsrc(p.part_kv + (int64_t)pair * p.nbr * C * 2 * kD, (uint32_t)((int64_t)p.nbr * C * 2 * kD * 4));
   const bool direct = p.nbr == 1;
 
-  for (int kt0 = 0; kt0 < nkt; kt0 += kKGroupWaves) {
+  {
+    const int kt0 = kKGroupWaves * kpass;
     const int kt = kt0 + wk;
     const int c = 16 * kt + lr;                  // this lane's key
     const bool kvalid = kt < nkt && c < C && t0 + c >= 0;
@@ -584,7 +587,6 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) dk[dt] = dv[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    __syncthreads();                             // the previous pass's LDS reads are done
     issue(0);
     for (int i = 0; i < nit; ++i) {
       // step i's tile landed for every wave of the group, and step i-1's slot is free: the next
@@ -776,10 +778,11 @@ AttnBwdPlan plan_attn_bwd(int S, int Hkv, int Hq, int C, int num_views, int ld_i
   if (nw < 1) nw = 1;
   pl.nW = (int)nw;
   pl.nblk_q = (int)((int64_t)pl.units * nw);
-  pl.nblk_kv = with_dkv ? S * Hkv * pl.nbr : 0;
+  pl.nblk_kv = with_dkv ? S * Hkv * pl.nbr * ((pl.nkt + kKGroupWaves - 1) / kKGroupWaves) : 0;   // 64 keys each
   pl.counter_bytes = BD_WS_COUNTER_BYTES;
   pl.q_record_bytes = nw > 1 ? align256(sizeof(float) * kRecFloats * (size_t)pl.units * kQWaves * nw) : 0;
-  pl.kv_record_bytes = with_dkv && pl.nbr > 1 ? align256(sizeof(float) * (size_t)pl.nblk_kv * C * 2 * kD) : 0;
+  pl.kv_record_bytes =
+      with_dkv && pl.nbr > 1 ? align256(sizeof(float) * (size_t)S * Hkv * pl.nbr * C * 2 * kD) : 0;   // per key
   pl.R_pad = pl.n_rb * 32;
   pl.d_bytes = with_dkv ? align256(sizeof(float) * 2 * (size_t)pl.nbr * S * Hkv * pl.R_pad) : 0;
   pl.ws_bytes = pl.counter_bytes + pl.q_record_bytes + pl.kv_record_bytes + pl.d_bytes;
