@@ -211,6 +211,23 @@ __device__ inline void dq_tile_step(f32x4 (&acc)[2][8], const DqRows& rw, const 
   }
 }
 
+// Every kernel argument line requested at entry, so the arguments cost one memory round trip (the
+// compiler would otherwise fetch each where it is first used).  The statements touch no memory and
+// return 0, which the caller adds to its block index.
+__device__ inline int fetch_bwd_args(const AttnBwdParams& p) {
+  int z0, z1;
+  asm("s_mov_b32 %0, 0" : "=s"(z0) : "s"(p.kv.k), "s"(p.kv.v), "s"(p.kv.seq_lens), "s"(p.kv.page_table),
+      "s"(p.kv.stride_seq), "s"(p.kv.stride_head), "s"(p.kv.stride_tok), "s"(p.kv.stride_page), "s"(p.q),
+      "s"(p.o32_g), "s"(p.lse_g), "s"(p.dout_g), "s"(p.o32_f), "s"(p.lse_f), "s"(p.dout_f));
+  asm("s_mov_b32 %0, 0" : "=s"(z1) : "s"(z0), "s"(p.idx), "s"(p.nsel), "s"(p.ld_idx), "s"(p.S), "s"(p.R),
+      "s"(p.nW), "s"(p.nkt), "s"(p.scale_log2), "s"(p.max_roff), "s"(p.dq), "s"(p.part_q), "s"(p.rstats),
+      "s"(p.R_pad), "s"(p.counters));
+  return z1;
+}
+// Workgroup barrier for LDS traffic: waits for this wave's LDS operations only, not for its global
+// loads in flight (which a __syncthreads fence would wait for).
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // The dQ kernel's cut of a unit's key stream (StreamCut): equal shares starting on whole tiles.
 // Weighting gathered entries more, as the forward does, was slower here (163 vs 144 us; 178 vs
 // 137 us with all pieces of a range in one slot table): the gathered tiles of the views, each row
@@ -226,7 +243,7 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
   const int lg = lane >> 4, lr = lane & 15;
 
   // ---- unit (sequence, KV head, row group) and this workgroup's share w of the unit's key stream
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int bid = xcd_remap(blockIdx.x + fetch_bwd_args(p), gridDim.x);
   const int w = bid % p.nW;
   const int unit = bid / p.nW;
   const int rg = unit % p.n_rg;
@@ -273,20 +290,38 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
     for (int kk = 0; kk < 4; ++kk)
       rw.qop[nt][kk] = as_bf16x8(rvalid[nt] ? load16(p.q + orow[nt] * kD + 32 * lg + 8 * kk) : u32x4{0u, 0u, 0u, 0u});
   }
-  auto load_branch_rows = [&](int b) {
+  // A branch's rows: the loads are issued before the piece's slot table is filled (its idx loads
+  // then share their round trip), the sums D = <dO, O> taken after it.
+  struct BranchRaw {
+    u32x4 dv[2][4];
+    f32x4 o[2][4][2];
+    float lse[2];
+  };
+  auto issue_branch_rows = [&](int b, BranchRaw& x) {
     const bool gb = b < p.V;
     const float* outb = gb ? p.o32_g + (int64_t)b * branch_rows * kD : p.o32_f;
     const uint16_t* doutb = gb ? p.dout_g + (int64_t)b * branch_rows * kD : p.dout_f;
     const float* lseb = gb ? p.lse_g + (int64_t)b * branch_rows : p.lse_f;
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
-      float dsum = 0.f;
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         const int64_t off = orow[nt] * kD + 32 * lg + 8 * kk;
-        const u32x4 dv = rvalid[nt] ? load16(doutb + off) : u32x4{0u, 0u, 0u, 0u};
-        const f32x4 o0 = rvalid[nt] ? *reinterpret_cast<const f32x4*>(outb + off) : f32x4{0.f, 0.f, 0.f, 0.f};
-        const f32x4 o1 = rvalid[nt] ? *reinterpret_cast<const f32x4*>(outb + off + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+        x.dv[nt][kk] = rvalid[nt] ? load16(doutb + off) : u32x4{0u, 0u, 0u, 0u};
+        x.o[nt][kk][0] = rvalid[nt] ? *reinterpret_cast<const f32x4*>(outb + off) : f32x4{0.f, 0.f, 0.f, 0.f};
+        x.o[nt][kk][1] = rvalid[nt] ? *reinterpret_cast<const f32x4*>(outb + off + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+      x.lse[nt] = rvalid[nt] ? lseb[orow[nt]] : INFINITY;
+    }
+  };
+  auto finish_branch_rows = [&](const BranchRaw& x) {
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      float dsum = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const u32x4 dv = x.dv[nt][kk];
+        const f32x4 o0 = x.o[nt][kk][0], o1 = x.o[nt][kk][1];
         rw.dop[nt][kk] = as_bf16x8(dv);
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
@@ -295,7 +330,7 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
         }
       }
       rw.Dr[nt] = sum_xor32(sum_xor16(dsum));
-      const float l2 = rvalid[nt] ? lseb[orow[nt]] * kLog2e : INFINITY;
+      const float l2 = x.lse[nt] * kLog2e;
       rw.lse2[nt] = l2 == -INFINITY ? INFINITY : l2;   // a row that saw no key has all-zero weights
     }
   };
@@ -372,18 +407,21 @@ __global__ __launch_bounds__(kQThreads) void dq_kernel(AttnBwdParams p) {
     off += n;
     if (lo >= hi) continue;
     const int e0 = lo - (off - n), e1 = hi - (off - n);
-    load_branch_rows(b);
+    BranchRaw raw;
+    issue_branch_rows(b, raw);
+    const int32_t* idx_row = b < p.V ? p.idx + (((int64_t)b * p.S + s) * p.Hkv + g) * p.ld_idx : nullptr;
+    const int nslots = ((e1 - e0 + kTile - 1) / kTile + kQRing) * kTile;
+    // these barriers wait for LDS traffic alone (a __syncthreads fence would wait for the rows too)
+    lds_barrier();                                // the previous piece's slot table and ring are free
+    fill_slot_table<PAGED, kQThreads, kQSlotCap>(p.kv, s, g, L, idx_row, e0, e1, nslots, sm.roff, sm.tpos, tid);
+    lds_barrier();
+    finish_branch_rows(raw);
     if (e0 == 0 && p.rstats && lg == 0) {         // the branch's first workgroup publishes the row stats
       float* rs = p.rstats + (((int64_t)b * p.S * p.Hkv + pair) * p.R_pad + rb * 32) * 2;
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt)
         if (rvalid[nt]) *reinterpret_cast<float2*>(rs + 2 * (16 * nt + lr)) = float2{rw.lse2[nt], rw.Dr[nt]};
     }
-    const int32_t* idx_row = b < p.V ? p.idx + (((int64_t)b * p.S + s) * p.Hkv + g) * p.ld_idx : nullptr;
-    const int nslots = ((e1 - e0 + kTile - 1) / kTile + kQRing) * kTile;
-    __syncthreads();                              // the previous piece's slot table and ring are free
-    fill_slot_table<PAGED, kQThreads, kQSlotCap>(p.kv, s, g, L, idx_row, e0, e1, nslots, sm.roff, sm.tpos, tid);
-    __syncthreads();
     stream(e0, e1);
   }
 
