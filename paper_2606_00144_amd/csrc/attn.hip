@@ -1288,9 +1288,13 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
       f32x4 sn[2][NT];
       bf16x8 pop[NT], plo[NT];
       float w[NT][8];
+      // raised issue priority for this half: the two waves of a SIMD drift into opposite halves of
+      // the step, one issuing score MFMAs and exponentials while the other runs its PV product
+      __builtin_amdgcn_s_setprio(1);
       block_qk<NT>(sn, kr, qop);
       block_weights<NT, TRAIN>(st, sc, p.scale_log2, pop, plo, w);
       interleave_mfma_valu<16, 3>();
+      __builtin_amdgcn_s_setprio(0);
       if (want_lx) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
