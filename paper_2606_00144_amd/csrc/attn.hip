@@ -236,14 +236,10 @@ struct RowState {
 // One 32-key tile of one wave.  `dirty` (wave-uniform) asks for the visibility mask: only tiles
 // at the causal edge, at the ragged end of a split or holding absent entries need it.  `want_lx`
 // (uniform) keeps the exact weight sum the log-sum-exp output is computed from.
-// TRAIN: each weight enters the PV product and the normaliser as a bf16 pair hi + lo (lo the rounded
-// remainder), so the output carries the weights to about 2^-17 instead of 2^-9: the fp32 output then
-// serves the backward's <dO, O> (which cancels against <dO, v_t>) without amplifying rounding.
 // `get_v` delivers the tile's V rows (8 x 16 bytes per lane) just before the PV product, so a caller
-// may read them from LDS only then.  VTR: `get_v` delivers the 8 V^T operands themselves
-// (read_vt_tr's layout: register r of d-tile dt in lane l holds d = 32*(l/16) + 4*dt + r);
-// otherwise they are transposed here (register i of d-tile dt holds d = 32*(l/16) + 8*i + dt).
-template <int NT, bool PAGED, bool TRAIN = false, bool VTR = false, class PosFn, class VFn>
+// may read them from LDS only then; they are transposed here (register i of d-tile dt holds
+// d = 32*(l/16) + 8*i + dt).
+template <int NT, bool PAGED, class PosFn, class VFn>
 __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T, const bf16x8 (&qop)[NT][4],
                                  const int (&rowpos)[NT], float scale_log2, bool dirty, bool want_lx,
                                  PosFn pos_of, VFn get_v) {
@@ -299,7 +295,6 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
 
   const bf16x8 ones = as_bf16x8(u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
   bf16x8 pop[NT];
-  bf16x8 plo[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const float muse = st.m[nt] == -INFINITY ? 0.f : st.m[nt];
@@ -310,13 +305,6 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
 #pragma unroll
     for (int i = 0; i < 4; ++i) pw[i] = pack_bf16x2(pv[2 * i], pv[2 * i + 1]);
     pop[nt] = as_bf16x8(pw);
-    if constexpr (TRAIN) {
-      u32x4 lw;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) lw[i] = pack_bf16x2(pv[2 * i] - bf16_lo(pw[i]), pv[2 * i + 1] - bf16_hi(pw[i]));
-      plo[nt] = as_bf16x8(lw);
-      st.l[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, plo[nt], st.l[nt], 0, 0, 0);
-    }
     if (want_lx) {
       float sx = 0.f;
 #pragma unroll
@@ -327,23 +315,14 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
     st.l[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pop[nt], st.l[nt], 0, 0, 0);
   }
 
-  auto pv = [&](int dt, const bf16x8& vt) {
+  u32x4 vrows[8];
+  get_v(vrows);
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
+  for (int dt = 0; dt < 8; ++dt) {
+    const bf16x8 vt = vt_operand(vrows, dt);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
       st.o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, pop[nt], st.o[nt][dt], 0, 0, 0);
-      if constexpr (TRAIN) st.o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt, plo[nt], st.o[nt][dt], 0, 0, 0);
-    }
-  };
-  if constexpr (VTR) {
-    bf16x8 vts[8];
-    get_v(vts);
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) pv(dt, vts[dt]);
-  } else {
-    u32x4 vrows[8];
-    get_v(vrows);
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) pv(dt, vt_operand(vrows, dt));
   }
 }
 
@@ -790,7 +769,8 @@ __device__ inline void dma_load(const KvView& kv, uint32_t r, uint32_t max_roff,
 // the scores of tile t into weights (phase A), then the PV product of tile t while the vector units
 // take the row maxima of tile t+1 (phase B).  Neither half's MFMA work depends on its VALU work, so
 // one wave keeps both units busy instead of alternating between them.  Per tile the arithmetic is
-// tile_step's, in the same order: the results are the same bits.
+// the split kernel's tile_step (plus the two-term weights of the training outputs), in the same
+// order, with the V^T operands from transposing LDS reads.
 
 // Scores S^T = K Q^T of one tile (unscaled): sub-tile sub, register r of lane l holds key
 // 16*sub + 4*(l/16) + r of row 16*nt + l%16.
@@ -852,9 +832,12 @@ __device__ inline void block_raise(RowState<NT>& st, const float (&mx)[NT]) {
   }
 }
 
-// Weights of a tile against the reference max, rounded to bf16 for the PV product (TRAIN: with the
-// bf16 remainder as a second operand), summed into the normaliser by MFMA; `w` keeps them unrounded
-// for the log-sum-exp sum.
+// Weights of a tile against the reference max, rounded to bf16 for the PV product, summed into the
+// normaliser by MFMA (which then sums exactly the rounded weights the PV product sees); `w` keeps
+// them unrounded for the log-sum-exp sum.  TRAIN: each weight enters the PV product and the
+// normaliser as a bf16 pair hi + lo (lo the rounded remainder), so the output carries the weights to
+// about 2^-17 instead of 2^-9: the fp32 output then serves the backward's <dO, O> (which cancels
+// against <dO, v_t>) without amplifying rounding.
 template <int NT, bool TRAIN>
 __device__ inline void block_weights(RowState<NT>& st, const f32x4 (&s)[2][NT], float scale_log2, bf16x8 (&pop)[NT],
                                      bf16x8 (&plo)[NT], float (&w)[NT][8]) {
