@@ -1,0 +1,174 @@
+"""Seeded sweeps of selection, decode and verify over random shapes against the fp64 oracle.
+
+Each case draws the batch, the KV head count and group size, and ragged cache lengths.  Selection
+cases also draw:
+  - the window (1..64 rows), budget (below, at and above the cache length), scale and pooling width;
+  - token or chunk mode (chunk sizes 1..16), with both budget readings;
+  - a contiguous or paged cache (random page order, page size 16 or 32).
+Decode and verify cases also draw:
+  - gamma (0..7) and the list width;
+  - per-sequence entry counts (zero, partial, full), absent (-1) and out-of-range entries, and
+    garbage past the count;
+  - a contiguous or paged cache.
+Outputs are preallocated and poisoned first (indices with a sentinel, floats with NaN), so an
+output the kernels never write fails.  Indices follow the two-part exact protocol of the selection
+tests; bf16 outputs are within 2e-2 + 1e-2 |oracle|, log-sum-exps within 1e-3.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2606_00144_amd as bd
+import synth
+from gpu_utils import (assert_close, assert_lse, bf16_dev, bf16_host64, case, check_chunk_selection,
+                       check_selection, i32_dev, oracle_chunk_selection, oracle_scores, paged_kv)
+
+pytestmark = pytest.mark.gpu
+
+
+def _bits(g, shape):
+    return synth.f32_to_bf16_bits(g.standard_normal(shape, dtype=np.float32))
+
+
+def _page_table(g, lens, ps):
+    """A random page order for every sequence's pages: table [S][max_pages] (-1 past a sequence's
+    last page) and the pool size."""
+    npg = [(int(L) + ps - 1) // ps for L in lens]
+    perm = g.permutation(sum(npg)).astype(np.int32)
+    table = np.full((len(lens), max(npg)), -1, np.int32)
+    o = 0
+    for s, n in enumerate(npg):
+        table[s, :n] = perm[o:o + n]
+        o += n
+    return table, int(sum(npg))
+
+
+def _cache(g, k, v, lens, paged):
+    """Device K/V (V may be None) as given, or scattered into a paged pool; the page table or None."""
+    if not paged:
+        return bf16_dev(k), (bf16_dev(v) if v is not None else None), None
+    ps = int(g.choice([16, 32]))
+    table, npages = _page_table(g, lens, ps)
+    ks = [k[s][:, :int(L)] for s, L in enumerate(lens)]
+    vs = [(v if v is not None else k)[s][:, :int(L)] for s, L in enumerate(lens)]
+    kd, vd = paged_kv(ks, vs, table, npages, ps)
+    return kd, (vd if v is not None else None), i32_dev(table)
+
+
+def _draw_select(seed):
+    g = np.random.default_rng(5000 + seed)
+    S = int(g.integers(1, 4))
+    Hkv = int(g.choice([1, 2, 4]))
+    G = int(g.choice([1, 2, 4, 8]))
+    W = int(g.choice([1, 4, 16, 32, 64]))
+    while W * G > 256:                       # up to two 128-row blocks; keeps the oracle quick
+        W //= 2
+    lens = [int(g.integers(W, 3000)) for _ in range(S)]
+    B = int(g.integers(W, 1400))
+    pool = int(g.choice([1, 3, 5, 7, 9]))
+    chunk = int(g.choice([0, 0, 1, 5, 8, 16]))   # 0: token mode
+    cw = bool(g.random() < 0.5)
+    paged = bool(g.random() < 0.35)
+    scale = None if g.random() < 0.7 else float(g.uniform(0.03, 0.2))
+    return g, S, Hkv, G, W, lens, B, pool, chunk, cw, paged, scale
+
+
+@pytest.mark.parametrize("seed", list(range(24)))
+def test_select_random_shapes(seed):
+    g, S, Hkv, G, W, lens, B, pool, chunk, cw, paged, scale = _draw_select(seed)
+    Hq = Hkv * G
+    k = _bits(g, (S, Hkv, max(lens), 128))
+    q = _bits(g, (S, W, Hq, 128))
+    kd, _, table = _cache(g, k, None, lens, paged)
+    what = (f"select sweep {seed}: S={S} Hkv={Hkv} G={G} W={W} B={B} lens={lens} pool={pool} chunk={chunk} "
+            f"cw={cw} paged={paged} scale={scale}")
+    case(what)
+    ld = B if (chunk == 0 or cw) else B + W
+    idx = torch.full((S, Hkv, ld), -7, dtype=torch.int32, device="cuda")
+    nsel = torch.full((S,), -7, dtype=torch.int32, device="cuda")
+    scores = torch.full((S, Hkv, max(lens)), float("nan"), dtype=torch.float32, device="cuda")
+    if chunk == 0:
+        bd.bd_select_kv(kd, bf16_dev(q), i32_dev(lens), B, pool_kernel=pool, scale=scale, return_scores=True,
+                        page_table=table, max_seq_len=max(lens), outputs=(idx, nsel, scores))
+    else:
+        bd.bd_select_kv_chunks(kd, bf16_dev(q), i32_dev(lens), B, chunk=chunk, budget_counts_window=cw,
+                               scale=scale, return_scores=True, page_table=table, max_seq_len=max(lens),
+                               outputs=(idx, nsel, scores))
+    torch.cuda.synchronize()
+    gi, gn, gs = idx.cpu().numpy(), nsel.cpu().numpy(), scores.cpu().numpy()
+    raws = oracle_scores(k, q, lens, Hq, scale)
+    if chunk == 0:
+        near = check_selection(gi, gn, gs, raws, lens, W, B, what, pool_kernel=pool, Hq=Hq)
+    else:
+        oi, on = oracle_chunk_selection(raws, lens, Hkv, W, B, chunk, cw)
+        near = check_chunk_selection(gi, gn, gs, oi, on, raws, lens, W, B, chunk, cw, what)
+    assert near <= S * Hkv, what
+
+
+def _draw_attn(seed):
+    g = np.random.default_rng(6000 + seed)
+    S = int(g.integers(1, 5))
+    Hkv = int(g.choice([1, 2, 4, 8]))
+    G = int(g.choice([1, 2, 4, 8]))
+    gamma = int(g.integers(0, 8))
+    lens = [int(g.integers(gamma + 1, 5000)) for _ in range(S)]
+    ld = int(g.integers(1, 2100))
+    paged = bool(g.random() < 0.4)
+    scale = None if g.random() < 0.7 else float(g.uniform(0.03, 0.2))
+    return g, S, Hkv, G, gamma, lens, ld, paged, scale
+
+
+def _lists(g, S, Hkv, lens, ld):
+    """Decode lists: per sequence an entry count (zero, partial or the full width); per head distinct
+    in-range positions with some absent (-1) and out-of-range (>= L) entries; garbage past the count."""
+    idx = g.integers(-5, max(lens) + 60, (S, Hkv, ld)).astype(np.int32)
+    nsel = np.zeros(S, np.int32)
+    for s, L in enumerate(lens):
+        r = g.random()
+        n = 0 if r < 0.1 else (ld if r < 0.4 else int(g.integers(1, ld + 1)))
+        nsel[s] = n
+        for h in range(Hkv):
+            m = min(n, L)
+            row = g.choice(L, m, replace=False).astype(np.int32)
+            if m:
+                holes = g.random(m) < 0.05
+                row[holes] = np.where(g.random(holes.sum()) < 0.5, -1, L + g.integers(0, 50, holes.sum()))
+            idx[s, h, :m] = row
+            idx[s, h, m:n] = -1
+    return idx, nsel
+
+
+@pytest.mark.parametrize("seed", list(range(24)))
+def test_decode_verify_random_shapes(seed):
+    g, S, Hkv, G, gamma, lens, ld, paged, scale = _draw_attn(seed)
+    Hq = Hkv * G
+    Lm = max(lens)
+    k, v = _bits(g, (S, Hkv, Lm, 128)), _bits(g, (S, Hkv, Lm, 128))
+    qv = _bits(g, (S, gamma + 1, Hq, 128))
+    qd = _bits(g, (S, Hq, 128))
+    idx, nsel = _lists(g, S, Hkv, lens, ld)
+    if seed % 4 == 3:
+        nsel[0] = 0                          # an empty list: zero output, -inf log-sum-exp
+    kd, vd, table = _cache(g, k, v, lens, paged)
+    what = f"attn sweep {seed}: S={S} Hkv={Hkv} G={G} gamma={gamma} ld={ld} lens={lens} paged={paged} scale={scale}"
+    nan16 = lambda shape: torch.full(shape, float("nan"), dtype=torch.bfloat16, device="cuda")
+    nan32 = lambda shape: torch.full(shape, float("nan"), dtype=torch.float32, device="cuda")
+
+    case(what + " decode")
+    out, lse = nan16((S, Hq, 128)), nan32((S, Hq))
+    bd.bd_sparse_decode_attn(kd, vd, bf16_dev(qd), i32_dev(idx), i32_dev(nsel), i32_dev(lens), scale=scale,
+                             return_lse=True, page_table=table, max_seq_len=Lm, out=out, lse=lse)
+    torch.cuda.synchronize()
+    ro, rl = O.sparse_decode_attn(k, v, qd, idx, nsel, lens, scale=scale)
+    assert_close(bf16_host64(out), ro, what + " decode")
+    assert_lse(lse.cpu().numpy().astype(np.float64), rl, what + " decode")
+
+    case(what + " verify")
+    out, lse = nan16((S, gamma + 1, Hq, 128)), nan32((S, gamma + 1, Hq))
+    bd.bd_verify_attn(kd, vd, bf16_dev(qv), i32_dev(lens), scale=scale, return_lse=True, page_table=table,
+                      max_seq_len=Lm, out=out, lse=lse)
+    torch.cuda.synchronize()
+    ro, rl = O.verify_attn(k, v, qv, lens, gamma, scale=scale)
+    assert_close(bf16_host64(out), ro, what + " verify")
+    assert_lse(lse.cpu().numpy().astype(np.float64), rl, what + " verify")
