@@ -1,4 +1,4 @@
-"""Seeded sweeps of selection, decode and verify over random shapes against the fp64 oracle.
+"""Seeded sweeps of selection, decode, verify and acceptance over random shapes against the fp64 oracle.
 
 Each case draws the batch, the KV head count and group size, and ragged cache lengths.  Selection
 cases also draw:
@@ -10,6 +10,8 @@ Decode and verify cases also draw:
   - per-sequence entry counts (zero, partial, full), absent (-1) and out-of-range entries, and
     garbage past the count;
   - a contiguous or paged cache.
+Acceptance cases draw the batch, gamma (0..15), vocabularies of 1..200K entries with padded rows,
+ties and entries at the most negative float.
 Outputs are preallocated and poisoned first (indices with a sentinel, floats with NaN), so an
 output the kernels never write fails.  Indices follow the two-part exact protocol of the selection
 tests; bf16 outputs are within 2e-2 + 1e-2 |oracle|, log-sum-exps within 1e-3.
@@ -172,3 +174,47 @@ def test_decode_verify_random_shapes(seed):
     ro, rl = O.verify_attn(k, v, qv, lens, gamma, scale=scale)
     assert_close(bf16_host64(out), ro, what + " verify")
     assert_lse(lse.cpu().numpy().astype(np.float64), rl, what + " verify")
+
+
+def _draw_accept(seed):
+    g = np.random.default_rng(7000 + seed)
+    S = int(g.integers(1, 65))
+    gamma = int(g.integers(0, 16))
+    V = int(g.choice([int(g.integers(1, 64)), int(g.integers(64, 5000)), int(g.integers(5000, 200000))]))
+    pad = int(g.choice([0, 0, 1, 3, 64]))    # row stride V + pad
+    ties = bool(g.random() < 0.4)
+    return g, S, gamma, V, pad, ties
+
+
+@pytest.mark.parametrize("seed", list(range(24)))
+def test_accept_random_shapes(seed):
+    """Greedy acceptance on seeded shapes: vocabularies of 1..200K (vector and scalar scans), padded
+    rows, heavy ties and entries at the most negative float, maxima at either end, drafts matching a
+    planted prefix; accepted lengths, bonus tokens and argmax bit-exact against the oracle."""
+    g, S, gamma, V, pad, ties = _draw_accept(seed)
+    R = gamma + 1
+    big = g.standard_normal((S, R, V + pad)).astype(np.float32)
+    if ties:
+        big = np.floor(big * 1.5).astype(np.float32)
+    big[g.random(big.shape) < 0.01] = -np.finfo(np.float32).max   # logits are finite by contract
+    for s in range(S):                       # maxima planted at the first or the last index of some rows
+        i = int(g.integers(0, R))
+        big[s, i, 0 if g.random() < 0.5 else V - 1] = 100.0
+    logits = big[:, :, :V]
+    am = np.array([[O.greedy_argmax(logits[s, i]) for i in range(R)] for s in range(S)], np.int32).reshape(S, R)
+    draft = g.integers(0, V, (S, gamma)).astype(np.int32)
+    for s in range(S):
+        m = int(g.integers(0, gamma + 1))
+        draft[s, :m] = am[s, :m]
+    what = f"accept sweep {seed}: S={S} gamma={gamma} V={V} pad={pad} ties={ties}"
+    case(what)
+    dbig = torch.from_numpy(big).to("cuda")
+    acc = torch.full((S,), -7, dtype=torch.int32, device="cuda")
+    bonus = torch.full((S,), -7, dtype=torch.int32, device="cuda")
+    gam = torch.full((S, R), -7, dtype=torch.int32, device="cuda")
+    bd.bd_accept_len(dbig[:, :, :V], i32_dev(draft), return_argmax=True, outputs=(acc, bonus, gam))
+    torch.cuda.synchronize()
+    ra, rb, ram = O.accept_len(logits, draft, gamma)
+    assert np.array_equal(gam.cpu().numpy(), ram), what
+    assert np.array_equal(acc.cpu().numpy(), ra), what
+    assert np.array_equal(bonus.cpu().numpy(), rb), what
