@@ -40,12 +40,15 @@
  *     writes its other scratch only past them.  One workspace can therefore
  *     serve any sequence of calls, of any operation and shape, issued on one
  *     stream.  Calls that overlap in time (two streams) must not share a
- *     workspace.  The library never allocates device memory.
+ *     workspace.  The library never allocates device memory.  A size function
+ *     returns 0 for arguments its operation rejects.
  *   - Errors: arguments are checked on the host before anything is launched;
  *     on error nothing is launched and no output is touched.  A launch failure
  *     reported by the HIP runtime is BD_ERR_DEVICE.  No C++ exception crosses
  *     this interface.  bd_last_error() gives the reason of the last failure
- *     on the calling thread.
+ *     on the calling thread.  Operations on the KV cache refuse more than 2^24
+ *     (sequence, KV head) pairs or more than 2^16 query heads per KV head as
+ *     BD_ERR_UNSUPPORTED.
  *   - Device-side bounds: entries of idx outside [0, L_s) are skipped, counts
  *     above the stated maxima are clamped, and paged keys whose page number is
  *     outside [0, num_pages) are skipped, so malformed device data cannot make

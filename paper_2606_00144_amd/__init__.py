@@ -34,7 +34,7 @@ __all__ = [
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-library_path = os.path.join(_HERE, "libbd.so")
+library_path = os.environ.get("BD_LIBRARY") or os.path.join(_HERE, "libbd.so")
 
 BD_OK, BD_ERR_INVALID_ARG, BD_ERR_UNSUPPORTED, BD_ERR_WORKSPACE, BD_ERR_DEVICE = range(5)
 HEAD_DIM = 128

@@ -157,12 +157,12 @@ AcceptPlan plan_accept(int S, int gamma, int vocab) {
   AcceptPlan pl;
   const int64_t rows = (int64_t)S * (gamma + 1);
   int64_t want = (kTargetBlocks + rows - 1) / rows;
-  const int64_t max_split = (vocab + 4 * kThreads - 1) / (4 * kThreads);   // >= 1024 floats per chunk
-  const int64_t min_split = (vocab + 4 * kThreads * kUnroll - 1) / (4 * kThreads * kUnroll);   // one load round
+  const int64_t max_split = ((int64_t)vocab + 4 * kThreads - 1) / (4 * kThreads);   // >= 1024 floats per chunk
+  const int64_t min_split = ((int64_t)vocab + 4 * kThreads * kUnroll - 1) / (4 * kThreads * kUnroll);   // one load round
   if (want > max_split) want = max_split;
   if (want < min_split) want = min_split;
   if (want < 1) want = 1;
-  int64_t chunk = (vocab + want - 1) / want;
+  int64_t chunk = ((int64_t)vocab + want - 1) / want;
   chunk = (chunk + 3) & ~int64_t(3);
   pl.chunk = (int)chunk;
   pl.nsplit = (int)((vocab + chunk - 1) / chunk);

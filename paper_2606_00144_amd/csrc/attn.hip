@@ -1469,11 +1469,15 @@ __global__ __launch_bounds__(kWave) void block_merge_kernel(AttnParams p) {
 
 }  // namespace
 
+// Counts held in int fields saturate at 2^30: the callers reject such shapes after planning (too many
+// work units or workgroups), and the products formed from them stay inside int64.
+static int sat_count(int64_t x) { return x > (int64_t(1) << 30) ? (1 << 30) : (int)x; }
+
 AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full, bool paged,
                    bool train) {
   AttnPlan pl{};
   const int G = Hq / Hkv;
-  pl.R = nq * G;
+  pl.R = sat_count((int64_t)nq * G);
   pl.nt = pl.R <= 16 ? 1 : 2;
   const int rows = 16 * pl.nt;
   pl.n_rb = (pl.R + rows - 1) / rows;
@@ -1486,8 +1490,13 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
     // workgroups per (sequence, KV head, row group) unit, each taking an equal share of the unit's
     // key stream: enough to fill the CUs once, and enough that no share (rounded up to whole tiles)
     // overflows the slot table
-    pl.units = S * Hkv * pl.n_rg;
-    pl.nbr = num_views + (with_full ? 1 : 0);
+    pl.units = sat_count((int64_t)S * Hkv * pl.n_rg);
+    pl.nbr = sat_count((int64_t)num_views + (with_full ? 1 : 0));
+    if (pl.nbr > kBMaxPieces) {      // more branches than a range holds pieces: not launchable
+      pl.nblk = -1;
+      pl.ws_bytes = pl.counter_bytes;
+      return pl;
+    }
     const int64_t stream_max = (int64_t)num_views * ld_idx + (with_full ? max_L : 0);
     int64_t nw = (kTargetBlocks + pl.units - 1) / pl.units;
     const int64_t nw_table = stream_cut_min_workgroups<kWGather, kWFull>(stream_max, kMaxSplitKeys);
@@ -1501,8 +1510,8 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
     pl.ws_bytes = pl.counter_bytes + pl.record_bytes;
     return pl;
   }
-  pl.units_g = num_views * S * Hkv * pl.n_rg;
-  pl.units_f = with_full ? S * Hkv * pl.n_rg : 0;
+  pl.units_g = sat_count((int64_t)num_views * S * Hkv * pl.n_rg);
+  pl.units_f = with_full ? sat_count((int64_t)S * Hkv * pl.n_rg) : 0;
   constexpr int64_t kStep = kWaves * kTile;       // one tile per wave of the split kernel
   auto round_up = [](int64_t x, int64_t m) { return (x + m - 1) / m * m; };
   const int64_t work = (int64_t)pl.units_g * ld_idx + (int64_t)pl.units_f * max_L;
@@ -1514,6 +1523,12 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
   // offsets and is not.
   int64_t kps = round_up((work + kTargetBlocks - 1) / kTargetBlocks, kStep);
   if (kps < kStep) kps = kStep;
+  // with more units than target workgroups no split count reaches the target: the search below
+  // would end at one split per unit, so it starts there
+  if ((int64_t)pl.units_g + pl.units_f > kTargetBlocks) {
+    const int64_t all = g_all > f_all ? g_all : f_all;
+    if (kps < all) kps = all;
+  }
   int64_t kg, kf, blocks;
   for (;;) {
     kg = kps < g_all ? kps : g_all;
@@ -1529,7 +1544,7 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
   pl.nsplit_g = ld_idx > 0 ? (int)((ld_idx + kg - 1) / kg) : 1;
   pl.nsplit_f = max_L > 0 ? (int)((max_L + kf - 1) / kf) : 1;
   blocks = (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f;
-  pl.nblk = (int)blocks;
+  pl.nblk = blocks > INT32_MAX ? -1 : (int)blocks;
   const bool split = (pl.units_g && pl.nsplit_g > 1) || (pl.units_f && pl.nsplit_f > 1);
   pl.record_bytes = split ? align256(sizeof(float) * attn_record_floats(pl.nt) * (size_t)blocks) : 0;
   pl.ws_bytes = pl.counter_bytes + pl.record_bytes;
@@ -1569,11 +1584,12 @@ hipError_t launch_attn(const AttnParams& args, const AttnPlan& pl, bool paged, h
 
 size_t attn_ws_bytes(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full,
                      bool train_capable) {
-  size_t best = 0;
+  size_t best = 0;   // over the variants that can launch; 0 if none can
   for (int paged = 0; paged < 2; ++paged)
     for (int train = 0; train <= (train_capable ? 1 : 0); ++train) {
-      const size_t b = plan_attn(S, Hkv, Hq, nq, num_views, ld_idx, max_L, with_full, paged != 0, train != 0).ws_bytes;
-      best = b > best ? b : best;
+      const AttnPlan pl = plan_attn(S, Hkv, Hq, nq, num_views, ld_idx, max_L, with_full, paged != 0, train != 0);
+      if (pl.nblk < 0) continue;
+      best = pl.ws_bytes > best ? pl.ws_bytes : best;
     }
   return best;
 }

@@ -800,12 +800,19 @@ __global__ __launch_bounds__(kWave) void bwd_merge_kernel(AttnBwdParams p, int n
 AttnBwdPlan plan_attn_bwd(int S, int Hkv, int Hq, int C, int num_views, int ld_idx, int max_L, bool with_full,
                           bool with_dkv) {
   AttnBwdPlan pl{};
+  // counts held in int fields saturate at 2^30 (the caller rejects such shapes after planning)
+  auto sat = [](int64_t x) { return x > (int64_t(1) << 30) ? (1 << 30) : (int)x; };
   const int G = Hq / Hkv;
-  pl.R = C * G;
+  pl.R = sat((int64_t)C * G);
   pl.n_rb = (pl.R + 31) / 32;
   pl.n_rg = (pl.n_rb + kQWaves - 1) / kQWaves;
-  pl.units = S * Hkv * pl.n_rg;
-  pl.nbr = num_views + (with_full ? 1 : 0);
+  pl.units = sat((int64_t)S * Hkv * pl.n_rg);
+  pl.nbr = sat((int64_t)num_views + (with_full ? 1 : 0));
+  pl.counter_bytes = BD_WS_COUNTER_BYTES;
+  if (pl.nbr > 64) {                 // more branches than supported: the caller rejects the shape
+    pl.ws_bytes = pl.counter_bytes;
+    return pl;
+  }
   pl.nkt = (C + 15) / 16;
   // workgroups per unit: enough to fill the CUs once, and enough that no range overflows the slot
   // table (a piece's range is at most kMaxSplitKeys entries)
@@ -815,9 +822,9 @@ AttnBwdPlan plan_attn_bwd(int S, int Hkv, int Hq, int C, int num_views, int ld_i
   if (nw < nw_table) nw = nw_table;
   if (nw < 1) nw = 1;
   pl.nW = (int)nw;
-  pl.nblk_q = (int)((int64_t)pl.units * nw);
-  pl.nblk_kv = with_dkv ? S * Hkv * pl.nbr * ((pl.nkt + kKGroupWaves - 1) / kKGroupWaves) : 0;   // 64 keys each
-  pl.counter_bytes = BD_WS_COUNTER_BYTES;
+  pl.nblk_q = sat((int64_t)pl.units * nw);
+  // dK/dV workgroups: 64 keys each
+  pl.nblk_kv = with_dkv ? sat((int64_t)S * Hkv * pl.nbr * ((pl.nkt + kKGroupWaves - 1) / kKGroupWaves)) : 0;
   pl.q_record_bytes = nw > 1 ? align256(sizeof(float) * kRecFloats * (size_t)pl.units * kQWaves * nw) : 0;
   pl.kv_record_bytes =
       with_dkv && pl.nbr > 1 ? align256(sizeof(float) * (size_t)S * Hkv * pl.nbr * C * 2 * kD) : 0;   // per key

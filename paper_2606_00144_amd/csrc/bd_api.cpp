@@ -28,6 +28,15 @@ bd_status fail(bd_status st, const char* fmt, ...) {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// Bounds on the batch shape under which every plan's arithmetic stays in range: (sequence, KV head)
+// pairs and query heads per KV head.  The operations reject larger shapes as unsupported and the
+// workspace-size functions answer 0 for them.
+constexpr int64_t kMaxPairs = (int64_t)1 << 24;
+constexpr int32_t kMaxGroup = 1 << 16;
+bool shape_ok(int32_t S, int32_t Hkv, int32_t Hq) {
+  return S >= 1 && Hkv >= 1 && Hq >= 1 && Hq % Hkv == 0 && (int64_t)S * Hkv <= kMaxPairs && Hq / Hkv <= kMaxGroup;
+}
+
 // Checks shared by every operation that reads the KV cache.
 bd_status check_kv(const bd_kv_desc* kv, bool need_v, int32_t num_q_heads) {
   if (!kv) return fail(BD_ERR_INVALID_ARG, "kv descriptor is NULL");
@@ -41,6 +50,8 @@ bd_status check_kv(const bd_kv_desc* kv, bool need_v, int32_t num_q_heads) {
   if (num_q_heads < 1 || num_q_heads % kv->num_kv_heads != 0)
     return fail(BD_ERR_INVALID_ARG, "num_q_heads %d is not a positive multiple of num_kv_heads %d", num_q_heads,
                 kv->num_kv_heads);
+  if ((int64_t)kv->num_seqs * kv->num_kv_heads > kMaxPairs || num_q_heads / kv->num_kv_heads > kMaxGroup)
+    return fail(BD_ERR_UNSUPPORTED, "more than 2^24 (sequence, KV head) pairs or 2^16 query heads per KV head");
   if (kv->stride_head < 0 || kv->stride_tok < 0 || kv->stride_head % 8 || kv->stride_tok % 8)
     return fail(BD_ERR_INVALID_ARG, "stride_head and stride_tok must be non-negative multiples of 8 elements");
   if (kv->page_table) {
@@ -129,6 +140,7 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
   const bd::AttnPlan pl =
       bd::plan_attn(kv->num_seqs, kv->num_kv_heads, Hq, nq, num_views, ld_idx, kv->max_seq_len, out_full != nullptr,
                     kv->page_table != nullptr, train);
+  if (pl.block && pl.nbr > 64) return fail(BD_ERR_UNSUPPORTED, "more than 63 views with a block of more than 32 rows");
   if (pl.nblk < 0 || (!pl.block && (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f > INT32_MAX))
     return fail(BD_ERR_UNSUPPORTED, "problem too large for one launch");
   if (kv_extent(kv) > ((int64_t)1 << 34))
@@ -137,7 +149,6 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
     return fail(BD_ERR_UNSUPPORTED, "more than %d work units", BD_WS_COUNTER_LINES);
   if (pl.block && (int64_t)(pl.nW + pl.nbr) * 8 * bd::attn_record_floats(2) * 4 > INT32_MAX)
     return fail(BD_ERR_UNSUPPORTED, "too many partial records per unit");
-  if (pl.block && pl.nbr > 64) return fail(BD_ERR_UNSUPPORTED, "more than 63 views with a block of more than 32 rows");
   bd_status st = BD_OK;
   if (use_fixed_scratch) {
     if (pl.ws_bytes > (size_t)BD_NOALLOC_SCRATCH_BYTES)
@@ -211,7 +222,9 @@ int32_t bd_abi_version(void) { return BD_ABI_VERSION; }
 // ---------------------------------------------------------------- select
 size_t bd_select_kv_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads, int32_t window,
                                     int32_t max_seq_len) {
-  if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || window < 1 || max_seq_len < 0) return 0;
+  if (!shape_ok(num_seqs, num_kv_heads, num_q_heads) || window < 1 || max_seq_len < 0) return 0;
+  if ((int64_t)max_seq_len - window > BD_SELECT_MAX_PREFIX || (int64_t)window * (num_q_heads / num_kv_heads) > 4096)
+    return 0;
   return bd::plan_select(num_seqs, num_kv_heads, num_q_heads, window, max_seq_len, true).ws_bytes;
 }
 
@@ -236,7 +249,8 @@ bd_status run_select(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_
   if (!idx_out || !nsel_out) return fail(BD_ERR_INVALID_ARG, "idx_out and nsel_out are required");
   if ((int64_t)kv->max_seq_len - window > BD_SELECT_MAX_PREFIX)
     return fail(BD_ERR_UNSUPPORTED, "max_seq_len - window exceeds %d", BD_SELECT_MAX_PREFIX);
-  if (window * (num_q_heads / kv->num_kv_heads) > 4096) return fail(BD_ERR_UNSUPPORTED, "window * group above 4096 rows");
+  if ((int64_t)window * (num_q_heads / kv->num_kv_heads) > 4096)
+    return fail(BD_ERR_UNSUPPORTED, "window * group above 4096 rows");
   if (kv_extent(kv) > ((int64_t)1 << 34))
     return fail(BD_ERR_UNSUPPORTED, "K layout spans more than 2^34 elements");
   const bd::SelectPlan pl = bd::plan_select(kv->num_seqs, kv->num_kv_heads, num_q_heads, window, kv->max_seq_len,
@@ -295,7 +309,7 @@ bd_status bd_select_kv_chunks(const bd_kv_desc* kv, const uint16_t* q_win, int32
 // ---------------------------------------------------------------- sparse decode
 size_t bd_sparse_decode_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
                                              int32_t ld_idx) {
-  if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || ld_idx < 0) return 0;
+  if (!shape_ok(num_seqs, num_kv_heads, num_q_heads) || ld_idx < 0) return 0;
   return bd::attn_ws_bytes(num_seqs, num_kv_heads, num_q_heads, 1, 1, ld_idx, 0, false);
 }
 
@@ -317,8 +331,8 @@ bd_status bd_sparse_decode_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t
 size_t bd_multiview_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
                                          int32_t block_len, int32_t num_views, int32_t ld_idx, int32_t max_seq_len,
                                          int32_t with_full) {
-  if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || block_len < 1 || num_views < 0 || ld_idx < 0 ||
-      max_seq_len < 0)
+  if (!shape_ok(num_seqs, num_kv_heads, num_q_heads) || block_len < 1 || num_views < 0 || ld_idx < 0 ||
+      max_seq_len < 0 || (int64_t)block_len * (num_q_heads / num_kv_heads) > (1 << 20))
     return 0;
   return bd::attn_ws_bytes(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld_idx, max_seq_len,
                            with_full != 0, true);
@@ -331,7 +345,7 @@ bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t
                             hipStream_t stream) {
   bd_status st = check_kv(kv, true, num_q_heads);
   if (st != BD_OK) return st;
-  if (block_len < 1 || num_views < 0 || num_views + (out_full ? 1 : 0) < 1)
+  if (block_len < 1 || num_views < 0 || (num_views < 1 && !out_full))
     return fail(BD_ERR_INVALID_ARG, "need block_len >= 1 and at least one view or the full branch");
   if (!q_blk || !aligned(q_blk, 16)) return fail(BD_ERR_INVALID_ARG, "q_blk is NULL or not 16-byte aligned");
   if (num_views > 0 && (!idx_views || !nsel_views || !out_views || !aligned(out_views, 16) || ld_idx < 0))
@@ -351,8 +365,9 @@ bd_status bd_multiview_attn(const bd_kv_desc* kv, const uint16_t* q_blk, int32_t
 size_t bd_multiview_attn_bwd_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads,
                                              int32_t block_len, int32_t num_views, int32_t ld_idx,
                                              int32_t max_seq_len, int32_t with_full) {
-  if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || block_len < 1 || num_views < 0 || ld_idx < 0 ||
-      max_seq_len < 0)
+  if (!shape_ok(num_seqs, num_kv_heads, num_q_heads) || block_len < 1 || block_len > bd::kMaxBwdBlock ||
+      num_views < 0 || num_views > 64 - (with_full != 0 ? 1 : 0) || ld_idx < 0 || max_seq_len < 0 ||
+      (int64_t)block_len * (num_q_heads / num_kv_heads) > (1 << 20))
     return 0;
   const int32_t ld = num_views > 0 ? ld_idx : 0;
   return bd::plan_attn_bwd(num_seqs, num_kv_heads, num_q_heads, block_len, num_views, ld, max_seq_len,
@@ -368,7 +383,7 @@ bd_status bd_multiview_attn_bwd(const bd_kv_desc* kv, const uint16_t* q_blk, int
   bd_status st = check_kv(kv, true, num_q_heads);
   if (st != BD_OK) return st;
   const bool full = dout_full != nullptr;
-  if (block_len < 1 || num_views < 0 || num_views + (full ? 1 : 0) < 1)
+  if (block_len < 1 || num_views < 0 || (num_views < 1 && !full))
     return fail(BD_ERR_INVALID_ARG, "need block_len >= 1 and at least one view or the full branch");
   if (block_len > bd::kMaxBwdBlock) return fail(BD_ERR_UNSUPPORTED, "block_len above %d", bd::kMaxBwdBlock);
   if ((int64_t)block_len * (num_q_heads / kv->num_kv_heads) > (1 << 20))
@@ -446,7 +461,7 @@ bd_status bd_multiview_attn_bwd(const bd_kv_desc* kv, const uint16_t* q_blk, int
 // ---------------------------------------------------------------- verify
 size_t bd_verify_attn_workspace_bytes(int32_t num_seqs, int32_t num_kv_heads, int32_t num_q_heads, int32_t gamma,
                                       int32_t max_seq_len) {
-  if (num_seqs < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || gamma < 0 || max_seq_len < 0) return 0;
+  if (!shape_ok(num_seqs, num_kv_heads, num_q_heads) || gamma < 0 || gamma > 4095 || max_seq_len < 0) return 0;
   return bd::attn_ws_bytes(num_seqs, num_kv_heads, num_q_heads, gamma + 1, 0, 0, max_seq_len, true);
 }
 
@@ -481,7 +496,7 @@ bd_status bd_verify_attn_noalloc(const bd_kv_desc* kv, const uint16_t* q, int32_
 
 // ---------------------------------------------------------------- accept
 size_t bd_accept_len_workspace_bytes(int32_t num_seqs, int32_t gamma, int32_t vocab) {
-  if (num_seqs < 1 || gamma < 0 || vocab < 1) return 0;
+  if (num_seqs < 1 || gamma < 0 || gamma > 63 || vocab < 1) return 0;
   return bd::plan_accept(num_seqs, gamma, vocab).ws_bytes;
 }
 

@@ -167,13 +167,13 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(const float* u, int32_
 
 CePlan plan_ce(int rows, int vocab) {
   CePlan pl;
-  int64_t want = (kTargetBlocks + rows - 1) / rows;
-  const int64_t max_split = (vocab + 4 * kThreads - 1) / (4 * kThreads);
-  const int64_t min_split = (vocab + 4 * kThreads * kUnroll - 1) / (4 * kThreads * kUnroll);
+  int64_t want = ((int64_t)kTargetBlocks + rows - 1) / rows;
+  const int64_t max_split = ((int64_t)vocab + 4 * kThreads - 1) / (4 * kThreads);
+  const int64_t min_split = ((int64_t)vocab + 4 * kThreads * kUnroll - 1) / (4 * kThreads * kUnroll);
   if (want > max_split) want = max_split;
   if (want < min_split) want = min_split;
   if (want < 1) want = 1;
-  int64_t chunk = (vocab + want - 1) / want;
+  int64_t chunk = ((int64_t)vocab + want - 1) / want;
   chunk = (chunk + 3) & ~int64_t(3);
   pl.chunk = (int)chunk;
   pl.nsplit = (int)((vocab + chunk - 1) / chunk);
@@ -188,8 +188,8 @@ hipError_t launch_ce(const CeParams& p, hipStream_t stream) {
 }
 
 hipError_t launch_sample(const float* u, int32_t count, const SampleTable& t, int32_t* out, hipStream_t stream) {
-  hipLaunchKernelGGL(sample_kernel, dim3((count + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, u, count, t,
-                     out);
+  const unsigned nb = (unsigned)(((int64_t)count + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(sample_kernel, dim3(nb), dim3(kThreads), 0, stream, u, count, t, out);
   return hipGetLastError();
 }
 

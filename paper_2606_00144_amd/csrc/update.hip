@@ -92,12 +92,14 @@ hipError_t launch_append(const AppendParams& p, hipStream_t stream) {
   hipLaunchKernelGGL(append_rows_kernel, dim3(p.kv.num_seqs * p.n), dim3(kThreads), 0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(append_advance_kernel, dim3((p.kv.num_seqs + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, p);
+  const unsigned nb = (unsigned)(((int64_t)p.kv.num_seqs + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(append_advance_kernel, dim3(nb), dim3(kThreads), 0, stream, p);
   return hipGetLastError();
 }
 
 hipError_t launch_rollback(const RollbackParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL(rollback_kernel, dim3((p.S + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, p);
+  const unsigned nb = (unsigned)(((int64_t)p.S + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(rollback_kernel, dim3(nb), dim3(kThreads), 0, stream, p);
   return hipGetLastError();
 }
 

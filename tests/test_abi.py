@@ -185,3 +185,46 @@ def test_update_rejections(L):
     assert R(FAKE, None, FAKE, 0, 5, None, None, None) == bd.BD_ERR_INVALID_ARG
     assert R(FAKE, None, FAKE, 2, -1, None, None, None) == bd.BD_ERR_INVALID_ARG
     assert R(FAKE, None, FAKE, 2, 5, FAKE, FAKE, None) == bd.BD_ERR_INVALID_ARG     # base_nsel without nsel
+
+
+_EXTREME = [-2 ** 31, -1, 0, 1, 2, 7, 8, 32, 33, 64, 4096, 16384, 32768, 65536, 2 ** 24, 2 ** 30, 2 ** 31 - 1]
+
+
+def test_workspace_sizes_of_extreme_shapes(L):
+    """Every size function answers for any arguments (0 for shapes its operation rejects) and never
+    fails: seeded random and extreme arguments.  Built with the host sanitizers (build.py
+    --host-sanitize) this run also shows that the planning arithmetic stays in range."""
+    import random
+    sizes = {n: len(sig[1]) for n, sig in bd._SIGNATURES.items() if n.endswith("_workspace_bytes")}
+    rng = random.Random(11)
+    for name, nargs in sizes.items():
+        f = getattr(L, name)
+        for _ in range(3000):
+            args = [rng.choice(_EXTREME) if rng.random() < 0.6 else rng.randint(-10, 70000) for _ in range(nargs)]
+            assert f(*args) >= 0, (name, args)
+    # shapes the operations reject give 0
+    assert L.bd_verify_attn_workspace_bytes(2 ** 16, 2 ** 9, 2 ** 9, 5, 4096) == 0       # more than 2^24 pairs
+    assert L.bd_verify_attn_workspace_bytes(8, 8, 32, 4096, 16384) == 0                   # gamma above 4095
+    assert L.bd_sparse_decode_attn_workspace_bytes(8, 1, 2 ** 17, 1024) == 0              # group above 2^16
+    assert L.bd_select_kv_workspace_bytes(8, 8, 32, 2 ** 31 - 1, 16384) == 0              # window * group
+    assert L.bd_select_kv_workspace_bytes(8, 8, 32, 32, 40000) == 0                       # prefix above the cap
+    assert L.bd_multiview_attn_workspace_bytes(4, 8, 32, 2 ** 19, 4, 2048, 8192, 1) == 0  # block * group
+    assert L.bd_multiview_attn_bwd_workspace_bytes(4, 8, 32, 64, 64, 2048, 8192, 1) == 0  # 65 branches
+    assert L.bd_accept_len_workspace_bytes(8, 64, 128256) == 0                            # gamma above 63
+
+
+def test_extreme_shapes_are_refused_before_launch(L):
+    """Sizes whose plans would leave 32- or 64-bit range are refused by the host checks."""
+    assert _verify(L, _kv(num_seqs=2 ** 20, num_kv_heads=32), hq=32) == bd.BD_ERR_UNSUPPORTED   # 2^25 pairs
+    assert _verify(L, _kv(num_kv_heads=1), hq=2 ** 17) == bd.BD_ERR_UNSUPPORTED                 # group 2^17
+    assert _verify(L, _kv(), gamma=2 ** 31 - 1) == bd.BD_ERR_INVALID_ARG
+    kv = _kv()
+    sel = lambda W, hq: L.bd_select_kv(ctypes.byref(kv), FAKE, hq, W, 2 ** 31 - 1, 7, 0.1, None, FAKE, FAKE, None,
+                                       FAKE, 1 << 40, None)
+    assert sel(2 ** 31 - 1, 64) == bd.BD_ERR_UNSUPPORTED       # window * group overflows 32 bits
+    assert sel(4096, 64) == bd.BD_ERR_UNSUPPORTED
+    mv = lambda C, V: L.bd_multiview_attn(ctypes.byref(kv), FAKE, 32, C, V, FAKE, 2 ** 31 - 1, FAKE, 0.1, FAKE, None,
+                                          None, FAKE, None, None, FAKE, 1 << 40, None)
+    assert mv(1, 2 ** 31 - 1) == bd.BD_ERR_UNSUPPORTED           # views x pairs: too many work units
+    assert mv(64, 2 ** 31 - 1) == bd.BD_ERR_UNSUPPORTED          # block mode: too many branches
+    assert mv(2 ** 31 - 1, 4) == bd.BD_ERR_UNSUPPORTED           # block * group
