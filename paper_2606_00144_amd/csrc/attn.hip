@@ -744,6 +744,14 @@ constexpr int kBTileBytes = 8192 + kRmTileBytes;
 struct BlockPiece {
   int32_t b, e0, e1, t0, nwg, slot, wo;
 };
+// A piece read from LDS, made wave-uniform: the record address built from it then stays in scalar
+// registers (a per-lane address would turn every record store into a loop over distinct values).
+__device__ inline BlockPiece uniform_piece(const BlockPiece& x) {
+  return BlockPiece{__builtin_amdgcn_readfirstlane(x.b), __builtin_amdgcn_readfirstlane(x.e0),
+                    __builtin_amdgcn_readfirstlane(x.e1), __builtin_amdgcn_readfirstlane(x.t0),
+                    __builtin_amdgcn_readfirstlane(x.nwg), __builtin_amdgcn_readfirstlane(x.slot),
+                    __builtin_amdgcn_readfirstlane(x.wo)};
+}
 
 struct BlockSmem {
   alignas(16) int32_t roff[kBSlotCap];
@@ -1243,7 +1251,7 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
     };
     reset();
     int k = 0;
-    BlockPiece pc = sm.pc[0];
+    BlockPiece pc = uniform_piece(sm.pc[0]);
     int t_end = pc.t0 + (pc.e1 - pc.e0 + kTile - 1) / kTile;
     bool want_lx = (pc.b < p.V ? p.lse_g : p.lse_f) != nullptr;
     u32x4 kr[2][4], tp[2];
@@ -1335,7 +1343,7 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
         }
         reset();
         if (++k < npc) {
-          pc = sm.pc[k];
+          pc = uniform_piece(sm.pc[k]);
           t_end = pc.t0 + (pc.e1 - pc.e0 + kTile - 1) / kTile;
           want_lx = (pc.b < p.V ? p.lse_g : p.lse_f) != nullptr;
         }
