@@ -4,7 +4,8 @@ Each case draws the number of sequences, KV heads, group size, block length, vie
 capacity and fill, the sequence lengths (down to shorter than the block) and whether the training
 outputs are requested, so that workgroup ranges start and end at every offset of the tile pipeline
 (odd and even tile counts, pieces ending between the paired barriers, one-tile and empty ranges) and
-views hold absent, out-of-range and repeated entries.  Outputs are poisoned with NaN first, so a row
+views hold absent, out-of-range and repeated entries.  Forward cases also draw the query magnitude
+(standard deviation 1, 4 or 16: logits spanning up to tens of nats).  Outputs are poisoned with NaN first, so a row
 that is never written fails.  Tolerances as elsewhere: bf16 outputs within 2e-2 + 1e-2 |oracle|, fp32
 outputs within 1e-4 max|oracle| + 1e-4 |oracle|, log-sum-exps within 1e-3.
 """
@@ -45,8 +46,8 @@ def _draw(seed):
     return S, Hkv, G, C, V, full, train, lens, ld, idx, nsel
 
 
-def _bits(g, shape):
-    return synth.f32_to_bf16_bits(g.standard_normal(shape, dtype=np.float32))
+def _bits(g, shape, sd=1.0):
+    return synth.f32_to_bf16_bits((sd * g.standard_normal(shape, dtype=np.float32)).astype(np.float32))
 
 
 @pytest.mark.parametrize("seed", list(range(16)))
@@ -55,14 +56,15 @@ def test_multiview_random_shapes(seed):
     g = np.random.default_rng(2000 + seed)
     Lm = max(lens)
     k, v = _bits(g, (S, Hkv, Lm, 128)), _bits(g, (S, Hkv, Lm, 128))
-    qb = _bits(g, (S, C, Hkv * G, 128))
+    qsd = float(g.choice([1.0, 4.0, 16.0]))         # query magnitude: logits spanning up to tens of nats
+    qb = _bits(g, (S, C, Hkv * G, 128), qsd)
     Hq = Hkv * G
     nan16 = lambda shape: torch.full(shape, float("nan"), dtype=torch.bfloat16, device="cuda")
     nan32 = lambda shape: torch.full(shape, float("nan"), dtype=torch.float32, device="cuda")
     outs = (nan16((V, S, C, Hq, 128)) if V else None, nan16((S, C, Hq, 128)) if full else None,
             nan32((V, S, C, Hq, 128)) if (V and train) else None, nan32((V, S, C, Hq)) if (V and train) else None,
             nan32((S, C, Hq, 128)) if (full and train) else None, nan32((S, C, Hq)) if (full and train) else None)
-    what = f"sweep {seed}: S={S} Hkv={Hkv} G={G} C={C} V={V} ld={ld} full={full} train={train} lens={lens}"
+    what = f"sweep {seed}: S={S} Hkv={Hkv} G={G} C={C} V={V} ld={ld} full={full} train={train} lens={lens} q_sd={qsd}"
     case(what)
     res = bd.bd_multiview_attn(bf16_dev(k), bf16_dev(v), bf16_dev(qb), i32_dev(idx) if V else None,
                                i32_dev(nsel) if V else None, i32_dev(lens), full=full, train=train, outputs=outs)

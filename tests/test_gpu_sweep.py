@@ -3,10 +3,12 @@
 Each case draws the batch, the KV head count and group size, and ragged cache lengths.  Selection
 cases also draw:
   - the window (1..64 rows), budget (below, at and above the cache length), scale and pooling width;
+  - the query magnitude (standard deviation 1 or 4);
   - token or chunk mode (chunk sizes 1..16), with both budget readings;
   - a contiguous or paged cache (random page order, page size 16 or 32).
 Decode and verify cases also draw:
-  - gamma (0..7) and the list width;
+  - gamma (0..7), the list width and the query magnitude (standard deviation 1, 4 or 16: logits
+    spanning tens of nats, so the lazily raised reference maximum moves often);
   - per-sequence entry counts (zero, partial, full), absent (-1) and out-of-range entries, and
     garbage past the count;
   - a contiguous or paged cache.
@@ -29,8 +31,8 @@ from gpu_utils import (assert_close, assert_lse, bf16_dev, bf16_host64, case, ch
 pytestmark = pytest.mark.gpu
 
 
-def _bits(g, shape):
-    return synth.f32_to_bf16_bits(g.standard_normal(shape, dtype=np.float32))
+def _bits(g, shape, sd=1.0):
+    return synth.f32_to_bf16_bits((sd * g.standard_normal(shape, dtype=np.float32)).astype(np.float32))
 
 
 def _page_table(g, lens, ps):
@@ -73,18 +75,21 @@ def _draw_select(seed):
     cw = bool(g.random() < 0.5)
     paged = bool(g.random() < 0.35)
     scale = None if g.random() < 0.7 else float(g.uniform(0.03, 0.2))
-    return g, S, Hkv, G, W, lens, B, pool, chunk, cw, paged, scale
+    # query magnitude: up to sd 4, so the boundary scores stay normal fp32 numbers (where they would
+    # underflow in fp32 but not in fp64, the two precisions rank them differently by definition)
+    qsd = float(g.choice([1.0, 4.0]))
+    return g, S, Hkv, G, W, lens, B, pool, chunk, cw, paged, scale, qsd
 
 
 @pytest.mark.parametrize("seed", list(range(24)))
 def test_select_random_shapes(seed):
-    g, S, Hkv, G, W, lens, B, pool, chunk, cw, paged, scale = _draw_select(seed)
+    g, S, Hkv, G, W, lens, B, pool, chunk, cw, paged, scale, qsd = _draw_select(seed)
     Hq = Hkv * G
     k = _bits(g, (S, Hkv, max(lens), 128))
-    q = _bits(g, (S, W, Hq, 128))
+    q = _bits(g, (S, W, Hq, 128), qsd)
     kd, _, table = _cache(g, k, None, lens, paged)
     what = (f"select sweep {seed}: S={S} Hkv={Hkv} G={G} W={W} B={B} lens={lens} pool={pool} chunk={chunk} "
-            f"cw={cw} paged={paged} scale={scale}")
+            f"cw={cw} paged={paged} scale={scale} q_sd={qsd}")
     case(what)
     ld = B if (chunk == 0 or cw) else B + W
     idx = torch.full((S, Hkv, ld), -7, dtype=torch.int32, device="cuda")
@@ -118,7 +123,8 @@ def _draw_attn(seed):
     ld = int(g.integers(1, 2100))
     paged = bool(g.random() < 0.4)
     scale = None if g.random() < 0.7 else float(g.uniform(0.03, 0.2))
-    return g, S, Hkv, G, gamma, lens, ld, paged, scale
+    qsd = float(g.choice([1.0, 4.0, 16.0]))
+    return g, S, Hkv, G, gamma, lens, ld, paged, scale, qsd
 
 
 def _lists(g, S, Hkv, lens, ld):
@@ -143,17 +149,18 @@ def _lists(g, S, Hkv, lens, ld):
 
 @pytest.mark.parametrize("seed", list(range(24)))
 def test_decode_verify_random_shapes(seed):
-    g, S, Hkv, G, gamma, lens, ld, paged, scale = _draw_attn(seed)
+    g, S, Hkv, G, gamma, lens, ld, paged, scale, qsd = _draw_attn(seed)
     Hq = Hkv * G
     Lm = max(lens)
     k, v = _bits(g, (S, Hkv, Lm, 128)), _bits(g, (S, Hkv, Lm, 128))
-    qv = _bits(g, (S, gamma + 1, Hq, 128))
-    qd = _bits(g, (S, Hq, 128))
+    qv = _bits(g, (S, gamma + 1, Hq, 128), qsd)
+    qd = _bits(g, (S, Hq, 128), qsd)
     idx, nsel = _lists(g, S, Hkv, lens, ld)
     if seed % 4 == 3:
         nsel[0] = 0                          # an empty list: zero output, -inf log-sum-exp
     kd, vd, table = _cache(g, k, v, lens, paged)
-    what = f"attn sweep {seed}: S={S} Hkv={Hkv} G={G} gamma={gamma} ld={ld} lens={lens} paged={paged} scale={scale}"
+    what = (f"attn sweep {seed}: S={S} Hkv={Hkv} G={G} gamma={gamma} ld={ld} lens={lens} paged={paged} "
+            f"scale={scale} q_sd={qsd}")
     nan16 = lambda shape: torch.full(shape, float("nan"), dtype=torch.bfloat16, device="cuda")
     nan32 = lambda shape: torch.full(shape, float("nan"), dtype=torch.float32, device="cuda")
 
