@@ -228,3 +228,35 @@ def test_extreme_shapes_are_refused_before_launch(L):
     assert mv(1, 2 ** 31 - 1) == bd.BD_ERR_UNSUPPORTED           # views x pairs: too many work units
     assert mv(64, 2 ** 31 - 1) == bd.BD_ERR_UNSUPPORTED          # block mode: too many branches
     assert mv(2 ** 31 - 1, 4) == bd.BD_ERR_UNSUPPORTED           # block * group
+
+
+def test_header_serves_a_c_program(L, tmp_path):
+    """include/bd.h compiles as C11 (warnings as errors for the program's own code) and a C program
+    links against the library and calls it: a refused call gives its status and reason."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not found")
+    src = tmp_path / "abi.c"
+    src.write_text(
+        '#include "bd.h"\n#include <stdio.h>\n'
+        "int main(void) {\n"
+        "  bd_kv_desc kv = {0};\n"
+        "  kv.head_dim = 64;\n"
+        "  bd_status st = bd_verify_attn(&kv, NULL, 32, 5, 0.1f, NULL, NULL, NULL, 0, NULL);\n"
+        '  printf("%d %d %s\\n", bd_abi_version(), (int)st, bd_last_error());\n'
+        "  return st == BD_ERR_UNSUPPORTED ? 0 : 1;\n"
+        "}\n")
+    exe = tmp_path / "abi"
+    libdir = os.path.dirname(bd.library_path)
+    libname = os.path.basename(bd.library_path)
+    r = subprocess.run([gcc, "-std=c11", "-Wall", "-Wextra", "-Werror", "-isystem", "/opt/rocm/include",
+                        "-D__HIP_PLATFORM_AMD__", f"-I{os.path.dirname(HEADER)}", str(src), f"-L{libdir}",
+                        f"-l:{libname}", f"-Wl,-rpath,{libdir}", "-o", str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    out = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0, (out.stdout, out.stderr)
+    version, status, reason = out.stdout.split(" ", 2)
+    assert int(version) == L.bd_abi_version() and int(status) == bd.BD_ERR_UNSUPPORTED
+    assert "head_dim 64" in reason
