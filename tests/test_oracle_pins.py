@@ -437,6 +437,27 @@ def test_decode_is_order_invariant_and_nsel_clamps():
     assert np.all(e == 0) and np.all(le == -np.inf)
 
 
+def test_decode_counts_a_repeated_entry_as_often_as_listed():
+    """The index list is a multiset (R12): doubling every entry scales every weight's numerator and
+    the normaliser alike (same output, log-sum-exp up by ln 2), and one key listed twice returns its
+    value row with log-sum-exp = its logit + ln 2."""
+    k, v = _kv(1, 2, 96, 17)
+    q = bits(np.random.default_rng(18).standard_normal((1, 8, 128)))
+    sel = np.random.default_rng(19).choice(96, 30, replace=False).astype(np.int32)
+    a, la = O.sparse_decode_attn(k, v, q, np.tile(sel, (1, 2, 1)), [30], [96])
+    b, lb = O.sparse_decode_attn(k, v, q, np.tile(np.r_[sel, sel[::-1]], (1, 2, 1)), [60], [96])
+    np.testing.assert_allclose(b, a, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(lb - la, math.log(2), rtol=1e-12)
+    two = np.full((1, 2, 2), 41, np.int32)
+    c, lc = O.sparse_decode_attn(k, v, q, two, [2], [96])
+    scale = float(np.float32(1 / math.sqrt(128)))
+    for h in range(8):
+        g = h // 4
+        np.testing.assert_allclose(c[0, h], O.bf16_to_f64(v[0, g, 41]), rtol=1e-14, atol=1e-15)
+        logit = scale * float(O.bf16_to_f64(q[0, h]) @ O.bf16_to_f64(k[0, g, 41]))
+        np.testing.assert_allclose(lc[0, h], logit + math.log(2), rtol=1e-12, atol=1e-12)
+
+
 def test_decode_matches_torch_sdpa():
     S, Hkv, G, L = 2, 2, 4, 96
     k, v = _kv(S, Hkv, L, 17)
