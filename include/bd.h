@@ -81,7 +81,7 @@ extern "C" {
 typedef int32_t bd_status;
 #define BD_OK 0
 #define BD_ERR_INVALID_ARG 1 /* a pointer, size or shape that the contract forbids */
-#define BD_ERR_UNSUPPORTED 2 /* a valid request this build does not implement (head_dim != 128,
+#define BD_ERR_UNSUPPORTED 2 /* a valid request the library does not implement (head_dim != 128,
                                launches of 2^22 or more workgroups, ...) */
 #define BD_ERR_WORKSPACE 3   /* workspace missing, too small or misaligned */
 #define BD_ERR_DEVICE 4      /* the HIP runtime rejected a launch */

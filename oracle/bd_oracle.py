@@ -7,9 +7,9 @@ arrays and are widened here, exactly, to float64.
 
 Every function states the passage of the paper it follows.  Where the paper
 is silent, the reading taken is stated in the docstring (the selection
-policy, window, pooling and tie rules come from the workload description of
-this build, not from the paper, which only names chunk-level selection by
-"cumulative attention weight" in Sec. 3.4).
+policy, window, pooling and tie rules come from the workload description the
+kernels are measured on, not from the paper, which only names chunk-level
+selection ranked by accumulated attention weight, in Sec. 3.4).
 
 Conventions (shared with the C ABI):
   * Query head h reads KV head g(h) = h // G, G = Hq / Hkv (contiguous groups).
@@ -78,13 +78,13 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, visible: np.ndarray, sca
 
 
 # --------------------------------------------------------------------------
-# Budgeted KV selection (Alg. 2 "sparsify"; Sec. 3.4 "cumulative attention weight")
+# Budgeted KV selection (Alg. 2 "sparsify"; Sec. 3.4: entries ranked by accumulated attention weight)
 # --------------------------------------------------------------------------
 
 def window_scores(k_g: np.ndarray, q_obs: np.ndarray, L: int, scale: float) -> np.ndarray:
     """Cumulative attention weight of every cached key under the observation rows.
 
-    Sec. 3.4 scores cache entries "by cumulative attention weight"; here the
+    Sec. 3.4 ranks cache entries by the attention weight they accumulate; here the
     weights are those of the W observation rows of every query head of the
     group (reading: probabilities, each row normalised over its own causal
     key range, summed over rows and heads).
