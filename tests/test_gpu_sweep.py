@@ -14,6 +14,7 @@ Decode and verify cases also draw:
   - a contiguous or paged cache.
 Acceptance cases draw the batch, gamma (0..15), vocabularies of 1..200K entries with padded rows,
 ties and entries at the most negative float.
+A last case runs verify and decode over one 131,072-row cache (the drafter model's context length).
 Outputs are preallocated and poisoned first (indices with a sentinel, floats with NaN), so an
 output the kernels never write fails.  Indices follow the two-part exact protocol of the selection
 tests; bf16 outputs are within 2e-2 + 1e-2 |oracle|, log-sum-exps within 1e-3.
@@ -225,3 +226,35 @@ def test_accept_random_shapes(seed):
     assert np.array_equal(gam.cpu().numpy(), ram), what
     assert np.array_equal(acc.cpu().numpy(), ra), what
     assert np.array_equal(bonus.cpu().numpy(), rb), what
+
+
+def test_long_context_verify_and_decode():
+    """One sequence with 131,072 cache rows (the drafter model's context length), GQA 32/8: verify at
+    gamma = 5 over the whole cache, and decode over 2,048 entries spread across it, against the
+    oracle; outputs poisoned first."""
+    g = np.random.default_rng(8000)
+    L, Hkv, G, gamma = 131072, 8, 4, 5
+    Hq = Hkv * G
+    k, v = _bits(g, (1, Hkv, L, 128)), _bits(g, (1, Hkv, L, 128))
+    q = _bits(g, (1, gamma + 1, Hq, 128))
+    idx = np.stack([np.sort(g.choice(L, 2048, replace=False)) for _ in range(Hkv)]).astype(np.int32)[None]
+    kd, vd = bf16_dev(k), bf16_dev(v)
+    what = f"long context L={L} Hkv={Hkv} G={G}"
+    case(what + " verify")
+    out = torch.full((1, gamma + 1, Hq, 128), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lse = torch.full((1, gamma + 1, Hq), float("nan"), dtype=torch.float32, device="cuda")
+    bd.bd_verify_attn(kd, vd, bf16_dev(q), i32_dev([L]), return_lse=True, out=out, lse=lse)
+    torch.cuda.synchronize()
+    ro, rl = O.verify_attn(k, v, q, [L], gamma)
+    assert_close(bf16_host64(out), ro, what + " verify")
+    assert_lse(lse.cpu().numpy().astype(np.float64), rl, what + " verify")
+    case(what + " decode")
+    out = torch.full((1, Hq, 128), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lse = torch.full((1, Hq), float("nan"), dtype=torch.float32, device="cuda")
+    qd = np.ascontiguousarray(q[:, -1])
+    bd.bd_sparse_decode_attn(kd, vd, bf16_dev(qd), i32_dev(idx), i32_dev([2048]), i32_dev([L]), return_lse=True,
+                             out=out, lse=lse)
+    torch.cuda.synchronize()
+    ro, rl = O.sparse_decode_attn(k, v, qd, idx, [2048], [L])
+    assert_close(bf16_host64(out), ro, what + " decode")
+    assert_lse(lse.cpu().numpy().astype(np.float64), rl, what + " decode")
