@@ -345,7 +345,11 @@ __device__ inline int fetch_args(const AttnParams& p) {
   return z2;
 }
 
-template <int NT, bool PAGED>
+// Records merged by one batch of loads; units with more splits merge in two levels (TWO_LEVEL, chosen
+// per launch when some unit has more than kMergeGroup splits; the one-level merge keeps its own code).
+constexpr int kMergeGroup = 8;
+
+template <int NT, bool PAGED, bool TWO_LEVEL>
 __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   using RB = RowBlock<NT>;
   __shared__ AttnSmem<NT> sm;
@@ -659,61 +663,156 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
       make_rsrc(rec_base + (int64_t)unit_local * nsplit * RB::kRec, (uint32_t)(nsplit * RB::kRec * 4));
   constexpr int kChunks = kPerThread / 4;
   constexpr uint32_t kOutOff = 16 * RB::kRows;
-  if (row_valid) {
-    const uint32_t rec = (uint32_t)split * RB::kRec * 4;
-    if (d0 == 0) store16_coherent(urec, rec + 16 * r, f32x4{M, Lsum, Lx, 0.f});
-#pragma unroll
-    for (int c = 0; c < kChunks; ++c)
-      store16_coherent(urec, rec + kOutOff + 16 * (c * kThreads + tid),
-                       f32x4{acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]});
-  }
-  wait_vmem();
-  __syncthreads();
-  if (tid == 0) sm.last = arrive(counter_line(p.counters, unit), (uint32_t)nsplit);
-  __syncthreads();
-  if (!sm.last) return;
-  if (tid == 0) reset_counter(counter_line(p.counters, unit));   // ready for the next call
-  if (!row_valid) return;
+  if constexpr (!TWO_LEVEL) {
+    if (row_valid) {
+      const uint32_t rec = (uint32_t)split * RB::kRec * 4;
+      if (d0 == 0) store16_coherent(urec, rec + 16 * r, f32x4{M, Lsum, Lx, 0.f});
+  #pragma unroll
+      for (int c = 0; c < kChunks; ++c)
+        store16_coherent(urec, rec + kOutOff + 16 * (c * kThreads + tid),
+                         f32x4{acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]});
+    }
+    wait_vmem();
+    __syncthreads();
+    if (tid == 0) sm.last = arrive(counter_line(p.counters, unit), (uint32_t)nsplit);
+    __syncthreads();
+    if (!sm.last) return;
+    if (tid == 0) reset_counter(counter_line(p.counters, unit));   // ready for the next call
+    if (!row_valid) return;
 
-  // merge the splits in split order with an online rescale, a batch of records at a time; every
-  // load of a batch is issued before any of its results is used
-  constexpr int kBatch = 8;
-  float Mg = -INFINITY, Lg = 0.f, Lxg = 0.f, ag[kPerThread];
-#pragma unroll
-  for (int e = 0; e < kPerThread; ++e) ag[e] = 0.f;
-  for (int sp0 = 0; sp0 < nsplit; sp0 += kBatch) {
-    f32x4 sv[kBatch], ov[kBatch][kChunks];
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const uint32_t rec = (uint32_t)(sp0 + u) * RB::kRec * 4;
-      const bool ok = sp0 + u < nsplit;
-      sv[u] = ok ? load16_coherent(urec, rec + 16 * r) : f32x4{-INFINITY, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int c = 0; c < kChunks; ++c)
-        ov[u][c] = ok ? load16_coherent(urec, rec + kOutOff + 16 * (c * kThreads + tid)) : f32x4{0.f, 0.f, 0.f, 0.f};
+    // merge the splits in split order with an online rescale, a batch of records at a time; every
+    // load of a batch is issued before any of its results is used
+    constexpr int kBatch = 8;
+    float Mg = -INFINITY, Lg = 0.f, Lxg = 0.f, ag[kPerThread];
+  #pragma unroll
+    for (int e = 0; e < kPerThread; ++e) ag[e] = 0.f;
+    for (int sp0 = 0; sp0 < nsplit; sp0 += kBatch) {
+      f32x4 sv[kBatch], ov[kBatch][kChunks];
+  #pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const uint32_t rec = (uint32_t)(sp0 + u) * RB::kRec * 4;
+        const bool ok = sp0 + u < nsplit;
+        sv[u] = ok ? load16_coherent(urec, rec + 16 * r) : f32x4{-INFINITY, 0.f, 0.f, 0.f};
+  #pragma unroll
+        for (int c = 0; c < kChunks; ++c)
+          ov[u][c] = ok ? load16_coherent(urec, rec + kOutOff + 16 * (c * kThreads + tid)) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+      float mb = Mg;
+  #pragma unroll
+      for (int u = 0; u < kBatch; ++u) mb = fmaxf(mb, sv[u][0]);
+      const float mbu = mb == -INFINITY ? 0.f : mb;
+      const float sc = exp2f(Mg - mbu);
+      Lg *= sc;
+      Lxg *= sc;
+  #pragma unroll
+      for (int e = 0; e < kPerThread; ++e) ag[e] *= sc;
+  #pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const float wt = exp2f(sv[u][0] - mbu);
+        Lg += wt * sv[u][1];
+        Lxg += wt * sv[u][2];
+  #pragma unroll
+        for (int c = 0; c < kChunks; ++c)
+  #pragma unroll
+          for (int i = 0; i < 4; ++i) ag[4 * c + i] += wt * ov[u][c][i];
+      }
+      Mg = mb;
     }
-    float mb = Mg;
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) mb = fmaxf(mb, sv[u][0]);
-    const float mbu = mb == -INFINITY ? 0.f : mb;
-    const float sc = exp2f(Mg - mbu);
-    Lg *= sc;
-    Lxg *= sc;
-#pragma unroll
-    for (int e = 0; e < kPerThread; ++e) ag[e] *= sc;
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const float wt = exp2f(sv[u][0] - mbu);
-      Lg += wt * sv[u][1];
-      Lxg += wt * sv[u][2];
-#pragma unroll
+    write_final(Mg, Lg, Lxg, ag);
+  } else {
+    auto store_record = [&](int slot, float Mr, float Lr, float Lxr, const float* a) {
+      if (!row_valid) return;
+      const uint32_t rec = (uint32_t)slot * RB::kRec * 4;
+      if (d0 == 0) store16_coherent(urec, rec + 16 * r, f32x4{Mr, Lr, Lxr, 0.f});
+  #pragma unroll
       for (int c = 0; c < kChunks; ++c)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) ag[4 * c + i] += wt * ov[u][c][i];
+        store16_coherent(urec, rec + kOutOff + 16 * (c * kThreads + tid),
+                         f32x4{a[4 * c], a[4 * c + 1], a[4 * c + 2], a[4 * c + 3]});
+    };
+    // Merge `count` records at slots first, first + stride, ... in that order with an online rescale,
+    // a batch of records at a time (every load of a batch issued before any of its results is used).
+    float Mg, Lg, Lxg, ag[kPerThread];
+    auto merge_records = [&](int first, int count, int stride) {
+      Mg = -INFINITY;
+      Lg = Lxg = 0.f;
+  #pragma unroll
+      for (int e = 0; e < kPerThread; ++e) ag[e] = 0.f;
+      if (!row_valid) return;
+      for (int sp0 = 0; sp0 < count; sp0 += kMergeGroup) {
+        f32x4 sv[kMergeGroup], ov[kMergeGroup][kChunks];
+  #pragma unroll
+        for (int u = 0; u < kMergeGroup; ++u) {
+          const uint32_t rec = (uint32_t)(first + (sp0 + u) * stride) * RB::kRec * 4;
+          const bool ok = sp0 + u < count;
+          sv[u] = ok ? load16_coherent(urec, rec + 16 * r) : f32x4{-INFINITY, 0.f, 0.f, 0.f};
+  #pragma unroll
+          for (int c = 0; c < kChunks; ++c)
+            ov[u][c] = ok ? load16_coherent(urec, rec + kOutOff + 16 * (c * kThreads + tid))
+                          : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        float mb = Mg;
+  #pragma unroll
+        for (int u = 0; u < kMergeGroup; ++u) mb = fmaxf(mb, sv[u][0]);
+        const float mbu = mb == -INFINITY ? 0.f : mb;
+        const float sc = exp2f(Mg - mbu);
+        Lg *= sc;
+        Lxg *= sc;
+  #pragma unroll
+        for (int e = 0; e < kPerThread; ++e) ag[e] *= sc;
+  #pragma unroll
+        for (int u = 0; u < kMergeGroup; ++u) {
+          const float wt = exp2f(sv[u][0] - mbu);
+          Lg += wt * sv[u][1];
+          Lxg += wt * sv[u][2];
+  #pragma unroll
+          for (int c = 0; c < kChunks; ++c)
+  #pragma unroll
+            for (int i = 0; i < 4; ++i) ag[4 * c + i] += wt * ov[u][c][i];
+        }
+        Mg = mb;
+      }
+    };
+
+    // A unit of at most kMergeGroup splits is merged by its last split.  A larger one merges in two
+    // levels, each one batch of loads: the last split of each group of kMergeGroup consecutive splits
+    // merges the group into the group's first slot, and the last group merges the groups in order.
+    store_record(split, M, Lsum, Lx, acc);
+    const bool two_level = nsplit > kMergeGroup;
+    const int grp = split / kMergeGroup;
+    const int ngroups = (nsplit + kMergeGroup - 1) / kMergeGroup;
+    const int g_first = two_level ? grp * kMergeGroup : 0;
+    const int g_count = two_level ? (nsplit - g_first < kMergeGroup ? nsplit - g_first : kMergeGroup) : nsplit;
+    wait_vmem();
+    __syncthreads();
+    if (tid == 0) {
+      uint32_t* c = two_level ? counter_line(p.counters, p.units_all + (int64_t)unit * p.ngrp + grp)
+                              : counter_line(p.counters, unit);
+      const bool last = arrive(c, (uint32_t)g_count);
+      if (last) reset_counter(c);                      // ready for the next call
+      sm.last = last;
     }
-    Mg = mb;
+    __syncthreads();
+    if (!sm.last) return;
+    merge_records(g_first, g_count, 1);
+    if (!two_level) {
+      write_final(Mg, Lg, Lxg, ag);
+      return;
+    }
+    __syncthreads();   // every row's loads of the group's first slot are done before it is rewritten
+    store_record(g_first, Mg, Lg, Lxg, ag);
+    wait_vmem();
+    __syncthreads();
+    if (tid == 0) {
+      uint32_t* c = counter_line(p.counters, unit);
+      const bool last = arrive(c, (uint32_t)ngroups);
+      if (last) reset_counter(c);
+      sm.last = last;
+    }
+    __syncthreads();
+    if (!sm.last) return;
+    merge_records(0, ngroups, kMergeGroup);
+    write_final(Mg, Lg, Lxg, ag);
   }
-  write_final(Mg, Lg, Lxg, ag);
 }
 
 // ---- block mode: many query rows per (sequence, KV head) ---------------------
@@ -1553,6 +1652,10 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
   pl.nsplit_f = max_L > 0 ? (int)((max_L + kf - 1) / kf) : 1;
   blocks = (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f;
   pl.nblk = blocks > INT32_MAX ? -1 : (int)blocks;
+  // group counters per unit for the two-level merge (units of more than kMergeGroup splits)
+  auto groups = [](int n) { return n > kMergeGroup ? (n + kMergeGroup - 1) / kMergeGroup : 0; };
+  const int gg = pl.units_g ? groups(pl.nsplit_g) : 0, gf = pl.units_f ? groups(pl.nsplit_f) : 0;
+  pl.ngrp = gg > gf ? gg : gf;
   const bool split = (pl.units_g && pl.nsplit_g > 1) || (pl.units_f && pl.nsplit_f > 1);
   pl.record_bytes = split ? align256(sizeof(float) * attn_record_floats(pl.nt) * (size_t)blocks) : 0;
   pl.ws_bytes = pl.counter_bytes + pl.record_bytes;
@@ -1560,8 +1663,9 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
 }
 
 template <int NT, bool PAGED>
-static hipError_t launch_nt(const AttnParams& p, int nblocks, hipStream_t stream) {
-  hipLaunchKernelGGL((attn_kernel<NT, PAGED>), dim3(nblocks), dim3(kThreads), 0, stream, p);
+static hipError_t launch_nt(const AttnParams& p, int nblocks, bool two_level, hipStream_t stream) {
+  if (two_level) hipLaunchKernelGGL((attn_kernel<NT, PAGED, true>), dim3(nblocks), dim3(kThreads), 0, stream, p);
+  else hipLaunchKernelGGL((attn_kernel<NT, PAGED, false>), dim3(nblocks), dim3(kThreads), 0, stream, p);
   return hipGetLastError();
 }
 
@@ -1586,8 +1690,10 @@ hipError_t launch_attn(const AttnParams& args, const AttnPlan& pl, bool paged, h
     }
     return hipGetLastError();
   }
-  if (pl.nt == 1) return paged ? launch_nt<1, true>(p, pl.nblk, stream) : launch_nt<1, false>(p, pl.nblk, stream);
-  return paged ? launch_nt<2, true>(p, pl.nblk, stream) : launch_nt<2, false>(p, pl.nblk, stream);
+  const bool two = pl.ngrp > 0;
+  if (pl.nt == 1)
+    return paged ? launch_nt<1, true>(p, pl.nblk, two, stream) : launch_nt<1, false>(p, pl.nblk, two, stream);
+  return paged ? launch_nt<2, true>(p, pl.nblk, two, stream) : launch_nt<2, false>(p, pl.nblk, two, stream);
 }
 
 size_t attn_ws_bytes(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full,

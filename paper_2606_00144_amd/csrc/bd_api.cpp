@@ -145,8 +145,11 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
     return fail(BD_ERR_UNSUPPORTED, "problem too large for one launch");
   if (kv_extent(kv) > ((int64_t)1 << 34))
     return fail(BD_ERR_UNSUPPORTED, "K/V layout spans more than 2^34 elements");
-  if ((pl.block ? (int64_t)pl.units * pl.nbr : (int64_t)pl.units_g + pl.units_f) > BD_WS_COUNTER_LINES)
-    return fail(BD_ERR_UNSUPPORTED, "more than %d work units", BD_WS_COUNTER_LINES);
+  // counter lines: one per unit (block mode: per unit and branch), and the split kernel's group
+  // counters of the two-level merge
+  const int64_t lines = pl.block ? (int64_t)pl.units * pl.nbr
+                                 : ((int64_t)pl.units_g + pl.units_f) * (1 + (int64_t)pl.ngrp);
+  if (lines > BD_WS_COUNTER_LINES) return fail(BD_ERR_UNSUPPORTED, "more than %d work units", BD_WS_COUNTER_LINES);
   if (pl.block && (int64_t)(pl.nW + pl.nbr) * 8 * bd::attn_record_floats(2) * 4 > INT32_MAX)
     return fail(BD_ERR_UNSUPPORTED, "too many partial records per unit");
   bd_status st = BD_OK;
@@ -189,6 +192,8 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
   p.nsplit_f = pl.nsplit_f;
   p.kps_f = pl.kps_f;
   p.units_g = pl.units_g;
+  p.units_all = pl.units_g + pl.units_f;
+  p.ngrp = pl.ngrp;
   p.nblk_g = pl.units_g * pl.nsplit_g;
   p.V = num_views;
   p.nbr = pl.nbr;

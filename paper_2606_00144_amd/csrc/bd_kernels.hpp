@@ -34,6 +34,8 @@ struct AttnParams {
   int32_t nsplit_g, kps_g;  // gathered units: splits and entries per split
   int32_t nsplit_f, kps_f;  // full units: splits and keys per split
   int32_t units_g;          // gathered units (their blocks come first)
+  int32_t units_all;        // gathered and full units: counter lines 0 .. units_all-1
+  int32_t ngrp;             // two-level merge: group counter lines per unit (0 when no unit needs them)
   int32_t nblk_g;           // blocks of gathered units
   int32_t V, nbr;           // block mode: views, and branches (views + full)
   int32_t nW;               // block mode: workgroups per (s, g, row group), equal shares of its key stream
@@ -50,6 +52,7 @@ struct AttnPlan {
   int n_rg;
   int nsplit_g, kps_g, nsplit_f, kps_f;
   int units_g, units_f, nblk;
+  int ngrp;                 // group counters per unit of the two-level split merge (0: none)
   int units, nbr, nW;       // block mode: (s, g, row group) units, branches, workgroups per unit
   size_t counter_bytes, record_bytes, ws_bytes;
 };
