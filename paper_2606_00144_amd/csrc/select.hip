@@ -225,12 +225,8 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
 
   float* raw_part = p.raw_part + ((int64_t)pair * p.n_rb + rb) * p.max_L;
 
-  // 16 keys x 16*NT rows of one sub-tile; keys tb .. tb+3 belong to this lane.  `dirty` is a
-  // compile-time flag: a runtime one was if-converted, and every tile paid the mask (a compare, a
-  // select and a mask merge per score: a third of the loop's VALU instructions).
-  auto sub_step = [&](const u32x4 (&kr)[4], int tb, auto dirty_tag) {
-    constexpr bool dirty = decltype(dirty_tag)::value;
-    f32x4 acc[NT];
+  // Scores of one 16-key sub-tile against the 16*NT rows; keys tb .. tb+3 belong to this lane.
+  auto sub_products = [&](f32x4 (&acc)[NT], const u32x4 (&kr)[4]) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       f32x4 a = {0.f, 0.f, 0.f, 0.f};
@@ -238,54 +234,89 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
       for (int j = 0; j < 4; ++j) a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[j]), qop[nt][j], a, 0, 0, 0);
       acc[nt] = a;
     }
-    if constexpr (dirty) {
+  };
+  // Causal and split mask of a sub-tile.  Only tiles that can hold a masked key call it: a mask
+  // behind a runtime flag was if-converted, and every tile paid it (a compare, a select and a mask
+  // merge per score: a third of the loop's VALU instructions).
+  auto sub_mask = [&](f32x4 (&acc)[NT], int tb) {
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int t = tb + i;
-          if (!(t < k1 && t <= rowpos[nt])) acc[nt][i] = -INFINITY;
-        }
+      for (int i = 0; i < 4; ++i) {
+        const int t = tb + i;
+        if (!(t < k1 && t <= rowpos[nt])) acc[nt][i] = -INFINITY;
+      }
+  };
+
+  // Pass 1 over a 32-key tile: per-lane running sums with a lazily raised reference, so weights stay
+  // <= 2^kSlack.  Both sub-tiles' products come first and one check covers the tile: it compares raw
+  // logits with a per-row threshold, and the raise is a wave-uniform branch (the common tile pays
+  // max and compare instructions, no extra exponential).  One branch per tile instead of one per
+  // sub-tile leaves the scheduler one block of 64 products to interleave with the exponentials.
+  auto pass1_tile = [&](const u32x4 (&kt)[2][4], int tb, auto dirty_tag) {
+    f32x4 acc[2][NT];
+    sub_products(acc[0], kt[0]);
+    sub_products(acc[1], kt[1]);
+    if constexpr (decltype(dirty_tag)::value) {
+      sub_mask(acc[0], tb);
+      sub_mask(acc[1], tb + 16);
     }
-    if constexpr (PASS == 1) {
-      // per-lane running sum with a lazily raised reference: weights stay <= 2^kSlack.  The check
-      // compares raw logits with a per-row threshold, and the raise is a wave-uniform branch (the
-      // common tile pays two max and one compare per row tile, no exponential)
-      float mx[NT];
-      bool raise = false;
+    float mx[NT];
+    bool raise = false;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      mx[nt] = fmaxf(fmaxf(fmaxf(acc[0][nt][0], acc[0][nt][1]), fmaxf(acc[0][nt][2], acc[0][nt][3])),
+                     fmaxf(fmaxf(acc[1][nt][0], acc[1][nt][1]), fmaxf(acc[1][nt][2], acc[1][nt][3])));
+      raise |= mx[nt] > rthr[nt];
+    }
+    if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        mx[nt] = fmaxf(fmaxf(acc[nt][0], acc[nt][1]), fmaxf(acc[nt][2], acc[nt][3]));
-        raise |= mx[nt] > rthr[nt];
-      }
-      if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          if (mx[nt] > rthr[nt]) {
-            const float m2 = mx[nt] * p.scale_log2;    // scale > 0: the max commutes with it
-            rl[nt] = rl[nt] > 0.f ? rl[nt] * exp2f(rm[nt] - m2) : 0.f;
-            rm[nt] = m2;
-            rthr[nt] = (m2 + kSlack) / p.scale_log2;
-          }
+        if (mx[nt] > rthr[nt]) {
+          const float m2 = mx[nt] * p.scale_log2;    // scale > 0: the max commutes with it
+          rl[nt] = rl[nt] > 0.f ? rl[nt] * exp2f(rm[nt] - m2) : 0.f;
+          rm[nt] = m2;
+          rthr[nt] = (m2 + kSlack) / p.scale_log2;
         }
       }
+    }
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) rl[nt] += __builtin_amdgcn_exp2f(fmaf(acc[nt][i], p.scale_log2, -rm[nt]));
+        for (int i = 0; i < 4; ++i) rl[nt] += __builtin_amdgcn_exp2f(fmaf(acc[sub][nt][i], p.scale_log2, -rm[nt]));
+  };
+
+  // Pass 2 over a 16-key sub-tile: each key's column sum of the rows' normalised weights.  After the
+  // 16-lane reduction every lane of a row holds the same four sums (each step adds a lane pair in
+  // both orders), so in a mask-free tile all 64 lanes store, four lanes per key with equal bits,
+  // and no branch splits the loop body: the next sub-tile's products can overlap this one's sums.
+  auto pass2_sub = [&](const u32x4 (&kr)[4], int tb, auto dirty_tag) {
+    constexpr bool dirty = decltype(dirty_tag)::value;
+    f32x4 acc[NT];
+    sub_products(acc, kr);
+    if constexpr (dirty) sub_mask(acc, tb);
+    float col[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) col[i] = __builtin_amdgcn_exp2f(fmaf(acc[0][i], p.scale_log2, -lse2[0]));
+#pragma unroll
+    for (int nt = 1; nt < NT; ++nt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) col[i] += __builtin_amdgcn_exp2f(fmaf(acc[nt][i], p.scale_log2, -lse2[nt]));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) col[i] = sum16(col[i]);
+    // opaque to the compiler, which would otherwise finish the reduction only for the column a lane
+    // stores, behind branches on the lane index
+    asm("" : "+v"(col[0]), "+v"(col[1]), "+v"(col[2]), "+v"(col[3]));
+    const int q = lr & 3;
+    const float v01 = (q & 1) ? col[1] : col[0], v23 = (q & 1) ? col[3] : col[2];
+    const float v = (q & 2) ? v23 : v01;
+    const int t = tb + q;
+    if constexpr (dirty) {
+      if (lr < 4 && t < k1) raw_part[t] = v;
     } else {
-      float col[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) col[i] += __builtin_amdgcn_exp2f(fmaf(acc[nt][i], p.scale_log2, -lse2[nt]));
-#pragma unroll
-      for (int i = 0; i < 4; ++i) col[i] = sum16(col[i]);
-      if (lr < 4) {
-        const float v = lr == 0 ? col[0] : lr == 1 ? col[1] : lr == 2 ? col[2] : col[3];
-        const int t = tb + lr;
-        if (t < k1) raw_part[t] = v;
-      }
+      raw_part[t] = v;                     // a mask-free tile lies inside the split: t < k1
     }
   };
 
@@ -324,8 +355,12 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
       read_ktile(kt, ring_lds + slot * kTileBytes, lane);
       issue(it + kRing * kWaves, slot);
       const int tb = k0 + kTile * real(it) + 4 * lg;
-      sub_step(kt[0], tb, dirty_tag);
-      sub_step(kt[1], tb + 16, dirty_tag);
+      if constexpr (PASS == 1) {
+        pass1_tile(kt, tb, dirty_tag);
+      } else {
+        pass2_sub(kt[0], tb, dirty_tag);
+        pass2_sub(kt[1], tb + 16, dirty_tag);
+      }
       ++j;
       return it + kWaves >= ntiles;
     };
