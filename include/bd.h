@@ -93,7 +93,12 @@ typedef int32_t bd_status;
  * Paged layout (page_table != NULL): element (s, g, t, d) lives at
  *   page_table[s*max_pages_per_seq + t/page_size]*stride_page
  *     + g*stride_head + (t % page_size)*stride_tok + d.
- * In both layouts d is contiguous.  K and V share the layout. */
+ * In both layouts d is contiguous.  K and V share the layout.  Page numbers
+ * belong in [0, num_pages): no value makes a kernel read outside the pool,
+ * and the attention calls treat the keys of a page numbered outside it as
+ * absent (they take no weight).  A page_size that is a multiple of 16 lets
+ * the verifier's full-cache pass read through one table entry per page,
+ * which allows far longer splits per workgroup than other page sizes. */
 typedef struct bd_kv_desc {
   const uint16_t* k;          /* bf16 keys */
   const uint16_t* v;          /* bf16 values (ignored, may be NULL, for bd_select_kv) */

@@ -331,6 +331,7 @@ __device__ inline void tile_step(RowState<NT>& st, const TileRegs<NT, PAGED>& T,
 // the first data load and again before the merge.  Naming them all at entry has every line
 // requested at once, so the arguments cost one round trip.  The statements touch no memory (so the
 // uniform loads after them stay scalar) and return 0, which the caller adds to its block index.
+template <bool PAGED>
 __device__ inline int fetch_args(const AttnParams& p) {
   int z0, z1, z2;
   asm("s_mov_b32 %0, 0" : "=s"(z0) : "s"(p.kv.k), "s"(p.kv.v), "s"(p.kv.seq_lens), "s"(p.kv.page_table),
@@ -342,6 +343,7 @@ __device__ inline int fetch_args(const AttnParams& p) {
   asm("s_mov_b32 %0, 0" : "=s"(z2) : "s"(z1), "s"(p.nsplit_g), "s"(p.kps_g), "s"(p.nsplit_f), "s"(p.kps_f),
       "s"(p.units_g), "s"(p.nblk_g), "s"(p.nblk), "s"(p.scale_log2), "s"(p.max_roff), "s"(p.part),
       "s"(p.counters));
+  if constexpr (PAGED) asm("s_mov_b32 %0, 0" : "=s"(z2) : "s"(z2), "s"(p.page_arith));
   return z2;
 }
 
@@ -358,7 +360,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   const int lg = lane >> 4, lr = lane & 15;
 
   // ---- which (kind, unit, split) this workgroup owns
-  const int bid = xcd_remap(blockIdx.x + fetch_args(p), p.nblk);
+  const int bid = xcd_remap(blockIdx.x + fetch_args<PAGED>(p), p.nblk);
   const bool gather = bid < p.nblk_g;
   const int local = gather ? bid : bid - p.nblk_g;
   const int nsplit = gather ? p.nsplit_g : p.nsplit_f;
@@ -394,14 +396,34 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) qop[nt][kk] = as_bf16x8(valid ? load16(qrow + 8 * kk) : u32x4{0u, 0u, 0u, 0u});
   }
-  // the causal prefix of a contiguous cache needs no slot table: row offsets are computed
+  // the causal prefix of a contiguous cache needs no slot table: row offsets are computed.  So are
+  // they for the prefix of a paged cache whose pages hold whole 16-key sub-tiles (page_size a
+  // multiple of 16, checked on the host), from a table of page offsets: one entry per page, so the
+  // split is bounded by kSlotCap pages rather than kSlotCap keys
   const bool arith = !PAGED && !gather;
-  const int e_begin = split * kps;
+  const bool page_arith = PAGED && !gather && p.page_arith != 0;
+  const int e_begin = split * kps;       // a multiple of kWaves * kTile
   // slot-table entries: the idx loads do not wait for the entry count (every entry of the split
   // below ld_idx lies in the list's row; those past the count are dropped once it has arrived)
   constexpr int kPer = (kSlotCap + kThreads - 1) / kThreads;
   int tv[kPer];
-  if (!arith) {
+  // page table: the entries of every page the split can touch below max_seq_len (the length is not
+  // waited for; pages past it are dropped once it has arrived).  key / page_size is computed as
+  // (key / 16) / (page_size / 16), exact for keys below 2^26 (host-checked)
+  const int psub = PAGED ? p.kv.page_size >> 4 : 1;
+  const float inv_psub = __builtin_amdgcn_rcpf((float)psub);
+  const int page0 = page_arith ? div_small(e_begin >> 4, psub, inv_psub) : 0;
+  int npg_ld = 0;
+  if (page_arith) {
+    const int kend = e_begin + kps < p.kv.max_seq_len ? e_begin + kps : p.kv.max_seq_len;
+    npg_ld = kend > e_begin ? div_small((kend - 1) >> 4, psub, inv_psub) - page0 + 1 : 0;
+    const int32_t* prow = p.kv.page_table + (int64_t)s * p.kv.max_pages_per_seq + page0;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int j = tid + k * kThreads;
+      tv[k] = j < npg_ld ? prow[j] : -1;
+    }
+  } else if (!arith) {
     const int e_lim = gather ? (e_begin + kps < p.ld_idx ? e_begin + kps : p.ld_idx) : e_begin + kps;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
@@ -424,7 +446,24 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   // a tile needs the visibility mask when one of its slots is absent or lies after the earliest
   // row position of this row block; the first such tile bounds the mask-free ones
   const int minpos = L - p.nq + div_small(rb * RB::kRows, p.G);
-  if (!arith) {
+  bool page_bad = false;                 // a page the split needs is outside the pool: its keys are absent
+  if (page_arith) {
+    // page offsets in 16-byte units of head g; -1 marks an entry outside the pool (offsets stay below
+    // max_roff < 2^31, host-checked)
+    const int npg = e_end > e_begin ? div_small((e_end - 1) >> 4, psub, inv_psub) - page0 + 1 : 0;
+    int bad = 0;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int j = tid + k * kThreads;
+      if (j < npg_ld) {
+        const bool ok = (unsigned)tv[k] < (unsigned)p.kv.num_pages;
+        sm.u.slots.roff[j] =
+            ok ? (int)(((int64_t)tv[k] * p.kv.stride_page + (int64_t)g * p.kv.stride_head) >> 3) : -1;
+        bad |= (j < npg && !ok) ? 1 : 0;
+      }
+    }
+    page_bad = __syncthreads_or(bad) != 0;
+  } else if (!arith) {
     // entries past the split's end or outside [0, L) become padding; all page-table loads are
     // issued before any result is used
 #pragma unroll
@@ -477,12 +516,13 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
     __syncthreads();
   }
   int first_dirty;
-  if (arith) {
+  if (arith || page_arith) {
     // tile t is clean when its keys all lie inside the split and at or before minpos
     const int c1 = minpos - e_begin - (kTile - 1);
     const int fd1 = c1 < 0 ? 0 : c1 / kTile + 1;
     const int fd2 = (e_end - e_begin) / kTile;
     first_dirty = fd1 < fd2 ? fd1 : fd2;
+    if (page_bad) first_dirty = 0;
   } else {
     first_dirty = sm.first_dirty[0];
 #pragma unroll
@@ -555,6 +595,78 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
         dma_tile(p.kv, A, p.max_roff, slot_b, lane, !gather);
         tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it + kWaves >= first_dirty, want_lx,
                              pos_at(kTile * (it + kWaves)), pass_v(T));
+        if (it + 2 * kWaves >= ntiles) break;
+      }
+    } else if (page_arith) {
+      // row offset of key t = offset of its page (LDS table) + (t % page_size) * stride_tok.  A tile
+      // starts at a multiple of 32 keys, so each 16-key sub-tile lies in one page; vb bit h records
+      // whether sub-tile h's page is in the pool (absent keys are masked by their positions)
+      const uint32_t roff_lds = lds_addr(sm.u.slots.roff);
+      const uint32_t tok16 = (uint32_t)(p.kv.stride_tok >> 3);
+      const int P = p.kv.page_size;
+      const uint32_t off_k = (uint32_t)lr, off_v = (uint32_t)(4 * lg);
+      auto rows_at = [&](int slot0, uint32_t& vb) {
+        vb = 0u;
+        if (slot0 >= ntiles * kTile) {   // a padding tile past this wave's last: row 0, a cache-resident address
+          A.k[0] = A.k[1] = 0u;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) A.v[h] = u32x4{0u, 0u, 0u, 0u};
+          return;
+        }
+        uint32_t a[2], w[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int t = e_begin + slot0 + 16 * h;
+          const int pi = div_small(t >> 4, psub, inv_psub);
+          // a sub-tile wholly past the split reads entry 0 (always loaded) and is masked anyway
+          const int j = t < e_end ? pi - page0 : 0;
+          a[h] = roff_lds + 4 * (uint32_t)j;
+          w[h] = (uint32_t)(t - pi * P);
+        }
+        uint32_t b[2];
+        asm volatile(
+            "ds_read_b32 %0, %2\n"
+            "ds_read_b32 %1, %3\n"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(b[0]), "=&v"(b[1])
+            : "v"(a[0]), "v"(a[1]));
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const bool ok = b[h] != 0xFFFFFFFFu;
+          vb |= ok ? (1u << h) : 0u;
+          const uint32_t base = ok ? b[h] : 0u;
+          A.k[h] = base + (w[h] + off_k) * tok16;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) A.v[h][i] = base + (w[h] + off_v + (uint32_t)i) * tok16;
+        }
+      };
+      auto pos_at = [&](int slot0, uint32_t vb) {
+        return [=](int i) {
+          const int e = e_begin + slot0 + 16 * (i >> 2) + 4 * lg + (i & 3);
+          return (e < e_end && ((vb >> (i >> 2)) & 1u)) ? e : -1;
+        };
+      };
+      uint32_t vb_a, vb_b;
+      rows_at(kTile * wave, vb_a);
+      dma_tile(p.kv, A, p.max_roff, slot_a, lane, true);
+      rows_at(kTile * (wave + kWaves), vb_b);
+      dma_tile(p.kv, A, p.max_roff, slot_b, lane, true);
+      for (int it = wave;; it += 2 * kWaves) {
+        asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+        read_tile<NT, PAGED>(T, slot_a_lds, lane);
+        const uint32_t vb_now = vb_a;
+        rows_at(kTile * (it + 2 * kWaves), vb_a);
+        dma_tile(p.kv, A, p.max_roff, slot_a, lane, true);
+        tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it >= first_dirty, want_lx, pos_at(kTile * it, vb_now),
+                             pass_v(T));
+        if (it + kWaves >= ntiles) break;
+        asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+        read_tile<NT, PAGED>(T, slot_b_lds, lane);
+        const uint32_t vb_next = vb_b;
+        rows_at(kTile * (it + 3 * kWaves), vb_b);
+        dma_tile(p.kv, A, p.max_roff, slot_b, lane, true);
+        tile_step<NT, PAGED>(st, T, qop, rowpos, p.scale_log2, it + kWaves >= first_dirty, want_lx,
+                             pos_at(kTile * (it + kWaves), vb_next), pass_v(T));
         if (it + 2 * kWaves >= ntiles) break;
       }
     } else {
@@ -1141,7 +1253,7 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
   const int lg = lane >> 4, lr = lane & 15;
 
   // ---- unit (sequence, KV head, row group) and this workgroup's share w of the unit's key stream
-  const int bid = xcd_remap(blockIdx.x + fetch_args(p), gridDim.x);   // kernel arguments in one round trip
+  const int bid = xcd_remap(blockIdx.x + fetch_args<false>(p), gridDim.x);   // kernel arguments in one round trip
   const int w = bid % p.nW;
   const int unit = bid / p.nW;
   const int rg = unit % p.n_rg;
@@ -1581,7 +1693,7 @@ __global__ __launch_bounds__(kWave) void block_merge_kernel(AttnParams p) {
 static int sat_count(int64_t x) { return x > (int64_t(1) << 30) ? (1 << 30) : (int)x; }
 
 AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full, bool paged,
-                   bool train) {
+                   bool train, int page_size) {
   AttnPlan pl{};
   const int G = Hq / Hkv;
   pl.R = sat_count((int64_t)nq * G);
@@ -1636,12 +1748,17 @@ AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, in
     const int64_t all = g_all > f_all ? g_all : f_all;
     if (kps < all) kps = all;
   }
+  // the paged full branch: its table holds kSlotCap entries, one per key, or one per page when pages
+  // hold whole 16-key sub-tiles (a split of kf keys spans at most kf / page_size + 2 pages); key
+  // indices below 2^26 keep the kernel's page division in its exact range
+  pl.page_arith = paged && page_size > 0 && page_size % 16 == 0 && max_L <= (1 << 26) - 64;
+  const int64_t kf_cap = pl.page_arith ? ((int64_t)(kSlotCap - 2) * page_size) / kStep * kStep : kMaxSplitKeys;
   int64_t kg, kf, blocks;
   for (;;) {
     kg = kps < g_all ? kps : g_all;
     if (kg > kMaxSplitKeys) kg = kMaxSplitKeys;
     kf = kps < f_all ? kps : f_all;
-    if (paged && kf > kMaxSplitKeys) kf = kMaxSplitKeys;
+    if (paged && kf > kf_cap) kf = kf_cap;
     blocks = (int64_t)pl.units_g * ((g_all + kg - 1) / kg) + (int64_t)pl.units_f * ((f_all + kf - 1) / kf);
     if (blocks <= kTargetBlocks || (kps >= g_all && kps >= f_all)) break;
     kps += kStep;

@@ -139,7 +139,7 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
   const bool train = o32_views || o32_full;
   const bd::AttnPlan pl =
       bd::plan_attn(kv->num_seqs, kv->num_kv_heads, Hq, nq, num_views, ld_idx, kv->max_seq_len, out_full != nullptr,
-                    kv->page_table != nullptr, train);
+                    kv->page_table != nullptr, train, kv->page_table ? kv->page_size : 0);
   if (pl.block && pl.nbr > 64) return fail(BD_ERR_UNSUPPORTED, "more than 63 views with a block of more than 32 rows");
   if (pl.nblk < 0 || (!pl.block && (int64_t)pl.units_g * pl.nsplit_g + (int64_t)pl.units_f * pl.nsplit_f > INT32_MAX))
     return fail(BD_ERR_UNSUPPORTED, "problem too large for one launch");
@@ -195,6 +195,7 @@ bd_status run_attn(const bd_kv_desc* kv, const uint16_t* q, int32_t Hq, int32_t 
   p.units_all = pl.units_g + pl.units_f;
   p.ngrp = pl.ngrp;
   p.nblk_g = pl.units_g * pl.nsplit_g;
+  p.page_arith = pl.page_arith ? 1 : 0;
   p.V = num_views;
   p.nbr = pl.nbr;
   p.nW = pl.nW;

@@ -44,6 +44,7 @@ struct AttnParams {
   uint32_t max_roff;        // largest valid row offset of the K/V layout, 16-byte units
   float* part;              // partial records
   uint32_t* counters;       // one per unit
+  int32_t page_arith;       // 1: the full branch of the paged cache reads its rows through a table of page offsets
 };
 
 struct AttnPlan {
@@ -53,15 +54,18 @@ struct AttnPlan {
   int nsplit_g, kps_g, nsplit_f, kps_f;
   int units_g, units_f, nblk;
   int ngrp;                 // group counters per unit of the two-level split merge (0: none)
+  bool page_arith;          // paged full branch through the table of page offsets (pages of 16k rows)
   int units, nbr, nW;       // block mode: (s, g, row group) units, branches, workgroups per unit
   size_t counter_bytes, record_bytes, ws_bytes;
 };
 
-// `paged`: the cache is paged (the full branch then also goes through the slot table, which
-// bounds its splits).  `train`: fp32 outputs are requested (block mode with two-term weights).
-// Workspace queries that do not know the layout take the largest of the plans (attn_ws_bytes).
+// `paged`: the cache is paged.  Its full branch goes through a table that bounds the splits: one
+// entry per key, or with `page_size` a multiple of 16 (pages hold whole 16-key sub-tiles) one entry
+// per page, which bounds them far less.  `train`: fp32 outputs are requested (block mode with
+// two-term weights).  Workspace queries that do not know the layout take the largest of the plans
+// (attn_ws_bytes: the per-key table's plan, which never needs less scratch than the per-page one).
 AttnPlan plan_attn(int S, int Hkv, int Hq, int nq, int num_views, int ld_idx, int max_L, bool with_full, bool paged,
-                   bool train = false);
+                   bool train = false, int page_size = 0);
 hipError_t launch_attn(const AttnParams& p, const AttnPlan& pl, bool paged, hipStream_t stream);
 size_t attn_record_floats(int nt);
 // Workspace bytes that serve either layout (paged or contiguous) of the given shape, and with

@@ -87,9 +87,10 @@ def test_verify_noalloc_rejections(L):
     assert na(_kv(), g=-1) == bd.BD_ERR_INVALID_ARG
     assert na(_kv(), out=FAKE + 2) == bd.BD_ERR_INVALID_ARG
     assert na(_kv(head_dim=64)) == bd.BD_ERR_UNSUPPORTED
-    # 64 sequences x 32 KV heads paged up to 16384 rows: the plan's records exceed the fixed scratch
-    big = _kv(num_seqs=64, num_kv_heads=32, max_seq_len=16384, page_table=FAKE, page_size=16,
-              max_pages_per_seq=1024, num_pages=65536, stride_page=32 * 16 * 128, stride_head=16 * 128)
+    # 64 sequences x 32 KV heads paged up to 16384 rows in pages of 8 (the per-key table bounds the
+    # splits to 2,048 keys): the plan's records exceed the fixed scratch
+    big = _kv(num_seqs=64, num_kv_heads=32, max_seq_len=16384, page_table=FAKE, page_size=8,
+              max_pages_per_seq=2048, num_pages=131072, stride_page=32 * 8 * 128, stride_head=8 * 128)
     assert na(big) == bd.BD_ERR_UNSUPPORTED
     assert b"scratch" in L.bd_last_error()
 

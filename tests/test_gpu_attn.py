@@ -186,6 +186,73 @@ def test_verify_paged_ragged_mha():
                   kdev=kd, vdev=vd, page_table=i32_dev(table))
 
 
+def _paged_pool(k, v, lens, ps, seed):
+    """Scatter [S][Hkv][Lmax][D] caches into a pool of ps-row pages under a seeded page order."""
+    g = np.random.default_rng(seed)
+    npg = [(int(L) + ps - 1) // ps for L in lens]
+    perm = g.permutation(sum(npg)).astype(np.int32)
+    table = np.full((len(lens), max(npg)), -1, np.int32)
+    o = 0
+    for s, n in enumerate(npg):
+        table[s, :n] = perm[o:o + n]
+        o += n
+    ks = [k[s][:, :int(L)] for s, L in enumerate(lens)]
+    vs = [v[s][:, :int(L)] for s, L in enumerate(lens)]
+    kd, vd = paged_kv(ks, vs, table, int(sum(npg)), ps)
+    return kd, vd, table
+
+
+@pytest.mark.parametrize("ps", [8, 16, 48, 64])
+def test_verify_paged_page_sizes(ps):
+    """Pages that hold whole 16-key sub-tiles (16, 48, 64) read the full cache through a table of page
+    offsets; other sizes (8) through the per-key table.  At 48 rows the pages straddle the splits'
+    starts, and the 9,000-row sequence takes more than 8 splits per unit (the two-level merge)."""
+    S, Hkv, G, gamma = 3, 2, 4, 5
+    lens = [9000, 2049, 777]
+    k = _rand_bits((S, Hkv, max(lens), 128), 910 + ps)
+    v = _rand_bits((S, Hkv, max(lens), 128), 920 + ps)
+    q = _rand_bits((S, gamma + 1, Hkv * G, 128), 930 + ps)
+    kd, vd, table = _paged_pool(k, v, lens, ps, 940 + ps)
+    _verify_check(k, v, q, lens, gamma, f"paged pages of {ps}", kdev=kd, vdev=vd, page_table=i32_dev(table))
+
+
+@pytest.mark.parametrize("ps", [8, 32])
+def test_verify_paged_page_outside_pool(ps):
+    """A page number outside [0, num_pages) makes that page's keys absent: every row attends over the
+    visible keys of the other pages (reference: the oracle's attention with those keys masked)."""
+    S, Hkv, G, gamma = 2, 2, 4, 5
+    lens = [3000, 1100]
+    k = _rand_bits((S, Hkv, max(lens), 128), 950 + ps)
+    v = _rand_bits((S, Hkv, max(lens), 128), 960 + ps)
+    q = _rand_bits((S, gamma + 1, Hkv * G, 128), 970 + ps)
+    kd, vd, table = _paged_pool(k, v, lens, ps, 980 + ps)
+    npages = int(kd.shape[0])
+    bad = [(0, 5, npages + 3), (1, 2, -2)]              # (sequence, page index, out-of-pool number)
+    absent = [np.zeros(L, bool) for L in lens]
+    for s, j, num in bad:
+        table[s, j] = num
+        absent[s][j * ps:(j + 1) * ps] = True
+    case(f"verify paged, pages outside the pool, pages of {ps}")
+    out, lse = bd.bd_verify_attn(kd, vd, bf16_dev(q), i32_dev(lens), return_lse=True, page_table=i32_dev(table))
+    torch.cuda.synchronize()
+    sc = 1.0 / np.sqrt(128.0)
+    R, Hq = gamma + 1, Hkv * G
+    ro = np.zeros((S, R, Hq, 128))
+    rl = np.full((S, R, Hq), -np.inf)
+    for s, L in enumerate(lens):
+        pos = L - gamma - 1 + np.arange(R)
+        vis = (np.arange(L)[None, :] <= pos[:, None]) & ~absent[s][None, :]
+        qs = O.bf16_to_f64(q[s])
+        for g in range(Hkv):
+            o, l = O.attend(qs[:, g * G:(g + 1) * G].reshape(R * G, 128), O.bf16_to_f64(k[s][g, :L]),
+                            O.bf16_to_f64(v[s][g, :L]), np.repeat(vis, G, axis=0), sc)
+            ro[s, :, g * G:(g + 1) * G] = o.reshape(R, G, 128)
+            rl[s, :, g * G:(g + 1) * G] = l.reshape(R, G)
+    what = f"paged, pages outside the pool, pages of {ps}"
+    assert_close(bf16_host64(out), ro, what)
+    assert_lse(lse.cpu().numpy().astype(np.float64), rl, what)
+
+
 # ------------------------------------------------------------------ multiview
 
 def _multiview_check(k, v, qb, idx_views, nsel_views, lens, what, full=True):

@@ -53,7 +53,7 @@ def _cache(g, k, v, lens, paged):
     """Device K/V (V may be None) as given, or scattered into a paged pool; the page table or None."""
     if not paged:
         return bf16_dev(k), (bf16_dev(v) if v is not None else None), None
-    ps = int(g.choice([16, 32]))
+    ps = int(g.choice([8, 16, 32, 48]))   # multiples of 16 take the per-page table, 8 the per-key one
     table, npages = _page_table(g, lens, ps)
     ks = [k[s][:, :int(L)] for s, L in enumerate(lens)]
     vs = [(v if v is not None else k)[s][:, :int(L)] for s, L in enumerate(lens)]

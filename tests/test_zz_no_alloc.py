@@ -64,8 +64,9 @@ def test_noalloc_repeated_calls_and_oversized_shape_rejected():
         assert torch.equal(first[0].view(torch.int16), again[0].view(torch.int16))
     cfg, q, k, v, lens = _pair("16k-collapse-b8", S=2)
     _run_both(cfg, q, k, v, lens, "16K, two sequences")
-    # 64 sequences x 32 KV heads, paged at 16 tokens a page, up to 16384 rows: 133 MiB of records
-    S, H, P = 64, 32, 16
+    # 64 sequences x 32 KV heads, paged at 8 tokens a page (the per-key table bounds the splits to
+    # 2,048 keys), up to 16384 rows: 133 MiB of records
+    S, H, P = 64, 32, 8
     pages = torch.zeros((1, H, P, 128), dtype=torch.bfloat16, device="cuda")
     table = torch.zeros((S, 16384 // P), dtype=torch.int32, device="cuda")
     qq = torch.zeros((S, 6, H, 128), dtype=torch.bfloat16, device="cuda")
