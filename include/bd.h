@@ -97,8 +97,9 @@ typedef int32_t bd_status;
  * belong in [0, num_pages): no value makes a kernel read outside the pool,
  * and the attention calls treat the keys of a page numbered outside it as
  * absent (they take no weight).  A page_size that is a multiple of 16 lets
- * the verifier's full-cache pass read through one table entry per page,
- * which allows far longer splits per workgroup than other page sizes. */
+ * the verifier's full-cache pass and the selection's scoring passes read
+ * through one table entry per page, which allows far longer splits per
+ * workgroup than other page sizes. */
 typedef struct bd_kv_desc {
   const uint16_t* k;          /* bf16 keys */
   const uint16_t* v;          /* bf16 values (ignored, may be NULL, for bd_select_kv) */

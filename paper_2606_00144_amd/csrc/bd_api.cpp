@@ -260,7 +260,7 @@ bd_status run_select(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_
   if (kv_extent(kv) > ((int64_t)1 << 34))
     return fail(BD_ERR_UNSUPPORTED, "K layout spans more than 2^34 elements");
   const bd::SelectPlan pl = bd::plan_select(kv->num_seqs, kv->num_kv_heads, num_q_heads, window, kv->max_seq_len,
-                                            kv->page_table != nullptr);
+                                            kv->page_table != nullptr, kv->page_table ? kv->page_size : 0);
   st = check_ws(ws, ws_bytes, pl.ws_bytes);
   if (st != BD_OK) return st;
   bd::SelectParams p{};
@@ -290,6 +290,7 @@ bd_status run_select(const bd_kv_desc* kv, const uint16_t* q_win, int32_t num_q_
   p.raw = scores_out;   // nullable: the total scores are exported only on request
   p.idx_out = idx_out;
   p.nsel_out = nsel_out;
+  p.page_arith = pl.page_arith ? 1 : 0;
   return launched(bd::launch_select(p, kv->page_table != nullptr, stream));
 }
 }  // namespace

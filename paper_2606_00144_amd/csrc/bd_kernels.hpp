@@ -165,16 +165,20 @@ struct SelectParams {
   float* raw;               // nullable [S][Hkv][max_L] total raw scores (the caller's scores_out)
   int32_t* idx_out;         // [S][Hkv][ld]
   int32_t* nsel_out;        // [S]
+  int32_t page_arith;       // 1: paged rows through a table of page offsets (pages of 16k rows)
 };
 
 struct SelectPlan {
   int n_rb, nsplit, kps;
+  bool page_arith;          // paged splits through the table of page offsets
   size_t stats_bytes, raw_part_bytes, ws_bytes;
 };
 
-// `paged`: the cache is paged (its splits then go through a slot table of bounded size); workspace
-// queries that do not know the layout use paged = true, which has at least as many splits.
-SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L, bool paged);
+// `paged`: the cache is paged; its splits then go through a table of bounded size, with one entry per
+// key, or with `page_size` a multiple of 16 (pages hold whole 16-key sub-tiles) one per page.
+// Workspace queries that do not know the layout use paged = true with the per-key table, which has
+// at least as many splits.
+SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L, bool paged, int page_size = 0);
 hipError_t launch_select(const SelectParams& p, bool paged, hipStream_t stream);
 
 // ---- per-round cache updates -------------------------------------------------

@@ -154,7 +154,34 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
   }
 
   const int ntiles = k1 > k0 ? (k1 - k0 + kTile - 1) / kTile : 0;
-  if constexpr (PAGED) {
+  // pages holding whole 16-key sub-tiles (page_size a multiple of 16, host-checked): a table of page
+  // offsets, one entry per page; k / page_size is computed as (k / 16) / (page_size / 16), exact for
+  // keys below 2^26 (host-checked); k0 is a multiple of kWaves * kTile
+  const bool page_arith = PAGED && p.page_arith != 0;
+  const int psub = PAGED ? p.kv.page_size >> 4 : 1;
+  const float inv_psub = __builtin_amdgcn_rcpf((float)psub);
+  const int page0 = page_arith ? div_small(k0 >> 4, psub, inv_psub) : 0;
+  if (page_arith) {
+    // entry j: offset (16-byte units) of page page0 + j for head g, 0 for a page outside the pool (its
+    // keys read pool rows and score as whatever those hold); all page-table loads issued first
+    constexpr int kPer = (kSlotCap + kThreads - 1) / kThreads;
+    const int npg = k1 > k0 ? div_small((k1 - 1) >> 4, psub, inv_psub) - page0 + 1 : 0;
+    const int32_t* prow = p.kv.page_table + (int64_t)s * p.kv.max_pages_per_seq + page0;
+    int pg[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int j = tid + k * kThreads;
+      pg[k] = j < npg ? prow[j] : -1;
+    }
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int j = tid + k * kThreads;
+      if (j < npg)
+        sm.roff[j] = (unsigned)pg[k] < (unsigned)p.kv.num_pages
+                         ? (int)(((int64_t)pg[k] * p.kv.stride_page + (int64_t)g * p.kv.stride_head) >> 3)
+                         : 0;
+    }
+  } else if constexpr (PAGED) {
     // slot table of this split: all page-table loads issued before any result is used; padding
     // slots (past the split) hold row 0, a safe, cache-resident address
     constexpr int kPer = (kSlotCap + kThreads - 1) / kThreads;
@@ -331,8 +358,30 @@ __global__ __launch_bounds__(kThreads) void score_kernel(SelectParams p) {
     auto issue = [&](int tile, int slot) {
       uint32_t r[2];
       if constexpr (PAGED) {
-        if (tile >= ntiles) r[0] = r[1] = 0u;
-        else read_krows(r, roff_lds, kTile * real(tile), lane);
+        if (tile >= ntiles) {
+          r[0] = r[1] = 0u;
+        } else if (page_arith) {
+          // sub-tile h (keys tb+16h .. +15) lies in one page: its offset + (key mod page_size) rows
+          const int tb = k0 + kTile * real(tile);
+          uint32_t a[2], w[2], b[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int t = tb + 16 * h;
+            const int pi = div_small(t >> 4, psub, inv_psub);
+            a[h] = roff_lds + 4 * (uint32_t)(t < k1 ? pi - page0 : 0);   // past the split: entry 0, masked
+            w[h] = (uint32_t)(t - pi * p.kv.page_size);
+          }
+          asm volatile(
+              "ds_read_b32 %0, %2\n"
+              "ds_read_b32 %1, %3\n"
+              "s_waitcnt lgkmcnt(0)"
+              : "=&v"(b[0]), "=&v"(b[1])
+              : "v"(a[0]), "v"(a[1]));
+#pragma unroll
+          for (int h = 0; h < 2; ++h) r[h] = b[h] + (w[h] + (uint32_t)lr) * tok16;
+        } else {
+          read_krows(r, roff_lds, kTile * real(tile), lane);
+        }
       } else if (tile >= ntiles) {
         r[0] = r[1] = 0u;                  // padding: row 0, a safe, cache-resident address
       } else {
@@ -748,7 +797,7 @@ int select_nt(int R) {
 
 }  // namespace
 
-SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L, bool paged) {
+SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L, bool paged, int page_size) {
   SelectPlan pl;
   const int G = Hq / Hkv;
   const int R = W * G;
@@ -760,7 +809,12 @@ SelectPlan plan_select(int S, int Hkv, int Hq, int W, int max_L, bool paged) {
   int64_t kps = (per_block + kStep - 1) / kStep * kStep;
   const int64_t cap = ((int64_t)max_L + kStep - 1) / kStep * kStep;
   if (kps > cap) kps = cap;
-  if (paged && kps > kMaxPagedKeys) kps = kMaxPagedKeys;
+  // a paged split's table holds kSlotCap entries: one per key, or one per page when pages hold whole
+  // 16-key sub-tiles (kps keys span at most kps / page_size + 2 pages); keys below 2^26 keep the
+  // kernel's page division exact
+  pl.page_arith = paged && page_size > 0 && page_size % 16 == 0 && max_L <= (1 << 26) - 64;
+  const int64_t paged_cap = pl.page_arith ? ((int64_t)(kSlotCap - 2) * page_size) / kStep * kStep : kMaxPagedKeys;
+  if (paged && kps > paged_cap) kps = paged_cap;
   if (kps < kStep) kps = kStep;
   pl.kps = (int)kps;
   pl.nsplit = max_L > 0 ? (int)((max_L + kps - 1) / kps) : 1;
