@@ -202,7 +202,7 @@ def _paged_pool(k, v, lens, ps, seed):
     return kd, vd, table
 
 
-@pytest.mark.parametrize("ps", [8, 16, 48, 64])
+@pytest.mark.parametrize("ps", [8, 16, 48, 64, 1024])
 def test_verify_paged_page_sizes(ps):
     """Pages that hold whole 16-key sub-tiles (16, 48, 64) read the full cache through a table of page
     offsets; other sizes (8) through the per-key table.  At 48 rows the pages straddle the splits'
