@@ -1578,14 +1578,29 @@ __global__ __launch_bounds__(kBThreads) void block_kernel(AttnParams p) {
 // launch spreads the merge over the whole chip: merged by the workgroup that finished last, a branch
 // split over 7 workgroups pulled 7 records of 128 KiB into one CU, ~16 us at one CU's bandwidth.
 // Every load a wave needs is issued before any result is used: the branch lengths (lane b holds
-// branch b's), then up to kMBatch records at a time.
-constexpr int kMBatch = 8;
+// branch b's), then up to kMBatch records at a time.  Four records a batch keep the wave at 86 VGPRs
+// (bf16 outputs), so the launch's 5120 waves are resident at once; batches of 8 (132 VGPRs, two
+// rounds of waves) took 11.1 us on the multiview workload, batches of 4 9.1 us, of 2 9.5 us.
+constexpr int kMBatch = 4;
+// The merge's kernel arguments, all requested at entry (as fetch_args does for the other kernels):
+// fetched where first used they took four round trips before the first record load.
+__device__ inline int fetch_merge_args(const AttnParams& p) {
+  int z0, z1;
+  asm("s_mov_b32 %0, 0" : "=s"(z0) : "s"(p.kv.seq_lens), "s"(p.kv.max_seq_len), "s"(p.nsel), "s"(p.ld_idx), "s"(p.S),
+      "s"(p.V), "s"(p.nbr), "s"(p.nW), "s"(p.n_rg), "s"(p.n_rb), "s"(p.Hkv), "s"(p.part));
+  asm("s_mov_b32 %0, 0" : "=s"(z1) : "s"(z0), "s"(p.out_g), "s"(p.out_f), "s"(p.lse_g), "s"(p.lse_f), "s"(p.o32_g),
+      "s"(p.o32_f), "s"(p.nq), "s"(p.Hq), "s"(p.G), "s"(p.R));
+  return z1;
+}
+
 template <bool TRAIN>
-__global__ __launch_bounds__(kWave) void block_merge_kernel(AttnParams p) {
+__global__ __launch_bounds__(4 * kWave) void block_merge_kernel(AttnParams p) {
   constexpr int NT = 2;
   using RB = RowBlock<NT>;
-  const int lane = threadIdx.x, lg = lane >> 4, lr = lane & 15;
-  int id = blockIdx.x;
+  const int lane = threadIdx.x & (kWave - 1), lg = lane >> 4, lr = lane & 15;
+  // the waves work independently (no barrier): four per workgroup, since 5120 single-wave
+  // workgroups cost 4.8 us of dispatch alone on the multiview workload
+  int id = 4 * blockIdx.x + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) + fetch_merge_args(p);
   const int dh = id & 1, nt = (id >> 1) & 1;
   id >>= 2;
   const int rbl = id % kBWaves;
@@ -1595,8 +1610,11 @@ __global__ __launch_bounds__(kWave) void block_merge_kernel(AttnParams p) {
   const int g = pair % p.Hkv, s = pair / p.Hkv;
   const int rb = rg * kBWaves + rbl;
   if (rb >= p.n_rb) return;
+  // lane b holds branch b's length (nbr <= 64 lanes): the views' entry counts are requested before
+  // the cache length is waited for, so both loads share one round trip
+  const int n_raw = lane < p.V ? p.nsel[lane * p.S + s] : 0;
   const int L = seq_len(p.kv, s);
-  const int my_len = lane < p.nbr ? block_branch_len(p, s, L, lane) : 0;   // nbr <= 64 lanes
+  const int my_len = lane < p.V ? (n_raw < 0 ? 0 : (n_raw > p.ld_idx ? p.ld_idx : n_raw)) : (lane < p.nbr ? L : 0);
   // the branch's offset in the stream, its length, the stream total and the branch's record slot
   // (one slot per workgroup that met each earlier non-empty branch)
   int total = 0, vt = 0, off_b = 0, n = 0;
@@ -1626,37 +1644,40 @@ __global__ __launch_bounds__(kWave) void block_merge_kernel(AttnParams p) {
   f32x4 og[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) og[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // a batch keeps the records as loaded (bf16 outputs still packed, unpacked when merged): fewer
+  // VGPRs, so more of the launch's waves are resident at once
+  constexpr int kOutWords = TRAIN ? 4 : 2;       // 16-byte output pieces per record and lane
   for (int k0 = 0; k0 < nwg; k0 += kMBatch) {
-    f32x4 sv[kMBatch], ov[kMBatch][4];
+    f32x4 sv[kMBatch], ow[kMBatch][kOutWords];
 #pragma unroll
     for (int u = 0; u < kMBatch; ++u) {
       const uint32_t rec = (uint32_t)(k0 + u) * kBWaves * RB::kRec * 4;
       const bool ok = k0 + u < nwg;
       sv[u] = ok ? load16_coherent(urec, rec + 16 * (16 * nt + lr)) : f32x4{-INFINITY, 0.f, 0.f, 0.f};
-      if constexpr (TRAIN) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          ov[u][i] = ok ? load16_coherent(urec, rec + kOutOff + 16 * ((nt * 8 + 4 * dh + i) * kWave + lane))
-                        : f32x4{0.f, 0.f, 0.f, 0.f};
-      } else {
-#pragma unroll
-        for (int k = 0; k < 2; ++k) {
-          const f32x4 w = ok ? load16_coherent(urec, rec + kOutOff + 16 * ((nt * 4 + 2 * dh + k) * kWave + lane))
-                             : f32x4{0.f, 0.f, 0.f, 0.f};
-          unpack_record_bf16(as_u32x4(w), ov[u][2 * k], ov[u][2 * k + 1]);
-        }
+      for (int i = 0; i < kOutWords; ++i) {
+        const uint32_t piece = TRAIN ? (uint32_t)(nt * 8 + 4 * dh + i) : (uint32_t)(nt * 4 + 2 * dh + i);
+        ow[u][i] = ok ? load16_coherent(urec, rec + kOutOff + 16 * (piece * kWave + lane)) : f32x4{0.f, 0.f, 0.f, 0.f};
       }
     }
 #pragma unroll
     for (int u = 0; u < kMBatch; ++u) {
       if (k0 + u >= nwg) break;
+      f32x4 ov[4];
+      if constexpr (TRAIN) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ov[i] = ow[u][i];
+      } else {
+#pragma unroll
+        for (int k = 0; k < 2; ++k) unpack_record_bf16(as_u32x4(ow[u][k]), ov[2 * k], ov[2 * k + 1]);
+      }
       const float mb = fmaxf(Mg, sv[u][0]);
       const float mbu = mb == -INFINITY ? 0.f : mb;
       const float sc = exp2f(Mg - mbu), wt = exp2f(sv[u][0] - mbu);
       Lg = Lg * sc + wt * sv[u][1];
       Lxg = Lxg * sc + wt * sv[u][2];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) og[i] = og[i] * sc + ov[u][i] * wt;
+      for (int i = 0; i < 4; ++i) og[i] = og[i] * sc + ov[i] * wt;
       Mg = mb;
     }
   }
@@ -1801,9 +1822,10 @@ hipError_t launch_attn(const AttnParams& args, const AttnPlan& pl, bool paged, h
     if (pl.nW > 1) {                               // some branch may be split: merge its records
       const hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
-      const int64_t mblocks = (int64_t)pl.units * pl.nbr * kBWaves * 4;   // (row tile, d half) waves
-      if (train) hipLaunchKernelGGL((block_merge_kernel<true>), dim3((unsigned)mblocks), dim3(kWave), 0, stream, p);
-      else hipLaunchKernelGGL((block_merge_kernel<false>), dim3((unsigned)mblocks), dim3(kWave), 0, stream, p);
+      // one workgroup per (unit, branch, row block): its four waves take the (row tile, d half) pairs
+      const int64_t mblocks = (int64_t)pl.units * pl.nbr * kBWaves;
+      if (train) hipLaunchKernelGGL((block_merge_kernel<true>), dim3((unsigned)mblocks), dim3(4 * kWave), 0, stream, p);
+      else hipLaunchKernelGGL((block_merge_kernel<false>), dim3((unsigned)mblocks), dim3(4 * kWave), 0, stream, p);
     }
     return hipGetLastError();
   }
