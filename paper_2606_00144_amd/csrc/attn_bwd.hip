@@ -224,6 +224,20 @@ __device__ inline int fetch_bwd_args(const AttnBwdParams& p) {
       "s"(p.R_pad), "s"(p.counters));
   return z1;
 }
+// The dK/dV kernel's arguments, requested at entry the same way (fetched where first used they took
+// four round trips before its first data load).
+__device__ inline int fetch_dkv_args(const AttnBwdParams& p) {
+  int z0, z1, z2;
+  asm("s_mov_b32 %0, 0" : "=s"(z0) : "s"(p.kv.k), "s"(p.kv.v), "s"(p.kv.seq_lens), "s"(p.kv.page_table),
+      "s"(p.kv.stride_seq), "s"(p.kv.stride_head), "s"(p.kv.stride_tok), "s"(p.kv.stride_page), "s"(p.kv.max_seq_len),
+      "s"(p.kv.page_size), "s"(p.kv.max_pages_per_seq), "s"(p.kv.num_pages));
+  asm("s_mov_b32 %0, 0" : "=s"(z1) : "s"(z0), "s"(p.q), "s"(p.o32_g), "s"(p.lse_g), "s"(p.dout_g), "s"(p.o32_f),
+      "s"(p.lse_f), "s"(p.dout_f), "s"(p.idx), "s"(p.nsel), "s"(p.ld_idx), "s"(p.S), "s"(p.Hkv), "s"(p.Hq));
+  asm("s_mov_b32 %0, 0" : "=s"(z2) : "s"(z1), "s"(p.G), "s"(p.C), "s"(p.V), "s"(p.R), "s"(p.n_rb), "s"(p.nbr),
+      "s"(p.nkt), "s"(p.scale), "s"(p.scale_log2), "s"(p.inv_G), "s"(p.max_roff), "s"(p.dk), "s"(p.dv),
+      "s"(p.part_kv), "s"(p.rstats), "s"(p.R_pad));
+  return z2;
+}
 // Workgroup barrier for LDS traffic: waits for this wave's LDS operations only, not for its global
 // loads in flight (which a __syncthreads fence would wait for).
 __device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
@@ -533,7 +547,7 @@ __global__ __launch_bounds__(kKThreads) void dkv_kernel(AttnBwdParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave / kKGroupWaves, wk = wave % kKGroupWaves;
   const int lg = lane >> 4, lr = lane & 15;
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int bid = xcd_remap(blockIdx.x + fetch_dkv_args(p), gridDim.x);
   const int br = bid % p.nbr;
   const int npass = (p.nkt + kKGroupWaves - 1) / kKGroupWaves;
   const int kpass = (bid / p.nbr) % npass;       // the block keys' pass: key tiles 4*kpass .. +3
