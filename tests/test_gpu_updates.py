@@ -26,8 +26,10 @@ def _u16(t):
     return t.cpu().view(torch.int16).numpy().view(np.uint16)
 
 
-def test_append_matches_oracle_with_clamps():
-    S, Hkv, cap, n, ld = 3, 2, 100, 8, 20
+@pytest.mark.parametrize("n", [8, 40])
+def test_append_matches_oracle_with_clamps(n):
+    # 8 rows: one launch (a workgroup per sequence); 40 rows: a workgroup per row and a second launch
+    S, Hkv, cap, ld = 3, 2, 100, 20
     k, v = _bits((S, Hkv, cap, 128), 1), _bits((S, Hkv, cap, 128), 2)
     kn, vn = _bits((S, n, Hkv, 128), 3), _bits((S, n, Hkv, 128), 4)
     lens, nsel = [10, 95, 100], [5, 15, 18]
@@ -35,17 +37,18 @@ def test_append_matches_oracle_with_clamps():
     for s in range(S):
         idx[s, :, :nsel[s]] = np.arange(nsel[s])
     ok, ov, ol, oi, on = O.cache_append(k, v, lens, kn, vn, idx, nsel)
-    case("append with capacity and list clamps")
+    case(f"append of {n} rows with capacity and list clamps")
     kd, vd, ld_, idd, nd = bf16_dev(k), bf16_dev(v), i32_dev(lens), i32_dev(idx), i32_dev(nsel)
     bd.bd_cache_append(kd, vd, ld_, bf16_dev(kn), bf16_dev(vn), idx=idd, nsel=nd)
     torch.cuda.synchronize()
     assert np.array_equal(_u16(kd), ok) and np.array_equal(_u16(vd), ov)
-    assert ld_.cpu().tolist() == ol.tolist() == [18, 100, 100]
-    assert np.array_equal(idd.cpu().numpy(), oi) and nd.cpu().tolist() == on.tolist() == [13, 20, 18]
+    assert ld_.cpu().tolist() == ol.tolist() == [10 + n, 100, 100]
+    assert np.array_equal(idd.cpu().numpy(), oi) and nd.cpu().tolist() == on.tolist() == [min(5 + n, 20), 20, 18]
 
 
-def test_append_paged_layout():
-    S, Hkv, page, pages_per_seq, n = 2, 2, 16, 4, 5
+@pytest.mark.parametrize("n", [5, 20])
+def test_append_paged_layout(n):
+    S, Hkv, page, pages_per_seq = 2, 2, 16, 4
     num_pages = S * pages_per_seq
     g = np.random.default_rng(5)
     perm = g.permutation(num_pages).astype(np.int32)
@@ -62,7 +65,7 @@ def test_append_paged_layout():
         return np.stack([np.concatenate([pool[table[s, p]] for p in range(pages_per_seq)], axis=1) for s in range(S)])
     ok, ov, ol = O.cache_append(logical(pool_k), logical(pool_v), lens, kn, vn)
     assert np.array_equal(logical(_u16(kd)), ok) and np.array_equal(logical(_u16(vd)), ov)
-    assert ld_.cpu().tolist() == ol.tolist() == [35, 64]
+    assert ld_.cpu().tolist() == ol.tolist() == [30 + n, 64]
 
 
 def test_rollback_matches_oracle():
