@@ -338,6 +338,10 @@ def main():
                         "step_gbps": round(step2_bytes / (us_step2 * 1e-6) / 1e9, 1)},
         "roofline": roofline,
         "cpu_baseline": None,
+        # context only, not comparable: the paper's whole-model end-to-end speedups over AR decoding
+        "paper_context": {"speedup_vs_ar_end_to_end": {"4K": 6.55, "8K": 4.46, "16K": 2.10},
+                          "hardware": "one NVIDIA A100 80GB", "scope": "whole 7B verifier + 68M drafter, prefill included",
+                          "source": "Sec. 4 main results"},
     }
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host (one step)")
