@@ -347,6 +347,16 @@ __device__ inline int fetch_args(const AttnParams& p) {
   return z2;
 }
 
+__device__ inline f32x4 as_f32x4(const u32x4& v) { return __builtin_bit_cast(f32x4, v); }
+__device__ inline u32x4 as_u32x4(const f32x4& v) { return __builtin_bit_cast(u32x4, v); }
+__device__ inline u32x4 pack_record_bf16(const f32x4& a, const f32x4& b) {
+  return u32x4{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3])};
+}
+__device__ inline void unpack_record_bf16(const u32x4& w, f32x4& a, f32x4& b) {
+  a = f32x4{bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
+  b = f32x4{bf16_lo(w[2]), bf16_hi(w[2]), bf16_lo(w[3]), bf16_hi(w[3])};
+}
+
 // Records merged by one batch of loads; units with more splits merge in two levels (TWO_LEVEL, chosen
 // per launch when some unit has more than kMergeGroup splits; the one-level merge keeps its own code).
 constexpr int kMergeGroup = 8;
@@ -776,13 +786,23 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   constexpr int kChunks = kPerThread / 4;
   constexpr uint32_t kOutOff = 16 * RB::kRows;
   if constexpr (!TWO_LEVEL) {
+    // verify's records (NT = 2) hold the unnormalised outputs in bf16, eight per 16 bytes; the row
+    // statistics stay fp32.  A merged output is a weighted mean of the records' rows, so their
+    // rounding (relative 2^-9) adds at most 2^-9 of the output's scale before its own bf16 rounding.
+    constexpr bool kBf16 = NT == 2;
+    constexpr int kWords = kBf16 ? kChunks / 2 : kChunks;     // 16-byte output words per thread
     if (row_valid) {
       const uint32_t rec = (uint32_t)split * RB::kRec * 4;
       if (d0 == 0) store16_coherent(urec, rec + 16 * r, f32x4{M, Lsum, Lx, 0.f});
   #pragma unroll
-      for (int c = 0; c < kChunks; ++c)
-        store16_coherent(urec, rec + kOutOff + 16 * (c * kThreads + tid),
-                         f32x4{acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]});
+      for (int c = 0; c < kWords; ++c) {
+        const uint32_t off = rec + kOutOff + 16 * (c * kThreads + tid);
+        if constexpr (kBf16)
+          store16_coherent(urec, off, as_f32x4(pack_record_bf16(f32x4{acc[8 * c], acc[8 * c + 1], acc[8 * c + 2], acc[8 * c + 3]},
+                                                                f32x4{acc[8 * c + 4], acc[8 * c + 5], acc[8 * c + 6], acc[8 * c + 7]})));
+        else
+          store16_coherent(urec, off, f32x4{acc[4 * c], acc[4 * c + 1], acc[4 * c + 2], acc[4 * c + 3]});
+      }
     }
     wait_vmem();
     __syncthreads();
@@ -799,15 +819,15 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
   #pragma unroll
     for (int e = 0; e < kPerThread; ++e) ag[e] = 0.f;
     for (int sp0 = 0; sp0 < nsplit; sp0 += kBatch) {
-      f32x4 sv[kBatch], ov[kBatch][kChunks];
+      f32x4 sv[kBatch], ow[kBatch][kWords];
   #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         const uint32_t rec = (uint32_t)(sp0 + u) * RB::kRec * 4;
         const bool ok = sp0 + u < nsplit;
         sv[u] = ok ? load16_coherent(urec, rec + 16 * r) : f32x4{-INFINITY, 0.f, 0.f, 0.f};
   #pragma unroll
-        for (int c = 0; c < kChunks; ++c)
-          ov[u][c] = ok ? load16_coherent(urec, rec + kOutOff + 16 * (c * kThreads + tid)) : f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < kWords; ++c)
+          ow[u][c] = ok ? load16_coherent(urec, rec + kOutOff + 16 * (c * kThreads + tid)) : f32x4{0.f, 0.f, 0.f, 0.f};
       }
       float mb = Mg;
   #pragma unroll
@@ -823,10 +843,18 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p) {
         const float wt = exp2f(sv[u][0] - mbu);
         Lg += wt * sv[u][1];
         Lxg += wt * sv[u][2];
+        f32x4 ov[kChunks];
+        if constexpr (kBf16) {
+  #pragma unroll
+          for (int c = 0; c < kWords; ++c) unpack_record_bf16(as_u32x4(ow[u][c]), ov[2 * c], ov[2 * c + 1]);
+        } else {
+  #pragma unroll
+          for (int c = 0; c < kChunks; ++c) ov[c] = ow[u][c];
+        }
   #pragma unroll
         for (int c = 0; c < kChunks; ++c)
   #pragma unroll
-          for (int i = 0; i < 4; ++i) ag[4 * c + i] += wt * ov[u][c][i];
+          for (int i = 0; i < 4; ++i) ag[4 * c + i] += wt * ov[c][i];
       }
       Mg = mb;
     }
@@ -1178,16 +1206,6 @@ __device__ inline bool block_dirty(const u32x4 (&tp)[2], int minpos) {
 // lane in 16 bytes.  Each merged output is a weighted mean of the records' rows, so their rounding
 // (relative 2^-9 per element) adds at most 2^-9 of the output's scale before its own bf16 rounding.
 // The training path (fp32 outputs) keeps fp32 records.
-__device__ inline f32x4 as_f32x4(const u32x4& v) { return __builtin_bit_cast(f32x4, v); }
-__device__ inline u32x4 as_u32x4(const f32x4& v) { return __builtin_bit_cast(u32x4, v); }
-__device__ inline u32x4 pack_record_bf16(const f32x4& a, const f32x4& b) {
-  return u32x4{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3])};
-}
-__device__ inline void unpack_record_bf16(const u32x4& w, f32x4& a, f32x4& b) {
-  a = f32x4{bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1])};
-  b = f32x4{bf16_lo(w[2]), bf16_hi(w[2]), bf16_lo(w[3]), bf16_hi(w[3])};
-}
-
 // Workgroup barrier for LDS traffic: waits for this wave's LDS operations only, not for its global
 // loads in flight.
 __device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
