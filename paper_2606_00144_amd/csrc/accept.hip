@@ -77,7 +77,8 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(AcceptParams p) {
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         const int c = base + u * 4 * kThreads;
-        x[u] = c + 4 <= c1 ? *reinterpret_cast<const f32x4*>(row + c) : f32x4{0.f, 0.f, 0.f, 0.f};
+        // non-temporal: the logits are read once per step, after verify has streamed the caches
+        x[u] = c + 4 <= c1 ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + c)) : f32x4{0.f, 0.f, 0.f, 0.f};
       }
       if (first < 0) first = base;
 #pragma unroll
